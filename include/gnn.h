@@ -1,0 +1,293 @@
+/*
+ * gnn.h -- C ABI of the MI355X (gfx950) sampled-GNN training hot path.
+ *
+ * One mini-batch iteration of sampled GNN training as the paper describes it
+ * (HyScale-GNN, Section II-B and Figure 1): a sampler turns the input graph
+ * into one bipartite block per layer, a feature loader gathers the rows of the
+ * sampled input vertices (Section III-A, Feature Loader), each layer
+ * aggregates neighbour features and applies the update (Section II-A,
+ * equations 1-2, with the GCN and GraphSAGE operators), a loss is taken on
+ * the target vertices, the same operators run backwards to produce weight
+ * gradients, and the weights are updated.
+ *
+ * Conventions shared by every call:
+ *  - Pointers marked [device] are HIP device pointers (from hipMalloc or a
+ *    torch CUDA/HIP tensor); [host] pointers are ordinary host memory;
+ *    [pinned] is host memory from hipHostMalloc (mapped into the device's
+ *    address space).  The caller owns every buffer.  The library never
+ *    allocates or frees memory and keeps no pointer after a call returns.
+ *  - Every call enqueues its kernels on the given stream (a hipStream_t, or
+ *    NULL for the null stream) and returns without synchronising.  Outputs
+ *    are valid once the stream reaches that point; inputs must stay alive
+ *    until then.
+ *  - Counts produced on the device (rows of a block, sampled edges) are read
+ *    from device memory by later kernels: no call ever copies them to the
+ *    host.  Grids are sized by the host-side capacities and the surplus
+ *    workgroups exit at once.
+ *  - Matrices are dense row-major with the stated row length; activation
+ *    rows of layer l have f^l elements.
+ *  - bf16 values are stored as raw 16-bit patterns; narrowing from fp32
+ *    rounds to nearest, ties to even.
+ *  - Validation (null pointers, alignment, sizes, dtypes, capacities) runs on
+ *    the host before anything is enqueued; a failed check returns an error
+ *    code and enqueues nothing.  HIP launch failures return GNN_EHIP.  The
+ *    text of the last error on the calling thread is in gnn_last_error().
+ *    Device-content errors (a vertex id >= n, a label >= C, duplicate
+ *    targets) are not detected and give undefined results.
+ *  - Calls on different streams may run concurrently when their buffers and
+ *    workspaces do not overlap.
+ */
+#ifndef GNN_H
+#define GNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t gnn_status;
+#define GNN_OK 0
+#define GNN_EINVAL (-1)        /* bad argument: null pointer, negative size, misalignment */
+#define GNN_ESIZE (-2)         /* a capacity or workspace is too small */
+#define GNN_EHIP (-3)          /* a HIP runtime call or kernel launch failed */
+#define GNN_EUNSUPPORTED (-4)  /* valid but unsupported combination (dtype, location) */
+
+typedef enum { GNN_F32 = 0, GNN_BF16 = 1, GNN_F16 = 2 } gnn_dtype;
+typedef enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1 } gnn_agg;
+typedef enum { GNN_LOC_DEVICE = 0, GNN_LOC_HOST_PINNED = 1 } gnn_loc;
+typedef void *gnn_stream; /* hipStream_t */
+
+#define GNN_MAX_LAYERS 4
+#define GNN_MAX_FANOUT 1024
+#define GNN_MAX_DIM 65536
+#define GNN_ABI_VERSION 1
+
+/* Text of the last error reported on the calling thread ("" if none).  Valid
+ * until the next gnn_* call on this thread. */
+const char *gnn_last_error(void);
+int32_t gnn_abi_version(void);
+
+/* Input graph G(V, E) (Table I): int64 CSR.  Row v lists the stored edges
+ * (v, u) -- the neighbours N(v) -- in ascending u; repeated entries
+ * (multi-edges) are allowed.  rowptr [device] has n+1 entries, col [device]
+ * nnz entries. */
+typedef struct gnn_graph {
+    int64_t n;
+    int64_t nnz;
+    const int64_t *rowptr;
+    const int64_t *col;
+} gnn_graph;
+
+/* GCN normalisation factor per vertex (GCN operator of Section II-A): the
+ * degree D(v) is the input-graph degree plus the self loop, and
+ * nrm[v] = fp32(1 / sqrt(D(v))) computed in double before narrowing.
+ * nrm_out [device] has g->n floats. */
+gnn_status gnn_gcn_norm(const gnn_graph *g, float *nrm_out, gnn_stream s);
+
+/* ------------------------------------------------------------------------
+ * Mini-batch sampler (Section III-A, Mini-batch Sampler; the GraphSAGE
+ * neighbour sampler of Section VI-A).
+ *
+ * A block is the mini-batch topology G(V^l, E^l) of one layer: n_dst
+ * destination rows and n_src sources, where the sources are the destinations
+ * (same order) followed by every newly reached vertex in ascending id order.
+ * Row i lists the local source index of each sampled neighbour of dst i, in
+ * ascending position within i's adjacency row.  The transpose (CSC) lists,
+ * for each source j, the rows i that sampled it, ascending.
+ *
+ * counts [device] int64[4] is written by gnn_build_block:
+ *   counts[0] = n_dst, counts[1] = n_src, counts[2] = nnz (sampled edges).
+ * ------------------------------------------------------------------------ */
+typedef struct gnn_block {
+    int64_t cap_dst;   /* [host] capacity of destination rows */
+    int64_t cap_src;   /* [host] capacity of src_ids / cscptr rows */
+    int64_t cap_nnz;   /* [host] capacity of sampled edges */
+    int64_t *counts;   /* [device] int64[4], see above */
+    int64_t *src_ids;  /* [device] int64[cap_src]: global vertex id of each local source */
+    int64_t *rowptr;   /* [device] int64[cap_dst + 1] */
+    int32_t *col;      /* [device] int32[cap_nnz]: local source index per sampled edge */
+    int64_t *cscptr;   /* [device] int64[cap_src + 1], or NULL when no transpose is wanted */
+    int32_t *cscrow;   /* [device] int32[cap_nnz], or NULL together with cscptr */
+    float *src_norm;   /* [device] float[cap_src]: GCN nrm of each source, or NULL */
+} gnn_block;
+
+/* Capacities that always suffice for a block of cap_dst destinations with the
+ * given fanout in a graph of graph_n vertices:
+ *   cap_nnz = cap_dst * fanout, cap_src = min(cap_dst + cap_nnz, graph_n). */
+gnn_status gnn_block_bounds(int64_t graph_n, int64_t cap_dst, int32_t fanout, int64_t *cap_src, int64_t *cap_nnz);
+
+/* Workspace of gnn_build_block.  It holds a per-vertex map and bitmap that
+ * must be initialised once with gnn_sampler_workspace_init; every
+ * gnn_build_block call leaves them in that initial state again.  One
+ * workspace serves any number of sequential calls on one stream. */
+gnn_status gnn_sampler_workspace_size(int64_t graph_n, int64_t cap_dst, int32_t fanout, size_t *bytes);
+gnn_status gnn_sampler_workspace_init(void *ws, size_t ws_bytes, int64_t graph_n, gnn_stream s);
+
+/* Build one block (one hop of the sampler; hop 1 is sampled around the
+ * targets and yields the block of the last layer).
+ *   dst_ids   [device] destination vertex ids, distinct.
+ *   n_dst_dev [device] int64 count of dst_ids, or NULL to use out->cap_dst
+ *             (e.g. the targets of hop 1; for later hops pass the previous
+ *             block's &counts[1]).
+ *   fanout    k in [1, GNN_MAX_FANOUT].  Every dst vertex v with degree d
+ *             keeps all d neighbours when d <= k, else k positions drawn
+ *             without replacement by Floyd's algorithm, where draw t of
+ *             vertex v is Lemire's multiply-shift of the key
+ *             mix(mix(mix(mix(mix(seed)^step)^hop)^v)^t) (mix = the
+ *             SplitMix64 output function) into [0, d-k+t].
+ *   gcn_norm  [device] per-vertex norms (gnn_gcn_norm) to fill
+ *             out->src_norm, or NULL.
+ *   want_csc  nonzero to also build out->cscptr / out->cscrow.
+ * Degrees must be below 2^32 and n below 2^31. */
+gnn_status gnn_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
+                           const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
+                           int32_t want_csc, gnn_block *out, void *ws, size_t ws_bytes, gnn_stream s);
+
+/* ------------------------------------------------------------------------
+ * Feature loader (Section III-A; the Feature Loading and Data Transfer
+ * stages of Section III-B): X' = X[ids].
+ *   table      [device] or [pinned] (loc) n_rows x row_stride elements of tdt.
+ *   ids        [device] int64 row ids; n_ids_dev [device] their count, or
+ *              NULL to use cap_ids.
+ *   out        [device] cap_ids x dim elements of odt.
+ * Supported (tdt -> odt): F32->F32, F32->BF16, F16->F16, F16->F32,
+ * F16->BF16, BF16->BF16.  Same-type copies are bit copies.  A pinned table is
+ * read directly over the host link by the gather kernel (zero copy).
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, int64_t n_rows, int64_t dim,
+                               int64_t row_stride, const int64_t *ids, const int64_t *n_ids_dev, int64_t cap_ids,
+                               void *out, gnn_dtype odt, gnn_stream s);
+
+/* ------------------------------------------------------------------------
+ * Aggregation (equation 1; GCN and GraphSAGE operators of Section II-A).
+ *   h_src [device] block->cap_src x f (hdt in {F32, BF16}); row j is source j.
+ *   out   [device] block->cap_dst x f (odt in {F32, BF16}).
+ *   SAGE: out[i] = mean of h_src[col] over row i (zero when row i is empty).
+ *   GCN:  out[i] = nrm_i^2 h_src[i] + sum over row i of nrm_i nrm_j h_src[j],
+ *         each weight one fp32 product of block->src_norm entries.
+ * Sums are accumulated in fp32.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
+                             void *out, gnn_dtype odt, gnn_stream s);
+
+/* Backward of the aggregation for layers above the first (the backward pass
+ * repeats the forward operators in reverse, Section II-B).  Reads the block's
+ * transpose; uses no atomics, so results are bitwise reproducible.
+ *   d_a     [device] fp32 rows of the update input gradient: SAGE rows hold
+ *           2f values (self part, then neighbour part), GCN rows f values.
+ *   h_below [device] block->cap_src x f activations of the layer below
+ *           (hbdt F32 or BF16) for the ReLU mask, or NULL for no mask.
+ *   d_src   [device] fp32 block->cap_src x f, overwritten:
+ *     SAGE: d_src[j] = [j < n_dst] d_a[j, :f] + sum_{i samples j} d_a[i, f:] / deg_i
+ *     GCN:  d_src[j] = [j < n_dst] nrm_j^2 d_a[j] + sum_{i samples j} nrm_i nrm_j d_a[i]
+ *     then d_src[j] *= 1[h_below[j] > 0] elementwise when h_below is given. */
+gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a, int64_t f, const void *h_below,
+                             gnn_dtype hbdt, float *d_src, gnn_stream s);
+
+/* ------------------------------------------------------------------------
+ * Update (equation 2): Z = A W + b with A = [a_self || a_nbr] (SAGE) or
+ * A = a_self (GCN, a_nbr NULL); K = 2*k_each or k_each.
+ *   a_self, a_nbr [device] row-major, row length k_each, adt in {F32, BF16}.
+ *   m_dev   [device] int64 row count, or NULL to use cap_m.
+ *   w       [device] fp32 K x n_out row-major; bias [device] fp32 n_out or NULL.
+ *   gemm_dt GNN_BF16: operands rounded to bf16, matrix cores, fp32 accumulate;
+ *           GNN_F32: fp32 throughout.
+ *   out     [device] cap_m x n_out of odt; ReLU applied when relu != 0.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
+                          const int64_t *m_dev, int64_t cap_m, const float *w, const float *bias, int64_t n_out,
+                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, gnn_stream s);
+
+/* Gradients of the update given g = dLoss/dZ (fp32, cap_m x n_out):
+ *   dw = A^T g (K x n_out), db = column sums of g (unrounded),
+ *   d_a = g W^T (cap_m x K, fp32) when d_a is not NULL (layers above the
+ *   first; Section V, equation T_Trainer: the first layer's backward is the
+ *   update alone).  The weight gradient is reduced in a fixed order through
+ *   the workspace, so results are bitwise reproducible. */
+gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, size_t *bytes);
+gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
+                          const int64_t *m_dev, int64_t cap_m, const float *w, const float *g, int64_t n_out,
+                          gnn_dtype gemm_dt, float *dw, float *db, float *d_a, void *ws, size_t ws_bytes,
+                          gnn_stream s);
+
+/* Loss against the ground truth (Section II-B): mean softmax cross-entropy
+ * over the b target rows of logits [device] (fp32 b x c).  The label of row
+ * i is labels[targets[i]] (labels/targets [device] int64; targets NULL means
+ * labels[i]).  Writes g_out [device] fp32 b x c = (softmax - onehot) / b and
+ * loss_out [device] fp32 scalar.  ws must hold gnn_softmax_ce_workspace_size
+ * bytes. */
+gnn_status gnn_softmax_ce_workspace_size(int64_t b, size_t *bytes);
+gnn_status gnn_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels, const int64_t *targets,
+                          float *g_out, float *loss_out, void *ws, size_t ws_bytes, gnn_stream s);
+
+/* Plain SGD (synchronous SGD of Section II-B on one device): w -= lr * dw
+ * over n fp32 values [device]. */
+gnn_status gnn_sgd(float *w, const float *dw, int64_t n, float lr, gnn_stream s);
+
+/* ------------------------------------------------------------------------
+ * One whole training iteration (Section II-B, Figure 1): sample L blocks,
+ * gather X', L forward layers, loss, backward in reverse order (no input
+ * gradient below layer 1), SGD.
+ *
+ * Storage precision: with precision GNN_BF16, X', the aggregation outputs and
+ * hidden activations are stored bf16 and every GEMM operand is rounded to
+ * bf16 (fp32 accumulate); logits, gradients and weights stay fp32.  With
+ * GNN_F32 everything is fp32.
+ * ------------------------------------------------------------------------ */
+typedef struct gnn_model {
+    int32_t num_layers;                 /* L in [1, GNN_MAX_LAYERS] */
+    int32_t kind;                       /* gnn_agg */
+    int32_t precision;                  /* GNN_F32 or GNN_BF16 */
+    int32_t dims[GNN_MAX_LAYERS + 1];   /* f^0 .. f^L (f^L = number of classes) */
+    int32_t fanouts[GNN_MAX_LAYERS];    /* hop order: fanouts[0] is sampled around the targets */
+    float *w[GNN_MAX_LAYERS];           /* [device] fp32 K_l x f^l, K_l = 2 f^{l-1} (SAGE) or f^{l-1} (GCN) */
+    float *b[GNN_MAX_LAYERS];           /* [device] fp32 f^l */
+    float *dw[GNN_MAX_LAYERS];          /* [device] fp32 K_l x f^l, written */
+    float *db[GNN_MAX_LAYERS];          /* [device] fp32 f^l, written */
+} gnn_model;
+
+/* Offsets (bytes from the workspace base) of the step's internal buffers, for
+ * inspection.  Block h (1-based hop) is the block of layer L-h+1. */
+typedef struct gnn_step_layout {
+    size_t total_bytes;
+    size_t sampler_ws, sampler_ws_bytes;
+    int64_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS], cap_nnz[GNN_MAX_LAYERS]; /* per hop */
+    size_t blk_counts[GNN_MAX_LAYERS], blk_src_ids[GNN_MAX_LAYERS], blk_rowptr[GNN_MAX_LAYERS],
+        blk_col[GNN_MAX_LAYERS], blk_cscptr[GNN_MAX_LAYERS], blk_cscrow[GNN_MAX_LAYERS],
+        blk_src_norm[GNN_MAX_LAYERS]; /* per hop; 0 when absent */
+    size_t x0;                          /* gathered X' (cap_src of hop L rows) */
+    size_t agg[GNN_MAX_LAYERS + 1];     /* per layer l: aggregation output */
+    size_t h[GNN_MAX_LAYERS + 1];       /* per layer l: H^l (l < L) or logits (l = L) */
+    size_t grad[GNN_MAX_LAYERS + 1];    /* per layer l: G^l = dLoss/dZ^l, fp32 */
+    size_t d_a[GNN_MAX_LAYERS + 1];     /* per layer l >= 2: dLoss/dA^l, fp32 */
+    size_t bwd_ws, bwd_ws_bytes;        /* update-backward workspace */
+    size_t loss_ws, loss_ws_bytes;      /* loss workspace */
+    size_t edges;                       /* int64 sampled edges of the step */
+    size_t loss;                        /* fp32 loss of the step */
+} gnn_step_layout;
+
+gnn_status gnn_train_step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_step_layout *out);
+gnn_status gnn_train_step_workspace_size(const gnn_model *m, int64_t graph_n, int64_t batch, size_t *bytes);
+/* Initialise a step workspace once (sampler state); keep using it for every
+ * step with the same model shape, graph size and batch. */
+gnn_status gnn_train_step_workspace_init(const gnn_model *m, int64_t graph_n, int64_t batch, void *ws,
+                                         size_t ws_bytes, gnn_stream s);
+
+/* One training step.  table/tdt/loc/row_stride as in gnn_gather_features
+ * (dim = m->dims[0]); labels [device] int64[graph n]; targets [device]
+ * int64[batch] distinct vertex ids; gcn_norm [device] (required for GCN).
+ * Writes m->dw, m->db, updates m->w, m->b in place, and writes the loss
+ * (loss_dev, fp32) and the number of sampled edges sum_l |E^l| (edges_dev,
+ * int64) when those pointers are not NULL. */
+gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                          gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
+                          const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
+                          float *loss_dev, int64_t *edges_dev, void *ws, size_t ws_bytes, gnn_stream s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GNN_H */

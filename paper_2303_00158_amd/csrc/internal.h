@@ -1,0 +1,157 @@
+// Internal declarations shared by the HIP sources of libgnn.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "gnn.h"
+
+namespace gnn {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+gnn_status fail(gnn_status code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+gnn_status launch_status(const char *what);  // hipGetLastError after a launch
+
+#define GNN_CHECK(cond, code, ...)                                   \
+    do {                                                             \
+        if (!(cond)) return ::gnn::fail((code), __VA_ARGS__);        \
+    } while (0)
+#define GNN_HIP(call)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return ::gnn::fail(GNN_EHIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+#define GNN_TRY(expr)                      \
+    do {                                   \
+        gnn_status st_ = (expr);           \
+        if (st_ != GNN_OK) return st_;     \
+    } while (0)
+#define GNN_LAUNCHED(what) GNN_TRY(::gnn::launch_status(what))
+
+inline hipStream_t stream_of(gnn_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+inline size_t dtype_size(int dt) { return dt == GNN_F32 ? 4 : 2; }
+
+// Carves aligned sub-buffers out of a caller workspace.  With base == nullptr
+// it only measures.
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+    size_t take(size_t bytes, size_t align = 256) {
+        off = round_up(off, align);
+        size_t at = off;
+        off += round_up(bytes, 8);
+        return at;
+    }
+    template <class T>
+    T *ptr(size_t at) const { return base ? reinterpret_cast<T *>(base + at) : nullptr; }
+};
+
+// Grid limit used for capacity-sized launches (1-D grids up to 2^31-1 blocks).
+constexpr int64_t kMaxGrid = (1ll << 31) - 1;
+
+// ---------------------------------------------------------------------------
+// device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+    _Float16 v = __builtin_bit_cast(_Float16, h);
+    return static_cast<float>(v);
+}
+
+// Typed element access: activations are float or raw bf16 bits (uint16_t).
+template <class T> struct Elem;
+template <> struct Elem<float> {
+    __device__ __forceinline__ static float load(const float *p, int64_t i) { return p[i]; }
+    __device__ __forceinline__ static void store(float *p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<uint16_t> {
+    __device__ __forceinline__ static float load(const uint16_t *p, int64_t i) { return bf16_to_f32(p[i]); }
+    __device__ __forceinline__ static void store(uint16_t *p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+// Four consecutive elements starting at p[i] (i a multiple of 4 and the row
+// 4-element aligned) as floats.
+__device__ __forceinline__ float4 load4(const float *p, int64_t i) {
+    return *reinterpret_cast<const float4 *>(p + i);
+}
+__device__ __forceinline__ float4 load4(const uint16_t *p, int64_t i) {
+    uint2 v = *reinterpret_cast<const uint2 *>(p + i);
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+__device__ __forceinline__ void store4(float *p, int64_t i, float4 v) { *reinterpret_cast<float4 *>(p + i) = v; }
+__device__ __forceinline__ void store4(uint16_t *p, int64_t i, float4 v) {
+    uint2 o;
+    o.x = static_cast<uint32_t>(f32_to_bf16(v.x)) | (static_cast<uint32_t>(f32_to_bf16(v.y)) << 16);
+    o.y = static_cast<uint32_t>(f32_to_bf16(v.z)) | (static_cast<uint32_t>(f32_to_bf16(v.w)) << 16);
+    *reinterpret_cast<uint2 *>(p + i) = o;
+}
+
+__device__ __forceinline__ int64_t dev_count(const int64_t *dev, int64_t fallback) {
+    return dev ? *dev : fallback;
+}
+
+// ---------------------------------------------------------------------------
+// building blocks implemented in scan.hip
+// ---------------------------------------------------------------------------
+// Exclusive scan of n int64 values: out[0] = 0, out[i+1] = in[0] + ... + in[i]
+// for i < n (so out has n+1 entries; out[n] is the total).  n is read from
+// n_dev when given (bounded by cap), else cap.  `total_to` (may be null)
+// receives the total as well.  tmp must hold scan_tmp_bytes(cap).
+size_t scan_tmp_bytes(int64_t cap);
+gnn_status exclusive_scan(const int64_t *in, int64_t *out, const int64_t *n_dev, int64_t cap, int64_t *total_to,
+                          void *tmp, hipStream_t s);
+
+// Stable LSD radix sort of (key, value) int32 pairs by key, keys in
+// [0, 2^key_bits).  n is read from n_dev (bounded by cap).  Results land in
+// keys_out / vals_out.  tmp must hold radix_tmp_bytes(cap).
+size_t radix_tmp_bytes(int64_t cap);
+gnn_status radix_sort_pairs(const int32_t *keys_in, const int32_t *vals_in, int32_t *keys_out, int32_t *vals_out,
+                            const int64_t *n_dev, int64_t cap, int key_bits, void *tmp, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// validation helpers (abi.hip)
+// ---------------------------------------------------------------------------
+gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const char *who);
+
+// Internal launchers reused by the training step (no host validation).
+gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,
+                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, hipStream_t s);
+gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
+                                hipStream_t s);
+gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
+                                int hbdt, float *d_src, hipStream_t s);
+gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
+                             int64_t cap_m, const float *w, const float *bias, int64_t n_out, int relu, int gemm_dt,
+                             void *out, int odt, hipStream_t s);
+size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m);
+gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
+                             int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt, float *dw,
+                             float *db, float *d_a, void *ws, hipStream_t s);
+size_t softmax_ce_ws_bytes(int64_t b);
+gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels,
+                             const int64_t *targets, float *g_out, float *loss_out, void *ws, hipStream_t s);
+gnn_status launch_sgd(float *w, const float *dw, int64_t n, float lr, hipStream_t s);
+size_t sampler_ws_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout);
+gnn_status launch_sampler_ws_init(void *ws, int64_t graph_n, hipStream_t s);
+gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
+                              const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
+                              bool want_csc, const gnn_block *out, void *ws, hipStream_t s);
+
+}  // namespace gnn

@@ -1,0 +1,165 @@
+// One training iteration composed from the kernels: sample L blocks, gather
+// X', L forward layers, loss, backward in reverse order (no input gradient
+// below the first layer), SGD.  Everything is enqueued on one stream and the
+// host never waits: counts produced on the device are read by later kernels.
+#include <algorithm>
+
+#include "internal.h"
+
+namespace gnn {
+
+namespace {
+
+__global__ void step_tail_kernel(const int64_t *c0, const int64_t *c1, const int64_t *c2, const int64_t *c3,
+                                 const float *loss_src, int64_t *edges, int64_t *edges_out, float *loss_out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int64_t e = c0[2];
+    if (c1) e += c1[2];
+    if (c2) e += c2[2];
+    if (c3) e += c3[2];
+    *edges = e;
+    if (edges_out) *edges_out = e;
+    if (loss_out) *loss_out = *loss_src;
+}
+
+int64_t k_of(const gnn_model *m, int l) {  // reduction width of layer l (1-based)
+    const int64_t f = m->dims[l - 1];
+    return m->kind == GNN_AGG_SAGE_MEAN ? 2 * f : f;
+}
+
+}  // namespace
+
+gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_step_layout *o) {
+    const int L = m->num_layers;
+    *o = gnn_step_layout{};
+    const int act = m->precision;
+    const size_t asz = dtype_size(act);
+    Carver c(nullptr);
+    // capacities per hop
+    int64_t cap_dst = batch;
+    size_t samp = 0;
+    for (int h = 0; h < L; ++h) {
+        const int64_t k = m->fanouts[h];
+        o->cap_dst[h] = cap_dst;
+        o->cap_nnz[h] = cap_dst * k;
+        o->cap_src[h] = std::min<int64_t>(cap_dst + cap_dst * k, std::max<int64_t>(graph_n, cap_dst));
+        samp = std::max(samp, sampler_ws_bytes(graph_n, cap_dst, static_cast<int32_t>(k)));
+        cap_dst = o->cap_src[h];
+    }
+    o->sampler_ws = c.take(samp);
+    o->sampler_ws_bytes = samp;
+    for (int h = 0; h < L; ++h) {
+        o->blk_counts[h] = c.take(4 * 8);
+        o->blk_src_ids[h] = c.take(static_cast<size_t>(o->cap_src[h]) * 8);
+        o->blk_rowptr[h] = c.take(static_cast<size_t>(o->cap_dst[h] + 1) * 8);
+        o->blk_col[h] = c.take(static_cast<size_t>(std::max<int64_t>(o->cap_nnz[h], 1)) * 4);
+        if (h < L - 1) {
+            o->blk_cscptr[h] = c.take(static_cast<size_t>(o->cap_src[h] + 1) * 8);
+            o->blk_cscrow[h] = c.take(static_cast<size_t>(std::max<int64_t>(o->cap_nnz[h], 1)) * 4);
+        }
+        if (m->kind == GNN_AGG_GCN_SYM) o->blk_src_norm[h] = c.take(static_cast<size_t>(o->cap_src[h]) * 4);
+    }
+    o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
+    size_t bwd = 0;
+    for (int l = 1; l <= L; ++l) {
+        const int hb = L - l;
+        const int64_t rows = o->cap_dst[hb];
+        o->agg[l] = c.take(static_cast<size_t>(rows) * m->dims[l - 1] * asz);
+        o->h[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
+        o->grad[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * 4);
+        if (l >= 2) o->d_a[l] = c.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
+        bwd = std::max(bwd, update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows));
+    }
+    o->bwd_ws = c.take(bwd);
+    o->bwd_ws_bytes = bwd;
+    o->loss_ws_bytes = softmax_ce_ws_bytes(batch);
+    o->loss_ws = c.take(o->loss_ws_bytes);
+    o->edges = c.take(8);
+    o->loss = c.take(4);
+    o->total_bytes = round_up(c.off, 256);
+    return GNN_OK;
+}
+
+static gnn_block block_view(const gnn_step_layout &o, int h, char *base) {
+    gnn_block b{};
+    b.cap_dst = o.cap_dst[h];
+    b.cap_src = o.cap_src[h];
+    b.cap_nnz = o.cap_nnz[h];
+    b.counts = reinterpret_cast<int64_t *>(base + o.blk_counts[h]);
+    b.src_ids = reinterpret_cast<int64_t *>(base + o.blk_src_ids[h]);
+    b.rowptr = reinterpret_cast<int64_t *>(base + o.blk_rowptr[h]);
+    b.col = reinterpret_cast<int32_t *>(base + o.blk_col[h]);
+    b.cscptr = o.blk_cscptr[h] ? reinterpret_cast<int64_t *>(base + o.blk_cscptr[h]) : nullptr;
+    b.cscrow = o.blk_cscrow[h] ? reinterpret_cast<int32_t *>(base + o.blk_cscrow[h]) : nullptr;
+    b.src_norm = o.blk_src_norm[h] ? reinterpret_cast<float *>(base + o.blk_src_norm[h]) : nullptr;
+    return b;
+}
+
+gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                          int tdt, int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
+                          uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
+                          hipStream_t s) {
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, g->n, batch, &o));
+    char *base = static_cast<char *>(ws);
+    const int L = m->num_layers;
+    const int act = m->precision;
+    gnn_block blk[GNN_MAX_LAYERS];
+    for (int h = 0; h < L; ++h) blk[h] = block_view(o, h, base);
+
+    // sampling: hop 1 around the targets, then outwards
+    for (int h = 0; h < L; ++h) {
+        const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
+        const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
+        GNN_TRY(launch_build_block(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h],
+                                   seed, step, h + 1, h < L - 1, &blk[h], base + o.sampler_ws, s));
+    }
+    // feature loading: rows of the input layer's sources
+    const gnn_block &b0 = blk[L - 1];
+    void *x0 = base + o.x0;
+    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act, s));
+
+    // forward
+    for (int l = 1; l <= L; ++l) {
+        const gnn_block &b = blk[L - l];
+        const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);
+        void *agg = base + o.agg[l];
+        const int64_t f_in = m->dims[l - 1];
+        GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
+        const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
+        GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
+                                  m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l], l < L ? act : GNN_F32,
+                                  s));
+    }
+    // loss on the targets
+    float *loss_slot = reinterpret_cast<float *>(base + o.loss);
+    GNN_TRY(launch_softmax_ce(reinterpret_cast<const float *>(base + o.h[L]), batch, m->dims[L], labels, targets,
+                              reinterpret_cast<float *>(base + o.grad[L]), loss_slot, base + o.loss_ws, s));
+    // backward
+    for (int l = L; l >= 1; --l) {
+        const gnn_block &b = blk[L - l];
+        const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);
+        const void *agg = base + o.agg[l];
+        const int64_t f_in = m->dims[l - 1];
+        const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
+        float *d_a = l > 1 ? reinterpret_cast<float *>(base + o.d_a[l]) : nullptr;
+        GNN_TRY(launch_update_bwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst,
+                                  m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l],
+                                  m->precision, m->dw[l - 1], m->db[l - 1], d_a, base + o.bwd_ws, s));
+        if (l > 1)
+            GNN_TRY(launch_aggregate_bwd(&b, m->kind, d_a, f_in, hin, act,
+                                         reinterpret_cast<float *>(base + o.grad[l - 1]), s));
+    }
+    // weight update
+    for (int l = 1; l <= L; ++l) {
+        GNN_TRY(launch_sgd(m->w[l - 1], m->dw[l - 1], k_of(m, l) * m->dims[l], lr, s));
+        GNN_TRY(launch_sgd(m->b[l - 1], m->db[l - 1], m->dims[l], lr, s));
+    }
+    step_tail_kernel<<<1, 64, 0, s>>>(blk[0].counts, L > 1 ? blk[1].counts : nullptr, L > 2 ? blk[2].counts : nullptr,
+                                      L > 3 ? blk[3].counts : nullptr, loss_slot,
+                                      reinterpret_cast<int64_t *>(base + o.edges), edges_dev, loss_dev);
+    GNN_LAUNCHED("step_tail");
+    return GNN_OK;
+}
+
+}  // namespace gnn

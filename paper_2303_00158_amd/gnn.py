@@ -1,0 +1,361 @@
+"""ctypes binding of libgnn.so (see include/gnn.h).
+
+Argument marshalling only: torch tensors supply device memory and the current
+HIP stream; every step runs in the library's kernels.  Importing this module
+does not need a GPU; calling anything that launches work does.  If the
+library has not been built the first call raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgnn.so")
+
+GNN_OK, GNN_EINVAL, GNN_ESIZE, GNN_EHIP, GNN_EUNSUPPORTED = 0, -1, -2, -3, -4
+GNN_F32, GNN_BF16, GNN_F16 = 0, 1, 2
+GNN_AGG_SAGE_MEAN, GNN_AGG_GCN_SYM = 0, 1
+GNN_LOC_DEVICE, GNN_LOC_HOST_PINNED = 0, 1
+GNN_MAX_LAYERS = 4
+
+_i64, _i32, _u64, _f32, _vp, _sz = (ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64, ctypes.c_float,
+                                    ctypes.c_void_p, ctypes.c_size_t)
+
+
+class GnnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class Graph(ctypes.Structure):
+    _fields_ = [("n", _i64), ("nnz", _i64), ("rowptr", _vp), ("col", _vp)]
+
+
+class Block(ctypes.Structure):
+    _fields_ = [("cap_dst", _i64), ("cap_src", _i64), ("cap_nnz", _i64), ("counts", _vp), ("src_ids", _vp),
+                ("rowptr", _vp), ("col", _vp), ("cscptr", _vp), ("cscrow", _vp), ("src_norm", _vp)]
+
+
+class Model(ctypes.Structure):
+    _fields_ = [("num_layers", _i32), ("kind", _i32), ("precision", _i32),
+                ("dims", _i32 * (GNN_MAX_LAYERS + 1)), ("fanouts", _i32 * GNN_MAX_LAYERS),
+                ("w", _vp * GNN_MAX_LAYERS), ("b", _vp * GNN_MAX_LAYERS),
+                ("dw", _vp * GNN_MAX_LAYERS), ("db", _vp * GNN_MAX_LAYERS)]
+
+
+_ML = GNN_MAX_LAYERS
+
+
+class StepLayout(ctypes.Structure):
+    _fields_ = [("total_bytes", _sz), ("sampler_ws", _sz), ("sampler_ws_bytes", _sz),
+                ("cap_dst", _i64 * _ML), ("cap_src", _i64 * _ML), ("cap_nnz", _i64 * _ML),
+                ("blk_counts", _sz * _ML), ("blk_src_ids", _sz * _ML), ("blk_rowptr", _sz * _ML),
+                ("blk_col", _sz * _ML), ("blk_cscptr", _sz * _ML), ("blk_cscrow", _sz * _ML),
+                ("blk_src_norm", _sz * _ML),
+                ("x0", _sz), ("agg", _sz * (_ML + 1)), ("h", _sz * (_ML + 1)), ("grad", _sz * (_ML + 1)),
+                ("d_a", _sz * (_ML + 1)), ("bwd_ws", _sz), ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
+                ("loss_ws_bytes", _sz), ("edges", _sz), ("loss", _sz)]
+
+
+_P = ctypes.POINTER
+_SIGNATURES = {
+    "gnn_last_error": (ctypes.c_char_p, []),
+    "gnn_abi_version": (_i32, []),
+    "gnn_gcn_norm": (_i32, [_P(Graph), _vp, _vp]),
+    "gnn_block_bounds": (_i32, [_i64, _i64, _i32, _P(_i64), _P(_i64)]),
+    "gnn_sampler_workspace_size": (_i32, [_i64, _i64, _i32, _P(_sz)]),
+    "gnn_sampler_workspace_init": (_i32, [_vp, _sz, _i64, _vp]),
+    "gnn_build_block": (_i32, [_P(Graph), _vp, _vp, _vp, _i32, _u64, _u64, _i32, _i32, _P(Block), _vp, _sz, _vp]),
+    "gnn_gather_features": (_i32, [_vp, _i32, _i32, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _i32, _vp]),
+    "gnn_aggregate_fwd": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
+    "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
+    "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp]),
+    "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _P(_sz)]),
+    "gnn_update_bwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _sz,
+                              _vp]),
+    "gnn_softmax_ce_workspace_size": (_i32, [_i64, _P(_sz)]),
+    "gnn_softmax_ce": (_i32, [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gnn_sgd": (_i32, [_vp, _vp, _i64, _f32, _vp]),
+    "gnn_train_step_layout": (_i32, [_P(Model), _i64, _i64, _P(StepLayout)]),
+    "gnn_train_step_workspace_size": (_i32, [_P(Model), _i64, _i64, _P(_sz)]),
+    "gnn_train_step_workspace_init": (_i32, [_P(Model), _i64, _i64, _vp, _sz, _vp]),
+    "gnn_train_step": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64, _u64, _u64, _f32,
+                              _vp, _vp, _vp, _sz, _vp]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgnn.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2303_00158_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_symbols() -> List[str]:
+    return list(_SIGNATURES)
+
+
+def _check(code: int) -> None:
+    if code != GNN_OK:
+        raise GnnError(code, lib().gnn_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    return {torch.float32: GNN_F32, torch.bfloat16: GNN_BF16, torch.float16: GNN_F16}[dt]
+
+
+def torch_dtype(code: int) -> torch.dtype:
+    return {GNN_F32: torch.float32, GNN_BF16: torch.bfloat16, GNN_F16: torch.float16}[code]
+
+
+def _aligned_empty(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# graph and blocks
+# ---------------------------------------------------------------------------
+
+class DeviceGraph:
+    """An int64 CSR on the device plus its ctypes descriptor."""
+
+    def __init__(self, rowptr: torch.Tensor, col: torch.Tensor):
+        assert rowptr.dtype == torch.int64 and col.dtype == torch.int64
+        self.rowptr = rowptr.contiguous()
+        self.col = col.contiguous()
+        self.n = self.rowptr.numel() - 1
+        self.c = Graph(self.n, self.col.numel(), _ptr(self.rowptr), _ptr(self.col))
+
+
+def gcn_norm(graph: DeviceGraph, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if out is None:
+        out = torch.empty(graph.n, dtype=torch.float32, device=graph.rowptr.device)
+    _check(lib().gnn_gcn_norm(ctypes.byref(graph.c), _ptr(out), _stream(stream)))
+    return out
+
+
+def block_bounds(graph_n: int, cap_dst: int, fanout: int):
+    cs, cn = _i64(), _i64()
+    _check(lib().gnn_block_bounds(graph_n, cap_dst, fanout, ctypes.byref(cs), ctypes.byref(cn)))
+    return cs.value, cn.value
+
+
+class DeviceBlock:
+    """Device buffers of one block at its capacity bounds."""
+
+    def __init__(self, graph_n: int, cap_dst: int, fanout: int, want_csc: bool, want_norm: bool, device):
+        cap_src, cap_nnz = block_bounds(graph_n, cap_dst, fanout)
+        z = lambda n, dt: torch.zeros(max(n, 1), dtype=dt, device=device)  # noqa: E731
+        self.counts = z(4, torch.int64)
+        self.src_ids = z(cap_src, torch.int64)
+        self.rowptr = z(cap_dst + 1, torch.int64)
+        self.col = z(cap_nnz, torch.int32)
+        self.cscptr = z(cap_src + 1, torch.int64) if want_csc else None
+        self.cscrow = z(cap_nnz, torch.int32) if want_csc else None
+        self.src_norm = z(cap_src, torch.float32) if want_norm else None
+        self.c = Block(cap_dst, cap_src, cap_nnz, _ptr(self.counts), _ptr(self.src_ids), _ptr(self.rowptr),
+                       _ptr(self.col), _ptr(self.cscptr), _ptr(self.cscrow), _ptr(self.src_norm))
+
+    def host(self) -> dict:
+        """Copy the used part of the block to host numpy arrays (synchronises)."""
+        c = self.counts.cpu().tolist()
+        n_dst, n_src, nnz = int(c[0]), int(c[1]), int(c[2])
+        out = {
+            "n_dst": n_dst, "n_src": n_src, "nnz": nnz,
+            "src_ids": self.src_ids[:n_src].cpu().numpy(),
+            "rowptr": self.rowptr[:n_dst + 1].cpu().numpy(),
+            "col": self.col[:nnz].cpu().numpy(),
+        }
+        if self.cscptr is not None:
+            out["cscptr"] = self.cscptr[:n_src + 1].cpu().numpy()
+            out["cscrow"] = self.cscrow[:nnz].cpu().numpy()
+        if self.src_norm is not None:
+            out["src_norm"] = self.src_norm[:n_src].cpu().numpy()
+        return out
+
+
+def sampler_workspace(graph_n: int, cap_dst: int, fanout: int, device, stream=None) -> torch.Tensor:
+    nb = _sz()
+    _check(lib().gnn_sampler_workspace_size(graph_n, cap_dst, fanout, ctypes.byref(nb)))
+    ws = _aligned_empty(nb.value, device)
+    _check(lib().gnn_sampler_workspace_init(_ptr(ws), ws.numel(), graph_n, _stream(stream)))
+    return ws
+
+
+def build_block(graph: DeviceGraph, dst_ids: torch.Tensor, fanout: int, seed: int, step: int, hop: int,
+                out: DeviceBlock, ws: torch.Tensor, n_dst_dev: Optional[torch.Tensor] = None,
+                gcn_norm_t: Optional[torch.Tensor] = None, want_csc: bool = True, stream=None) -> DeviceBlock:
+    _check(lib().gnn_build_block(ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(dst_ids), _ptr(n_dst_dev), fanout,
+                                 seed, step, hop, int(want_csc), ctypes.byref(out.c), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# kernels of one layer
+# ---------------------------------------------------------------------------
+
+def gather_features(table: torch.Tensor, ids: torch.Tensor, out: torch.Tensor, n_ids_dev: Optional[torch.Tensor] = None,
+                    loc: int = GNN_LOC_DEVICE, row_stride: Optional[int] = None, stream=None) -> torch.Tensor:
+    n_rows, dim = table.shape
+    rs = table.stride(0) if row_stride is None else row_stride
+    _check(lib().gnn_gather_features(_ptr(table), dtype_code(table.dtype), loc, n_rows, dim, rs, _ptr(ids),
+                                     _ptr(n_ids_dev), out.shape[0], _ptr(out), dtype_code(out.dtype),
+                                     _stream(stream)))
+    return out
+
+
+def aggregate_fwd(block: DeviceBlock, kind: int, h_src: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    f = h_src.shape[1]
+    _check(lib().gnn_aggregate_fwd(ctypes.byref(block.c), kind, _ptr(h_src), dtype_code(h_src.dtype), f, _ptr(out),
+                                   dtype_code(out.dtype), _stream(stream)))
+    return out
+
+
+def aggregate_bwd(block: DeviceBlock, kind: int, d_a: torch.Tensor, f: int, d_src: torch.Tensor,
+                  h_below: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    hb_code = dtype_code(h_below.dtype) if h_below is not None else GNN_F32
+    _check(lib().gnn_aggregate_bwd(ctypes.byref(block.c), kind, _ptr(d_a), f, _ptr(h_below), hb_code, _ptr(d_src),
+                                   _stream(stream)))
+    return d_src
+
+
+def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],
+               out: torch.Tensor, relu: bool, gemm_dtype: int, m_dev: Optional[torch.Tensor] = None,
+               cap_m: Optional[int] = None, stream=None) -> torch.Tensor:
+    cap = a_self.shape[0] if cap_m is None else cap_m
+    _check(lib().gnn_update_fwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev), cap,
+                                _ptr(w), _ptr(bias), w.shape[1], int(relu), gemm_dtype, _ptr(out),
+                                dtype_code(out.dtype), _stream(stream)))
+    return out
+
+
+def update_bwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, g: torch.Tensor,
+               dw: torch.Tensor, db: Optional[torch.Tensor], d_a: Optional[torch.Tensor], gemm_dtype: int,
+               m_dev: Optional[torch.Tensor] = None, cap_m: Optional[int] = None, ws: Optional[torch.Tensor] = None,
+               stream=None):
+    cap = a_self.shape[0] if cap_m is None else cap_m
+    K = a_self.shape[1] * (2 if a_nbr is not None else 1)
+    if ws is None:
+        nb = _sz()
+        _check(lib().gnn_update_bwd_workspace_size(K, w.shape[1], cap, ctypes.byref(nb)))
+        ws = _aligned_empty(nb.value, a_self.device)
+    _check(lib().gnn_update_bwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev),
+                                cap, _ptr(w), _ptr(g), w.shape[1], gemm_dtype, _ptr(dw), _ptr(db), _ptr(d_a),
+                                _ptr(ws), ws.numel(), _stream(stream)))
+    return dw, db, d_a
+
+
+def softmax_ce(logits: torch.Tensor, labels: torch.Tensor, targets: Optional[torch.Tensor], g_out: torch.Tensor,
+               loss_out: torch.Tensor, stream=None):
+    b, c = logits.shape
+    nb = _sz()
+    _check(lib().gnn_softmax_ce_workspace_size(b, ctypes.byref(nb)))
+    ws = _aligned_empty(nb.value, logits.device)
+    _check(lib().gnn_softmax_ce(_ptr(logits), b, c, _ptr(labels), _ptr(targets), _ptr(g_out), _ptr(loss_out),
+                                _ptr(ws), ws.numel(), _stream(stream)))
+    return g_out, loss_out
+
+
+def sgd(w: torch.Tensor, dw: torch.Tensor, lr: float, stream=None) -> torch.Tensor:
+    _check(lib().gnn_sgd(_ptr(w), _ptr(dw), w.numel(), float(lr), _stream(stream)))
+    return w
+
+
+# ---------------------------------------------------------------------------
+# whole training step
+# ---------------------------------------------------------------------------
+
+class Trainer:
+    """Owns the model buffers (fp32 master weights, gradients) and the step
+    workspace, and calls gnn_train_step."""
+
+    def __init__(self, kind: int, dims: Sequence[int], fanouts: Sequence[int], precision: int, graph_n: int,
+                 batch: int, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor], device="cuda"):
+        L = len(dims) - 1
+        assert len(fanouts) == L and len(weights) == L and len(biases) == L
+        self.device = torch.device(device)
+        self.kind, self.dims, self.fanouts, self.precision = kind, list(dims), list(fanouts), precision
+        self.graph_n, self.batch = graph_n, batch
+        self.w = [w.to(self.device, torch.float32).contiguous().clone() for w in weights]
+        self.b = [b.to(self.device, torch.float32).contiguous().clone() for b in biases]
+        self.dw = [torch.zeros_like(w) for w in self.w]
+        self.db = [torch.zeros_like(b) for b in self.b]
+        m = Model()
+        m.num_layers, m.kind, m.precision = L, kind, precision
+        for i, d in enumerate(dims):
+            m.dims[i] = d
+        for i, k in enumerate(fanouts):
+            m.fanouts[i] = k
+        for l in range(L):
+            m.w[l], m.b[l], m.dw[l], m.db[l] = _ptr(self.w[l]), _ptr(self.b[l]), _ptr(self.dw[l]), _ptr(self.db[l])
+        self.model = m
+        self.layout = StepLayout()
+        _check(lib().gnn_train_step_layout(ctypes.byref(m), graph_n, batch, ctypes.byref(self.layout)))
+        self.ws = _aligned_empty(self.layout.total_bytes, self.device)
+        _check(lib().gnn_train_step_workspace_init(ctypes.byref(m), graph_n, batch, _ptr(self.ws), self.ws.numel(),
+                                                   _stream(None)))
+        self.loss = torch.zeros(1, dtype=torch.float32, device=self.device)
+        self.edges = torch.zeros(1, dtype=torch.int64, device=self.device)
+
+    def step(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets: torch.Tensor, seed: int,
+             step: int, lr: float, gcn_norm_t: Optional[torch.Tensor] = None, loc: int = GNN_LOC_DEVICE,
+             stream=None) -> None:
+        _check(lib().gnn_train_step(ctypes.byref(self.model), ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(table),
+                                    dtype_code(table.dtype), loc, table.stride(0), _ptr(labels), _ptr(targets),
+                                    self.batch, seed, step, float(lr), _ptr(self.loss), _ptr(self.edges),
+                                    _ptr(self.ws), self.ws.numel(), _stream(stream)))
+
+    # --- views into the workspace (for inspection and tests) ---------------
+    def _view(self, off: int, numel: int, dtype: torch.dtype) -> torch.Tensor:
+        esz = torch.empty(0, dtype=dtype).element_size()
+        return self.ws[off:off + numel * esz].view(dtype)
+
+    def block_view(self, h: int) -> dict:
+        """Host copy of the block built at hop h (1-based)."""
+        lay = self.layout
+        i = h - 1
+        counts = self._view(lay.blk_counts[i], 4, torch.int64).cpu().tolist()
+        n_dst, n_src, nnz = counts[0], counts[1], counts[2]
+        out = {
+            "n_dst": n_dst, "n_src": n_src, "nnz": nnz,
+            "src_ids": self._view(lay.blk_src_ids[i], n_src, torch.int64).cpu().numpy(),
+            "rowptr": self._view(lay.blk_rowptr[i], n_dst + 1, torch.int64).cpu().numpy(),
+            "col": self._view(lay.blk_col[i], nnz, torch.int32).cpu().numpy(),
+        }
+        if lay.blk_cscptr[i]:
+            out["cscptr"] = self._view(lay.blk_cscptr[i], n_src + 1, torch.int64).cpu().numpy()
+            out["cscrow"] = self._view(lay.blk_cscrow[i], nnz, torch.int32).cpu().numpy()
+        return out
+
+    def act_dtype(self) -> torch.dtype:
+        return torch_dtype(self.precision)
+
+    def tensor(self, name: str, layer: int, rows: int, cols: int, dtype: torch.dtype) -> torch.Tensor:
+        off = getattr(self.layout, name)[layer] if name in ("agg", "h", "grad", "d_a") else getattr(self.layout, name)
+        return self._view(off, rows * cols, dtype).view(rows, cols)

@@ -1,0 +1,116 @@
+"""The C ABI library loads, exports every entry point its header declares,
+and rejects bad arguments on the host before touching the GPU.  CPU only:
+nothing here launches a kernel."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnn.h")
+
+
+@pytest.fixture(scope="module")
+def gnn():
+    from paper_2303_00158_amd import gnn as g
+    if not os.path.exists(g.LIB_PATH):
+        from paper_2303_00158_amd import build
+        build.build()
+    return g
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gnn_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_paper_calls():
+    names = header_functions()
+    for f in ("gnn_build_block", "gnn_gather_features", "gnn_aggregate_fwd", "gnn_aggregate_bwd",
+              "gnn_update_fwd", "gnn_update_bwd", "gnn_train_step"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(gnn):
+    out = subprocess.run(["nm", "-D", "--defined-only", gnn.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(line.split()[-1] for line in out.stdout.splitlines() if line.strip())
+    missing = [f for f in header_functions() if f not in exported]
+    assert not missing, missing
+    lib = gnn.lib()
+    for f in header_functions():
+        assert hasattr(lib, f)
+    # the binding declares a signature for every header function
+    assert sorted(gnn.exported_symbols()) == header_functions()
+
+
+def test_host_validation_errors(gnn):
+    lib = gnn.lib()
+    cs, cn = ctypes.c_int64(), ctypes.c_int64()
+    assert lib.gnn_block_bounds(100, 10, 0, ctypes.byref(cs), ctypes.byref(cn)) == gnn.GNN_EINVAL
+    assert b"fanout" in lib.gnn_last_error()
+    assert lib.gnn_block_bounds(100, 10, 25, ctypes.byref(cs), ctypes.byref(cn)) == gnn.GNN_OK
+    assert (cs.value, cn.value) == (100, 250)
+    assert lib.gnn_block_bounds(10**9, 1024, 25, ctypes.byref(cs), ctypes.byref(cn)) == gnn.GNN_OK
+    assert (cs.value, cn.value) == (1024 * 26, 1024 * 25)
+    assert lib.gnn_last_error() == b""
+    # NULL weights, unsupported dtypes, bad sizes: rejected before any launch
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+                              gnn.GNN_F32, None) == gnn.GNN_EINVAL
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F16, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+                              gnn.GNN_F32, None) == gnn.GNN_EUNSUPPORTED
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 0, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+                              gnn.GNN_F32, None) == gnn.GNN_EINVAL
+    assert lib.gnn_gather_features(None, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 10, 4, 4, None, None, 3, None,
+                                   gnn.GNN_F16, None) == gnn.GNN_EUNSUPPORTED
+    assert lib.gnn_gather_features(None, gnn.GNN_F32, 7, 10, 4, 4, None, None, 3, None,
+                                   gnn.GNN_F32, None) == gnn.GNN_EINVAL
+    assert lib.gnn_gather_features(None, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 10, 4, 2, None, None, 3, None,
+                                   gnn.GNN_F32, None) == gnn.GNN_EINVAL
+    assert lib.gnn_sgd(None, None, -1, 0.1, None) == gnn.GNN_EINVAL
+    assert lib.gnn_aggregate_fwd(None, 0, None, 0, 4, None, 0, None) == gnn.GNN_EINVAL
+    assert lib.gnn_softmax_ce(None, 4, 0, None, None, None, None, None, 0, None) == gnn.GNN_EINVAL
+    blk = gnn.Block(4, 8, 8, None, None, None, None, None, None, None)
+    assert lib.gnn_aggregate_bwd(ctypes.byref(blk), 0, None, 4, None, 0, None, None) == gnn.GNN_EINVAL
+    g = gnn.Graph(10, 20, None, None)
+    assert lib.gnn_build_block(ctypes.byref(g), None, None, None, 5, 0, 0, 1, 1, ctypes.byref(blk), None, 0,
+                               None) == gnn.GNN_EINVAL
+    nb = ctypes.c_size_t()
+    assert lib.gnn_update_bwd_workspace_size(0, 4, 4, ctypes.byref(nb)) == gnn.GNN_EINVAL
+
+
+def _model(gnn, kind, dims, fanouts, precision):
+    m = gnn.Model()
+    m.num_layers, m.kind, m.precision = len(dims) - 1, kind, precision
+    for i, d in enumerate(dims):
+        m.dims[i] = d
+    for i, k in enumerate(fanouts):
+        m.fanouts[i] = k
+    return m
+
+
+def test_step_layout_capacities_and_disjoint_buffers(gnn):
+    lib = gnn.lib()
+    m = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (100, 256, 47), (25, 10), gnn.GNN_BF16)
+    lay = gnn.StepLayout()
+    assert lib.gnn_train_step_layout(ctypes.byref(m), 2_449_029, 1024, ctypes.byref(lay)) == gnn.GNN_OK
+    # no-duplicate upper bounds of the two hops
+    assert list(lay.cap_dst[:2]) == [1024, 26_624]
+    assert list(lay.cap_nnz[:2]) == [25_600, 266_240]
+    assert list(lay.cap_src[:2]) == [26_624, 292_864]
+    # hop 1 (the last layer's block) has a transpose, hop 2 (first layer) has none
+    assert lay.blk_cscptr[0] and not lay.blk_cscptr[1]
+    offs = [lay.sampler_ws, lay.x0, lay.bwd_ws, lay.loss_ws, lay.edges, lay.loss]
+    offs += [lay.blk_counts[h] for h in range(2)] + [lay.agg[l] for l in (1, 2)] + [lay.h[l] for l in (1, 2)]
+    assert len(set(offs)) == len(offs)
+    assert max(offs) < lay.total_bytes
+    nb = ctypes.c_size_t()
+    assert lib.gnn_train_step_workspace_size(ctypes.byref(m), 2_449_029, 1024, ctypes.byref(nb)) == gnn.GNN_OK
+    assert nb.value == lay.total_bytes
+    bad = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (100, 256, 47), (25, 0), gnn.GNN_BF16)
+    assert lib.gnn_train_step_workspace_size(ctypes.byref(bad), 1000, 10, ctypes.byref(nb)) == gnn.GNN_EINVAL
+    bad = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (100, 256, 47), (25, 10), gnn.GNN_F16)
+    assert lib.gnn_train_step_workspace_size(ctypes.byref(bad), 1000, 10, ctypes.byref(nb)) == gnn.GNN_EUNSUPPORTED
+    assert lib.gnn_train_step_workspace_size(ctypes.byref(m), 1000, 2000, ctypes.byref(nb)) == gnn.GNN_EINVAL

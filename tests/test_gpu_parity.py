@@ -1,0 +1,455 @@
+"""Parity of every C-ABI call against the CPU oracle, on the GPU.
+
+Integer work (sampling, block ids, transposes, gathers) must match bit for
+bit.  Floating point is compared normwise, max|x - r| / max|r|, against
+1e-4 (fp32 arithmetic) or 2e-2 (bf16 storage / GEMM operands), with the
+oracle rounding at the same points as the kernels.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests import dense
+
+pytestmark = pytest.mark.gpu
+
+gnn = pytest.importorskip("paper_2303_00158_amd.gnn")
+
+DEV = torch.device("cuda:0")
+TOL = {oracle.F32: 1e-4, oracle.BF16: 2e-2}
+
+
+def relerr(got, want):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    assert got.shape == want.shape, (got.shape, want.shape)
+    den = max(np.abs(want).max() if want.size else 0.0, 1e-30)
+    return float(np.abs(got - want).max() / den) if want.size else 0.0
+
+
+def to_np_act(t: torch.Tensor) -> np.ndarray:
+    """Device activation -> oracle array (bf16 as raw uint16 bits)."""
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16).copy()
+    return t.numpy().copy()
+
+
+def from_np_act(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def upload_block(blk: "oracle.Block", src_norm=None) -> "gnn.DeviceBlock":
+    """Device copy of an oracle block (capacities = exact sizes)."""
+    b = gnn.DeviceBlock.__new__(gnn.DeviceBlock)
+    mk = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dtype=dt) if len(a) else np.zeros(1, dt)).to(DEV)  # noqa
+    b.counts = torch.tensor([blk.n_dst, blk.n_src, blk.nnz, 0], dtype=torch.int64, device=DEV)
+    b.src_ids = mk(blk.src_ids, np.int64)
+    b.rowptr = mk(blk.rowptr, np.int64)
+    b.col = mk(blk.col, np.int32)
+    b.cscptr = mk(blk.cscptr, np.int64)
+    b.cscrow = mk(blk.cscrow, np.int32)
+    b.src_norm = mk(src_norm, np.float32) if src_norm is not None else None
+    b.c = gnn.Block(blk.n_dst, blk.n_src, blk.nnz, b.counts.data_ptr(), b.src_ids.data_ptr(), b.rowptr.data_ptr(),
+                    b.col.data_ptr(), b.cscptr.data_ptr(), b.cscrow.data_ptr(),
+                    b.src_norm.data_ptr() if b.src_norm is not None else None)
+    return b
+
+
+def test_library_is_the_hip_build():
+    assert gnn.lib().gnn_abi_version() == 1
+    x = torch.ones(4, device=DEV)
+    gnn.sgd(x, torch.ones(4, device=DEV), 0.5)
+    torch.cuda.synchronize()
+    assert torch.equal(x.cpu(), torch.full((4,), 0.5))
+
+
+# ---------------------------------------------------------------------------
+# GCN norms
+# ---------------------------------------------------------------------------
+
+def test_gcn_norm_bitexact():
+    deg = np.concatenate([np.arange(0, 5000), np.array([65535, 65536, 999_999, 1_000_000, 123_456_789 // 100])])
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int64)
+    g = gnn.DeviceGraph(torch.from_numpy(rowptr).to(DEV), torch.zeros(1, dtype=torch.int64, device=DEV))
+    got = gnn.gcn_norm(g).cpu().numpy()
+    want = oracle.gcn_norm(rowptr)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# sampler
+# ---------------------------------------------------------------------------
+
+def _graph_cases():
+    rng = np.random.default_rng(0)
+    rp, cl = dense.small_multigraph(rng, 300, avg_deg=8, hubs=3, isolated=10)
+    yield "multigraph300", rp, cl
+    rp, cl = workloads.rmat_graph(20_000, 150_000, seed=1)
+    yield "rmat20k", rp.numpy(), cl.numpy()
+    rp, cl = workloads.er_graph(10_000, 50_000, seed=0)
+    yield "er10k", rp.numpy(), cl.numpy()
+
+
+@pytest.mark.parametrize("fanout", [1, 5, 25, 70, 300])
+def test_build_block_bitexact(fanout):
+    for name, rowptr, col in _graph_cases():
+        n = rowptr.size - 1
+        g = gnn.DeviceGraph(torch.from_numpy(rowptr).to(DEV), torch.from_numpy(col).to(DEV))
+        nrm_d = gnn.gcn_norm(g)
+        nrm_h = oracle.gcn_norm(rowptr)
+        rng = np.random.default_rng(fanout)
+        n_dst = min(n, 257)
+        dst = rng.choice(n, size=n_dst, replace=False).astype(np.int64)
+        # chain two hops: hop 2 reads hop 1's sources and its device count
+        blk1 = gnn.DeviceBlock(n, n_dst, fanout, True, True, DEV)
+        ws = gnn.sampler_workspace(n, blk1.c.cap_src, fanout, DEV)
+        gnn.build_block(g, torch.from_numpy(dst).to(DEV), fanout, 7, 3, 1, blk1, ws, gcn_norm_t=nrm_d)
+        blk2 = gnn.DeviceBlock(n, blk1.c.cap_src, fanout, True, True, DEV)
+        gnn.build_block(g, blk1.src_ids, fanout, 7, 3, 2, blk2, ws, n_dst_dev=blk1.counts[1:2], gcn_norm_t=nrm_d)
+        torch.cuda.synchronize()
+        ref1 = oracle.build_block(rowptr, col, dst, fanout, 7, 3, 1)
+        ref2 = oracle.build_block(rowptr, col, ref1.src_ids, fanout, 7, 3, 2)
+        for got, ref in ((blk1.host(), ref1), (blk2.host(), ref2)):
+            assert got["n_dst"] == ref.n_dst and got["n_src"] == ref.n_src and got["nnz"] == ref.nnz, name
+            assert np.array_equal(got["src_ids"], ref.src_ids), name
+            assert np.array_equal(got["rowptr"], ref.rowptr), name
+            assert np.array_equal(got["col"], ref.col), name
+            assert np.array_equal(got["cscptr"], ref.cscptr), name
+            assert np.array_equal(got["cscrow"], ref.cscrow), name
+            assert np.array_equal(got["src_norm"].view(np.uint32), nrm_h[ref.src_ids].view(np.uint32)), name
+        # the workspace is left clean: rebuilding gives the same block
+        gnn.build_block(g, torch.from_numpy(dst).to(DEV), fanout, 7, 3, 1, blk1, ws, gcn_norm_t=nrm_d)
+        torch.cuda.synchronize()
+        again = blk1.host()
+        assert np.array_equal(again["col"], ref1.col) and np.array_equal(again["src_ids"], ref1.src_ids)
+
+
+def test_build_block_degenerate_cases():
+    # isolated destinations, a destination whose neighbours are all destinations, an empty batch
+    rowptr = np.array([0, 0, 2, 4, 4, 5], dtype=np.int64)
+    col = np.array([2, 3, 1, 1, 0], dtype=np.int64)
+    n = 5
+    g = gnn.DeviceGraph(torch.from_numpy(rowptr).to(DEV), torch.from_numpy(col).to(DEV))
+    ws = gnn.sampler_workspace(n, 16, 3, DEV)
+    for dst in ([0, 3], [1, 2, 3], [4, 0], [2]):
+        d = np.array(dst, dtype=np.int64)
+        blk = gnn.DeviceBlock(n, len(dst), 3, True, False, DEV)
+        gnn.build_block(g, torch.from_numpy(d).to(DEV), 3, 0, 0, 1, blk, ws)
+        torch.cuda.synchronize()
+        got = blk.host()
+        ref = oracle.build_block(rowptr, col, d, 3, 0, 0, 1)
+        assert np.array_equal(got["src_ids"], ref.src_ids) and np.array_equal(got["col"], ref.col)
+        assert np.array_equal(got["cscptr"], ref.cscptr) and np.array_equal(got["cscrow"], ref.cscrow)
+    # n_dst = 0 through a device count
+    blk = gnn.DeviceBlock(n, 4, 3, True, False, DEV)
+    zero = torch.zeros(1, dtype=torch.int64, device=DEV)
+    gnn.build_block(g, torch.zeros(4, dtype=torch.int64, device=DEV), 3, 0, 0, 1, blk, ws, n_dst_dev=zero)
+    torch.cuda.synchronize()
+    got = blk.host()
+    assert got["n_dst"] == 0 and got["n_src"] == 0 and got["nnz"] == 0 and got["cscptr"].tolist() == [0]
+
+
+def test_build_block_rejects_bad_arguments():
+    rowptr = torch.tensor([0, 1, 2], dtype=torch.int64, device=DEV)
+    col = torch.tensor([1, 0], dtype=torch.int64, device=DEV)
+    g = gnn.DeviceGraph(rowptr, col)
+    ws = gnn.sampler_workspace(2, 2, 1, DEV)
+    blk = gnn.DeviceBlock(2, 2, 1, True, False, DEV)
+    with pytest.raises(gnn.GnnError) as e:
+        gnn.build_block(g, torch.tensor([0, 1], device=DEV), 0, 0, 0, 1, blk, ws)
+    assert e.value.code == gnn.GNN_EINVAL
+    small = torch.empty(256, dtype=torch.uint8, device=DEV)
+    with pytest.raises(gnn.GnnError) as e:
+        gnn.build_block(g, torch.tensor([0, 1], device=DEV), 1, 0, 0, 1, blk, small)
+    assert e.value.code == gnn.GNN_ESIZE
+
+
+# ---------------------------------------------------------------------------
+# gather
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dim", [4, 13, 100, 128, 768])
+def test_gather_bitexact(dim):
+    rng = np.random.default_rng(dim)
+    n = 5000
+    table = rng.standard_normal((n, dim)).astype(np.float32)
+    table.view(np.uint32)[7, 1] = 0x7FC0BEEF
+    ids = rng.integers(0, n, size=3001).astype(np.int64)
+    ids[:3] = 7
+    t_d = torch.from_numpy(table).to(DEV)
+    ids_d = torch.from_numpy(ids).to(DEV)
+    out = torch.empty((ids.size, dim), dtype=torch.float32, device=DEV)
+    gnn.gather_features(t_d, ids_d, out)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), oracle.gather(table, ids, oracle.F32).view(np.uint32))
+    out_b = torch.empty((ids.size, dim), dtype=torch.bfloat16, device=DEV)
+    gnn.gather_features(t_d, ids_d, out_b)
+    assert np.array_equal(to_np_act(out_b), oracle.gather(table, ids, oracle.BF16))
+    # fp16 table -> bf16 and -> fp32
+    h16 = table.astype(np.float16)
+    h_d = torch.from_numpy(h16).to(DEV)
+    gnn.gather_features(h_d, ids_d, out_b)
+    assert np.array_equal(to_np_act(out_b), oracle.gather(h16, ids, oracle.BF16))
+    gnn.gather_features(h_d, ids_d, out)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), oracle.gather(h16, ids, oracle.F32).view(np.uint32))
+    # a device count below the capacity leaves the tail untouched
+    out.fill_(-5.0)
+    n_dev = torch.tensor([1000], dtype=torch.int64, device=DEV)
+    gnn.gather_features(t_d, ids_d, out, n_ids_dev=n_dev)
+    o = out.cpu().numpy()
+    assert np.array_equal(o[:1000].view(np.uint32), table[ids[:1000]].view(np.uint32)) and np.all(o[1000:] == -5.0)
+
+
+def test_gather_pinned_host_table_zero_copy():
+    rng = np.random.default_rng(3)
+    n, dim = 4096, 96
+    table = torch.from_numpy(rng.standard_normal((n, dim)).astype(np.float16)).pin_memory()
+    ids = rng.integers(0, n, size=777).astype(np.int64)
+    out = torch.empty((ids.size, dim), dtype=torch.bfloat16, device=DEV)
+    gnn.gather_features(table, torch.from_numpy(ids).to(DEV), out, loc=gnn.GNN_LOC_HOST_PINNED)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_act(out), oracle.gather(table.numpy(), ids, oracle.BF16))
+
+
+# ---------------------------------------------------------------------------
+# aggregation with oracle-supplied blocks
+# ---------------------------------------------------------------------------
+
+def _oracle_block(seed, n=3000, n_dst=400, fanout=12):
+    rp, cl = workloads.rmat_graph(n, n * 6, seed=seed)
+    rp, cl = rp.numpy(), cl.numpy()
+    rng = np.random.default_rng(seed)
+    dst = rng.choice(n, size=n_dst, replace=False).astype(np.int64)
+    blk = oracle.build_block(rp, cl, dst, fanout, seed, 0, 1)
+    nrm = oracle.gcn_norm(rp)[blk.src_ids]
+    return blk, nrm
+
+
+def _act(rng, rows, f, code):
+    x = rng.standard_normal((rows, f)).astype(np.float32)
+    return oracle.f32_to_bf16_bits(x) if code == oracle.BF16 else x
+
+
+@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
+def test_aggregate_fwd_parity(f, kind, code):
+    blk, nrm = _oracle_block(f + 10 * kind)
+    rng = np.random.default_rng(f)
+    h = _act(rng, blk.n_src, f, code)
+    want = oracle.aggregate_fwd(kind, blk, nrm if kind == oracle.GCN else None, h, code)
+    db = upload_block(blk, nrm if kind == oracle.GCN else None)
+    out = torch.empty((blk.n_dst, f), dtype=torch.bfloat16 if code == oracle.BF16 else torch.float32, device=DEV)
+    gnn.aggregate_fwd(db, kind, from_np_act(h), out)
+    got = to_np_act(out)
+    assert relerr(oracle.to_float64(got), oracle.to_float64(want)) <= (1e-5 if code == oracle.F32 else 8e-3)
+
+
+@pytest.mark.parametrize("f", [4, 13, 100, 256])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("hb_code", [None, oracle.F32, oracle.BF16])
+def test_aggregate_bwd_parity(f, kind, hb_code):
+    blk, nrm = _oracle_block(3 + f + kind)
+    rng = np.random.default_rng(f)
+    ka = 2 * f if kind == oracle.SAGE else f
+    da = rng.standard_normal((blk.n_dst, ka)).astype(np.float32)
+    hb = _act(rng, blk.n_src, f, hb_code) if hb_code is not None else None
+    want = oracle.aggregate_bwd(kind, blk, nrm if kind == oracle.GCN else None, da, f, hb, oracle.F32)
+    db = upload_block(blk, nrm if kind == oracle.GCN else None)
+    out = torch.empty((blk.n_src, f), dtype=torch.float32, device=DEV)
+    gnn.aggregate_bwd(db, kind, from_np_act(da), f, out, h_below=from_np_act(hb) if hb is not None else None)
+    assert relerr(out.cpu().numpy(), want) <= 1e-5
+
+
+def test_aggregate_bwd_is_bitwise_reproducible():
+    blk, nrm = _oracle_block(99, n_dst=800, fanout=25)
+    f = 256
+    rng = np.random.default_rng(0)
+    da = from_np_act(rng.standard_normal((blk.n_dst, 2 * f)).astype(np.float32))
+    db = upload_block(blk)
+    a = torch.empty((blk.n_src, f), dtype=torch.float32, device=DEV)
+    b = torch.empty_like(a)
+    gnn.aggregate_bwd(db, oracle.SAGE, da, f, a)
+    gnn.aggregate_bwd(db, oracle.SAGE, da, f, b)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+# ---------------------------------------------------------------------------
+# update GEMMs
+# ---------------------------------------------------------------------------
+
+SHAPES = [(1, 4, 1), (77, 3, 47), (300, 100, 256), (1000, 256, 47), (530, 16, 8), (129, 128, 130)]
+
+
+@pytest.mark.parametrize("m,ke,n", SHAPES)
+@pytest.mark.parametrize("sage", [True, False])
+@pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
+def test_update_fwd_parity(m, ke, n, sage, code):
+    rng = np.random.default_rng(m + ke + n)
+    a_s = _act(rng, m, ke, code)
+    a_n = _act(rng, m, ke, code) if sage else None
+    K = 2 * ke if sage else ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    b = rng.standard_normal(n).astype(np.float32)
+    for relu, ocode in ((True, code), (False, oracle.F32)):
+        want = oracle.update_fwd(a_s, a_n, w, b, relu, code, ocode)
+        out = torch.empty((m, n), dtype=torch.bfloat16 if ocode == oracle.BF16 else torch.float32, device=DEV)
+        gnn.update_fwd(from_np_act(a_s), from_np_act(a_n) if sage else None, from_np_act(w), from_np_act(b), out,
+                       relu, code)
+        err = relerr(oracle.to_float64(to_np_act(out)), oracle.to_float64(want))
+        assert err <= (1e-5 if code == oracle.F32 else 8e-3), (relu, err)
+
+
+def test_update_fwd_device_row_count():
+    rng = np.random.default_rng(1)
+    m, ke, n = 500, 64, 96
+    a = rng.standard_normal((m, ke)).astype(np.float32)
+    w = rng.standard_normal((ke, n)).astype(np.float32)
+    out = torch.full((m, n), 7.0, device=DEV)
+    m_dev = torch.tensor([201], dtype=torch.int64, device=DEV)
+    gnn.update_fwd(from_np_act(a), None, from_np_act(w), None, out, False, gnn.GNN_F32, m_dev=m_dev, cap_m=m)
+    o = out.cpu().numpy()
+    want = oracle.update_fwd(a[:201], None, w, None, False, oracle.F32, oracle.F32)
+    assert relerr(o[:201], want) <= 1e-5 and np.all(o[201:] == 7.0)
+
+
+@pytest.mark.parametrize("m,ke,n", SHAPES + [(26624 // 8, 100, 256)])
+@pytest.mark.parametrize("sage", [True, False])
+@pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
+def test_update_bwd_parity(m, ke, n, sage, code):
+    rng = np.random.default_rng(m * 3 + ke + n)
+    a_s = _act(rng, m, ke, code)
+    a_n = _act(rng, m, ke, code) if sage else None
+    K = 2 * ke if sage else ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    g = rng.standard_normal((m, n)).astype(np.float32)
+    dw_w, db_w, da_w = oracle.update_bwd(a_s, a_n, w, g, code, want_da=True)
+    dw = torch.empty((K, n), device=DEV)
+    db = torch.empty(n, device=DEV)
+    da = torch.empty((m, K), device=DEV)
+    gnn.update_bwd(from_np_act(a_s), from_np_act(a_n) if sage else None, from_np_act(w), from_np_act(g), dw, db, da,
+                   code)
+    tol = 1e-5 if code == oracle.F32 else 8e-3
+    assert relerr(dw.cpu().numpy(), dw_w) <= tol
+    assert relerr(db.cpu().numpy(), db_w) <= 1e-5
+    assert relerr(da.cpu().numpy(), da_w) <= tol
+
+
+# ---------------------------------------------------------------------------
+# loss and optimizer
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("b,c", [(1, 8), (256, 8), (1024, 47), (1000, 172), (33, 153)])
+def test_softmax_ce_parity(b, c):
+    rng = np.random.default_rng(b + c)
+    z = (rng.standard_normal((b, c)) * 4).astype(np.float32)
+    labels = rng.integers(0, c, size=5000).astype(np.int64)
+    targets = rng.choice(5000, size=b, replace=False).astype(np.int64)
+    loss_w, g_w = oracle.softmax_ce(z, labels[targets])
+    g = torch.empty((b, c), device=DEV)
+    loss = torch.empty(1, device=DEV)
+    gnn.softmax_ce(from_np_act(z), from_np_act(labels), from_np_act(targets), g, loss)
+    assert abs(loss.item() - loss_w) <= 1e-5 * max(1, abs(loss_w))
+    assert relerr(g.cpu().numpy(), g_w) <= 1e-5
+
+
+def test_sgd_parity():
+    rng = np.random.default_rng(0)
+    w = rng.standard_normal(10_001).astype(np.float32)
+    dw = rng.standard_normal(10_001).astype(np.float32)
+    wd = from_np_act(w)
+    gnn.sgd(wd, from_np_act(dw), 0.05)
+    assert relerr(wd.cpu().numpy(), oracle.sgd(w, dw, 0.05)) <= 1e-7
+
+
+# ---------------------------------------------------------------------------
+# whole training step
+# ---------------------------------------------------------------------------
+
+def _step_case(kind, precision, dims, fanouts, n, m, batch, graph="er", steps=1, seed=0):
+    if graph == "er":
+        rowptr, col = workloads.er_graph(n, m, seed=seed)
+    else:
+        rowptr, col = workloads.rmat_graph(n, m, seed=seed)
+    table = workloads.features(n, dims[0], seed=seed)
+    labels = workloads.labels(n, dims[-1], seed=seed)
+    perm = workloads.target_batches(n, batch, seed=seed)
+    L = len(dims) - 1
+    sage = kind == gnn.GNN_AGG_SAGE_MEAN
+    ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], seed, l) for l in range(L)]
+    bs = [torch.zeros(dims[l + 1]) for l in range(L)]
+    g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
+    nrm = gnn.gcn_norm(g)
+    tr = gnn.Trainer(kind, dims, fanouts, precision, n, batch, ws, bs, device=DEV)
+    okind = oracle.GCN if kind == gnn.GNN_AGG_GCN_SYM else oracle.SAGE
+    oprec = oracle.F32 if precision == gnn.GNN_F32 else oracle.BF16
+    rp_h, col_h, nrm_h = rowptr.numpy(), col.numpy(), oracle.gcn_norm(rowptr.numpy())
+    w_ref = [w.numpy() for w in ws]
+    b_ref = [b.numpy() for b in bs]
+    t_d, lab_d = table.to(DEV), labels.to(DEV)
+    for s in range(steps):
+        targets = workloads.targets_for_step(perm, batch, s)
+        tr.step(g, t_d, lab_d, targets.to(DEV), seed=seed, step=s, lr=0.05, gcn_norm_t=nrm)
+        torch.cuda.synchronize()
+        cfg = oracle.StepConfig(kind=okind, dims=dims, fanouts=fanouts, precision=oprec, seed=seed, step=s, lr=0.05)
+        ref = oracle.train_step(rp_h, col_h, nrm_h, table.numpy(), labels.numpy(), targets.numpy(), w_ref, b_ref, cfg)
+        yield tr, ref, oprec
+        w_ref = [w.cpu().numpy() for w in tr.w]   # continue from the GPU's weights
+        b_ref = [b.cpu().numpy() for b in tr.b]
+
+
+def _check_step(tr, ref, oprec, L):
+    tol = TOL[oprec]
+    for h in range(1, L + 1):
+        got = tr.block_view(h)
+        want = ref["blocks"][h - 1]
+        assert np.array_equal(got["src_ids"], want.src_ids)
+        assert np.array_equal(got["rowptr"], want.rowptr)
+        assert np.array_equal(got["col"], want.col)
+        if h < L:
+            assert np.array_equal(got["cscptr"], want.cscptr) and np.array_equal(got["cscrow"], want.cscrow)
+    assert int(tr.edges.item()) == ref["edges"]
+    assert abs(tr.loss.item() - ref["loss"]) <= tol * max(1.0, abs(ref["loss"]))
+    for l in range(1, L + 1):
+        assert relerr(tr.dw[l - 1].cpu().numpy(), ref["dW"][l]) <= tol, ("dW", l)
+        assert relerr(tr.db[l - 1].cpu().numpy(), ref["dB"][l]) <= tol, ("dB", l)
+        assert relerr(tr.w[l - 1].cpu().numpy(), ref["new_w"][l - 1]) <= tol, ("W", l)
+
+
+def test_train_step_tiny_gcn_fp32():
+    dims, fan = (32, 16, 8), (5, 5)
+    for tr, ref, oprec in _step_case(gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, dims, fan, 10_000, 50_000, 256, steps=3):
+        _check_step(tr, ref, oprec, 2)
+        # the gathered features are bit-exact
+        x0 = tr.tensor("x0", 0, ref["x0"].shape[0], 32, torch.float32).cpu().numpy()
+        assert np.array_equal(x0, ref["x0"])
+
+
+@pytest.mark.parametrize("kind", [gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_AGG_GCN_SYM])
+def test_train_step_rmat_bf16(kind):
+    dims, fan = (100, 256, 47), (25, 10)
+    for tr, ref, oprec in _step_case(kind, gnn.GNN_BF16, dims, fan, 30_000, 400_000, 512, graph="rmat", steps=2):
+        _check_step(tr, ref, oprec, 2)
+
+
+def test_train_step_three_layer_sage_bf16():
+    dims, fan = (128, 256, 256, 172), (15, 10, 5)
+    for tr, ref, oprec in _step_case(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, dims, fan, 40_000, 500_000, 256,
+                                     graph="rmat"):
+        _check_step(tr, ref, oprec, 3)
+
+
+def test_train_step_is_bitwise_reproducible():
+    dims, fan = (100, 256, 47), (25, 10)
+    outs = []
+    for _ in range(2):
+        for tr, ref, _o in _step_case(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, dims, fan, 30_000, 400_000, 512,
+                                      graph="rmat"):
+            outs.append([t.cpu().clone() for t in tr.w + tr.b] + [tr.loss.cpu().clone()])
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
