@@ -1,0 +1,330 @@
+"""Throughput of sampled mini-batch GNN training steps on one MI355X.
+
+Default workload: R-MAT graph with 2,449,029 vertices and 61,859,140
+undirected edges (products-sized), 100-dim fp32 features resident in HBM,
+47 classes, 2-layer GraphSAGE-mean (hidden 256), batch 1024, fanouts (25, 10),
+bf16 GEMM operands with fp32 accumulation.  Inputs are synthetic and seeded.
+
+One step = sample both hops, gather X', forward, loss, backward, SGD, all in
+one gnn_train_step call.  Prints one JSON line:
+  value          sampled edges per second over the timed steps (sum of the
+                 device edge counters / elapsed time)
+  steps_per_s    training steps per second
+  roofline       the dominant single-kernel stage, timed with HIP events in a
+                 staged run of the same step, against its algorithmic bytes
+  cpu_baseline   the CPU oracle on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+FP32_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default=workloads.RMAT_SAGE.name, choices=sorted(workloads.PRESETS))
+    p.add_argument("--stage-steps", type=int, default=5, help="steps of the event-instrumented staged run")
+    p.add_argument("--no-stages", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for the CPU baseline")
+    p.add_argument("--lr", type=float, default=0.01)
+    return p.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# staged step: the same iteration through the individual ABI calls, with HIP
+# events between them (on torch's current stream, which the calls use)
+# ---------------------------------------------------------------------------
+
+class StagedStep:
+    def __init__(self, gnn, w: workloads.Workload, graph, batch_size, act):
+        self.gnn, self.w, self.graph, self.act = gnn, w, graph, act
+        dev = graph.rowptr.device
+        L = w.num_layers
+        self.L = L
+        self.kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+        self.blocks = []
+        cap = batch_size
+        ws_bytes = 0
+        for h in range(L):
+            blk = gnn.DeviceBlock(graph.n, cap, w.fanouts[h], h < L - 1, w.kind == "gcn", dev)
+            self.blocks.append(blk)
+            nb = ctypes.c_size_t()
+            gnn._check(gnn.lib().gnn_sampler_workspace_size(graph.n, cap, w.fanouts[h], ctypes.byref(nb)))
+            ws_bytes = max(ws_bytes, nb.value)
+            cap = blk.c.cap_src
+        self.samp_ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        gnn._check(gnn.lib().gnn_sampler_workspace_init(self.samp_ws.data_ptr(), ws_bytes, graph.n,
+                                                        gnn._stream(None)))
+        dims = w.dims
+        self.x0 = torch.empty((self.blocks[-1].c.cap_src, dims[0]), dtype=act, device=dev)
+        self.agg, self.h, self.grad, self.da = {}, {}, {}, {}
+        for l in range(1, L + 1):
+            rows = self.blocks[L - l].c.cap_dst
+            self.agg[l] = torch.empty((rows, dims[l - 1]), dtype=act, device=dev)
+            self.h[l] = torch.empty((rows, dims[l]), dtype=act if l < L else torch.float32, device=dev)
+            self.grad[l] = torch.empty((rows, dims[l]), dtype=torch.float32, device=dev)
+            if l > 1:
+                self.da[l] = torch.empty((rows, w.k_of_layer(l)), dtype=torch.float32, device=dev)
+        self.loss = torch.zeros(1, device=dev)
+
+    def run(self, trainer, table, labels, targets, nrm, seed, step, lr, events=None):
+        """Enqueue one step; when `events` is a list, record (name, event) pairs."""
+        gnn, L, w = self.gnn, self.L, self.w
+
+        def mark(name):
+            if events is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                events.append((name, e))
+
+        mark("begin")
+        dst, n_dst = targets, None
+        for h in range(L):
+            blk = self.blocks[h]
+            gnn.build_block(self.graph, dst, w.fanouts[h], seed, step, h + 1, blk, self.samp_ws, n_dst_dev=n_dst,
+                            gcn_norm_t=nrm if w.kind == "gcn" else None, want_csc=h < L - 1)
+            mark(f"sample_hop{h + 1}")
+            dst, n_dst = blk.src_ids, blk.counts[1:2]
+        b0 = self.blocks[-1]
+        gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2])
+        mark("gather")
+        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
+        for l in range(1, L + 1):
+            blk = self.blocks[L - l]
+            hin = self.x0 if l == 1 else self.h[l - 1]
+            gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])
+            mark(f"agg_fwd_l{l}")
+            gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
+                           trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst)
+            mark(f"update_fwd_l{l}")
+        gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
+        mark("loss")
+        for l in range(L, 0, -1):
+            blk = self.blocks[L - l]
+            hin = self.x0 if l == 1 else self.h[l - 1]
+            gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
+                           self.grad[l], trainer.dw[l - 1], trainer.db[l - 1], self.da.get(l), gemm,
+                           m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst)
+            mark(f"update_bwd_l{l}")
+            if l > 1:
+                gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1], h_below=hin)
+                mark(f"agg_bwd_l{l}")
+        for l in range(L):
+            gnn.sgd(trainer.w[l], trainer.dw[l], lr)
+            gnn.sgd(trainer.b[l], trainer.db[l], lr)
+        mark("sgd")
+
+    def stage_bytes(self, name: str):
+        """Algorithmic HBM bytes (and flops) of a single-kernel stage, from the
+        block sizes of the last run (host copies; call after synchronising)."""
+        L, w = self.L, self.w
+        S_H = 2 if self.act == torch.bfloat16 else 4
+        if name == "gather":
+            b = self.blocks[-1].host()
+            n0 = b["n_src"]
+            return n0 * w.dims[0] * (4 + S_H) + 8 * n0, 0
+        if name.startswith("agg_fwd_l"):
+            l = int(name[-1])
+            b = self.blocks[L - l].host()
+            f = w.dims[l - 1]
+            R = np.unique(b["col"]).size
+            extra = (b["n_dst"] * f * S_H + 4 * b["n_src"]) if w.kind == "gcn" else 0
+            return R * f * S_H + 4 * b["nnz"] + 8 * (b["n_dst"] + 1) + b["n_dst"] * f * S_H + extra, 0
+        if name.startswith("update_fwd_l"):
+            l = int(name[-1])
+            b = self.blocks[L - l].host()
+            M, K, N = b["n_dst"], w.k_of_layer(l), w.dims[l]
+            out = S_H if l < L else 4
+            return M * K * S_H + K * N * 4 + N * 4 + M * N * out, 2 * M * K * N
+        if name.startswith("agg_bwd_l"):
+            l = int(name[-1])
+            b = self.blocks[L - l].host()
+            f = w.dims[l - 1]
+            rows_used = np.unique(b["cscrow"]).size
+            return (rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
+                    + 8 * (b["n_dst"] + 1) + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
+        return None, None
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
+                                   "described in the design notes, not built)", "n_gpus": args.gpus}))
+        sys.exit(1)
+    from paper_2303_00158_amd import gnn
+    if not os.path.exists(gnn.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = workloads.PRESETS[args.workload]
+    act = torch.bfloat16 if w.precision == "bf16" else torch.float32
+    precision = gnn.GNN_BF16 if w.precision == "bf16" else gnn.GNN_F32
+    kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+
+    t0 = time.time()
+    log(f"generating {w.name}: {w.graph} n={w.n} m={w.m}")
+    rowptr, col = workloads.make_graph(w, device=dev)
+    graph = gnn.DeviceGraph(rowptr, col)
+    table = workloads.features(w.n, w.dims[0], seed=w.seed, device=dev,
+                               dtype=torch.float16 if w.table_dtype == "f16" else torch.float32)
+    labels = workloads.labels(w.n, w.num_classes, seed=w.seed, device=dev)
+    perm = workloads.target_batches(w.n, w.batch, seed=w.seed, device=dev)
+    L = w.num_layers
+    weights = [workloads.glorot(w.k_of_layer(l + 1), w.dims[l + 1], w.seed, l) for l in range(L)]
+    biases = [torch.zeros(w.dims[l + 1]) for l in range(L)]
+    nrm = gnn.gcn_norm(graph)
+    torch.cuda.synchronize()
+    stats = workloads.graph_stats(rowptr, col)
+    log(f"inputs ready in {time.time() - t0:.1f}s: {stats}")
+
+    tr = gnn.Trainer(kind, w.dims, w.fanouts, precision, w.n, w.batch, weights, biases, device=dev)
+    nb = w.n // w.batch
+    tgt = [workloads.targets_for_step(perm, w.batch, s).contiguous() for s in range(min(nb, args.warmup + args.steps))]
+    edges = torch.zeros(args.steps, dtype=torch.int64, device=dev)
+
+    def step(s, edges_out=None):
+        tr.step(graph, table, labels, tgt[s % len(tgt)], w.seed, s, args.lr, gcn_norm_t=nrm,
+                loc=gnn.GNN_LOC_HOST_PINNED if w.table_loc == "host" else gnn.GNN_LOC_DEVICE, edges_out=edges_out)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps), loss {tr.loss.item():.4f}")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    ev0.record()
+    for i in range(args.steps):
+        step(args.warmup + i, edges[i:i + 1])
+    ev1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = ev0.elapsed_time(ev1)
+    total_edges = int(edges.sum().item())
+    ms_per_step = ms_total / args.steps
+    value = total_edges / (ms_total / 1e3)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}), "
+        f"{total_edges / args.steps:.0f} edges/step, loss {tr.loss.item():.4f}")
+
+    result = {
+        "metric": "sampled edges/sec (fwd+bwd) and train steps/sec, 2-layer GraphSAGE, 1 GPU",
+        "value": value,
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "steps_per_s": 1e3 / ms_per_step,
+        "edges_per_step": total_edges / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if act == torch.bfloat16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "graph": f"{w.graph} n={w.n} m={w.m} {'directed' if w.directed else 'undirected'}",
+            "aggregation": w.kind, "dims": list(w.dims), "fanouts": list(w.fanouts), "batch": w.batch,
+            "features": f"{w.table_dtype} in {'pinned host memory' if w.table_loc == 'host' else 'HBM'}",
+            "scope": "sample + gather + forward + loss + backward + SGD",
+            "parallelism": "single GPU",
+        },
+    }
+
+    # ---- staged run with events per stage --------------------------------
+    if not args.no_stages:
+        staged = StagedStep(gnn, w, graph, w.batch, act)
+        sums, counts = {}, {}
+        for s in range(args.stage_steps + 1):
+            evs = []
+            torch.cuda.synchronize()
+            if hasattr(torch.cuda, "_sleep"):
+                torch.cuda._sleep(20_000_000)  # let the host enqueue the whole step before the GPU starts it
+            staged.run(tr, table, labels, tgt[s % len(tgt)], nrm, w.seed, 10_000 + s, args.lr, events=evs)
+            torch.cuda.synchronize()
+            if s == 0:
+                continue  # first staged step warms up the allocations
+            for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
+                sums[n1] = sums.get(n1, 0.0) + e0.elapsed_time(e1)
+                counts[n1] = counts.get(n1, 0) + 1
+        stage_ms = {k: sums[k] / counts[k] for k in sums}
+        result["stages_ms"] = {k: round(v, 5) for k, v in stage_ms.items()}
+        single = [k for k in stage_ms if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "agg_bwd"))]
+        dom = max(single, key=lambda k: stage_ms[k])
+        byts, flops = staged.stage_bytes(dom)
+        t = stage_ms[dom] / 1e3
+        if flops and flops / max(byts, 1) > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+            ach = flops / t / 1e12
+            roof = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": ach / BF16_PEAK_TFLOPS}
+        else:
+            ach = byts / t / 1e9
+            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS}
+        roof.update({"kernel": dom, "algorithmic_bytes": int(byts), "flops": int(flops or 0),
+                     "avg_ms": stage_ms[dom], "traffic": None})
+        result["roofline"] = roof
+        log(f"stages (ms): {json.dumps(result['stages_ms'])}")
+
+    # ---- CPU oracle baseline ---------------------------------------------
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0))
+        oracle.set_threads(threads)
+        rp_h, col_h = rowptr.cpu().numpy(), col.cpu().numpy()
+        nrm_h = nrm.cpu().numpy()
+        table_h = table.cpu().numpy()
+        labels_h = labels.cpu().numpy()
+        w_h = [x.numpy() for x in weights]
+        b_h = [x.numpy() for x in biases]
+        okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
+        oprec = oracle.BF16 if w.precision == "bf16" else oracle.F32
+        tot_e, tot_t = 0, 0.0
+        for s in range(args.cpu_steps):
+            cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oprec, seed=w.seed,
+                                    step=s, lr=args.lr)
+            tt = time.perf_counter()
+            ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt[s].cpu().numpy(), w_h, b_h, cfg)
+            tot_t += time.perf_counter() - tt
+            tot_e += ref["edges"]
+            w_h, b_h = ref["new_w"], ref["new_b"]
+        result["cpu_baseline"] = {
+            "value": tot_e / tot_t, "unit": "edges/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "sample": f"{args.cpu_steps} full training steps (sample, gather, forward, loss, backward, SGD) of the "
+                      f"same workload, fp64 sums; {tot_t:.2f} s",
+            "steps_per_s": args.cpu_steps / tot_t,
+        }
+        log(f"cpu oracle: {tot_e / tot_t:.0f} edges/s with {oracle.get_threads()} threads")
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -325,10 +325,14 @@ class Trainer:
 
     def step(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets: torch.Tensor, seed: int,
              step: int, lr: float, gcn_norm_t: Optional[torch.Tensor] = None, loc: int = GNN_LOC_DEVICE,
-             stream=None) -> None:
+             edges_out: Optional[torch.Tensor] = None, stream=None) -> None:
+        """Enqueue one training step.  The loss lands in self.loss and the
+        sampled-edge count in edges_out (an int64 device scalar view) or
+        self.edges."""
+        e = self.edges if edges_out is None else edges_out
         _check(lib().gnn_train_step(ctypes.byref(self.model), ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(table),
                                     dtype_code(table.dtype), loc, table.stride(0), _ptr(labels), _ptr(targets),
-                                    self.batch, seed, step, float(lr), _ptr(self.loss), _ptr(self.edges),
+                                    self.batch, seed, step, float(lr), _ptr(self.loss), _ptr(e),
                                     _ptr(self.ws), self.ws.numel(), _stream(stream)))
 
     # --- views into the workspace (for inspection and tests) ---------------
