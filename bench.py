@@ -91,6 +91,14 @@ class StagedStep:
             if l > 1:
                 self.da[l] = torch.empty((rows, w.k_of_layer(l)), dtype=torch.float32, device=dev)
         self.loss = torch.zeros(1, device=dev)
+        gemm = gnn.GNN_BF16 if act == torch.bfloat16 else gnn.GNN_F32
+        self.fwd_ws, self.bwd_ws = {}, {}
+        for l in range(1, L + 1):
+            rows = self.blocks[L - l].c.cap_dst
+            nb = ctypes.c_size_t()
+            gnn._check(gnn.lib().gnn_update_fwd_workspace_size(w.k_of_layer(l), dims[l], rows, gemm, ctypes.byref(nb)))
+            self.fwd_ws[l] = torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=dev)
+            self.bwd_ws[l] = gnn.update_bwd_workspace(w.k_of_layer(l), dims[l], rows, gemm, dev)
 
     def run(self, trainer, table, labels, targets, nrm, seed, step, lr, events=None):
         """Enqueue one step; when `events` is a list, record (name, event) pairs."""
@@ -121,7 +129,8 @@ class StagedStep:
             gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])
             mark(f"agg_fwd_l{l}")
             gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
-                           trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst)
+                           trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
+                           ws=self.fwd_ws[l])
             mark(f"update_fwd_l{l}")
         gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
         mark("loss")
@@ -130,7 +139,7 @@ class StagedStep:
             hin = self.x0 if l == 1 else self.h[l - 1]
             gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
                            self.grad[l], trainer.dw[l - 1], trainer.db[l - 1], self.da.get(l), gemm,
-                           m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst)
+                           m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.bwd_ws[l])
             mark(f"update_bwd_l{l}")
             if l > 1:
                 gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1], h_below=hin)

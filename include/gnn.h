@@ -195,18 +195,29 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
  *   gemm_dt GNN_BF16: operands rounded to bf16, matrix cores, fp32 accumulate;
  *           GNN_F32: fp32 throughout.
  *   out     [device] cap_m x n_out of odt; ReLU applied when relu != 0.
+ *   ws      [device] workspace of gnn_update_fwd_workspace_size bytes, or
+ *           NULL.  With a workspace the reduction over K may be split across
+ *           workgroups; the partial tiles are then summed in a fixed order by
+ *           the last workgroup of each output tile, so results stay bitwise
+ *           reproducible.  The workspace must be zero-filled before its first
+ *           use and is left zero-filled by every call; calls sharing one
+ *           workspace must not overlap.
  * ------------------------------------------------------------------------ */
+gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
 gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
                           const int64_t *m_dev, int64_t cap_m, const float *w, const float *bias, int64_t n_out,
-                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, gnn_stream s);
+                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws, size_t ws_bytes,
+                          gnn_stream s);
 
 /* Gradients of the update given g = dLoss/dZ (fp32, cap_m x n_out):
- *   dw = A^T g (K x n_out), db = column sums of g (unrounded),
+ *   dw = A^T g (K x n_out), db = column sums of g (unrounded, may be NULL),
  *   d_a = g W^T (cap_m x K, fp32) when d_a is not NULL (layers above the
  *   first; Section V, equation T_Trainer: the first layer's backward is the
- *   update alone).  The weight gradient is reduced in a fixed order through
- *   the workspace, so results are bitwise reproducible. */
-gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, size_t *bytes);
+ *   update alone).  The reduction over rows is split across workgroups and
+ *   summed in a fixed order, so results are bitwise reproducible.  ws must
+ *   hold gnn_update_bwd_workspace_size bytes, zero-filled before its first use
+ *   (every call leaves it zero-filled); calls sharing it must not overlap. */
+gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
 gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
                           const int64_t *m_dev, int64_t cap_m, const float *w, const float *g, int64_t n_out,
                           gnn_dtype gemm_dt, float *dw, float *db, float *d_a, void *ws, size_t ws_bytes,
@@ -262,6 +273,7 @@ typedef struct gnn_step_layout {
     size_t h[GNN_MAX_LAYERS + 1];       /* per layer l: H^l (l < L) or logits (l = L) */
     size_t grad[GNN_MAX_LAYERS + 1];    /* per layer l: G^l = dLoss/dZ^l, fp32 */
     size_t d_a[GNN_MAX_LAYERS + 1];     /* per layer l >= 2: dLoss/dA^l, fp32 */
+    size_t fwd_ws, fwd_ws_bytes;        /* update-forward workspace */
     size_t bwd_ws, bwd_ws_bytes;        /* update-backward workspace */
     size_t loss_ws, loss_ws_bytes;      /* loss workspace */
     size_t edges;                       /* int64 sampled edges of the step */

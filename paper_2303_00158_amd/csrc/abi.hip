@@ -180,7 +180,7 @@ gnn_status gnn_build_block(const gnn_graph *g, const float *gcn_norm, const int6
     const size_t need = sampler_ws_bytes(g->n, out->cap_dst, fanout);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     return launch_build_block(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, want_csc != 0, out, ws,
-                              stream_of(s));
+                              false, stream_of(s));
 }
 
 gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, int64_t n_rows, int64_t dim,
@@ -203,7 +203,7 @@ gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, in
     GNN_CHECK(aligned(table, dtype_size(tdt)) && aligned(out, dtype_size(odt)), GNN_EINVAL, "%s: misaligned data", who);
     const void *t = nullptr;
     GNN_TRY(device_view(table, loc, &t, who));
-    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, stream_of(s));
+    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, nullptr, stream_of(s));
 }
 
 gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
@@ -235,9 +235,19 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
     return launch_aggregate_bwd(b, kind, d_a, f, h_below, hbdt, d_src, stream_of(s));
 }
 
+gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes) {
+    clear_error();
+    GNN_CHECK(bytes, GNN_EINVAL, "gnn_update_fwd_workspace_size: bytes is NULL");
+    GNN_CHECK(k >= 1 && n_out >= 1 && cap_m >= 0, GNN_EINVAL, "gnn_update_fwd_workspace_size: bad size");
+    GNN_CHECK(act_dtype(gemm_dt), GNN_EUNSUPPORTED, "gnn_update_fwd_workspace_size: bad gemm dtype");
+    *bytes = update_fwd_ws_bytes(k, n_out, cap_m, gemm_dt);
+    return GNN_OK;
+}
+
 gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
                           const int64_t *m_dev, int64_t cap_m, const float *w, const float *bias, int64_t n_out,
-                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, gnn_stream s) {
+                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws, size_t ws_bytes,
+                          gnn_stream s) {
     clear_error();
     const char *who = "gnn_update_fwd";
     GNN_CHECK(act_dtype(adt) && act_dtype(odt) && act_dtype(gemm_dt), GNN_EUNSUPPORTED,
@@ -249,15 +259,22 @@ gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
     GNN_CHECK(aligned(a_self, dtype_size(adt)) && aligned(a_nbr, dtype_size(adt)) && aligned(w, 4) &&
                   aligned(bias, 4) && aligned(out, dtype_size(odt)) && aligned(m_dev, 8),
               GNN_EINVAL, "%s: misaligned data", who);
-    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, bias, n_out, relu, gemm_dt, out, odt,
+    if (ws) {
+        const int64_t K = a_nbr ? 2 * k_each : k_each;
+        const size_t need = update_fwd_ws_bytes(K, n_out, cap_m, gemm_dt);
+        GNN_CHECK(aligned(ws, 256), GNN_EINVAL, "%s: ws must be 256-byte aligned", who);
+        GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
+    }
+    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, bias, n_out, relu, gemm_dt, out, odt, ws,
                              stream_of(s));
 }
 
-gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, size_t *bytes) {
+gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes) {
     clear_error();
     GNN_CHECK(bytes, GNN_EINVAL, "gnn_update_bwd_workspace_size: bytes is NULL");
     GNN_CHECK(k >= 1 && n_out >= 1 && cap_m >= 0, GNN_EINVAL, "gnn_update_bwd_workspace_size: bad size");
-    *bytes = update_bwd_ws_bytes(k, n_out, cap_m);
+    GNN_CHECK(act_dtype(gemm_dt), GNN_EUNSUPPORTED, "gnn_update_bwd_workspace_size: bad gemm dtype");
+    *bytes = update_bwd_ws_bytes(k, n_out, cap_m, gemm_dt);
     return GNN_OK;
 }
 
@@ -275,11 +292,11 @@ gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
                   aligned(dw, 4) && aligned(db, 4) && aligned(d_a, 4) && aligned(m_dev, 8),
               GNN_EINVAL, "%s: misaligned data", who);
     const int64_t K = a_nbr ? 2 * k_each : k_each;
-    const size_t need = update_bwd_ws_bytes(K, n_out, cap_m);
+    const size_t need = update_bwd_ws_bytes(K, n_out, cap_m, gemm_dt);
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     return launch_update_bwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, g, n_out, gemm_dt, dw, db, d_a, ws,
-                             stream_of(s));
+                             nullptr, nullptr, 0.f, stream_of(s));
 }
 
 gnn_status gnn_softmax_ce_workspace_size(int64_t b, size_t *bytes) {
@@ -337,6 +354,8 @@ gnn_status gnn_train_step_workspace_init(const gnn_model *m, int64_t graph_n, in
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "gnn_train_step_workspace_init: ws must be 256-byte aligned");
     GNN_CHECK(ws_bytes >= o.total_bytes, GNN_ESIZE, "gnn_train_step_workspace_init: workspace %zu bytes, need %zu",
               ws_bytes, o.total_bytes);
+    GNN_TRY(launch_fill_zero(static_cast<char *>(ws) + o.fwd_ws, o.fwd_ws_bytes, stream_of(s)));
+    GNN_TRY(launch_fill_zero(static_cast<char *>(ws) + o.bwd_ws, o.bwd_ws_bytes, stream_of(s)));
     return launch_sampler_ws_init(static_cast<char *>(ws) + o.sampler_ws, graph_n, stream_of(s));
 }
 

@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include <algorithm>
+
 #include "gnn.h"
 
 namespace gnn {
@@ -36,6 +38,9 @@ gnn_status launch_status(const char *what);  // hipGetLastError after a launch
 inline hipStream_t stream_of(gnn_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+__device__ __forceinline__ bool aligned_dev(const void *p, size_t a) {
+    return (reinterpret_cast<uintptr_t>(p) % a) == 0;
+}
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 inline size_t dtype_size(int dt) { return dt == GNN_F32 ? 4 : 2; }
@@ -62,11 +67,13 @@ constexpr int64_t kMaxGrid = (1ll << 31) - 1;
 // ---------------------------------------------------------------------------
 // device helpers
 // ---------------------------------------------------------------------------
+// fp32 -> bf16, round to nearest even; NaNs stay NaN (quiet bit set).
+// Written without branches so it vectorises inside unrolled loops.
 __device__ __forceinline__ uint16_t f32_to_bf16(float x) {
-    uint32_t u = __float_as_uint(x);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t quiet = (u >> 16) | 0x40u;
+    return static_cast<uint16_t>(((u & 0x7fffffffu) > 0x7f800000u) ? quiet : rounded);
 }
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
 __device__ __forceinline__ float f16_to_f32(uint16_t h) {
@@ -131,27 +138,40 @@ gnn_status radix_sort_pairs(const int32_t *keys_in, const int32_t *vals_in, int3
 gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const char *who);
 
 // Internal launchers reused by the training step (no host validation).
+// reset_map (may be null): the sampler's vertex map; the gather sets
+// reset_map[ids[r]] = -1 for every row it copies (the training step defers
+// the sampler's map reset to this kernel).
 gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,
-                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, hipStream_t s);
+                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, int32_t *reset_map,
+                         hipStream_t s);
 gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
                                 hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
                                 int hbdt, float *d_src, hipStream_t s);
+// Update GEMMs.  Their workspaces start with per-tile integer tickets that
+// must be zero before the first use; every call leaves them zero.  A null
+// forward workspace disables the reduction split.
+size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt);
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
                              int64_t cap_m, const float *w, const float *bias, int64_t n_out, int relu, int gemm_dt,
-                             void *out, int odt, hipStream_t s);
-size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m);
+                             void *out, int odt, void *ws, hipStream_t s);
+size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt);
+// w_upd / b_upd (may be null): SGD applied to them with the final gradients.
 gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
                              int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt, float *dw,
-                             float *db, float *d_a, void *ws, hipStream_t s);
+                             float *db, float *d_a, void *ws, float *w_upd, float *b_upd, float lr, hipStream_t s);
+gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 size_t softmax_ce_ws_bytes(int64_t b);
 gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels,
                              const int64_t *targets, float *g_out, float *loss_out, void *ws, hipStream_t s);
 gnn_status launch_sgd(float *w, const float *dw, int64_t n, float lr, hipStream_t s);
 size_t sampler_ws_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout);
 gnn_status launch_sampler_ws_init(void *ws, int64_t graph_n, hipStream_t s);
+// defer_reset: leave the vertex map set for the block's sources (the next
+// hop of the same step, or the gather, consumes and resets it).
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              bool want_csc, const gnn_block *out, void *ws, hipStream_t s);
+                              bool want_csc, const gnn_block *out, void *ws, bool defer_reset, hipStream_t s);
+int32_t *sampler_map(void *ws);
 
 }  // namespace gnn

@@ -1,6 +1,23 @@
 // Mini-batch sampler: one block (hop) of uniform neighbour sampling without
 // replacement, relabelled to local indices, with its transpose.
 //
+// A hop is four kernels (plus one for the transpose):
+//   1. prepare   one wavefront per destination: map the destination to its
+//                local index, draw its sample (Floyd), write the sampled
+//                neighbour ids to a padded [n_dst][k] staging array.
+//   2. mark      one thread per destination: set the bitmap bit of every
+//                sampled id that is not a destination, and scan the sample
+//                counts into the block's row pointer.
+//   3. emit      walk the bitmap in vertex order: every set bit becomes the
+//                next new source (so new sources come out in ascending id
+//                order), and the bitmap is cleared.
+//   4. relabel   one thread per staged sample: local index via the map.
+//   5. transpose one workgroup: stable radix sort of the edges by source.
+// Steps 2 and 3 are single-pass scans: workgroups take tickets in the order
+// they start and add the prefix of earlier tickets (decoupled look-back),
+// so a workgroup only waits on workgroups that are already running.  Every
+// wait is bounded; a wait that runs out flags counts[3].
+//
 // Device workspace (sampler_ws_bytes):
 //   map  int32[graph_n]  vertex -> local source index, -1 when unused
 //   bits uint32[W]       one bit per vertex: "reached, not a destination"
@@ -14,12 +31,84 @@ namespace gnn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBitTile = kThreads * 8;  // bitmap words per block in the scan kernels
+constexpr int kBitWords = 8;                      // bitmap words per thread in the emit kernel
+constexpr int kBitTile = kThreads * kBitWords;    // bitmap words per workgroup
+constexpr int kSortThreads = 1024;
+constexpr int kSortWaves = kSortThreads / 64;
+constexpr uint64_t kFlagAgg = 1ull << 62, kFlagPrefix = 2ull << 62, kValueMask = (1ull << 62) - 1;
+constexpr uint32_t kSpinLimit = 1u << 22;
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
     z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
     return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint64_t load_status(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_status(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Logical workgroup index: the order in which workgroups started.
+__device__ __forceinline__ int64_t take_ticket(int *ticket) {
+    __shared__ int64_t t;
+    if (threadIdx.x == 0) t = atomicAdd(ticket, 1);
+    __syncthreads();
+    return t;
+}
+
+// Called by one thread: publish this workgroup's aggregate, add up the
+// aggregates / prefixes of earlier tickets, publish the inclusive prefix, and
+// return the exclusive prefix.
+__device__ int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, int64_t *err) {
+    if (blk == 0) {
+        store_status(&status[0], kFlagPrefix | static_cast<uint64_t>(agg));
+        return 0;
+    }
+    store_status(&status[blk], kFlagAgg | static_cast<uint64_t>(agg));
+    int64_t excl = 0;
+    int64_t p = blk - 1;
+    uint32_t spins = 0;
+    while (p >= 0) {
+        const uint64_t s = load_status(&status[p]);
+        const uint64_t flag = s & ~kValueMask;
+        if (flag == 0) {
+            if (++spins > kSpinLimit) {
+                *err = 1;  // an earlier workgroup never published: flag it and stop waiting
+                break;
+            }
+            continue;
+        }
+        excl += static_cast<int64_t>(s & kValueMask);
+        if (flag == kFlagPrefix) break;
+        --p;
+    }
+    store_status(&status[blk], kFlagPrefix | static_cast<uint64_t>(excl + agg));
+    return excl;
+}
+
+__device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t *total) {
+    __shared__ int64_t sh[kThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) sh[wave] = inc;
+    __syncthreads();
+    int64_t base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+        if (w < wave) base += sh[w];
+        tot += sh[w];
+    }
+    __syncthreads();
+    *total = tot;
+    return base + inc - v;
 }
 
 __global__ void gcn_norm_kernel(const int64_t *__restrict__ rowptr, int64_t n, float *__restrict__ nrm) {
@@ -35,65 +124,79 @@ __global__ void fill_i32_kernel(int32_t *p, int64_t n, int32_t v) {
         p[i] = v;
 }
 
-// Per destination row: sample count min(deg, k); map the destination to its
-// local index; it is also source i.
-__global__ void sample_count_kernel(const int64_t *__restrict__ dst, const int64_t *n_dst_dev, int64_t cap_dst,
-                                    const int64_t *__restrict__ rowptr, int32_t fanout, int32_t *__restrict__ map,
-                                    int64_t *__restrict__ cnt, int64_t *__restrict__ src_ids,
-                                    int64_t *__restrict__ counts) {
-    const int64_t n_dst = n_dst_dev ? min(*n_dst_dev, cap_dst) : cap_dst;
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i == 0) counts[0] = n_dst;
-    if (i >= n_dst) return;
-    const int64_t v = dst[i];
-    const int64_t d = rowptr[v + 1] - rowptr[v];
-    cnt[i] = d < fanout ? d : fanout;
-    map[v] = static_cast<int32_t>(i);
-    src_ids[i] = v;
-}
+struct HopArgs {
+    const int64_t *rowptr, *col;  // graph
+    const float *gcn_norm;        // per vertex, or null
+    const int64_t *dst;
+    const int64_t *n_dst_dev;
+    int64_t cap_dst;
+    int32_t k;
+    uint64_t seed, step, hop;
+    // block
+    int64_t *counts, *src_ids, *brow;
+    int32_t *bcol;
+    float *src_norm;
+    // workspace
+    int32_t *map;
+    uint32_t *bits;
+    int64_t words;
+    int64_t *gpad;      // [cap_dst][k] sampled global ids
+    int32_t *cnt;       // [cap_dst] sample counts
+    int32_t *erow;      // [cap_nnz] row of each edge (for the transpose) or null
+    uint64_t *status;   // [nb_rows + nb_bits] look-back words
+    int *tickets;       // [2]
+    int64_t nb_rows, nb_bits;
+};
 
-// One wavefront per destination row.  Rows with d <= k keep every position;
-// otherwise Floyd's algorithm draws k distinct positions, held R per lane
-// (slot s lives in lane s % 64, register s / 64), which are then ranked to
-// write the sampled neighbours in ascending position order.
+// 1. prepare: one wavefront per destination row.  R drawn positions per lane
+// (slot s lives in lane s % 64, register s / 64).
 template <int R>
-__global__ void __launch_bounds__(kThreads) sample_floyd_kernel(
-    const int64_t *__restrict__ dst, const int64_t *__restrict__ counts, const int64_t *__restrict__ rowptr,
-    const int64_t *__restrict__ col, const int64_t *__restrict__ brow, int32_t k, uint64_t seed, uint64_t step,
-    uint64_t hop, int64_t *__restrict__ gcol) {
+__global__ void __launch_bounds__(kThreads) hop_prepare_kernel(HopArgs a) {
+    const int64_t gtid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    const int64_t gsize = static_cast<int64_t>(gridDim.x) * kThreads;
+    const int64_t n_dst = a.n_dst_dev ? min(*a.n_dst_dev, a.cap_dst) : a.cap_dst;
+    // reset the look-back state of steps 2 and 3
+    for (int64_t i = gtid; i < a.nb_rows + a.nb_bits; i += gsize) a.status[i] = 0;
+    if (gtid < 2) a.tickets[gtid] = 0;
+    if (gtid == 0) {
+        a.counts[0] = n_dst;
+        a.counts[3] = 0;
+    }
     const int lane = threadIdx.x & 63;
-    const int64_t row = (static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x) >> 6;
-    const int64_t n_dst = counts[0];
+    const int64_t row = gtid >> 6;
     if (row >= n_dst) return;
-    const int64_t v = dst[row];
-    const int64_t beg = rowptr[v];
-    const int64_t d = rowptr[v + 1] - beg;
-    const int64_t ob = brow[row];
+    const int64_t v = a.dst[row];
+    const int64_t beg = a.rowptr[v];
+    const int64_t d = a.rowptr[v + 1] - beg;
+    const int32_t k = a.k;
+    int64_t *out = a.gpad + row * k;
+    if (lane == 0) {
+        a.map[v] = static_cast<int32_t>(row);
+        a.src_ids[row] = v;
+        if (a.src_norm) a.src_norm[row] = a.gcn_norm[v];
+        a.cnt[row] = static_cast<int32_t>(d < k ? d : k);
+    }
     if (d <= k) {
-        for (int64_t p = lane; p < d; p += 64) gcol[ob + p] = col[beg + p];
+        for (int64_t p = lane; p < d; p += 64) out[p] = a.col[beg + p];
         return;
     }
     uint32_t slot[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) slot[r] = 0xffffffffu;
-    const uint64_t pk = mix64(mix64(mix64(mix64(seed) ^ step) ^ hop) ^ static_cast<uint64_t>(v));
+    const uint64_t pk = mix64(mix64(mix64(mix64(a.seed) ^ a.step) ^ a.hop) ^ static_cast<uint64_t>(v));
     for (int32_t t = 0; t < k; ++t) {
         const uint64_t j = static_cast<uint64_t>(d - k + t);
         const uint64_t key = mix64(pk ^ static_cast<uint64_t>(t));
         const uint32_t x = static_cast<uint32_t>(((key >> 32) * (j + 1)) >> 32);
         bool mine = false;
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int s = r * 64 + lane;
-            mine |= (s < t) && (slot[r] == x);
-        }
+        for (int r = 0; r < R; ++r) mine |= (r * 64 + lane < t) && (slot[r] == x);
         const bool found = __ballot(mine) != 0ull;
         const uint32_t val = found ? static_cast<uint32_t>(j) : x;
-        const int treg = t >> 6;
         if (lane == (t & 63)) {
 #pragma unroll
             for (int r = 0; r < R; ++r)
-                if (r == treg) slot[r] = val;
+                if (r == (t >> 6)) slot[r] = val;
         }
     }
     // rank of each drawn position among all k (they are distinct)
@@ -101,163 +204,249 @@ __global__ void __launch_bounds__(kThreads) sample_floyd_kernel(
 #pragma unroll
     for (int r = 0; r < R; ++r) rank[r] = 0;
     for (int32_t s = 0; s < k; ++s) {
-        const int sreg = s >> 6;
         uint32_t mine = 0;
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            if (r == sreg) mine = slot[r];
+            if (r == (s >> 6)) mine = slot[r];
         const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine), s & 63));
 #pragma unroll
         for (int r = 0; r < R; ++r) rank[r] += (other < slot[r]) ? 1 : 0;
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int s = r * 64 + lane;
-        if (s < k) gcol[ob + rank[r]] = col[beg + slot[r]];
-    }
+    for (int r = 0; r < R; ++r)
+        if (r * 64 + lane < k) out[rank[r]] = a.col[beg + slot[r]];
 }
 
-// Sampled ids that are not destinations: set their bit.
-__global__ void mark_new_kernel(const int64_t *__restrict__ gcol, const int64_t *__restrict__ counts,
-                                const int32_t *__restrict__ map, uint32_t *__restrict__ bits) {
-    const int64_t nnz = counts[2];
-    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
-         e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t u = gcol[e];
-        if (map[u] < 0) atomicOr(&bits[u >> 5], 1u << (u & 31));
+// 2. mark new ids and scan the sample counts into the row pointer.  A
+// workgroup owns 256 destination rows; its threads walk the rows' staged
+// samples together (slot-parallel, so the loads are independent).
+__global__ void __launch_bounds__(kThreads) hop_mark_kernel(HopArgs a) {
+    __shared__ int32_t rc[kThreads];
+    const int64_t blk = take_ticket(&a.tickets[0]);
+    const int64_t n_dst = a.counts[0];
+    const int64_t row0 = blk * kThreads;
+    const int64_t i = row0 + threadIdx.x;
+    const int64_t c = (i < n_dst) ? a.cnt[i] : 0;
+    rc[threadIdx.x] = static_cast<int32_t>(c);
+    __syncthreads();
+    const int64_t k = a.k;
+    const int64_t nrows = max<int64_t>(0, min<int64_t>(kThreads, n_dst - row0));
+    const int64_t slots = nrows * k;
+    const int64_t *g = a.gpad + row0 * k;
+    for (int64_t s0 = 0; s0 < slots; s0 += 4 * kThreads) {
+        int64_t u[4];
+        bool ok[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t sl = s0 + q * kThreads + threadIdx.x;
+            const int64_t r = sl / k;
+            ok[q] = sl < slots && (sl - r * k) < rc[sl < slots ? r : 0];
+            u[q] = g[ok[q] ? sl : 0];
+        }
+        int32_t mv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mv[q] = a.map[ok[q] ? u[q] : 0];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (ok[q] && mv[q] < 0) atomicOr(&a.bits[u[q] >> 5], 1u << (u[q] & 31));
     }
+    int64_t total;
+    const int64_t excl_in_block = block_excl_scan(c, &total);
+    __shared__ int64_t base;
+    if (threadIdx.x == 0) base = look_back(a.status, blk, total, &a.counts[3]);
+    __syncthreads();
+    if (i < n_dst) a.brow[i + 1] = base + excl_in_block + c;
+    if (blk == 0 && threadIdx.x == 0) a.brow[0] = 0;
+    if (blk == a.nb_rows - 1 && threadIdx.x == 0) a.counts[2] = base + total;
 }
 
-__global__ void __launch_bounds__(kThreads) bitmap_count_kernel(const uint32_t *__restrict__ bits, int64_t words,
-                                                                 int64_t *__restrict__ pc) {
-    __shared__ int64_t sh[kThreads / 64];
-    const int64_t w0 = static_cast<int64_t>(blockIdx.x) * kBitTile + threadIdx.x * 8;
+// 3. new sources in ascending vertex order.
+__global__ void __launch_bounds__(kThreads) hop_emit_kernel(HopArgs a) {
+    const int64_t blk = take_ticket(&a.tickets[1]);
+    const int64_t n_dst = a.counts[0];
+    const int64_t w0 = blk * kBitTile + threadIdx.x * kBitWords;
+    uint32_t wv[kBitWords];
     int64_t c = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (w0 + i < words) c += __popc(bits[w0 + i]);
-    // block sum
-    for (int o = 32; o > 0; o >>= 1) c += __shfl_down(c, o, 64);
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = c;
+    for (int q = 0; q < kBitWords; ++q) {
+        wv[q] = (w0 + q < a.words) ? a.bits[w0 + q] : 0u;
+        c += __popc(wv[q]);
+    }
+    int64_t total;
+    const int64_t excl_in_block = block_excl_scan(c, &total);
+    __shared__ int64_t base;
+    if (threadIdx.x == 0) base = look_back(a.status + a.nb_rows, blk, total, &a.counts[3]);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int64_t t = 0;
-        for (int w = 0; w < kThreads / 64; ++w) t += sh[w];
-        pc[blockIdx.x] = t;
-    }
-}
-
-// Emit the set bits in ascending vertex order as new sources n_dst + r, map
-// them, and clear the bitmap.
-__global__ void __launch_bounds__(kThreads) bitmap_emit_kernel(uint32_t *__restrict__ bits, int64_t words,
-                                                                const int64_t *__restrict__ pcoff,
-                                                                const int64_t *__restrict__ new_total,
-                                                                int64_t *__restrict__ counts,
-                                                                int64_t *__restrict__ src_ids,
-                                                                int32_t *__restrict__ map) {
-    __shared__ int64_t sh[kThreads / 64];
-    const int64_t n_dst = counts[0];
-    if (blockIdx.x == 0 && threadIdx.x == 0) counts[1] = n_dst + *new_total;
-    const int64_t w0 = static_cast<int64_t>(blockIdx.x) * kBitTile + threadIdx.x * 8;
-    uint32_t wv[8];
-    int64_t c = 0;
+    int64_t r = n_dst + base + excl_in_block;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        wv[i] = (w0 + i < words) ? bits[w0 + i] : 0u;
-        c += __popc(wv[i]);
-    }
-    // exclusive scan of c over the block
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int64_t inc = c;
-    for (int o = 1; o < 64; o <<= 1) {
-        int64_t y = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += y;
-    }
-    if (lane == 63) sh[wave] = inc;
-    __syncthreads();
-    int64_t base = pcoff[blockIdx.x] + n_dst + inc - c;
-    for (int w = 0; w < wave; ++w) base += sh[w];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        uint32_t m = wv[i];
+    for (int q = 0; q < kBitWords; ++q) {
+        uint32_t m = wv[q];
         if (!m) continue;
-        const int64_t wbase = (w0 + i) * 32;
+        const int64_t wbase = (w0 + q) * 32;
         while (m) {
             const int b = __builtin_ctz(m);
             m &= m - 1;
             const int64_t u = wbase + b;
-            src_ids[base] = u;
-            map[u] = static_cast<int32_t>(base);
-            ++base;
+            a.src_ids[r] = u;
+            a.map[u] = static_cast<int32_t>(r);
+            if (a.src_norm) a.src_norm[r] = a.gcn_norm[u];
+            ++r;
         }
-        bits[w0 + i] = 0u;
+        a.bits[w0 + q] = 0u;
+    }
+    if (blk == a.nb_bits - 1 && threadIdx.x == 0) a.counts[1] = n_dst + base + total;
+}
+
+// 4. local source index of every sampled edge.
+__global__ void __launch_bounds__(kThreads) hop_relabel_kernel(HopArgs a) {
+    const int64_t n_dst = a.counts[0];
+    const int64_t total = n_dst * a.k;
+    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; q < total;
+         q += static_cast<int64_t>(gridDim.x) * kThreads) {
+        const int64_t i = q / a.k, t = q - i * a.k;
+        if (t >= a.cnt[i]) continue;
+        const int64_t e = a.brow[i] + t;
+        a.bcol[e] = a.map[a.gpad[q]];
+        if (a.erow) a.erow[e] = static_cast<int32_t>(i);
     }
 }
 
-__global__ void relabel_kernel(const int64_t *__restrict__ gcol, const int64_t *__restrict__ counts,
-                               const int32_t *__restrict__ map, int32_t *__restrict__ col_out) {
-    const int64_t nnz = counts[2];
-    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < nnz;
-         e += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        col_out[e] = map[gcol[e]];
-}
-
-__global__ void finish_kernel(const int64_t *__restrict__ src_ids, const int64_t *__restrict__ counts,
-                              int32_t *__restrict__ map, const float *__restrict__ gcn_norm,
-                              float *__restrict__ src_norm) {
+// Standalone calls: put the map back to all -1.
+__global__ void hop_finish_kernel(const int64_t *__restrict__ src_ids, const int64_t *__restrict__ counts,
+                                  int32_t *__restrict__ map) {
     const int64_t n_src = counts[1];
     for (int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; j < n_src;
-         j += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t u = src_ids[j];
-        if (src_norm) src_norm[j] = gcn_norm[u];
-        map[u] = -1;
-    }
+         j += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        map[src_ids[j]] = -1;
 }
 
-__global__ void edge_rows_kernel(const int64_t *__restrict__ brow, const int64_t *__restrict__ counts,
-                                 int32_t *__restrict__ erow) {
-    const int64_t n_dst = counts[0];
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= n_dst) return;
-    for (int64_t e = brow[i]; e < brow[i + 1]; ++e) erow[e] = static_cast<int32_t>(i);
-}
-
-// cscptr[j] = first position of key j in the sorted keys (lower bound).
-__global__ void csc_ptr_kernel(const int32_t *__restrict__ skey, const int64_t *__restrict__ counts,
-                               int64_t *__restrict__ cscptr) {
-    const int64_t n_src = counts[1], nnz = counts[2];
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (j > n_src) return;
-    int64_t lo = 0, hi = nnz;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (skey[mid] < j) lo = mid + 1; else hi = mid;
+// 5. stable transpose in one workgroup: LSD radix sort of (source, row) by
+// source, 8 bits per pass.  Each wavefront owns a contiguous segment of the
+// edge list; per pass the segments' digit histograms give every (segment,
+// digit) its output offset, and the segments are scattered in order with
+// ballot-based ranks, which keeps equal keys in edge order.  Then the row
+// pointer of the transpose is read off the sorted keys.
+__global__ void __launch_bounds__(kSortThreads) csc_build_kernel(const int32_t *__restrict__ keys_in,
+                                                                  const int32_t *__restrict__ vals_in,
+                                                                  const int64_t *__restrict__ counts, int key_bits,
+                                                                  int32_t *ka, int32_t *va, int32_t *kb, int32_t *vb,
+                                                                  int32_t *__restrict__ cscrow,
+                                                                  int64_t *__restrict__ cscptr) {
+    __shared__ int hist[kSortWaves][256];
+    __shared__ int tot[256];
+    const int64_t n = counts[2], n_src = counts[1];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t seg = ceil_div(ceil_div(n > 0 ? n : 1, kSortWaves), 64) * 64;
+    const int64_t chunks = seg / 64;
+    const int passes = key_bits <= 8 ? 1 : (key_bits + 7) / 8;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int32_t *ks = keys_in, *vs = vals_in;
+    int32_t *kfinal = ka;
+    for (int p = 0; p < passes; ++p) {
+        const int shift = 8 * p;
+        const bool last = p == passes - 1;
+        int32_t *kd = (p % 2 == 0) ? ka : kb;
+        int32_t *vd = last ? cscrow : ((p % 2 == 0) ? va : vb);
+        for (int d = threadIdx.x; d < kSortWaves * 256; d += kSortThreads) (&hist[0][0])[d] = 0;
+        __syncthreads();
+        const int64_t s0 = wave * seg;
+        const int64_t s1 = min(n, s0 + seg);
+        for (int64_t q0 = s0 + lane; q0 < s1; q0 += 4 * 64) {
+            int32_t kk[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) kk[b] = ks[min(q0 + b * 64, s1 - 1)];
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                if (q0 + b * 64 < s1) atomicAdd(&hist[wave][(kk[b] >> shift) & 255], 1);
+        }
+        __syncthreads();
+        if (threadIdx.x < 256) {
+            int s = 0;
+            for (int w = 0; w < kSortWaves; ++w) s += hist[w][threadIdx.x];
+            tot[threadIdx.x] = s;
+        }
+        __syncthreads();
+        if (threadIdx.x < 256) {
+            int base = 0;
+            for (int d = 0; d < static_cast<int>(threadIdx.x); ++d) base += tot[d];
+            for (int w = 0; w < kSortWaves; ++w) {
+                const int h = hist[w][threadIdx.x];
+                hist[w][threadIdx.x] = base;
+                base += h;
+            }
+        }
+        __syncthreads();
+        int32_t kb[4], vb4[4];
+        for (int64_t ch = 0; ch < chunks; ++ch) {
+            const int64_t q = s0 + ch * 64 + lane;
+            const bool valid = q < n && q < s0 + seg;
+            if ((ch & 3) == 0) {
+                // load the next four chunks of this segment at once
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const int64_t qb = q + b * 64;
+                    const int64_t qc = (qb < n) ? qb : (n > 0 ? n - 1 : 0);
+                    kb[b] = ks[qc];
+                    vb4[b] = vs[qc];
+                }
+            }
+            const int32_t key = valid ? kb[ch & 3] : 0;
+            const int32_t val = valid ? vb4[ch & 3] : 0;
+            const int d = (key >> shift) & 255;
+            uint64_t peers = __ballot(valid);
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const bool bit = (d >> b) & 1;
+                const uint64_t m = __ballot(valid && bit);
+                peers &= bit ? m : ~m;
+            }
+            const int rank = __popcll(peers & lt);
+            const int at = valid ? hist[wave][d] : 0;
+            __syncthreads();
+            if (valid) {
+                kd[at + rank] = key;
+                vd[at + rank] = val;
+                if (rank == 0) hist[wave][d] = at + __popcll(peers);
+            }
+            __syncthreads();
+        }
+        __threadfence_block();
+        __syncthreads();
+        ks = kd;
+        vs = vd;
+        kfinal = kd;
     }
-    cscptr[j] = lo;
+    // cscptr[j] = first position of key j
+    if (n == 0) {
+        for (int64_t j = threadIdx.x; j <= n_src; j += kSortThreads) cscptr[j] = 0;
+        return;
+    }
+    for (int64_t pos = threadIdx.x; pos <= n; pos += kSortThreads) {
+        const int64_t lo = (pos == 0) ? -1 : kfinal[pos - 1];
+        const int64_t hi = (pos == n) ? n_src : kfinal[pos];
+        for (int64_t j = lo + 1; j <= hi; ++j) cscptr[j] = pos;
+    }
 }
 
 struct SamplerWs {
-    size_t map, bits, gcol, cnt, scan, pc, pcoff, pcscan, newtot, erow, skey, radix, total;
+    size_t map, bits, gpad, cnt, erow, status, tickets, sort, total;
 };
 
 SamplerWs sampler_layout(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
     const int64_t words = ceil_div(graph_n > 0 ? graph_n : 1, 32);
-    const int64_t nbw = ceil_div(words, kBitTile);
-    const int64_t cap_nnz = cap_dst * fanout;
+    const int64_t nb_rows = ceil_div(cap_dst > 0 ? cap_dst : 1, kThreads);
+    const int64_t nb_bits = ceil_div(words, kBitTile);
+    const int64_t cap_nnz = std::max<int64_t>(cap_dst * fanout, 1);
     Carver c(nullptr);
     SamplerWs w;
     w.map = c.take(static_cast<size_t>(graph_n > 0 ? graph_n : 1) * 4);
     w.bits = c.take(static_cast<size_t>(words) * 4);
-    w.gcol = c.take(static_cast<size_t>(cap_nnz > 0 ? cap_nnz : 1) * 8);
-    w.cnt = c.take(static_cast<size_t>(cap_dst > 0 ? cap_dst : 1) * 8);
-    w.scan = c.take(scan_tmp_bytes(cap_dst));
-    w.pc = c.take(static_cast<size_t>(nbw) * 8);
-    w.pcoff = c.take(static_cast<size_t>(nbw + 1) * 8);
-    w.pcscan = c.take(scan_tmp_bytes(nbw));
-    w.newtot = c.take(8);
-    w.erow = c.take(static_cast<size_t>(cap_nnz > 0 ? cap_nnz : 1) * 4);
-    w.skey = c.take(static_cast<size_t>(cap_nnz > 0 ? cap_nnz : 1) * 4);
-    w.radix = c.take(radix_tmp_bytes(cap_nnz));
+    w.gpad = c.take(static_cast<size_t>(cap_nnz) * 8);
+    w.cnt = c.take(static_cast<size_t>(cap_dst > 0 ? cap_dst : 1) * 4);
+    w.erow = c.take(static_cast<size_t>(cap_nnz) * 4);
+    w.status = c.take(static_cast<size_t>(nb_rows + nb_bits) * 8);
+    w.tickets = c.take(2 * 4);
+    w.sort = c.take(static_cast<size_t>(cap_nnz) * 4 * 4);  // two key / value ping-pong pairs
     w.total = round_up(c.off, 256);
     return w;
 }
@@ -300,72 +489,65 @@ gnn_status launch_gcn_norm(const gnn_graph *g, float *nrm, hipStream_t s) {
     return GNN_OK;
 }
 
+int32_t *sampler_map(void *ws) { return reinterpret_cast<int32_t *>(static_cast<char *>(ws) + sampler_layout(1, 1, 1).map); }
+
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              bool want_csc, const gnn_block *out, void *ws, hipStream_t s) {
+                              bool want_csc, const gnn_block *out, void *ws, bool defer_reset, hipStream_t s) {
     const SamplerWs w = sampler_layout(g->n, out->cap_dst, fanout);
     char *base = static_cast<char *>(ws);
-    int32_t *map = reinterpret_cast<int32_t *>(base + w.map);
-    uint32_t *bits = reinterpret_cast<uint32_t *>(base + w.bits);
-    int64_t *gcol = reinterpret_cast<int64_t *>(base + w.gcol);
-    int64_t *cnt = reinterpret_cast<int64_t *>(base + w.cnt);
-    int64_t *pc = reinterpret_cast<int64_t *>(base + w.pc);
-    int64_t *pcoff = reinterpret_cast<int64_t *>(base + w.pcoff);
-    int64_t *newtot = reinterpret_cast<int64_t *>(base + w.newtot);
-    const int64_t words = ceil_div(g->n > 0 ? g->n : 1, 32);
-    const int64_t nbw = ceil_div(words, kBitTile);
-    const int64_t cap_dst = out->cap_dst;
-    const int64_t cap_nnz = cap_dst * fanout;
+    HopArgs a;
+    a.rowptr = g->rowptr;
+    a.col = g->col;
+    a.gcn_norm = out->src_norm ? gcn_norm : nullptr;
+    a.dst = dst_ids;
+    a.n_dst_dev = n_dst_dev;
+    a.cap_dst = out->cap_dst;
+    a.k = fanout;
+    a.seed = seed;
+    a.step = step;
+    a.hop = static_cast<uint64_t>(static_cast<int64_t>(hop));
+    a.counts = out->counts;
+    a.src_ids = out->src_ids;
+    a.brow = out->rowptr;
+    a.bcol = out->col;
+    a.src_norm = out->src_norm;
+    a.map = reinterpret_cast<int32_t *>(base + w.map);
+    a.bits = reinterpret_cast<uint32_t *>(base + w.bits);
+    a.words = ceil_div(g->n > 0 ? g->n : 1, 32);
+    a.gpad = reinterpret_cast<int64_t *>(base + w.gpad);
+    a.cnt = reinterpret_cast<int32_t *>(base + w.cnt);
+    a.erow = want_csc ? reinterpret_cast<int32_t *>(base + w.erow) : nullptr;
+    a.status = reinterpret_cast<uint64_t *>(base + w.status);
+    a.tickets = reinterpret_cast<int *>(base + w.tickets);
+    a.nb_rows = ceil_div(out->cap_dst > 0 ? out->cap_dst : 1, kThreads);
+    a.nb_bits = ceil_div(a.words, kBitTile);
 
-    sample_count_kernel<<<grid_for(cap_dst, kThreads, kMaxGrid), kThreads, 0, s>>>(
-        dst_ids, n_dst_dev, cap_dst, g->rowptr, fanout, map, cnt, out->src_ids, out->counts);
-    GNN_LAUNCHED("sample_count");
-    GNN_TRY(exclusive_scan(cnt, out->rowptr, out->counts, cap_dst, out->counts + 2, base + w.scan, s));
-
-    const unsigned gw = grid_for(cap_dst * 64, kThreads, kMaxGrid);
-    const uint64_t h = static_cast<uint64_t>(static_cast<int64_t>(hop));
-    if (fanout <= 64)
-        sample_floyd_kernel<1><<<gw, kThreads, 0, s>>>(dst_ids, out->counts, g->rowptr, g->col, out->rowptr, fanout,
-                                                        seed, step, h, gcol);
-    else if (fanout <= 128)
-        sample_floyd_kernel<2><<<gw, kThreads, 0, s>>>(dst_ids, out->counts, g->rowptr, g->col, out->rowptr, fanout,
-                                                        seed, step, h, gcol);
-    else if (fanout <= 256)
-        sample_floyd_kernel<4><<<gw, kThreads, 0, s>>>(dst_ids, out->counts, g->rowptr, g->col, out->rowptr, fanout,
-                                                        seed, step, h, gcol);
-    else if (fanout <= 512)
-        sample_floyd_kernel<8><<<gw, kThreads, 0, s>>>(dst_ids, out->counts, g->rowptr, g->col, out->rowptr, fanout,
-                                                        seed, step, h, gcol);
-    else
-        sample_floyd_kernel<16><<<gw, kThreads, 0, s>>>(dst_ids, out->counts, g->rowptr, g->col, out->rowptr,
-                                                         fanout, seed, step, h, gcol);
-    GNN_LAUNCHED("sample_floyd");
-
-    const unsigned ge = grid_for(cap_nnz, kThreads, 1 << 16);
-    mark_new_kernel<<<ge, kThreads, 0, s>>>(gcol, out->counts, map, bits);
-    GNN_LAUNCHED("mark_new");
-    bitmap_count_kernel<<<static_cast<unsigned>(nbw), kThreads, 0, s>>>(bits, words, pc);
-    GNN_LAUNCHED("bitmap_count");
-    GNN_TRY(exclusive_scan(pc, pcoff, nullptr, nbw, newtot, base + w.pcscan, s));
-    bitmap_emit_kernel<<<static_cast<unsigned>(nbw), kThreads, 0, s>>>(bits, words, pcoff, newtot, out->counts,
-                                                                       out->src_ids, map);
-    GNN_LAUNCHED("bitmap_emit");
-    relabel_kernel<<<ge, kThreads, 0, s>>>(gcol, out->counts, map, out->col);
-    GNN_LAUNCHED("relabel");
-    finish_kernel<<<grid_for(out->cap_src, kThreads, 1 << 16), kThreads, 0, s>>>(out->src_ids, out->counts, map,
-                                                                                 gcn_norm, out->src_norm);
-    GNN_LAUNCHED("finish");
-
+    const unsigned gw = grid_for(std::max<int64_t>(out->cap_dst, 1) * 64, kThreads, kMaxGrid);
+    if (fanout <= 64) hop_prepare_kernel<1><<<gw, kThreads, 0, s>>>(a);
+    else if (fanout <= 128) hop_prepare_kernel<2><<<gw, kThreads, 0, s>>>(a);
+    else if (fanout <= 256) hop_prepare_kernel<4><<<gw, kThreads, 0, s>>>(a);
+    else if (fanout <= 512) hop_prepare_kernel<8><<<gw, kThreads, 0, s>>>(a);
+    else hop_prepare_kernel<16><<<gw, kThreads, 0, s>>>(a);
+    GNN_LAUNCHED("hop_prepare");
+    hop_mark_kernel<<<static_cast<unsigned>(a.nb_rows), kThreads, 0, s>>>(a);
+    GNN_LAUNCHED("hop_mark");
+    hop_emit_kernel<<<static_cast<unsigned>(a.nb_bits), kThreads, 0, s>>>(a);
+    GNN_LAUNCHED("hop_emit");
+    hop_relabel_kernel<<<grid_for(std::max<int64_t>(out->cap_dst, 1) * fanout, kThreads, 1 << 16), kThreads, 0, s>>>(a);
+    GNN_LAUNCHED("hop_relabel");
     if (want_csc) {
-        int32_t *erow = reinterpret_cast<int32_t *>(base + w.erow);
-        int32_t *skey = reinterpret_cast<int32_t *>(base + w.skey);
-        edge_rows_kernel<<<grid_for(cap_dst, kThreads, kMaxGrid), kThreads, 0, s>>>(out->rowptr, out->counts, erow);
-        GNN_LAUNCHED("edge_rows");
-        GNN_TRY(radix_sort_pairs(out->col, erow, skey, out->cscrow, out->counts + 2, cap_nnz,
-                                 bits_for(out->cap_src), base + w.radix, s));
-        csc_ptr_kernel<<<grid_for(out->cap_src + 1, kThreads, kMaxGrid), kThreads, 0, s>>>(skey, out->counts,
-                                                                                          out->cscptr);
-        GNN_LAUNCHED("csc_ptr");
+        int32_t *sort = reinterpret_cast<int32_t *>(base + w.sort);
+        const int64_t cap_nnz = std::max<int64_t>(out->cap_dst * fanout, 1);
+        csc_build_kernel<<<1, kSortThreads, 0, s>>>(out->col, a.erow, out->counts, bits_for(out->cap_src), sort,
+                                                    sort + cap_nnz, sort + 2 * cap_nnz, sort + 3 * cap_nnz,
+                                                    out->cscrow, out->cscptr);
+        GNN_LAUNCHED("csc_build");
+    }
+    if (!defer_reset) {
+        hop_finish_kernel<<<grid_for(out->cap_src, kThreads, 1 << 16), kThreads, 0, s>>>(out->src_ids, out->counts,
+                                                                                        a.map);
+        GNN_LAUNCHED("hop_finish");
     }
     return GNN_OK;
 }

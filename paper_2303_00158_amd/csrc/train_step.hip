@@ -60,7 +60,7 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         if (m->kind == GNN_AGG_GCN_SYM) o->blk_src_norm[h] = c.take(static_cast<size_t>(o->cap_src[h]) * 4);
     }
     o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
-    size_t bwd = 0;
+    size_t bwd = 0, fwd = 0;
     for (int l = 1; l <= L; ++l) {
         const int hb = L - l;
         const int64_t rows = o->cap_dst[hb];
@@ -68,8 +68,11 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         o->h[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
         o->grad[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * 4);
         if (l >= 2) o->d_a[l] = c.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
-        bwd = std::max(bwd, update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows));
+        fwd = std::max(fwd, update_fwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
+        bwd = std::max(bwd, update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
     }
+    o->fwd_ws = c.take(fwd);
+    o->fwd_ws_bytes = fwd;
     o->bwd_ws = c.take(bwd);
     o->bwd_ws_bytes = bwd;
     o->loss_ws_bytes = softmax_ce_ws_bytes(batch);
@@ -112,12 +115,15 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
         const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
         GNN_TRY(launch_build_block(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h],
-                                   seed, step, h + 1, h < L - 1, &blk[h], base + o.sampler_ws, s));
+                                   seed, step, h + 1, h < L - 1, &blk[h], base + o.sampler_ws, true, s));
     }
     // feature loading: rows of the input layer's sources
     const gnn_block &b0 = blk[L - 1];
     void *x0 = base + o.x0;
-    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act, s));
+    // the last block's sources include every vertex the hops mapped: the
+    // gather puts the sampler's vertex map back to -1 as it reads them
+    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act,
+                          sampler_map(base + o.sampler_ws), s));
 
     // forward
     for (int l = 1; l <= L; ++l) {
@@ -129,7 +135,7 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
                                   m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l], l < L ? act : GNN_F32,
-                                  s));
+                                  base + o.fwd_ws, s));
     }
     // loss on the targets
     float *loss_slot = reinterpret_cast<float *>(base + o.loss);
@@ -143,17 +149,15 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         const int64_t f_in = m->dims[l - 1];
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         float *d_a = l > 1 ? reinterpret_cast<float *>(base + o.d_a[l]) : nullptr;
+        // the weight gradient kernel also applies SGD to W^l and b^l: every
+        // later backward step reads only lower layers' weights
         GNN_TRY(launch_update_bwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst,
                                   m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l],
-                                  m->precision, m->dw[l - 1], m->db[l - 1], d_a, base + o.bwd_ws, s));
+                                  m->precision, m->dw[l - 1], m->db[l - 1], d_a, base + o.bwd_ws, m->w[l - 1],
+                                  m->b[l - 1], lr, s));
         if (l > 1)
             GNN_TRY(launch_aggregate_bwd(&b, m->kind, d_a, f_in, hin, act,
                                          reinterpret_cast<float *>(base + o.grad[l - 1]), s));
-    }
-    // weight update
-    for (int l = 1; l <= L; ++l) {
-        GNN_TRY(launch_sgd(m->w[l - 1], m->dw[l - 1], k_of(m, l) * m->dims[l], lr, s));
-        GNN_TRY(launch_sgd(m->b[l - 1], m->db[l - 1], m->dims[l], lr, s));
     }
     step_tail_kernel<<<1, 64, 0, s>>>(blk[0].counts, L > 1 ? blk[1].counts : nullptr, L > 2 ? blk[2].counts : nullptr,
                                       L > 3 ? blk[3].counts : nullptr, loss_slot,

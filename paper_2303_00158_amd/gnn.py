@@ -58,7 +58,8 @@ class StepLayout(ctypes.Structure):
                 ("blk_col", _sz * _ML), ("blk_cscptr", _sz * _ML), ("blk_cscrow", _sz * _ML),
                 ("blk_src_norm", _sz * _ML),
                 ("x0", _sz), ("agg", _sz * (_ML + 1)), ("h", _sz * (_ML + 1)), ("grad", _sz * (_ML + 1)),
-                ("d_a", _sz * (_ML + 1)), ("bwd_ws", _sz), ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
+                ("d_a", _sz * (_ML + 1)), ("fwd_ws", _sz), ("fwd_ws_bytes", _sz), ("bwd_ws", _sz),
+                ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
                 ("loss_ws_bytes", _sz), ("edges", _sz), ("loss", _sz)]
 
 
@@ -74,8 +75,9 @@ _SIGNATURES = {
     "gnn_gather_features": (_i32, [_vp, _i32, _i32, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_fwd": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
-    "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp]),
-    "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _P(_sz)]),
+    "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
+    "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz, _vp]),
+    "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_bwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _sz,
                               _vp]),
     "gnn_softmax_ce_workspace_size": (_i32, [_i64, _P(_sz)]),
@@ -247,12 +249,27 @@ def aggregate_bwd(block: DeviceBlock, kind: int, d_a: torch.Tensor, f: int, d_sr
 
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],
                out: torch.Tensor, relu: bool, gemm_dtype: int, m_dev: Optional[torch.Tensor] = None,
-               cap_m: Optional[int] = None, stream=None) -> torch.Tensor:
+               cap_m: Optional[int] = None, ws: Optional[torch.Tensor] = None, split: bool = True,
+               stream=None) -> torch.Tensor:
+    """ws: zero-filled workspace reused across calls (allocated when None and
+    split is True); split=False runs without a workspace (no reduction split)."""
     cap = a_self.shape[0] if cap_m is None else cap_m
+    K = a_self.shape[1] * (2 if a_nbr is not None else 1)
+    if ws is None and split:
+        nb = _sz()
+        _check(lib().gnn_update_fwd_workspace_size(K, w.shape[1], cap, gemm_dtype, ctypes.byref(nb)))
+        ws = torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=a_self.device)
     _check(lib().gnn_update_fwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev), cap,
                                 _ptr(w), _ptr(bias), w.shape[1], int(relu), gemm_dtype, _ptr(out),
-                                dtype_code(out.dtype), _stream(stream)))
+                                dtype_code(out.dtype), _ptr(ws), ws.numel() if ws is not None else 0,
+                                _stream(stream)))
     return out
+
+
+def update_bwd_workspace(k: int, n_out: int, cap_m: int, gemm_dtype: int, device) -> torch.Tensor:
+    nb = _sz()
+    _check(lib().gnn_update_bwd_workspace_size(k, n_out, cap_m, gemm_dtype, ctypes.byref(nb)))
+    return torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=device)
 
 
 def update_bwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, g: torch.Tensor,
@@ -262,9 +279,7 @@ def update_bwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Ten
     cap = a_self.shape[0] if cap_m is None else cap_m
     K = a_self.shape[1] * (2 if a_nbr is not None else 1)
     if ws is None:
-        nb = _sz()
-        _check(lib().gnn_update_bwd_workspace_size(K, w.shape[1], cap, ctypes.byref(nb)))
-        ws = _aligned_empty(nb.value, a_self.device)
+        ws = update_bwd_workspace(K, w.shape[1], cap, gemm_dtype, a_self.device)
     _check(lib().gnn_update_bwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev),
                                 cap, _ptr(w), _ptr(g), w.shape[1], gemm_dtype, _ptr(dw), _ptr(db), _ptr(d_a),
                                 _ptr(ws), ws.numel(), _stream(stream)))

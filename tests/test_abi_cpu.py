@@ -58,11 +58,11 @@ def test_host_validation_errors(gnn):
     assert lib.gnn_last_error() == b""
     # NULL weights, unsupported dtypes, bad sizes: rejected before any launch
     assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
-                              gnn.GNN_F32, None) == gnn.GNN_EINVAL
+                              gnn.GNN_F32, None, 0, None) == gnn.GNN_EINVAL
     assert lib.gnn_update_fwd(None, None, gnn.GNN_F16, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
-                              gnn.GNN_F32, None) == gnn.GNN_EUNSUPPORTED
+                              gnn.GNN_F32, None, 0, None) == gnn.GNN_EUNSUPPORTED
     assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 0, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
-                              gnn.GNN_F32, None) == gnn.GNN_EINVAL
+                              gnn.GNN_F32, None, 0, None) == gnn.GNN_EINVAL
     assert lib.gnn_gather_features(None, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 10, 4, 4, None, None, 3, None,
                                    gnn.GNN_F16, None) == gnn.GNN_EUNSUPPORTED
     assert lib.gnn_gather_features(None, gnn.GNN_F32, 7, 10, 4, 4, None, None, 3, None,
@@ -78,7 +78,9 @@ def test_host_validation_errors(gnn):
     assert lib.gnn_build_block(ctypes.byref(g), None, None, None, 5, 0, 0, 1, 1, ctypes.byref(blk), None, 0,
                                None) == gnn.GNN_EINVAL
     nb = ctypes.c_size_t()
-    assert lib.gnn_update_bwd_workspace_size(0, 4, 4, ctypes.byref(nb)) == gnn.GNN_EINVAL
+    assert lib.gnn_update_bwd_workspace_size(0, 4, 4, gnn.GNN_BF16, ctypes.byref(nb)) == gnn.GNN_EINVAL
+    assert lib.gnn_update_fwd_workspace_size(8, 4, 4, gnn.GNN_F16, ctypes.byref(nb)) == gnn.GNN_EUNSUPPORTED
+    assert lib.gnn_update_fwd_workspace_size(8, 4, 1000, gnn.GNN_BF16, ctypes.byref(nb)) == gnn.GNN_OK
 
 
 def _model(gnn, kind, dims, fanouts, precision):

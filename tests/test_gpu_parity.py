@@ -305,6 +305,80 @@ def test_update_fwd_parity(m, ke, n, sage, code):
         assert err <= (1e-5 if code == oracle.F32 else 8e-3), (relu, err)
 
 
+def test_update_fwd_split_workspace_is_reusable():
+    # the split reduction keeps per-tile tickets in the workspace; a second
+    # call on the same workspace (smaller rows, other data) must be exact too
+    rng = np.random.default_rng(7)
+    ke, n = 256, 47
+    w = (rng.standard_normal((2 * ke, n)) / 16).astype(np.float32)
+    ws = None
+    for m in (1024, 333):
+        a_s = _act(rng, m, ke, oracle.BF16)
+        a_n = _act(rng, m, ke, oracle.BF16)
+        want = oracle.update_fwd(a_s, a_n, w, None, False, oracle.BF16, oracle.F32)
+        if ws is None:
+            nb = gnn._sz()
+            gnn._check(gnn.lib().gnn_update_fwd_workspace_size(2 * ke, n, 1024, gnn.GNN_BF16, gnn.ctypes.byref(nb)))
+            ws = torch.zeros(nb.value, dtype=torch.uint8, device=DEV)
+        out = torch.empty((1024, n), dtype=torch.float32, device=DEV)
+        m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
+        a_s_d = torch.zeros((1024, ke), dtype=torch.bfloat16, device=DEV)
+        a_n_d = torch.zeros((1024, ke), dtype=torch.bfloat16, device=DEV)
+        a_s_d[:m] = from_np_act(a_s)
+        a_n_d[:m] = from_np_act(a_n)
+        gnn.update_fwd(a_s_d, a_n_d, from_np_act(w), None, out, False, gnn.GNN_BF16, m_dev=m_dev, cap_m=1024, ws=ws)
+        assert relerr(out[:m].cpu().numpy(), want) <= 8e-3
+    torch.cuda.synchronize()
+    assert int(ws[:32768].view(torch.int32).abs().sum().item()) == 0  # tickets left at zero
+
+
+def test_update_workspaces_shared_across_shapes():
+    # one forward and one backward workspace serve GEMMs of different shapes
+    # in turn (as the layers of a training step do), twice over
+    rng = np.random.default_rng(9)
+    shapes = [(3000, 100, 256, True), (512, 256, 47, True), (3000, 100, 256, True), (512, 256, 47, True)]
+    nb = gnn._sz()
+    fw, bw = 0, 0
+    for m, ke, n, sage in shapes:
+        K = 2 * ke if sage else ke
+        gnn._check(gnn.lib().gnn_update_fwd_workspace_size(K, n, m, gnn.GNN_BF16, gnn.ctypes.byref(nb)))
+        fw = max(fw, nb.value)
+        gnn._check(gnn.lib().gnn_update_bwd_workspace_size(K, n, m, gnn.GNN_BF16, gnn.ctypes.byref(nb)))
+        bw = max(bw, nb.value)
+    ws_f = torch.zeros(fw, dtype=torch.uint8, device=DEV)
+    ws_b = torch.zeros(bw, dtype=torch.uint8, device=DEV)
+    for m, ke, n, sage in shapes:
+        a_s = _act(rng, m, ke, oracle.BF16)
+        a_n = _act(rng, m, ke, oracle.BF16)
+        K = 2 * ke
+        w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+        g = rng.standard_normal((m, n)).astype(np.float32)
+        out = torch.empty((m, n), dtype=torch.float32, device=DEV)
+        gnn.update_fwd(from_np_act(a_s), from_np_act(a_n), from_np_act(w), None, out, False, gnn.GNN_BF16, ws=ws_f)
+        assert relerr(out.cpu().numpy(), oracle.update_fwd(a_s, a_n, w, None, False, oracle.BF16, oracle.F32)) <= 8e-3
+        dw_w, db_w, da_w = oracle.update_bwd(a_s, a_n, w, g, oracle.BF16, want_da=True)
+        dw = torch.empty((K, n), device=DEV)
+        db = torch.empty(n, device=DEV)
+        da = torch.empty((m, K), device=DEV)
+        gnn.update_bwd(from_np_act(a_s), from_np_act(a_n), from_np_act(w), from_np_act(g), dw, db, da, gnn.GNN_BF16,
+                       ws=ws_b)
+        assert relerr(dw.cpu().numpy(), dw_w) <= 8e-3 and relerr(db.cpu().numpy(), db_w) <= 1e-5
+        assert relerr(da.cpu().numpy(), da_w) <= 8e-3
+
+
+@pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
+def test_update_fwd_without_workspace(code):
+    rng = np.random.default_rng(8)
+    m, ke, n = 700, 100, 256
+    a_s = _act(rng, m, ke, code)
+    a_n = _act(rng, m, ke, code)
+    w = (rng.standard_normal((2 * ke, n)) / 14).astype(np.float32)
+    want = oracle.update_fwd(a_s, a_n, w, None, True, code, code)
+    out = torch.empty((m, n), dtype=torch.bfloat16 if code == oracle.BF16 else torch.float32, device=DEV)
+    gnn.update_fwd(from_np_act(a_s), from_np_act(a_n), from_np_act(w), None, out, True, code, split=False)
+    assert relerr(oracle.to_float64(to_np_act(out)), oracle.to_float64(want)) <= (1e-5 if code == oracle.F32 else 8e-3)
+
+
 def test_update_fwd_device_row_count():
     rng = np.random.default_rng(1)
     m, ke, n = 500, 64, 96
