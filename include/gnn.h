@@ -195,13 +195,13 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
  *   gemm_dt GNN_BF16: operands rounded to bf16, matrix cores, fp32 accumulate;
  *           GNN_F32: fp32 throughout.
  *   out     [device] cap_m x n_out of odt; ReLU applied when relu != 0.
- *   ws      [device] workspace of gnn_update_fwd_workspace_size bytes, or
- *           NULL.  With a workspace the reduction over K may be split across
- *           workgroups; the partial tiles are then summed in a fixed order by
- *           the last workgroup of each output tile, so results stay bitwise
- *           reproducible.  The workspace must be zero-filled before its first
- *           use and is left zero-filled by every call; calls sharing one
- *           workspace must not overlap.
+ *   ws      [device] 256-byte aligned workspace of
+ *           gnn_update_fwd_workspace_size bytes (the size may be 0), or NULL.
+ *           With a workspace, a long reduction over few output tiles may be
+ *           split across workgroups; the fp32 partial tiles are then summed
+ *           in split order by a second kernel, so results stay bitwise
+ *           reproducible.  No state is kept in it between calls; calls
+ *           sharing one workspace must not overlap.
  * ------------------------------------------------------------------------ */
 gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
 gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
@@ -213,10 +213,11 @@ gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
  *   dw = A^T g (K x n_out), db = column sums of g (unrounded, may be NULL),
  *   d_a = g W^T (cap_m x K, fp32) when d_a is not NULL (layers above the
  *   first; Section V, equation T_Trainer: the first layer's backward is the
- *   update alone).  The reduction over rows is split across workgroups and
- *   summed in a fixed order, so results are bitwise reproducible.  ws must
- *   hold gnn_update_bwd_workspace_size bytes, zero-filled before its first use
- *   (every call leaves it zero-filled); calls sharing it must not overlap. */
+ *   update alone).  The reduction over rows is split across workgroups; the
+ *   fp32 partials go to ws and a second kernel sums them in split order, so
+ *   results are bitwise reproducible.  ws [device] must be 256-byte aligned
+ *   and hold gnn_update_bwd_workspace_size bytes; no state is kept in it
+ *   between calls; calls sharing it must not overlap. */
 gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
 gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
                           const int64_t *m_dev, int64_t cap_m, const float *w, const float *g, int64_t n_out,

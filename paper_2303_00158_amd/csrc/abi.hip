@@ -354,8 +354,6 @@ gnn_status gnn_train_step_workspace_init(const gnn_model *m, int64_t graph_n, in
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "gnn_train_step_workspace_init: ws must be 256-byte aligned");
     GNN_CHECK(ws_bytes >= o.total_bytes, GNN_ESIZE, "gnn_train_step_workspace_init: workspace %zu bytes, need %zu",
               ws_bytes, o.total_bytes);
-    GNN_TRY(launch_fill_zero(static_cast<char *>(ws) + o.fwd_ws, o.fwd_ws_bytes, stream_of(s)));
-    GNN_TRY(launch_fill_zero(static_cast<char *>(ws) + o.bwd_ws, o.bwd_ws_bytes, stream_of(s)));
     return launch_sampler_ws_init(static_cast<char *>(ws) + o.sampler_ws, graph_n, stream_of(s));
 }
 

@@ -9,23 +9,28 @@
 //   weights   dW = A^T G, db = colsum(G)    (optionally followed by SGD)
 //
 // One engine serves all three: a 256-thread workgroup (4 wavefronts as 2 x 2)
-// computes a BM x BN tile (128 x 128 or 64 x 64) of C = P Q^T, walking the
+// computes a BM x BN tile (64 x 64 or 128 x 128) of C = P Q^T, walking the
 // reduction in chunks of BK (64 for bf16, 32 for fp32).  Both operand tiles
 // are staged in LDS with the reduction index contiguous (Ps[row][r],
-// Qs[col][r]); each operand source knows its memory layout.  The next chunk
-// is fetched into registers while the matrix cores work on the current one.
-// Every global load is issued unconditionally from a clamped, in-bounds
-// address and masked afterwards, so a chunk's loads are all in flight at once.
+// Qs[col][r]); each operand source knows its memory layout.
 //   bf16: v_mfma_f32_16x16x32_bf16, operands rounded to bf16 on staging;
 //   fp32: v_mfma_f32_16x16x4_f32.
 // Accumulation is fp32.
 //
-// The shapes of a sampled mini-batch are small and latency-bound, so the
-// reduction can be split over blockIdx.z.  Each split writes its partial
-// tile to the workspace in register order, and the last workgroup to finish
-// a tile (an integer ticket per tile) sums all partials in split order and
-// runs the epilogue.  The order of the sum is fixed, so results are bitwise
-// reproducible, and no extra kernel launch is needed.
+// The shapes of a sampled mini-batch are small, so every kernel here is
+// bound by memory latency rather than bandwidth or matrix-core rate.  The
+// engine is written around that:
+//  * a ring of D register stages keeps D chunks of loads in flight while the
+//    matrix cores work on an earlier chunk;
+//  * every global load is issued from a clamped, in-bounds address with no
+//    per-element branch, so a chunk's loads issue back to back;
+//  * epilogue operands (bias, the weights an SGD step updates) are loaded
+//    once, before the stores, never inside a load-use chain;
+//  * reductions that are split across workgroups never synchronise inside
+//    the kernel: each split writes a row-major partial tile and a separate
+//    reduction kernel sums the partials in split order.  (A device-scope
+//    fence per workgroup costs an L2 writeback on this part, far more than
+//    one extra launch.)  The fixed order keeps results bitwise reproducible.
 #pragma once
 
 #include "internal.h"
@@ -42,12 +47,10 @@ template <bool BF16> struct Cfg;
 template <> struct Cfg<true> {
     using T = uint16_t;
     static constexpr int BK = 64, LDK = BK + 8;
-    __device__ __forceinline__ static T cvt(float x) { return f32_to_bf16(x); }
 };
 template <> struct Cfg<false> {
     using T = float;
     static constexpr int BK = 32, LDK = BK + 4;
-    __device__ __forceinline__ static T cvt(float x) { return x; }
 };
 
 // A chunk of four source elements kept in its storage form until commit:
@@ -67,6 +70,15 @@ template <> struct Raw<uint16_t> {
                            __uint_as_float(v.y & 0xffff0000u));
     }
     __device__ __forceinline__ static uint2 to_bf16(type v) { return v; }
+    __device__ __forceinline__ static float elem(type v, int e) {
+        const uint32_t w = e < 2 ? v.x : v.y;
+        return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    }
+    // element e as bf16 bits
+    __device__ __forceinline__ static uint32_t bits(type v, int e) {
+        const uint32_t w = e < 2 ? v.x : v.y;
+        return (e & 1) ? (w >> 16) : (w & 0xffffu);
+    }
 };
 template <> struct Raw<float> {
     using type = float4;
@@ -79,11 +91,16 @@ template <> struct Raw<float> {
         return make_uint2(static_cast<uint32_t>(f32_to_bf16(v.x)) | (static_cast<uint32_t>(f32_to_bf16(v.y)) << 16),
                           static_cast<uint32_t>(f32_to_bf16(v.z)) | (static_cast<uint32_t>(f32_to_bf16(v.w)) << 16));
     }
+    __device__ __forceinline__ static float elem(type v, int e) {
+        return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
+    }
+    __device__ __forceinline__ static uint32_t bits(type v, int e) { return f32_to_bf16(elem(v, e)); }
 };
 
 // ---------------------------------------------------------------------------
-// operand sources: fetch() loads this thread's chunks of the tile for
-// reduction offset r0 into registers; commit() writes them to LDS.
+// operand sources: fetch(s, r0) loads this thread's chunks of the tile for
+// reduction offset r0 into register stage s; commit(s, lds) writes stage s
+// to LDS.  Stage indices must be compile-time constants after unrolling.
 // ---------------------------------------------------------------------------
 
 // Rows of a row-major matrix, 4 consecutive reduction elements per chunk
@@ -92,110 +109,135 @@ template <> struct Raw<float> {
 // ld).  Element (tile row t, red r) = X[row0 + t][r].  Requires rows >= 1,
 // cols >= 1; with VEC, cols and split are multiples of 4 and the rows are
 // 4-element aligned.
-template <bool BF16, int ROWS, class TX, bool VEC>
+template <bool BF16, int ROWS, class TX, bool VEC, int D>
 struct SrcRows {
     static constexpr int BK = Cfg<BF16>::BK;
     static constexpr int CPR = BK / 4;                       // chunks per tile row
     static constexpr int NCH = ROWS * BK / 4 / kThreads;     // chunks per thread
     const TX *x0, *x1;
     int64_t ld, split, rows, cols, row0;
-    typename Raw<TX>::type reg[NCH];
+    typename Raw<TX>::type reg[D][NCH];
+    // branch-free choice between the two halves of the concatenation
     __device__ __forceinline__ const TX *addr(int64_t t, int64_t r) const {
-        return (x1 != nullptr && r >= split) ? x1 + t * split + (r - split) : x0 + t * ld + r;
+        const bool hi = x1 != nullptr && r >= split;
+        const TX *base = hi ? x1 : x0;
+        return base + (hi ? t * split + (r - split) : t * ld + r);
     }
     // Out-of-range indices are clamped to valid ones: tile rows past `rows`
     // only feed output rows that are never stored, and reduction indices past
     // the range are zeroed in LDS by zero_tail().
-    __device__ void fetch(int64_t r0) {
+    __device__ __forceinline__ void fetch(int s, int64_t r0) {
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int q = threadIdx.x + i * kThreads;
             const int64_t t = row0 + q / CPR, r = r0 + (q % CPR) * 4;
             const int64_t tc = t < rows ? t : rows - 1;
             if constexpr (VEC) {
-                reg[i] = Raw<TX>::load(addr(tc, r < cols ? r : 0));
+                reg[s][i] = Raw<TX>::load(addr(tc, r < cols ? r : 0));
             } else {
-                reg[i] = Raw<TX>::load_each(addr(tc, r < cols ? r : 0), addr(tc, r + 1 < cols ? r + 1 : 0),
-                                            addr(tc, r + 2 < cols ? r + 2 : 0), addr(tc, r + 3 < cols ? r + 3 : 0));
+                reg[s][i] = Raw<TX>::load_each(addr(tc, r < cols ? r : 0), addr(tc, r + 1 < cols ? r + 1 : 0),
+                                               addr(tc, r + 2 < cols ? r + 2 : 0), addr(tc, r + 3 < cols ? r + 3 : 0));
             }
         }
     }
-    __device__ void commit(typename Cfg<BF16>::T *lds) const {
+    __device__ __forceinline__ void commit(int s, typename Cfg<BF16>::T *lds) const {
         using CV = Cfg<BF16>;
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int q = threadIdx.x + i * kThreads;
             typename CV::T *p = lds + (q / CPR) * CV::LDK + (q % CPR) * 4;
             if constexpr (BF16)
-                *reinterpret_cast<uint2 *>(p) = Raw<TX>::to_bf16(reg[i]);
+                *reinterpret_cast<uint2 *>(p) = Raw<TX>::to_bf16(reg[s][i]);
             else
-                *reinterpret_cast<float4 *>(p) = Raw<TX>::to_f32(reg[i]);
+                *reinterpret_cast<float4 *>(p) = Raw<TX>::to_f32(reg[s][i]);
         }
     }
 };
 
 // Columns of a row-major matrix Y, read as element (tile row t, red r) =
-// Y[r][col0 + t], 4 consecutive tile rows per chunk ("T-contiguous").  Y may
-// be the concatenation [y0 || y1] along its columns (each of width `split`).
-// Requires ncols >= 1; with VEC, ncols and split are multiples of 4.
-template <bool BF16, int ROWS, class TY, bool VEC>
+// Y[r][col0 + t]: each thread loads 4 consecutive tile rows ("T-contiguous")
+// for NCH consecutive reduction indices, and transposes the 4 x 4 blocks in
+// registers so that LDS receives 4 consecutive reduction elements per write.
+// Y may be the concatenation [y0 || y1] along its columns (each of width
+// `split`).  Requires ncols >= 1; with VEC, ncols and split are multiples of 4.
+template <bool BF16, int ROWS, class TY, bool VEC, int D>
 struct SrcCols {
     static constexpr int BK = Cfg<BF16>::BK;
     static constexpr int TPR = ROWS / 4;                     // threads per reduction index
     static constexpr int RPP = kThreads / TPR;               // reduction indices per pass
-    static constexpr int NCH = BK / RPP;
+    static constexpr int NCH = BK / RPP;                     // consecutive reduction indices per thread
     const TY *y0, *y1;
     int64_t ld, split, ncols, r_end, col0;
-    typename Raw<TY>::type reg[NCH];
+    typename Raw<TY>::type reg[D][NCH];
     __device__ __forceinline__ int my_t() const { return (threadIdx.x % TPR) * 4; }
-    __device__ __forceinline__ int my_r(int i) const { return threadIdx.x / TPR + i * RPP; }
+    __device__ __forceinline__ int my_r(int i) const { return (threadIdx.x / TPR) * NCH + i; }
     __device__ __forceinline__ const TY *addr(int64_t r, int64_t t) const {
-        return (y1 != nullptr && t >= split) ? y1 + r * split + (t - split) : y0 + r * ld + t;
+        const bool hi = y1 != nullptr && t >= split;
+        const TY *base = hi ? y1 : y0;
+        return base + (hi ? r * split + (t - split) : r * ld + t);
     }
     // Clamped like SrcRows: columns past ncols only feed outputs that are not
     // stored; reduction rows past r_end are zeroed in LDS.
-    __device__ void fetch(int64_t r0) {
+    __device__ __forceinline__ void fetch(int s, int64_t r0) {
         const int64_t t = col0 + my_t();
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int64_t r = r0 + my_r(i);
             const int64_t rc = r < r_end ? r : r_end - 1;
             if constexpr (VEC) {
-                reg[i] = Raw<TY>::load(addr(rc, t < ncols ? t : 0));
+                reg[s][i] = Raw<TY>::load(addr(rc, t < ncols ? t : 0));
             } else {
-                reg[i] = Raw<TY>::load_each(addr(rc, t < ncols ? t : 0), addr(rc, t + 1 < ncols ? t + 1 : 0),
-                                            addr(rc, t + 2 < ncols ? t + 2 : 0), addr(rc, t + 3 < ncols ? t + 3 : 0));
+                reg[s][i] = Raw<TY>::load_each(addr(rc, t < ncols ? t : 0), addr(rc, t + 1 < ncols ? t + 1 : 0),
+                                               addr(rc, t + 2 < ncols ? t + 2 : 0), addr(rc, t + 3 < ncols ? t + 3 : 0));
             }
         }
     }
-    __device__ void commit(typename Cfg<BF16>::T *lds) const {
+    __device__ __forceinline__ void commit(int s, typename Cfg<BF16>::T *lds) const {
         using CV = Cfg<BF16>;
+        const int tt = my_t();
+        if constexpr (NCH % 4 == 0) {
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            const int kk = my_r(i), tt = my_t();
-            if constexpr (BF16) {
-                const uint2 b = Raw<TY>::to_bf16(reg[i]);
-                lds[(tt + 0) * CV::LDK + kk] = static_cast<uint16_t>(b.x & 0xffffu);
-                lds[(tt + 1) * CV::LDK + kk] = static_cast<uint16_t>(b.x >> 16);
-                lds[(tt + 2) * CV::LDK + kk] = static_cast<uint16_t>(b.y & 0xffffu);
-                lds[(tt + 3) * CV::LDK + kk] = static_cast<uint16_t>(b.y >> 16);
-            } else {
-                const float4 v = Raw<TY>::to_f32(reg[i]);
-                lds[(tt + 0) * CV::LDK + kk] = v.x;
-                lds[(tt + 1) * CV::LDK + kk] = v.y;
-                lds[(tt + 2) * CV::LDK + kk] = v.z;
-                lds[(tt + 3) * CV::LDK + kk] = v.w;
+            for (int g = 0; g < NCH / 4; ++g) {
+                const int kk = my_r(4 * g);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    typename CV::T *p = lds + (tt + e) * CV::LDK + kk;
+                    if constexpr (BF16) {
+                        const uint2 v = make_uint2(
+                            Raw<TY>::bits(reg[s][4 * g + 0], e) | (Raw<TY>::bits(reg[s][4 * g + 1], e) << 16),
+                            Raw<TY>::bits(reg[s][4 * g + 2], e) | (Raw<TY>::bits(reg[s][4 * g + 3], e) << 16));
+                        *reinterpret_cast<uint2 *>(p) = v;
+                    } else {
+                        const float4 v = make_float4(Raw<TY>::elem(reg[s][4 * g + 0], e),
+                                                     Raw<TY>::elem(reg[s][4 * g + 1], e),
+                                                     Raw<TY>::elem(reg[s][4 * g + 2], e),
+                                                     Raw<TY>::elem(reg[s][4 * g + 3], e));
+                        *reinterpret_cast<float4 *>(p) = v;
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int kk = my_r(i);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if constexpr (BF16)
+                        lds[(tt + e) * CV::LDK + kk] = static_cast<uint16_t>(Raw<TY>::bits(reg[s][i], e));
+                    else
+                        lds[(tt + e) * CV::LDK + kk] = Raw<TY>::elem(reg[s][i], e);
+                }
             }
         }
     }
-    // fp32 sums of the fetched values over this thread's reduction rows
-    // below r_end (when `tail` is false every fetched row is in range).
-    __device__ void add_colsum(float4 &s, int64_t r0, bool tail) const {
+    // fp32 sums of stage s over this thread's reduction rows below r_end
+    // (when `tail` is false every fetched row is in range).
+    __device__ __forceinline__ void add_colsum(int s, float4 &sum, int64_t r0, bool tail) const {
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             if (tail && r0 + my_r(i) >= r_end) continue;
-            const float4 v = Raw<TY>::to_f32(reg[i]);
-            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+            const float4 v = Raw<TY>::to_f32(reg[s][i]);
+            sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
         }
     }
 };
@@ -206,7 +248,6 @@ struct SrcCols {
 template <int BM, int BN>
 struct Acc {
     static constexpr int WI = BM / 32, WJ = BN / 32;  // 16 x 16 MFMA tiles per wavefront
-    static constexpr int N = WI * WJ * 4;             // floats per thread
     f32x4 c[WI][WJ];
 };
 
@@ -280,9 +321,15 @@ __device__ __forceinline__ void zero_tail(typename Cfg<BF16>::T *Ps, typename Cf
     }
 }
 
-// acc = sum over r in [r_beg, r_end) of P[.., r] Q[.., r].  colsum(src, r0,
-// tail) is called once per chunk with the right operand's staged registers.
-template <bool BF16, int BM, int BN, class SP, class SQ, class ColSum>
+// acc = sum over r in [r_beg, r_end) of P[.., r] Q[.., r], with a ring of D
+// register stages.  colsum(sq, stage, r0, tail) is called once per chunk
+// with the right operand's staged registers.
+//
+// Every stage is fetched unconditionally, also for chunks past the end
+// (their clamped addresses re-read cached lines and the data is never
+// committed): the number of loads in flight behind each stage is then the
+// same on every path, so the wait before a commit covers that stage alone.
+template <bool BF16, int D, int BM, int BN, class SP, class SQ, class ColSum>
 __device__ __forceinline__ void run_tile(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64_t r_beg, int64_t r_end, char *lds,
                                          ColSum &&colsum) {
     using CV = Cfg<BF16>;
@@ -294,82 +341,67 @@ __device__ __forceinline__ void run_tile(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64
 #pragma unroll
         for (int j = 0; j < Acc<BM, BN>::WJ; ++j) acc.c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (r_beg >= r_end) return;
-    sp.fetch(r_beg);
-    sq.fetch(r_beg);
-    for (int64_t r0 = r_beg; r0 < r_end; r0 += CV::BK) {
+    const int64_t nch = ceil_div(r_end - r_beg, CV::BK);
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+        sp.fetch(s, r_beg + s * CV::BK);
+        sq.fetch(s, r_beg + s * CV::BK);
+    }
+    // one chunk through stage s: commit, refill the stage D chunks ahead,
+    // multiply
+    auto step = [&](int s, int64_t c) {
+        const int64_t r0 = r_beg + c * CV::BK;
         const bool tail = r0 + CV::BK > r_end;
-        colsum(sq, r0, tail);  // reads the staged registers, which the commit waits for anyway
-        sp.commit(Ps);
-        sq.commit(Qs);
+        colsum(sq, s, r0, tail);
+        sp.commit(s, Ps);
+        sq.commit(s, Qs);
         if (tail) {
             __syncthreads();
             zero_tail<BF16, BM, BN>(Ps, Qs, static_cast<int>(r_end - r0));
         }
         __syncthreads();
-        if (r0 + CV::BK < r_end) {
-            sp.fetch(r0 + CV::BK);
-            sq.fetch(r0 + CV::BK);
-        }
+        sp.fetch(s, r0 + D * CV::BK);
+        sq.fetch(s, r0 + D * CV::BK);
         mma_chunk<BF16, BM, BN>(acc, Ps, Qs);
         __syncthreads();
+    };
+    // Whole groups of D chunks, then the remainder outside the loop, so that
+    // the loop's back edge sees the same loads in flight on every path.
+    int64_t c0 = 0;
+    for (; c0 + D <= nch; c0 += D) {
+#pragma unroll
+        for (int s = 0; s < D; ++s) step(s, c0 + s);
     }
+#pragma unroll
+    for (int s = 0; s < D - 1; ++s)
+        if (c0 + s < nch) step(s, c0 + s);
 }
 
-// Split reduction.  Returns false when this workgroup is not the last of its
-// tile (it has written its partial and must exit); otherwise acc holds the
-// sum over all splits in split order.
+// ---------------------------------------------------------------------------
+// epilogue: the tile is staged through LDS so that every thread ends up with
+// row-contiguous 4-column chunks.  The chunk set of a thread is known before
+// the staging (TileOut), so callers load epilogue operands up front.
+// ---------------------------------------------------------------------------
 template <int BM, int BN>
-__device__ __forceinline__ bool reduce_splits(Acc<BM, BN> &acc, float *part, int *tickets, int tile, int ntiles,
-                                              int nsplit, int split) {
-    if (nsplit == 1) return true;
-    constexpr int WI = Acc<BM, BN>::WI, WJ = Acc<BM, BN>::WJ, NA = Acc<BM, BN>::N;
-    __shared__ int is_last;
-    float4 *mine = reinterpret_cast<float4 *>(part + (static_cast<int64_t>(split) * ntiles + tile) * kThreads * NA) +
-                   threadIdx.x * (NA / 4);
-#pragma unroll
-    for (int i = 0; i < WI; ++i)
-#pragma unroll
-        for (int j = 0; j < WJ; ++j)
-            mine[i * WJ + j] = make_float4(acc.c[i][j][0], acc.c[i][j][1], acc.c[i][j][2], acc.c[i][j][3]);
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) is_last = (atomicAdd(&tickets[tile], 1) == nsplit - 1);
-    __syncthreads();
-    if (!is_last) return false;
-    __threadfence();
-#pragma unroll
-    for (int i = 0; i < WI; ++i)
-#pragma unroll
-        for (int j = 0; j < WJ; ++j) acc.c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < nsplit; ++s) {
-        const float4 *src = reinterpret_cast<const float4 *>(part + (static_cast<int64_t>(s) * ntiles + tile) *
-                                                                        kThreads * NA) + threadIdx.x * (NA / 4);
-        float4 v[WI * WJ];
-#pragma unroll
-        for (int x = 0; x < WI * WJ; ++x) v[x] = src[x];
-#pragma unroll
-        for (int i = 0; i < WI; ++i)
-#pragma unroll
-            for (int j = 0; j < WJ; ++j) {
-                acc.c[i][j][0] += v[i * WJ + j].x;
-                acc.c[i][j][1] += v[i * WJ + j].y;
-                acc.c[i][j][2] += v[i * WJ + j].z;
-                acc.c[i][j][3] += v[i * WJ + j].w;
-            }
+struct TileOut {
+    static constexpr int CPR = BN / 4;              // 4-column chunks per row
+    static constexpr int RPI = kThreads / CPR;      // rows per pass
+    static constexpr int PER_HALF = (BM / 2) / RPI; // passes per half tile
+    static constexpr int NIT = 2 * PER_HALF;
+    __device__ __forceinline__ static int col() { return (threadIdx.x % CPR) * 4; }
+    __device__ __forceinline__ static int row(int it) {
+        return (it / PER_HALF) * (BM / 2) + (it % PER_HALF) * RPI + threadIdx.x / CPR;
     }
-    if (threadIdx.x == 0) tickets[tile] = 0;  // ready for the next launch
-    return true;
-}
+};
 
-// Write the tile through LDS so global stores are row-contiguous:
-// out[(row0 + r) * ld + col0 + c] = f(col, value) for rows < rows_valid,
-// columns < cols_valid.  Two passes of BM/2 rows.
-template <int BM, int BN, class TO, class F>
-__device__ __forceinline__ void store_tile(const Acc<BM, BN> &acc, char *lds, TO *out, int64_t ld, int64_t row0,
-                                           int64_t col0, int64_t rows_valid, int64_t cols_valid, F &&f) {
+// emit(it, tile_row, tile_col, float4) for each of this thread's NIT chunks.
+template <int BM, int BN, class Emit>
+__device__ __forceinline__ void emit_tile(const Acc<BM, BN> &acc, char *lds, Emit &&emit) {
+    using TO = TileOut<BM, BN>;
     float *st = reinterpret_cast<float *>(lds);
     constexpr int LD = BN + 4, HR = BM / 2;
     const int wave = threadIdx.x >> 6;
+#pragma unroll
     for (int half = 0; half < 2; ++half) {
         __syncthreads();
         if ((wave >> 1) == half) {
@@ -382,26 +414,73 @@ __device__ __forceinline__ void store_tile(const Acc<BM, BN> &acc, char *lds, TO
                         st[(acc_row<BM, BN>(i, q) - half * HR) * LD + acc_col<BM, BN>(j)] = acc.c[i][j][q];
         }
         __syncthreads();
-        for (int q = threadIdx.x; q < HR * (BN / 4); q += kThreads) {
-            const int r = q / (BN / 4), c = (q % (BN / 4)) * 4;
-            const int64_t gr = row0 + half * HR + r;
-            if (gr >= rows_valid) continue;
-            const int64_t gc = col0 + c;
-            const float4 v = *reinterpret_cast<const float4 *>(st + r * LD + c);
-            const float vv[4] = {v.x, v.y, v.z, v.w};
-            if (gc + 3 < cols_valid && aligned_dev(out + gr * ld + gc, sizeof(TO) * 4)) {
-                float o[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) o[e] = f(gc + e, vv[e]);
-                store4(out, gr * ld + gc, make_float4(o[0], o[1], o[2], o[3]));
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (gc + e < cols_valid) Elem<TO>::store(out, gr * ld + gc + e, f(gc + e, vv[e]));
-            }
+        for (int k = 0; k < TO::PER_HALF; ++k) {
+            const int it = half * TO::PER_HALF + k;
+            const int r = TO::row(it), c = TO::col();
+            emit(it, r, c, *reinterpret_cast<const float4 *>(st + (r - half * HR) * LD + c));
         }
     }
 }
+
+// Four consecutive elements p[i..i+3] of a row whose valid length ends at
+// `lim` (exclusive), as floats.  With VEC the row is 4-aligned and i < lim
+// implies i + 3 < lim; past-the-end elements read a clamped index.
+template <bool VEC>
+__device__ __forceinline__ float4 load4_clamped(const float *p, int64_t row_base, int64_t i, int64_t lim) {
+    if constexpr (VEC) {
+        return *reinterpret_cast<const float4 *>(p + row_base + (i < lim ? i : 0));
+    } else {
+        const int64_t last = lim - 1;
+        return make_float4(p[row_base + min(i, last)], p[row_base + min(i + 1, last)], p[row_base + min(i + 2, last)],
+                           p[row_base + min(i + 3, last)]);
+    }
+}
+
+// Store elements i..i+3 (those below lim) of a row; VEC as in load4_clamped.
+template <bool VEC, class TO>
+__device__ __forceinline__ void store4_masked(TO *p, int64_t row_base, int64_t i, int64_t lim, float4 v) {
+    if (i >= lim) return;
+    if constexpr (VEC) {
+        store4(p, row_base + i, v);
+    } else {
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (i + e < lim) Elem<TO>::store(p, row_base + i + e, vv[e]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// launch plans
+// ---------------------------------------------------------------------------
+inline int bk_of(bool bf16) { return bf16 ? Cfg<true>::BK : Cfg<false>::BK; }
+
+// 128 x 128 tiles only when even they give two workgroups per CU.
+inline int pick_tile(int64_t rows, int64_t cols) {
+    const int64_t t128 = ceil_div(std::max<int64_t>(rows, 1), 128) * ceil_div(std::max<int64_t>(cols, 1), 128);
+    return t128 >= 512 ? 128 : 64;
+}
+
+// Register stages in flight per tile size.
+template <int TILE> constexpr int depth() { return TILE == 64 ? 3 : 2; }
+
+// Workgroup -> output tile mapping.  Workgroups are dealt round-robin to
+// the 8 XCDs (each with its own L2); consecutive workgroups of one XCD take
+// the column tiles of one row block, so the row block's operand rows are
+// fetched into that XCD's L2 once.
+constexpr int kXcds = 8;
+struct TileMap {
+    int64_t mt, nt;  // row and column tiles
+    __host__ __device__ int64_t groups() const { return ceil_div(mt, kXcds); }
+    __host__ __device__ int64_t blocks() const { return groups() * kXcds * nt; }
+    __device__ void tile_of(int64_t b, int64_t *x, int64_t *y) const {
+        const int64_t per_group = kXcds * nt;
+        const int64_t g = b / per_group, j = b % per_group;
+        *x = g * kXcds + j % kXcds;
+        *y = j / kXcds;
+    }
+};
 
 // Reduction range of split `split` out of `nsplit` over [0, total), in
 // whole chunks.
@@ -412,63 +491,42 @@ __device__ __forceinline__ void split_range(int64_t total, int nsplit, int split
     *end = min(total, *beg + per);
 }
 
-// ---------------------------------------------------------------------------
-// launch plans
-// ---------------------------------------------------------------------------
-struct Plan {
-    int tile;  // 128 or 64 (square tiles)
-    dim3 grid;
-    int ntiles, nsplit;
-};
+// Leading dimension of the fp32 partial tiles of a split reduction.
+__host__ __device__ inline int64_t part_ld(int64_t cols) { return (cols + 3) / 4 * 4; }
 
-// Every GEMM workspace starts with a fixed ticket area (independent of the
-// shape, so a workspace can be reused by calls of different shapes without
-// partial tiles ever landing on tickets).  Launches with more tiles than
-// tickets run unsplit.
-constexpr size_t kTicketBytes = 32768;
-constexpr int kMaxTickets = static_cast<int>(kTicketBytes / 4);
-
-inline int bk_of(bool bf16) { return bf16 ? Cfg<true>::BK : Cfg<false>::BK; }
-
-inline Plan make_plan(int tile, int64_t rows, int64_t cols, int64_t red, bool bf16, int max_split, int target) {
-    Plan p;
-    p.tile = tile;
-    const int64_t mt = ceil_div(std::max<int64_t>(rows, 1), tile), nt = ceil_div(std::max<int64_t>(cols, 1), tile);
-    p.ntiles = static_cast<int>(mt * nt);
-    int64_t s = 1;
-    if (p.ntiles <= kMaxTickets) {
-        s = ceil_div(target, p.ntiles);
-        s = std::min<int64_t>(s, ceil_div(std::max<int64_t>(red, 1), bk_of(bf16)));
-        s = std::min<int64_t>(s, max_split);
-        s = std::max<int64_t>(s, 1);
+// Sum over splits s = 0..nsplit-1, in that order, of the float4 at
+// p + s * stride.  Loads are issued eight splits at a time.
+__device__ __forceinline__ float4 sum_splits(const float *p, int64_t stride, int nsplit) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < nsplit; s0 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int g = 0; g < 8; ++g)
+            v[g] = *reinterpret_cast<const float4 *>(p + static_cast<int64_t>(min(s0 + g, nsplit - 1)) * stride);
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            if (s0 + g < nsplit) {
+                acc.x += v[g].x;
+                acc.y += v[g].y;
+                acc.z += v[g].z;
+                acc.w += v[g].w;
+            }
+        }
     }
-    p.nsplit = static_cast<int>(s);
-    p.grid = dim3(static_cast<unsigned>(mt), static_cast<unsigned>(nt), static_cast<unsigned>(p.nsplit));
-    return p;
+    return acc;
 }
 
-// Output tiles of rows x cols with a reduction of `red`: big outputs use
-// 128 x 128 tiles unsplit; small ones 64 x 64 tiles with the reduction split
-// to reach about one workgroup per CU.
-inline Plan plan_fwd(int64_t rows, int64_t cols, int64_t red, bool bf16) {
-    const int64_t t128 = ceil_div(std::max<int64_t>(rows, 1), 128) * ceil_div(std::max<int64_t>(cols, 1), 128);
-    if (t128 >= 192) return make_plan(128, rows, cols, red, bf16, 1, 256);
-    return make_plan(64, rows, cols, red, bf16, 8, 256);
-}
-
-inline Plan plan_dw(int64_t K, int64_t n_out, int64_t cap_m, bool bf16) {
-    const int64_t t64 = ceil_div(K, 64) * ceil_div(n_out, 64);
-    if (t64 >= 512) return make_plan(128, K, n_out, cap_m, bf16, 16, 512);
-    return make_plan(64, K, n_out, cap_m, bf16, 16, 256);
-}
-
-inline size_t part_bytes(const Plan &p) {
-    const size_t per_thread = static_cast<size_t>(p.tile / 32) * (p.tile / 32) * 4;
-    return p.nsplit > 1 ? static_cast<size_t>(p.nsplit) * p.ntiles * kThreads * per_thread * 4 : 0;
-}
-
-inline size_t dbpart_bytes(const Plan &p, int64_t n_out) {
-    return static_cast<size_t>(p.nsplit) * ceil_div(n_out, p.tile) * p.tile * 4;
+// Bias add and ReLU (non-positive and NaN inputs give 0) of the forward
+// epilogue.
+__device__ __forceinline__ float4 bias_act(float4 v, float4 b, int relu) {
+    float4 z = make_float4(v.x + b.x, v.y + b.y, v.z + b.z, v.w + b.w);
+    if (relu) {
+        z.x = z.x > 0.f ? z.x : 0.f;
+        z.y = z.y > 0.f ? z.y : 0.f;
+        z.z = z.z > 0.f ? z.z : 0.f;
+        z.w = z.w > 0.f ? z.w : 0.f;
+    }
+    return z;
 }
 
 }  // namespace gemm

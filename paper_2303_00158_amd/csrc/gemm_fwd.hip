@@ -1,5 +1,10 @@
 // Forward update (equation 2): Z = [A_self || A_nbr] W + b with the ReLU
 // and narrowing epilogue, on the matrix-core engine of gemm_engine.h.
+//
+// The whole reduction of a tile normally runs in one workgroup.  Only when
+// the output has few tiles and K is long is the reduction split; the
+// partial tiles then go to the workspace and fwd_reduce_kernel finishes
+// them (sum in split order, bias, ReLU, narrowing).
 #include "gemm_engine.h"
 
 namespace gnn {
@@ -8,45 +13,89 @@ namespace {
 
 using namespace gemm;
 
-// ---------------------------------------------------------------------------
-// forward: out = act([self || nbr] W + b)
-// ---------------------------------------------------------------------------
-template <bool BF16, int BM, int BN, class TA, class TO, bool VA, bool VW>
+template <bool BF16, int TILE, class TA, class TO, bool VA, bool VW, bool VO>
 __global__ void __launch_bounds__(kThreads) update_fwd_kernel(const TA *__restrict__ a_self,
                                                                const TA *__restrict__ a_nbr, int64_t k_each,
                                                                const int64_t *m_dev, int64_t cap_m,
                                                                const float *__restrict__ w,
                                                                const float *__restrict__ bias, int64_t n_out,
-                                                               int relu, TO *__restrict__ out, float *part,
-                                                               int *tickets) {
-    __shared__ __attribute__((aligned(16))) char lds[lds_bytes<BM, BN>()];
+                                                               int relu, TO *__restrict__ out,
+                                                               float *__restrict__ part, TileMap map) {
+    constexpr int D = depth<TILE>();
+    __shared__ __attribute__((aligned(16))) char lds[lds_bytes<TILE, TILE>()];
+    int64_t tx, ty;
+    map.tile_of(blockIdx.x, &tx, &ty);
     const int64_t M = m_dev ? min(*m_dev, cap_m) : cap_m;
-    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * BM;
-    const int64_t col0 = static_cast<int64_t>(blockIdx.y) * BN;
-    if (row0 >= M) return;
+    const int64_t row0 = tx * TILE, col0 = ty * TILE;
+    if (tx >= map.mt || row0 >= M) return;
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     int64_t r_beg, r_end;
     split_range<Cfg<BF16>::BK>(K, gridDim.z, blockIdx.z, &r_beg, &r_end);
-    SrcRows<BF16, BM, TA, VA> sp{a_self, a_nbr, k_each, k_each, M, K, row0, {}};
-    SrcCols<BF16, BN, float, VW> sq{w, nullptr, n_out, n_out, n_out, r_end, col0, {}};
-    Acc<BM, BN> acc;
-    run_tile<BF16>(acc, sp, sq, r_beg, r_end, lds, [](const auto &, int64_t, bool) {});
-    const int tile = blockIdx.y * gridDim.x + blockIdx.x;
-    if (!reduce_splits(acc, part, tickets, tile, gridDim.x * gridDim.y, gridDim.z, blockIdx.z)) return;
-    store_tile(acc, lds, out, n_out, row0, col0, M, n_out, [&](int64_t n, float v) {
-        float z = v + (bias ? bias[n] : 0.f);
-        if (relu && !(z > 0.f)) z = 0.f;
-        return z;
+    SrcRows<BF16, TILE, TA, VA, D> sp{a_self, a_nbr, k_each, k_each, M, K, row0, {}};
+    SrcCols<BF16, TILE, float, VW, D> sq{w, nullptr, n_out, n_out, n_out, r_end, col0, {}};
+    Acc<TILE, TILE> acc;
+    run_tile<BF16, D>(acc, sp, sq, r_beg, r_end, lds, [](const auto &, int, int64_t, bool) {});
+    const int64_t gc = col0 + TileOut<TILE, TILE>::col();
+    if (gridDim.z > 1) {
+        const int64_t ldp = part_ld(n_out);
+        float *pp = part + static_cast<int64_t>(blockIdx.z) * cap_m * ldp;
+        emit_tile(acc, lds, [&](int, int r, int, float4 v) {
+            const int64_t gr = row0 + r;
+            if (gr < M && gc < ldp) *reinterpret_cast<float4 *>(pp + gr * ldp + gc) = v;
+        });
+        return;
+    }
+    const float4 b4 = bias ? load4_clamped<VO>(bias, 0, gc, n_out) : make_float4(0.f, 0.f, 0.f, 0.f);
+    emit_tile(acc, lds, [&](int, int r, int, float4 v) {
+        const int64_t gr = row0 + r;
+        if (gr < M) store4_masked<VO>(out, gr * n_out, gc, n_out, bias_act(v, b4, relu));
     });
+}
+
+// out[r] = act(sum over splits of part[s][r] + b) for the rows below M.
+template <class TO, bool VO>
+__global__ void __launch_bounds__(256) fwd_reduce_kernel(const float *__restrict__ part, int nsplit,
+                                                         const int64_t *m_dev, int64_t cap_m, int64_t n_out,
+                                                         const float *__restrict__ bias, int relu,
+                                                         TO *__restrict__ out) {
+    const int64_t M = m_dev ? min(*m_dev, cap_m) : cap_m;
+    const int64_t ldp = part_ld(n_out), chunks = ldp / 4;
+    for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < M * chunks;
+         t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t r = t / chunks, c = (t % chunks) * 4;
+        const float4 b4 = bias ? load4_clamped<VO>(bias, 0, c, n_out) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 s = sum_splits(part + r * ldp + c, cap_m * ldp, nsplit);
+        store4_masked<VO>(out, r * n_out, c, n_out, bias_act(s, b4, relu));
+    }
+}
+
+struct FwdPlan {
+    int tile, nsplit;
+    TileMap map;
+};
+
+FwdPlan plan_fwd(int64_t cap_m, int64_t n_out, int64_t K, bool bf16) {
+    FwdPlan p;
+    p.tile = pick_tile(cap_m, n_out);
+    p.map = TileMap{ceil_div(std::max<int64_t>(cap_m, 1), p.tile), ceil_div(n_out, p.tile)};
+    const int64_t tiles = p.map.mt * p.map.nt;
+    const int64_t nch = ceil_div(K, bk_of(bf16));
+    // split only long reductions over few tiles, at least 8 chunks a split
+    int64_t s = 1;
+    if (tiles < 128 && nch >= 16) s = std::min<int64_t>({nch / 8, ceil_div(256, tiles), 16});
+    p.nsplit = static_cast<int>(s);
+    return p;
+}
+
+size_t part_bytes(const FwdPlan &p, int64_t cap_m, int64_t n_out) {
+    return p.nsplit > 1 ? static_cast<size_t>(p.nsplit) * cap_m * part_ld(n_out) * 4 : 0;
 }
 
 }  // namespace
 
-using gemm::kTicketBytes;
-
 size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt) {
-    const Plan p = plan_fwd(cap_m, n_out, k, gemm_dt == GNN_BF16);
-    return kTicketBytes + round_up(part_bytes(p), 256);
+    const FwdPlan p = plan_fwd(cap_m, n_out, k, gemm_dt == GNN_BF16);
+    return round_up(part_bytes(p, cap_m, n_out), 256);
 }
 
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
@@ -55,26 +104,32 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
     if (cap_m == 0 || n_out == 0) return GNN_OK;
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
-    Plan p = plan_fwd(cap_m, n_out, K, bf);
-    if (ws == nullptr) {
-        p.nsplit = 1;
-        p.grid.z = 1;
-    }
-    int *tickets = static_cast<int *>(ws);
-    float *part = ws ? reinterpret_cast<float *>(static_cast<char *>(ws) + kTicketBytes) : nullptr;
-    const size_t asz = dtype_size(adt);
+    FwdPlan p = plan_fwd(cap_m, n_out, K, bf);
+    if (ws == nullptr) p.nsplit = 1;
+    GNN_CHECK(p.map.blocks() <= kMaxGrid, GNN_ESIZE, "update_fwd: cap_m exceeds the grid limit");
+    float *part = static_cast<float *>(ws);
+    const dim3 grid(static_cast<unsigned>(p.map.blocks()), 1, static_cast<unsigned>(p.nsplit));
+    const size_t asz = dtype_size(adt), osz = dtype_size(odt);
     const bool vec_a = (k_each % 4 == 0) && aligned(a_self, 4 * asz) && (!a_nbr || aligned(a_nbr, 4 * asz));
     const bool vec_w = (n_out % 4 == 0) && aligned(w, 16);
+    const bool vec_o = (n_out % 4 == 0) && aligned(out, 4 * osz) && aligned(bias, 16);
 #define FWD(BFV, T, TA, TO, VA, VW)                                                                                 \
-    update_fwd_kernel<BFV, T, T, TA, TO, VA, VW><<<p.grid, kThreads, 0, s>>>(                                      \
-        static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, m_dev, cap_m, w, bias, n_out, relu, \
-        static_cast<TO *>(out), part, tickets)
-#define FWD_V(BFV, T, TA, TO)                              \
-    do {                                                   \
-        if (vec_a && vec_w) FWD(BFV, T, TA, TO, true, true);      \
-        else if (vec_a) FWD(BFV, T, TA, TO, true, false);         \
-        else if (vec_w) FWD(BFV, T, TA, TO, false, true);         \
-        else FWD(BFV, T, TA, TO, false, false);                   \
+    do {                                                                                                            \
+        if (vec_o)                                                                                                  \
+            update_fwd_kernel<BFV, T, TA, TO, VA, VW, true><<<grid, kThreads, 0, s>>>(                             \
+                static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, m_dev, cap_m, w, bias,     \
+                n_out, relu, static_cast<TO *>(out), part, p.map);                                                  \
+        else                                                                                                        \
+            update_fwd_kernel<BFV, T, TA, TO, VA, VW, false><<<grid, kThreads, 0, s>>>(                            \
+                static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, m_dev, cap_m, w, bias,     \
+                n_out, relu, static_cast<TO *>(out), part, p.map);                                                  \
+    } while (0)
+#define FWD_V(BFV, T, TA, TO)                                  \
+    do {                                                       \
+        if (vec_a && vec_w) FWD(BFV, T, TA, TO, true, true);   \
+        else if (vec_a) FWD(BFV, T, TA, TO, true, false);      \
+        else if (vec_w) FWD(BFV, T, TA, TO, false, true);      \
+        else FWD(BFV, T, TA, TO, false, false);                \
     } while (0)
 #define FWD_T(BFV, TA, TO)            \
     do {                              \
@@ -98,6 +153,26 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
 #undef FWD_V
 #undef FWD
     GNN_LAUNCHED("update_fwd");
+    if (p.nsplit > 1) {
+        const int64_t work = cap_m * (part_ld(n_out) / 4);
+        const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>(ceil_div(work, 256), 1 << 20));
+        if (odt == GNN_BF16) {
+            if (vec_o)
+                fwd_reduce_kernel<uint16_t, true><<<rgrid, 256, 0, s>>>(part, p.nsplit, m_dev, cap_m, n_out, bias,
+                                                                         relu, static_cast<uint16_t *>(out));
+            else
+                fwd_reduce_kernel<uint16_t, false><<<rgrid, 256, 0, s>>>(part, p.nsplit, m_dev, cap_m, n_out, bias,
+                                                                          relu, static_cast<uint16_t *>(out));
+        } else {
+            if (vec_o)
+                fwd_reduce_kernel<float, true><<<rgrid, 256, 0, s>>>(part, p.nsplit, m_dev, cap_m, n_out, bias, relu,
+                                                                      static_cast<float *>(out));
+            else
+                fwd_reduce_kernel<float, false><<<rgrid, 256, 0, s>>>(part, p.nsplit, m_dev, cap_m, n_out, bias,
+                                                                       relu, static_cast<float *>(out));
+        }
+        GNN_LAUNCHED("update_fwd_reduce");
+    }
     return GNN_OK;
 }
 

@@ -148,9 +148,9 @@ gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int
                                 hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
                                 int hbdt, float *d_src, hipStream_t s);
-// Update GEMMs.  Their workspaces start with per-tile integer tickets that
-// must be zero before the first use; every call leaves them zero.  A null
-// forward workspace disables the reduction split.
+// Update GEMMs.  Their workspaces hold fp32 partial tiles of split
+// reductions (no state survives a call).  A null forward workspace disables
+// the reduction split.
 size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt);
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
                              int64_t cap_m, const float *w, const float *bias, int64_t n_out, int relu, int gemm_dt,

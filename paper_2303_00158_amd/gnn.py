@@ -251,8 +251,8 @@ def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Ten
                out: torch.Tensor, relu: bool, gemm_dtype: int, m_dev: Optional[torch.Tensor] = None,
                cap_m: Optional[int] = None, ws: Optional[torch.Tensor] = None, split: bool = True,
                stream=None) -> torch.Tensor:
-    """ws: zero-filled workspace reused across calls (allocated when None and
-    split is True); split=False runs without a workspace (no reduction split)."""
+    """ws: workspace for split reductions (allocated when None and split is
+    True); split=False runs without a workspace (no reduction split)."""
     cap = a_self.shape[0] if cap_m is None else cap_m
     K = a_self.shape[1] * (2 if a_nbr is not None else 1)
     if ws is None and split:

@@ -305,31 +305,35 @@ def test_update_fwd_parity(m, ke, n, sage, code):
         assert err <= (1e-5 if code == oracle.F32 else 8e-3), (relu, err)
 
 
-def test_update_fwd_split_workspace_is_reusable():
-    # the split reduction keeps per-tile tickets in the workspace; a second
-    # call on the same workspace (smaller rows, other data) must be exact too
+@pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
+def test_update_fwd_split_reduction_and_workspace_reuse(code):
+    # a long reduction over few output tiles is split across workgroups and
+    # finished by a second kernel; a second call on the same workspace
+    # (fewer rows, other data) must be as exact as the first
     rng = np.random.default_rng(7)
-    ke, n = 256, 47
-    w = (rng.standard_normal((2 * ke, n)) / 16).astype(np.float32)
-    ws = None
+    ke, n, cap = 1024, 153, 1024
+    K = 2 * ke
+    nb = gnn._sz()
+    gnn._check(gnn.lib().gnn_update_fwd_workspace_size(K, n, cap, code, gnn.ctypes.byref(nb)))
+    assert nb.value > 0  # this shape takes the split path
+    ws = torch.full((nb.value,), 0xFF, dtype=torch.uint8, device=DEV)  # no zero-fill needed
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    b = rng.standard_normal(n).astype(np.float32)
+    tdt = torch.bfloat16 if code == oracle.BF16 else torch.float32
     for m in (1024, 333):
-        a_s = _act(rng, m, ke, oracle.BF16)
-        a_n = _act(rng, m, ke, oracle.BF16)
-        want = oracle.update_fwd(a_s, a_n, w, None, False, oracle.BF16, oracle.F32)
-        if ws is None:
-            nb = gnn._sz()
-            gnn._check(gnn.lib().gnn_update_fwd_workspace_size(2 * ke, n, 1024, gnn.GNN_BF16, gnn.ctypes.byref(nb)))
-            ws = torch.zeros(nb.value, dtype=torch.uint8, device=DEV)
-        out = torch.empty((1024, n), dtype=torch.float32, device=DEV)
+        a_s = _act(rng, m, ke, code)
+        a_n = _act(rng, m, ke, code)
+        want = oracle.update_fwd(a_s, a_n, w, b, True, code, code)
+        out = torch.full((cap, n), 3.0, dtype=tdt, device=DEV)
         m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
-        a_s_d = torch.zeros((1024, ke), dtype=torch.bfloat16, device=DEV)
-        a_n_d = torch.zeros((1024, ke), dtype=torch.bfloat16, device=DEV)
+        a_s_d = torch.zeros((cap, ke), dtype=tdt, device=DEV)
+        a_n_d = torch.zeros((cap, ke), dtype=tdt, device=DEV)
         a_s_d[:m] = from_np_act(a_s)
         a_n_d[:m] = from_np_act(a_n)
-        gnn.update_fwd(a_s_d, a_n_d, from_np_act(w), None, out, False, gnn.GNN_BF16, m_dev=m_dev, cap_m=1024, ws=ws)
-        assert relerr(out[:m].cpu().numpy(), want) <= 8e-3
-    torch.cuda.synchronize()
-    assert int(ws[:32768].view(torch.int32).abs().sum().item()) == 0  # tickets left at zero
+        gnn.update_fwd(a_s_d, a_n_d, from_np_act(w), from_np_act(b), out, True, code, m_dev=m_dev, cap_m=cap, ws=ws)
+        got = oracle.to_float64(to_np_act(out))
+        assert relerr(got[:m], oracle.to_float64(want)) <= (1e-5 if code == oracle.F32 else 8e-3)
+        assert np.all(got[m:] == 3.0)  # rows past the device count untouched
 
 
 def test_update_workspaces_shared_across_shapes():
