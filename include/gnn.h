@@ -118,10 +118,11 @@ typedef struct gnn_block {
  *   cap_nnz = cap_dst * fanout, cap_src = min(cap_dst + cap_nnz, graph_n). */
 gnn_status gnn_block_bounds(int64_t graph_n, int64_t cap_dst, int32_t fanout, int64_t *cap_src, int64_t *cap_nnz);
 
-/* Workspace of gnn_build_block.  It holds a per-vertex map and bitmap that
- * must be initialised once with gnn_sampler_workspace_init; every
- * gnn_build_block call leaves them in that initial state again.  One
- * workspace serves any number of sequential calls on one stream. */
+/* Workspace of gnn_build_block.  It holds a per-vertex map and two
+ * per-vertex bitmaps; the bitmaps must be zeroed once with
+ * gnn_sampler_workspace_init and every gnn_build_block call leaves them zero
+ * again.  One workspace serves any number of sequential calls on one
+ * stream (calls that share it must not overlap). */
 gnn_status gnn_sampler_workspace_size(int64_t graph_n, int64_t cap_dst, int32_t fanout, size_t *bytes);
 gnn_status gnn_sampler_workspace_init(void *ws, size_t ws_bytes, int64_t graph_n, gnn_stream s);
 
@@ -269,6 +270,7 @@ typedef struct gnn_step_layout {
     size_t blk_counts[GNN_MAX_LAYERS], blk_src_ids[GNN_MAX_LAYERS], blk_rowptr[GNN_MAX_LAYERS],
         blk_col[GNN_MAX_LAYERS], blk_cscptr[GNN_MAX_LAYERS], blk_cscrow[GNN_MAX_LAYERS],
         blk_src_norm[GNN_MAX_LAYERS]; /* per hop; 0 when absent */
+    size_t blk_csc_ws[GNN_MAX_LAYERS]; /* per hop with a transpose: its scratch; else 0 */
     size_t x0;                          /* gathered X' (cap_src of hop L rows) */
     size_t agg[GNN_MAX_LAYERS + 1];     /* per layer l: aggregation output */
     size_t h[GNN_MAX_LAYERS + 1];       /* per layer l: H^l (l < L) or logits (l = L) */

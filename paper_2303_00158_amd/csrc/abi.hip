@@ -179,8 +179,10 @@ gnn_status gnn_build_block(const gnn_graph *g, const float *gcn_norm, const int6
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
     const size_t need = sampler_ws_bytes(g->n, out->cap_dst, fanout);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
-    return launch_build_block(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, want_csc != 0, out, ws,
-                              false, stream_of(s));
+    void *csc_ws = want_csc ? sampler_csc_ws(ws, g->n, out->cap_dst, fanout) : nullptr;
+    GNN_TRY(launch_build_block(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, out, ws, csc_ws,
+                               stream_of(s)));
+    return want_csc ? launch_block_csc(out, csc_ws, out->cap_dst * fanout, stream_of(s)) : GNN_OK;
 }
 
 gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, int64_t n_rows, int64_t dim,
@@ -203,7 +205,7 @@ gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, in
     GNN_CHECK(aligned(table, dtype_size(tdt)) && aligned(out, dtype_size(odt)), GNN_EINVAL, "%s: misaligned data", who);
     const void *t = nullptr;
     GNN_TRY(device_view(table, loc, &t, who));
-    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, nullptr, stream_of(s));
+    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, stream_of(s));
 }
 
 gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,

@@ -22,7 +22,7 @@ template <class T>
 __global__ void __launch_bounds__(kThreads) gather_copy4_kernel(const T *__restrict__ table, int64_t row_stride,
                                                                  const int64_t *__restrict__ ids,
                                                                  const int64_t *n_dev, int64_t cap, int64_t dim,
-                                                                 T *__restrict__ out, int32_t *reset_map) {
+                                                                 T *__restrict__ out) {
     using R = typename Raw4<T>::type;
     const int64_t n = n_dev ? min(*n_dev, cap) : cap;
     const int64_t chunks = dim >> 2;
@@ -34,7 +34,6 @@ __global__ void __launch_bounds__(kThreads) gather_copy4_kernel(const T *__restr
         const int64_t src = ids[r];
         const R v = *reinterpret_cast<const R *>(table + src * row_stride + c * 4);
         *reinterpret_cast<R *>(out + r * dim + c * 4) = v;
-        if (reset_map && c == 0) reset_map[src] = -1;
     }
 }
 
@@ -51,7 +50,7 @@ __global__ void __launch_bounds__(kThreads) gather_convert4_kernel(const void *_
                                                                     int64_t row_stride,
                                                                     const int64_t *__restrict__ ids,
                                                                     const int64_t *n_dev, int64_t cap, int64_t dim,
-                                                                    TOut *__restrict__ out, int32_t *reset_map) {
+                                                                    TOut *__restrict__ out) {
     const int64_t n = n_dev ? min(*n_dev, cap) : cap;
     const int64_t chunks = dim >> 2;
     const int64_t total = n * chunks;
@@ -61,7 +60,6 @@ __global__ void __launch_bounds__(kThreads) gather_convert4_kernel(const void *_
         const int64_t c = t - r * chunks;
         const int64_t src = ids[r];
         const int64_t off = src * row_stride + c * 4;
-        if (reset_map && c == 0) reset_map[src] = -1;
         float4 v;
         if constexpr (SRC_F16)
             v = load4_f16(static_cast<const uint16_t *>(table) + off);
@@ -76,7 +74,7 @@ template <int TDT, int ODT>
 __global__ void __launch_bounds__(kThreads) gather_scalar_kernel(const void *__restrict__ table, int64_t row_stride,
                                                                   const int64_t *__restrict__ ids,
                                                                   const int64_t *n_dev, int64_t cap, int64_t dim,
-                                                                  void *__restrict__ out, int32_t *reset_map) {
+                                                                  void *__restrict__ out) {
     const int64_t n = n_dev ? min(*n_dev, cap) : cap;
     const int64_t total = n * dim;
     for (int64_t t = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; t < total;
@@ -84,7 +82,6 @@ __global__ void __launch_bounds__(kThreads) gather_scalar_kernel(const void *__r
         const int64_t r = t / dim;
         const int64_t c = t - r * dim;
         const int64_t off = ids[r] * row_stride + c;
-        if (reset_map && c == 0) reset_map[ids[r]] = -1;
         if constexpr (TDT == ODT) {
             if constexpr (TDT == GNN_F32)
                 static_cast<uint32_t *>(out)[t] = static_cast<const uint32_t *>(table)[off];
@@ -113,8 +110,7 @@ unsigned gather_grid(int64_t work) {
 }  // namespace
 
 gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,
-                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, int32_t *reset_map,
-                         hipStream_t s) {
+                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, hipStream_t s) {
     if (cap_ids == 0 || dim == 0) return GNN_OK;
     const size_t tsz = dtype_size(tdt), osz = dtype_size(odt);
     const bool vec = (dim % 4 == 0) && (row_stride % 4 == 0) && aligned(table, 4 * tsz) && aligned(out, 4 * osz);
@@ -122,44 +118,44 @@ gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_st
         const unsigned grid = gather_grid(cap_ids * (dim / 4));
         if (tdt == odt && tdt == GNN_F32)
             gather_copy4_kernel<float><<<grid, kThreads, 0, s>>>(static_cast<const float *>(table), row_stride, ids,
-                                                                 n_ids_dev, cap_ids, dim, static_cast<float *>(out), reset_map);
+                                                                 n_ids_dev, cap_ids, dim, static_cast<float *>(out));
         else if (tdt == odt)
             gather_copy4_kernel<uint16_t><<<grid, kThreads, 0, s>>>(static_cast<const uint16_t *>(table), row_stride,
                                                                     ids, n_ids_dev, cap_ids, dim,
-                                                                    static_cast<uint16_t *>(out), reset_map);
+                                                                    static_cast<uint16_t *>(out));
         else if (tdt == GNN_F32 && odt == GNN_BF16)
             gather_convert4_kernel<false, uint16_t><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
                                                                               cap_ids, dim,
-                                                                              static_cast<uint16_t *>(out), reset_map);
+                                                                              static_cast<uint16_t *>(out));
         else if (tdt == GNN_F16 && odt == GNN_BF16)
             gather_convert4_kernel<true, uint16_t><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
                                                                              cap_ids, dim,
-                                                                             static_cast<uint16_t *>(out), reset_map);
+                                                                             static_cast<uint16_t *>(out));
         else if (tdt == GNN_F16 && odt == GNN_F32)
             gather_convert4_kernel<true, float><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev, cap_ids,
-                                                                          dim, static_cast<float *>(out), reset_map);
+                                                                          dim, static_cast<float *>(out));
         else
             return fail(GNN_EUNSUPPORTED, "gather: unsupported dtype pair %d -> %d", tdt, odt);
     } else {
         const unsigned grid = gather_grid(cap_ids * dim);
         if (tdt == GNN_F32 && odt == GNN_F32)
             gather_scalar_kernel<GNN_F32, GNN_F32><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                             cap_ids, dim, out, reset_map);
+                                                                             cap_ids, dim, out);
         else if (tdt == GNN_F32 && odt == GNN_BF16)
             gather_scalar_kernel<GNN_F32, GNN_BF16><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                              cap_ids, dim, out, reset_map);
+                                                                              cap_ids, dim, out);
         else if (tdt == GNN_F16 && odt == GNN_F16)
             gather_scalar_kernel<GNN_F16, GNN_F16><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                             cap_ids, dim, out, reset_map);
+                                                                             cap_ids, dim, out);
         else if (tdt == GNN_BF16 && odt == GNN_BF16)
             gather_scalar_kernel<GNN_BF16, GNN_BF16><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                               cap_ids, dim, out, reset_map);
+                                                                               cap_ids, dim, out);
         else if (tdt == GNN_F16 && odt == GNN_F32)
             gather_scalar_kernel<GNN_F16, GNN_F32><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                             cap_ids, dim, out, reset_map);
+                                                                             cap_ids, dim, out);
         else if (tdt == GNN_F16 && odt == GNN_BF16)
             gather_scalar_kernel<GNN_F16, GNN_BF16><<<grid, kThreads, 0, s>>>(table, row_stride, ids, n_ids_dev,
-                                                                              cap_ids, dim, out, reset_map);
+                                                                              cap_ids, dim, out);
         else
             return fail(GNN_EUNSUPPORTED, "gather: unsupported dtype pair %d -> %d", tdt, odt);
     }

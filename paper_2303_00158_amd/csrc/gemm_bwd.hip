@@ -44,27 +44,28 @@ __global__ void __launch_bounds__(kThreads) update_dinput_kernel(const float *__
 // ---------------------------------------------------------------------------
 // weight gradient partials: part[split][k][n] = sum over this split's rows
 // of A[row][k] g[row][n]; part[split][K][n] = sum of g[row][n] (db).
-// The tile map runs over (n_out tiles, K tiles) so that the workgroups of
-// one XCD share the g rows of one column block.
 // ---------------------------------------------------------------------------
 template <bool BF16, int TILE, class TA, bool VA, bool VG>
 __global__ void __launch_bounds__(kThreads) update_dweight_kernel(const TA *__restrict__ a_self,
                                                                    const TA *__restrict__ a_nbr, int64_t k_each,
                                                                    const float *__restrict__ g, const int64_t *m_dev,
                                                                    int64_t cap_m, int64_t n_out, int want_db,
-                                                                   float *__restrict__ part, TileMap map) {
+                                                                   float *__restrict__ part, SplitMap map,
+                                                                   int64_t k_tiles) {
     constexpr int D = depth<TILE>();
     using SQ = SrcCols<BF16, TILE, float, VG, D>;
     __shared__ __attribute__((aligned(16))) char lds[lds_bytes<TILE, TILE>()];
     __shared__ float cs[SQ::RPP][TILE];
-    int64_t tn, tk;
-    map.tile_of(blockIdx.x, &tn, &tk);
-    if (tn >= map.mt) return;
+    int split;
+    int64_t tile;
+    map.of(blockIdx.x, &split, &tile);
+    if (split >= map.nsplit) return;
+    const int64_t tk = tile % k_tiles, tn = tile / k_tiles;
     const int64_t M = m_dev ? min(*m_dev, cap_m) : cap_m;
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const int64_t row0 = tk * TILE;  // over K
     const int64_t col0 = tn * TILE;  // over n_out
-    const int nsplit = gridDim.z, split = blockIdx.z;
+    const int nsplit = map.nsplit;
     int64_t r_beg, r_end;
     split_range<Cfg<BF16>::BK>(M, nsplit, split, &r_beg, &r_end);
     SrcCols<BF16, TILE, TA, VA, D> sp{a_self, a_nbr, k_each, k_each, K, r_end, row0, {}};
@@ -125,16 +126,18 @@ __global__ void __launch_bounds__(256) dw_reduce_kernel(const float *__restrict_
 
 struct DwPlan {
     int tile, nsplit;
-    TileMap map;  // over (n_out tiles, K tiles)
+    int64_t k_tiles;
+    SplitMap map;
 };
 
 DwPlan plan_dw(int64_t K, int64_t n_out, int64_t cap_m, bool bf16) {
     DwPlan p;
     p.tile = pick_tile(K, n_out);
-    p.map = TileMap{ceil_div(n_out, p.tile), ceil_div(K, p.tile)};
-    const int64_t tiles = p.map.mt * p.map.nt;
+    p.k_tiles = ceil_div(K, p.tile);
+    const int64_t tiles = p.k_tiles * ceil_div(n_out, p.tile);
     const int64_t nch = std::max<int64_t>(ceil_div(cap_m, bk_of(bf16)), 1);
     p.nsplit = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({ceil_div(512, tiles), 64, nch})));
+    p.map = SplitMap{tiles, p.nsplit};
     return p;
 }
 
@@ -195,12 +198,13 @@ gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int
 #undef DA
         GNN_LAUNCHED("update_dinput");
     }
-    const dim3 grid(static_cast<unsigned>(pw.map.blocks()), 1, static_cast<unsigned>(pw.nsplit));
+    GNN_CHECK(pw.map.blocks() <= kMaxGrid, GNN_ESIZE, "update_bwd: too many weight-gradient tiles");
+    const dim3 grid(static_cast<unsigned>(pw.map.blocks()));
     const int want_db = db != nullptr;
 #define DW(BFV, T, TA, VA, VG)                                                                                  \
     update_dweight_kernel<BFV, T, TA, VA, VG><<<grid, kThreads, 0, s>>>(                                       \
         static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, g, m_dev, cap_m, n_out, want_db, \
-        part, pw.map)
+        part, pw.map, pw.k_tiles)
 #define DW_V(BFV, T, TA)                              \
     do {                                              \
         if (vec_a && vec_g) DW(BFV, T, TA, true, true);      \

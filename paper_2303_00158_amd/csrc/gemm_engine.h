@@ -43,14 +43,23 @@ constexpr int kThreads = 256;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Staged tiles in LDS: row r (a tile row), reduction index k.  bf16 rows
+// are unpadded and their 16-byte granules (8 elements) are XOR-swizzled by
+// bits 2..3 of the row.  That spreads over all banks both the MFMA operand
+// reads (16 rows x one granule) and the transposing commits of SrcCols
+// (4 consecutive rows x half a granule per thread).  fp32 rows are padded.
 template <bool BF16> struct Cfg;
 template <> struct Cfg<true> {
     using T = uint16_t;
-    static constexpr int BK = 64, LDK = BK + 8;
+    static constexpr int BK = 64, LDK = BK;
+    __device__ __forceinline__ static int idx(int r, int k) {
+        return r * LDK + ((((k >> 3) ^ (((r >> 2) & 3) << 1)) << 3) | (k & 7));
+    }
 };
 template <> struct Cfg<false> {
     using T = float;
     static constexpr int BK = 32, LDK = BK + 4;
+    __device__ __forceinline__ static int idx(int r, int k) { return r * LDK + k; }
 };
 
 // A chunk of four source elements kept in its storage form until commit:
@@ -145,7 +154,7 @@ struct SrcRows {
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int q = threadIdx.x + i * kThreads;
-            typename CV::T *p = lds + (q / CPR) * CV::LDK + (q % CPR) * 4;
+            typename CV::T *p = lds + CV::idx(q / CPR, (q % CPR) * 4);
             if constexpr (BF16)
                 *reinterpret_cast<uint2 *>(p) = Raw<TX>::to_bf16(reg[s][i]);
             else
@@ -201,7 +210,7 @@ struct SrcCols {
                 const int kk = my_r(4 * g);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    typename CV::T *p = lds + (tt + e) * CV::LDK + kk;
+                    typename CV::T *p = lds + CV::idx(tt + e, kk);
                     if constexpr (BF16) {
                         const uint2 v = make_uint2(
                             Raw<TY>::bits(reg[s][4 * g + 0], e) | (Raw<TY>::bits(reg[s][4 * g + 1], e) << 16),
@@ -223,9 +232,9 @@ struct SrcCols {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     if constexpr (BF16)
-                        lds[(tt + e) * CV::LDK + kk] = static_cast<uint16_t>(Raw<TY>::bits(reg[s][i], e));
+                        lds[CV::idx(tt + e, kk)] = static_cast<uint16_t>(Raw<TY>::bits(reg[s][i], e));
                     else
-                        lds[(tt + e) * CV::LDK + kk] = Raw<TY>::elem(reg[s][i], e);
+                        lds[CV::idx(tt + e, kk)] = Raw<TY>::elem(reg[s][i], e);
                 }
             }
         }
@@ -269,16 +278,17 @@ __device__ __forceinline__ void mma_chunk(Acc<BM, BN> &acc, const typename Cfg<B
     constexpr int WI = Acc<BM, BN>::WI, WJ = Acc<BM, BN>::WJ;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lr = lane & 15, lg = lane >> 4;
-    const typename CV::T *pa = Ps + ((wave >> 1) * (BM / 2) + lr) * CV::LDK;
-    const typename CV::T *pb = Qs + ((wave & 1) * (BN / 2) + lr) * CV::LDK;
+    const int ra = (wave >> 1) * (BM / 2) + lr, rb = (wave & 1) * (BN / 2) + lr;
     if constexpr (BF16) {
 #pragma unroll
         for (int kk = 0; kk < CV::BK; kk += 32) {
             bf16x8 a[WI], b[WJ];
 #pragma unroll
-            for (int i = 0; i < WI; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(pa + i * 16 * CV::LDK + kk + lg * 8);
+            for (int i = 0; i < WI; ++i)
+                a[i] = *reinterpret_cast<const bf16x8 *>(Ps + CV::idx(ra + i * 16, kk + lg * 8));
 #pragma unroll
-            for (int j = 0; j < WJ; ++j) b[j] = *reinterpret_cast<const bf16x8 *>(pb + j * 16 * CV::LDK + kk + lg * 8);
+            for (int j = 0; j < WJ; ++j)
+                b[j] = *reinterpret_cast<const bf16x8 *>(Qs + CV::idx(rb + j * 16, kk + lg * 8));
 #pragma unroll
             for (int i = 0; i < WI; ++i)
 #pragma unroll
@@ -290,9 +300,9 @@ __device__ __forceinline__ void mma_chunk(Acc<BM, BN> &acc, const typename Cfg<B
         for (int kk = 0; kk < CV::BK; kk += 4) {
             float a[WI], b[WJ];
 #pragma unroll
-            for (int i = 0; i < WI; ++i) a[i] = pa[i * 16 * CV::LDK + kk + lg];
+            for (int i = 0; i < WI; ++i) a[i] = Ps[CV::idx(ra + i * 16, kk + lg)];
 #pragma unroll
-            for (int j = 0; j < WJ; ++j) b[j] = pb[j * 16 * CV::LDK + kk + lg];
+            for (int j = 0; j < WJ; ++j) b[j] = Qs[CV::idx(rb + j * 16, kk + lg)];
 #pragma unroll
             for (int i = 0; i < WI; ++i)
 #pragma unroll
@@ -305,7 +315,7 @@ __device__ __forceinline__ void mma_chunk(Acc<BM, BN> &acc, const typename Cfg<B
 // LDS for the operand tiles, reused as the epilogue staging area.
 template <int BM, int BN>
 constexpr int lds_bytes() {
-    constexpr int ops = (BM + BN) * 72 * 2;  // bf16 [*][72] and fp32 [*][36] take the same bytes
+    constexpr int ops = (BM + BN) * 36 * 4;  // fp32 [*][36]; bf16 [*][64] takes less
     constexpr int stage = (BM / 2) * (BN + 4) * 4;
     return ops > stage ? ops : stage;
 }
@@ -317,7 +327,10 @@ __device__ __forceinline__ void zero_tail(typename Cfg<BF16>::T *Ps, typename Cf
     const int w = CV::BK - valid;
     for (int q = threadIdx.x; q < (BM + BN) * w; q += kThreads) {
         const int row = q / w, col = valid + q % w;
-        (row < BM ? Ps + row * CV::LDK : Qs + (row - BM) * CV::LDK)[col] = typename CV::T(0);
+        if (row < BM)
+            Ps[CV::idx(row, col)] = typename CV::T(0);
+        else
+            Qs[CV::idx(row - BM, col)] = typename CV::T(0);
     }
 }
 
@@ -466,19 +479,40 @@ inline int pick_tile(int64_t rows, int64_t cols) {
 template <int TILE> constexpr int depth() { return TILE == 64 ? 3 : 2; }
 
 // Workgroup -> output tile mapping.  Workgroups are dealt round-robin to
-// the 8 XCDs (each with its own L2); consecutive workgroups of one XCD take
-// the column tiles of one row block, so the row block's operand rows are
-// fetched into that XCD's L2 once.
+// the 8 XCDs (each with its own L2).  With at least 8 row tiles,
+// consecutive workgroups of one XCD take the column tiles of one row block,
+// so the row block's operand rows are fetched into that XCD's L2 once
+// (row tiles past mt in the last group have nothing to do).  With fewer
+// row tiles the tiles are dealt row-major so that every XCD gets work.
 constexpr int kXcds = 8;
 struct TileMap {
     int64_t mt, nt;  // row and column tiles
-    __host__ __device__ int64_t groups() const { return ceil_div(mt, kXcds); }
-    __host__ __device__ int64_t blocks() const { return groups() * kXcds * nt; }
+    __host__ __device__ bool grouped() const { return mt >= kXcds; }
+    __host__ __device__ int64_t blocks() const { return grouped() ? ceil_div(mt, kXcds) * kXcds * nt : mt * nt; }
     __device__ void tile_of(int64_t b, int64_t *x, int64_t *y) const {
+        if (!grouped()) {
+            *x = b % mt;
+            *y = b / mt;
+            return;
+        }
         const int64_t per_group = kXcds * nt;
         const int64_t g = b / per_group, j = b % per_group;
         *x = g * kXcds + j % kXcds;
         *y = j / kXcds;
+    }
+};
+
+// Workgroup -> (split, tile) for reductions split over rows (dW): all tiles
+// of one split run on one XCD, where they share the split's operand rows,
+// and consecutive splits go to consecutive XCDs.  nsplit is padded to a
+// multiple of 8; workgroups of padding splits have nothing to do.
+struct SplitMap {
+    int64_t tiles;  // output tiles
+    int nsplit;
+    __host__ __device__ int64_t blocks() const { return ceil_div(nsplit, kXcds) * kXcds * tiles; }
+    __device__ void of(int64_t b, int *split, int64_t *tile) const {
+        *split = static_cast<int>((b / (kXcds * tiles)) * kXcds + b % kXcds);
+        *tile = (b / kXcds) % tiles;
     }
 };
 

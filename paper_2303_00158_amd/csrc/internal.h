@@ -138,12 +138,8 @@ gnn_status radix_sort_pairs(const int32_t *keys_in, const int32_t *vals_in, int3
 gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const char *who);
 
 // Internal launchers reused by the training step (no host validation).
-// reset_map (may be null): the sampler's vertex map; the gather sets
-// reset_map[ids[r]] = -1 for every row it copies (the training step defers
-// the sampler's map reset to this kernel).
 gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,
-                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, int32_t *reset_map,
-                         hipStream_t s);
+                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, hipStream_t s);
 gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
                                 hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
@@ -167,11 +163,16 @@ gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const in
 gnn_status launch_sgd(float *w, const float *dw, int64_t n, float lr, hipStream_t s);
 size_t sampler_ws_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout);
 gnn_status launch_sampler_ws_init(void *ws, int64_t graph_n, hipStream_t s);
-// defer_reset: leave the vertex map set for the block's sources (the next
-// hop of the same step, or the gather, consumes and resets it).
+// Builds the block's CSR part (ids, row pointer, columns, norms).  csc_ws
+// (may be null) receives the row of every edge for a later
+// launch_block_csc with the same csc_ws, of block_csc_ws_bytes(scratch_nnz)
+// bytes for a scratch_nnz of at least cap_dst * fanout.
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              bool want_csc, const gnn_block *out, void *ws, bool defer_reset, hipStream_t s);
-int32_t *sampler_map(void *ws);
+                              const gnn_block *out, void *ws, void *csc_ws, hipStream_t s);
+size_t block_csc_ws_bytes(int64_t cap_nnz);
+gnn_status launch_block_csc(const gnn_block *out, void *csc_ws, int64_t scratch_nnz, hipStream_t s);
+// The transpose scratch inside a sampler workspace (for standalone calls).
+void *sampler_csc_ws(void *ws, int64_t graph_n, int64_t cap_dst, int32_t fanout);
 
 }  // namespace gnn

@@ -1,29 +1,31 @@
 // Mini-batch sampler: one block (hop) of uniform neighbour sampling without
 // replacement, relabelled to local indices, with its transpose.
 //
-// A hop is four kernels (plus one for the transpose):
+// A hop is three kernels (plus one for the transpose):
 //   1. prepare   one wavefront per destination: map the destination to its
-//                local index, draw its sample (Floyd), write the sampled
-//                neighbour ids to a padded [n_dst][k] staging array.
-//   2. mark      one thread per destination: set the bitmap bit of every
-//                sampled id that is not a destination, and scan the sample
-//                counts into the block's row pointer.
-//   3. emit      walk the bitmap in vertex order: every set bit becomes the
-//                next new source (so new sources come out in ascending id
-//                order), and the bitmap is cleared.
-//   4. relabel   one thread per staged sample: local index via the map.
-//   5. transpose one workgroup: stable radix sort of the edges by source.
-// Steps 2 and 3 are single-pass scans: workgroups take tickets in the order
-// they start and add the prefix of earlier tickets (decoupled look-back),
-// so a workgroup only waits on workgroups that are already running.  Every
-// wait is bounded; a wait that runs out flags counts[3].
+//                local index and mark it in the destination bitmap, draw its
+//                sample (Floyd), write the sampled neighbour ids to a padded
+//                [n_dst][k] staging array and mark them in the sample bitmap.
+//   2. emit      the first workgroups scan the sample counts into the
+//                block's row pointer; the rest walk the bitmaps in vertex
+//                order: every vertex that was sampled and is not a
+//                destination becomes the next new source (so new sources
+//                come out in ascending id order); both bitmaps are cleared.
+//   3. relabel   one thread per staged sample: local index via the map.
+//   4. transpose one workgroup: stable radix sort of the edges by source.
+// The scans in step 2 are single-pass: workgroups take tickets in the order
+// they start and add the prefix of earlier tickets (decoupled look-back,
+// one wavefront reading 64 predecessors at a time), so a workgroup only
+// waits on workgroups that are already running.  Every wait is bounded; a
+// wait that runs out flags counts[3].
 //
 // Device workspace (sampler_ws_bytes):
-//   map  int32[graph_n]  vertex -> local source index, -1 when unused
-//   bits uint32[W]       one bit per vertex: "reached, not a destination"
+//   map   int32[graph_n]   vertex -> local source index (valid only for the
+//                          vertices of the current block)
+//   bits  uint32[W]        one bit per vertex: "sampled"
+//   dbits uint32[W]        one bit per vertex: "destination"
 //   ... per-call scratch
-// map and bits are all -1 / 0 between calls; each call restores that state by
-// resetting exactly the entries it touched.
+// Both bitmaps are all zero between calls; each call clears the words it set.
 #include "internal.h"
 
 namespace gnn {
@@ -59,33 +61,46 @@ __device__ __forceinline__ int64_t take_ticket(int *ticket) {
     return t;
 }
 
-// Called by one thread: publish this workgroup's aggregate, add up the
-// aggregates / prefixes of earlier tickets, publish the inclusive prefix, and
+__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Called by all 64 lanes of one wavefront: publish this workgroup's
+// aggregate, add up the aggregates / prefixes of earlier tickets 64 at a
+// time (lane j reads ticket blk-1-j-64w), publish the inclusive prefix, and
 // return the exclusive prefix.
 __device__ int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, int64_t *err) {
+    const int lane = threadIdx.x & 63;
     if (blk == 0) {
-        store_status(&status[0], kFlagPrefix | static_cast<uint64_t>(agg));
+        if (lane == 0) store_status(&status[0], kFlagPrefix | static_cast<uint64_t>(agg));
         return 0;
     }
-    store_status(&status[blk], kFlagAgg | static_cast<uint64_t>(agg));
+    if (lane == 0) store_status(&status[blk], kFlagAgg | static_cast<uint64_t>(agg));
     int64_t excl = 0;
-    int64_t p = blk - 1;
+    int64_t hi = blk - 1;
     uint32_t spins = 0;
-    while (p >= 0) {
-        const uint64_t s = load_status(&status[p]);
+    while (true) {
+        const int64_t p = hi - lane;
+        // tickets before 0 read as a zero prefix, which ends every walk
+        const uint64_t s = p >= 0 ? load_status(&status[p]) : kFlagPrefix;
         const uint64_t flag = s & ~kValueMask;
-        if (flag == 0) {
+        const uint64_t pre = __ballot(flag == kFlagPrefix);
+        const int first = pre ? static_cast<int>(__builtin_ctzll(pre)) : 63;
+        const uint64_t need = (first == 63) ? ~0ull : ((1ull << (first + 1)) - 1);
+        if (__ballot(flag == 0) & need) {
             if (++spins > kSpinLimit) {
-                *err = 1;  // an earlier workgroup never published: flag it and stop waiting
+                if (lane == 0) *err = 1;  // an earlier workgroup never published: flag it and stop
                 break;
             }
             continue;
         }
-        excl += static_cast<int64_t>(s & kValueMask);
-        if (flag == kFlagPrefix) break;
-        --p;
+        excl += wave_sum64(lane <= first ? static_cast<int64_t>(s & kValueMask) : 0);
+        if (pre) break;
+        hi -= 64;
     }
-    store_status(&status[blk], kFlagPrefix | static_cast<uint64_t>(excl + agg));
+    if (lane == 0) store_status(&status[blk], kFlagPrefix | static_cast<uint64_t>(excl + agg));
     return excl;
 }
 
@@ -138,15 +153,19 @@ struct HopArgs {
     float *src_norm;
     // workspace
     int32_t *map;
-    uint32_t *bits;
+    uint32_t *bits, *dbits;
     int64_t words;
     int64_t *gpad;      // [cap_dst][k] sampled global ids
     int32_t *cnt;       // [cap_dst] sample counts
     int32_t *erow;      // [cap_nnz] row of each edge (for the transpose) or null
     uint64_t *status;   // [nb_rows + nb_bits] look-back words
-    int *tickets;       // [2]
+    int *ticket;
     int64_t nb_rows, nb_bits;
 };
+
+__device__ __forceinline__ void set_bit(uint32_t *bm, int64_t v) {
+    atomicOr(&bm[v >> 5], 1u << (v & 31));
+}
 
 // 1. prepare: one wavefront per destination row.  R drawn positions per lane
 // (slot s lives in lane s % 64, register s / 64).
@@ -155,10 +174,10 @@ __global__ void __launch_bounds__(kThreads) hop_prepare_kernel(HopArgs a) {
     const int64_t gtid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     const int64_t gsize = static_cast<int64_t>(gridDim.x) * kThreads;
     const int64_t n_dst = a.n_dst_dev ? min(*a.n_dst_dev, a.cap_dst) : a.cap_dst;
-    // reset the look-back state of steps 2 and 3
+    // reset the look-back state of the emit kernel
     for (int64_t i = gtid; i < a.nb_rows + a.nb_bits; i += gsize) a.status[i] = 0;
-    if (gtid < 2) a.tickets[gtid] = 0;
     if (gtid == 0) {
+        *a.ticket = 0;
         a.counts[0] = n_dst;
         a.counts[3] = 0;
     }
@@ -175,9 +194,14 @@ __global__ void __launch_bounds__(kThreads) hop_prepare_kernel(HopArgs a) {
         a.src_ids[row] = v;
         if (a.src_norm) a.src_norm[row] = a.gcn_norm[v];
         a.cnt[row] = static_cast<int32_t>(d < k ? d : k);
+        set_bit(a.dbits, v);
     }
     if (d <= k) {
-        for (int64_t p = lane; p < d; p += 64) out[p] = a.col[beg + p];
+        for (int64_t p = lane; p < d; p += 64) {
+            const int64_t u = a.col[beg + p];
+            out[p] = u;
+            set_bit(a.bits, u);
+        }
         return;
     }
     uint32_t slot[R];
@@ -213,75 +237,62 @@ __global__ void __launch_bounds__(kThreads) hop_prepare_kernel(HopArgs a) {
         for (int r = 0; r < R; ++r) rank[r] += (other < slot[r]) ? 1 : 0;
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-        if (r * 64 + lane < k) out[rank[r]] = a.col[beg + slot[r]];
+    for (int r = 0; r < R; ++r) {
+        if (r * 64 + lane < k) {
+            const int64_t u = a.col[beg + slot[r]];
+            out[rank[r]] = u;
+            set_bit(a.bits, u);
+        }
+    }
 }
 
-// 2. mark new ids and scan the sample counts into the row pointer.  A
-// workgroup owns 256 destination rows; its threads walk the rows' staged
-// samples together (slot-parallel, so the loads are independent).
-__global__ void __launch_bounds__(kThreads) hop_mark_kernel(HopArgs a) {
-    __shared__ int32_t rc[kThreads];
-    const int64_t blk = take_ticket(&a.tickets[0]);
-    const int64_t n_dst = a.counts[0];
-    const int64_t row0 = blk * kThreads;
-    const int64_t i = row0 + threadIdx.x;
+// 2a. row pointer of the block: scan of the sample counts (logical block
+// `blk` owns rows [256 blk, 256 blk + 256)).
+__device__ void emit_rows(const HopArgs &a, int64_t blk, int64_t n_dst) {
+    const int64_t i = blk * kThreads + threadIdx.x;
     const int64_t c = (i < n_dst) ? a.cnt[i] : 0;
-    rc[threadIdx.x] = static_cast<int32_t>(c);
-    __syncthreads();
-    const int64_t k = a.k;
-    const int64_t nrows = max<int64_t>(0, min<int64_t>(kThreads, n_dst - row0));
-    const int64_t slots = nrows * k;
-    const int64_t *g = a.gpad + row0 * k;
-    for (int64_t s0 = 0; s0 < slots; s0 += 4 * kThreads) {
-        int64_t u[4];
-        bool ok[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t sl = s0 + q * kThreads + threadIdx.x;
-            const int64_t r = sl / k;
-            ok[q] = sl < slots && (sl - r * k) < rc[sl < slots ? r : 0];
-            u[q] = g[ok[q] ? sl : 0];
-        }
-        int32_t mv[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) mv[q] = a.map[ok[q] ? u[q] : 0];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (ok[q] && mv[q] < 0) atomicOr(&a.bits[u[q] >> 5], 1u << (u[q] & 31));
-    }
     int64_t total;
     const int64_t excl_in_block = block_excl_scan(c, &total);
     __shared__ int64_t base;
-    if (threadIdx.x == 0) base = look_back(a.status, blk, total, &a.counts[3]);
+    if (threadIdx.x < 64) {
+        const int64_t b = look_back(a.status, blk, total, &a.counts[3]);
+        if (threadIdx.x == 0) base = b;
+    }
     __syncthreads();
     if (i < n_dst) a.brow[i + 1] = base + excl_in_block + c;
     if (blk == 0 && threadIdx.x == 0) a.brow[0] = 0;
     if (blk == a.nb_rows - 1 && threadIdx.x == 0) a.counts[2] = base + total;
 }
 
-// 3. new sources in ascending vertex order.
-__global__ void __launch_bounds__(kThreads) hop_emit_kernel(HopArgs a) {
-    const int64_t blk = take_ticket(&a.tickets[1]);
-    const int64_t n_dst = a.counts[0];
+// 2b. new sources in ascending vertex order (logical block `blk` owns
+// kBitTile bitmap words).
+__device__ void emit_sources(const HopArgs &a, int64_t blk, int64_t n_dst) {
     const int64_t w0 = blk * kBitTile + threadIdx.x * kBitWords;
-    uint32_t wv[kBitWords];
+    uint32_t sw[kBitWords], dw[kBitWords];
+#pragma unroll
+    for (int q = 0; q < kBitWords; ++q) {
+        const int64_t w = (w0 + q < a.words) ? w0 + q : 0;
+        sw[q] = a.bits[w];
+        dw[q] = a.dbits[w];
+    }
     int64_t c = 0;
 #pragma unroll
     for (int q = 0; q < kBitWords; ++q) {
-        wv[q] = (w0 + q < a.words) ? a.bits[w0 + q] : 0u;
-        c += __popc(wv[q]);
+        if (w0 + q >= a.words) sw[q] = dw[q] = 0u;
+        c += __popc(sw[q] & ~dw[q]);
     }
     int64_t total;
     const int64_t excl_in_block = block_excl_scan(c, &total);
     __shared__ int64_t base;
-    if (threadIdx.x == 0) base = look_back(a.status + a.nb_rows, blk, total, &a.counts[3]);
+    if (threadIdx.x < 64) {
+        const int64_t b = look_back(a.status + a.nb_rows, blk, total, &a.counts[3]);
+        if (threadIdx.x == 0) base = b;
+    }
     __syncthreads();
     int64_t r = n_dst + base + excl_in_block;
 #pragma unroll
     for (int q = 0; q < kBitWords; ++q) {
-        uint32_t m = wv[q];
-        if (!m) continue;
+        uint32_t m = sw[q] & ~dw[q];
         const int64_t wbase = (w0 + q) * 32;
         while (m) {
             const int b = __builtin_ctz(m);
@@ -292,12 +303,24 @@ __global__ void __launch_bounds__(kThreads) hop_emit_kernel(HopArgs a) {
             if (a.src_norm) a.src_norm[r] = a.gcn_norm[u];
             ++r;
         }
-        a.bits[w0 + q] = 0u;
+        if (sw[q]) a.bits[w0 + q] = 0u;
+        if (dw[q]) a.dbits[w0 + q] = 0u;
     }
     if (blk == a.nb_bits - 1 && threadIdx.x == 0) a.counts[1] = n_dst + base + total;
 }
 
-// 4. local source index of every sampled edge.
+// 2. one launch, two roles: the first nb_rows tickets scan the rows, the
+// rest emit the new sources.  The role is uniform per workgroup.
+__global__ void __launch_bounds__(kThreads) hop_emit_kernel(HopArgs a) {
+    const int64_t t = take_ticket(a.ticket);
+    const int64_t n_dst = a.counts[0];
+    if (t < a.nb_rows)
+        emit_rows(a, t, n_dst);
+    else
+        emit_sources(a, t - a.nb_rows, n_dst);
+}
+
+// 3. local source index of every sampled edge.
 __global__ void __launch_bounds__(kThreads) hop_relabel_kernel(HopArgs a) {
     const int64_t n_dst = a.counts[0];
     const int64_t total = n_dst * a.k;
@@ -311,16 +334,7 @@ __global__ void __launch_bounds__(kThreads) hop_relabel_kernel(HopArgs a) {
     }
 }
 
-// Standalone calls: put the map back to all -1.
-__global__ void hop_finish_kernel(const int64_t *__restrict__ src_ids, const int64_t *__restrict__ counts,
-                                  int32_t *__restrict__ map) {
-    const int64_t n_src = counts[1];
-    for (int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; j < n_src;
-         j += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        map[src_ids[j]] = -1;
-}
-
-// 5. stable transpose in one workgroup: LSD radix sort of (source, row) by
+// 4. stable transpose in one workgroup: LSD radix sort of (source, row) by
 // source, 8 bits per pass.  Each wavefront owns a contiguous segment of the
 // edge list; per pass the segments' digit histograms give every (segment,
 // digit) its output offset, and the segments are scattered in order with
@@ -429,9 +443,11 @@ __global__ void __launch_bounds__(kSortThreads) csc_build_kernel(const int32_t *
 }
 
 struct SamplerWs {
-    size_t map, bits, gpad, cnt, erow, status, tickets, sort, total;
+    size_t map, bits, dbits, gpad, cnt, status, ticket, csc, total;
 };
 
+// map, bits and dbits depend on graph_n only, so one workspace serves hops
+// of any size.
 SamplerWs sampler_layout(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
     const int64_t words = ceil_div(graph_n > 0 ? graph_n : 1, 32);
     const int64_t nb_rows = ceil_div(cap_dst > 0 ? cap_dst : 1, kThreads);
@@ -441,12 +457,12 @@ SamplerWs sampler_layout(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
     SamplerWs w;
     w.map = c.take(static_cast<size_t>(graph_n > 0 ? graph_n : 1) * 4);
     w.bits = c.take(static_cast<size_t>(words) * 4);
+    w.dbits = c.take(static_cast<size_t>(words) * 4);
     w.gpad = c.take(static_cast<size_t>(cap_nnz) * 8);
     w.cnt = c.take(static_cast<size_t>(cap_dst > 0 ? cap_dst : 1) * 4);
-    w.erow = c.take(static_cast<size_t>(cap_nnz) * 4);
     w.status = c.take(static_cast<size_t>(nb_rows + nb_bits) * 8);
-    w.tickets = c.take(2 * 4);
-    w.sort = c.take(static_cast<size_t>(cap_nnz) * 4 * 4);  // two key / value ping-pong pairs
+    w.ticket = c.take(4);
+    w.csc = c.take(block_csc_ws_bytes(cap_nnz));
     w.total = round_up(c.off, 256);
     return w;
 }
@@ -465,6 +481,12 @@ int bits_for(int64_t v) {  // bits needed to represent values in [0, v)
 
 }  // namespace
 
+// Transpose scratch: the row of every edge, then two key / value ping-pong
+// pairs for the radix sort.
+size_t block_csc_ws_bytes(int64_t cap_nnz) {
+    return round_up(static_cast<size_t>(std::max<int64_t>(cap_nnz, 1)) * 4 * 5, 256);
+}
+
 size_t sampler_ws_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
     return sampler_layout(graph_n, cap_dst, fanout).total;
 }
@@ -476,8 +498,9 @@ gnn_status launch_sampler_ws_init(void *ws, int64_t graph_n, hipStream_t s) {
     fill_i32_kernel<<<grid_for(graph_n, kThreads, 65536), kThreads, 0, s>>>(
         reinterpret_cast<int32_t *>(base + w.map), graph_n, -1);
     GNN_LAUNCHED("sampler_ws_init(map)");
-    fill_i32_kernel<<<grid_for(words, kThreads, 65536), kThreads, 0, s>>>(
-        reinterpret_cast<int32_t *>(base + w.bits), words, 0);
+    // bits and dbits are adjacent: clear both
+    fill_i32_kernel<<<grid_for(2 * words, kThreads, 65536), kThreads, 0, s>>>(
+        reinterpret_cast<int32_t *>(base + w.bits), static_cast<int64_t>((w.gpad - w.bits) / 4), 0);
     GNN_LAUNCHED("sampler_ws_init(bits)");
     return GNN_OK;
 }
@@ -489,11 +512,13 @@ gnn_status launch_gcn_norm(const gnn_graph *g, float *nrm, hipStream_t s) {
     return GNN_OK;
 }
 
-int32_t *sampler_map(void *ws) { return reinterpret_cast<int32_t *>(static_cast<char *>(ws) + sampler_layout(1, 1, 1).map); }
+void *sampler_csc_ws(void *ws, int64_t graph_n, int64_t cap_dst, int32_t fanout) {
+    return static_cast<char *>(ws) + sampler_layout(graph_n, cap_dst, fanout).csc;
+}
 
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              bool want_csc, const gnn_block *out, void *ws, bool defer_reset, hipStream_t s) {
+                              const gnn_block *out, void *ws, void *csc_ws, hipStream_t s) {
     const SamplerWs w = sampler_layout(g->n, out->cap_dst, fanout);
     char *base = static_cast<char *>(ws);
     HopArgs a;
@@ -514,12 +539,13 @@ gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const i
     a.src_norm = out->src_norm;
     a.map = reinterpret_cast<int32_t *>(base + w.map);
     a.bits = reinterpret_cast<uint32_t *>(base + w.bits);
+    a.dbits = reinterpret_cast<uint32_t *>(base + w.dbits);
     a.words = ceil_div(g->n > 0 ? g->n : 1, 32);
     a.gpad = reinterpret_cast<int64_t *>(base + w.gpad);
     a.cnt = reinterpret_cast<int32_t *>(base + w.cnt);
-    a.erow = want_csc ? reinterpret_cast<int32_t *>(base + w.erow) : nullptr;
+    a.erow = static_cast<int32_t *>(csc_ws);
     a.status = reinterpret_cast<uint64_t *>(base + w.status);
-    a.tickets = reinterpret_cast<int *>(base + w.tickets);
+    a.ticket = reinterpret_cast<int *>(base + w.ticket);
     a.nb_rows = ceil_div(out->cap_dst > 0 ? out->cap_dst : 1, kThreads);
     a.nb_bits = ceil_div(a.words, kBitTile);
 
@@ -530,25 +556,21 @@ gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const i
     else if (fanout <= 512) hop_prepare_kernel<8><<<gw, kThreads, 0, s>>>(a);
     else hop_prepare_kernel<16><<<gw, kThreads, 0, s>>>(a);
     GNN_LAUNCHED("hop_prepare");
-    hop_mark_kernel<<<static_cast<unsigned>(a.nb_rows), kThreads, 0, s>>>(a);
-    GNN_LAUNCHED("hop_mark");
-    hop_emit_kernel<<<static_cast<unsigned>(a.nb_bits), kThreads, 0, s>>>(a);
+    hop_emit_kernel<<<static_cast<unsigned>(a.nb_rows + a.nb_bits), kThreads, 0, s>>>(a);
     GNN_LAUNCHED("hop_emit");
     hop_relabel_kernel<<<grid_for(std::max<int64_t>(out->cap_dst, 1) * fanout, kThreads, 1 << 16), kThreads, 0, s>>>(a);
     GNN_LAUNCHED("hop_relabel");
-    if (want_csc) {
-        int32_t *sort = reinterpret_cast<int32_t *>(base + w.sort);
-        const int64_t cap_nnz = std::max<int64_t>(out->cap_dst * fanout, 1);
-        csc_build_kernel<<<1, kSortThreads, 0, s>>>(out->col, a.erow, out->counts, bits_for(out->cap_src), sort,
-                                                    sort + cap_nnz, sort + 2 * cap_nnz, sort + 3 * cap_nnz,
-                                                    out->cscrow, out->cscptr);
-        GNN_LAUNCHED("csc_build");
-    }
-    if (!defer_reset) {
-        hop_finish_kernel<<<grid_for(out->cap_src, kThreads, 1 << 16), kThreads, 0, s>>>(out->src_ids, out->counts,
-                                                                                        a.map);
-        GNN_LAUNCHED("hop_finish");
-    }
+    return GNN_OK;
+}
+
+gnn_status launch_block_csc(const gnn_block *out, void *csc_ws, int64_t scratch_nnz, hipStream_t s) {
+    const int64_t cap_nnz = std::max<int64_t>(scratch_nnz, 1);
+    int32_t *erow = static_cast<int32_t *>(csc_ws);
+    int32_t *sort = erow + cap_nnz;
+    csc_build_kernel<<<1, kSortThreads, 0, s>>>(out->col, erow, out->counts, bits_for(out->cap_src), sort,
+                                                sort + cap_nnz, sort + 2 * cap_nnz, sort + 3 * cap_nnz, out->cscrow,
+                                                out->cscptr);
+    GNN_LAUNCHED("csc_build");
     return GNN_OK;
 }
 

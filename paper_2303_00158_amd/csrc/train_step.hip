@@ -1,8 +1,14 @@
 // One training iteration composed from the kernels: sample L blocks, gather
 // X', L forward layers, loss, backward in reverse order (no input gradient
-// below the first layer), SGD.  Everything is enqueued on one stream and the
-// host never waits: counts produced on the device are read by later kernels.
+// below the first layer), SGD.  The host never waits: counts produced on the
+// device are read by later kernels.
+//
+// Everything runs on the caller's stream except the block transposes (CSC),
+// which only the backward pass reads: they run on a helper stream of the
+// library, forked after each block is built and joined before the backward
+// pass, so they overlap the gather and the forward layers.
 #include <algorithm>
+#include <mutex>
 
 #include "internal.h"
 
@@ -20,6 +26,34 @@ __global__ void step_tail_kernel(const int64_t *c0, const int64_t *c1, const int
     *edges = e;
     if (edges_out) *edges_out = e;
     if (loss_out) *loss_out = *loss_src;
+}
+
+// One helper stream and its events per device, created on first use and
+// kept until the process ends.  g_helper_mu serialises training-step
+// enqueues, which share them.
+struct Helper {
+    bool ready = false;
+    hipStream_t stream = nullptr;
+    hipEvent_t fork[GNN_MAX_LAYERS] = {};
+    hipEvent_t join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_helper_mu;
+Helper g_helper[kMaxDevices];
+
+gnn_status helper_for_current_device(Helper **out) {
+    int dev = 0;
+    GNN_HIP(hipGetDevice(&dev));
+    GNN_CHECK(dev >= 0 && dev < kMaxDevices, GNN_EUNSUPPORTED, "train_step: device %d out of range", dev);
+    Helper &h = g_helper[dev];
+    if (!h.ready) {
+        GNN_HIP(hipStreamCreateWithFlags(&h.stream, hipStreamNonBlocking));
+        for (int i = 0; i < GNN_MAX_LAYERS; ++i) GNN_HIP(hipEventCreateWithFlags(&h.fork[i], hipEventDisableTiming));
+        GNN_HIP(hipEventCreateWithFlags(&h.join, hipEventDisableTiming));
+        h.ready = true;
+    }
+    *out = &h;
+    return GNN_OK;
 }
 
 int64_t k_of(const gnn_model *m, int l) {  // reduction width of layer l (1-based)
@@ -58,6 +92,7 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
             o->blk_cscrow[h] = c.take(static_cast<size_t>(std::max<int64_t>(o->cap_nnz[h], 1)) * 4);
         }
         if (m->kind == GNN_AGG_GCN_SYM) o->blk_src_norm[h] = c.take(static_cast<size_t>(o->cap_src[h]) * 4);
+        if (h < L - 1) o->blk_csc_ws[h] = c.take(block_csc_ws_bytes(o->cap_nnz[h]));
     }
     o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
     size_t bwd = 0, fwd = 0;
@@ -110,20 +145,28 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     gnn_block blk[GNN_MAX_LAYERS];
     for (int h = 0; h < L; ++h) blk[h] = block_view(o, h, base);
 
-    // sampling: hop 1 around the targets, then outwards
+    std::lock_guard<std::mutex> lock(g_helper_mu);
+    Helper *hp = nullptr;
+    if (L > 1) GNN_TRY(helper_for_current_device(&hp));
+    // sampling: hop 1 around the targets, then outwards; the transposes of
+    // all blocks but the last go to the helper stream
     for (int h = 0; h < L; ++h) {
         const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
         const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
+        void *csc_ws = h < L - 1 ? base + o.blk_csc_ws[h] : nullptr;
         GNN_TRY(launch_build_block(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h],
-                                   seed, step, h + 1, h < L - 1, &blk[h], base + o.sampler_ws, true, s));
+                                   seed, step, h + 1, &blk[h], base + o.sampler_ws, csc_ws, s));
+        if (csc_ws) {
+            GNN_HIP(hipEventRecord(hp->fork[h], s));
+            GNN_HIP(hipStreamWaitEvent(hp->stream, hp->fork[h], 0));
+            GNN_TRY(launch_block_csc(&blk[h], csc_ws, o.cap_nnz[h], hp->stream));
+        }
     }
+    if (hp) GNN_HIP(hipEventRecord(hp->join, hp->stream));
     // feature loading: rows of the input layer's sources
     const gnn_block &b0 = blk[L - 1];
     void *x0 = base + o.x0;
-    // the last block's sources include every vertex the hops mapped: the
-    // gather puts the sampler's vertex map back to -1 as it reads them
-    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act,
-                          sampler_map(base + o.sampler_ws), s));
+    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act, s));
 
     // forward
     for (int l = 1; l <= L; ++l) {
@@ -141,7 +184,8 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     float *loss_slot = reinterpret_cast<float *>(base + o.loss);
     GNN_TRY(launch_softmax_ce(reinterpret_cast<const float *>(base + o.h[L]), batch, m->dims[L], labels, targets,
                               reinterpret_cast<float *>(base + o.grad[L]), loss_slot, base + o.loss_ws, s));
-    // backward
+    // backward (reads the transposes)
+    if (hp) GNN_HIP(hipStreamWaitEvent(s, hp->join, 0));
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);

@@ -56,7 +56,7 @@ class StepLayout(ctypes.Structure):
                 ("cap_dst", _i64 * _ML), ("cap_src", _i64 * _ML), ("cap_nnz", _i64 * _ML),
                 ("blk_counts", _sz * _ML), ("blk_src_ids", _sz * _ML), ("blk_rowptr", _sz * _ML),
                 ("blk_col", _sz * _ML), ("blk_cscptr", _sz * _ML), ("blk_cscrow", _sz * _ML),
-                ("blk_src_norm", _sz * _ML),
+                ("blk_src_norm", _sz * _ML), ("blk_csc_ws", _sz * _ML),
                 ("x0", _sz), ("agg", _sz * (_ML + 1)), ("h", _sz * (_ML + 1)), ("grad", _sz * (_ML + 1)),
                 ("d_a", _sz * (_ML + 1)), ("fwd_ws", _sz), ("fwd_ws_bytes", _sz), ("bwd_ws", _sz),
                 ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
