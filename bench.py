@@ -46,7 +46,9 @@ def parse():
     p.add_argument("--stage-steps", type=int, default=5, help="steps of the event-instrumented staged run")
     p.add_argument("--no-stages", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for the CPU baseline")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="CPU oracle baseline: run whole oracle steps until this much time has passed")
+    p.add_argument("--replays", type=int, default=20, help="back-to-back launches timing the roofline kernel")
     p.add_argument("--lr", type=float, default=0.01)
     return p.parse_args()
 
@@ -99,6 +101,48 @@ class StagedStep:
             gnn._check(gnn.lib().gnn_update_fwd_workspace_size(w.k_of_layer(l), dims[l], rows, gemm, ctypes.byref(nb)))
             self.fwd_ws[l] = torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=dev)
             self.bwd_ws[l] = gnn.update_bwd_workspace(w.k_of_layer(l), dims[l], rows, gemm, dev)
+
+    def replay(self, name: str, trainer, table, reps: int) -> float:
+        """Launch the single ABI call of stage `name` `reps` times back to back
+        on the blocks of the last run; returns the mean ms per launch (HIP
+        events on the stream the call uses)."""
+        gnn, L, w = self.gnn, self.L, self.w
+        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
+        if name == "gather":
+            b0 = self.blocks[-1]
+            call = lambda: gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2])  # noqa
+        elif name.startswith("agg_fwd_l"):
+            l = int(name[-1])
+            blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            call = lambda: gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])  # noqa
+        elif name.startswith("update_fwd_l"):
+            l = int(name[-1])
+            blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            call = lambda: gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None,  # noqa
+                                          trainer.w[l - 1], trainer.b[l - 1], self.h[l], l < L, gemm,
+                                          m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.fwd_ws[l])
+        elif name.startswith("agg_bwd_l"):
+            l = int(name[-1])
+            blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            call = lambda: gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1],  # noqa
+                                             h_below=hin)
+        else:
+            raise ValueError(name)
+        call()
+        torch.cuda.synchronize()
+        if hasattr(torch.cuda, "_sleep"):
+            torch.cuda._sleep(20_000_000)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    def block_sizes(self):
+        return [{k: int(v) for k, v in blk.host().items() if k in ("n_dst", "n_src", "nnz")} for blk in self.blocks]
 
     def run(self, trainer, table, labels, targets, nrm, seed, step, lr, events=None):
         """Enqueue one step; when `events` is a list, record (name, event) pairs."""
@@ -287,20 +331,33 @@ def main():
         stage_ms = {k: sums[k] / counts[k] for k in sums}
         result["stages_ms"] = {k: round(v, 5) for k, v in stage_ms.items()}
         single = [k for k in stage_ms if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "agg_bwd"))]
-        dom = max(single, key=lambda k: stage_ms[k])
-        byts, flops = staged.stage_bytes(dom)
-        t = stage_ms[dom] / 1e3
-        if flops and flops / max(byts, 1) > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-            ach = flops / t / 1e12
-            roof = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / BF16_PEAK_TFLOPS}
-        else:
-            ach = byts / t / 1e9
-            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS}
-        roof.update({"kernel": dom, "algorithmic_bytes": int(byts), "flops": int(flops or 0),
-                     "avg_ms": stage_ms[dom], "traffic": None})
+        ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+        def roof_of(name, ms):
+            byts, flops = staged.stage_bytes(name)
+            t = ms / 1e3
+            if flops and flops / max(byts, 1) > ridge:
+                ach = flops / t / 1e12
+                r = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / BF16_PEAK_TFLOPS}
+            else:
+                ach = byts / t / 1e9
+                r = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS}
+            r.update({"algorithmic_bytes": int(byts), "flops": int(flops or 0), "avg_ms": ms})
+            return r
+
+        # per-launch time of each single-kernel stage: back-to-back replays
+        launch_ms = {k: staged.replay(k, tr, table, args.replays) for k in single}
+        dom = max(single, key=lambda k: launch_ms[k])
+        roof = roof_of(dom, launch_ms[dom])
+        roof.update({"kernel": dom, "traffic": None})
         result["roofline"] = roof
+        result["kernels"] = {k: {kk: (round(vv, 6) if isinstance(vv, float) else vv)
+                                 for kk, vv in roof_of(k, launch_ms[k]).items()} for k in single}
+        result["block_sizes"] = staged.block_sizes()
         log(f"stages (ms): {json.dumps(result['stages_ms'])}")
+        log(f"per-launch (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
 
     # ---- CPU oracle baseline ---------------------------------------------
     if not args.no_cpu_baseline:
@@ -315,20 +372,23 @@ def main():
         b_h = [x.numpy() for x in biases]
         okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
         oprec = oracle.BF16 if w.precision == "bf16" else oracle.F32
-        tot_e, tot_t = 0, 0.0
-        for s in range(args.cpu_steps):
+        tot_e, tot_t, n_steps = 0, 0.0, 0
+        while n_steps < 2 or tot_t < args.cpu_seconds:
+            s = n_steps
             cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oprec, seed=w.seed,
                                     step=s, lr=args.lr)
             tt = time.perf_counter()
-            ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt[s].cpu().numpy(), w_h, b_h, cfg)
+            ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt[s % len(tgt)].cpu().numpy(), w_h,
+                                    b_h, cfg)
             tot_t += time.perf_counter() - tt
             tot_e += ref["edges"]
             w_h, b_h = ref["new_w"], ref["new_b"]
+            n_steps += 1
         result["cpu_baseline"] = {
             "value": tot_e / tot_t, "unit": "edges/s", "cores": oracle.get_threads(), "kind": "oracle",
-            "sample": f"{args.cpu_steps} full training steps (sample, gather, forward, loss, backward, SGD) of the "
-                      f"same workload, fp64 sums; {tot_t:.2f} s",
-            "steps_per_s": args.cpu_steps / tot_t,
+            "sample": f"{n_steps} full training steps (sample, gather, forward, loss, backward, SGD) of the "
+                      f"same workload, fp64 sums, {tot_t:.1f} s",
+            "steps_per_s": n_steps / tot_t,
         }
         log(f"cpu oracle: {tot_e / tot_t:.0f} edges/s with {oracle.get_threads()} threads")
 
