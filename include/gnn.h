@@ -259,7 +259,17 @@ typedef struct gnn_model {
     float *b[GNN_MAX_LAYERS];           /* [device] fp32 f^l */
     float *dw[GNN_MAX_LAYERS];          /* [device] fp32 K_l x f^l, written */
     float *db[GNN_MAX_LAYERS];          /* [device] fp32 f^l, written */
+    uint16_t *wt[GNN_MAX_LAYERS];       /* [device] optional bf16 shadow f^l x K_l = bf16(W^T), 8-byte aligned,
+                                           for GNN_BF16 models (NULL: the GEMMs round W as they load it) */
 } gnn_model;
+
+/* Write every non-NULL shadow m->wt[l] = bf16(m->w[l]^T) (round to nearest
+ * even).  A model with shadows must be synced once before its first
+ * gnn_train_step and after any change to W made outside the library;
+ * gnn_train_step's SGD keeps the shadows in step with W.  The forward update
+ * reads the shadow instead of W, which gives the same bf16 operand values
+ * (Section II-A, equation 2, with operands rounded as in bf16 mode). */
+gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s);
 
 /* Offsets (bytes from the workspace base) of the step's internal buffers, for
  * inspection.  Block h (1-based hop) is the block of layer L-h+1. */

@@ -88,6 +88,8 @@ gnn_status check_model_buffers(const gnn_model *m, const char *who) {
                   l + 1);
         GNN_CHECK(aligned(m->w[l], 16) && aligned(m->dw[l], 16) && aligned(m->b[l], 4) && aligned(m->db[l], 4),
                   GNN_EINVAL, "%s: weights must be 16-byte aligned", who);
+        GNN_CHECK(!m->wt[l] || (m->precision == GNN_BF16 && aligned(m->wt[l], 8)), GNN_EINVAL,
+                  "%s: layer %d shadow must be 8-byte aligned and needs a GNN_BF16 model", who, l + 1);
     }
     return GNN_OK;
 }
@@ -267,7 +269,7 @@ gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
         GNN_CHECK(aligned(ws, 256), GNN_EINVAL, "%s: ws must be 256-byte aligned", who);
         GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     }
-    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, bias, n_out, relu, gemm_dt, out, odt, ws,
+    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, nullptr, bias, n_out, relu, gemm_dt, out, odt, ws,
                              stream_of(s));
 }
 
@@ -298,7 +300,7 @@ gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     return launch_update_bwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, g, n_out, gemm_dt, dw, db, d_a, ws,
-                             nullptr, nullptr, 0.f, stream_of(s));
+                             nullptr, nullptr, nullptr, 0.f, stream_of(s));
 }
 
 gnn_status gnn_softmax_ce_workspace_size(int64_t b, size_t *bytes) {
@@ -357,6 +359,19 @@ gnn_status gnn_train_step_workspace_init(const gnn_model *m, int64_t graph_n, in
     GNN_CHECK(ws_bytes >= o.total_bytes, GNN_ESIZE, "gnn_train_step_workspace_init: workspace %zu bytes, need %zu",
               ws_bytes, o.total_bytes);
     return launch_sampler_ws_init(static_cast<char *>(ws) + o.sampler_ws, graph_n, stream_of(s));
+}
+
+gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_model_sync_shadow";
+    GNN_TRY(check_model(m, who));
+    GNN_TRY(check_model_buffers(m, who));
+    for (int l = 0; l < m->num_layers; ++l) {
+        if (!m->wt[l]) continue;
+        const int64_t K = (m->kind == GNN_AGG_SAGE_MEAN ? 2 : 1) * static_cast<int64_t>(m->dims[l]);
+        GNN_TRY(launch_shadow_sync(m->w[l], K, m->dims[l + 1], m->wt[l], stream_of(s)));
+    }
+    return GNN_OK;
 }
 
 gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,

@@ -106,7 +106,8 @@ template <bool VO>
 __global__ void __launch_bounds__(256) dw_reduce_kernel(const float *__restrict__ part, int nsplit, int64_t K,
                                                         int64_t n_out, float *__restrict__ dw,
                                                         float *__restrict__ db, float *__restrict__ w_upd,
-                                                        float *__restrict__ b_upd, float lr) {
+                                                        float *__restrict__ b_upd, uint16_t *__restrict__ wt_upd,
+                                                        float lr) {
     const int64_t ldp = part_ld(n_out), chunks = ldp / 4;
     const int64_t rows = K + (db ? 1 : 0);
     for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < rows * chunks;
@@ -118,9 +119,26 @@ __global__ void __launch_bounds__(256) dw_reduce_kernel(const float *__restrict_
         const float4 old = upd ? load4_clamped<VO>(upd, base, c, n_out) : make_float4(0.f, 0.f, 0.f, 0.f);
         const float4 s = sum_splits(part + r * ldp + c, (K + 1) * ldp, nsplit);
         store4_masked<VO>(brow ? db : dw, base, c, n_out, s);
-        if (upd)
-            store4_masked<VO>(upd, base, c, n_out,
-                              make_float4(old.x - lr * s.x, old.y - lr * s.y, old.z - lr * s.z, old.w - lr * s.w));
+        if (upd) {
+            const float4 nw = make_float4(old.x - lr * s.x, old.y - lr * s.y, old.z - lr * s.z, old.w - lr * s.w);
+            store4_masked<VO>(upd, base, c, n_out, nw);
+            if (wt_upd && !brow) {
+                const float v[4] = {nw.x, nw.y, nw.z, nw.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (c + e < n_out) wt_upd[(c + e) * K + r] = f32_to_bf16(v[e]);
+            }
+        }
+    }
+}
+
+// wt[n][k] = bf16(w[k][n]): one thread per element, writes coalesced.
+__global__ void __launch_bounds__(256) shadow_sync_kernel(const float *__restrict__ w, int64_t K, int64_t n,
+                                                          uint16_t *__restrict__ wt) {
+    for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < K * n;
+         t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t j = t / K, k = t - j * K;
+        wt[t] = f32_to_bf16(w[k * n + j]);
     }
 }
 
@@ -163,9 +181,18 @@ size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt)
     return round_up(dw_part_bytes(plan_dw(k, n_out, cap_m, gemm_dt == GNN_BF16), k, n_out), 256);
 }
 
+gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s) {
+    if (K * n == 0) return GNN_OK;
+    const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(K * n, 256), 1 << 16));
+    shadow_sync_kernel<<<grid, 256, 0, s>>>(w, K, n, wt);
+    GNN_LAUNCHED("shadow_sync");
+    return GNN_OK;
+}
+
 gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
                              int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt, float *dw,
-                             float *db, float *d_a, void *ws, float *w_upd, float *b_upd, float lr, hipStream_t s) {
+                             float *db, float *d_a, void *ws, float *w_upd, float *b_upd, uint16_t *wt_upd, float lr,
+                             hipStream_t s) {
     if (n_out == 0) return GNN_OK;
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
@@ -233,9 +260,9 @@ gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int
     const int64_t work = (K + 1) * (part_ld(n_out) / 4);
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>(ceil_div(work, 256), 1 << 20));
     if (vec_r)
-        dw_reduce_kernel<true><<<rgrid, 256, 0, s>>>(part, pw.nsplit, K, n_out, dw, db, w_upd, b_upd, lr);
+        dw_reduce_kernel<true><<<rgrid, 256, 0, s>>>(part, pw.nsplit, K, n_out, dw, db, w_upd, b_upd, wt_upd, lr);
     else
-        dw_reduce_kernel<false><<<rgrid, 256, 0, s>>>(part, pw.nsplit, K, n_out, dw, db, w_upd, b_upd, lr);
+        dw_reduce_kernel<false><<<rgrid, 256, 0, s>>>(part, pw.nsplit, K, n_out, dw, db, w_upd, b_upd, wt_upd, lr);
     GNN_LAUNCHED("update_dw_reduce");
     return GNN_OK;
 }

@@ -13,11 +13,42 @@ namespace {
 
 using namespace gemm;
 
-template <bool BF16, int TILE, class TA, class TO, bool VA, bool VW, bool VO>
+// Where the W operand comes from.
+enum WSrc {
+    kWCols = 0,     // fp32 W (K x n_out), element loads (n_out not a multiple of 4)
+    kWColsVec = 1,  // fp32 W, 16-byte loads
+    kWtBf16 = 2,    // bf16 shadow W^T (n_out x K), 8-byte loads, no transpose
+};
+
+template <bool BF16, int TILE, int WS, int D> struct WOperand;
+template <bool BF16, int TILE, int D> struct WOperand<BF16, TILE, kWCols, D> {
+    using type = SrcCols<BF16, TILE, float, false, D>;
+    __device__ static type make(const float *w, const uint16_t *, int64_t K, int64_t n_out, int64_t r_end,
+                                int64_t col0) {
+        return type{w, nullptr, n_out, n_out, n_out, r_end, col0, {}};
+    }
+};
+template <bool BF16, int TILE, int D> struct WOperand<BF16, TILE, kWColsVec, D> {
+    using type = SrcCols<BF16, TILE, float, true, D>;
+    __device__ static type make(const float *w, const uint16_t *, int64_t K, int64_t n_out, int64_t r_end,
+                                int64_t col0) {
+        return type{w, nullptr, n_out, n_out, n_out, r_end, col0, {}};
+    }
+};
+template <int TILE, int D> struct WOperand<true, TILE, kWtBf16, D> {
+    using type = SrcRows<true, TILE, uint16_t, true, D>;
+    __device__ static type make(const float *, const uint16_t *wt, int64_t K, int64_t n_out, int64_t,
+                                int64_t col0) {
+        return type{wt, nullptr, K, K, n_out, K, col0, {}};
+    }
+};
+
+template <bool BF16, int TILE, class TA, class TO, bool VA, int WS, bool VO>
 __global__ void __launch_bounds__(kThreads) update_fwd_kernel(const TA *__restrict__ a_self,
                                                                const TA *__restrict__ a_nbr, int64_t k_each,
                                                                const int64_t *m_dev, int64_t cap_m,
                                                                const float *__restrict__ w,
+                                                               const uint16_t *__restrict__ wt,
                                                                const float *__restrict__ bias, int64_t n_out,
                                                                int relu, TO *__restrict__ out,
                                                                float *__restrict__ part, TileMap map) {
@@ -32,7 +63,7 @@ __global__ void __launch_bounds__(kThreads) update_fwd_kernel(const TA *__restri
     int64_t r_beg, r_end;
     split_range<Cfg<BF16>::BK>(K, gridDim.z, blockIdx.z, &r_beg, &r_end);
     SrcRows<BF16, TILE, TA, VA, D> sp{a_self, a_nbr, k_each, k_each, M, K, row0, {}};
-    SrcCols<BF16, TILE, float, VW, D> sq{w, nullptr, n_out, n_out, n_out, r_end, col0, {}};
+    auto sq = WOperand<BF16, TILE, WS, D>::make(w, wt, K, n_out, r_end, col0);
     Acc<TILE, TILE> acc;
     run_tile<BF16, D>(acc, sp, sq, r_beg, r_end, lds, [](const auto &, int, int64_t, bool) {});
     const int64_t gc = col0 + TileOut<TILE, TILE>::col();
@@ -91,6 +122,56 @@ size_t part_bytes(const FwdPlan &p, int64_t cap_m, int64_t n_out) {
     return p.nsplit > 1 ? static_cast<size_t>(p.nsplit) * cap_m * part_ld(n_out) * 4 : 0;
 }
 
+// Launch-time dispatch over the kernel's template parameters.
+struct FwdLaunch {
+    const void *a_self, *a_nbr;
+    int64_t k_each;
+    const int64_t *m_dev;
+    int64_t cap_m;
+    const float *w;
+    const uint16_t *wt;
+    const float *bias;
+    int64_t n_out;
+    int relu;
+    void *out;
+    float *part;
+    TileMap map;
+    dim3 grid;
+    hipStream_t s;
+};
+
+template <bool BF16, int T, class TA, class TO, bool VA, int WS>
+void fwd_launch(const FwdLaunch &L, bool vec_o) {
+    const TA *as = static_cast<const TA *>(L.a_self), *an = static_cast<const TA *>(L.a_nbr);
+    TO *o = static_cast<TO *>(L.out);
+    if (vec_o)
+        update_fwd_kernel<BF16, T, TA, TO, VA, WS, true><<<L.grid, kThreads, 0, L.s>>>(
+            as, an, L.k_each, L.m_dev, L.cap_m, L.w, L.wt, L.bias, L.n_out, L.relu, o, L.part, L.map);
+    else
+        update_fwd_kernel<BF16, T, TA, TO, VA, WS, false><<<L.grid, kThreads, 0, L.s>>>(
+            as, an, L.k_each, L.m_dev, L.cap_m, L.w, L.wt, L.bias, L.n_out, L.relu, o, L.part, L.map);
+}
+
+template <bool BF16, int T, class TA, class TO, bool VA>
+void fwd_by_wsrc(const FwdLaunch &L, int wsrc, bool vec_o) {
+    if constexpr (BF16) {
+        if (wsrc == kWtBf16) return fwd_launch<BF16, T, TA, TO, VA, kWtBf16>(L, vec_o);
+    }
+    if (wsrc == kWColsVec) fwd_launch<BF16, T, TA, TO, VA, kWColsVec>(L, vec_o);
+    else fwd_launch<BF16, T, TA, TO, VA, kWCols>(L, vec_o);
+}
+
+template <bool BF16, class TA, class TO>
+void fwd_by_tile(const FwdLaunch &L, int tile, bool vec_a, int wsrc, bool vec_o) {
+    if (tile == 128) {
+        if (vec_a) fwd_by_wsrc<BF16, 128, TA, TO, true>(L, wsrc, vec_o);
+        else fwd_by_wsrc<BF16, 128, TA, TO, false>(L, wsrc, vec_o);
+    } else {
+        if (vec_a) fwd_by_wsrc<BF16, 64, TA, TO, true>(L, wsrc, vec_o);
+        else fwd_by_wsrc<BF16, 64, TA, TO, false>(L, wsrc, vec_o);
+    }
+}
+
 }  // namespace
 
 size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt) {
@@ -99,8 +180,8 @@ size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt)
 }
 
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
-                             int64_t cap_m, const float *w, const float *bias, int64_t n_out, int relu, int gemm_dt,
-                             void *out, int odt, void *ws, hipStream_t s) {
+                             int64_t cap_m, const float *w, const uint16_t *wt, const float *bias, int64_t n_out,
+                             int relu, int gemm_dt, void *out, int odt, void *ws, hipStream_t s) {
     if (cap_m == 0 || n_out == 0) return GNN_OK;
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
@@ -111,47 +192,22 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
     const dim3 grid(static_cast<unsigned>(p.map.blocks()), 1, static_cast<unsigned>(p.nsplit));
     const size_t asz = dtype_size(adt), osz = dtype_size(odt);
     const bool vec_a = (k_each % 4 == 0) && aligned(a_self, 4 * asz) && (!a_nbr || aligned(a_nbr, 4 * asz));
-    const bool vec_w = (n_out % 4 == 0) && aligned(w, 16);
+    const bool use_wt = bf && wt != nullptr && K % 4 == 0 && aligned(wt, 8);
+    const int wsrc = use_wt ? kWtBf16 : ((n_out % 4 == 0) && aligned(w, 16) ? kWColsVec : kWCols);
     const bool vec_o = (n_out % 4 == 0) && aligned(out, 4 * osz) && aligned(bias, 16);
-#define FWD(BFV, T, TA, TO, VA, VW)                                                                                 \
-    do {                                                                                                            \
-        if (vec_o)                                                                                                  \
-            update_fwd_kernel<BFV, T, TA, TO, VA, VW, true><<<grid, kThreads, 0, s>>>(                             \
-                static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, m_dev, cap_m, w, bias,     \
-                n_out, relu, static_cast<TO *>(out), part, p.map);                                                  \
-        else                                                                                                        \
-            update_fwd_kernel<BFV, T, TA, TO, VA, VW, false><<<grid, kThreads, 0, s>>>(                            \
-                static_cast<const TA *>(a_self), static_cast<const TA *>(a_nbr), k_each, m_dev, cap_m, w, bias,     \
-                n_out, relu, static_cast<TO *>(out), part, p.map);                                                  \
-    } while (0)
-#define FWD_V(BFV, T, TA, TO)                                  \
-    do {                                                       \
-        if (vec_a && vec_w) FWD(BFV, T, TA, TO, true, true);   \
-        else if (vec_a) FWD(BFV, T, TA, TO, true, false);      \
-        else if (vec_w) FWD(BFV, T, TA, TO, false, true);      \
-        else FWD(BFV, T, TA, TO, false, false);                \
-    } while (0)
-#define FWD_T(BFV, TA, TO)            \
-    do {                              \
-        if (p.tile == 128)            \
-            FWD_V(BFV, 128, TA, TO);  \
-        else                          \
-            FWD_V(BFV, 64, TA, TO);   \
-    } while (0)
+    const FwdLaunch L{static_cast<const void *>(a_self), a_nbr, k_each, m_dev, cap_m, w, wt, bias, n_out, relu, out,
+                      part, p.map, grid, s};
     if (bf) {
-        if (adt == GNN_BF16 && odt == GNN_BF16) FWD_T(true, uint16_t, uint16_t);
-        else if (adt == GNN_BF16 && odt == GNN_F32) FWD_T(true, uint16_t, float);
-        else if (adt == GNN_F32 && odt == GNN_BF16) FWD_T(true, float, uint16_t);
-        else FWD_T(true, float, float);
+        if (adt == GNN_BF16 && odt == GNN_BF16) fwd_by_tile<true, uint16_t, uint16_t>(L, p.tile, vec_a, wsrc, vec_o);
+        else if (adt == GNN_BF16 && odt == GNN_F32) fwd_by_tile<true, uint16_t, float>(L, p.tile, vec_a, wsrc, vec_o);
+        else if (adt == GNN_F32 && odt == GNN_BF16) fwd_by_tile<true, float, uint16_t>(L, p.tile, vec_a, wsrc, vec_o);
+        else fwd_by_tile<true, float, float>(L, p.tile, vec_a, wsrc, vec_o);
     } else {
-        if (adt == GNN_BF16 && odt == GNN_BF16) FWD_T(false, uint16_t, uint16_t);
-        else if (adt == GNN_BF16 && odt == GNN_F32) FWD_T(false, uint16_t, float);
-        else if (adt == GNN_F32 && odt == GNN_BF16) FWD_T(false, float, uint16_t);
-        else FWD_T(false, float, float);
+        if (adt == GNN_BF16 && odt == GNN_BF16) fwd_by_tile<false, uint16_t, uint16_t>(L, p.tile, vec_a, wsrc, vec_o);
+        else if (adt == GNN_BF16 && odt == GNN_F32) fwd_by_tile<false, uint16_t, float>(L, p.tile, vec_a, wsrc, vec_o);
+        else if (adt == GNN_F32 && odt == GNN_BF16) fwd_by_tile<false, float, uint16_t>(L, p.tile, vec_a, wsrc, vec_o);
+        else fwd_by_tile<false, float, float>(L, p.tile, vec_a, wsrc, vec_o);
     }
-#undef FWD_T
-#undef FWD_V
-#undef FWD
     GNN_LAUNCHED("update_fwd");
     if (p.nsplit > 1) {
         const int64_t work = cap_m * (part_ld(n_out) / 4);

@@ -148,14 +148,19 @@ gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, 
 // reductions (no state survives a call).  A null forward workspace disables
 // the reduction split.
 size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt);
+// wt (may be null): bf16 shadow W^T (n_out x K) read instead of w in bf16 mode.
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
-                             int64_t cap_m, const float *w, const float *bias, int64_t n_out, int relu, int gemm_dt,
-                             void *out, int odt, void *ws, hipStream_t s);
+                             int64_t cap_m, const float *w, const uint16_t *wt, const float *bias, int64_t n_out,
+                             int relu, int gemm_dt, void *out, int odt, void *ws, hipStream_t s);
 size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt);
-// w_upd / b_upd (may be null): SGD applied to them with the final gradients.
+// w_upd / b_upd (may be null): SGD applied to them with the final gradients;
+// wt_upd (may be null, needs w_upd): its bf16 shadow W^T, refreshed too.
 gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
                              int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt, float *dw,
-                             float *db, float *d_a, void *ws, float *w_upd, float *b_upd, float lr, hipStream_t s);
+                             float *db, float *d_a, void *ws, float *w_upd, float *b_upd, uint16_t *wt_upd, float lr,
+                             hipStream_t s);
+// wt = bf16(w^T) for a K x n row-major w.
+gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
 gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 size_t softmax_ce_ws_bytes(int64_t b);
 gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels,

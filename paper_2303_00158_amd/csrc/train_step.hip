@@ -177,8 +177,8 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
-                                  m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l], l < L ? act : GNN_F32,
-                                  base + o.fwd_ws, s));
+                                  m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l],
+                                  l < L ? act : GNN_F32, base + o.fwd_ws, s));
     }
     // loss on the targets
     float *loss_slot = reinterpret_cast<float *>(base + o.loss);
@@ -198,7 +198,7 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         GNN_TRY(launch_update_bwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst,
                                   m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l],
                                   m->precision, m->dw[l - 1], m->db[l - 1], d_a, base + o.bwd_ws, m->w[l - 1],
-                                  m->b[l - 1], lr, s));
+                                  m->b[l - 1], m->wt[l - 1], lr, s));
         if (l > 1)
             GNN_TRY(launch_aggregate_bwd(&b, m->kind, d_a, f_in, hin, act,
                                          reinterpret_cast<float *>(base + o.grad[l - 1]), s));

@@ -45,7 +45,7 @@ class Model(ctypes.Structure):
     _fields_ = [("num_layers", _i32), ("kind", _i32), ("precision", _i32),
                 ("dims", _i32 * (GNN_MAX_LAYERS + 1)), ("fanouts", _i32 * GNN_MAX_LAYERS),
                 ("w", _vp * GNN_MAX_LAYERS), ("b", _vp * GNN_MAX_LAYERS),
-                ("dw", _vp * GNN_MAX_LAYERS), ("db", _vp * GNN_MAX_LAYERS)]
+                ("dw", _vp * GNN_MAX_LAYERS), ("db", _vp * GNN_MAX_LAYERS), ("wt", _vp * GNN_MAX_LAYERS)]
 
 
 _ML = GNN_MAX_LAYERS
@@ -83,6 +83,7 @@ _SIGNATURES = {
     "gnn_softmax_ce_workspace_size": (_i32, [_i64, _P(_sz)]),
     "gnn_softmax_ce": (_i32, [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gnn_sgd": (_i32, [_vp, _vp, _i64, _f32, _vp]),
+    "gnn_model_sync_shadow": (_i32, [_P(Model), _vp]),
     "gnn_train_step_layout": (_i32, [_P(Model), _i64, _i64, _P(StepLayout)]),
     "gnn_train_step_workspace_size": (_i32, [_P(Model), _i64, _i64, _P(_sz)]),
     "gnn_train_step_workspace_init": (_i32, [_P(Model), _i64, _i64, _vp, _sz, _vp]),
@@ -307,11 +308,13 @@ def sgd(w: torch.Tensor, dw: torch.Tensor, lr: float, stream=None) -> torch.Tens
 # ---------------------------------------------------------------------------
 
 class Trainer:
-    """Owns the model buffers (fp32 master weights, gradients) and the step
-    workspace, and calls gnn_train_step."""
+    """Owns the model buffers (fp32 master weights, gradients, and for bf16
+    models the bf16 W^T shadows) and the step workspace, and calls
+    gnn_train_step."""
 
     def __init__(self, kind: int, dims: Sequence[int], fanouts: Sequence[int], precision: int, graph_n: int,
-                 batch: int, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor], device="cuda"):
+                 batch: int, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor], device="cuda",
+                 shadows: bool = True):
         L = len(dims) - 1
         assert len(fanouts) == L and len(weights) == L and len(biases) == L
         self.device = torch.device(device)
@@ -329,7 +332,14 @@ class Trainer:
             m.fanouts[i] = k
         for l in range(L):
             m.w[l], m.b[l], m.dw[l], m.db[l] = _ptr(self.w[l]), _ptr(self.b[l]), _ptr(self.dw[l]), _ptr(self.db[l])
+        self.wt = []
+        if shadows and precision == GNN_BF16:
+            self.wt = [torch.empty((w.shape[1], w.shape[0]), dtype=torch.bfloat16, device=self.device) for w in self.w]
+            for l in range(L):
+                m.wt[l] = _ptr(self.wt[l])
         self.model = m
+        if self.wt:
+            _check(lib().gnn_model_sync_shadow(ctypes.byref(m), _stream(None)))
         self.layout = StepLayout()
         _check(lib().gnn_train_step_layout(ctypes.byref(m), graph_n, batch, ctypes.byref(self.layout)))
         self.ws = _aligned_empty(self.layout.total_bytes, self.device)

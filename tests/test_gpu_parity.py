@@ -531,3 +531,53 @@ def test_train_step_is_bitwise_reproducible():
             outs.append([t.cpu().clone() for t in tr.w + tr.b] + [tr.loss.cpu().clone()])
     for a, b in zip(outs[0], outs[1]):
         assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+# ---------------------------------------------------------------------------
+# bf16 W^T shadows
+# ---------------------------------------------------------------------------
+
+def _shadow_bits(w: torch.Tensor) -> np.ndarray:
+    return oracle.f32_to_bf16_bits(np.ascontiguousarray(w.cpu().numpy().T))
+
+
+def test_model_sync_shadow_is_rne_transpose():
+    rng = np.random.default_rng(5)
+    dims = (100, 256, 47)
+    ws = [torch.from_numpy(rng.standard_normal((2 * dims[l], dims[l + 1])).astype(np.float32)) for l in range(2)]
+    ws[0][0, :4] = torch.tensor([float("nan"), float("inf"), -0.0, 1.0 + 2.0 ** -8])  # NaN, inf, sign, tie
+    bs = [torch.zeros(dims[l + 1]) for l in range(2)]
+    tr = gnn.Trainer(gnn.GNN_AGG_SAGE_MEAN, dims, (25, 10), gnn.GNN_BF16, 1000, 64, ws, bs, device=DEV)
+    torch.cuda.synchronize()
+    for l in range(2):
+        got = tr.wt[l].cpu().view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(got, _shadow_bits(tr.w[l]))
+
+
+def test_train_step_keeps_shadows_and_matches_unshadowed_step():
+    # the shadow gives the GEMMs the same bf16 operands as rounding W on load,
+    # so a step with shadows is bitwise the step without them; after SGD the
+    # shadows equal bf16(W_new^T)
+    dims, fan, n, m, batch = (100, 256, 47), (25, 10), 30_000, 400_000, 512
+    rowptr, col = workloads.rmat_graph(n, m, seed=0)
+    table = workloads.features(n, dims[0], seed=0).to(DEV)
+    labels = workloads.labels(n, dims[-1], seed=0).to(DEV)
+    perm = workloads.target_batches(n, batch, seed=0)
+    ws = [workloads.glorot(2 * dims[l], dims[l + 1], 0, l) for l in range(2)]
+    bs = [torch.zeros(dims[l + 1]) for l in range(2)]
+    g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
+    runs = []
+    for shadows in (True, False):
+        tr = gnn.Trainer(gnn.GNN_AGG_SAGE_MEAN, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV,
+                         shadows=shadows)
+        assert bool(tr.wt) == shadows
+        for s in range(3):
+            tr.step(g, table, labels, workloads.targets_for_step(perm, batch, s).to(DEV), seed=0, step=s, lr=0.05)
+        torch.cuda.synchronize()
+        if shadows:
+            for l in range(2):
+                got = tr.wt[l].cpu().view(torch.int16).numpy().view(np.uint16)
+                assert np.array_equal(got, _shadow_bits(tr.w[l])), l
+        runs.append([t.cpu().clone() for t in tr.w + tr.b + tr.dw] + [tr.loss.cpu().clone()])
+    for a, b in zip(runs[0], runs[1]):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
