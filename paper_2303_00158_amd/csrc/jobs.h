@@ -1,0 +1,49 @@
+// Jobs: the body of a kernel as a value that knows how to run one logical
+// workgroup, so that one launch can serve two independent pieces of work.
+//
+// A job type J has `__device__ void run(int64_t blk, int64_t nblk) const`,
+// which does the work of logical workgroup blk out of nblk (256 threads).
+// job2_kernel gives the first workgroups of the grid to one job and the
+// rest to another.  Merging independent steps this way saves a launch and
+// lets the latencies of the two overlap; every job runs with the launch
+// bounds of 256 threads, and the LDS of both is reserved.
+#pragma once
+
+#include "internal.h"
+
+namespace gnn {
+
+template <class J>
+__global__ void __launch_bounds__(256) job_kernel(J j) {
+    j.run(blockIdx.x, gridDim.x);
+}
+
+// Workgroups [0, na) run a, [na_pad, grid) run b; na_pad (a multiple of 8)
+// keeps b's logical workgroup index congruent to its physical one modulo the
+// XCD count, which jobs that map work to XCDs rely on.
+template <class A, class B>
+__global__ void __launch_bounds__(256) job2_kernel(A a, unsigned na, unsigned na_pad, B b) {
+    if (blockIdx.x < na_pad) {
+        if (blockIdx.x < na) a.run(blockIdx.x, na);
+    } else {
+        b.run(blockIdx.x - na_pad, gridDim.x - na_pad);
+    }
+}
+
+template <class J>
+gnn_status launch_job(const J &j, unsigned grid, hipStream_t s, const char *what) {
+    if (grid == 0) return GNN_OK;
+    job_kernel<J><<<grid, 256, 0, s>>>(j);
+    return launch_status(what);
+}
+
+template <class A, class B>
+gnn_status launch_job2(const A &a, unsigned na, const B &b, unsigned nb, hipStream_t s, const char *what) {
+    if (na == 0) return launch_job(b, nb, s, what);
+    if (nb == 0) return launch_job(a, na, s, what);
+    const unsigned pad = (na + 7) / 8 * 8;
+    job2_kernel<A, B><<<pad + nb, 256, 0, s>>>(a, na, pad, b);
+    return launch_status(what);
+}
+
+}  // namespace gnn

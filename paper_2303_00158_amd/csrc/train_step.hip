@@ -10,7 +10,10 @@
 #include <algorithm>
 #include <mutex>
 
+#include "gather_dev.h"
 #include "internal.h"
+#include "jobs.h"
+#include "sampler_dev.h"
 
 namespace gnn {
 
@@ -71,15 +74,18 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
     Carver c(nullptr);
     // capacities per hop
     int64_t cap_dst = batch;
-    size_t samp = 0;
+    size_t hop_max = 0;
     for (int h = 0; h < L; ++h) {
         const int64_t k = m->fanouts[h];
         o->cap_dst[h] = cap_dst;
         o->cap_nnz[h] = cap_dst * k;
         o->cap_src[h] = std::min<int64_t>(cap_dst + cap_dst * k, std::max<int64_t>(graph_n, cap_dst));
-        samp = std::max(samp, sampler_ws_bytes(graph_n, cap_dst, static_cast<int32_t>(k)));
+        hop_max = std::max(hop_max, sampler_hop_bytes(graph_n, cap_dst, static_cast<int32_t>(k)));
         cap_dst = o->cap_src[h];
     }
+    // the shared part and two hop scratch regions: consecutive hops overlap
+    // (relabel of one hop runs with the prepare of the next)
+    const size_t samp = sampler_shared_bytes(graph_n) + 2 * hop_max;
     o->sampler_ws = c.take(samp);
     o->sampler_ws_bytes = samp;
     for (int h = 0; h < L; ++h) {
@@ -148,25 +154,57 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     std::lock_guard<std::mutex> lock(g_helper_mu);
     Helper *hp = nullptr;
     if (L > 1) GNN_TRY(helper_for_current_device(&hp));
-    // sampling: hop 1 around the targets, then outwards; the transposes of
-    // all blocks but the last go to the helper stream
+
+    // sampling: hop 1 around the targets, then outwards.  Hop h's relabel
+    // shares a launch with hop h+1's prepare (both only need hop h's
+    // sources), and the last hop's relabel shares one with the gather.  The
+    // transposes of all blocks but the last run on the helper stream.
+    char *shared = base + o.sampler_ws;
+    size_t hop_max = 0;
+    for (int h = 0; h < L; ++h)
+        hop_max = std::max(hop_max, sampler_hop_bytes(g->n, o.cap_dst[h], m->fanouts[h]));
+    samp::HopPlan plan[GNN_MAX_LAYERS];
     for (int h = 0; h < L; ++h) {
         const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
         const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
+        void *scratch = shared + sampler_shared_bytes(g->n) + (h % 2) * hop_max;
         void *csc_ws = h < L - 1 ? base + o.blk_csc_ws[h] : nullptr;
-        GNN_TRY(launch_build_block(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h],
-                                   seed, step, h + 1, &blk[h], base + o.sampler_ws, csc_ws, s));
-        if (csc_ws) {
-            GNN_HIP(hipEventRecord(hp->fork[h], s));
-            GNN_HIP(hipStreamWaitEvent(hp->stream, hp->fork[h], 0));
-            GNN_TRY(launch_block_csc(&blk[h], csc_ws, o.cap_nnz[h], hp->stream));
-        }
+        plan[h] = plan_hop(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h], seed, step,
+                           h + 1, &blk[h], shared, scratch, csc_ws);
+    }
+    auto fork_csc = [&](int h) -> gnn_status {
+        GNN_HIP(hipEventRecord(hp->fork[h], s));
+        GNN_HIP(hipStreamWaitEvent(hp->stream, hp->fork[h], 0));
+        return launch_block_csc(&blk[h], base + o.blk_csc_ws[h], o.cap_nnz[h], hp->stream);
+    };
+    GNN_TRY(launch_hop_prepare(plan[0], s));
+    GNN_TRY(launch_hop_emit(plan[0], s));
+    for (int h = 1; h < L; ++h) {
+        gnn_status st = GNN_OK;
+        samp::with_prepare_job(plan[h], [&](auto job) {
+            st = launch_job2(samp::RelabelJob{plan[h - 1].a}, plan[h - 1].relabel_grid, job, plan[h].prep_grid, s,
+                             "hop_relabel+prepare");
+        });
+        GNN_TRY(st);
+        GNN_TRY(fork_csc(h - 1));
+        GNN_TRY(launch_hop_emit(plan[h], s));
     }
     if (hp) GNN_HIP(hipEventRecord(hp->join, hp->stream));
-    // feature loading: rows of the input layer's sources
+    // feature loading (rows of the input layer's sources) with the last
+    // hop's relabel
     const gnn_block &b0 = blk[L - 1];
     void *x0 = base + o.x0;
-    GNN_TRY(launch_gather(table, tdt, m->dims[0], row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, x0, act, s));
+    {
+        const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0], x0};
+        const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act));
+        gnn_status st = GNN_OK;
+        const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
+            st = launch_job2(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid, job, ggrid, s,
+                             "hop_relabel+gather");
+        });
+        GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
+        GNN_TRY(st);
+    }
 
     // forward
     for (int l = 1; l <= L; ++l) {
