@@ -7,283 +7,30 @@
 // two slots of 25 lanes), and the slot partial sums are folded with lane
 // shuffles at the end.  Up to 64 neighbour indices and weights of the row are
 // held one per lane and broadcast with shuffles.  Sums are fp32.
-#include "internal.h"
+#include "aggregate_dev.h"
+#include "jobs.h"
 
 namespace gnn {
-
-namespace {
-
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-
-// Elements e0 .. e0+3 of a row starting at row_off (zero past f).  Loads are
-// issued unconditionally from in-bounds addresses and masked afterwards.
-template <bool VEC, class T>
-__device__ __forceinline__ float4 load_chunk(const T *p, int64_t row_off, int64_t e0, int64_t f) {
-    if constexpr (VEC) return load4(p, row_off + e0);
-    float v[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const bool ok = e0 + q < f;
-        const float x = Elem<T>::load(p, row_off + (ok ? e0 + q : f - 1));
-        v[q] = ok ? x : 0.f;
-    }
-    return make_float4(v[0], v[1], v[2], v[3]);
-}
-
-template <bool VEC, class T>
-__device__ __forceinline__ void store_chunk(T *p, int64_t row_off, int64_t e0, int64_t f, float4 v) {
-    if constexpr (VEC) {
-        store4(p, row_off + e0, v);
-        return;
-    }
-    const float a[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-        if (e0 + q < f) Elem<T>::store(p, row_off + e0 + q, a[q]);
-}
-
-__device__ __forceinline__ void fma4(float4 &acc, float w, const float4 &v) {
-    acc.x = fmaf(w, v.x, acc.x);
-    acc.y = fmaf(w, v.y, acc.y);
-    acc.z = fmaf(w, v.z, acc.z);
-    acc.w = fmaf(w, v.w, acc.w);
-}
-
-__device__ __forceinline__ float4 shfl4(const float4 &v, int src) {
-    return make_float4(__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64));
-}
-
-// Accumulate sum_{t in this lane's slot} w_t * x[idx_t][chunk] over one
-// window of up to 64 (index, weight) pairs held one per lane.  Every lane runs
-// the same number of iterations so the shuffles stay convergent.  Lanes past
-// the window hold index 0 (a valid row) and the loads are issued
-// unconditionally; invalid terms are masked to zero before the FMA.  The
-// caller passes an in-row chunk offset for inactive lanes.
-template <bool VEC, class T>
-__device__ __forceinline__ void window_accumulate(float4 &acc, const T *x, int64_t stride, int64_t col_off,
-                                                  int64_t f, int32_t my_idx, float my_w, int wn, int slot, int S,
-                                                  bool active, int64_t e0) {
-    for (int tb = 0; tb < wn; tb += 4 * S) {
-        int32_t j[4];
-        float w[4];
-        bool ok[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int t = tb + q * S + slot;
-            ok[q] = active && (t < wn);
-            j[q] = __shfl(my_idx, t & 63, 64);
-            w[q] = __shfl(my_w, t & 63, 64);
-        }
-        float4 v[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = load_chunk<VEC>(x, static_cast<int64_t>(j[q]) * stride + col_off, e0, f);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float wq = ok[q] ? w[q] : 0.f;
-            const float4 vq = ok[q] ? v[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-            fma4(acc, wq, vq);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// forward
-// ---------------------------------------------------------------------------
-template <int KIND, class TIn, class TOut, bool VEC>
-__global__ void __launch_bounds__(kThreads) agg_fwd_kernel(const int64_t *__restrict__ counts,
-                                                            const int64_t *__restrict__ rowptr,
-                                                            const int32_t *__restrict__ col,
-                                                            const float *__restrict__ src_norm,
-                                                            const TIn *__restrict__ h, int64_t f, int C, int S,
-                                                            TOut *__restrict__ out) {
-    const int lane = threadIdx.x & 63;
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
-    if (row >= counts[0]) return;
-    const int64_t beg = rowptr[row], end = rowptr[row + 1];
-    const int64_t deg = end - beg;
-    const float wi = (KIND == GNN_AGG_GCN_SYM) ? src_norm[row] : 1.f;
-    const int groups = (C + 63) / 64;
-    const int slot = (S > 1) ? lane / C : 0;
-    for (int g = 0; g < groups; ++g) {
-        const int chunk = (S > 1) ? lane % C : g * 64 + lane;
-        const bool active = (S > 1) ? (slot < S) : (chunk < C);
-        const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int64_t wb = beg; wb < end; wb += 64) {
-            const int wn = static_cast<int>(min<int64_t>(64, end - wb));
-            int32_t my_idx = 0;
-            float my_w = 0.f;
-            if (lane < wn) {
-                my_idx = col[wb + lane];
-                my_w = (KIND == GNN_AGG_GCN_SYM) ? wi * src_norm[my_idx] : 1.f;
-            }
-            window_accumulate<VEC>(acc, h, f, 0, f, my_idx, my_w, wn, slot, S, active, e0);
-        }
-        // fold the slots into slot 0
-        for (int s2 = 1; s2 < S; ++s2) {
-            const float4 o = shfl4(acc, lane + s2 * C);
-            if (slot == 0) {
-                acc.x += o.x;
-                acc.y += o.y;
-                acc.z += o.z;
-                acc.w += o.w;
-            }
-        }
-        if (slot != 0 || !active) continue;
-        if (KIND == GNN_AGG_SAGE_MEAN) {
-            if (deg > 0) {
-                const float d = static_cast<float>(deg);
-                acc.x /= d;
-                acc.y /= d;
-                acc.z /= d;
-                acc.w /= d;
-            }
-        } else {
-            const float ws = wi * wi;
-            fma4(acc, ws, load_chunk<VEC>(h, row * f, e0, f));
-        }
-        store_chunk<VEC>(out, row * f, e0, f, acc);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// backward: d_src[j] = self(j) + sum_{i in csc(j)} w_ij d_a[i, nbr part]
-// ---------------------------------------------------------------------------
-template <int KIND, class THB, bool VEC>
-__global__ void __launch_bounds__(kThreads) agg_bwd_kernel(const int64_t *__restrict__ counts,
-                                                            const int64_t *__restrict__ rowptr,
-                                                            const int64_t *__restrict__ cscptr,
-                                                            const int32_t *__restrict__ cscrow,
-                                                            const float *__restrict__ src_norm,
-                                                            const float *__restrict__ d_a, int64_t f, int C, int S,
-                                                            const THB *__restrict__ h_below,
-                                                            float *__restrict__ d_src) {
-    const int lane = threadIdx.x & 63;
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
-    const int64_t n_dst = counts[0];
-    if (j >= counts[1]) return;
-    const int64_t ka = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * f : f;
-    const int64_t nbr_off = (KIND == GNN_AGG_SAGE_MEAN) ? f : 0;
-    const int64_t beg = cscptr[j], end = cscptr[j + 1];
-    const float wj = (KIND == GNN_AGG_GCN_SYM) ? src_norm[j] : 1.f;
-    const int groups = (C + 63) / 64;
-    const int slot = (S > 1) ? lane / C : 0;
-    for (int g = 0; g < groups; ++g) {
-        const int chunk = (S > 1) ? lane % C : g * 64 + lane;
-        const bool active = (S > 1) ? (slot < S) : (chunk < C);
-        const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int64_t wb = beg; wb < end; wb += 64) {
-            const int wn = static_cast<int>(min<int64_t>(64, end - wb));
-            int32_t my_idx = 0;
-            float my_w = 0.f;
-            if (lane < wn) {
-                my_idx = cscrow[wb + lane];
-                if (KIND == GNN_AGG_GCN_SYM)
-                    my_w = src_norm[my_idx] * wj;
-                else
-                    my_w = 1.f / static_cast<float>(rowptr[my_idx + 1] - rowptr[my_idx]);
-            }
-            window_accumulate<VEC>(acc, d_a, ka, nbr_off, f, my_idx, my_w, wn, slot, S, active, e0);
-        }
-        for (int s2 = 1; s2 < S; ++s2) {
-            const float4 o = shfl4(acc, lane + s2 * C);
-            if (slot == 0) {
-                acc.x += o.x;
-                acc.y += o.y;
-                acc.z += o.z;
-                acc.w += o.w;
-            }
-        }
-        if (slot != 0 || !active) continue;
-        if (j < n_dst) {
-            const float ws = (KIND == GNN_AGG_GCN_SYM) ? wj * wj : 1.f;
-            fma4(acc, ws, load_chunk<VEC>(d_a, j * ka, e0, f));
-        }
-        if (h_below) {
-            const float4 hb = load_chunk<VEC>(h_below, j * f, e0, f);
-            if (!(hb.x > 0.f)) acc.x = 0.f;
-            if (!(hb.y > 0.f)) acc.y = 0.f;
-            if (!(hb.z > 0.f)) acc.z = 0.f;
-            if (!(hb.w > 0.f)) acc.w = 0.f;
-        }
-        store_chunk<VEC>(d_src, j * f, e0, f, acc);
-    }
-}
-
-void split_row(int64_t f, int *C, int *S) {
-    const int64_t c = ceil_div(f, 4);
-    *C = static_cast<int>(c);
-    *S = (c <= 32) ? static_cast<int>(64 / c) : 1;
-}
-
-unsigned row_grid(int64_t rows) {
-    return static_cast<unsigned>(ceil_div(rows > 0 ? rows : 1, kWaves));
-}
-
-template <int KIND>
-gnn_status fwd_dispatch(const gnn_block *b, const void *h, int hdt, int64_t f, void *out, int odt, hipStream_t s) {
-    int C, S;
-    split_row(f, &C, &S);
-    const bool vec = (f % 4 == 0) && aligned(h, 4 * dtype_size(hdt)) && aligned(out, 4 * dtype_size(odt));
-    const unsigned grid = row_grid(b->cap_dst);
-#define AGG_FWD_V(TI, TO, V)                                                                                  \
-    agg_fwd_kernel<KIND, TI, TO, V><<<grid, kThreads, 0, s>>>(b->counts, b->rowptr, b->col, b->src_norm,      \
-                                                             static_cast<const TI *>(h), f, C, S,            \
-                                                             static_cast<TO *>(out))
-#define AGG_FWD(TI, TO)                 \
-    do {                                \
-        if (vec) AGG_FWD_V(TI, TO, true);  \
-        else AGG_FWD_V(TI, TO, false);     \
-    } while (0)
-    if (hdt == GNN_F32 && odt == GNN_F32) AGG_FWD(float, float);
-    else if (hdt == GNN_F32 && odt == GNN_BF16) AGG_FWD(float, uint16_t);
-    else if (hdt == GNN_BF16 && odt == GNN_F32) AGG_FWD(uint16_t, float);
-    else if (hdt == GNN_BF16 && odt == GNN_BF16) AGG_FWD(uint16_t, uint16_t);
-    else return fail(GNN_EUNSUPPORTED, "aggregate_fwd: unsupported dtypes %d -> %d", hdt, odt);
-#undef AGG_FWD
-#undef AGG_FWD_V
-    GNN_LAUNCHED("aggregate_fwd");
-    return GNN_OK;
-}
-
-template <int KIND>
-gnn_status bwd_dispatch(const gnn_block *b, const float *d_a, int64_t f, const void *h_below, int hbdt, float *d_src,
-                        hipStream_t s) {
-    int C, S;
-    split_row(f, &C, &S);
-    const bool vec = (f % 4 == 0) && aligned(d_a, 16) && aligned(d_src, 16) &&
-                     (!h_below || aligned(h_below, 4 * dtype_size(hbdt)));
-    const unsigned grid = row_grid(b->cap_src);
-#define AGG_BWD(THB, V)                                                                                        \
-    agg_bwd_kernel<KIND, THB, V><<<grid, kThreads, 0, s>>>(b->counts, b->rowptr, b->cscptr, b->cscrow,         \
-                                                           b->src_norm, d_a, f, C, S,                          \
-                                                           static_cast<const THB *>(h_below), d_src)
-    if (!h_below || hbdt == GNN_F32) {
-        if (vec) AGG_BWD(float, true); else AGG_BWD(float, false);
-    } else {
-        if (vec) AGG_BWD(uint16_t, true); else AGG_BWD(uint16_t, false);
-    }
-#undef AGG_BWD
-    GNN_LAUNCHED("aggregate_bwd");
-    return GNN_OK;
-}
-
-}  // namespace
 
 gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
                                 hipStream_t s) {
     if (b->cap_dst == 0 || f == 0) return GNN_OK;
-    if (kind == GNN_AGG_SAGE_MEAN) return fwd_dispatch<GNN_AGG_SAGE_MEAN>(b, h, hdt, f, out, odt, s);
-    return fwd_dispatch<GNN_AGG_GCN_SYM>(b, h, hdt, f, out, odt, s);
+    gnn_status st = GNN_OK;
+    const bool ok = agg::with_fwd_job(b, kind, h, hdt, f, out, odt, [&](auto job) {
+        st = launch_job(job, agg::row_grid(b->cap_dst), s, "aggregate_fwd");
+    });
+    if (!ok) return fail(GNN_EUNSUPPORTED, "aggregate_fwd: unsupported dtypes %d -> %d", hdt, odt);
+    return st;
 }
 
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
                                 int hbdt, float *d_src, hipStream_t s) {
     if (b->cap_src == 0 || f == 0) return GNN_OK;
-    if (kind == GNN_AGG_SAGE_MEAN) return bwd_dispatch<GNN_AGG_SAGE_MEAN>(b, d_a, f, h_below, hbdt, d_src, s);
-    return bwd_dispatch<GNN_AGG_GCN_SYM>(b, d_a, f, h_below, hbdt, d_src, s);
+    gnn_status st = GNN_OK;
+    agg::with_bwd_job(b, kind, d_a, f, h_below, hbdt, d_src, [&](auto job) {
+        st = launch_job(job, agg::row_grid(b->cap_src), s, "aggregate_bwd");
+    });
+    return st;
 }
 
 }  // namespace gnn

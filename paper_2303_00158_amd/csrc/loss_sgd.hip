@@ -1,65 +1,12 @@
 // Loss against the ground truth (mean softmax cross-entropy over the target
 // rows, fused forward and gradient), the SGD step, and small helpers of the
 // training step.  Reductions run in a fixed order (no atomics).
-#include "internal.h"
+#include "jobs.h"
+#include "loss_dev.h"
 
 namespace gnn {
 
 namespace {
-
-constexpr int kThreads = 256;
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
-// One wavefront per target row.
-__global__ void __launch_bounds__(kThreads) softmax_ce_kernel(const float *__restrict__ z, int64_t b, int64_t c,
-                                                               const int64_t *__restrict__ labels,
-                                                               const int64_t *__restrict__ targets,
-                                                               float *__restrict__ g, float *__restrict__ row_loss) {
-    const int lane = threadIdx.x & 63;
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
-    if (i >= b) return;
-    const float *zi = z + i * c;
-    float mx = -INFINITY;
-    for (int64_t k = lane; k < c; k += 64) mx = fmaxf(mx, zi[k]);
-    mx = wave_max(mx);
-    float s = 0.f;
-    for (int64_t k = lane; k < c; k += 64) s += expf(zi[k] - mx);
-    s = wave_sum(s);
-    const float lse = mx + logf(s);
-    const int64_t y = labels[targets ? targets[i] : i];
-    const float inv_b = 1.f / static_cast<float>(b);
-    for (int64_t k = lane; k < c; k += 64) {
-        const float p = expf(zi[k] - lse);
-        g[i * c + k] = (p - (k == y ? 1.f : 0.f)) * inv_b;
-    }
-    if (lane == 0) row_loss[i] = lse - zi[y];
-}
-
-// Single block: loss = (sum of row losses) / b in a fixed order.
-__global__ void __launch_bounds__(kThreads) loss_reduce_kernel(const float *__restrict__ row_loss, int64_t b,
-                                                                float *__restrict__ loss) {
-    __shared__ float sh[kThreads / 64];
-    float s = 0.f;
-    for (int64_t i = threadIdx.x; i < b; i += kThreads) s += row_loss[i];
-    s = wave_sum(s);
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = s;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float t = 0.f;
-        for (int w = 0; w < kThreads / 64; ++w) t += sh[w];
-        *loss = b > 0 ? t / static_cast<float>(b) : 0.f;
-    }
-}
 
 __global__ void zero_words_kernel(uint32_t *p, int64_t n) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
@@ -80,14 +27,10 @@ size_t softmax_ce_ws_bytes(int64_t b) { return round_up(static_cast<size_t>(b > 
 gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels,
                              const int64_t *targets, float *g_out, float *loss_out, void *ws, hipStream_t s) {
     float *row_loss = static_cast<float *>(ws);
-    if (b > 0) {
-        softmax_ce_kernel<<<static_cast<unsigned>(ceil_div(b, kThreads / 64)), kThreads, 0, s>>>(
-            logits, b, c, labels, targets, g_out, row_loss);
-        GNN_LAUNCHED("softmax_ce");
-    }
-    loss_reduce_kernel<<<1, kThreads, 0, s>>>(row_loss, b, loss_out);
-    GNN_LAUNCHED("loss_reduce");
-    return GNN_OK;
+    if (b > 0)
+        GNN_TRY(launch_job(loss::SoftmaxJob{logits, b, c, labels, targets, g_out, row_loss},
+                           static_cast<unsigned>(ceil_div(b, loss::kThreads / 64)), s, "softmax_ce"));
+    return launch_job(loss::LossReduceJob{row_loss, b, loss_out}, 1, s, "loss_reduce");
 }
 
 gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s) {

@@ -10,26 +10,17 @@
 #include <algorithm>
 #include <mutex>
 
+#include "aggregate_dev.h"
 #include "gather_dev.h"
+#include "gemm_bwd_dev.h"
 #include "internal.h"
 #include "jobs.h"
+#include "loss_dev.h"
 #include "sampler_dev.h"
 
 namespace gnn {
 
 namespace {
-
-__global__ void step_tail_kernel(const int64_t *c0, const int64_t *c1, const int64_t *c2, const int64_t *c3,
-                                 const float *loss_src, int64_t *edges, int64_t *edges_out, float *loss_out) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int64_t e = c0[2];
-    if (c1) e += c1[2];
-    if (c2) e += c2[2];
-    if (c3) e += c3[2];
-    *edges = e;
-    if (edges_out) *edges_out = e;
-    if (loss_out) *loss_out = *loss_src;
-}
 
 // One helper stream and its events per device, created on first use and
 // kept until the process ends.  g_helper_mu serialises training-step
@@ -218,33 +209,55 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
                                   m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l],
                                   l < L ? act : GNN_F32, base + o.fwd_ws, s));
     }
-    // loss on the targets
-    float *loss_slot = reinterpret_cast<float *>(base + o.loss);
-    GNN_TRY(launch_softmax_ce(reinterpret_cast<const float *>(base + o.h[L]), batch, m->dims[L], labels, targets,
-                              reinterpret_cast<float *>(base + o.grad[L]), loss_slot, base + o.loss_ws, s));
-    // backward (reads the transposes)
+    // loss on the targets: gradient and row losses now, the mean with the
+    // last kernel of the step
+    float *row_loss = reinterpret_cast<float *>(base + o.loss_ws);
+    GNN_TRY(launch_job(loss::SoftmaxJob{reinterpret_cast<const float *>(base + o.h[L]), batch, m->dims[L], labels,
+                                        targets, reinterpret_cast<float *>(base + o.grad[L]), row_loss},
+                       static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64)), s, "softmax_ce"));
+    // backward (reads the transposes).  Per layer: the dA and dW GEMMs in
+    // one launch, then the dW reduction (with SGD on W^l, b^l and the
+    // shadow) in one launch with the aggregation backward of the layer, or
+    // with the end of the step for layer 1.  Every later step reads only
+    // lower layers' weights.
     if (hp) GNN_HIP(hipStreamWaitEvent(s, hp->join, 0));
+    loss::TailJob tail{};
+    for (int h = 0; h < L; ++h) tail.counts[h] = blk[h].counts;
+    tail.num_blocks = L;
+    tail.row_loss = row_loss;
+    tail.b = batch;
+    tail.loss = reinterpret_cast<float *>(base + o.loss);
+    tail.loss_out = loss_dev;
+    tail.edges = reinterpret_cast<int64_t *>(base + o.edges);
+    tail.edges_out = edges_dev;
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);
-        const void *agg = base + o.agg[l];
+        const void *agg_out = base + o.agg[l];
         const int64_t f_in = m->dims[l - 1];
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         float *d_a = l > 1 ? reinterpret_cast<float *>(base + o.d_a[l]) : nullptr;
-        // the weight gradient kernel also applies SGD to W^l and b^l: every
-        // later backward step reads only lower layers' weights
-        GNN_TRY(launch_update_bwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst,
-                                  m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l],
-                                  m->precision, m->dw[l - 1], m->db[l - 1], d_a, base + o.bwd_ws, m->w[l - 1],
-                                  m->b[l - 1], m->wt[l - 1], lr, s));
-        if (l > 1)
-            GNN_TRY(launch_aggregate_bwd(&b, m->kind, d_a, f_in, hin, act,
-                                         reinterpret_cast<float *>(base + o.grad[l - 1]), s));
+        const gbwd::Args a{sage ? hin : agg_out, sage ? agg_out : nullptr, act, f_in, b.counts, b.cap_dst,
+                           m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l], m->precision,
+                           m->dw[l - 1], m->db[l - 1], d_a, reinterpret_cast<float *>(base + o.bwd_ws), m->w[l - 1],
+                           m->b[l - 1], m->wt[l - 1], lr};
+        const gbwd::Plan p = gbwd::plan(a);
+        GNN_TRY(launch_update_bwd_gemms(a, p, s));
+        gnn_status st = GNN_OK;
+        if (l > 1) {
+            float *d_src = reinterpret_cast<float *>(base + o.grad[l - 1]);
+            agg::with_bwd_job(&b, m->kind, d_a, f_in, hin, act, d_src, [&](auto aj) {
+                gbwd::with_reduce_job(a, p, [&](auto rj) {
+                    st = launch_job2(rj, p.red_grid, aj, agg::row_grid(b.cap_src), s, "update_dw_reduce+aggregate_bwd");
+                });
+            });
+        } else {
+            gbwd::with_reduce_job(a, p, [&](auto rj) {
+                st = launch_job2(rj, p.red_grid, tail, 1, s, "update_dw_reduce+step_tail");
+            });
+        }
+        GNN_TRY(st);
     }
-    step_tail_kernel<<<1, 64, 0, s>>>(blk[0].counts, L > 1 ? blk[1].counts : nullptr, L > 2 ? blk[2].counts : nullptr,
-                                      L > 3 ? blk[3].counts : nullptr, loss_slot,
-                                      reinterpret_cast<int64_t *>(base + o.edges), edges_dev, loss_dev);
-    GNN_LAUNCHED("step_tail");
     return GNN_OK;
 }
 
