@@ -20,8 +20,9 @@
 // The shapes of a sampled mini-batch are small, so every kernel here is
 // bound by memory latency rather than bandwidth or matrix-core rate.  The
 // engine is written around that:
-//  * a ring of D register stages keeps D chunks of loads in flight while the
-//    matrix cores work on an earlier chunk;
+//  * a ring of two register stages keeps two chunks of loads in flight while
+//    the matrix cores work on an earlier one (deeper rings measured slower:
+//    more code and registers for the same latency);
 //  * every global load is issued from a clamped, in-bounds address with no
 //    per-element branch, so a chunk's loads issue back to back;
 //  * epilogue operands (bias, the weights an SGD step updates) are loaded
@@ -476,7 +477,7 @@ inline int pick_tile(int64_t rows, int64_t cols) {
 }
 
 // Register stages in flight per tile size.
-template <int TILE> constexpr int depth() { return TILE == 64 ? 3 : 2; }
+template <int TILE> constexpr int depth() { return TILE == 64 ? 2 : 1; }
 
 // Workgroup -> output tile mapping.  Workgroups are dealt round-robin to
 // the 8 XCDs (each with its own L2).  With at least 8 row tiles,
