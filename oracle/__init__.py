@@ -341,14 +341,39 @@ def sample_blocks(rowptr, col, targets, cfg: StepConfig) -> List[Block]:
     return blocks
 
 
+def _flip_decisions(h: np.ndarray, flip: np.ndarray) -> np.ndarray:
+    """Copy of stored activations h whose test h > 0 is inverted where flip
+    is True (values elsewhere unchanged).  Only the backward ReLU mask reads
+    the copy."""
+    hv = to_float64(h)
+    f = np.asarray(flip, dtype=bool)
+    assert f.shape == hv.shape
+    out = np.array(h, copy=True)
+    off = f & (hv > 0)
+    on = f & ~(hv > 0)
+    if out.dtype == np.uint16:          # bf16 bits
+        out[off] = 0
+        out[on] = 0x3F80                # 1.0
+    else:
+        out[off] = 0
+        out[on] = 1
+    return out
+
+
 def train_step(rowptr, col, nrm, table, labels, targets, weights, biases, cfg: StepConfig,
-               blocks: Optional[List[Block]] = None) -> dict:
+               blocks: Optional[List[Block]] = None, relu_flip: Optional[dict] = None) -> dict:
     """One iteration of sampled mini-batch training; returns every
     intermediate plus the updated weights.
 
     Storage precision: X', M^l (or A^l) and H^l (l < L) are stored in the
     precision mode (bf16 in bf16 mode); logits, gradients and weights are
     fp32 (fp64 in fp64 mode).  GEMM operands are rounded to bf16 in bf16 mode.
+
+    relu_flip (optional): {l: bool array shaped like H^l} inverting the
+    backward's ReLU decision (H^l > 0) at the marked positions, for parity
+    checks where an implementation that sums in another order takes the other
+    side of a decision whose pre-activation is within rounding of zero.  The
+    forward pass is not changed.
     """
     L = len(cfg.dims) - 1
     assert len(cfg.fanouts) == L and len(weights) == L
@@ -386,7 +411,10 @@ def train_step(rowptr, col, nrm, table, labels, targets, weights, biases, cfg: S
         dW[l], dB[l] = dw, db
         if l > 1:
             f = cfg.dims[l - 1]
-            GR[l - 1] = aggregate_bwd(cfg.kind, blk, src_norms.get(l), da, f, H[l - 1], wide)
+            h_mask = H[l - 1]
+            if relu_flip and (l - 1) in relu_flip:
+                h_mask = _flip_decisions(H[l - 1], relu_flip[l - 1])
+            GR[l - 1] = aggregate_bwd(cfg.kind, blk, src_norms.get(l), da, f, h_mask, wide)
     new_w = [sgd(weights[l - 1], dW[l], cfg.lr) for l in range(1, L + 1)]
     new_b = [sgd(biases[l - 1], dB[l], cfg.lr) for l in range(1, L + 1)]
     return {

@@ -1,0 +1,143 @@
+"""Parity of whole training steps at the full workload sizes, in the launch
+configuration bench.py times (gnn_train_step, bf16 shadows), against the CPU
+oracle on the same inputs.
+
+Sampled blocks (ids, row pointers, columns, transposes) and the edge counts
+must match bit for bit; the loss, dW, db and the updated W within the bf16
+tolerance (2e-2 normwise).  The graphs are generated on the GPU and copied to
+the host for the oracle.
+
+A ReLU decision whose pre-activation is within rounding of zero can go
+either way between an fp32 kernel and the fp64 oracle (both are correct);
+at full size a hub row can carry such a decision, and the flipped gradient
+element then moves a whole column of the layer below's dW.  The tests check
+that every differing decision is ambiguous in that sense, then hold the
+gradients to the tolerance against the oracle's backward with those
+decisions taken the GPU's way.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+gnn = pytest.importorskip("paper_2303_00158_amd.gnn")
+
+DEV = torch.device("cuda:0")
+TOL = 2e-2
+
+
+def relerr(got, want):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    den = max(np.abs(want).max() if want.size else 0.0, 1e-30)
+    return float(np.abs(got - want).max() / den) if want.size else 0.0
+
+
+def _ambiguous_flips(tr, ref, w, w_ref, b_ref, L):
+    """ReLU decisions of hidden layers that differ between the GPU and the
+    oracle.  Each must be ambiguous: the oracle's own fp64 pre-activation
+    lies within 2^-7 * sum_k |A_ik| |W_kj| of zero, the size of a change
+    that one-ulp bf16 differences of the layer's inputs can make.  Returns
+    {l: flip mask} for the oracle's backward."""
+    flips = {}
+    for l in range(1, L):
+        blk = ref["blocks"][L - l]
+        n = blk.n_dst
+        got = tr.tensor("h", l, n, w.dims[l], torch.bfloat16).cpu().view(torch.int16).numpy().view(np.uint16)
+        gpu_on = oracle.to_float64(got) > 0
+        ora_on = oracle.to_float64(ref["H"][l]) > 0
+        f = gpu_on != ora_on
+        if not f.any():
+            continue
+        if w.kind == "sage":
+            a = np.concatenate([oracle.to_float64(ref["H"][l - 1][:n]), oracle.to_float64(ref["AGG"][l])], axis=1)
+        else:
+            a = oracle.to_float64(ref["AGG"][l])
+        wq = oracle.to_float64(oracle.f32_to_bf16_bits(w_ref[l - 1]))
+        z = a @ wq + np.asarray(b_ref[l - 1], dtype=np.float64)
+        rows, cols = np.nonzero(f)
+        scale = np.abs(a[rows]) @ np.abs(wq)
+        bound = 2.0 ** -7 * scale[np.arange(rows.size), cols]
+        assert np.all(np.abs(z[rows, cols]) <= bound), ("unambiguous ReLU decision differs", l,
+                                                        np.abs(z[rows, cols]).max(), bound.min())
+        print(f"[fullsize] layer {l}: {rows.size} ReLU decisions within rounding of zero taken the GPU's way",
+              flush=True)
+        flips[l] = f
+    return flips
+
+
+def _run(w: workloads.Workload, steps: int, check_x0_rows: int = 0):
+    print(f"[fullsize] {w.name}: generating n={w.n} m={w.m}", flush=True)
+    rowptr, col = workloads.make_graph(w, device=DEV)
+    graph = gnn.DeviceGraph(rowptr, col)
+    table = workloads.features(w.n, w.dims[0], seed=w.seed, device=DEV)
+    labels = workloads.labels(w.n, w.num_classes, seed=w.seed, device=DEV)
+    perm = workloads.target_batches(w.n, w.batch, seed=w.seed, device=DEV)
+    L = w.num_layers
+    weights = [workloads.glorot(w.k_of_layer(l + 1), w.dims[l + 1], w.seed, l) for l in range(L)]
+    biases = [torch.zeros(w.dims[l + 1]) for l in range(L)]
+    kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+    nrm = gnn.gcn_norm(graph)
+    tr = gnn.Trainer(kind, w.dims, w.fanouts, gnn.GNN_BF16, w.n, w.batch, weights, biases, device=DEV)
+    torch.cuda.synchronize()
+    print("[fullsize] copying inputs to the host", flush=True)
+    rp_h, col_h = rowptr.cpu().numpy(), col.cpu().numpy()
+    table_h, labels_h = table.cpu().numpy(), labels.cpu().numpy()
+    nrm_h = oracle.gcn_norm(rp_h) if w.kind == "gcn" else None
+    w_ref = [x.numpy() for x in weights]
+    b_ref = [x.numpy() for x in biases]
+    okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
+    for s in range(steps):
+        tgt = workloads.targets_for_step(perm, w.batch, s).contiguous()
+        tr.step(graph, table, labels, tgt, w.seed, s, 0.01, gcn_norm_t=nrm)
+        torch.cuda.synchronize()
+        cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oracle.BF16, seed=w.seed,
+                                step=s, lr=0.01)
+        print(f"[fullsize] step {s}: oracle", flush=True)
+        ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt.cpu().numpy(), w_ref, b_ref, cfg)
+        for h in range(1, L + 1):
+            got, want = tr.block_view(h), ref["blocks"][h - 1]
+            assert np.array_equal(got["src_ids"], want.src_ids), (s, h)
+            assert np.array_equal(got["rowptr"], want.rowptr), (s, h)
+            assert np.array_equal(got["col"], want.col), (s, h)
+            if h < L:
+                assert np.array_equal(got["cscptr"], want.cscptr) and np.array_equal(got["cscrow"], want.cscrow)
+        assert int(tr.edges.item()) == ref["edges"]
+        assert abs(tr.loss.item() - ref["loss"]) <= TOL * max(1.0, abs(ref["loss"]))
+        flips = _ambiguous_flips(tr, ref, w, w_ref, b_ref, L)
+        if flips:
+            ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt.cpu().numpy(), w_ref, b_ref, cfg,
+                                    blocks=ref["blocks"], relu_flip=flips)
+        for l in range(1, L + 1):
+            assert relerr(tr.dw[l - 1].cpu().numpy(), ref["dW"][l]) <= TOL, ("dW", s, l)
+            assert relerr(tr.db[l - 1].cpu().numpy(), ref["dB"][l]) <= TOL, ("dB", s, l)
+            assert relerr(tr.w[l - 1].cpu().numpy(), ref["new_w"][l - 1]) <= TOL, ("W", s, l)
+        if check_x0_rows:
+            n0 = ref["x0"].shape[0]
+            x0 = tr.tensor("x0", 0, n0, w.dims[0], torch.bfloat16)
+            got = x0.cpu().view(torch.int16).numpy().view(np.uint16)
+            assert np.array_equal(got, ref["x0"])  # bf16 RNE of the gathered rows, bit for bit
+        print(f"[fullsize] step {s}: ok, {ref['edges']} edges, loss {ref['loss']:.4f}", flush=True)
+        w_ref = [x.cpu().numpy() for x in tr.w]  # continue from the GPU's weights
+        b_ref = [x.cpu().numpy() for x in tr.b]
+
+
+@pytest.mark.timeout(300)
+def test_fullsize_rmat2_4m_sage():
+    _run(workloads.RMAT_SAGE, steps=2, check_x0_rows=1)
+
+
+@pytest.mark.timeout(300)
+def test_fullsize_rmat2_4m_gcn():
+    _run(workloads.RMAT_GCN, steps=2)
+
+
+@pytest.mark.timeout(900)
+def test_fullsize_rmat111m_sage3():
+    # 111M vertices, 1.6B directed edges, 57 GB fp32 table in HBM; the oracle
+    # gets host copies of the graph and table (about 71 GB)
+    _run(workloads.RMAT_SAGE3, steps=1)

@@ -526,3 +526,33 @@ def test_table3_shapes_pin_workload_presets():
     q = rows["ogbn-papers100M"]
     assert (workloads.RMAT_SAGE3.n, workloads.RMAT_SAGE3.m) == (int(q[1]), int(q[2]))
     assert workloads.RMAT_SAGE3.dims[0] == int(q[3]) and workloads.RMAT_SAGE3.dims[-1] == int(q[5])
+
+
+def test_relu_flip_inverts_only_the_marked_backward_decisions():
+    # a flipped decision zeroes (or passes) exactly that element of the
+    # gradient below, and nothing in the forward pass changes
+    rng = np.random.default_rng(3)
+    n, f = 60, 6
+    rp = np.concatenate([[0], np.cumsum(rng.integers(1, 5, n))]).astype(np.int64)
+    col = rng.integers(0, n, rp[-1]).astype(np.int64)
+    col = np.concatenate([np.sort(col[rp[i]:rp[i + 1]]) for i in range(n)]).astype(np.int64)
+    table = rng.standard_normal((n, f)).astype(np.float32)
+    labels = rng.integers(0, 3, n).astype(np.int64)
+    targets = np.arange(8, dtype=np.int64)
+    dims, fan = (f, 5, 3), (3, 3)
+    ws = [rng.standard_normal((2 * dims[l], dims[l + 1])).astype(np.float32) for l in range(2)]
+    bs = [np.zeros(dims[l + 1], np.float32) for l in range(2)]
+    cfg = oracle.StepConfig(kind=oracle.SAGE, dims=dims, fanouts=fan, precision=oracle.F32, seed=1, step=0)
+    ref = oracle.train_step(rp, col, None, table, labels, targets, ws, bs, cfg)
+    h1 = ref["H"][1]
+    on = np.argwhere(h1 > 0)[0]
+    off = np.argwhere(h1 <= 0)[0]
+    flip = np.zeros(h1.shape, dtype=bool)
+    flip[tuple(on)] = flip[tuple(off)] = True
+    alt = oracle.train_step(rp, col, None, table, labels, targets, ws, bs, cfg, blocks=ref["blocks"],
+                            relu_flip={1: flip})
+    assert alt["loss"] == ref["loss"] and np.array_equal(alt["H"][1], h1)
+    g_ref, g_alt = ref["G"][1], alt["G"][1]
+    assert g_alt[tuple(on)] == 0.0 and g_ref[tuple(on)] != 0.0
+    keep = ~flip
+    assert np.array_equal(g_alt[keep], g_ref[keep])
