@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 import workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+HOST_LINK_PEAK_GBS = 64.0  # PCIe Gen5 x16, one direction
 BF16_PEAK_TFLOPS = 2500.0
 FP32_PEAK_TFLOPS = 157.3
 
@@ -50,6 +51,12 @@ def parse():
                    help="CPU oracle baseline: run whole oracle steps until this much time has passed")
     p.add_argument("--replays", type=int, default=20, help="back-to-back launches timing the roofline kernel")
     p.add_argument("--lr", type=float, default=0.01)
+    p.add_argument("--scale-n", type=int, default=0, help="run the workload's model on an R-MAT graph of this many "
+                   "vertices (the edge count scales with it unless --scale-m is given)")
+    p.add_argument("--scale-m", type=int, default=0)
+    p.add_argument("--pipeline", action=argparse.BooleanOptionalAction, default=None,
+                   help="two-stage steps with the prepare stage (sampling, gather) of step s+1 overlapping the "
+                        "compute stage of step s (default: on for host-resident tables)")
     return p.parse_args()
 
 
@@ -63,8 +70,8 @@ def log(msg):
 # ---------------------------------------------------------------------------
 
 class StagedStep:
-    def __init__(self, gnn, w: workloads.Workload, graph, batch_size, act):
-        self.gnn, self.w, self.graph, self.act = gnn, w, graph, act
+    def __init__(self, gnn, w: workloads.Workload, graph, batch_size, act, loc):
+        self.gnn, self.w, self.graph, self.act, self.loc = gnn, w, graph, act, loc
         dev = graph.rowptr.device
         L = w.num_layers
         self.L = L
@@ -111,7 +118,8 @@ class StagedStep:
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         if name == "gather":
             b0 = self.blocks[-1]
-            call = lambda: gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2])  # noqa
+            call = lambda: gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2],  # noqa
+                                               loc=self.loc)
         elif name.startswith("agg_fwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -163,7 +171,7 @@ class StagedStep:
             mark(f"sample_hop{h + 1}")
             dst, n_dst = blk.src_ids, blk.counts[1:2]
         b0 = self.blocks[-1]
-        gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2])
+        gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2], loc=self.loc)
         mark("gather")
         sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
@@ -198,10 +206,13 @@ class StagedStep:
         block sizes of the last run (host copies; call after synchronising)."""
         L, w = self.L, self.w
         S_H = 2 if self.act == torch.bfloat16 else 4
+        S_X = 2 if w.table_dtype == "f16" else 4
         if name == "gather":
             b = self.blocks[-1].host()
             n0 = b["n_src"]
-            return n0 * w.dims[0] * (4 + S_H) + 8 * n0, 0
+            if self.loc == self.gnn.GNN_LOC_HOST_PINNED:
+                return n0 * w.dims[0] * S_X, 0  # bytes over the host link
+            return n0 * w.dims[0] * (S_X + S_H) + 8 * n0, 0
         if name.startswith("agg_fwd_l"):
             l = int(name[-1])
             b = self.blocks[L - l].host()
@@ -239,6 +250,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     w = workloads.PRESETS[args.workload]
+    if args.scale_n:
+        m = args.scale_m or int(round(w.m * args.scale_n / w.n))
+        w = workloads.scaled(w, args.scale_n, m)
+    host_table = w.table_loc == "host"
+    loc = gnn.GNN_LOC_HOST_PINNED if host_table else gnn.GNN_LOC_DEVICE
+    pipeline = host_table if args.pipeline is None else args.pipeline
     act = torch.bfloat16 if w.precision == "bf16" else torch.float32
     precision = gnn.GNN_BF16 if w.precision == "bf16" else gnn.GNN_F32
     kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
@@ -247,8 +264,13 @@ def main():
     log(f"generating {w.name}: {w.graph} n={w.n} m={w.m}")
     rowptr, col = workloads.make_graph(w, device=dev)
     graph = gnn.DeviceGraph(rowptr, col)
-    table = workloads.features(w.n, w.dims[0], seed=w.seed, device=dev,
-                               dtype=torch.float16 if w.table_dtype == "f16" else torch.float32)
+    tdt = torch.float16 if w.table_dtype == "f16" else torch.float32
+    if host_table:
+        # drawn on the GPU in chunks and copied into pinned host memory
+        table = torch.empty((w.n, w.dims[0]), dtype=tdt, pin_memory=True)
+        workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, out=table)
+    else:
+        table = workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, dtype=tdt)
     labels = workloads.labels(w.n, w.num_classes, seed=w.seed, device=dev)
     perm = workloads.target_batches(w.n, w.batch, seed=w.seed, device=dev)
     L = w.num_layers
@@ -259,36 +281,51 @@ def main():
     stats = workloads.graph_stats(rowptr, col)
     log(f"inputs ready in {time.time() - t0:.1f}s: {stats}")
 
-    tr = gnn.Trainer(kind, w.dims, w.fanouts, precision, w.n, w.batch, weights, biases, device=dev)
+    tr = gnn.Trainer(kind, w.dims, w.fanouts, precision, w.n, w.batch, weights, biases, device=dev,
+                     prepare_slots=2 if pipeline else 0)
     nb = w.n // w.batch
     tgt = [workloads.targets_for_step(perm, w.batch, s).contiguous() for s in range(min(nb, args.warmup + args.steps))]
     edges = torch.zeros(args.steps, dtype=torch.int64, device=dev)
+    prep_stream = torch.cuda.Stream(dev) if pipeline else None
 
-    def step(s, edges_out=None):
-        tr.step(graph, table, labels, tgt[s % len(tgt)], w.seed, s, args.lr, gcn_norm_t=nrm,
-                loc=gnn.GNN_LOC_HOST_PINNED if w.table_loc == "host" else gnn.GNN_LOC_DEVICE, edges_out=edges_out)
+    def run_steps(first, count, edges_out=None, pipelined=pipeline):
+        if pipelined:
+            tr.run_pipelined(graph, table, labels, lambda s: tgt[s % len(tgt)], w.seed, first, count, args.lr,
+                             gcn_norm_t=nrm, loc=loc, edges_out=edges_out, prep_stream=prep_stream)
+            return
+        for i in range(count):
+            tr.step(graph, table, labels, tgt[(first + i) % len(tgt)], w.seed, first + i, args.lr, gcn_norm_t=nrm,
+                    loc=loc, edges_out=None if edges_out is None else edges_out[i:i + 1])
 
-    for s in range(args.warmup):
-        step(s)
+    def timed(first, count, edges_out, pipelined=pipeline):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        ev0.record()
+        run_steps(first, count, edges_out, pipelined)
+        t_enq = time.perf_counter() - t
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1), time.perf_counter() - t, t_enq
+
+    run_steps(0, args.warmup)
     torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps), loss {tr.loss.item():.4f}")
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    ev0.record()
-    for i in range(args.steps):
-        step(args.warmup + i, edges[i:i + 1])
-    t_enqueue = time.perf_counter() - t_wall
-    ev1.record()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_total = ev0.elapsed_time(ev1)
+    log(f"warmup done ({args.warmup} steps, {'pipelined two-stage' if pipeline else 'one-call'} steps), "
+        f"loss {tr.loss.item():.4f}")
+    ms_total, t_wall, t_enqueue = timed(args.warmup, args.steps, edges)
     total_edges = int(edges.sum().item())
     ms_per_step = ms_total / args.steps
     value = total_edges / (ms_total / 1e3)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}, host enqueue "
         f"{1e3 * t_enqueue / args.steps:.3f}), "
         f"{total_edges / args.steps:.0f} edges/step, loss {tr.loss.item():.4f}")
+    sequential_ms = None
+    if pipeline and tr.ws is not None:
+        # the same steps without the overlap (one-call steps on one stream)
+        e2 = torch.zeros(args.steps, dtype=torch.int64, device=dev)
+        ms2, _, _ = timed(args.warmup + args.steps, args.steps, e2, pipelined=False)
+        sequential_ms = ms2 / args.steps
+        log(f"without the overlap: {sequential_ms:.3f} ms/step")
 
     result = {
         "metric": "sampled edges/sec (fwd+bwd) and train steps/sec, 2-layer GraphSAGE, 1 GPU",
@@ -301,6 +338,8 @@ def main():
         "steps_per_s": 1e3 / ms_per_step,
         "edges_per_step": total_edges / args.steps,
         "host_enqueue_ms_per_step": 1e3 * t_enqueue / args.steps,
+        "step_mode": "two-stage pipelined (prepare of step s+1 overlaps compute of step s)" if pipeline
+                     else "one call per step",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -311,13 +350,17 @@ def main():
             "aggregation": w.kind, "dims": list(w.dims), "fanouts": list(w.fanouts), "batch": w.batch,
             "features": f"{w.table_dtype} in {'pinned host memory' if w.table_loc == 'host' else 'HBM'}",
             "scope": "sample + gather + forward + loss + backward + SGD",
+            "scaled_from": None if not args.scale_n else workloads.PRESETS[args.workload].name,
             "parallelism": "single GPU",
         },
     }
 
+    if sequential_ms is not None:
+        result["sequential_ms_per_step"] = sequential_ms
+
     # ---- staged run with events per stage --------------------------------
     if not args.no_stages:
-        staged = StagedStep(gnn, w, graph, w.batch, act)
+        staged = StagedStep(gnn, w, graph, w.batch, act, loc)
         sums, counts = {}, {}
         for s in range(args.stage_steps + 1):
             evs = []
@@ -339,7 +382,11 @@ def main():
         def roof_of(name, ms):
             byts, flops = staged.stage_bytes(name)
             t = ms / 1e3
-            if flops and flops / max(byts, 1) > ridge:
+            if name == "gather" and loc == gnn.GNN_LOC_HOST_PINNED:
+                ach = byts / t / 1e9
+                r = {"bound": "host_link", "achieved": ach, "peak": HOST_LINK_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HOST_LINK_PEAK_GBS}
+            elif flops and flops / max(byts, 1) > ridge:
                 ach = flops / t / 1e12
                 r = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": ach / BF16_PEAK_TFLOPS}
@@ -359,6 +406,12 @@ def main():
         result["kernels"] = {k: {kk: (round(vv, 6) if isinstance(vv, float) else vv)
                                  for kk, vv in roof_of(k, launch_ms[k]).items()} for k in single}
         result["block_sizes"] = staged.block_sizes()
+        if host_table:
+            # X' rows moved over the host link per step, against the step time
+            link_bytes = staged.stage_bytes("gather")[0]
+            ach = link_bytes / (ms_per_step / 1e3) / 1e9
+            result["host_link"] = {"bytes_per_step": int(link_bytes), "achieved": ach, "peak": HOST_LINK_PEAK_GBS,
+                                   "unit": "GB/s", "frac": ach / HOST_LINK_PEAK_GBS}
         log(f"stages (ms): {json.dumps(result['stages_ms'])}")
         log(f"per-launch (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
 
@@ -376,7 +429,7 @@ def main():
         okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
         oprec = oracle.BF16 if w.precision == "bf16" else oracle.F32
         tot_e, tot_t, n_steps = 0, 0.0, 0
-        while n_steps < 2 or tot_t < args.cpu_seconds:
+        while n_steps < 1 or tot_t < args.cpu_seconds:
             s = n_steps
             cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oprec, seed=w.seed,
                                     step=s, lr=args.lr)

@@ -271,10 +271,19 @@ typedef struct gnn_model {
  * (Section II-A, equation 2, with operands rounded as in bf16 mode). */
 gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s);
 
-/* Offsets (bytes from the workspace base) of the step's internal buffers, for
- * inspection.  Block h (1-based hop) is the block of layer L-h+1. */
+/* Layout of a training step's internal buffers, for sizing and inspection.
+ * Block h (1-based hop) is the block of layer L-h+1.
+ *
+ * The step has two stages: prepare (sampling of all hops and the gather of
+ * X', Section IV-B's first stage) and compute (forward, loss, backward and
+ * SGD).  Each has its own workspace.  Offsets of the prepare buffers
+ * (sampler_ws .. x0) are bytes from the prepare workspace, those of the
+ * compute buffers (agg .. loss) bytes from the compute workspace.  The
+ * one-call step's workspace (total_bytes) holds the prepare workspace at
+ * byte 0 and the compute workspace at byte prep_bytes. */
 typedef struct gnn_step_layout {
-    size_t total_bytes;
+    size_t total_bytes;                 /* prep_bytes + compute_bytes */
+    size_t prep_bytes, compute_bytes;   /* sizes of the two workspaces (multiples of 256) */
     size_t sampler_ws, sampler_ws_bytes;
     int64_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS], cap_nnz[GNN_MAX_LAYERS]; /* per hop */
     size_t blk_counts[GNN_MAX_LAYERS], blk_src_ids[GNN_MAX_LAYERS], blk_rowptr[GNN_MAX_LAYERS],
@@ -310,6 +319,39 @@ gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *g
                           gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
                           const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
                           float *loss_dev, int64_t *edges_dev, void *ws, size_t ws_bytes, gnn_stream s);
+
+/* The two stages of gnn_train_step as separate calls, so that the prepare
+ * stage of step s+1 can run on a second stream while the compute stage of
+ * step s runs (two-stage feature prefetching, Section IV-B): with a pinned
+ * host table, the transfer of X' over the host link is then hidden behind
+ * the GPU's computation.  gnn_step_prepare(..., step=s) followed by
+ * gnn_step_compute on the same prepare workspace gives the same results,
+ * bit for bit, as gnn_train_step(..., step=s).
+ *
+ * Ownership and ordering are the caller's: a prepare workspace is written by
+ * gnn_step_prepare and read by the gnn_step_compute that consumes it, so the
+ * next gnn_step_prepare into it must be ordered after that compute (an event
+ * on the compute stream); computes that share a model or a compute
+ * workspace must be ordered among themselves.  The prepare stage reads no
+ * model buffer (only its shape), so it may run while a compute updates W.
+ *
+ * gnn_step_prepare_workspace_init: once per prepare workspace (sampler
+ *   state), as gnn_train_step_workspace_init for the one-call workspace.
+ * gnn_step_prepare: arguments as gnn_train_step; writes the blocks, their
+ *   transposes and X' into prep_ws (prep_bytes >= layout.prep_bytes).
+ * gnn_step_compute: graph_n and batch as given to gnn_step_prepare; labels
+ *   [device] int64[graph_n]; the targets are read back from prep_ws (the
+ *   first batch sources of hop 1); writes m->dw, m->db, updates m->w, m->b
+ *   (and shadows), loss_dev and edges_dev as gnn_train_step.  comp_ws
+ *   (comp_bytes >= layout.compute_bytes) needs no initialisation. */
+gnn_status gnn_step_prepare_workspace_init(const gnn_model *m, int64_t graph_n, int64_t batch, void *prep_ws,
+                                           size_t prep_bytes, gnn_stream s);
+gnn_status gnn_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                            gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *targets, int64_t batch,
+                            uint64_t seed, uint64_t step, void *prep_ws, size_t prep_bytes, gnn_stream s);
+gnn_status gnn_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, size_t prep_bytes, void *comp_ws,
+                            size_t comp_bytes, gnn_stream s);
 
 #ifdef __cplusplus
 }

@@ -34,6 +34,11 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
                           int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
                           uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
                           hipStream_t s);
+gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                            int tdt, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
+                            uint64_t step, void *prep_ws, hipStream_t s);
+gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s);
 
 namespace {
 
@@ -374,14 +379,13 @@ gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s) {
     return GNN_OK;
 }
 
-gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
-                          gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
-                          const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
-                          float *loss_dev, int64_t *edges_dev, void *ws, size_t ws_bytes, gnn_stream s) {
-    clear_error();
-    const char *who = "gnn_train_step";
+namespace {
+
+// Checks shared by the one-call step and its prepare stage.
+gnn_status check_prepare_args(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                              gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *targets, int64_t batch,
+                              const char *who) {
     GNN_TRY(check_model(m, who));
-    GNN_TRY(check_model_buffers(m, who));
     GNN_TRY(check_graph(g, who));
     GNN_CHECK(g->n >= 1, GNN_EINVAL, "%s: empty graph", who);
     GNN_CHECK(batch >= 1 && batch <= g->n, GNN_EINVAL, "%s: batch %lld out of [1, n]", who, (long long)batch);
@@ -390,11 +394,31 @@ gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     GNN_CHECK(tdt == GNN_F32 || tdt == GNN_F16 || (tdt == GNN_BF16 && m->precision == GNN_BF16), GNN_EUNSUPPORTED,
               "%s: table dtype %d is not supported with precision %d", who, tdt, m->precision);
     GNN_CHECK(loc == GNN_LOC_DEVICE || loc == GNN_LOC_HOST_PINNED, GNN_EINVAL, "%s: unknown location", who);
-    GNN_CHECK(table && labels && targets, GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK(table && targets, GNN_EINVAL, "%s: NULL pointer", who);
     GNN_CHECK(row_stride >= m->dims[0], GNN_EINVAL, "%s: row_stride below dims[0]", who);
-    GNN_CHECK(aligned(labels, 8) && aligned(targets, 8) && aligned(loss_dev, 4) && aligned(edges_dev, 8) &&
-                  aligned(table, dtype_size(tdt)),
-              GNN_EINVAL, "%s: misaligned data", who);
+    GNN_CHECK(aligned(targets, 8) && aligned(table, dtype_size(tdt)), GNN_EINVAL, "%s: misaligned data", who);
+    return GNN_OK;
+}
+
+gnn_status check_compute_args(const gnn_model *m, const int64_t *labels, const float *loss_dev,
+                              const int64_t *edges_dev, const char *who) {
+    GNN_TRY(check_model_buffers(m, who));
+    GNN_CHECK(labels, GNN_EINVAL, "%s: NULL labels", who);
+    GNN_CHECK(aligned(labels, 8) && aligned(loss_dev, 4) && aligned(edges_dev, 8), GNN_EINVAL,
+              "%s: misaligned data", who);
+    return GNN_OK;
+}
+
+}  // namespace
+
+gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                          gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
+                          const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
+                          float *loss_dev, int64_t *edges_dev, void *ws, size_t ws_bytes, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_train_step";
+    GNN_TRY(check_prepare_args(m, g, gcn_norm, table, tdt, loc, row_stride, targets, batch, who));
+    GNN_TRY(check_compute_args(m, labels, loss_dev, edges_dev, who));
     gnn_step_layout o;
     GNN_TRY(step_layout(m, g->n, batch, &o));
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
@@ -403,6 +427,50 @@ gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     GNN_TRY(device_view(table, loc, &t, who));
     return run_train_step(m, g, gcn_norm, t, tdt, row_stride, labels, targets, batch, seed, step, lr, loss_dev,
                           edges_dev, ws, stream_of(s));
+}
+
+gnn_status gnn_step_prepare_workspace_init(const gnn_model *m, int64_t graph_n, int64_t batch, void *prep_ws,
+                                           size_t prep_bytes, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_step_prepare_workspace_init";
+    gnn_step_layout o;
+    GNN_TRY(gnn_train_step_layout(m, graph_n, batch, &o));
+    GNN_CHECK(prep_ws && aligned(prep_ws, 256), GNN_EINVAL, "%s: prep_ws must be 256-byte aligned", who);
+    GNN_CHECK(prep_bytes >= o.prep_bytes, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, prep_bytes,
+              o.prep_bytes);
+    return launch_sampler_ws_init(static_cast<char *>(prep_ws) + o.sampler_ws, graph_n, stream_of(s));
+}
+
+gnn_status gnn_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                            gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *targets, int64_t batch,
+                            uint64_t seed, uint64_t step, void *prep_ws, size_t prep_bytes, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_step_prepare";
+    GNN_TRY(check_prepare_args(m, g, gcn_norm, table, tdt, loc, row_stride, targets, batch, who));
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, g->n, batch, &o));
+    GNN_CHECK(prep_ws && aligned(prep_ws, 256), GNN_EINVAL, "%s: prep_ws must be non-NULL and 256-byte aligned", who);
+    GNN_CHECK(prep_bytes >= o.prep_bytes, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, prep_bytes,
+              o.prep_bytes);
+    const void *t = nullptr;
+    GNN_TRY(device_view(table, loc, &t, who));
+    return run_step_prepare(m, g, gcn_norm, t, tdt, row_stride, targets, batch, seed, step, prep_ws, stream_of(s));
+}
+
+gnn_status gnn_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, size_t prep_bytes, void *comp_ws,
+                            size_t comp_bytes, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_step_compute";
+    gnn_step_layout o;
+    GNN_TRY(gnn_train_step_layout(m, graph_n, batch, &o));
+    GNN_TRY(check_compute_args(m, labels, loss_dev, edges_dev, who));
+    GNN_CHECK(prep_ws && aligned(prep_ws, 256) && comp_ws && aligned(comp_ws, 256), GNN_EINVAL,
+              "%s: workspaces must be non-NULL and 256-byte aligned", who);
+    GNN_CHECK(prep_bytes >= o.prep_bytes && comp_bytes >= o.compute_bytes, GNN_ESIZE,
+              "%s: workspaces %zu and %zu bytes, need %zu and %zu", who, prep_bytes, comp_bytes, o.prep_bytes,
+              o.compute_bytes);
+    return run_step_compute(m, graph_n, labels, batch, lr, loss_dev, edges_dev, prep_ws, comp_ws, stream_of(s));
 }
 
 }  // extern "C"

@@ -3,10 +3,17 @@
 // below the first layer), SGD.  The host never waits: counts produced on the
 // device are read by later kernels.
 //
-// Everything runs on the caller's stream except the block transposes (CSC),
-// which only the backward pass reads: they run on a helper stream of the
-// library, forked after each block is built and joined before the backward
-// pass, so they overlap the gather and the forward layers.
+// The step has two stages with separate workspaces: prepare (sampling and the
+// gather of X') and compute (the rest).  A caller can run the prepare stage
+// of the next step on a second stream while the compute stage of this one
+// runs, which hides the feature loading from a host-resident table (two-stage
+// feature prefetching, Section IV-B).
+//
+// In the one-call step everything runs on the caller's stream except the
+// block transposes (CSC), which only the backward pass reads: they run on a
+// helper stream of the library, forked after each block is built and joined
+// before the backward pass, so they overlap the gather and the forward
+// layers.  The separate prepare stage runs them on its own stream.
 #include <algorithm>
 #include <mutex>
 
@@ -62,8 +69,8 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
     *o = gnn_step_layout{};
     const int act = m->precision;
     const size_t asz = dtype_size(act);
+    // prepare part: sampler state, blocks, transposes, X'
     Carver c(nullptr);
-    // capacities per hop
     int64_t cap_dst = batch;
     size_t hop_max = 0;
     for (int h = 0; h < L; ++h) {
@@ -92,26 +99,30 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         if (h < L - 1) o->blk_csc_ws[h] = c.take(block_csc_ws_bytes(o->cap_nnz[h]));
     }
     o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
+    o->prep_bytes = round_up(c.off, 256);
+    // compute part: activations, gradients, GEMM and loss scratch, outputs
+    Carver d(nullptr);
     size_t bwd = 0, fwd = 0;
     for (int l = 1; l <= L; ++l) {
         const int hb = L - l;
         const int64_t rows = o->cap_dst[hb];
-        o->agg[l] = c.take(static_cast<size_t>(rows) * m->dims[l - 1] * asz);
-        o->h[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
-        o->grad[l] = c.take(static_cast<size_t>(rows) * m->dims[l] * 4);
-        if (l >= 2) o->d_a[l] = c.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
+        o->agg[l] = d.take(static_cast<size_t>(rows) * m->dims[l - 1] * asz);
+        o->h[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
+        o->grad[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * 4);
+        if (l >= 2) o->d_a[l] = d.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
         fwd = std::max(fwd, update_fwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
         bwd = std::max(bwd, update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
     }
-    o->fwd_ws = c.take(fwd);
+    o->fwd_ws = d.take(fwd);
     o->fwd_ws_bytes = fwd;
-    o->bwd_ws = c.take(bwd);
+    o->bwd_ws = d.take(bwd);
     o->bwd_ws_bytes = bwd;
     o->loss_ws_bytes = softmax_ce_ws_bytes(batch);
-    o->loss_ws = c.take(o->loss_ws_bytes);
-    o->edges = c.take(8);
-    o->loss = c.take(4);
-    o->total_bytes = round_up(c.off, 256);
+    o->loss_ws = d.take(o->loss_ws_bytes);
+    o->edges = d.take(8);
+    o->loss = d.take(4);
+    o->compute_bytes = round_up(d.off, 256);
+    o->total_bytes = o->prep_bytes + o->compute_bytes;
     return GNN_OK;
 }
 
@@ -130,27 +141,28 @@ static gnn_block block_view(const gnn_step_layout &o, int h, char *base) {
     return b;
 }
 
-gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
-                          int tdt, int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
-                          uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
-                          hipStream_t s) {
-    gnn_step_layout o;
-    GNN_TRY(step_layout(m, g->n, batch, &o));
-    char *base = static_cast<char *>(ws);
+namespace {
+
+void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_block *blk) {
+    for (int h = 0; h < m->num_layers; ++h) blk[h] = block_view(o, h, prep);
+}
+
+// Sampling of all hops and the gather of X' into a prepare workspace.  With
+// a helper (hp), the transposes run on its stream and hp->join is recorded
+// after the last one; without, they run on s.
+gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
+                       int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step,
+                       char *prep, const gnn_step_layout &o, Helper *hp, hipStream_t s) {
+    (void)batch;
     const int L = m->num_layers;
     const int act = m->precision;
     gnn_block blk[GNN_MAX_LAYERS];
-    for (int h = 0; h < L; ++h) blk[h] = block_view(o, h, base);
-
-    std::lock_guard<std::mutex> lock(g_helper_mu);
-    Helper *hp = nullptr;
-    if (L > 1) GNN_TRY(helper_for_current_device(&hp));
+    block_views(m, o, prep, blk);
 
     // sampling: hop 1 around the targets, then outwards.  Hop h's relabel
     // shares a launch with hop h+1's prepare (both only need hop h's
-    // sources), and the last hop's relabel shares one with the gather.  The
-    // transposes of all blocks but the last run on the helper stream.
-    char *shared = base + o.sampler_ws;
+    // sources), and the last hop's relabel shares one with the gather.
+    char *shared = prep + o.sampler_ws;
     size_t hop_max = 0;
     for (int h = 0; h < L; ++h)
         hop_max = std::max(hop_max, sampler_hop_bytes(g->n, o.cap_dst[h], m->fanouts[h]));
@@ -159,14 +171,15 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
         const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
         void *scratch = shared + sampler_shared_bytes(g->n) + (h % 2) * hop_max;
-        void *csc_ws = h < L - 1 ? base + o.blk_csc_ws[h] : nullptr;
+        void *csc_ws = h < L - 1 ? prep + o.blk_csc_ws[h] : nullptr;
         plan[h] = plan_hop(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h], seed, step,
                            h + 1, &blk[h], shared, scratch, csc_ws);
     }
-    auto fork_csc = [&](int h) -> gnn_status {
+    auto csc = [&](int h) -> gnn_status {
+        if (!hp) return launch_block_csc(&blk[h], prep + o.blk_csc_ws[h], o.cap_nnz[h], s);
         GNN_HIP(hipEventRecord(hp->fork[h], s));
         GNN_HIP(hipStreamWaitEvent(hp->stream, hp->fork[h], 0));
-        return launch_block_csc(&blk[h], base + o.blk_csc_ws[h], o.cap_nnz[h], hp->stream);
+        return launch_block_csc(&blk[h], prep + o.blk_csc_ws[h], o.cap_nnz[h], hp->stream);
     };
     GNN_TRY(launch_hop_prepare(plan[0], s));
     GNN_TRY(launch_hop_emit(plan[0], s));
@@ -177,43 +190,53 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
                              "hop_relabel+prepare");
         });
         GNN_TRY(st);
-        GNN_TRY(fork_csc(h - 1));
+        GNN_TRY(csc(h - 1));
         GNN_TRY(launch_hop_emit(plan[h], s));
     }
     if (hp) GNN_HIP(hipEventRecord(hp->join, hp->stream));
     // feature loading (rows of the input layer's sources) with the last
     // hop's relabel
     const gnn_block &b0 = blk[L - 1];
-    void *x0 = base + o.x0;
-    {
-        const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0], x0};
-        const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act));
-        gnn_status st = GNN_OK;
-        const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
-            st = launch_job2(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid, job, ggrid, s,
-                             "hop_relabel+gather");
-        });
-        GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
-        GNN_TRY(st);
-    }
+    const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0], prep + o.x0};
+    const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act));
+    gnn_status st = GNN_OK;
+    const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
+        st = launch_job2(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid, job, ggrid, s,
+                         "hop_relabel+gather");
+    });
+    GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
+    return st;
+}
+
+// Forward, loss, backward and SGD from a prepared workspace.  The targets are
+// the first rows of hop 1's sources (destinations come first).  With a
+// helper, the backward pass waits for hp->join (the transposes).
+gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch, float lr, float *loss_dev,
+                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o, Helper *hp,
+                       hipStream_t s) {
+    const int L = m->num_layers;
+    const int act = m->precision;
+    gnn_block blk[GNN_MAX_LAYERS];
+    block_views(m, o, prep, blk);
+    const void *x0 = prep + o.x0;
 
     // forward
     for (int l = 1; l <= L; ++l) {
         const gnn_block &b = blk[L - l];
-        const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);
-        void *agg = base + o.agg[l];
+        const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
+        void *agg = comp + o.agg[l];
         const int64_t f_in = m->dims[l - 1];
         GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
-                                  m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, base + o.h[l],
-                                  l < L ? act : GNN_F32, base + o.fwd_ws, s));
+                                  m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, comp + o.h[l],
+                                  l < L ? act : GNN_F32, comp + o.fwd_ws, s));
     }
     // loss on the targets: gradient and row losses now, the mean with the
     // last kernel of the step
-    float *row_loss = reinterpret_cast<float *>(base + o.loss_ws);
-    GNN_TRY(launch_job(loss::SoftmaxJob{reinterpret_cast<const float *>(base + o.h[L]), batch, m->dims[L], labels,
-                                        targets, reinterpret_cast<float *>(base + o.grad[L]), row_loss},
+    float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
+    GNN_TRY(launch_job(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L], labels,
+                                        blk[0].src_ids, reinterpret_cast<float *>(comp + o.grad[L]), row_loss},
                        static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64)), s, "softmax_ce"));
     // backward (reads the transposes).  Per layer: the dA and dW GEMMs in
     // one launch, then the dW reduction (with SGD on W^l, b^l and the
@@ -226,26 +249,26 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     tail.num_blocks = L;
     tail.row_loss = row_loss;
     tail.b = batch;
-    tail.loss = reinterpret_cast<float *>(base + o.loss);
+    tail.loss = reinterpret_cast<float *>(comp + o.loss);
     tail.loss_out = loss_dev;
-    tail.edges = reinterpret_cast<int64_t *>(base + o.edges);
+    tail.edges = reinterpret_cast<int64_t *>(comp + o.edges);
     tail.edges_out = edges_dev;
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
-        const void *hin = (l == 1) ? x0 : static_cast<const void *>(base + o.h[l - 1]);
-        const void *agg_out = base + o.agg[l];
+        const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
+        const void *agg_out = comp + o.agg[l];
         const int64_t f_in = m->dims[l - 1];
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
-        float *d_a = l > 1 ? reinterpret_cast<float *>(base + o.d_a[l]) : nullptr;
+        float *d_a = l > 1 ? reinterpret_cast<float *>(comp + o.d_a[l]) : nullptr;
         const gbwd::Args a{sage ? hin : agg_out, sage ? agg_out : nullptr, act, f_in, b.counts, b.cap_dst,
-                           m->w[l - 1], reinterpret_cast<const float *>(base + o.grad[l]), m->dims[l], m->precision,
-                           m->dw[l - 1], m->db[l - 1], d_a, reinterpret_cast<float *>(base + o.bwd_ws), m->w[l - 1],
+                           m->w[l - 1], reinterpret_cast<const float *>(comp + o.grad[l]), m->dims[l], m->precision,
+                           m->dw[l - 1], m->db[l - 1], d_a, reinterpret_cast<float *>(comp + o.bwd_ws), m->w[l - 1],
                            m->b[l - 1], m->wt[l - 1], lr};
         const gbwd::Plan p = gbwd::plan(a);
         GNN_TRY(launch_update_bwd_gemms(a, p, s));
         gnn_status st = GNN_OK;
         if (l > 1) {
-            float *d_src = reinterpret_cast<float *>(base + o.grad[l - 1]);
+            float *d_src = reinterpret_cast<float *>(comp + o.grad[l - 1]);
             agg::with_bwd_job(&b, m->kind, d_a, f_in, hin, act, d_src, [&](auto aj) {
                 gbwd::with_reduce_job(a, p, [&](auto rj) {
                     st = launch_job2(rj, p.red_grid, aj, agg::row_grid(b.cap_src), s, "update_dw_reduce+aggregate_bwd");
@@ -259,6 +282,41 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
         GNN_TRY(st);
     }
     return GNN_OK;
+}
+
+}  // namespace
+
+// The whole step on one stream, the transposes on the helper stream.
+gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                          int tdt, int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
+                          uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
+                          hipStream_t s) {
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, g->n, batch, &o));
+    char *prep = static_cast<char *>(ws);
+    char *comp = prep + o.prep_bytes;
+    std::lock_guard<std::mutex> lock(g_helper_mu);
+    Helper *hp = nullptr;
+    if (m->num_layers > 1) GNN_TRY(helper_for_current_device(&hp));
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, row_stride, targets, batch, seed, step, prep, o, hp, s));
+    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, hp, s);
+}
+
+gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                            int tdt, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
+                            uint64_t step, void *prep_ws, hipStream_t s) {
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, g->n, batch, &o));
+    return run_prepare(m, g, gcn_norm, table, tdt, row_stride, targets, batch, seed, step,
+                       static_cast<char *>(prep_ws), o, nullptr, s);
+}
+
+gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s) {
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, graph_n, batch, &o));
+    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, static_cast<char *>(prep_ws),
+                       static_cast<char *>(comp_ws), o, nullptr, s);
 }
 
 }  // namespace gnn

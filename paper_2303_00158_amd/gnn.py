@@ -52,7 +52,8 @@ _ML = GNN_MAX_LAYERS
 
 
 class StepLayout(ctypes.Structure):
-    _fields_ = [("total_bytes", _sz), ("sampler_ws", _sz), ("sampler_ws_bytes", _sz),
+    _fields_ = [("total_bytes", _sz), ("prep_bytes", _sz), ("compute_bytes", _sz),
+                ("sampler_ws", _sz), ("sampler_ws_bytes", _sz),
                 ("cap_dst", _i64 * _ML), ("cap_src", _i64 * _ML), ("cap_nnz", _i64 * _ML),
                 ("blk_counts", _sz * _ML), ("blk_src_ids", _sz * _ML), ("blk_rowptr", _sz * _ML),
                 ("blk_col", _sz * _ML), ("blk_cscptr", _sz * _ML), ("blk_cscrow", _sz * _ML),
@@ -89,6 +90,10 @@ _SIGNATURES = {
     "gnn_train_step_workspace_init": (_i32, [_P(Model), _i64, _i64, _vp, _sz, _vp]),
     "gnn_train_step": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64, _u64, _u64, _f32,
                               _vp, _vp, _vp, _sz, _vp]),
+    "gnn_step_prepare_workspace_init": (_i32, [_P(Model), _i64, _i64, _vp, _sz, _vp]),
+    "gnn_step_prepare": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _i64, _u64, _u64, _vp, _sz,
+                                _vp]),
+    "gnn_step_compute": (_i32, [_P(Model), _i64, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
 }
 
 _lib = None
@@ -307,14 +312,22 @@ def sgd(w: torch.Tensor, dw: torch.Tensor, lr: float, stream=None) -> torch.Tens
 # whole training step
 # ---------------------------------------------------------------------------
 
+_COMPUTE_BUFFERS = ("agg", "h", "grad", "d_a", "fwd_ws", "bwd_ws", "loss_ws", "edges", "loss")
+
+
 class Trainer:
     """Owns the model buffers (fp32 master weights, gradients, and for bf16
-    models the bf16 W^T shadows) and the step workspace, and calls
-    gnn_train_step."""
+    models the bf16 W^T shadows) and the step workspaces.
+
+    step() calls gnn_train_step on one workspace.  With prepare_slots > 0
+    the trainer also owns that many prepare workspaces and one compute
+    workspace for the two-stage calls (prepare() / compute(), and
+    run_pipelined(), which overlaps the prepare stage of step s+1 with the
+    compute stage of step s on two streams)."""
 
     def __init__(self, kind: int, dims: Sequence[int], fanouts: Sequence[int], precision: int, graph_n: int,
                  batch: int, weights: Sequence[torch.Tensor], biases: Sequence[torch.Tensor], device="cuda",
-                 shadows: bool = True):
+                 shadows: bool = True, prepare_slots: int = 0, one_call: bool = True):
         L = len(dims) - 1
         assert len(fanouts) == L and len(weights) == L and len(biases) == L
         self.device = torch.device(device)
@@ -342,11 +355,21 @@ class Trainer:
             _check(lib().gnn_model_sync_shadow(ctypes.byref(m), _stream(None)))
         self.layout = StepLayout()
         _check(lib().gnn_train_step_layout(ctypes.byref(m), graph_n, batch, ctypes.byref(self.layout)))
-        self.ws = _aligned_empty(self.layout.total_bytes, self.device)
-        _check(lib().gnn_train_step_workspace_init(ctypes.byref(m), graph_n, batch, _ptr(self.ws), self.ws.numel(),
-                                                   _stream(None)))
+        self.ws = None
+        if one_call:
+            self.ws = _aligned_empty(self.layout.total_bytes, self.device)
+            _check(lib().gnn_train_step_workspace_init(ctypes.byref(m), graph_n, batch, _ptr(self.ws),
+                                                       self.ws.numel(), _stream(None)))
+        self.prep_ws: List[torch.Tensor] = []
+        for _ in range(prepare_slots):
+            ws = _aligned_empty(self.layout.prep_bytes, self.device)
+            _check(lib().gnn_step_prepare_workspace_init(ctypes.byref(m), graph_n, batch, _ptr(ws), ws.numel(),
+                                                         _stream(None)))
+            self.prep_ws.append(ws)
+        self.comp_ws = _aligned_empty(self.layout.compute_bytes, self.device) if prepare_slots else None
         self.loss = torch.zeros(1, dtype=torch.float32, device=self.device)
         self.edges = torch.zeros(1, dtype=torch.int64, device=self.device)
+        self._viewing = None  # (prepare ws, compute ws) that the views read
 
     def step(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets: torch.Tensor, seed: int,
              step: int, lr: float, gcn_norm_t: Optional[torch.Tensor] = None, loc: int = GNN_LOC_DEVICE,
@@ -359,14 +382,78 @@ class Trainer:
                                     dtype_code(table.dtype), loc, table.stride(0), _ptr(labels), _ptr(targets),
                                     self.batch, seed, step, float(lr), _ptr(self.loss), _ptr(e),
                                     _ptr(self.ws), self.ws.numel(), _stream(stream)))
+        self._viewing = None
 
-    # --- views into the workspace (for inspection and tests) ---------------
-    def _view(self, off: int, numel: int, dtype: torch.dtype) -> torch.Tensor:
+    def prepare(self, slot: int, graph: DeviceGraph, table: torch.Tensor, targets: torch.Tensor, seed: int, step: int,
+                gcn_norm_t: Optional[torch.Tensor] = None, loc: int = GNN_LOC_DEVICE, stream=None) -> None:
+        """Enqueue the prepare stage of one step into prepare slot ``slot``."""
+        ws = self.prep_ws[slot]
+        _check(lib().gnn_step_prepare(ctypes.byref(self.model), ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(table),
+                                      dtype_code(table.dtype), loc, table.stride(0), _ptr(targets), self.batch, seed,
+                                      step, _ptr(ws), ws.numel(), _stream(stream)))
+
+    def compute(self, slot: int, labels: torch.Tensor, lr: float, edges_out: Optional[torch.Tensor] = None,
+                stream=None) -> None:
+        """Enqueue the compute stage of the step prepared in slot ``slot``."""
+        e = self.edges if edges_out is None else edges_out
+        ws = self.prep_ws[slot]
+        _check(lib().gnn_step_compute(ctypes.byref(self.model), self.graph_n, _ptr(labels), self.batch, float(lr),
+                                      _ptr(self.loss), _ptr(e), _ptr(ws), ws.numel(), _ptr(self.comp_ws),
+                                      self.comp_ws.numel(), _stream(stream)))
+        self._viewing = (ws, self.comp_ws)
+
+    def run_pipelined(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets_of, seed: int,
+                      first_step: int, steps: int, lr: float, gcn_norm_t: Optional[torch.Tensor] = None,
+                      loc: int = GNN_LOC_DEVICE, edges_out: Optional[torch.Tensor] = None, prep_stream=None,
+                      stream=None) -> None:
+        """Enqueue ``steps`` steps with the prepare stage (sampling and the
+        gather of X') of step s+1 overlapping the compute stage of step s.
+        targets_of(s) gives the target ids of step s (kept alive by the
+        caller until the work is done); edges_out, if given, is an int64
+        device tensor of ``steps`` counts.  Slots rotate over the prepare
+        workspaces; a slot is refilled only after the compute that read it
+        (events), and each compute waits for its prepare."""
+        nslot = len(self.prep_ws)
+        assert nslot >= 2, "run_pipelined needs prepare_slots >= 2"
+        cs = torch.cuda.current_stream(self.device) if stream is None else stream
+        ps = prep_stream if prep_stream is not None else torch.cuda.Stream(self.device)
+        prepared = [torch.cuda.Event() for _ in range(nslot)]
+        consumed = [None] * nslot
+        ps.wait_stream(cs)  # inputs written on the compute stream
+
+        def enqueue_prepare(i):
+            slot = i % nslot
+            if consumed[slot] is not None:
+                ps.wait_event(consumed[slot])
+            self.prepare(slot, graph, table, targets_of(first_step + i), seed, first_step + i, gcn_norm_t, loc,
+                         stream=ps)
+            prepared[slot].record(ps)
+
+        for i in range(min(nslot - 1, steps)):
+            enqueue_prepare(i)
+        for i in range(steps):
+            if i + nslot - 1 < steps:
+                enqueue_prepare(i + nslot - 1)
+            slot = i % nslot
+            cs.wait_event(prepared[slot])
+            e = None if edges_out is None else edges_out[i:i + 1]
+            self.compute(slot, labels, lr, edges_out=e, stream=cs)
+            ev = torch.cuda.Event()
+            ev.record(cs)
+            consumed[slot] = ev
+        cs.wait_stream(ps)
+
+    # --- views into the workspaces (for inspection and tests) --------------
+    def _view(self, off: int, numel: int, dtype: torch.dtype, compute: bool = False) -> torch.Tensor:
         esz = torch.empty(0, dtype=dtype).element_size()
-        return self.ws[off:off + numel * esz].view(dtype)
+        if self._viewing is not None:
+            base = self._viewing[1] if compute else self._viewing[0]
+        else:
+            base = self.ws[self.layout.prep_bytes:] if compute else self.ws
+        return base[off:off + numel * esz].view(dtype)
 
     def block_view(self, h: int) -> dict:
-        """Host copy of the block built at hop h (1-based)."""
+        """Host copy of the block built at hop h (1-based) by the last step."""
         lay = self.layout
         i = h - 1
         counts = self._view(lay.blk_counts[i], 4, torch.int64).cpu().tolist()
@@ -386,5 +473,7 @@ class Trainer:
         return torch_dtype(self.precision)
 
     def tensor(self, name: str, layer: int, rows: int, cols: int, dtype: torch.dtype) -> torch.Tensor:
+        """View of a step buffer of the last step (agg/h/grad/d_a per layer;
+        x0 and the rest by name)."""
         off = getattr(self.layout, name)[layer] if name in ("agg", "h", "grad", "d_a") else getattr(self.layout, name)
-        return self._view(off, rows * cols, dtype).view(rows, cols)
+        return self._view(off, rows * cols, dtype, compute=name in _COMPUTE_BUFFERS).view(rows, cols)

@@ -104,10 +104,26 @@ def test_step_layout_capacities_and_disjoint_buffers(gnn):
     assert list(lay.cap_src[:2]) == [26_624, 292_864]
     # hop 1 (the last layer's block) has a transpose, hop 2 (first layer) has none
     assert lay.blk_cscptr[0] and not lay.blk_cscptr[1]
-    offs = [lay.sampler_ws, lay.x0, lay.bwd_ws, lay.loss_ws, lay.edges, lay.loss]
-    offs += [lay.blk_counts[h] for h in range(2)] + [lay.agg[l] for l in (1, 2)] + [lay.h[l] for l in (1, 2)]
-    assert len(set(offs)) == len(offs)
-    assert max(offs) < lay.total_bytes
+    # the prepare buffers tile the prepare workspace without overlap, the
+    # compute buffers the compute workspace
+    cd, cs, cn = lay.cap_dst, lay.cap_src, lay.cap_nnz
+    prep = [(lay.sampler_ws, lay.sampler_ws_bytes), (lay.x0, cs[1] * 100 * 2)]
+    for h in range(2):
+        prep += [(lay.blk_counts[h], 32), (lay.blk_src_ids[h], cs[h] * 8), (lay.blk_rowptr[h], (cd[h] + 1) * 8),
+                 (lay.blk_col[h], cn[h] * 4)]
+    prep += [(lay.blk_cscptr[0], (cs[0] + 1) * 8), (lay.blk_cscrow[0], cn[0] * 4), (lay.blk_csc_ws[0], 1)]
+    comp = [(lay.fwd_ws, lay.fwd_ws_bytes), (lay.bwd_ws, lay.bwd_ws_bytes), (lay.loss_ws, lay.loss_ws_bytes),
+            (lay.edges, 8), (lay.loss, 4)]
+    for l, rows in ((1, cd[1]), (2, cd[0])):
+        f_in, f_out = (100, 256, 47)[l - 1], (100, 256, 47)[l]
+        comp += [(lay.agg[l], rows * f_in * 2), (lay.h[l], rows * f_out * (2 if l < 2 else 4)),
+                 (lay.grad[l], rows * f_out * 4)]
+    comp += [(lay.d_a[2], cd[0] * 512 * 4)]
+    for spans, size in ((prep, lay.prep_bytes), (comp, lay.compute_bytes)):
+        spans = sorted(spans)
+        assert all(a + n <= b for (a, n), (b, _) in zip(spans, spans[1:])), spans
+        assert spans[-1][0] + spans[-1][1] <= size and size % 256 == 0
+    assert lay.total_bytes == lay.prep_bytes + lay.compute_bytes
     nb = ctypes.c_size_t()
     assert lib.gnn_train_step_workspace_size(ctypes.byref(m), 2_449_029, 1024, ctypes.byref(nb)) == gnn.GNN_OK
     assert nb.value == lay.total_bytes
@@ -116,3 +132,34 @@ def test_step_layout_capacities_and_disjoint_buffers(gnn):
     bad = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (100, 256, 47), (25, 10), gnn.GNN_F16)
     assert lib.gnn_train_step_workspace_size(ctypes.byref(bad), 1000, 10, ctypes.byref(nb)) == gnn.GNN_EUNSUPPORTED
     assert lib.gnn_train_step_workspace_size(ctypes.byref(m), 1000, 2000, ctypes.byref(nb)) == gnn.GNN_EINVAL
+
+
+def test_two_stage_step_validation(gnn):
+    # argument checks of the prepare / compute entry points run on the host
+    # before anything is enqueued (the pointers below are never dereferenced)
+    lib = gnn.lib()
+    m = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (32, 16, 8), (5, 5), gnn.GNN_F32)
+    for l in range(2):
+        m.w[l] = m.b[l] = m.dw[l] = m.db[l] = 1 << 20
+    lay = gnn.StepLayout()
+    assert lib.gnn_train_step_layout(ctypes.byref(m), 1000, 64, ctypes.byref(lay)) == gnn.GNN_OK
+    fake = 1 << 24
+    assert lib.gnn_step_prepare_workspace_init(ctypes.byref(m), 1000, 64, fake, lay.prep_bytes - 256,
+                                               None) == gnn.GNN_ESIZE
+    assert lib.gnn_step_prepare_workspace_init(ctypes.byref(m), 1000, 64, fake + 8, lay.prep_bytes,
+                                               None) == gnn.GNN_EINVAL
+    assert lib.gnn_step_compute(ctypes.byref(m), 1000, fake, 64, 0.1, None, None, fake, lay.prep_bytes, fake,
+                                lay.compute_bytes - 256, None) == gnn.GNN_ESIZE
+    assert lib.gnn_step_compute(ctypes.byref(m), 1000, fake, 64, 0.1, None, None, fake, lay.prep_bytes - 256, fake,
+                                lay.compute_bytes, None) == gnn.GNN_ESIZE
+    assert lib.gnn_step_compute(ctypes.byref(m), 1000, None, 64, 0.1, None, None, fake, lay.prep_bytes, fake,
+                                lay.compute_bytes, None) == gnn.GNN_EINVAL
+    assert lib.gnn_step_compute(ctypes.byref(m), 1000, fake, 2000, 0.1, None, None, fake, lay.prep_bytes, fake,
+                                lay.compute_bytes, None) == gnn.GNN_EINVAL
+    g = gnn.Graph(1000, 5000, fake, fake)
+    assert lib.gnn_step_prepare(ctypes.byref(m), None, None, fake, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 32, fake, 64, 0,
+                                0, fake, lay.prep_bytes, None) == gnn.GNN_EINVAL
+    assert lib.gnn_step_prepare(ctypes.byref(m), ctypes.byref(g), None, fake, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 32,
+                                fake, 64, 0, 0, fake, lay.prep_bytes - 256, None) == gnn.GNN_ESIZE
+    assert lib.gnn_step_prepare(ctypes.byref(m), ctypes.byref(g), None, fake, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 16,
+                                fake, 64, 0, 0, fake, lay.prep_bytes, None) == gnn.GNN_EINVAL

@@ -5,6 +5,7 @@ bit.  Floating point is compared normwise, max|x - r| / max|r|, against
 1e-4 (fp32 arithmetic) or 2e-2 (bf16 storage / GEMM operands), with the
 oracle rounding at the same points as the kernels.
 """
+
 import numpy as np
 import pytest
 import torch
@@ -581,3 +582,91 @@ def test_train_step_keeps_shadows_and_matches_unshadowed_step():
         runs.append([t.cpu().clone() for t in tr.w + tr.b + tr.dw] + [tr.loss.cpu().clone()])
     for a, b in zip(runs[0], runs[1]):
         assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+# ---------------------------------------------------------------------------
+# two-stage step: prepare / compute, pipelined
+# ---------------------------------------------------------------------------
+
+def _pipeline_inputs(kind, dims, fanouts, n, m, batch, table_dtype=torch.float32, seed=0):
+    rowptr, col = workloads.rmat_graph(n, m, seed=seed)
+    table = workloads.features(n, dims[0], seed=seed, dtype=table_dtype)
+    labels = workloads.labels(n, dims[-1], seed=seed).to(DEV)
+    perm = workloads.target_batches(n, batch, seed=seed)
+    L = len(dims) - 1
+    sage = kind == gnn.GNN_AGG_SAGE_MEAN
+    ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], seed, l) for l in range(L)]
+    bs = [torch.zeros(dims[l + 1]) for l in range(L)]
+    g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
+    targets = [workloads.targets_for_step(perm, batch, s).to(DEV) for s in range(n // batch)]
+    return rowptr, col, table, labels, ws, bs, g, targets
+
+
+def _state(tr):
+    return [t.cpu().clone() for t in tr.w + tr.b + tr.dw + tr.db] + [tr.loss.cpu().clone()]
+
+
+@pytest.mark.parametrize("kind,precision", [(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16), (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32)])
+def test_pipelined_two_stage_steps_equal_one_call_steps(kind, precision):
+    # five steps through two rotating prepare slots (each refilled after the
+    # compute that read it) give bit for bit what five one-call steps give
+    dims, fan, n, m, batch, steps = (100, 256, 47), (25, 10), 30_000, 400_000, 512, 5
+    _rp, _col, table, labels, ws, bs, g, targets = _pipeline_inputs(kind, dims, fan, n, m, batch)
+    table = table.to(DEV)
+    nrm = gnn.gcn_norm(g)
+    print(f"[pipeline] kind={kind} precision={precision}: one-call steps", flush=True)
+    ref = gnn.Trainer(kind, dims, fan, precision, n, batch, ws, bs, device=DEV)
+    edges_ref = torch.zeros(steps, dtype=torch.int64, device=DEV)
+    for s in range(steps):
+        ref.step(g, table, labels, targets[s], seed=3, step=s, lr=0.05, gcn_norm_t=nrm, edges_out=edges_ref[s:s + 1])
+    torch.cuda.synchronize()
+    print("[pipeline] two-stage pipelined steps", flush=True)
+    tr = gnn.Trainer(kind, dims, fan, precision, n, batch, ws, bs, device=DEV, prepare_slots=2, one_call=False)
+    edges = torch.zeros(steps, dtype=torch.int64, device=DEV)
+    tr.run_pipelined(g, table, labels, lambda s: targets[s], seed=3, first_step=0, steps=steps, lr=0.05,
+                     gcn_norm_t=nrm, edges_out=edges)
+    torch.cuda.synchronize()
+    assert torch.equal(edges, edges_ref)
+    for a, b in zip(_state(tr), _state(ref)):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    for h in (1, 2):
+        got, want = tr.block_view(h), ref.block_view(h)
+        for key in want:
+            assert np.array_equal(np.asarray(got[key]), np.asarray(want[key])), (h, key)
+
+
+def test_prepare_then_compute_from_pinned_host_fp16_table_matches_oracle():
+    # the host-table model shape (768 -> 1024 -> 153, fanouts 25/15) on a
+    # small R-MAT graph: fp16 table in pinned host memory, read over the host
+    # link by the gather, bf16 GEMMs; one step against the oracle, then a
+    # pipelined run against one-call steps on an HBM copy of the table
+    dims, fan, n, m, batch = (768, 1024, 153), (25, 15), 20_000, 200_000, 64
+    kind = gnn.GNN_AGG_SAGE_MEAN
+    rowptr, col, table, labels, ws, bs, g, targets = _pipeline_inputs(kind, dims, fan, n, m, batch,
+                                                                      table_dtype=torch.float16)
+    pinned = table.pin_memory()
+    print("[host-table] prepare + compute, one step", flush=True)
+    tr = gnn.Trainer(kind, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV, prepare_slots=2, one_call=False)
+    tr.prepare(0, g, pinned, targets[0], seed=1, step=0, loc=gnn.GNN_LOC_HOST_PINNED)
+    tr.compute(0, labels, lr=0.05)
+    torch.cuda.synchronize()
+    cfg = oracle.StepConfig(kind=oracle.SAGE, dims=dims, fanouts=fan, precision=oracle.BF16, seed=1, step=0, lr=0.05)
+    ref = oracle.train_step(rowptr.numpy(), col.numpy(), None, table.numpy(), labels.cpu().numpy(),
+                            targets[0].cpu().numpy(), [w.numpy() for w in ws], [b.numpy() for b in bs], cfg)
+    _check_step(tr, ref, oracle.BF16, 2)
+    x0 = tr.tensor("x0", 0, ref["x0"].shape[0], dims[0], torch.bfloat16).cpu().view(torch.int16).numpy()
+    assert np.array_equal(x0.view(np.uint16), ref["x0"])
+
+    steps = 4
+    print("[host-table] pipelined from the pinned table vs one-call from HBM", flush=True)
+    a = gnn.Trainer(kind, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV, prepare_slots=2, one_call=False)
+    a.run_pipelined(g, pinned, labels, lambda s: targets[s], seed=1, first_step=0, steps=steps, lr=0.05,
+                    loc=gnn.GNN_LOC_HOST_PINNED)
+    b = gnn.Trainer(kind, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV)
+    t_dev = table.to(DEV)
+    for s in range(steps):
+        b.step(g, t_dev, labels, targets[s], seed=1, step=s, lr=0.05)
+    torch.cuda.synchronize()
+    for x, y in zip(_state(a), _state(b)):
+        assert torch.equal(x.view(torch.int32), y.view(torch.int32))
+
