@@ -31,12 +31,12 @@ gnn_status launch_status(const char *what) {
 gnn_status launch_gcn_norm(const gnn_graph *g, float *nrm, hipStream_t s);
 gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_step_layout *o);
 gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
-                          int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
-                          uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
-                          hipStream_t s);
+                          bool host_table, int64_t row_stride, const int64_t *labels, const int64_t *targets,
+                          int64_t batch, uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev,
+                          void *ws, hipStream_t s);
 gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
-                            int tdt, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
-                            uint64_t step, void *prep_ws, hipStream_t s);
+                            int tdt, bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch,
+                            uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s);
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
                             float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s);
 
@@ -212,7 +212,8 @@ gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, in
     GNN_CHECK(aligned(table, dtype_size(tdt)) && aligned(out, dtype_size(odt)), GNN_EINVAL, "%s: misaligned data", who);
     const void *t = nullptr;
     GNN_TRY(device_view(table, loc, &t, who));
-    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, stream_of(s));
+    return launch_gather(t, tdt, dim, row_stride, ids, n_ids_dev, cap_ids, out, odt, loc == GNN_LOC_HOST_PINNED,
+                         stream_of(s));
 }
 
 gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
@@ -425,7 +426,7 @@ gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     GNN_CHECK(ws_bytes >= o.total_bytes, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, o.total_bytes);
     const void *t = nullptr;
     GNN_TRY(device_view(table, loc, &t, who));
-    return run_train_step(m, g, gcn_norm, t, tdt, row_stride, labels, targets, batch, seed, step, lr, loss_dev,
+    return run_train_step(m, g, gcn_norm, t, tdt, loc == GNN_LOC_HOST_PINNED, row_stride, labels, targets, batch, seed, step, lr, loss_dev,
                           edges_dev, ws, stream_of(s));
 }
 
@@ -454,7 +455,7 @@ gnn_status gnn_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
               o.prep_bytes);
     const void *t = nullptr;
     GNN_TRY(device_view(table, loc, &t, who));
-    return run_step_prepare(m, g, gcn_norm, t, tdt, row_stride, targets, batch, seed, step, prep_ws, stream_of(s));
+    return run_step_prepare(m, g, gcn_norm, t, tdt, loc == GNN_LOC_HOST_PINNED, row_stride, targets, batch, seed, step, prep_ws, stream_of(s));
 }
 
 gnn_status gnn_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,

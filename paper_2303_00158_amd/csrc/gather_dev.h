@@ -177,7 +177,14 @@ struct Scalar {
 
 // Workgroups for `cap` rows of `dim` elements: the vector variants give
 // each slot kUnroll rows; the scalar one a thread per element.
-inline unsigned grid_for(int64_t cap, int64_t dim, bool vec) {
+// A table in pinned host memory is read over the host link, which a few
+// hundred wavefronts with several rows in flight each already saturate; a
+// grid sized by the row count would hold every compute unit waiting on the
+// link and keep concurrent work (the compute stage of the previous step) off
+// the GPU.
+constexpr int64_t kHostGrid = 256;
+
+inline unsigned grid_for(int64_t cap, int64_t dim, bool vec, bool host) {
     int64_t b;
     if (vec) {
         const RowSlots rs = RowSlots::of(dim);
@@ -186,6 +193,7 @@ inline unsigned grid_for(int64_t cap, int64_t dim, bool vec) {
         b = ceil_div(cap * dim > 0 ? cap * dim : 1, kThreads);
     }
     if (b > (1 << 20)) b = 1 << 20;
+    if (host && b > kHostGrid) b = kHostGrid;
     return static_cast<unsigned>(b);
 }
 

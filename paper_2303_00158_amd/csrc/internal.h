@@ -139,7 +139,7 @@ gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const 
 
 // Internal launchers reused by the training step (no host validation).
 gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,
-                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, hipStream_t s);
+                         const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, bool host, hipStream_t s);
 gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
                                 hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,

@@ -13,7 +13,8 @@
 // block transposes (CSC), which only the backward pass reads: they run on a
 // helper stream of the library, forked after each block is built and joined
 // before the backward pass, so they overlap the gather and the forward
-// layers.  The separate prepare stage runs them on its own stream.
+// layers.  The separate prepare stage forks them the same way and joins them
+// back into its stream before it ends.
 #include <algorithm>
 #include <mutex>
 
@@ -151,8 +152,8 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
 // a helper (hp), the transposes run on its stream and hp->join is recorded
 // after the last one; without, they run on s.
 gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
-                       int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step,
-                       char *prep, const gnn_step_layout &o, Helper *hp, hipStream_t s) {
+                       bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
+                       uint64_t step, char *prep, const gnn_step_layout &o, Helper *hp, hipStream_t s) {
     (void)batch;
     const int L = m->num_layers;
     const int act = m->precision;
@@ -198,7 +199,7 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     // hop's relabel
     const gnn_block &b0 = blk[L - 1];
     const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0], prep + o.x0};
-    const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act));
+    const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act), host_table);
     gnn_status st = GNN_OK;
     const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
         st = launch_job2(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid, job, ggrid, s,
@@ -288,9 +289,9 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
 
 // The whole step on one stream, the transposes on the helper stream.
 gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
-                          int tdt, int64_t row_stride, const int64_t *labels, const int64_t *targets, int64_t batch,
-                          uint64_t seed, uint64_t step, float lr, float *loss_dev, int64_t *edges_dev, void *ws,
-                          hipStream_t s) {
+                          int tdt, bool host_table, int64_t row_stride, const int64_t *labels,
+                          const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
+                          float *loss_dev, int64_t *edges_dev, void *ws, hipStream_t s) {
     gnn_step_layout o;
     GNN_TRY(step_layout(m, g->n, batch, &o));
     char *prep = static_cast<char *>(ws);
@@ -298,17 +299,23 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     std::lock_guard<std::mutex> lock(g_helper_mu);
     Helper *hp = nullptr;
     if (m->num_layers > 1) GNN_TRY(helper_for_current_device(&hp));
-    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, row_stride, targets, batch, seed, step, prep, o, hp, s));
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, batch, seed, step, prep, o, hp,
+                        s));
     return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, hp, s);
 }
 
 gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
-                            int tdt, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
-                            uint64_t step, void *prep_ws, hipStream_t s) {
+                            int tdt, bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch,
+                            uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s) {
     gnn_step_layout o;
     GNN_TRY(step_layout(m, g->n, batch, &o));
-    return run_prepare(m, g, gcn_norm, table, tdt, row_stride, targets, batch, seed, step,
-                       static_cast<char *>(prep_ws), o, nullptr, s);
+    std::lock_guard<std::mutex> lock(g_helper_mu);
+    Helper *hp = nullptr;
+    if (m->num_layers > 1) GNN_TRY(helper_for_current_device(&hp));
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, batch, seed, step,
+                        static_cast<char *>(prep_ws), o, hp, s));
+    if (hp) GNN_HIP(hipStreamWaitEvent(s, hp->join, 0));  // the stage ends when the transposes are done
+    return GNN_OK;
 }
 
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
