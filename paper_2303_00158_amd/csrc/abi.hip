@@ -3,6 +3,7 @@
 #include <cstdarg>
 #include <cstdio>
 
+#include "csc_dev.h"
 #include "internal.h"
 
 namespace gnn {
@@ -186,10 +187,13 @@ gnn_status gnn_build_block(const gnn_graph *g, const float *gcn_norm, const int6
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
     const size_t need = sampler_ws_bytes(g->n, out->cap_dst, fanout);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
-    void *csc_ws = want_csc ? sampler_csc_ws(ws, g->n, out->cap_dst, fanout) : nullptr;
-    GNN_TRY(launch_build_block(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, out, ws, csc_ws,
-                               stream_of(s)));
-    return want_csc ? launch_block_csc(out, csc_ws, out->cap_dst * fanout, stream_of(s)) : GNN_OK;
+    csc::Args ca{};
+    if (want_csc)
+        ca = csc_args(out, sampler_csc_ws(ws, g->n, out->cap_dst, fanout), src_bound(g->n, out->cap_dst, fanout),
+                      out->cap_dst * fanout);
+    GNN_TRY(launch_build_block(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, out, ws,
+                               want_csc ? &ca : nullptr, stream_of(s)));
+    return want_csc ? launch_block_csc(ca, stream_of(s)) : GNN_OK;
 }
 
 gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, int64_t n_rows, int64_t dim,

@@ -168,15 +168,17 @@ gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const in
 gnn_status launch_sgd(float *w, const float *dw, int64_t n, float lr, hipStream_t s);
 size_t sampler_ws_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout);
 gnn_status launch_sampler_ws_init(void *ws, int64_t graph_n, hipStream_t s);
-// Builds the block's CSR part (ids, row pointer, columns, norms).  csc_ws
-// (may be null) receives the row of every edge for a later
-// launch_block_csc with the same csc_ws, of block_csc_ws_bytes(scratch_nnz)
-// bytes for a scratch_nnz of at least cap_dst * fanout.
+// Builds the block's CSR part (ids, row pointer, columns, norms).  With csc
+// (the block's transpose arguments, csc_dev.h) the relabel also records the
+// edges' rows and counts the columns for a later launch_block_csc.
+namespace csc {
+struct Args;
+}
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              const gnn_block *out, void *ws, void *csc_ws, hipStream_t s);
-size_t block_csc_ws_bytes(int64_t cap_nnz);
-gnn_status launch_block_csc(const gnn_block *out, void *csc_ws, int64_t scratch_nnz, hipStream_t s);
+                              const gnn_block *out, void *ws, const csc::Args *csc, hipStream_t s);
+// Bound on a block's sources (gnn_block_bounds).
+int64_t src_bound(int64_t graph_n, int64_t cap_dst, int32_t fanout);
 // The transpose scratch inside a sampler workspace (for standalone calls).
 void *sampler_csc_ws(void *ws, int64_t graph_n, int64_t cap_dst, int32_t fanout);
 

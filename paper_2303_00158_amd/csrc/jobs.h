@@ -30,6 +30,53 @@ __global__ void __launch_bounds__(256) job2_kernel(A a, unsigned na, unsigned na
     }
 }
 
+// Any number of roles in one launch: Pack<J0, J1, ...> gives each role a
+// range of workgroups, every range but the last padded to a multiple of 8
+// (as in job2_kernel).  A role with zero workgroups takes none.
+template <class... J> struct Pack;
+template <> struct Pack<> {
+    __device__ void run(unsigned) const {}
+    unsigned grid() const { return 0; }
+};
+template <class J, class... R> struct Pack<J, R...> {
+    J j;
+    unsigned n, npad;
+    Pack<R...> rest;
+    __device__ void run(unsigned b) const {
+        if (b < npad) {
+            if (b < n) j.run(b, n);
+        } else {
+            rest.run(b - npad);
+        }
+    }
+    unsigned grid() const {
+        const unsigned g = rest.grid();
+        return g == 0 ? n : npad + g;  // the last non-empty role needs no padding
+    }
+};
+
+// A role of a packed launch: a job and its workgroup count.
+template <class J> struct Role {
+    J j;
+    unsigned n;
+};
+template <class J> Role<J> role(const J &j, unsigned n) { return Role<J>{j, n}; }
+
+inline Pack<> make_pack() { return Pack<>{}; }
+template <class J, class... R> Pack<J, R...> make_pack(const Role<J> &r, const Role<R> &...rest) {
+    Pack<J, R...> p;
+    p.j = r.j;
+    p.n = r.n;
+    p.npad = (r.n + 7) / 8 * 8;
+    p.rest = make_pack(rest...);
+    return p;
+}
+
+template <class P>
+__global__ void __launch_bounds__(256) pack_kernel(P p) {
+    p.run(blockIdx.x);
+}
+
 template <class J>
 gnn_status launch_job(const J &j, unsigned grid, hipStream_t s, const char *what) {
     if (grid == 0) return GNN_OK;
@@ -43,6 +90,16 @@ gnn_status launch_job2(const A &a, unsigned na, const B &b, unsigned nb, hipStre
     if (nb == 0) return launch_job(a, na, s, what);
     const unsigned pad = (na + 7) / 8 * 8;
     job2_kernel<A, B><<<pad + nb, 256, 0, s>>>(a, na, pad, b);
+    return launch_status(what);
+}
+
+// Launches the roles together (in one kernel) on s.
+template <class... J>
+gnn_status launch_jobs(hipStream_t s, const char *what, const Role<J> &...roles) {
+    const auto p = make_pack(roles...);
+    const unsigned grid = p.grid();
+    if (grid == 0) return GNN_OK;
+    pack_kernel<decltype(p)><<<grid, 256, 0, s>>>(p);
     return launch_status(what);
 }
 

@@ -11,8 +11,10 @@
 //                order: every vertex that was sampled and is not a
 //                destination becomes the next new source (so new sources
 //                come out in ascending id order); both bitmaps are cleared.
-//   3. relabel   one thread per staged sample: local index via the map.
-//   4. transpose one workgroup: stable radix sort of the edges by source.
+//   3. relabel   one thread per staged sample: local index via the map
+//                (and, for a block with a transpose, the count phase of the
+//                transpose).
+//   4. transpose scan, place and sort phases (csc_dev.h).
 // The scans in step 2 are single-pass: workgroups take tickets in the order
 // they start and add the prefix of earlier tickets (decoupled look-back,
 // one wavefront reading 64 predecessors at a time), so a workgroup only
@@ -26,14 +28,14 @@
 //   dbits uint32[W]        one bit per vertex: "destination"
 //   ... per-call scratch
 // Both bitmaps are all zero between calls; each call clears the words it set.
+#include "csc_dev.h"
+#include "jobs.h"
 #include "sampler_dev.h"
 
 namespace gnn {
 
 namespace {
 
-constexpr int kSortThreads = 1024;
-constexpr int kSortWaves = kSortThreads / 64;
 using namespace samp;
 
 __global__ void gcn_norm_kernel(const int64_t *__restrict__ rowptr, int64_t n, float *__restrict__ nrm) {
@@ -58,114 +60,6 @@ __global__ void __launch_bounds__(kThreads) hop_emit_kernel(HopArgs a) { hop_emi
 
 __global__ void __launch_bounds__(kThreads) hop_relabel_kernel(HopArgs a) {
     hop_relabel_body(a, blockIdx.x, gridDim.x);
-}
-
-// 4. stable transpose in one workgroup: LSD radix sort of (source, row) by
-// source, 8 bits per pass.  Each wavefront owns a contiguous segment of the
-// edge list; per pass the segments' digit histograms give every (segment,
-// digit) its output offset, and the segments are scattered in order with
-// ballot-based ranks, which keeps equal keys in edge order.  Then the row
-// pointer of the transpose is read off the sorted keys.
-__global__ void __launch_bounds__(kSortThreads) csc_build_kernel(const int32_t *__restrict__ keys_in,
-                                                                  const int32_t *__restrict__ vals_in,
-                                                                  const int64_t *__restrict__ counts, int key_bits,
-                                                                  int32_t *ka, int32_t *va, int32_t *kb, int32_t *vb,
-                                                                  int32_t *__restrict__ cscrow,
-                                                                  int64_t *__restrict__ cscptr) {
-    __shared__ int hist[kSortWaves][256];
-    __shared__ int tot[256];
-    const int64_t n = counts[2], n_src = counts[1];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t seg = ceil_div(ceil_div(n > 0 ? n : 1, kSortWaves), 64) * 64;
-    const int64_t chunks = seg / 64;
-    const int passes = key_bits <= 8 ? 1 : (key_bits + 7) / 8;
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int32_t *ks = keys_in, *vs = vals_in;
-    int32_t *kfinal = ka;
-    for (int p = 0; p < passes; ++p) {
-        const int shift = 8 * p;
-        const bool last = p == passes - 1;
-        int32_t *kd = (p % 2 == 0) ? ka : kb;
-        int32_t *vd = last ? cscrow : ((p % 2 == 0) ? va : vb);
-        for (int d = threadIdx.x; d < kSortWaves * 256; d += kSortThreads) (&hist[0][0])[d] = 0;
-        __syncthreads();
-        const int64_t s0 = wave * seg;
-        const int64_t s1 = min(n, s0 + seg);
-        for (int64_t q0 = s0 + lane; q0 < s1; q0 += 4 * 64) {
-            int32_t kk[4];
-#pragma unroll
-            for (int b = 0; b < 4; ++b) kk[b] = ks[min(q0 + b * 64, s1 - 1)];
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-                if (q0 + b * 64 < s1) atomicAdd(&hist[wave][(kk[b] >> shift) & 255], 1);
-        }
-        __syncthreads();
-        if (threadIdx.x < 256) {
-            int s = 0;
-            for (int w = 0; w < kSortWaves; ++w) s += hist[w][threadIdx.x];
-            tot[threadIdx.x] = s;
-        }
-        __syncthreads();
-        if (threadIdx.x < 256) {
-            int base = 0;
-            for (int d = 0; d < static_cast<int>(threadIdx.x); ++d) base += tot[d];
-            for (int w = 0; w < kSortWaves; ++w) {
-                const int h = hist[w][threadIdx.x];
-                hist[w][threadIdx.x] = base;
-                base += h;
-            }
-        }
-        __syncthreads();
-        int32_t kb[4], vb4[4];
-        for (int64_t ch = 0; ch < chunks; ++ch) {
-            const int64_t q = s0 + ch * 64 + lane;
-            const bool valid = q < n && q < s0 + seg;
-            if ((ch & 3) == 0) {
-                // load the next four chunks of this segment at once
-#pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const int64_t qb = q + b * 64;
-                    const int64_t qc = (qb < n) ? qb : (n > 0 ? n - 1 : 0);
-                    kb[b] = ks[qc];
-                    vb4[b] = vs[qc];
-                }
-            }
-            const int32_t key = valid ? kb[ch & 3] : 0;
-            const int32_t val = valid ? vb4[ch & 3] : 0;
-            const int d = (key >> shift) & 255;
-            uint64_t peers = __ballot(valid);
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const bool bit = (d >> b) & 1;
-                const uint64_t m = __ballot(valid && bit);
-                peers &= bit ? m : ~m;
-            }
-            const int rank = __popcll(peers & lt);
-            const int at = valid ? hist[wave][d] : 0;
-            __syncthreads();
-            if (valid) {
-                kd[at + rank] = key;
-                vd[at + rank] = val;
-                if (rank == 0) hist[wave][d] = at + __popcll(peers);
-            }
-            __syncthreads();
-        }
-        __threadfence_block();
-        __syncthreads();
-        ks = kd;
-        vs = vd;
-        kfinal = kd;
-    }
-    // cscptr[j] = first position of key j
-    if (n == 0) {
-        for (int64_t j = threadIdx.x; j <= n_src; j += kSortThreads) cscptr[j] = 0;
-        return;
-    }
-    for (int64_t pos = threadIdx.x; pos <= n; pos += kSortThreads) {
-        const int64_t lo = (pos == 0) ? -1 : kfinal[pos - 1];
-        const int64_t hi = (pos == n) ? n_src : kfinal[pos];
-        for (int64_t j = lo + 1; j <= hi; ++j) cscptr[j] = pos;
-    }
 }
 
 // Shared part: depends on graph_n only, so one serves hops of any size.
@@ -198,7 +92,7 @@ HopWs hop_layout(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
     w.cnt = c.take(static_cast<size_t>(cap_dst > 0 ? cap_dst : 1) * 4);
     w.status = c.take(static_cast<size_t>(nb_rows + nb_bits) * 8);
     w.ticket = c.take(4);
-    w.csc = c.take(block_csc_ws_bytes(cap_nnz));
+    w.csc = c.take(block_csc_ws_bytes(src_bound(graph_n, cap_dst, fanout), cap_nnz));
     w.total = round_up(c.off, 256);
     return w;
 }
@@ -209,18 +103,64 @@ unsigned grid_for(int64_t items, int threads, int64_t max_blocks = 1 << 20) {
     return static_cast<unsigned>(b);
 }
 
-int bits_for(int64_t v) {  // bits needed to represent values in [0, v)
-    int b = 0;
-    while (b < 62 && (1ll << b) < v) ++b;
-    return b;
+// Transpose scratch: edge rows, column counters, scan look-back state.
+struct CscWs {
+    size_t erow, cnt, status, ticket, total;
+    int64_t nb_scan;
+};
+CscWs csc_layout(int64_t cap_src, int64_t cap_nnz) {
+    CscWs w;
+    w.nb_scan = ceil_div(cap_src + 1, csc::kScanTile);
+    Carver c(nullptr);
+    w.erow = c.take(static_cast<size_t>(std::max<int64_t>(cap_nnz, 1)) * 4);
+    w.cnt = c.take(static_cast<size_t>(std::max<int64_t>(cap_src, 1)) * 4);
+    w.status = c.take(static_cast<size_t>(w.nb_scan) * 8);
+    w.ticket = c.take(4);
+    w.total = round_up(c.off, 256);
+    return w;
 }
 
 }  // namespace
 
-// Transpose scratch: the row of every edge, then two key / value ping-pong
-// pairs for the radix sort.
-size_t block_csc_ws_bytes(int64_t cap_nnz) {
-    return round_up(static_cast<size_t>(std::max<int64_t>(cap_nnz, 1)) * 4 * 5, 256);
+// Bound on a block's sources: destinations plus sampled edges, at most the
+// graph (the capacity rule of gnn_block_bounds).
+int64_t src_bound(int64_t graph_n, int64_t cap_dst, int32_t fanout) {
+    return std::min<int64_t>(cap_dst + cap_dst * fanout, std::max<int64_t>(graph_n, cap_dst));
+}
+
+size_t block_csc_ws_bytes(int64_t cap_src, int64_t cap_nnz) { return csc_layout(cap_src, cap_nnz).total; }
+
+csc::Args csc_args(const gnn_block *out, void *csc_ws, int64_t ws_src, int64_t ws_nnz) {
+    const CscWs w = csc_layout(ws_src, ws_nnz);
+    char *base = static_cast<char *>(csc_ws);
+    csc::Args a;
+    a.counts = out->counts;
+    a.bcol = out->col;
+    a.erow = reinterpret_cast<int32_t *>(base + w.erow);
+    a.cap_src = std::min(out->cap_src, ws_src);
+    a.cap_nnz = std::min(out->cap_nnz, ws_nnz);
+    a.cnt = reinterpret_cast<int32_t *>(base + w.cnt);
+    a.status = reinterpret_cast<uint64_t *>(base + w.status);
+    a.ticket = reinterpret_cast<int *>(base + w.ticket);
+    a.nb_scan = ceil_div(a.cap_src + 1, csc::kScanTile);
+    a.cscptr = out->cscptr;
+    a.cscrow = out->cscrow;
+    return a;
+}
+
+csc::Grids csc_grids(const csc::Args &a) {
+    csc::Grids g;
+    g.scan = static_cast<unsigned>(a.nb_scan);
+    g.place = grid_for(a.cap_nnz, csc::kThreads, 2048);
+    g.sort = grid_for(ceil_div(a.cap_src, 64), csc::kThreads / 64, 2048);
+    return g;
+}
+
+gnn_status launch_block_csc(const csc::Args &a, hipStream_t s) {
+    const csc::Grids g = csc_grids(a);
+    GNN_TRY(launch_job(csc::ScanJob{a}, g.scan, s, "csc_scan"));
+    GNN_TRY(launch_job(csc::PlaceJob{a}, g.place, s, "csc_place"));
+    return launch_job(csc::SortJob{a}, g.sort, s, "csc_sort");
 }
 
 size_t sampler_shared_bytes(int64_t graph_n) { return shared_layout(graph_n).total; }
@@ -258,7 +198,7 @@ void *sampler_csc_ws(void *ws, int64_t graph_n, int64_t cap_dst, int32_t fanout)
 
 samp::HopPlan plan_hop(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids, const int64_t *n_dst_dev,
                        int32_t fanout, uint64_t seed, uint64_t step, int32_t hop, const gnn_block *out, void *shared,
-                       void *scratch, void *csc_ws) {
+                       void *scratch, const csc::Args *csc) {
     const SharedWs w = shared_layout(g->n);
     const HopWs hw = hop_layout(g->n, out->cap_dst, fanout);
     char *base = static_cast<char *>(shared);
@@ -286,7 +226,12 @@ samp::HopPlan plan_hop(const gnn_graph *g, const float *gcn_norm, const int64_t 
     a.words = ceil_div(g->n > 0 ? g->n : 1, 32);
     a.gpad = reinterpret_cast<int64_t *>(hbase + hw.gpad);
     a.cnt = reinterpret_cast<int32_t *>(hbase + hw.cnt);
-    a.erow = static_cast<int32_t *>(csc_ws);
+    a.erow = csc ? csc->erow : nullptr;
+    a.csc_cnt = csc ? csc->cnt : nullptr;
+    a.csc_cap_src = csc ? csc->cap_src : 0;
+    a.csc_status = csc ? csc->status : nullptr;
+    a.csc_ticket = csc ? csc->ticket : nullptr;
+    a.csc_nb = csc ? csc->nb_scan : 0;
     a.status = reinterpret_cast<uint64_t *>(hbase + hw.status);
     a.ticket = reinterpret_cast<int *>(hbase + hw.ticket);
     a.nb_rows = ceil_div(out->cap_dst > 0 ? out->cap_dst : 1, kThreads);
@@ -318,25 +263,14 @@ gnn_status launch_hop_emit(const samp::HopPlan &p, hipStream_t s) {
 
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
-                              const gnn_block *out, void *ws, void *csc_ws, hipStream_t s) {
+                              const gnn_block *out, void *ws, const csc::Args *csc, hipStream_t s) {
     void *scratch = static_cast<char *>(ws) + sampler_shared_bytes(g->n);
     const samp::HopPlan p =
-        plan_hop(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, out, ws, scratch, csc_ws);
+        plan_hop(g, gcn_norm, dst_ids, n_dst_dev, fanout, seed, step, hop, out, ws, scratch, csc);
     GNN_TRY(launch_hop_prepare(p, s));
     GNN_TRY(launch_hop_emit(p, s));
     hop_relabel_kernel<<<p.relabel_grid, kThreads, 0, s>>>(p.a);
     GNN_LAUNCHED("hop_relabel");
-    return GNN_OK;
-}
-
-gnn_status launch_block_csc(const gnn_block *out, void *csc_ws, int64_t scratch_nnz, hipStream_t s) {
-    const int64_t cap_nnz = std::max<int64_t>(scratch_nnz, 1);
-    int32_t *erow = static_cast<int32_t *>(csc_ws);
-    int32_t *sort = erow + cap_nnz;
-    csc_build_kernel<<<1, kSortThreads, 0, s>>>(out->col, erow, out->counts, bits_for(out->cap_src), sort,
-                                                sort + cap_nnz, sort + 2 * cap_nnz, sort + 3 * cap_nnz, out->cscrow,
-                                                out->cscptr);
-    GNN_LAUNCHED("csc_build");
     return GNN_OK;
 }
 

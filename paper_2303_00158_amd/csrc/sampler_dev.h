@@ -6,6 +6,9 @@
 #include "internal.h"
 
 namespace gnn {
+namespace csc {
+struct Args;
+}
 namespace samp {
 
 constexpr int kThreads = 256;
@@ -122,6 +125,13 @@ struct HopArgs {
     uint64_t *status;   // [nb_rows + nb_bits] look-back words
     int *ticket;
     int64_t nb_rows, nb_bits;
+    // count phase of the transpose (when erow is set): per-column counters
+    // and the transpose scan's look-back state, reset by the prepare
+    int32_t *csc_cnt;
+    int64_t csc_cap_src;
+    uint64_t *csc_status;
+    int *csc_ticket;
+    int64_t csc_nb;
 };
 
 __device__ __forceinline__ void set_bit(uint32_t *bm, int64_t v) {
@@ -135,8 +145,14 @@ __device__ __forceinline__ void hop_prepare_body(const HopArgs &a, int64_t blk, 
     const int64_t gtid = blk * kThreads + threadIdx.x;
     const int64_t gsize = nblk * kThreads;
     const int64_t n_dst = a.n_dst_dev ? min(*a.n_dst_dev, a.cap_dst) : a.cap_dst;
-    // reset the look-back state of the emit kernel
+    // reset the look-back state of the emit kernel and, for a block with a
+    // transpose, its column counters and scan state
     for (int64_t i = gtid; i < a.nb_rows + a.nb_bits; i += gsize) a.status[i] = 0;
+    if (a.erow) {
+        for (int64_t i = gtid; i < a.csc_cap_src; i += gsize) a.csc_cnt[i] = 0;
+        for (int64_t i = gtid; i < a.csc_nb; i += gsize) a.csc_status[i] = 0;
+        if (gtid == 0) *a.csc_ticket = 0;
+    }
     if (gtid == 0) {
         *a.ticket = 0;
         a.counts[0] = n_dst;
@@ -282,15 +298,25 @@ __device__ __forceinline__ void hop_emit_body(const HopArgs &a) {
 }
 
 // 3. local source index of every sampled edge.
+// With the transpose requested, also the row of every edge and the count
+// phase of the transpose (per-column counts).
 __device__ __forceinline__ void hop_relabel_body(const HopArgs &a, int64_t blk, int64_t nblk) {
     const int64_t n_dst = a.counts[0];
     const int64_t total = n_dst * a.k;
-    for (int64_t q = blk * kThreads + threadIdx.x; q < total; q += nblk * kThreads) {
+    const int64_t gtid = blk * kThreads + threadIdx.x, gsize = nblk * kThreads;
+    for (int64_t q = gtid; q < total; q += gsize) {
         const int64_t i = q / a.k, t = q - i * a.k;
         if (t >= a.cnt[i]) continue;
         const int64_t e = a.brow[i] + t;
-        a.bcol[e] = a.map[a.gpad[q]];
-        if (a.erow) a.erow[e] = static_cast<int32_t>(i);
+        const int32_t c = a.map[a.gpad[q]];
+        a.bcol[e] = c;
+        if (a.erow) {
+            a.erow[e] = static_cast<int32_t>(i);
+            if (c >= 0 && c < a.csc_cap_src)
+                atomicAdd(&a.csc_cnt[c], 1);
+            else
+                a.counts[3] = 1;
+        }
     }
 }
 
@@ -302,6 +328,11 @@ template <int R> struct PrepareJob {
 struct RelabelJob {
     HopArgs a;
     __device__ void run(int64_t blk, int64_t nblk) const { hop_relabel_body(a, blk, nblk); }
+};
+// Workgroups order themselves by ticket: the logical index is not used.
+struct EmitJob {
+    HopArgs a;
+    __device__ void run(int64_t, int64_t) const { hop_emit_body(a); }
 };
 
 // Launch parameters of one hop.
@@ -330,9 +361,11 @@ template <class F> void with_prepare_job(const HopPlan &p, F &&f) {
 // scratch.
 size_t sampler_shared_bytes(int64_t graph_n);
 size_t sampler_hop_bytes(int64_t graph_n, int64_t cap_dst, int32_t fanout);
+// csc: the transpose's arguments when the hop's block gets one (the relabel
+// then runs its count phase), else null.
 samp::HopPlan plan_hop(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids, const int64_t *n_dst_dev,
                        int32_t fanout, uint64_t seed, uint64_t step, int32_t hop, const gnn_block *out, void *shared,
-                       void *scratch, void *csc_ws);
+                       void *scratch, const csc::Args *csc);
 gnn_status launch_hop_prepare(const samp::HopPlan &p, hipStream_t s);
 gnn_status launch_hop_emit(const samp::HopPlan &p, hipStream_t s);
 }  // namespace gnn

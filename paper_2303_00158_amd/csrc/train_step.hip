@@ -9,16 +9,14 @@
 // runs, which hides the feature loading from a host-resident table (two-stage
 // feature prefetching, Section IV-B).
 //
-// In the one-call step everything runs on the caller's stream except the
-// block transposes (CSC), which only the backward pass reads: they run on a
-// helper stream of the library, forked after each block is built and joined
-// before the backward pass, so they overlap the gather and the forward
-// layers.  The separate prepare stage forks them the same way and joins them
-// back into its stream before it ends.
+// Everything runs on the caller's stream.  The block transposes (CSC), which
+// only the backward pass reads, cost no launch of their own: their phases
+// (csc_dev.h) ride along with the sampling launches of later hops, and the
+// last sort with the loss (or, in a separate prepare stage, at its end).
 #include <algorithm>
-#include <mutex>
 
 #include "aggregate_dev.h"
+#include "csc_dev.h"
 #include "gather_dev.h"
 #include "gemm_bwd_dev.h"
 #include "internal.h"
@@ -29,34 +27,6 @@
 namespace gnn {
 
 namespace {
-
-// One helper stream and its events per device, created on first use and
-// kept until the process ends.  g_helper_mu serialises training-step
-// enqueues, which share them.
-struct Helper {
-    bool ready = false;
-    hipStream_t stream = nullptr;
-    hipEvent_t fork[GNN_MAX_LAYERS] = {};
-    hipEvent_t join = nullptr;
-};
-constexpr int kMaxDevices = 64;
-std::mutex g_helper_mu;
-Helper g_helper[kMaxDevices];
-
-gnn_status helper_for_current_device(Helper **out) {
-    int dev = 0;
-    GNN_HIP(hipGetDevice(&dev));
-    GNN_CHECK(dev >= 0 && dev < kMaxDevices, GNN_EUNSUPPORTED, "train_step: device %d out of range", dev);
-    Helper &h = g_helper[dev];
-    if (!h.ready) {
-        GNN_HIP(hipStreamCreateWithFlags(&h.stream, hipStreamNonBlocking));
-        for (int i = 0; i < GNN_MAX_LAYERS; ++i) GNN_HIP(hipEventCreateWithFlags(&h.fork[i], hipEventDisableTiming));
-        GNN_HIP(hipEventCreateWithFlags(&h.join, hipEventDisableTiming));
-        h.ready = true;
-    }
-    *out = &h;
-    return GNN_OK;
-}
 
 int64_t k_of(const gnn_model *m, int l) {  // reduction width of layer l (1-based)
     const int64_t f = m->dims[l - 1];
@@ -97,7 +67,7 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
             o->blk_cscrow[h] = c.take(static_cast<size_t>(std::max<int64_t>(o->cap_nnz[h], 1)) * 4);
         }
         if (m->kind == GNN_AGG_GCN_SYM) o->blk_src_norm[h] = c.take(static_cast<size_t>(o->cap_src[h]) * 4);
-        if (h < L - 1) o->blk_csc_ws[h] = c.take(block_csc_ws_bytes(o->cap_nnz[h]));
+        if (h < L - 1) o->blk_csc_ws[h] = c.take(block_csc_ws_bytes(o->cap_src[h], o->cap_nnz[h]));
     }
     o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
     o->prep_bytes = round_up(c.off, 256);
@@ -148,21 +118,32 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
     for (int h = 0; h < m->num_layers; ++h) blk[h] = block_view(o, h, prep);
 }
 
-// Sampling of all hops and the gather of X' into a prepare workspace.  With
-// a helper (hp), the transposes run on its stream and hp->join is recorded
-// after the last one; without, they run on s.
+// Sampling of all hops and the gather of X' into a prepare workspace, with
+// the transposes of blocks 1 .. L-1 (0-based hops 0 .. L-2).  Launches, for
+// hop h >= 1 (relabel(h) also counts the columns of block h's transpose):
+//   A_h = relabel(h-1) + prepare(h) + place(h-2)
+//   B_h = emit(h) + scan(h-1) + sort(h-2)
+//   F   = relabel(L-1) + gather + place(L-2)
+// The sort of block L-2 is left to the caller (*last_sort; n = 0 if none).
 gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
-                       bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch, uint64_t seed,
-                       uint64_t step, char *prep, const gnn_step_layout &o, Helper *hp, hipStream_t s) {
-    (void)batch;
+                       bool host_table, int64_t row_stride, const int64_t *targets, uint64_t seed, uint64_t step,
+                       char *prep, const gnn_step_layout &o, Role<csc::SortJob> *last_sort, hipStream_t s) {
     const int L = m->num_layers;
     const int act = m->precision;
     gnn_block blk[GNN_MAX_LAYERS];
     block_views(m, o, prep, blk);
+    csc::Args ca[GNN_MAX_LAYERS] = {};
+    csc::Grids cg[GNN_MAX_LAYERS] = {};
+    for (int h = 0; h + 1 < L; ++h) {
+        ca[h] = csc_args(&blk[h], prep + o.blk_csc_ws[h], o.cap_src[h], o.cap_nnz[h]);
+        cg[h] = csc_grids(ca[h]);
+    }
+    auto place = [&](int h) { return role(csc::PlaceJob{ca[h >= 0 ? h : 0]}, h >= 0 ? cg[h].place : 0u); };
+    auto scan = [&](int h) { return role(csc::ScanJob{ca[h >= 0 ? h : 0]}, h >= 0 ? cg[h].scan : 0u); };
+    auto sort = [&](int h) { return role(csc::SortJob{ca[h >= 0 ? h : 0]}, h >= 0 ? cg[h].sort : 0u); };
 
-    // sampling: hop 1 around the targets, then outwards.  Hop h's relabel
-    // shares a launch with hop h+1's prepare (both only need hop h's
-    // sources), and the last hop's relabel shares one with the gather.
+    // hop 1 around the targets, then outwards; hop h's relabel only needs
+    // hop h's sources, like hop h+1's prepare
     char *shared = prep + o.sampler_ws;
     size_t hop_max = 0;
     for (int h = 0; h < L; ++h)
@@ -172,29 +153,22 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
         const int64_t *dst = h == 0 ? targets : blk[h - 1].src_ids;
         const int64_t *n_dst = h == 0 ? nullptr : blk[h - 1].counts + 1;
         void *scratch = shared + sampler_shared_bytes(g->n) + (h % 2) * hop_max;
-        void *csc_ws = h < L - 1 ? prep + o.blk_csc_ws[h] : nullptr;
         plan[h] = plan_hop(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h], seed, step,
-                           h + 1, &blk[h], shared, scratch, csc_ws);
+                           h + 1, &blk[h], shared, scratch, h + 1 < L ? &ca[h] : nullptr);
     }
-    auto csc = [&](int h) -> gnn_status {
-        if (!hp) return launch_block_csc(&blk[h], prep + o.blk_csc_ws[h], o.cap_nnz[h], s);
-        GNN_HIP(hipEventRecord(hp->fork[h], s));
-        GNN_HIP(hipStreamWaitEvent(hp->stream, hp->fork[h], 0));
-        return launch_block_csc(&blk[h], prep + o.blk_csc_ws[h], o.cap_nnz[h], hp->stream);
-    };
     GNN_TRY(launch_hop_prepare(plan[0], s));
     GNN_TRY(launch_hop_emit(plan[0], s));
     for (int h = 1; h < L; ++h) {
         gnn_status st = GNN_OK;
         samp::with_prepare_job(plan[h], [&](auto job) {
-            st = launch_job2(samp::RelabelJob{plan[h - 1].a}, plan[h - 1].relabel_grid, job, plan[h].prep_grid, s,
-                             "hop_relabel+prepare");
+            st = launch_jobs(s, "hop_relabel+prepare+csc_place", role(samp::RelabelJob{plan[h - 1].a},
+                                                                       plan[h - 1].relabel_grid),
+                             role(job, plan[h].prep_grid), place(h - 2));
         });
         GNN_TRY(st);
-        GNN_TRY(csc(h - 1));
-        GNN_TRY(launch_hop_emit(plan[h], s));
+        GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", role(samp::EmitJob{plan[h].a}, plan[h].emit_grid),
+                            scan(h - 1), sort(h - 2)));
     }
-    if (hp) GNN_HIP(hipEventRecord(hp->join, hp->stream));
     // feature loading (rows of the input layer's sources) with the last
     // hop's relabel
     const gnn_block &b0 = blk[L - 1];
@@ -202,18 +176,22 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act), host_table);
     gnn_status st = GNN_OK;
     const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
-        st = launch_job2(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid, job, ggrid, s,
-                         "hop_relabel+gather");
+        st = launch_jobs(s, "hop_relabel+gather+csc_place",
+                         role(samp::RelabelJob{plan[L - 1].a}, plan[L - 1].relabel_grid), role(job, ggrid),
+                         place(L - 2));
     });
     GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
+    *last_sort = sort(L - 2);
     return st;
 }
 
 // Forward, loss, backward and SGD from a prepared workspace.  The targets are
-// the first rows of hop 1's sources (destinations come first).  With a
-// helper, the backward pass waits for hp->join (the transposes).
+// the first rows of hop 1's sources (destinations come first).  pending is
+// a transpose sort still to run (n = 0 if none); it shares the loss launch,
+// before the backward pass reads the transposes.
 gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch, float lr, float *loss_dev,
-                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o, Helper *hp,
+                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o,
+                       const Role<csc::SortJob> &pending,
                        hipStream_t s) {
     const int L = m->num_layers;
     const int act = m->precision;
@@ -236,15 +214,17 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     // loss on the targets: gradient and row losses now, the mean with the
     // last kernel of the step
     float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
-    GNN_TRY(launch_job(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L], labels,
-                                        blk[0].src_ids, reinterpret_cast<float *>(comp + o.grad[L]), row_loss},
-                       static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64)), s, "softmax_ce"));
+    GNN_TRY(launch_jobs(s, "softmax_ce+csc_sort",
+                        role(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L],
+                                              labels, blk[0].src_ids, reinterpret_cast<float *>(comp + o.grad[L]),
+                                              row_loss},
+                             static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64))),
+                        pending));
     // backward (reads the transposes).  Per layer: the dA and dW GEMMs in
     // one launch, then the dW reduction (with SGD on W^l, b^l and the
     // shadow) in one launch with the aggregation backward of the layer, or
     // with the end of the step for layer 1.  Every later step reads only
     // lower layers' weights.
-    if (hp) GNN_HIP(hipStreamWaitEvent(s, hp->join, 0));
     loss::TailJob tail{};
     for (int h = 0; h < L; ++h) tail.counts[h] = blk[h].counts;
     tail.num_blocks = L;
@@ -287,7 +267,7 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
 
 }  // namespace
 
-// The whole step on one stream, the transposes on the helper stream.
+// The whole step on one stream.
 gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
                           int tdt, bool host_table, int64_t row_stride, const int64_t *labels,
                           const int64_t *targets, int64_t batch, uint64_t seed, uint64_t step, float lr,
@@ -296,12 +276,10 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     GNN_TRY(step_layout(m, g->n, batch, &o));
     char *prep = static_cast<char *>(ws);
     char *comp = prep + o.prep_bytes;
-    std::lock_guard<std::mutex> lock(g_helper_mu);
-    Helper *hp = nullptr;
-    if (m->num_layers > 1) GNN_TRY(helper_for_current_device(&hp));
-    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, batch, seed, step, prep, o, hp,
+    Role<csc::SortJob> pending{};
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step, prep, o, &pending,
                         s));
-    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, hp, s);
+    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, pending, s);
 }
 
 gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
@@ -309,13 +287,10 @@ gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
                             uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s) {
     gnn_step_layout o;
     GNN_TRY(step_layout(m, g->n, batch, &o));
-    std::lock_guard<std::mutex> lock(g_helper_mu);
-    Helper *hp = nullptr;
-    if (m->num_layers > 1) GNN_TRY(helper_for_current_device(&hp));
-    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, batch, seed, step,
-                        static_cast<char *>(prep_ws), o, hp, s));
-    if (hp) GNN_HIP(hipStreamWaitEvent(s, hp->join, 0));  // the stage ends when the transposes are done
-    return GNN_OK;
+    Role<csc::SortJob> pending{};
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step,
+                        static_cast<char *>(prep_ws), o, &pending, s));
+    return launch_job(pending.j, pending.n, s, "csc_sort");  // the stage ends with complete transposes
 }
 
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
@@ -323,7 +298,7 @@ gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *
     gnn_step_layout o;
     GNN_TRY(step_layout(m, graph_n, batch, &o));
     return run_compute(m, labels, batch, lr, loss_dev, edges_dev, static_cast<char *>(prep_ws),
-                       static_cast<char *>(comp_ws), o, nullptr, s);
+                       static_cast<char *>(comp_ws), o, Role<csc::SortJob>{}, s);
 }
 
 }  // namespace gnn

@@ -218,6 +218,10 @@ def sampler_workspace(graph_n: int, cap_dst: int, fanout: int, device, stream=No
 def build_block(graph: DeviceGraph, dst_ids: torch.Tensor, fanout: int, seed: int, step: int, hop: int,
                 out: DeviceBlock, ws: torch.Tensor, n_dst_dev: Optional[torch.Tensor] = None,
                 gcn_norm_t: Optional[torch.Tensor] = None, want_csc: bool = True, stream=None) -> DeviceBlock:
+    # the sampler reads up to cap_dst ids (the device count, if given, is
+    # clamped to cap_dst)
+    if dst_ids.numel() < out.c.cap_dst:
+        raise ValueError(f"dst_ids holds {dst_ids.numel()} ids, the block's cap_dst is {out.c.cap_dst}")
     _check(lib().gnn_build_block(ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(dst_ids), _ptr(n_dst_dev), fanout,
                                  seed, step, hop, int(want_csc), ctypes.byref(out.c), _ptr(ws), ws.numel(),
                                  _stream(stream)))

@@ -155,6 +155,57 @@ def test_build_block_degenerate_cases():
     assert got["n_dst"] == 0 and got["n_src"] == 0 and got["nnz"] == 0 and got["cscptr"].tolist() == [0]
 
 
+def _hub_graph():
+    # destinations 1..10000 (more rows than one LDS window of the transpose
+    # sort); every one links to hub 0, every 7th twice (a duplicate edge);
+    # rows 1..17 link to vertex 11000 (a column just over the one-lane sort
+    # limit), rows 18..33 to vertex 11001 (exactly at it); two more random
+    # neighbours each.  No degree exceeds the fanout, so all edges are kept.
+    rng = np.random.default_rng(11)
+    n = 12_000
+    nbrs = [[] for _ in range(n)]
+    for v in range(1, 10_001):
+        nbrs[v].append(0)
+        if v % 7 == 0:
+            nbrs[v].append(0)
+        if v <= 17:
+            nbrs[v].append(11_000)
+        elif v <= 33:
+            nbrs[v].append(11_001)
+        nbrs[v] += rng.integers(10_001, n, size=2).tolist()
+    rowptr = np.zeros(n + 1, dtype=np.int64)
+    rowptr[1:] = np.cumsum([len(x) for x in nbrs])
+    col = np.array([u for x in nbrs for u in x], dtype=np.int64)
+    return rowptr, col
+
+
+def test_build_block_transpose_long_columns():
+    rowptr, col = _hub_graph()
+    n = rowptr.size - 1
+    g = gnn.DeviceGraph(torch.from_numpy(rowptr).to(DEV), torch.from_numpy(col).to(DEV))
+    fanout = 8
+    dst_all = np.random.default_rng(3).permutation(np.arange(1, 10_001)).astype(np.int64)
+    ws = gnn.sampler_workspace(n, dst_all.size, fanout, DEV)
+    dst_d = torch.from_numpy(dst_all).to(DEV)
+    blk = gnn.DeviceBlock(n, dst_all.size, fanout, True, False, DEV)
+    for n_dst in (10_000, 4_097, 4_096, 300):  # the same workspace and block, shrinking batches
+        dst = dst_all[:n_dst]
+        n_dev = torch.tensor([n_dst], dtype=torch.int64, device=DEV)  # the first n_dst ids of dst_d
+        print(f"[transpose] hub graph, n_dst={n_dst}", flush=True)
+        gnn.build_block(g, dst_d, fanout, 5, 0, 1, blk, ws, n_dst_dev=n_dev)
+        torch.cuda.synchronize()
+        got = blk.host()
+        ref = oracle.build_block(rowptr, col, dst, fanout, 5, 0, 1)
+        assert int(blk.counts[3].item()) == 0
+        assert np.array_equal(got["col"], ref.col)
+        assert np.array_equal(got["cscptr"], ref.cscptr)
+        assert np.array_equal(got["cscrow"], ref.cscrow)
+        lens = np.diff(ref.cscptr)
+        assert lens.max() > n_dst // 2  # the hub's column
+        if n_dst == dst_all.size:
+            assert (lens == 17).any() and (lens == 16).any()
+
+
 def test_build_block_rejects_bad_arguments():
     rowptr = torch.tensor([0, 1, 2], dtype=torch.int64, device=DEV)
     col = torch.tensor([1, 0], dtype=torch.int64, device=DEV)
