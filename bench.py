@@ -54,9 +54,15 @@ def parse():
     p.add_argument("--scale-n", type=int, default=0, help="run the workload's model on an R-MAT graph of this many "
                    "vertices (the edge count scales with it unless --scale-m is given)")
     p.add_argument("--scale-m", type=int, default=0)
+    p.add_argument("--prepare-slots", type=int, default=8,
+                   help="prepare workspaces of the pipelined steps; steps go in groups of half as many")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="first run a plain device copy (fp32 -> int32 elementwise) of this many MiB three times, the "
+                        "known-size kernel that scales HBM traffic counters")
     p.add_argument("--pipeline", action=argparse.BooleanOptionalAction, default=None,
-                   help="two-stage steps with the prepare stage (sampling, gather) of step s+1 overlapping the "
-                        "compute stage of step s (default: on for host-resident tables)")
+                   help="two-stage steps (gnn_train_steps) with the prepare stage (sampling, gather) of step s+1 "
+                        "overlapping the compute stage of step s (default: on; --no-pipeline times one "
+                        "gnn_train_step call per step)")
     return p.parse_args()
 
 
@@ -249,13 +255,22 @@ def main():
         __graft_entry__.build()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.randn(n, device=dev)
+        dst = torch.empty(n, dtype=torch.int32, device=dev)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {args.copy_calibration} MiB read + {args.copy_calibration} MiB written per launch")
+        del src, dst
     w = workloads.PRESETS[args.workload]
     if args.scale_n:
         m = args.scale_m or int(round(w.m * args.scale_n / w.n))
         w = workloads.scaled(w, args.scale_n, m)
     host_table = w.table_loc == "host"
     loc = gnn.GNN_LOC_HOST_PINNED if host_table else gnn.GNN_LOC_DEVICE
-    pipeline = host_table if args.pipeline is None else args.pipeline
+    pipeline = True if args.pipeline is None else args.pipeline
     act = torch.bfloat16 if w.precision == "bf16" else torch.float32
     precision = gnn.GNN_BF16 if w.precision == "bf16" else gnn.GNN_F32
     kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
@@ -282,27 +297,32 @@ def main():
     log(f"inputs ready in {time.time() - t0:.1f}s: {stats}")
 
     tr = gnn.Trainer(kind, w.dims, w.fanouts, precision, w.n, w.batch, weights, biases, device=dev,
-                     prepare_slots=2 if pipeline else 0)
+                     prepare_slots=args.prepare_slots if pipeline else 0)
     nb = w.n // w.batch
     tgt = [workloads.targets_for_step(perm, w.batch, s).contiguous() for s in range(min(nb, args.warmup + args.steps))]
     edges = torch.zeros(args.steps, dtype=torch.int64, device=dev)
     prep_stream = torch.cuda.Stream(dev) if pipeline else None
 
-    def run_steps(first, count, edges_out=None, pipelined=pipeline):
+    def step_targets(first, count):
+        return torch.stack([tgt[(first + i) % len(tgt)] for i in range(count)])
+
+    def run_steps(first, count, edges_out=None, pipelined=pipeline, targets=None):
         if pipelined:
-            tr.run_pipelined(graph, table, labels, lambda s: tgt[s % len(tgt)], w.seed, first, count, args.lr,
-                             gcn_norm_t=nrm, loc=loc, edges_out=edges_out, prep_stream=prep_stream)
+            tr.run_pipelined(graph, table, labels, step_targets(first, count) if targets is None else targets,
+                             w.seed, first, count, args.lr, gcn_norm_t=nrm, loc=loc, edges_out=edges_out,
+                             prep_stream=prep_stream)
             return
         for i in range(count):
             tr.step(graph, table, labels, tgt[(first + i) % len(tgt)], w.seed, first + i, args.lr, gcn_norm_t=nrm,
                     loc=loc, edges_out=None if edges_out is None else edges_out[i:i + 1])
 
     def timed(first, count, edges_out, pipelined=pipeline):
+        targets = step_targets(first, count) if pipelined else None
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t = time.perf_counter()
         ev0.record()
-        run_steps(first, count, edges_out, pipelined)
+        run_steps(first, count, edges_out, pipelined, targets)
         t_enq = time.perf_counter() - t
         ev1.record()
         torch.cuda.synchronize()

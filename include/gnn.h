@@ -353,6 +353,36 @@ gnn_status gnn_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *
                             float *loss_dev, int64_t *edges_dev, void *prep_ws, size_t prep_bytes, void *comp_ws,
                             size_t comp_bytes, gnn_stream s);
 
+/* Several training steps, pipelined: the prepare stages of later steps run
+ * on prep_s while the compute stages of earlier ones run on s (the sampler /
+ * feature loader / trainer pipeline of Section III-A and the two-stage
+ * feature prefetching of Section IV-B, on one device).  Step i
+ * (0 <= i < steps) has step number first_step + i and targets
+ * targets[i * batch .. (i+1) * batch) ([device] int64, steps x batch, each
+ * row distinct vertex ids).  Results are those of `steps` gnn_train_step
+ * calls in order, bit for bit: the prepare stage reads no model buffer, and
+ * the computes run in step order on s.
+ *
+ * Steps go in groups of G = max(1, n_prep / 2): the prepares of group q+1
+ * overlap the computes of group q, and the two streams synchronise once per
+ * group (stream events cost the host more than a launch, so a larger G
+ * lowers the host cost per step; 8 slots give G = 4).
+ * prep_ws: n_prep (2 .. GNN_MAX_PREPARE_SLOTS) distinct prepare workspaces of
+ *   prep_bytes each, initialised with gnn_step_prepare_workspace_init.
+ *   comp_ws: one compute workspace (comp_bytes).
+ * loss_dev: NULL or [device] fp32[steps]; edges_dev: NULL or [device]
+ *   int64[steps]: per-step loss and sampled-edge count.
+ * Ordering: the first prepares wait for the work enqueued on s before the
+ *   call; every compute is on s, so work enqueued on s after the call runs
+ *   after all steps.  The call never waits on the host; it creates and
+ *   releases its own events.  prep_s may equal s (no overlap). */
+#define GNN_MAX_PREPARE_SLOTS 8
+gnn_status gnn_train_steps(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                           gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
+                           const int64_t *targets, int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps,
+                           float lr, float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int32_t n_prep,
+                           size_t prep_bytes, void *comp_ws, size_t comp_bytes, gnn_stream s, gnn_stream prep_s);
+
 #ifdef __cplusplus
 }
 #endif

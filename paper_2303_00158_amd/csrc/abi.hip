@@ -40,6 +40,11 @@ gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
                             uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s);
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
                             float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s);
+gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
+                           bool host_table, int64_t row_stride, const int64_t *labels, const int64_t *targets,
+                           int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps, float lr,
+                           float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int n_prep, void *comp_ws,
+                           hipStream_t s, hipStream_t ps);
 
 namespace {
 
@@ -476,6 +481,38 @@ gnn_status gnn_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *
               "%s: workspaces %zu and %zu bytes, need %zu and %zu", who, prep_bytes, comp_bytes, o.prep_bytes,
               o.compute_bytes);
     return run_step_compute(m, graph_n, labels, batch, lr, loss_dev, edges_dev, prep_ws, comp_ws, stream_of(s));
+}
+
+gnn_status gnn_train_steps(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                           gnn_dtype tdt, gnn_loc loc, int64_t row_stride, const int64_t *labels,
+                           const int64_t *targets, int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps,
+                           float lr, float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int32_t n_prep,
+                           size_t prep_bytes, void *comp_ws, size_t comp_bytes, gnn_stream s, gnn_stream prep_s) {
+    clear_error();
+    const char *who = "gnn_train_steps";
+    GNN_TRY(check_prepare_args(m, g, gcn_norm, table, tdt, loc, row_stride, targets, batch, who));
+    GNN_TRY(check_compute_args(m, labels, loss_dev, edges_dev, who));
+    GNN_CHECK(steps >= 0 && steps <= (int64_t{1} << 40), GNN_EINVAL, "%s: bad step count %lld", who,
+              static_cast<long long>(steps));
+    GNN_CHECK(n_prep >= 2 && n_prep <= GNN_MAX_PREPARE_SLOTS && prep_ws, GNN_EINVAL,
+              "%s: n_prep must be in [2, %d] with a workspace array", who, GNN_MAX_PREPARE_SLOTS);
+    gnn_step_layout o;
+    GNN_TRY(step_layout(m, g->n, batch, &o));
+    for (int i = 0; i < n_prep; ++i) {
+        GNN_CHECK(prep_ws[i] && aligned(prep_ws[i], 256), GNN_EINVAL,
+                  "%s: prepare workspace %d must be non-NULL and 256-byte aligned", who, i);
+        for (int j = 0; j < i; ++j)
+            GNN_CHECK(prep_ws[i] != prep_ws[j], GNN_EINVAL, "%s: prepare workspaces %d and %d are the same", who, j, i);
+    }
+    GNN_CHECK(comp_ws && aligned(comp_ws, 256), GNN_EINVAL, "%s: comp_ws must be non-NULL and 256-byte aligned", who);
+    GNN_CHECK(prep_bytes >= o.prep_bytes && comp_bytes >= o.compute_bytes, GNN_ESIZE,
+              "%s: workspaces %zu and %zu bytes, need %zu and %zu", who, prep_bytes, comp_bytes, o.prep_bytes,
+              o.compute_bytes);
+    const void *t = nullptr;
+    GNN_TRY(device_view(table, loc, &t, who));
+    return run_train_steps(m, g, gcn_norm, t, tdt, loc == GNN_LOC_HOST_PINNED, row_stride, labels, targets, batch,
+                           seed, first_step, steps, lr, loss_dev, edges_dev, prep_ws, n_prep, comp_ws, stream_of(s),
+                           stream_of(prep_s));
 }
 
 }  // extern "C"

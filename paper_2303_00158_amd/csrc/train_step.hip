@@ -301,4 +301,69 @@ gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *
                        static_cast<char *>(comp_ws), o, Role<csc::SortJob>{}, s);
 }
 
+namespace {
+
+// Events of one pipelined call, destroyed on every exit path (a pending
+// event's resources are released once it completes).
+struct EventSet {
+    hipEvent_t e[8] = {};
+    int n = 0;
+    gnn_status make(int count) {
+        for (; n < count; ++n) GNN_HIP(hipEventCreateWithFlags(&e[n], hipEventDisableTiming));
+        return GNN_OK;
+    }
+    ~EventSet() {
+        for (int i = 0; i < n; ++i) (void)hipEventDestroy(e[i]);
+    }
+};
+
+}  // namespace
+
+// `steps` training steps in groups of G = max(1, n_prep / 2): the prepare
+// stages of group q+1 run on ps while the computes of group q run on s.
+// Group q uses slots (q % 2) * G .. (q % 2) * G + G - 1.  The streams meet
+// once per group: a group's computes wait for all its prepares
+// (prepared[q % 2]), and a group's prepares wait for the computes that last
+// read its slots, those of group q-2 (consumed[q % 2]).  The first prepares
+// wait for the work already on s.  Host-side stream events are costly
+// relative to a launch, so grouping keeps them to about one per step.
+gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
+                           bool host_table, int64_t row_stride, const int64_t *labels, const int64_t *targets,
+                           int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps, float lr,
+                           float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int n_prep, void *comp_ws,
+                           hipStream_t s, hipStream_t ps) {
+    if (steps == 0) return GNN_OK;
+    const int G = std::max(1, n_prep / 2);
+    const int64_t groups = ceil_div(steps, G);
+    EventSet ev;
+    GNN_TRY(ev.make(5));
+    hipEvent_t prepared[2] = {ev.e[0], ev.e[1]}, consumed[2] = {ev.e[2], ev.e[3]}, start = ev.e[4];
+    GNN_HIP(hipEventRecord(start, s));
+    GNN_HIP(hipStreamWaitEvent(ps, start, 0));
+    auto prepare_group = [&](int64_t q) -> gnn_status {
+        const int half = static_cast<int>(q % 2);
+        if (q >= 2) GNN_HIP(hipStreamWaitEvent(ps, consumed[half], 0));
+        for (int j = 0; j < G && q * G + j < steps; ++j) {
+            const int64_t i = q * G + j;
+            GNN_TRY(run_step_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets + i * batch, batch,
+                                     seed, first_step + static_cast<uint64_t>(i), prep_ws[half * G + j], ps));
+        }
+        GNN_HIP(hipEventRecord(prepared[half], ps));
+        return GNN_OK;
+    };
+    GNN_TRY(prepare_group(0));
+    for (int64_t q = 0; q < groups; ++q) {
+        if (q + 1 < groups) GNN_TRY(prepare_group(q + 1));
+        const int half = static_cast<int>(q % 2);
+        GNN_HIP(hipStreamWaitEvent(s, prepared[half], 0));
+        for (int j = 0; j < G && q * G + j < steps; ++j) {
+            const int64_t i = q * G + j;
+            GNN_TRY(run_step_compute(m, g->n, labels, batch, lr, loss_dev ? loss_dev + i : nullptr,
+                                     edges_dev ? edges_dev + i : nullptr, prep_ws[half * G + j], comp_ws, s));
+        }
+        GNN_HIP(hipEventRecord(consumed[half], s));
+    }
+    return GNN_OK;
+}
+
 }  // namespace gnn

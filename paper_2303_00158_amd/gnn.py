@@ -94,6 +94,8 @@ _SIGNATURES = {
     "gnn_step_prepare": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _i64, _u64, _u64, _vp, _sz,
                                 _vp]),
     "gnn_step_compute": (_i32, [_P(Model), _i64, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
+    "gnn_train_steps": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64, _u64, _u64, _i64,
+                               _f32, _vp, _vp, _P(_vp), _i32, _sz, _vp, _sz, _vp, _vp]),
 }
 
 _lib = None
@@ -406,46 +408,41 @@ class Trainer:
                                       self.comp_ws.numel(), _stream(stream)))
         self._viewing = (ws, self.comp_ws)
 
-    def run_pipelined(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets_of, seed: int,
+    def run_pipelined(self, graph: DeviceGraph, table: torch.Tensor, labels: torch.Tensor, targets, seed: int,
                       first_step: int, steps: int, lr: float, gcn_norm_t: Optional[torch.Tensor] = None,
-                      loc: int = GNN_LOC_DEVICE, edges_out: Optional[torch.Tensor] = None, prep_stream=None,
-                      stream=None) -> None:
-        """Enqueue ``steps`` steps with the prepare stage (sampling and the
-        gather of X') of step s+1 overlapping the compute stage of step s.
-        targets_of(s) gives the target ids of step s (kept alive by the
-        caller until the work is done); edges_out, if given, is an int64
-        device tensor of ``steps`` counts.  Slots rotate over the prepare
-        workspaces; a slot is refilled only after the compute that read it
-        (events), and each compute waits for its prepare."""
+                      loc: int = GNN_LOC_DEVICE, edges_out: Optional[torch.Tensor] = None,
+                      loss_out: Optional[torch.Tensor] = None, prep_stream=None, stream=None) -> None:
+        """Enqueue ``steps`` steps through gnn_train_steps: the prepare stage
+        (sampling and the gather of X') of a later step runs on prep_stream
+        while the compute stage of the current one runs on ``stream``.
+        targets: int64 device tensor (steps x batch), or a callable giving
+        the target tensor of step number s (stacked here).  edges_out /
+        loss_out, if given, are int64 / fp32 device tensors of ``steps``
+        per-step values; self.loss holds the last step's loss."""
         nslot = len(self.prep_ws)
         assert nslot >= 2, "run_pipelined needs prepare_slots >= 2"
-        cs = torch.cuda.current_stream(self.device) if stream is None else stream
+        if steps == 0:
+            return
+        if callable(targets):
+            targets = torch.stack([targets(first_step + i) for i in range(steps)])
+        assert targets.dtype == torch.int64 and targets.is_contiguous() and targets.numel() == steps * self.batch
         ps = prep_stream if prep_stream is not None else torch.cuda.Stream(self.device)
-        prepared = [torch.cuda.Event() for _ in range(nslot)]
-        consumed = [None] * nslot
-        ps.wait_stream(cs)  # inputs written on the compute stream
+        ws = (_vp * nslot)(*[_ptr(w) for w in self.prep_ws])
+        lo = loss_out if loss_out is not None else self._loss_steps(steps)
+        _check(lib().gnn_train_steps(ctypes.byref(self.model), ctypes.byref(graph.c), _ptr(gcn_norm_t), _ptr(table),
+                                     dtype_code(table.dtype), loc, table.stride(0), _ptr(labels), _ptr(targets),
+                                     self.batch, seed, first_step, steps, float(lr), _ptr(lo), _ptr(edges_out), ws,
+                                     nslot, self.prep_ws[0].numel(), _ptr(self.comp_ws), self.comp_ws.numel(),
+                                     _stream(stream), _stream(ps)))
+        with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream(self.device)):
+            self.loss.copy_(lo[steps - 1:steps])
+        self._keep = (targets, lo)  # alive until the next call; the stream orders their reuse
+        self._viewing = (self.prep_ws[(steps - 1) % nslot], self.comp_ws)
 
-        def enqueue_prepare(i):
-            slot = i % nslot
-            if consumed[slot] is not None:
-                ps.wait_event(consumed[slot])
-            self.prepare(slot, graph, table, targets_of(first_step + i), seed, first_step + i, gcn_norm_t, loc,
-                         stream=ps)
-            prepared[slot].record(ps)
-
-        for i in range(min(nslot - 1, steps)):
-            enqueue_prepare(i)
-        for i in range(steps):
-            if i + nslot - 1 < steps:
-                enqueue_prepare(i + nslot - 1)
-            slot = i % nslot
-            cs.wait_event(prepared[slot])
-            e = None if edges_out is None else edges_out[i:i + 1]
-            self.compute(slot, labels, lr, edges_out=e, stream=cs)
-            ev = torch.cuda.Event()
-            ev.record(cs)
-            consumed[slot] = ev
-        cs.wait_stream(ps)
+    def _loss_steps(self, steps: int) -> torch.Tensor:
+        if getattr(self, "_loss_buf", None) is None or self._loss_buf.numel() < steps:
+            self._loss_buf = torch.zeros(steps, dtype=torch.float32, device=self.device)
+        return self._loss_buf[:steps]
 
     # --- views into the workspaces (for inspection and tests) --------------
     def _view(self, off: int, numel: int, dtype: torch.dtype, compute: bool = False) -> torch.Tensor:

@@ -163,3 +163,34 @@ def test_two_stage_step_validation(gnn):
                                 fake, 64, 0, 0, fake, lay.prep_bytes - 256, None) == gnn.GNN_ESIZE
     assert lib.gnn_step_prepare(ctypes.byref(m), ctypes.byref(g), None, fake, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 16,
                                 fake, 64, 0, 0, fake, lay.prep_bytes, None) == gnn.GNN_EINVAL
+
+
+def test_pipelined_steps_validation(gnn):
+    # gnn_train_steps checks its slot array, workspaces and counts on the
+    # host before creating events or enqueueing anything
+    lib = gnn.lib()
+    m = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (32, 16, 8), (5, 5), gnn.GNN_F32)
+    for l in range(2):
+        m.w[l] = m.b[l] = m.dw[l] = m.db[l] = 1 << 20
+    lay = gnn.StepLayout()
+    assert lib.gnn_train_step_layout(ctypes.byref(m), 1000, 64, ctypes.byref(lay)) == gnn.GNN_OK
+    fake = 1 << 24
+    g = gnn.Graph(1000, 5000, fake, fake)
+
+    def call(slots, n_prep=None, steps=3, prep_bytes=lay.prep_bytes, comp=fake, comp_bytes=lay.compute_bytes):
+        arr = (ctypes.c_void_p * max(len(slots), 1))(*slots)
+        return lib.gnn_train_steps(ctypes.byref(m), ctypes.byref(g), None, fake, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 32,
+                                   fake, fake, 64, 0, 0, steps, 0.1, None, None, arr,
+                                   len(slots) if n_prep is None else n_prep, prep_bytes, comp, comp_bytes, None, None)
+
+    a, b, c = fake, fake + (1 << 22), fake + (2 << 22)
+    assert call([a]) == gnn.GNN_EINVAL                      # one slot cannot overlap anything
+    assert b"n_prep" in lib.gnn_last_error()
+    assert call([a, b], n_prep=9) == gnn.GNN_EINVAL         # above GNN_MAX_PREPARE_SLOTS
+    assert call([a, a]) == gnn.GNN_EINVAL                   # the same workspace twice
+    assert call([a, b + 8]) == gnn.GNN_EINVAL               # misaligned
+    assert call([a, 0]) == gnn.GNN_EINVAL                   # NULL slot
+    assert call([a, b], steps=-1) == gnn.GNN_EINVAL
+    assert call([a, b, c], prep_bytes=lay.prep_bytes - 256) == gnn.GNN_ESIZE
+    assert call([a, b], comp_bytes=lay.compute_bytes - 256) == gnn.GNN_ESIZE
+    assert call([a, b], comp=None) == gnn.GNN_EINVAL

@@ -657,27 +657,41 @@ def _state(tr):
     return [t.cpu().clone() for t in tr.w + tr.b + tr.dw + tr.db] + [tr.loss.cpu().clone()]
 
 
-@pytest.mark.parametrize("kind,precision", [(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16), (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32)])
-def test_pipelined_two_stage_steps_equal_one_call_steps(kind, precision):
-    # five steps through two rotating prepare slots (each refilled after the
-    # compute that read it) give bit for bit what five one-call steps give
-    dims, fan, n, m, batch, steps = (100, 256, 47), (25, 10), 30_000, 400_000, 512, 5
+@pytest.mark.parametrize("kind,precision,nslot,steps", [(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 2, 5),
+                                                          (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 2, 5),
+                                                          (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 7),
+                                                          (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 1),
+                                                          (gnn.GNN_AGG_GCN_SYM, gnn.GNN_BF16, 4, 2),
+                                                          (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 8, 11),
+                                                          (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 8, 3)])
+def test_pipelined_two_stage_steps_equal_one_call_steps(kind, precision, nslot, steps):
+    # gnn_train_steps: steps in groups of n_prep // 2 through rotating
+    # prepare slots (each refilled after the computes that read it; partial
+    # last groups and fewer steps than slots included) give bit for bit what
+    # one-call steps give, per-step losses and edge counts too
+    dims, fan, n, m, batch = (100, 256, 47), (25, 10), 30_000, 400_000, 512
     _rp, _col, table, labels, ws, bs, g, targets = _pipeline_inputs(kind, dims, fan, n, m, batch)
     table = table.to(DEV)
     nrm = gnn.gcn_norm(g)
-    print(f"[pipeline] kind={kind} precision={precision}: one-call steps", flush=True)
+    print(f"[pipeline] kind={kind} precision={precision} slots={nslot} steps={steps}: one-call steps", flush=True)
     ref = gnn.Trainer(kind, dims, fan, precision, n, batch, ws, bs, device=DEV)
     edges_ref = torch.zeros(steps, dtype=torch.int64, device=DEV)
+    loss_ref = []
     for s in range(steps):
-        ref.step(g, table, labels, targets[s], seed=3, step=s, lr=0.05, gcn_norm_t=nrm, edges_out=edges_ref[s:s + 1])
+        ref.step(g, table, labels, targets[s % len(targets)], seed=3, step=s, lr=0.05, gcn_norm_t=nrm,
+                 edges_out=edges_ref[s:s + 1])
+        loss_ref.append(ref.loss.clone())
     torch.cuda.synchronize()
-    print("[pipeline] two-stage pipelined steps", flush=True)
-    tr = gnn.Trainer(kind, dims, fan, precision, n, batch, ws, bs, device=DEV, prepare_slots=2, one_call=False)
+    print("[pipeline] gnn_train_steps", flush=True)
+    tr = gnn.Trainer(kind, dims, fan, precision, n, batch, ws, bs, device=DEV, prepare_slots=nslot, one_call=False)
     edges = torch.zeros(steps, dtype=torch.int64, device=DEV)
-    tr.run_pipelined(g, table, labels, lambda s: targets[s], seed=3, first_step=0, steps=steps, lr=0.05,
-                     gcn_norm_t=nrm, edges_out=edges)
+    losses = torch.zeros(steps, dtype=torch.float32, device=DEV)
+    tr.run_pipelined(g, table, labels, lambda s: targets[s % len(targets)], seed=3, first_step=0, steps=steps,
+                     lr=0.05, gcn_norm_t=nrm, edges_out=edges, loss_out=losses)
     torch.cuda.synchronize()
     assert torch.equal(edges, edges_ref)
+    assert torch.equal(losses.view(torch.int32), torch.cat(loss_ref).view(torch.int32))
+    assert torch.equal(tr.loss.view(torch.int32), loss_ref[-1].view(torch.int32))
     for a, b in zip(_state(tr), _state(ref)):
         assert torch.equal(a.view(torch.int32), b.view(torch.int32))
     for h in (1, 2):
