@@ -188,6 +188,37 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
                              gnn_dtype hbdt, float *d_src, gnn_stream s);
 
 /* ------------------------------------------------------------------------
+ * One layer's forward in one launch, bf16 (equations 1 and 2 together: the
+ * aggregation of Section II-A feeding the update, as in the on-chip
+ * aggregate -> update datapath of Section IV-C), with the loss of Section
+ * II-B in the epilogue for the last layer.
+ *   h_src   [device] bf16 block->cap_src x f (row j is source j); f % 4 == 0.
+ *   wt      [device] bf16 W^T, n_out x K (K = 2f for SAGE, self rows of W
+ *           first; f for GCN), as kept by gnn_model_sync_shadow.
+ *   bias    [device] fp32 n_out, or NULL.
+ *   agg_out [device] bf16 block->cap_dst x f: written with the aggregation
+ *           (the mean for SAGE, the normalised sum for GCN), exactly what
+ *           gnn_aggregate_fwd would give up to fp32 summation order.
+ *   labels == NULL (hidden layer): out [device] bf16 cap_dst x n_out =
+ *           ReLU([h_src[i] || agg[i]] W + b) (SAGE) or ReLU(agg W + b) (GCN),
+ *           GEMM operands bf16, fp32 accumulate.
+ *   labels != NULL (last layer; n_out <= 64): out [device] fp32 logits
+ *           (no ReLU) for the first `batch` rows, whose targets are
+ *           block->src_ids[0 .. batch); g_out [device] fp32 batch x n_out =
+ *           (softmax - onehot(labels[target])) / batch; row_loss [device] fp32
+ *           batch = logsumexp - logit of the label (the loss is their mean).
+ *   max_row_len: the block's row-length bound (its fanout); it sizes the
+ *           LDS staging of column indices; longer rows stay correct.
+ * Returns GNN_EUNSUPPORTED when the weights do not fit the kernel's
+ * register tiles (n_out up to 256 with K <= 256, or n_out up to 128 with
+ * K <= 512) or the data are not 8-byte aligned; the caller then uses
+ * gnn_aggregate_fwd and gnn_update_fwd.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, const void *h_src, int64_t f,
+                         const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
+                         const int64_t *labels, int64_t batch, float *g_out, float *row_loss, gnn_stream s);
+
+/* ------------------------------------------------------------------------
  * Update (equation 2): Z = A W + b with A = [a_self || a_nbr] (SAGE) or
  * A = a_self (GCN, a_nbr NULL); K = 2*k_each or k_each.
  *   a_self, a_nbr [device] row-major, row length k_each, adt in {F32, BF16}.

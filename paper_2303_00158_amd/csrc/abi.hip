@@ -239,6 +239,33 @@ gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src
     return launch_aggregate_fwd(b, kind, h_src, hdt, f, out, odt, stream_of(s));
 }
 
+gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, const void *h_src, int64_t f,
+                         const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
+                         const int64_t *labels, int64_t batch, float *g_out, float *row_loss, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_layer_fwd";
+    GNN_CHECK(kind == GNN_AGG_SAGE_MEAN || kind == GNN_AGG_GCN_SYM, GNN_EINVAL, "%s: unknown aggregation %d", who,
+              kind);
+    GNN_TRY(check_block(b, false, kind == GNN_AGG_GCN_SYM, who));
+    GNN_CHECK(dim_ok(f) && dim_ok(n_out), GNN_EINVAL, "%s: f %lld or n_out %lld out of [1, %d]", who, (long long)f,
+              (long long)n_out, GNN_MAX_DIM);
+    GNN_CHECK(max_row_len >= 1, GNN_EINVAL, "%s: max_row_len must be >= 1", who);
+    const bool last = labels != nullptr;
+    GNN_CHECK(h_src && wt && agg_out && out, GNN_EINVAL, "%s: NULL pointer", who);
+    if (last) {
+        GNN_CHECK(g_out && row_loss, GNN_EINVAL, "%s: labels given without g_out and row_loss", who);
+        GNN_CHECK(batch >= 1 && batch <= b->cap_dst, GNN_EINVAL, "%s: batch must be in [1, cap_dst]", who);
+        GNN_CHECK(aligned(out, 4) && aligned(g_out, 4) && aligned(row_loss, 4) && aligned(labels, 8), GNN_EINVAL,
+                  "%s: misaligned data", who);
+    }
+    GNN_CHECK(fused_layer_ok(kind, GNN_BF16, f, n_out, b->cap_dst, max_row_len, last, h_src, wt, agg_out),
+              GNN_EUNSUPPORTED,
+              "%s: shape not supported (needs f %% 4 == 0, weights of at most 2 x 8 column tiles x 8 steps or "
+              "1 x 16, n_out <= 64 with labels, 8-byte aligned bf16 data)", who);
+    return launch_fused_layer(b, kind, max_row_len, h_src, f, wt, bias, n_out, agg_out, out, last, labels, g_out,
+                              row_loss, batch, stream_of(s));
+}
+
 gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a, int64_t f, const void *h_below,
                              gnn_dtype hbdt, float *d_src, gnn_stream s) {
     clear_error();

@@ -159,6 +159,18 @@ gnn_status launch_update_bwd(const void *a_self, const void *a_nbr, int adt, int
                              int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt, float *dw,
                              float *db, float *d_a, void *ws, float *w_upd, float *b_upd, uint16_t *wt_upd, float lr,
                              hipStream_t s);
+// Forward of one layer in one launch (fused_layer.hip): aggregation into
+// LDS, update on the matrix cores with W^T (bf16 shadow) in registers, and
+// for the last layer (last = true) the softmax cross-entropy gradient g and
+// row losses of the `batch` target rows instead of an activation.  Writes the
+// aggregation output agg_out (bf16) and out (bf16 ReLU(Z), or fp32 logits).
+// fused_layer_ok says whether the shapes, precision and alignment allow it.
+bool fused_layer_ok(int kind, int precision, int64_t f, int64_t n_out, int64_t cap_dst, int32_t maxdeg, bool last,
+                    const void *h, const uint16_t *wt, const void *agg_out);
+gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, const void *h, int64_t f,
+                              const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
+                              bool last, const int64_t *labels, float *g, float *row_loss, int64_t batch,
+                              hipStream_t s);
 // wt = bf16(w^T) for a K x n row-major w.
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
 gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s);

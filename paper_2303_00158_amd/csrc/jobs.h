@@ -72,6 +72,33 @@ template <class J, class... R> Pack<J, R...> make_pack(const Role<J> &r, const R
     return p;
 }
 
+// The same job for up to kMaxCopies independent instances (for example the
+// same sampling phase of several training steps): copy c takes workgroups
+// [c * npad, c * npad + n), npad = n rounded up to a multiple of 8 (as in a
+// Pack, so each copy's logical index stays congruent to its physical one
+// modulo the XCD count).  The copy index is uniform per workgroup.
+constexpr int kMaxCopies = 4;
+template <class J> struct Multi {
+    J j[kMaxCopies];
+    int g;
+    unsigned n, npad;
+    __device__ void run(int64_t b, int64_t) const {
+        const int c = static_cast<int>(b / npad);
+        const int64_t lb = b - static_cast<int64_t>(c) * npad;
+        if (c < g && lb < n) j[c].run(lb, n);
+    }
+};
+// make(c) gives copy c's job; g copies of n workgroups each.
+template <class Make> auto multi_role(Make &&make, int g, unsigned n) {
+    using J = decltype(make(0));
+    Multi<J> m{};
+    for (int c = 0; c < g; ++c) m.j[c] = make(c);
+    m.g = g;
+    m.n = n;
+    m.npad = (n + 7) / 8 * 8;
+    return Role<Multi<J>>{m, n ? m.npad * static_cast<unsigned>(g) : 0u};
+}
+
 template <class P>
 __global__ void __launch_bounds__(256) pack_kernel(P p) {
     p.run(blockIdx.x);
@@ -97,6 +124,7 @@ gnn_status launch_job2(const A &a, unsigned na, const B &b, unsigned nb, hipStre
 template <class... J>
 gnn_status launch_jobs(hipStream_t s, const char *what, const Role<J> &...roles) {
     const auto p = make_pack(roles...);
+    static_assert(sizeof(p) <= 4096, "kernel arguments of a packed launch exceed 4 KiB");
     const unsigned grid = p.grid();
     if (grid == 0) return GNN_OK;
     pack_kernel<decltype(p)><<<grid, 256, 0, s>>>(p);

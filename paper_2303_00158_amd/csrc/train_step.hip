@@ -14,6 +14,7 @@
 // (csc_dev.h) ride along with the sampling launches of later hops, and the
 // last sort with the loss (or, in a separate prepare stage, at its end).
 #include <algorithm>
+#include <type_traits>
 
 #include "aggregate_dev.h"
 #include "csc_dev.h"
@@ -185,6 +186,103 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     return st;
 }
 
+// The prepare stages of G (2 .. kMaxCopies) steps at once: the same
+// launches as run_prepare, each carrying one copy of every role per step
+// (Multi), so a group of steps pays the launch and latency chain of the
+// sampler once.  Step c of the group has targets targets + c * batch, step
+// number first_step + c and prepare workspace preps[c]; the transposes are
+// complete when the last launch ends.
+gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
+                             int tdt, bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch,
+                             uint64_t seed, uint64_t first_step, int G, void *const *preps,
+                             const gnn_step_layout &o, hipStream_t s) {
+    const int L = m->num_layers;
+    const int act = m->precision;
+    gnn_block blk[kMaxCopies][GNN_MAX_LAYERS];
+    csc::Args ca[kMaxCopies][GNN_MAX_LAYERS] = {};
+    csc::Grids cg[GNN_MAX_LAYERS] = {};
+    samp::HopPlan plan[kMaxCopies][GNN_MAX_LAYERS];
+    size_t hop_max = 0;
+    for (int h = 0; h < L; ++h)
+        hop_max = std::max(hop_max, sampler_hop_bytes(g->n, o.cap_dst[h], m->fanouts[h]));
+    for (int c = 0; c < G; ++c) {
+        char *prep = static_cast<char *>(preps[c]);
+        block_views(m, o, prep, blk[c]);
+        for (int h = 0; h + 1 < L; ++h) {
+            ca[c][h] = csc_args(&blk[c][h], prep + o.blk_csc_ws[h], o.cap_src[h], o.cap_nnz[h]);
+            cg[h] = csc_grids(ca[c][h]);
+        }
+        char *shared = prep + o.sampler_ws;
+        for (int h = 0; h < L; ++h) {
+            const int64_t *dst = h == 0 ? targets + c * batch : blk[c][h - 1].src_ids;
+            const int64_t *n_dst = h == 0 ? nullptr : blk[c][h - 1].counts + 1;
+            void *scratch = shared + sampler_shared_bytes(g->n) + (h % 2) * hop_max;
+            plan[c][h] = plan_hop(g, m->kind == GNN_AGG_GCN_SYM ? gcn_norm : nullptr, dst, n_dst, m->fanouts[h],
+                                  seed, first_step + static_cast<uint64_t>(c), h + 1, &blk[c][h], shared, scratch,
+                                  h + 1 < L ? &ca[c][h] : nullptr);
+        }
+    }
+    auto place = [&](int h) {
+        return multi_role([&](int c) { return csc::PlaceJob{ca[c][h >= 0 ? h : 0]}; }, G, h >= 0 ? cg[h].place : 0u);
+    };
+    auto scan = [&](int h) {
+        return multi_role([&](int c) { return csc::ScanJob{ca[c][h >= 0 ? h : 0]}; }, G, h >= 0 ? cg[h].scan : 0u);
+    };
+    auto sort = [&](int h) {
+        return multi_role([&](int c) { return csc::SortJob{ca[c][h >= 0 ? h : 0]}; }, G, h >= 0 ? cg[h].sort : 0u);
+    };
+    auto relabel = [&](int h) {
+        return multi_role([&](int c) { return samp::RelabelJob{plan[c][h].a}; }, G, plan[0][h].relabel_grid);
+    };
+    auto emit = [&](int h) {
+        return multi_role([&](int c) { return samp::EmitJob{plan[c][h].a}; }, G, plan[0][h].emit_grid);
+    };
+    gnn_status st = GNN_OK;
+    samp::with_prepare_job(plan[0][0], [&](auto job) {
+        using J = decltype(job);
+        st = launch_jobs(s, "hop_prepare", multi_role([&](int c) { return J{plan[c][0].a}; }, G,
+                                                       plan[0][0].prep_grid));
+    });
+    GNN_TRY(st);
+    GNN_TRY(launch_jobs(s, "hop_emit", emit(0)));
+    for (int h = 1; h < L; ++h) {
+        samp::with_prepare_job(plan[0][h], [&](auto job) {
+            using J = decltype(job);
+            st = launch_jobs(s, "hop_relabel+prepare+csc_place", relabel(h - 1),
+                             multi_role([&](int c) { return J{plan[c][h].a}; }, G, plan[0][h].prep_grid),
+                             place(h - 2));
+        });
+        GNN_TRY(st);
+        GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", emit(h), scan(h - 1), sort(h - 2)));
+    }
+    gath::Args ga[kMaxCopies];
+    for (int c = 0; c < G; ++c) {
+        const gnn_block &b0 = blk[c][L - 1];
+        ga[c] = gath::Args{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0],
+                           static_cast<char *>(preps[c]) + o.x0};
+    }
+    const unsigned ggrid = gath::grid_for(blk[0][L - 1].cap_src, m->dims[0], gath::vec_ok(ga[0], tdt, act),
+                                          host_table);
+    bool same = true;
+    const bool ok = gath::with_job(ga[0], tdt, act, [&](auto job) {
+        using J = decltype(job);
+        J js[kMaxCopies];
+        for (int c = 0; c < G; ++c)
+            gath::with_job(ga[c], tdt, act, [&](auto jc) {
+                if constexpr (std::is_same<decltype(jc), J>::value) js[c] = jc;
+                else same = false;
+            });
+        if (same)
+            st = launch_jobs(s, "hop_relabel+gather+csc_place", relabel(L - 1),
+                             multi_role([&](int c) { return js[c]; }, G, ggrid), place(L - 2));
+    });
+    GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
+    GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
+    GNN_TRY(st);
+    if (L >= 2) GNN_TRY(launch_jobs(s, "csc_sort", sort(L - 2)));
+    return GNN_OK;
+}
+
 // Forward, loss, backward and SGD from a prepared workspace.  The targets are
 // the first rows of hop 1's sources (destinations come first).  pending is
 // a transpose sort still to run (n = 0 if none); it shares the loss launch,
@@ -199,12 +297,25 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     block_views(m, o, prep, blk);
     const void *x0 = prep + o.x0;
 
-    // forward
+    // forward: one fused launch per layer where the shapes allow it (the
+    // last one with the loss in its epilogue), else aggregation and update
+    // as separate launches
+    float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
+    float *g_last = reinterpret_cast<float *>(comp + o.grad[L]);
+    bool loss_done = false;
     for (int l = 1; l <= L; ++l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
         void *agg = comp + o.agg[l];
         const int64_t f_in = m->dims[l - 1];
+        const int32_t maxdeg = m->fanouts[L - l];
+        if (fused_layer_ok(m->kind, m->precision, f_in, m->dims[l], b.cap_dst, maxdeg, l == L, hin, m->wt[l - 1],
+                           agg)) {
+            GNN_TRY(launch_fused_layer(&b, m->kind, maxdeg, hin, f_in, m->wt[l - 1], m->b[l - 1], m->dims[l], agg,
+                                       comp + o.h[l], l == L, labels, g_last, row_loss, batch, s));
+            loss_done = l == L;
+            continue;
+        }
         GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
         const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
@@ -212,14 +323,19 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
                                   l < L ? act : GNN_F32, comp + o.fwd_ws, s));
     }
     // loss on the targets: gradient and row losses now, the mean with the
-    // last kernel of the step
-    float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
-    GNN_TRY(launch_jobs(s, "softmax_ce+csc_sort",
-                        role(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L],
-                                              labels, blk[0].src_ids, reinterpret_cast<float *>(comp + o.grad[L]),
-                                              row_loss},
-                             static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64))),
-                        pending));
+    // last kernel of the step.  A pending transpose sort rides along, or,
+    // when the loss was fused into the last layer, with the first backward
+    // launch.
+    Role<csc::SortJob> bwd_extra{};
+    if (!loss_done) {
+        GNN_TRY(launch_jobs(s, "softmax_ce+csc_sort",
+                            role(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L],
+                                                  labels, blk[0].src_ids, g_last, row_loss},
+                                 static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64))),
+                            pending));
+    } else {
+        bwd_extra = pending;
+    }
     // backward (reads the transposes).  Per layer: the dA and dW GEMMs in
     // one launch, then the dW reduction (with SGD on W^l, b^l and the
     // shadow) in one launch with the aggregation backward of the layer, or
@@ -246,7 +362,7 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
                            m->dw[l - 1], m->db[l - 1], d_a, reinterpret_cast<float *>(comp + o.bwd_ws), m->w[l - 1],
                            m->b[l - 1], m->wt[l - 1], lr};
         const gbwd::Plan p = gbwd::plan(a);
-        GNN_TRY(launch_update_bwd_gemms(a, p, s));
+        GNN_TRY(launch_update_bwd_gemms(a, p, s, l == L ? bwd_extra : Role<csc::SortJob>{}));
         gnn_status st = GNN_OK;
         if (l > 1) {
             float *d_src = reinterpret_cast<float *>(comp + o.grad[l - 1]);
@@ -333,7 +449,7 @@ gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *
                            float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int n_prep, void *comp_ws,
                            hipStream_t s, hipStream_t ps) {
     if (steps == 0) return GNN_OK;
-    const int G = std::max(1, n_prep / 2);
+    const int G = std::min(kMaxCopies, std::max(1, n_prep / 2));
     const int64_t groups = ceil_div(steps, G);
     EventSet ev;
     GNN_TRY(ev.make(5));
@@ -343,10 +459,17 @@ gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *
     auto prepare_group = [&](int64_t q) -> gnn_status {
         const int half = static_cast<int>(q % 2);
         if (q >= 2) GNN_HIP(hipStreamWaitEvent(ps, consumed[half], 0));
-        for (int j = 0; j < G && q * G + j < steps; ++j) {
-            const int64_t i = q * G + j;
-            GNN_TRY(run_step_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets + i * batch, batch,
-                                     seed, first_step + static_cast<uint64_t>(i), prep_ws[half * G + j], ps));
+        const int64_t i0 = q * G;
+        const int gq = static_cast<int>(std::min<int64_t>(G, steps - i0));
+        if (gq == 1) {
+            GNN_TRY(run_step_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets + i0 * batch, batch,
+                                     seed, first_step + static_cast<uint64_t>(i0), prep_ws[half * G], ps));
+        } else {
+            gnn_step_layout o;
+            GNN_TRY(step_layout(m, g->n, batch, &o));
+            GNN_TRY(run_prepare_group(m, g, gcn_norm, table, tdt, host_table, row_stride, targets + i0 * batch,
+                                      batch, seed, first_step + static_cast<uint64_t>(i0), gq, prep_ws + half * G, o,
+                                      ps));
         }
         GNN_HIP(hipEventRecord(prepared[half], ps));
         return GNN_OK;

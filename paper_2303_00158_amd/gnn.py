@@ -76,6 +76,7 @@ _SIGNATURES = {
     "gnn_gather_features": (_i32, [_vp, _i32, _i32, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_fwd": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
+    "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz, _vp]),
     "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
@@ -257,6 +258,19 @@ def aggregate_bwd(block: DeviceBlock, kind: int, d_a: torch.Tensor, f: int, d_sr
     _check(lib().gnn_aggregate_bwd(ctypes.byref(block.c), kind, _ptr(d_a), f, _ptr(h_below), hb_code, _ptr(d_src),
                                    _stream(stream)))
     return d_src
+
+
+def layer_fwd(block: "DeviceBlock", kind: int, max_row_len: int, h_src: torch.Tensor, wt: torch.Tensor,
+              bias: Optional[torch.Tensor], agg_out: torch.Tensor, out: torch.Tensor,
+              labels: Optional[torch.Tensor] = None, batch: int = 0, g_out: Optional[torch.Tensor] = None,
+              row_loss: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """gnn_layer_fwd: aggregation and update of one layer in one launch (bf16
+    h_src, bf16 W^T wt).  With labels, out receives fp32 logits and g_out /
+    row_loss the loss gradient and per-row losses of the first batch rows."""
+    _check(lib().gnn_layer_fwd(ctypes.byref(block.c), kind, int(max_row_len), _ptr(h_src), h_src.shape[1], _ptr(wt),
+                               _ptr(bias), wt.shape[0], _ptr(agg_out), _ptr(out), _ptr(labels), int(batch),
+                               _ptr(g_out), _ptr(row_loss), _stream(stream)))
+    return out
 
 
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],

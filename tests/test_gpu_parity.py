@@ -332,6 +332,80 @@ def test_aggregate_bwd_is_bitwise_reproducible():
 
 
 # ---------------------------------------------------------------------------
+# one layer's forward in one launch (aggregation + update, loss for the last)
+# ---------------------------------------------------------------------------
+
+LAYER_CASES = [
+    # f, n_out, n_dst, fanout, last, row-length bound given to the kernel
+    (100, 256, 5000, 10, False, 10),   # 32-row tiles, 4-feature chunks, the first layer of the headline model
+    (256, 47, 1024, 25, True, 25),     # 16-row tiles, 8-feature chunks, its last layer with the loss
+    (32, 64, 301, 5, False, 5),        # ragged last tile
+    (64, 8, 77, 3, True, 3),
+    (128, 128, 600, 15, False, 15),    # K = 256 (SAGE) on the 2 x 8 register tiles
+    (256, 47, 700, 25, True, 1),       # bound far below the real rows: indices read in place
+]
+
+
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("f,n_out,n_dst,fanout,last,bound", LAYER_CASES)
+def test_layer_fwd_parity(kind, f, n_out, n_dst, fanout, last, bound):
+    seed = f + n_out + n_dst + kind
+    blk, nrm = _oracle_block(seed, n=max(3000, 2 * n_dst), n_dst=n_dst, fanout=fanout)
+    rng = np.random.default_rng(seed)
+    h = _act(rng, blk.n_src, f, oracle.BF16)
+    K = 2 * f if kind == oracle.SAGE else f
+    w = (rng.standard_normal((K, n_out)) / np.sqrt(K)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(n_out)).astype(np.float32)
+    agg = oracle.aggregate_fwd(kind, blk, nrm if kind == oracle.GCN else None, h, oracle.BF16)
+    a_self, a_nbr = (h[:blk.n_dst], agg) if kind == oracle.SAGE else (agg, None)
+    want = oracle.update_fwd(a_self, a_nbr, w, b, not last, oracle.BF16, oracle.F32 if last else oracle.BF16)
+
+    db = upload_block(blk, nrm if kind == oracle.GCN else None)
+    wt = torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
+    agg_out = torch.empty((blk.n_dst, f), dtype=torch.bfloat16, device=DEV)
+    out = torch.empty((blk.n_dst, n_out), dtype=torch.float32 if last else torch.bfloat16, device=DEV)
+    kw = {}
+    if last:
+        labels_np = rng.integers(0, n_out, size=max(3000, 2 * n_dst)).astype(np.int64)
+        kw = dict(labels=torch.from_numpy(labels_np).to(DEV), batch=blk.n_dst,
+                  g_out=torch.empty((blk.n_dst, n_out), dtype=torch.float32, device=DEV),
+                  row_loss=torch.empty(blk.n_dst, dtype=torch.float32, device=DEV))
+    print(f"[layer_fwd] kind={kind} f={f} n_out={n_out} n_dst={n_dst} last={last} bound={bound}", flush=True)
+    gnn.layer_fwd(db, kind, bound, from_np_act(h), wt, torch.from_numpy(b).to(DEV), agg_out, out, **kw)
+    torch.cuda.synchronize()
+    assert relerr(oracle.to_float64(to_np_act(agg_out)), oracle.to_float64(agg)) <= 8e-3
+    assert relerr(oracle.to_float64(to_np_act(out)), oracle.to_float64(want)) <= 8e-3
+    if last:
+        y = labels_np[blk.src_ids[:blk.n_dst]]
+        loss, g = oracle.softmax_ce(want, y)
+        assert relerr(kw["g_out"].cpu().numpy(), g) <= 2e-2
+        assert abs(float(kw["row_loss"].mean()) - loss) <= 2e-2 * max(1.0, abs(loss))
+
+
+def test_layer_fwd_rejects_unsupported_shapes():
+    blk, _ = _oracle_block(5, n_dst=50, fanout=4)
+    db = upload_block(blk)
+    h = torch.zeros((blk.n_src, 512), dtype=torch.bfloat16, device=DEV)
+    wt = torch.zeros((256, 1024), dtype=torch.bfloat16, device=DEV)   # K = 1024: beyond the register tiles
+    agg = torch.empty((blk.n_dst, 512), dtype=torch.bfloat16, device=DEV)
+    out = torch.empty((blk.n_dst, 256), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(gnn.GnnError) as e:
+        gnn.layer_fwd(db, oracle.SAGE, 4, h, wt, None, agg, out)
+    assert e.value.code == gnn.GNN_EUNSUPPORTED
+    # 100 classes: fine for a hidden layer, over the loss epilogue's 64
+    h = torch.zeros((blk.n_src, 64), dtype=torch.bfloat16, device=DEV)
+    wt = torch.zeros((100, 128), dtype=torch.bfloat16, device=DEV)
+    agg = torch.empty((blk.n_dst, 64), dtype=torch.bfloat16, device=DEV)
+    gnn.layer_fwd(db, oracle.SAGE, 4, h, wt, None, agg, torch.empty((blk.n_dst, 100), dtype=torch.bfloat16,
+                                                                    device=DEV))
+    with pytest.raises(gnn.GnnError) as e:
+        gnn.layer_fwd(db, oracle.SAGE, 4, h, wt, None, agg, torch.empty((blk.n_dst, 100), device=DEV),
+                      labels=torch.zeros(4000, dtype=torch.int64, device=DEV), batch=blk.n_dst,
+                      g_out=torch.empty((blk.n_dst, 100), device=DEV), row_loss=torch.empty(blk.n_dst, device=DEV))
+    assert e.value.code == gnn.GNN_EUNSUPPORTED
+
+
+# ---------------------------------------------------------------------------
 # update GEMMs
 # ---------------------------------------------------------------------------
 
