@@ -33,6 +33,16 @@ if ROOT not in sys.path:
 import workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+# Source files of each single-kernel stage's kernel (their hash ties a
+# counter measurement to the code it was taken on).
+KERNEL_SOURCES = {
+    "layer_fwd": ["paper_2303_00158_amd/csrc/fused_layer.hip", "paper_2303_00158_amd/csrc/internal.h"],
+    "gather": ["paper_2303_00158_amd/csrc/gather.hip", "paper_2303_00158_amd/csrc/gather_dev.h",
+               "paper_2303_00158_amd/csrc/internal.h"],
+    "agg_bwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
+                "paper_2303_00158_amd/csrc/internal.h"],
+}
 HOST_LINK_PEAK_GBS = 64.0  # PCIe Gen5 x16, one direction
 BF16_PEAK_TFLOPS = 2500.0
 FP32_PEAK_TFLOPS = 157.3
@@ -64,6 +74,39 @@ def parse():
                         "overlapping the compute stage of step s (default: on; --no-pipeline times one "
                         "gnn_train_step call per step)")
     return p.parse_args()
+
+
+def source_hash(stage: str) -> str:
+    import hashlib
+    key = next((k for k in KERNEL_SOURCES if stage.startswith(k)), None)
+    if key is None:
+        return ""
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[key]:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(stage: str, workload: str):
+    """HBM bytes per launch of `stage` on `workload` from the committed
+    counter summaries (profiles/*_hbm_counters.md: rows of
+    | stage | workload | source hash | FETCH_SIZE KiB | WRITE_SIZE KiB | fetch scale | write scale | bytes |),
+    or None when there is none for the current source of the kernel."""
+    if not os.path.isdir(PROFILES):
+        return None
+    want = source_hash(stage)
+    for fn in sorted(os.listdir(PROFILES)):
+        if not fn.endswith("_hbm_counters.md"):
+            continue
+        for line in open(os.path.join(PROFILES, fn)):
+            cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
+            if len(cells) == 8 and cells[0] == stage and cells[1] == workload and cells[2] == want and want:
+                try:
+                    return int(cells[7])
+                except ValueError:
+                    return None
+    return None
 
 
 def log(msg):
@@ -106,6 +149,8 @@ class StagedStep:
             if l > 1:
                 self.da[l] = torch.empty((rows, w.k_of_layer(l)), dtype=torch.float32, device=dev)
         self.loss = torch.zeros(1, device=dev)
+        self.row_loss = torch.empty(batch_size, device=dev)
+        self.fused = {}  # layer -> whether gnn_layer_fwd serves it (as inside the training step)
         gemm = gnn.GNN_BF16 if act == torch.bfloat16 else gnn.GNN_F32
         self.fwd_ws, self.bwd_ws = {}, {}
         for l in range(1, L + 1):
@@ -115,7 +160,17 @@ class StagedStep:
             self.fwd_ws[l] = torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=dev)
             self.bwd_ws[l] = gnn.update_bwd_workspace(w.k_of_layer(l), dims[l], rows, gemm, dev)
 
-    def replay(self, name: str, trainer, table, reps: int) -> float:
+    def layer_fwd(self, l, trainer, labels):
+        """gnn_layer_fwd for layer l on the blocks of the last run."""
+        gnn, L = self.gnn, self.L
+        blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+        kw = {}
+        if l == L:
+            kw = dict(labels=labels, batch=self.blocks[0].c.cap_dst, g_out=self.grad[L], row_loss=self.row_loss)
+        gnn.layer_fwd(blk, self.kind, self.w.fanouts[L - l], hin, trainer.wt[l - 1], trainer.b[l - 1], self.agg[l],
+                      self.h[l], **kw)
+
+    def replay(self, name: str, trainer, table, reps: int, labels=None) -> float:
         """Launch the single ABI call of stage `name` `reps` times back to back
         on the blocks of the last run; returns the mean ms per launch (HIP
         events on the stream the call uses)."""
@@ -136,6 +191,9 @@ class StagedStep:
             call = lambda: gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None,  # noqa
                                           trainer.w[l - 1], trainer.b[l - 1], self.h[l], l < L, gemm,
                                           m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.fwd_ws[l])
+        elif name.startswith("layer_fwd_l"):
+            l = int(name[-1])
+            call = lambda: self.layer_fwd(l, trainer, labels)  # noqa
         elif name.startswith("agg_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -181,17 +239,30 @@ class StagedStep:
         mark("gather")
         sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
+        loss_fused = False
         for l in range(1, L + 1):
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
+            if self.fused.get(l, bool(trainer.wt)):
+                try:
+                    self.layer_fwd(l, trainer, labels)
+                    self.fused[l] = True
+                    loss_fused = l == L
+                    mark(f"layer_fwd_l{l}")
+                    continue
+                except gnn.GnnError as e:
+                    if e.code != gnn.GNN_EUNSUPPORTED:
+                        raise
+            self.fused[l] = False
             gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])
             mark(f"agg_fwd_l{l}")
             gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
                            trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
                            ws=self.fwd_ws[l])
             mark(f"update_fwd_l{l}")
-        gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
-        mark("loss")
+        if not loss_fused:
+            gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
+            mark("loss")
         for l in range(L, 0, -1):
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
@@ -232,6 +303,22 @@ class StagedStep:
             M, K, N = b["n_dst"], w.k_of_layer(l), w.dims[l]
             out = S_H if l < L else 4
             return M * K * S_H + K * N * 4 + N * 4 + M * N * out, 2 * M * K * N
+        if name.startswith("layer_fwd_l"):
+            l = int(name[-1])
+            b = self.blocks[L - l].host()
+            f, N, K = w.dims[l - 1], w.dims[l], w.k_of_layer(l)
+            M = b["n_dst"]
+            # distinct source rows read: the sampled columns and the rows' own (self) rows
+            R = np.union1d(np.unique(b["col"]), np.arange(M)).size
+            byts = R * f * S_H + 4 * b["nnz"] + 8 * (M + 1) + K * N * 2 + 4 * N + M * f * S_H
+            if w.kind == "gcn":
+                byts += 4 * R
+            if l == L:
+                B = self.blocks[0].c.cap_dst
+                byts += M * N * 4 + B * (16 + N * 4 + 4)  # logits; labels, targets, gradient, row loss
+            else:
+                byts += M * N * S_H
+            return byts, 2 * M * K * N
         if name.startswith("agg_bwd_l"):
             l = int(name[-1])
             b = self.blocks[L - l].host()
@@ -397,7 +484,8 @@ def main():
                 counts[n1] = counts.get(n1, 0) + 1
         stage_ms = {k: sums[k] / counts[k] for k in sums}
         result["stages_ms"] = {k: round(v, 5) for k, v in stage_ms.items()}
-        single = [k for k in stage_ms if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "agg_bwd"))]
+        single = [k for k in stage_ms
+                  if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd"))]
         ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 
         def roof_of(name, ms):
@@ -419,10 +507,10 @@ def main():
             return r
 
         # per-launch time of each single-kernel stage: back-to-back replays
-        launch_ms = {k: staged.replay(k, tr, table, args.replays) for k in single}
+        launch_ms = {k: staged.replay(k, tr, table, args.replays, labels=labels) for k in single}
         dom = max(single, key=lambda k: launch_ms[k])
         roof = roof_of(dom, launch_ms[dom])
-        roof.update({"kernel": dom, "traffic": None})
+        roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "source_hash": source_hash(dom)})
         result["roofline"] = roof
         result["kernels"] = {k: {kk: (round(vv, 6) if isinstance(vv, float) else vv)
                                  for kk, vv in roof_of(k, launch_ms[k]).items()} for k in single}
