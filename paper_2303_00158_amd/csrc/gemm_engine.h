@@ -530,16 +530,18 @@ __device__ __forceinline__ void split_range(int64_t total, int nsplit, int split
 __host__ __device__ inline int64_t part_ld(int64_t cols) { return (cols + 3) / 4 * 4; }
 
 // Sum over splits s = 0..nsplit-1, in that order, of the float4 at
-// p + s * stride.  Loads are issued eight splits at a time.
+// p + s * stride.  Loads are issued sixteen splits at a time (one round trip
+// for the usual split counts).
 __device__ __forceinline__ float4 sum_splits(const float *p, int64_t stride, int nsplit) {
+    constexpr int kAtOnce = 16;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s0 = 0; s0 < nsplit; s0 += 8) {
-        float4 v[8];
+    for (int s0 = 0; s0 < nsplit; s0 += kAtOnce) {
+        float4 v[kAtOnce];
 #pragma unroll
-        for (int g = 0; g < 8; ++g)
+        for (int g = 0; g < kAtOnce; ++g)
             v[g] = *reinterpret_cast<const float4 *>(p + static_cast<int64_t>(min(s0 + g, nsplit - 1)) * stride);
 #pragma unroll
-        for (int g = 0; g < 8; ++g) {
+        for (int g = 0; g < kAtOnce; ++g) {
             if (s0 + g < nsplit) {
                 acc.x += v[g].x;
                 acc.y += v[g].y;
