@@ -98,13 +98,10 @@ __device__ __forceinline__ void window_accumulate(float4 &acc, const T *x, int64
 // forward
 // ---------------------------------------------------------------------------
 template <int KIND, class TIn, class TOut, bool VEC>
-__device__ __forceinline__ void agg_fwd_body(const int64_t *__restrict__ counts, const int64_t *__restrict__ rowptr,
-                                             const int32_t *__restrict__ col, const float *__restrict__ src_norm,
-                                             const TIn *__restrict__ h, int64_t f, int C, int S,
-                                             TOut *__restrict__ out, int64_t blk) {
+__device__ __forceinline__ void agg_fwd_row(const int64_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+                                            const float *__restrict__ src_norm, const TIn *__restrict__ h, int64_t f,
+                                            int C, int S, TOut *__restrict__ out, int64_t row) {
     const int lane = threadIdx.x & 63;
-    const int64_t row = blk * kWaves + (threadIdx.x >> 6);
-    if (row >= counts[0]) return;
     const int64_t beg = rowptr[row], end = rowptr[row + 1];
     const int64_t deg = end - beg;
     const float wi = (KIND == GNN_AGG_GCN_SYM) ? src_norm[row] : 1.f;
@@ -156,15 +153,12 @@ __device__ __forceinline__ void agg_fwd_body(const int64_t *__restrict__ counts,
 // backward: d_src[j] = self(j) + sum_{i in csc(j)} w_ij d_a[i, nbr part]
 // ---------------------------------------------------------------------------
 template <int KIND, class THB, bool VEC>
-__device__ __forceinline__ void agg_bwd_body(const int64_t *__restrict__ counts, const int64_t *__restrict__ rowptr,
-                                             const int64_t *__restrict__ cscptr, const int32_t *__restrict__ cscrow,
-                                             const float *__restrict__ src_norm, const float *__restrict__ d_a,
-                                             int64_t f, int C, int S, const THB *__restrict__ h_below,
-                                             float *__restrict__ d_src, int64_t blk) {
+__device__ __forceinline__ void agg_bwd_row(int64_t n_dst, const int64_t *__restrict__ rowptr,
+                                            const int64_t *__restrict__ cscptr, const int32_t *__restrict__ cscrow,
+                                            const float *__restrict__ src_norm, const float *__restrict__ d_a,
+                                            int64_t f, int C, int S, const THB *__restrict__ h_below,
+                                            float *__restrict__ d_src, int64_t j) {
     const int lane = threadIdx.x & 63;
-    const int64_t j = blk * kWaves + (threadIdx.x >> 6);
-    const int64_t n_dst = counts[0];
-    if (j >= counts[1]) return;
     const int64_t ka = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * f : f;
     const int64_t nbr_off = (KIND == GNN_AGG_SAGE_MEAN) ? f : 0;
     const int64_t beg = cscptr[j], end = cscptr[j + 1];
@@ -214,6 +208,11 @@ __device__ __forceinline__ void agg_bwd_body(const int64_t *__restrict__ counts,
     }
 }
 
+// One row per wavefront, the grid's wavefronts striding over the rows (a
+// grid of at most kMaxBlocks workgroups: capacity-sized grids would mostly
+// hold workgroups that read the row count only to exit).
+constexpr int64_t kMaxBlocks = 2048;
+
 template <int KIND, class TIn, class TOut, bool VEC>
 struct FwdJob {
     gnn_block b;
@@ -221,8 +220,10 @@ struct FwdJob {
     int64_t f;
     int C, S;
     TOut *out;
-    __device__ void run(int64_t blk, int64_t) const {
-        agg_fwd_body<KIND, TIn, TOut, VEC>(b.counts, b.rowptr, b.col, b.src_norm, h, f, C, S, out, blk);
+    __device__ void run(int64_t blk, int64_t nblk) const {
+        const int64_t n = b.counts[0];
+        for (int64_t row = blk * kWaves + (threadIdx.x >> 6); row < n; row += nblk * kWaves)
+            agg_fwd_row<KIND, TIn, TOut, VEC>(b.rowptr, b.col, b.src_norm, h, f, C, S, out, row);
     }
 };
 
@@ -234,9 +235,11 @@ struct BwdJob {
     int C, S;
     const THB *h_below;
     float *d_src;
-    __device__ void run(int64_t blk, int64_t) const {
-        agg_bwd_body<KIND, THB, VEC>(b.counts, b.rowptr, b.cscptr, b.cscrow, b.src_norm, d_a, f, C, S, h_below, d_src,
-                                     blk);
+    __device__ void run(int64_t blk, int64_t nblk) const {
+        const int64_t n_dst = b.counts[0], n_src = b.counts[1];
+        for (int64_t j = blk * kWaves + (threadIdx.x >> 6); j < n_src; j += nblk * kWaves)
+            agg_bwd_row<KIND, THB, VEC>(n_dst, b.rowptr, b.cscptr, b.cscrow, b.src_norm, d_a, f, C, S, h_below,
+                                        d_src, j);
     }
 };
 
@@ -246,7 +249,9 @@ inline void split_row(int64_t f, int *C, int *S) {
     *S = (c <= 32) ? static_cast<int>(64 / c) : 1;
 }
 
-inline unsigned row_grid(int64_t rows) { return static_cast<unsigned>(ceil_div(rows > 0 ? rows : 1, kWaves)); }
+inline unsigned row_grid(int64_t rows) {
+    return static_cast<unsigned>(std::min<int64_t>(ceil_div(rows > 0 ? rows : 1, kWaves), kMaxBlocks));
+}
 
 // f(job) with the forward job for (kind, hdt -> odt); false if unsupported.
 template <class F>

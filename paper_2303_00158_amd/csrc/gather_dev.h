@@ -192,7 +192,10 @@ inline unsigned grid_for(int64_t cap, int64_t dim, bool vec, bool host) {
     } else {
         b = ceil_div(cap * dim > 0 ? cap * dim : 1, kThreads);
     }
-    if (b > (1 << 20)) b = 1 << 20;
+    // rows are strided over the grid: 2048 workgroups cover the row counts
+    // of the workloads here in one or two rounds without dispatching
+    // workgroups that would only read the row count and exit
+    if (b > 2048) b = 2048;
     if (host && b > kHostGrid) b = kHostGrid;
     return static_cast<unsigned>(b);
 }

@@ -236,7 +236,10 @@ samp::HopPlan plan_hop(const gnn_graph *g, const float *gcn_norm, const int64_t 
     a.ticket = reinterpret_cast<int *>(hbase + hw.ticket);
     a.nb_rows = ceil_div(out->cap_dst > 0 ? out->cap_dst : 1, kThreads);
     a.nb_bits = ceil_div(a.words, kBitTile);
-    p.prep_grid = grid_for(std::max<int64_t>(out->cap_dst, 1) * 64, kThreads, kMaxGrid);
+    // one wavefront per destination row, at most 2048 workgroups (8192
+    // wavefronts) striding over the rows: capacity-sized grids would mostly
+    // hold workgroups that read the row count only to exit
+    p.prep_grid = grid_for(std::max<int64_t>(out->cap_dst, 1) * 64, kThreads, 2048);
     p.emit_grid = static_cast<unsigned>(a.nb_rows + a.nb_bits);
     p.relabel_grid = grid_for(std::max<int64_t>(out->cap_dst, 1) * fanout, kThreads, 1 << 16);
     p.r = fanout <= 64 ? 1 : fanout <= 128 ? 2 : fanout <= 256 ? 4 : fanout <= 512 ? 8 : 16;

@@ -159,66 +159,68 @@ __device__ __forceinline__ void hop_prepare_body(const HopArgs &a, int64_t blk, 
         a.counts[3] = 0;
     }
     const int lane = threadIdx.x & 63;
-    const int64_t row = gtid >> 6;
-    if (row >= n_dst) return;
-    const int64_t v = a.dst[row];
-    const int64_t beg = a.rowptr[v];
-    const int64_t d = a.rowptr[v + 1] - beg;
-    const int32_t k = a.k;
-    int64_t *out = a.gpad + row * k;
-    if (lane == 0) {
-        a.map[v] = static_cast<int32_t>(row);
-        a.src_ids[row] = v;
-        if (a.src_norm) a.src_norm[row] = a.gcn_norm[v];
-        a.cnt[row] = static_cast<int32_t>(d < k ? d : k);
-        set_bit(a.dbits, v);
-    }
-    if (d <= k) {
-        for (int64_t p = lane; p < d; p += 64) {
-            const int64_t u = a.col[beg + p];
-            out[p] = u;
-            set_bit(a.bits, u);
+    // one destination row per wavefront, the grid's wavefronts striding
+    // over the rows (the row is uniform per wavefront)
+    for (int64_t row = gtid >> 6; row < n_dst; row += gsize >> 6) {
+        const int64_t v = a.dst[row];
+        const int64_t beg = a.rowptr[v];
+        const int64_t d = a.rowptr[v + 1] - beg;
+        const int32_t k = a.k;
+        int64_t *out = a.gpad + row * k;
+        if (lane == 0) {
+            a.map[v] = static_cast<int32_t>(row);
+            a.src_ids[row] = v;
+            if (a.src_norm) a.src_norm[row] = a.gcn_norm[v];
+            a.cnt[row] = static_cast<int32_t>(d < k ? d : k);
+            set_bit(a.dbits, v);
         }
-        return;
-    }
-    uint32_t slot[R];
+        if (d <= k) {
+            for (int64_t p = lane; p < d; p += 64) {
+                const int64_t u = a.col[beg + p];
+                out[p] = u;
+                set_bit(a.bits, u);
+            }
+            continue;
+        }
+        uint32_t slot[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) slot[r] = 0xffffffffu;
-    const uint64_t pk = mix64(mix64(mix64(mix64(a.seed) ^ a.step) ^ a.hop) ^ static_cast<uint64_t>(v));
-    for (int32_t t = 0; t < k; ++t) {
-        const uint64_t j = static_cast<uint64_t>(d - k + t);
-        const uint64_t key = mix64(pk ^ static_cast<uint64_t>(t));
-        const uint32_t x = static_cast<uint32_t>(((key >> 32) * (j + 1)) >> 32);
-        bool mine = false;
+        for (int r = 0; r < R; ++r) slot[r] = 0xffffffffu;
+        const uint64_t pk = mix64(mix64(mix64(mix64(a.seed) ^ a.step) ^ a.hop) ^ static_cast<uint64_t>(v));
+        for (int32_t t = 0; t < k; ++t) {
+            const uint64_t j = static_cast<uint64_t>(d - k + t);
+            const uint64_t key = mix64(pk ^ static_cast<uint64_t>(t));
+            const uint32_t x = static_cast<uint32_t>(((key >> 32) * (j + 1)) >> 32);
+            bool mine = false;
 #pragma unroll
-        for (int r = 0; r < R; ++r) mine |= (r * 64 + lane < t) && (slot[r] == x);
-        const bool found = __ballot(mine) != 0ull;
-        const uint32_t val = found ? static_cast<uint32_t>(j) : x;
-        if (lane == (t & 63)) {
+            for (int r = 0; r < R; ++r) mine |= (r * 64 + lane < t) && (slot[r] == x);
+            const bool found = __ballot(mine) != 0ull;
+            const uint32_t val = found ? static_cast<uint32_t>(j) : x;
+            if (lane == (t & 63)) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    if (r == (t >> 6)) slot[r] = val;
+            }
+        }
+        // rank of each drawn position among all k (they are distinct)
+        int rank[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) rank[r] = 0;
+        for (int32_t s = 0; s < k; ++s) {
+            uint32_t mine = 0;
 #pragma unroll
             for (int r = 0; r < R; ++r)
-                if (r == (t >> 6)) slot[r] = val;
+                if (r == (s >> 6)) mine = slot[r];
+            const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine), s & 63));
+#pragma unroll
+            for (int r = 0; r < R; ++r) rank[r] += (other < slot[r]) ? 1 : 0;
         }
-    }
-    // rank of each drawn position among all k (they are distinct)
-    int rank[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) rank[r] = 0;
-    for (int32_t s = 0; s < k; ++s) {
-        uint32_t mine = 0;
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (r == (s >> 6)) mine = slot[r];
-        const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine), s & 63));
-#pragma unroll
-        for (int r = 0; r < R; ++r) rank[r] += (other < slot[r]) ? 1 : 0;
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if (r * 64 + lane < k) {
-            const int64_t u = a.col[beg + slot[r]];
-            out[rank[r]] = u;
-            set_bit(a.bits, u);
+        for (int r = 0; r < R; ++r) {
+            if (r * 64 + lane < k) {
+                const int64_t u = a.col[beg + slot[r]];
+                out[rank[r]] = u;
+                set_bit(a.bits, u);
+            }
         }
     }
 }
