@@ -186,6 +186,15 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     return st;
 }
 
+// Workgroups of a group's host-table gather, all copies together.  Reads of
+// host memory have microsecond latencies; with many in flight they hold up
+// the device-memory traffic of the compute stage running beside them (its
+// kernels ran up to 100x slower under a 256-workgroup gather).  64
+// workgroups still keep the host link near its rate: measured on the
+// 30M-vertex host-table workload, 64 -> 0.97 ms per step, 32 -> 0.97,
+// 16 -> 1.36 (link-starved), 256 -> 1.13.
+constexpr int kHostGroupGrid = 64;
+
 // The prepare stages of G (2 .. kMaxCopies) steps at once: the same
 // launches as run_prepare, each carrying one copy of every role per step
 // (Multi), so a group of steps pays the launch and latency chain of the
@@ -261,8 +270,11 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
         ga[c] = gath::Args{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0],
                            static_cast<char *>(preps[c]) + o.x0};
     }
-    const unsigned ggrid = gath::grid_for(blk[0][L - 1].cap_src, m->dims[0], gath::vec_ok(ga[0], tdt, act),
-                                          host_table);
+    // A host table's rows come over the host link, which a few hundred
+    // workgroups in total already saturate: the copies share that budget, so
+    // the rest of the GPU stays free for the compute stage running beside.
+    unsigned ggrid = gath::grid_for(blk[0][L - 1].cap_src, m->dims[0], gath::vec_ok(ga[0], tdt, act), host_table);
+    if (host_table) ggrid = std::max(1u, std::min(ggrid, static_cast<unsigned>(kHostGroupGrid / G)));
     bool same = true;
     const bool ok = gath::with_job(ga[0], tdt, act, [&](auto job) {
         using J = decltype(job);
