@@ -190,7 +190,8 @@ class StagedStep:
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
             call = lambda: gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None,  # noqa
                                           trainer.w[l - 1], trainer.b[l - 1], self.h[l], l < L, gemm,
-                                          m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.fwd_ws[l])
+                                          m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.fwd_ws[l],
+                                          wt=trainer.wt[l - 1] if trainer.wt else None)
         elif name.startswith("layer_fwd_l"):
             l = int(name[-1])
             call = lambda: self.layer_fwd(l, trainer, labels)  # noqa
@@ -243,7 +244,10 @@ class StagedStep:
         for l in range(1, L + 1):
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
-            if self.fused.get(l, bool(trainer.wt)):
+            # as in the training step: layer 1's aggregation belongs to the
+            # prepare stage, its update reads it (fused kernel in A-load mode
+            # inside gnn_update_fwd); later layers in one gnn_layer_fwd
+            if (l > 1 or L == 1) and self.fused.get(l, bool(trainer.wt)):
                 try:
                     self.layer_fwd(l, trainer, labels)
                     self.fused[l] = True
@@ -258,7 +262,7 @@ class StagedStep:
             mark(f"agg_fwd_l{l}")
             gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
                            trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
-                           ws=self.fwd_ws[l])
+                           ws=self.fwd_ws[l], wt=trainer.wt[l - 1] if trainer.wt else None)
             mark(f"update_fwd_l{l}")
         if not loss_fused:
             gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
@@ -302,7 +306,8 @@ class StagedStep:
             b = self.blocks[L - l].host()
             M, K, N = b["n_dst"], w.k_of_layer(l), w.dims[l]
             out = S_H if l < L else 4
-            return M * K * S_H + K * N * 4 + N * 4 + M * N * out, 2 * M * K * N
+            S_W = 2 if S_H == 2 else 4  # the bf16 shadow of W in bf16 mode
+            return M * K * S_H + K * N * S_W + N * 4 + M * N * out, 2 * M * K * N
         if name.startswith("layer_fwd_l"):
             l = int(name[-1])
             b = self.blocks[L - l].host()

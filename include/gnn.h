@@ -224,6 +224,12 @@ gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, 
  *   a_self, a_nbr [device] row-major, row length k_each, adt in {F32, BF16}.
  *   m_dev   [device] int64 row count, or NULL to use cap_m.
  *   w       [device] fp32 K x n_out row-major; bias [device] fp32 n_out or NULL.
+ *   wt      [device] NULL, or the bf16 shadow W^T (n_out x K, 8-byte aligned,
+ *           as kept by gnn_model_sync_shadow): with gemm_dt GNN_BF16 it is
+ *           read instead of w (the same bf16 operand values).  For a bf16
+ *           hidden layer (adt = odt = GNN_BF16, relu) whose W^T fits the
+ *           fused layer kernel's register tiles, that kernel runs with the A
+ *           rows loaded from a_self / a_nbr.
  *   gemm_dt GNN_BF16: operands rounded to bf16, matrix cores, fp32 accumulate;
  *           GNN_F32: fp32 throughout.
  *   out     [device] cap_m x n_out of odt; ReLU applied when relu != 0.
@@ -237,9 +243,9 @@ gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, 
  * ------------------------------------------------------------------------ */
 gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
 gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
-                          const int64_t *m_dev, int64_t cap_m, const float *w, const float *bias, int64_t n_out,
-                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws, size_t ws_bytes,
-                          gnn_stream s);
+                          const int64_t *m_dev, int64_t cap_m, const float *w, const uint16_t *wt, const float *bias,
+                          int64_t n_out, int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws,
+                          size_t ws_bytes, gnn_stream s);
 
 /* Gradients of the update given g = dLoss/dZ (fp32, cap_m x n_out):
  *   dw = A^T g (K x n_out), db = column sums of g (unrounded, may be NULL),
@@ -305,11 +311,12 @@ gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s);
 /* Layout of a training step's internal buffers, for sizing and inspection.
  * Block h (1-based hop) is the block of layer L-h+1.
  *
- * The step has two stages: prepare (sampling of all hops and the gather of
- * X', Section IV-B's first stage) and compute (forward, loss, backward and
- * SGD).  Each has its own workspace.  Offsets of the prepare buffers
- * (sampler_ws .. x0) are bytes from the prepare workspace, those of the
- * compute buffers (agg .. loss) bytes from the compute workspace.  The
+ * The step has two stages: prepare (sampling of all hops, the gather of X'
+ * (Section IV-B's first stage) and layer 1's aggregation, which needs no
+ * weights) and compute (the rest of the forward, loss, backward and SGD).
+ * Each has its own workspace.  Offsets of the prepare buffers (sampler_ws ..
+ * x0, agg[1]) are bytes from the prepare workspace, those of the compute
+ * buffers (agg[l >= 2] .. loss) bytes from the compute workspace.  The
  * one-call step's workspace (total_bytes) holds the prepare workspace at
  * byte 0 and the compute workspace at byte prep_bytes. */
 typedef struct gnn_step_layout {
@@ -322,7 +329,8 @@ typedef struct gnn_step_layout {
         blk_src_norm[GNN_MAX_LAYERS]; /* per hop; 0 when absent */
     size_t blk_csc_ws[GNN_MAX_LAYERS]; /* per hop with a transpose: its scratch; else 0 */
     size_t x0;                          /* gathered X' (cap_src of hop L rows) */
-    size_t agg[GNN_MAX_LAYERS + 1];     /* per layer l: aggregation output */
+    size_t agg[GNN_MAX_LAYERS + 1];     /* per layer l: aggregation output (layer 1's is computed by the
+                                           prepare stage and lives in the prepare workspace) */
     size_t h[GNN_MAX_LAYERS + 1];       /* per layer l: H^l (l < L) or logits (l = L) */
     size_t grad[GNN_MAX_LAYERS + 1];    /* per layer l: G^l = dLoss/dZ^l, fp32 */
     size_t d_a[GNN_MAX_LAYERS + 1];     /* per layer l >= 2: dLoss/dA^l, fp32 */
@@ -369,7 +377,8 @@ gnn_status gnn_train_step(const gnn_model *m, const gnn_graph *g, const float *g
  * gnn_step_prepare_workspace_init: once per prepare workspace (sampler
  *   state), as gnn_train_step_workspace_init for the one-call workspace.
  * gnn_step_prepare: arguments as gnn_train_step; writes the blocks, their
- *   transposes and X' into prep_ws (prep_bytes >= layout.prep_bytes).
+ *   transposes, X' and layer 1's aggregation into prep_ws (prep_bytes >=
+ *   layout.prep_bytes).
  * gnn_step_compute: graph_n and batch as given to gnn_step_prepare; labels
  *   [device] int64[graph_n]; the targets are read back from prep_ws (the
  *   first batch sources of hop 1); writes m->dw, m->db, updates m->w, m->b

@@ -291,9 +291,9 @@ gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m
 }
 
 gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
-                          const int64_t *m_dev, int64_t cap_m, const float *w, const float *bias, int64_t n_out,
-                          int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws, size_t ws_bytes,
-                          gnn_stream s) {
+                          const int64_t *m_dev, int64_t cap_m, const float *w, const uint16_t *wt, const float *bias,
+                          int64_t n_out, int32_t relu, gnn_dtype gemm_dt, void *out, gnn_dtype odt, void *ws,
+                          size_t ws_bytes, gnn_stream s) {
     clear_error();
     const char *who = "gnn_update_fwd";
     GNN_CHECK(act_dtype(adt) && act_dtype(odt) && act_dtype(gemm_dt), GNN_EUNSUPPORTED,
@@ -311,8 +311,9 @@ gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
         GNN_CHECK(aligned(ws, 256), GNN_EINVAL, "%s: ws must be 256-byte aligned", who);
         GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     }
-    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, nullptr, bias, n_out, relu, gemm_dt, out, odt, ws,
-                             stream_of(s));
+    GNN_CHECK(aligned(wt, 8), GNN_EINVAL, "%s: wt must be 8-byte aligned", who);
+    return launch_update_fwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, gemm_dt == GNN_BF16 ? wt : nullptr, bias,
+                             n_out, relu, gemm_dt, out, odt, ws, stream_of(s));
 }
 
 gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes) {

@@ -36,7 +36,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct FusedArgs {
-    const int64_t *counts;  // counts[0] = destination rows M
+    const int64_t *counts;  // counts[0] = destination rows M (null: M = cap_dst)
     const int64_t *rowptr;  // block CSR [M + 1]
     const int32_t *col;     // local source ids
     const float *src_norm;  // GCN normalisers per local source (destinations first), else null
@@ -56,6 +56,9 @@ struct FusedArgs {
     float *row_loss;        // [b]
     int64_t b;
     int kpad, ldk;          // K rounded up to 32; LDS row stride of the A tile (kpad + 8)
+    // A-load mode (a_nbr != null): the aggregation was done beforehand; the
+    // A rows are [a_self[i] || a_nbr[i]] (GraphSAGE) or a_nbr[i] (GCN), bf16
+    const uint16_t *a_self, *a_nbr;
 };
 
 // A 16-byte MFMA operand fragment of bf16 W^T row n: elements k0 .. k0+7,
@@ -177,6 +180,36 @@ __device__ __forceinline__ void zero_item(int64_t f, int64_t e0, uint16_t *arow)
     if (KIND == GNN_AGG_SAGE_MEAN) Chunk<CW>::store(arow + f + e0, Chunk<CW>::zero());
 }
 
+// A-load mode: the A tile's rows straight from HBM.  Chunk c of a row is
+// features c * CW .. of the self part (c < C, GraphSAGE) or of the
+// aggregation part.  Up to four chunks per thread are loaded before any is
+// stored, so their loads are in flight together.
+template <int KIND, int CW>
+__device__ __forceinline__ void load_a_tile(const FusedArgs &a, int64_t row0, int rows, int C, uint16_t *As) {
+    using Ch = Chunk<CW>;
+    const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;  // chunks per A row
+    const int total = rows * KC;
+    constexpr int kU = 4;
+    for (int base = threadIdx.x; base < total; base += kU * kThreads) {
+        typename Ch::raw v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int it = base + u * kThreads;
+            const int q = it < total ? it : 0;
+            const int r = q / KC, c = q % KC;
+            const bool self = KIND == GNN_AGG_SAGE_MEAN && c < C;
+            const uint16_t *src = self ? a.a_self : a.a_nbr;
+            const int64_t e0 = static_cast<int64_t>(c - ((KIND == GNN_AGG_SAGE_MEAN && !self) ? C : 0)) * CW;
+            v[u] = Ch::load(src + (row0 + r) * a.f + e0);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int it = base + u * kThreads;
+            if (it < total) Ch::store(As + (it / KC) * a.ldk + (it % KC) * CW, v[u]);
+        }
+    }
+}
+
 // LOGITS: the last layer (fp32 logits, softmax cross-entropy in the
 // epilogue; n_out <= 64 so wavefronts 0..3 hold every column); otherwise a
 // hidden layer (bias, ReLU, bf16 output).  TPW column tiles per wavefront,
@@ -207,10 +240,12 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
         bv[t] = (a.bias && n < a.n_out) ? a.bias[n] : 0.f;
     }
 
-    const int64_t M = min(a.counts[0], a.cap_dst);
+    const int64_t M = a.counts ? min(a.counts[0], a.cap_dst) : a.cap_dst;
     const int64_t ntiles = (M + BM - 1) / BM;
     // 8-feature chunks (16-byte accesses) when rows allow it
-    const bool w8 = (f % 8) == 0 && aligned_dev(a.h, 16) && aligned_dev(a.agg_out, 16);
+    const bool load_a = a.a_nbr != nullptr;
+    const bool w8 = (f % 8) == 0 && (load_a ? aligned_dev(a.a_self, 16) && aligned_dev(a.a_nbr, 16)
+                                            : aligned_dev(a.h, 16) && aligned_dev(a.agg_out, 16));
     const int cw = w8 ? 8 : 4;
     const int C = static_cast<int>(f / cw);  // chunks per row
     const int kq = static_cast<int>((a.kpad - K) / 4);  // zero 4-element groups of the reduction tail
@@ -218,6 +253,16 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t row0 = tile * BM;
         const int rows = static_cast<int>(min<int64_t>(BM, M - row0));
+        if (load_a) {
+            if (w8) load_a_tile<KIND, 8>(a, row0, rows, C, As);
+            else load_a_tile<KIND, 4>(a, row0, rows, C, As);
+            const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;
+            for (int q = tid; q < (BM - rows) * KC; q += kThreads) {
+                uint16_t *dst = As + (rows + q / KC) * a.ldk + (q % KC) * cw;
+                *reinterpret_cast<uint2 *>(dst) = make_uint2(0u, 0u);
+                if (w8) *reinterpret_cast<uint2 *>(dst + 4) = make_uint2(0u, 0u);
+            }
+        } else {
         for (int r = tid; r <= rows; r += kThreads) Rs[r] = a.rowptr[row0 + r];
         __syncthreads();
         const int64_t e_beg = Rs[0];
@@ -244,6 +289,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
             if (w8) aggregate_item<KIND, 8>(a, E, rb, re, row0 + r, e0, arow);
             else aggregate_item<KIND, 4>(a, E, rb, re, row0 + r, e0, arow);
         }
+        }  // aggregation mode
         for (int q = tid; q < BM * kq; q += kThreads) {
             const int r = q / kq, k = static_cast<int>(K) + (q % kq) * 4;
             *reinterpret_cast<uint2 *>(As + r * a.ldk + k) = make_uint2(0u, 0u);
@@ -387,6 +433,7 @@ gnn_status go_shape(const Shape &sh, const FusedArgs &a, unsigned grid, size_t l
 
 bool fused_layer_ok(int kind, int precision, int64_t f, int64_t n_out, int64_t cap_dst, int32_t maxdeg, bool last,
                     const void *h, const uint16_t *wt, const void *agg_out) {
+    // (in A-load mode h is the self part and agg_out the aggregation)
     if (precision != GNN_BF16 || wt == nullptr) return false;
     if (!aligned(h, 8) || !aligned(wt, 8) || !aligned(agg_out, 8)) return false;
     const Shape sh = fused_shape(kind, f, n_out, cap_dst, maxdeg, last);
@@ -396,10 +443,12 @@ bool fused_layer_ok(int kind, int precision, int64_t f, int64_t n_out, int64_t c
     return fused_lds(sh, kpad + 8, last, maxdeg) <= 64 * 1024;
 }
 
-gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, const void *h, int64_t f,
-                              const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
-                              bool last, const int64_t *labels, float *g, float *row_loss, int64_t batch,
-                              hipStream_t s) {
+namespace {
+
+gnn_status launch_fused(const gnn_block *b, int kind, int32_t maxdeg, const void *h, int64_t f, const uint16_t *wt,
+                        const float *bias, int64_t n_out, void *agg_out, const void *a_self, const void *a_nbr,
+                        void *out, bool last, const int64_t *labels, float *g, float *row_loss, int64_t batch,
+                        hipStream_t s) {
     const Shape sh = fused_shape(kind, f, n_out, b->cap_dst, maxdeg, last);
     GNN_CHECK(sh.ok, GNN_EUNSUPPORTED, "fused_layer: shape not supported");
     const int64_t K = kind == GNN_AGG_SAGE_MEAN ? 2 * f : f;
@@ -424,6 +473,8 @@ gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, cons
     a.b = batch;
     a.kpad = static_cast<int>(ceil_div(K, 32) * 32);
     a.ldk = a.kpad + 8;
+    a.a_self = static_cast<const uint16_t *>(a_self);
+    a.a_nbr = static_cast<const uint16_t *>(a_nbr);
     const size_t lds = fused_lds(sh, a.ldk, last, maxdeg);
     const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(std::max<int64_t>(b->cap_dst, 1), sh.bm),
                                                                   256));
@@ -432,6 +483,24 @@ gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, cons
                     : go_shape<GNN_AGG_SAGE_MEAN, false>(sh, a, grid, lds, s);
     return last ? go_shape<GNN_AGG_GCN_SYM, true>(sh, a, grid, lds, s)
                 : go_shape<GNN_AGG_GCN_SYM, false>(sh, a, grid, lds, s);
+}
+
+}  // namespace
+
+gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, const void *h, int64_t f,
+                              const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
+                              bool last, const int64_t *labels, float *g, float *row_loss, int64_t batch,
+                              hipStream_t s) {
+    return launch_fused(b, kind, maxdeg, h, f, wt, bias, n_out, agg_out, nullptr, nullptr, out, last, labels, g,
+                        row_loss, batch, s);
+}
+
+gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self, const void *a_nbr, int64_t f,
+                               const uint16_t *wt, const float *bias, int64_t n_out, void *out, bool last,
+                               const int64_t *labels, float *g, float *row_loss, int64_t batch, hipStream_t s) {
+    GNN_CHECK(a_nbr && (kind != GNN_AGG_SAGE_MEAN || a_self), GNN_EINVAL, "fused_update: NULL A operand");
+    return launch_fused(b, kind, 1, a_self ? a_self : a_nbr, f, wt, bias, n_out, nullptr, a_self, a_nbr, out, last,
+                        labels, g, row_loss, batch, s);
 }
 
 }  // namespace gnn

@@ -34,8 +34,7 @@ gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt
     return GNN_OK;
 }
 
-gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hipStream_t s,
-                                   const Role<csc::SortJob> &extra) {
+gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hipStream_t s) {
     GNN_CHECK(p.pa.map.blocks() <= kMaxGrid && p.pw.map.blocks() <= kMaxGrid, GNN_ESIZE,
               "update_bwd: too many tiles for one launch");
     // The common variants (64 x 64 tiles, vector activations and dA, the
@@ -45,11 +44,7 @@ gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hip
     if (p.din_grid && p.pa.tile == 64 && p.pw.tile == 64 && p.vec_o && p.vec_a && act_matches) {
         gnn_status st = GNN_OK;
         auto go = [&](auto din, auto dwj) {
-            if (extra.n)
-                st = launch_jobs(s, "update_dinput+dweight+csc_sort", role(din, p.din_grid), role(dwj, p.dw_grid),
-                                 extra);
-            else
-                st = launch_job2(din, p.din_grid, dwj, p.dw_grid, s, "update_dinput+dweight");
+            st = launch_job2(din, p.din_grid, dwj, p.dw_grid, s, "update_dinput+dweight");
         };
         if (p.bf) {
             if (p.vec_g)
@@ -66,7 +61,6 @@ gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hip
         }
         return st;
     }
-    GNN_TRY(launch_job(extra.j, extra.n, s, "csc_sort"));
     gnn_status st = GNN_OK;
     if (p.din_grid) gbwd::with_dinput_job(a, p, [&](auto job) { st = launch_job(job, p.din_grid, s, "update_dinput"); });
     GNN_TRY(st);

@@ -11,9 +11,7 @@
 
 #include <type_traits>
 
-#include "csc_dev.h"
 #include "gemm_engine.h"
-#include "jobs.h"
 
 namespace gnn {
 namespace gbwd {
@@ -307,9 +305,7 @@ template <class F> void with_reduce_job(const Args &a, const Plan &p, F &&f) {
 
 // Host side (gemm_bwd.hip).
 // The two GEMMs of a layer's update backward (dA when a.d_a is given, and
-// the dW partials), in one launch when their variants allow it.  `extra`
-// (n = 0: none) is an independent transpose sort that rides along with them.
-gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hipStream_t s,
-                                   const Role<csc::SortJob> &extra = Role<csc::SortJob>{});
+// the dW partials), in one launch when their variants allow it.
+gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hipStream_t s);
 
 }  // namespace gnn

@@ -183,6 +183,21 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
                              int64_t cap_m, const float *w, const uint16_t *wt, const float *bias, int64_t n_out,
                              int relu, int gemm_dt, void *out, int odt, void *ws, hipStream_t s) {
     if (cap_m == 0 || n_out == 0) return GNN_OK;
+    // A hidden bf16 layer whose bf16 W^T is given and fits the register
+    // tiles: the fused layer kernel in A-load mode (W^T fragments in
+    // registers, A rows staged through LDS, no reduction split).  GCN's
+    // single A operand is its "aggregation part".
+    if (gemm_dt == GNN_BF16 && wt && adt == GNN_BF16 && odt == GNN_BF16 && relu) {
+        const int kind = a_nbr ? GNN_AGG_SAGE_MEAN : GNN_AGG_GCN_SYM;
+        const void *agg = a_nbr ? a_nbr : a_self;
+        if (fused_layer_ok(kind, GNN_BF16, k_each, n_out, cap_m, 1, false, a_self, wt, agg)) {
+            gnn_block b{};
+            b.cap_dst = cap_m;
+            b.counts = const_cast<int64_t *>(m_dev);
+            return launch_fused_update(&b, kind, a_nbr ? a_self : nullptr, agg, k_each, wt, bias, n_out, out, false,
+                                       nullptr, nullptr, nullptr, 0, s);
+        }
+    }
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
     FwdPlan p = plan_fwd(cap_m, n_out, K, bf);

@@ -171,6 +171,14 @@ gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, cons
                               const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
                               bool last, const int64_t *labels, float *g, float *row_loss, int64_t batch,
                               hipStream_t s);
+// The same launch when the aggregation was done beforehand: the A rows are
+// [a_self[i] || a_nbr[i]] (GraphSAGE) or a_nbr[i] (GCN), bf16, f wide each
+// (a_self may be null for GCN); only the block's row count is read.  Check
+// with fused_layer_ok(kind, GNN_BF16, f, n_out, cap_dst, 1, last, a_self or
+// a_nbr, wt, a_nbr).
+gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self, const void *a_nbr, int64_t f,
+                               const uint16_t *wt, const float *bias, int64_t n_out, void *out, bool last,
+                               const int64_t *labels, float *g, float *row_loss, int64_t batch, hipStream_t s);
 // wt = bf16(w^T) for a K x n row-major w.
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
 gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s);

@@ -12,7 +12,8 @@
 // Everything runs on the caller's stream.  The block transposes (CSC), which
 // only the backward pass reads, cost no launch of their own: their phases
 // (csc_dev.h) ride along with the sampling launches of later hops, and the
-// last sort with the loss (or, in a separate prepare stage, at its end).
+// last sort with layer 1's aggregation, which the prepare stage computes
+// because it needs no weights.
 #include <algorithm>
 #include <type_traits>
 
@@ -71,6 +72,9 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         if (h < L - 1) o->blk_csc_ws[h] = c.take(block_csc_ws_bytes(o->cap_src[h], o->cap_nnz[h]));
     }
     o->x0 = c.take(static_cast<size_t>(o->cap_src[L - 1]) * m->dims[0] * asz);
+    // layer 1's aggregation: computed in the prepare stage (it needs no
+    // weights), so it lives with the prepare buffers
+    o->agg[1] = c.take(static_cast<size_t>(o->cap_dst[L - 1]) * m->dims[0] * asz);
     o->prep_bytes = round_up(c.off, 256);
     // compute part: activations, gradients, GEMM and loss scratch, outputs
     Carver d(nullptr);
@@ -78,7 +82,7 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
     for (int l = 1; l <= L; ++l) {
         const int hb = L - l;
         const int64_t rows = o->cap_dst[hb];
-        o->agg[l] = d.take(static_cast<size_t>(rows) * m->dims[l - 1] * asz);
+        if (l >= 2) o->agg[l] = d.take(static_cast<size_t>(rows) * m->dims[l - 1] * asz);
         o->h[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
         o->grad[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * 4);
         if (l >= 2) o->d_a[l] = d.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
@@ -119,16 +123,17 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
     for (int h = 0; h < m->num_layers; ++h) blk[h] = block_view(o, h, prep);
 }
 
-// Sampling of all hops and the gather of X' into a prepare workspace, with
-// the transposes of blocks 1 .. L-1 (0-based hops 0 .. L-2).  Launches, for
-// hop h >= 1 (relabel(h) also counts the columns of block h's transpose):
+// Sampling of all hops, the gather of X' and layer 1's aggregation (which
+// needs no weights) into a prepare workspace, with the transposes of blocks
+// 1 .. L-1 (0-based hops 0 .. L-2).  Launches, for hop h >= 1 (relabel(h)
+// also counts the columns of block h's transpose):
 //   A_h = relabel(h-1) + prepare(h) + place(h-2)
 //   B_h = emit(h) + scan(h-1) + sort(h-2)
 //   F   = relabel(L-1) + gather + place(L-2)
-// The sort of block L-2 is left to the caller (*last_sort; n = 0 if none).
+//   G   = sort(L-2) + aggregation of layer 1 (the input layer's block, X')
 gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
                        bool host_table, int64_t row_stride, const int64_t *targets, uint64_t seed, uint64_t step,
-                       char *prep, const gnn_step_layout &o, Role<csc::SortJob> *last_sort, hipStream_t s) {
+                       char *prep, const gnn_step_layout &o, hipStream_t s) {
     const int L = m->num_layers;
     const int act = m->precision;
     gnn_block blk[GNN_MAX_LAYERS];
@@ -182,7 +187,10 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
                          place(L - 2));
     });
     GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
-    *last_sort = sort(L - 2);
+    GNN_TRY(st);
+    agg::with_fwd_job(&b0, m->kind, prep + o.x0, act, m->dims[0], prep + o.agg[1], act, [&](auto aj) {
+        st = launch_jobs(s, "csc_sort+aggregate_l1", sort(L - 2), role(aj, agg::row_grid(b0.cap_dst)));
+    });
     return st;
 }
 
@@ -291,63 +299,76 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
     GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
     GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
     GNN_TRY(st);
-    if (L >= 2) GNN_TRY(launch_jobs(s, "csc_sort", sort(L - 2)));
-    return GNN_OK;
+    // last: the sort of block L-2 and layer 1's aggregation
+    agg::with_fwd_job(&blk[0][L - 1], m->kind, static_cast<char *>(preps[0]) + o.x0, act, m->dims[0],
+                      static_cast<char *>(preps[0]) + o.agg[1], act, [&](auto aj) {
+        using J = decltype(aj);
+        J js[kMaxCopies];
+        for (int c = 0; c < G; ++c)
+            agg::with_fwd_job(&blk[c][L - 1], m->kind, static_cast<char *>(preps[c]) + o.x0, act, m->dims[0],
+                              static_cast<char *>(preps[c]) + o.agg[1], act, [&](auto jc) {
+                if constexpr (std::is_same<decltype(jc), J>::value) js[c] = jc;
+                else same = false;
+            });
+        if (same)
+            st = launch_jobs(s, "csc_sort+aggregate_l1", sort(L - 2),
+                             multi_role([&](int c) { return js[c]; }, G, agg::row_grid(blk[0][L - 1].cap_dst)));
+    });
+    GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
+    return st;
 }
 
-// Forward, loss, backward and SGD from a prepared workspace.  The targets are
-// the first rows of hop 1's sources (destinations come first).  pending is
-// a transpose sort still to run (n = 0 if none); it shares the loss launch,
-// before the backward pass reads the transposes.
+// Forward, loss, backward and SGD from a prepared workspace (blocks, their
+// transposes, X' and layer 1's aggregation).  The targets are the first rows
+// of hop 1's sources (destinations come first).
 gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch, float lr, float *loss_dev,
-                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o,
-                       const Role<csc::SortJob> &pending,
-                       hipStream_t s) {
+                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o, hipStream_t s) {
     const int L = m->num_layers;
     const int act = m->precision;
     gnn_block blk[GNN_MAX_LAYERS];
     block_views(m, o, prep, blk);
     const void *x0 = prep + o.x0;
 
+    // aggregation output of layer l (layer 1's was made by the prepare stage)
+    auto agg_of = [&](int l) { return l == 1 ? prep + o.agg[1] : comp + o.agg[l]; };
+
     // forward: one fused launch per layer where the shapes allow it (the
-    // last one with the loss in its epilogue), else aggregation and update
-    // as separate launches
+    // last one with the loss in its epilogue; layer 1 only multiplies, its
+    // aggregation is done), else aggregation and update as separate launches
     float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
     float *g_last = reinterpret_cast<float *>(comp + o.grad[L]);
     bool loss_done = false;
+    const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
     for (int l = 1; l <= L; ++l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
-        void *agg = comp + o.agg[l];
+        void *agg = agg_of(l);
         const int64_t f_in = m->dims[l - 1];
-        const int32_t maxdeg = m->fanouts[L - l];
-        if (fused_layer_ok(m->kind, m->precision, f_in, m->dims[l], b.cap_dst, maxdeg, l == L, hin, m->wt[l - 1],
-                           agg)) {
-            GNN_TRY(launch_fused_layer(&b, m->kind, maxdeg, hin, f_in, m->wt[l - 1], m->b[l - 1], m->dims[l], agg,
-                                       comp + o.h[l], l == L, labels, g_last, row_loss, batch, s));
+        const int32_t maxdeg = l == 1 ? 1 : m->fanouts[L - l];
+        if ((l > 1 || l == L) && fused_layer_ok(m->kind, m->precision, f_in, m->dims[l], b.cap_dst, maxdeg, l == L,
+                                                 hin, m->wt[l - 1], agg)) {
+            if (l == 1)  // a one-layer model: the prepared aggregation, with the loss
+                GNN_TRY(launch_fused_update(&b, m->kind, sage ? hin : nullptr, agg, f_in, m->wt[0], m->b[0],
+                                            m->dims[1], comp + o.h[1], true, labels, g_last, row_loss, batch, s));
+            else
+                GNN_TRY(launch_fused_layer(&b, m->kind, maxdeg, hin, f_in, m->wt[l - 1], m->b[l - 1], m->dims[l],
+                                           agg, comp + o.h[l], l == L, labels, g_last, row_loss, batch, s));
             loss_done = l == L;
             continue;
         }
-        GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
-        const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
+        // (a hidden layer 1 with a bf16 W^T that fits takes the fused
+        // kernel in A-load mode inside launch_update_fwd)
+        if (l > 1) GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
                                   m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, comp + o.h[l],
                                   l < L ? act : GNN_F32, comp + o.fwd_ws, s));
     }
-    // loss on the targets: gradient and row losses now, the mean with the
-    // last kernel of the step.  A pending transpose sort rides along, or,
-    // when the loss was fused into the last layer, with the first backward
-    // launch.
-    Role<csc::SortJob> bwd_extra{};
-    if (!loss_done) {
-        GNN_TRY(launch_jobs(s, "softmax_ce+csc_sort",
-                            role(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L],
-                                                  labels, blk[0].src_ids, g_last, row_loss},
-                                 static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64))),
-                            pending));
-    } else {
-        bwd_extra = pending;
-    }
+    // loss on the targets (unless fused into the last layer): gradient and
+    // row losses now, the mean with the last kernel of the step
+    if (!loss_done)
+        GNN_TRY(launch_job(loss::SoftmaxJob{reinterpret_cast<const float *>(comp + o.h[L]), batch, m->dims[L], labels,
+                                            blk[0].src_ids, g_last, row_loss},
+                           static_cast<unsigned>(ceil_div(batch, loss::kThreads / 64)), s, "softmax_ce"));
     // backward (reads the transposes).  Per layer: the dA and dW GEMMs in
     // one launch, then the dW reduction (with SGD on W^l, b^l and the
     // shadow) in one launch with the aggregation backward of the layer, or
@@ -365,16 +386,15 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
-        const void *agg_out = comp + o.agg[l];
+        const void *agg_out = agg_of(l);
         const int64_t f_in = m->dims[l - 1];
-        const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
         float *d_a = l > 1 ? reinterpret_cast<float *>(comp + o.d_a[l]) : nullptr;
         const gbwd::Args a{sage ? hin : agg_out, sage ? agg_out : nullptr, act, f_in, b.counts, b.cap_dst,
                            m->w[l - 1], reinterpret_cast<const float *>(comp + o.grad[l]), m->dims[l], m->precision,
                            m->dw[l - 1], m->db[l - 1], d_a, reinterpret_cast<float *>(comp + o.bwd_ws), m->w[l - 1],
                            m->b[l - 1], m->wt[l - 1], lr};
         const gbwd::Plan p = gbwd::plan(a);
-        GNN_TRY(launch_update_bwd_gemms(a, p, s, l == L ? bwd_extra : Role<csc::SortJob>{}));
+        GNN_TRY(launch_update_bwd_gemms(a, p, s));
         gnn_status st = GNN_OK;
         if (l > 1) {
             float *d_src = reinterpret_cast<float *>(comp + o.grad[l - 1]);
@@ -404,10 +424,8 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     GNN_TRY(step_layout(m, g->n, batch, &o));
     char *prep = static_cast<char *>(ws);
     char *comp = prep + o.prep_bytes;
-    Role<csc::SortJob> pending{};
-    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step, prep, o, &pending,
-                        s));
-    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, pending, s);
+    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step, prep, o, s));
+    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, s);
 }
 
 gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
@@ -415,10 +433,8 @@ gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
                             uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s) {
     gnn_step_layout o;
     GNN_TRY(step_layout(m, g->n, batch, &o));
-    Role<csc::SortJob> pending{};
-    GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step,
-                        static_cast<char *>(prep_ws), o, &pending, s));
-    return launch_job(pending.j, pending.n, s, "csc_sort");  // the stage ends with complete transposes
+    return run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step,
+                       static_cast<char *>(prep_ws), o, s);
 }
 
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
@@ -426,7 +442,7 @@ gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *
     gnn_step_layout o;
     GNN_TRY(step_layout(m, graph_n, batch, &o));
     return run_compute(m, labels, batch, lr, loss_dev, edges_dev, static_cast<char *>(prep_ws),
-                       static_cast<char *>(comp_ws), o, Role<csc::SortJob>{}, s);
+                       static_cast<char *>(comp_ws), o, s);
 }
 
 namespace {

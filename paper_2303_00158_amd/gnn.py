@@ -78,7 +78,8 @@ _SIGNATURES = {
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
-    "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz, _vp]),
+    "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz,
+                              _vp]),
     "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_bwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _sz,
                               _vp]),
@@ -276,9 +277,10 @@ def layer_fwd(block: "DeviceBlock", kind: int, max_row_len: int, h_src: torch.Te
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],
                out: torch.Tensor, relu: bool, gemm_dtype: int, m_dev: Optional[torch.Tensor] = None,
                cap_m: Optional[int] = None, ws: Optional[torch.Tensor] = None, split: bool = True,
-               stream=None) -> torch.Tensor:
+               wt: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """ws: workspace for split reductions (allocated when None and split is
-    True); split=False runs without a workspace (no reduction split)."""
+    True); split=False runs without a workspace (no reduction split).  wt:
+    optional bf16 W^T shadow (n_out x K) read instead of w in bf16 mode."""
     cap = a_self.shape[0] if cap_m is None else cap_m
     K = a_self.shape[1] * (2 if a_nbr is not None else 1)
     if ws is None and split:
@@ -286,7 +288,7 @@ def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Ten
         _check(lib().gnn_update_fwd_workspace_size(K, w.shape[1], cap, gemm_dtype, ctypes.byref(nb)))
         ws = torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=a_self.device)
     _check(lib().gnn_update_fwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev), cap,
-                                _ptr(w), _ptr(bias), w.shape[1], int(relu), gemm_dtype, _ptr(out),
+                                _ptr(w), _ptr(wt), _ptr(bias), w.shape[1], int(relu), gemm_dtype, _ptr(out),
                                 dtype_code(out.dtype), _ptr(ws), ws.numel() if ws is not None else 0,
                                 _stream(stream)))
     return out
@@ -491,4 +493,5 @@ class Trainer:
         """View of a step buffer of the last step (agg/h/grad/d_a per layer;
         x0 and the rest by name)."""
         off = getattr(self.layout, name)[layer] if name in ("agg", "h", "grad", "d_a") else getattr(self.layout, name)
-        return self._view(off, rows * cols, dtype, compute=name in _COMPUTE_BUFFERS).view(rows, cols)
+        compute = name in _COMPUTE_BUFFERS and not (name == "agg" and layer == 1)  # layer 1's: prepare stage
+        return self._view(off, rows * cols, dtype, compute=compute).view(rows, cols)

@@ -57,12 +57,16 @@ def test_host_validation_errors(gnn):
     assert (cs.value, cn.value) == (1024 * 26, 1024 * 25)
     assert lib.gnn_last_error() == b""
     # NULL weights, unsupported dtypes, bad sizes: rejected before any launch
-    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 8, None, 4, None, None, None, 8, 0, gnn.GNN_F32, None,
                               gnn.GNN_F32, None, 0, None) == gnn.GNN_EINVAL
-    assert lib.gnn_update_fwd(None, None, gnn.GNN_F16, 8, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F16, 8, None, 4, None, None, None, 8, 0, gnn.GNN_F32, None,
                               gnn.GNN_F32, None, 0, None) == gnn.GNN_EUNSUPPORTED
-    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 0, None, 4, None, None, 8, 0, gnn.GNN_F32, None,
+    assert lib.gnn_update_fwd(None, None, gnn.GNN_F32, 0, None, 4, None, None, None, 8, 0, gnn.GNN_F32, None,
                               gnn.GNN_F32, None, 0, None) == gnn.GNN_EINVAL
+    # a bf16 shadow must be 8-byte aligned
+    fake = 1 << 24
+    assert lib.gnn_update_fwd(fake, fake, gnn.GNN_BF16, 8, None, 4, fake, fake + 2, None, 8, 1, gnn.GNN_BF16, fake,
+                              gnn.GNN_BF16, None, 0, None) == gnn.GNN_EINVAL
     assert lib.gnn_gather_features(None, gnn.GNN_F32, gnn.GNN_LOC_DEVICE, 10, 4, 4, None, None, 3, None,
                                    gnn.GNN_F16, None) == gnn.GNN_EUNSUPPORTED
     assert lib.gnn_gather_features(None, gnn.GNN_F32, 7, 10, 4, 4, None, None, 3, None,
@@ -112,12 +116,13 @@ def test_step_layout_capacities_and_disjoint_buffers(gnn):
         prep += [(lay.blk_counts[h], 32), (lay.blk_src_ids[h], cs[h] * 8), (lay.blk_rowptr[h], (cd[h] + 1) * 8),
                  (lay.blk_col[h], cn[h] * 4)]
     prep += [(lay.blk_cscptr[0], (cs[0] + 1) * 8), (lay.blk_cscrow[0], cn[0] * 4), (lay.blk_csc_ws[0], 1)]
+    prep += [(lay.agg[1], cd[1] * 100 * 2)]  # layer 1's aggregation is made by the prepare stage
     comp = [(lay.fwd_ws, lay.fwd_ws_bytes), (lay.bwd_ws, lay.bwd_ws_bytes), (lay.loss_ws, lay.loss_ws_bytes),
             (lay.edges, 8), (lay.loss, 4)]
+    comp += [(lay.agg[2], cd[0] * 256 * 2)]
     for l, rows in ((1, cd[1]), (2, cd[0])):
-        f_in, f_out = (100, 256, 47)[l - 1], (100, 256, 47)[l]
-        comp += [(lay.agg[l], rows * f_in * 2), (lay.h[l], rows * f_out * (2 if l < 2 else 4)),
-                 (lay.grad[l], rows * f_out * 4)]
+        f_out = (100, 256, 47)[l]
+        comp += [(lay.h[l], rows * f_out * (2 if l < 2 else 4)), (lay.grad[l], rows * f_out * 4)]
     comp += [(lay.d_a[2], cd[0] * 512 * 4)]
     for spans, size in ((prep, lay.prep_bytes), (comp, lay.compute_bytes)):
         spans = sorted(spans)

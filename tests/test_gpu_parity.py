@@ -382,6 +382,33 @@ def test_layer_fwd_parity(kind, f, n_out, n_dst, fanout, last, bound):
         assert abs(float(kw["row_loss"].mean()) - loss) <= 2e-2 * max(1.0, abs(loss))
 
 
+@pytest.mark.parametrize("sage", [True, False])
+@pytest.mark.parametrize("m,cap,ke,n", [(5000, 6000, 100, 256), (301, 301, 32, 64), (1024, 2048, 128, 128),
+                                         (77, 77, 64, 47)])
+def test_update_fwd_with_shadow_matches_oracle(sage, m, cap, ke, n):
+    # gnn_update_fwd given the bf16 W^T: a hidden bf16 layer whose weights fit
+    # the fused kernel's register tiles runs it in A-load mode (the layer-1
+    # update of the training step); capacity above the device row count
+    rng = np.random.default_rng(m + ke + n + sage)
+    a_s = oracle.f32_to_bf16_bits(rng.standard_normal((cap, ke)).astype(np.float32))
+    a_n = oracle.f32_to_bf16_bits(rng.standard_normal((cap, ke)).astype(np.float32)) if sage else None
+    K = (2 if sage else 1) * ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(n)).astype(np.float32)
+    want = oracle.update_fwd(a_s[:m], a_n[:m] if sage else None, w, b, True, oracle.BF16, oracle.BF16)
+    wt = torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
+    out = torch.full((cap, n), float("nan"), dtype=torch.bfloat16, device=DEV)
+    m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
+    print(f"[update_fwd shadow] sage={sage} m={m} cap={cap} ke={ke} n={n}", flush=True)
+    gnn.update_fwd(from_np_act(a_s), from_np_act(a_n) if sage else None, from_np_act(w), from_np_act(b), out, True,
+                   gnn.GNN_BF16, m_dev=m_dev, cap_m=cap, wt=wt)
+    torch.cuda.synchronize()
+    got = to_np_act(out)
+    assert relerr(oracle.to_float64(got[:m]), oracle.to_float64(want)) <= 8e-3
+    # rows past the device count are not written
+    assert torch.isnan(out[m:].float()).all()
+
+
 def test_layer_fwd_rejects_unsupported_shapes():
     blk, _ = _oracle_block(5, n_dst=50, fanout=4)
     db = upload_block(blk)
