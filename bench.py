@@ -38,10 +38,14 @@ PROFILES = os.path.join(ROOT, "profiles")
 # counter measurement to the code it was taken on).
 KERNEL_SOURCES = {
     "layer_fwd": ["paper_2303_00158_amd/csrc/fused_layer.hip", "paper_2303_00158_amd/csrc/internal.h"],
+    "update_fwd": ["paper_2303_00158_amd/csrc/gemm_fwd.hip", "paper_2303_00158_amd/csrc/fused_layer.hip",
+                   "paper_2303_00158_amd/csrc/gemm_engine.h", "paper_2303_00158_amd/csrc/internal.h"],
+    "agg_fwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
+                "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
     "gather": ["paper_2303_00158_amd/csrc/gather.hip", "paper_2303_00158_amd/csrc/gather_dev.h",
-               "paper_2303_00158_amd/csrc/internal.h"],
+               "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
     "agg_bwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
-                "paper_2303_00158_amd/csrc/internal.h"],
+                "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
 }
 HOST_LINK_PEAK_GBS = 64.0  # PCIe Gen5 x16, one direction
 BF16_PEAK_TFLOPS = 2500.0
@@ -517,8 +521,9 @@ def main():
         roof = roof_of(dom, launch_ms[dom])
         roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "source_hash": source_hash(dom)})
         result["roofline"] = roof
-        result["kernels"] = {k: {kk: (round(vv, 6) if isinstance(vv, float) else vv)
-                                 for kk, vv in roof_of(k, launch_ms[k]).items()} for k in single}
+        result["kernels"] = {k: {**{kk: (round(vv, 6) if isinstance(vv, float) else vv)
+                                    for kk, vv in roof_of(k, launch_ms[k]).items()},
+                                 "traffic": measured_traffic(k, w.name)} for k in single}
         result["block_sizes"] = staged.block_sizes()
         if host_table:
             # X' rows moved over the host link per step, against the step time
