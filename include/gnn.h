@@ -194,7 +194,10 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
  * II-B in the epilogue for the last layer.
  *   h_src   [device] bf16 block->cap_src x f (row j is source j); f % 4 == 0.
  *   wt      [device] bf16 W^T, n_out x K (K = 2f for SAGE, self rows of W
- *           first; f for GCN), as kept by gnn_model_sync_shadow.
+ *           first; f for GCN), as kept by gnn_model_sync_shadow.  The
+ *           reduction is padded to a multiple of 32 with zero A entries
+ *           that meet weights of the same row, so a non-finite weight makes
+ *           its output column NaN (it is non-finite in any case).
  *   bias    [device] fp32 n_out, or NULL.
  *   agg_out [device] bf16 block->cap_dst x f: written with the aggregation
  *           (the mean for SAGE, the normalised sum for GCN), exactly what
@@ -229,7 +232,9 @@ gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, 
  *           read instead of w (the same bf16 operand values).  For a bf16
  *           hidden layer (adt = odt = GNN_BF16, relu) whose W^T fits the
  *           fused layer kernel's register tiles, that kernel runs with the A
- *           rows loaded from a_self / a_nbr.
+ *           rows loaded from a_self / a_nbr; a_self and a_nbr must then span
+ *           cap_m rows (rows at or past the count may be read, never used),
+ *           and the padding note of gnn_layer_fwd applies to wt.
  *   gemm_dt GNN_BF16: operands rounded to bf16, matrix cores, fp32 accumulate;
  *           GNN_F32: fp32 throughout.
  *   out     [device] cap_m x n_out of odt; ReLU applied when relu != 0.

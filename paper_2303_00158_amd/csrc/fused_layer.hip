@@ -13,8 +13,8 @@
 //    count is even known, so their latency hides behind the first tile);
 //  * the workgroup walks row tiles of BM (16 or 32) destination rows; per
 //    tile the row pointers and then the column indices are staged in LDS,
-//    every thread aggregates (row, 4- or 8-feature chunk) items with up to 8
-//    neighbour loads in flight, and the bf16 A tile ([self || mean] for
+//    every thread aggregates (row, 4- or 8-feature chunk) items with up to
+//    kNbr neighbour loads in flight, and the bf16 A tile ([self || mean] for
 //    GraphSAGE, the normalised sum for GCN) lands in LDS;
 //  * v_mfma_f32_16x16x32_bf16 over the A tile and the register-resident
 //    W^T, then bias, ReLU (hidden layers) and bf16 stores, or the loss.
@@ -31,12 +31,13 @@ namespace {
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kLogitLd = 65;  // row stride of the staged logits (fp32)
+constexpr int kNbr = 16;      // neighbour loads in flight per aggregation item
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct FusedArgs {
-    const int64_t *counts;  // counts[0] = destination rows M (null: M = cap_dst)
+    const int64_t *counts;  // M = min((counts[0] & cnt_keep) | cnt_add, cap_dst) (never null)
     const int64_t *rowptr;  // block CSR [M + 1]
     const int32_t *col;     // local source ids
     const float *src_norm;  // GCN normalisers per local source (destinations first), else null
@@ -55,23 +56,47 @@ struct FusedArgs {
     float *g;               // (softmax - onehot) / b, [b x n_out]
     float *row_loss;        // [b]
     int64_t b;
-    int kpad, ldk;          // K rounded up to 32; LDS row stride of the A tile (kpad + 8)
+    int kpad, ldk;          // KSM x 32 (the reduction length the kernel runs); A tile row stride (kpad + 8)
     // A-load mode (a_nbr != null): the aggregation was done beforehand; the
     // A rows are [a_self[i] || a_nbr[i]] (GraphSAGE) or a_nbr[i] (GCN), bf16
     const uint16_t *a_self, *a_nbr;
+    int64_t cnt_keep, cnt_add;  // -1, 0 with a device row count; 0, cap_dst without one
 };
 
-// A 16-byte MFMA operand fragment of bf16 W^T row n: elements k0 .. k0+7,
-// zero outside [0, n_out) x [0, K).  K is a multiple of 4, so each 4-element
-// half lies wholly inside or outside the row.
-__device__ __forceinline__ bf16x8 load_wfrag(const uint16_t *wt, int64_t K, int64_t n_out, int64_t n, int64_t k0) {
-    uint2 lo = make_uint2(0u, 0u), hi = make_uint2(0u, 0u);
-    const bool nok = n < n_out;
-    const uint16_t *row = wt + (nok ? n : 0) * K;
-    if (nok && k0 < K) lo = *reinterpret_cast<const uint2 *>(row + k0);
-    if (nok && k0 + 4 < K) hi = *reinterpret_cast<const uint2 *>(row + k0 + 4);
-    const uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-    return __builtin_bit_cast(bf16x8, u);
+// Kernel arguments are read with scalar loads, which the compiler otherwise
+// places next to their first use: several dependent round trips to the
+// argument buffer before the first vector load.  Naming every field in an
+// empty asm statement at entry makes all of them one batch of loads.
+template <class T> __device__ __forceinline__ void in_sgpr(const T &v) { asm volatile("" ::"s"(v)); }
+__device__ __forceinline__ void args_up_front(const FusedArgs &a) {
+    in_sgpr(a.counts), in_sgpr(a.rowptr), in_sgpr(a.col), in_sgpr(a.src_norm), in_sgpr(a.cap_dst);
+    in_sgpr(a.es_cap), in_sgpr(a.h), in_sgpr(a.f), in_sgpr(a.wt), in_sgpr(a.bias), in_sgpr(a.n_out);
+    in_sgpr(a.agg_out), in_sgpr(a.out), in_sgpr(a.labels), in_sgpr(a.targets), in_sgpr(a.g), in_sgpr(a.row_loss);
+    in_sgpr(a.b), in_sgpr(a.kpad), in_sgpr(a.ldk), in_sgpr(a.a_self), in_sgpr(a.a_nbr), in_sgpr(a.cnt_keep);
+    in_sgpr(a.cnt_add);
+}
+
+// A 16-byte MFMA operand fragment of bf16 W^T: elements k .. k+7 of the row
+// starting at element `row`.  W16 (K a multiple of 8, W^T 16-byte aligned):
+// one 16-byte load, indices past K read the row's last eight elements;
+// otherwise two 8-byte halves (K is a multiple of 4), indices past K read
+// the last four.  Those values are not zeroed: they meet A entries that are
+// zero (the A tile's padding), so a finite weight there contributes exactly
+// 0.  A wavefront's fragment is then 16 rows x 64 contiguous bytes.  Offsets
+// are 32-bit (W^T is far below 4 GiB) and the loads are unconditional and
+// branch-free: they are the first thing a wavefront issues, and a branch
+// around them would make the compiler wait for all of them at its join.
+template <bool W16>
+__device__ __forceinline__ bf16x8 load_wfrag(const uint16_t *wt, uint32_t row, uint32_t K, uint32_t k) {
+    const char *base = reinterpret_cast<const char *>(wt);
+    if constexpr (W16) {
+        return *reinterpret_cast<const bf16x8 *>(base + 2u * (row + min(k, K - 8)));
+    } else {
+        const uint32_t last = K - 4;
+        const uint2 lo = *reinterpret_cast<const uint2 *>(base + 2u * (row + min(k, last)));
+        const uint2 hi = *reinterpret_cast<const uint2 *>(base + 2u * (row + min(k + 4u, last)));
+        return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+    }
 }
 
 // Features e0 .. e0 + CW - 1 (CW = 4 or 8 bf16, one 8- or 16-byte access) of
@@ -119,8 +144,9 @@ template <> struct Chunk<8> {
 
 // One (row, chunk) item of the aggregation: the chunk of the A row (self and
 // mean for GraphSAGE, the normalised sum for GCN) into LDS and the
-// aggregation output.  The edges [rb, re) of the row are read from Es, eight
-// neighbour loads in flight.
+// aggregation output.  The edges [rb, re) of the row are read from Es, kNbr
+// neighbour loads in flight (a row of the usual fanouts takes one or two
+// rounds of load latency).
 template <int KIND, int CW>
 __device__ __forceinline__ void aggregate_item(const FusedArgs &a, const int32_t *Es, int rb, int re, int64_t row,
                                                int64_t e0, uint16_t *arow) {
@@ -132,17 +158,17 @@ __device__ __forceinline__ void aggregate_item(const FusedArgs &a, const int32_t
     Ch acc;
 #pragma unroll
     for (int i = 0; i < CW; ++i) acc.v[i] = 0.f;
-    for (int e = rb; e < re; e += 8) {
-        typename Ch::raw v[8];
-        float w[8];
+    for (int e = rb; e < re; e += kNbr) {
+        typename Ch::raw v[kNbr];
+        float w[kNbr];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < kNbr; ++q) {
             const int j = Es[e + q < re ? e + q : rb];
             v[q] = Ch::load(h + static_cast<int64_t>(j) * f + e0);
             w[q] = (KIND == GNN_AGG_GCN_SYM) ? wi * a.src_norm[j] : 1.f;
         }
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < kNbr; ++q) {
             if (e + q < re) {
                 Ch x;
                 x.set(v[q]);
@@ -180,43 +206,62 @@ __device__ __forceinline__ void zero_item(int64_t f, int64_t e0, uint16_t *arow)
     if (KIND == GNN_AGG_SAGE_MEAN) Chunk<CW>::store(arow + f + e0, Chunk<CW>::zero());
 }
 
-// A-load mode: the A tile's rows straight from HBM.  Chunk c of a row is
-// features c * CW .. of the self part (c < C, GraphSAGE) or of the
-// aggregation part.  Up to four chunks per thread are loaded before any is
-// stored, so their loads are in flight together.
+// A-load mode: the A tile's rows straight from HBM.  Item q of a tile is
+// chunk q % KC of row q / KC (KC chunks per A row); chunk c holds features
+// c * CW .. of the self part (c < C, GraphSAGE) or of the aggregation part.
+// A round is kU items per thread, all loaded before any is stored so that
+// their loads are in flight together.  The loads read any row inside the
+// capacity (rows at or past the row count are stored as zeros), so a tile's
+// first round can be issued before the row count has arrived.
+constexpr int kU = 4;
 template <int KIND, int CW>
-__device__ __forceinline__ void load_a_tile(const FusedArgs &a, int64_t row0, int rows, int C, uint16_t *As) {
-    using Ch = Chunk<CW>;
-    const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;  // chunks per A row
-    const int total = rows * KC;
-    constexpr int kU = 4;
-    for (int base = threadIdx.x; base < total; base += kU * kThreads) {
-        typename Ch::raw v[kU];
+__device__ __forceinline__ void load_a_round(const FusedArgs &a, int64_t row0, int C, int items, int base,
+                                             uint4 (&v)[kU]) {
+    const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int it = base + u * kThreads;
-            const int q = it < total ? it : 0;
-            const int r = q / KC, c = q % KC;
-            const bool self = KIND == GNN_AGG_SAGE_MEAN && c < C;
-            const uint16_t *src = self ? a.a_self : a.a_nbr;
-            const int64_t e0 = static_cast<int64_t>(c - ((KIND == GNN_AGG_SAGE_MEAN && !self) ? C : 0)) * CW;
-            v[u] = Ch::load(src + (row0 + r) * a.f + e0);
+    for (int u = 0; u < kU; ++u) {
+        const int it = base + u * kThreads;
+        const int q = it < items ? it : 0;
+        const int r = q / KC, c = q % KC;
+        const bool self = KIND == GNN_AGG_SAGE_MEAN && c < C;
+        const uint16_t *src = self ? a.a_self : a.a_nbr;
+        const int64_t e0 = static_cast<int64_t>(c - ((KIND == GNN_AGG_SAGE_MEAN && !self) ? C : 0)) * CW;
+        const int64_t row = min<int64_t>(row0 + r, a.cap_dst - 1);
+        if constexpr (CW == 8) {
+            v[u] = Chunk<8>::load(src + row * a.f + e0);
+        } else {
+            const uint2 w = Chunk<4>::load(src + row * a.f + e0);
+            v[u] = make_uint4(w.x, w.y, 0u, 0u);
         }
+    }
+}
+template <int KIND, int CW>
+__device__ __forceinline__ void store_a_round(const FusedArgs &a, int rows, int C, int items, int base,
+                                              const uint4 (&v)[kU], uint16_t *As) {
+    const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int it = base + u * kThreads;
-            if (it < total) Ch::store(As + (it / KC) * a.ldk + (it % KC) * CW, v[u]);
-        }
+    for (int u = 0; u < kU; ++u) {
+        const int it = base + u * kThreads;
+        if (it >= items) continue;
+        const int r = it / KC;
+        uint16_t *dst = As + r * a.ldk + (it % KC) * CW;
+        const uint4 x = r < rows ? v[u] : make_uint4(0u, 0u, 0u, 0u);
+        if constexpr (CW == 8) Chunk<8>::store(dst, x);
+        else Chunk<4>::store(dst, make_uint2(x.x, x.y));
     }
 }
 
 // LOGITS: the last layer (fp32 logits, softmax cross-entropy in the
 // epilogue; n_out <= 64 so wavefronts 0..3 hold every column); otherwise a
 // hidden layer (bias, ReLU, bf16 output).  TPW column tiles per wavefront,
-// KSM reduction steps held in registers (kpad / 32 <= KSM).
-template <int KIND, int BM, int TPW, int KSM, bool LOGITS>
+// KSM reduction steps held in registers (kpad = 32 KSM >= K; the A tile's
+// columns K .. kpad are zero, so every step runs unconditionally).  W16: 16-byte
+// weight loads (see load_wfrag).  LOADA: A-load
+// mode (a_nbr set), else aggregation mode.
+template <int KIND, int BM, int TPW, int KSM, bool LOGITS, bool LOADA, bool W16>
 __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
+    args_up_front(a);
     uint16_t *As = reinterpret_cast<uint16_t *>(smem);  // BM x ldk bf16; reused for the logits
     const size_t as_bytes = static_cast<size_t>(
         max(BM * a.ldk * 2, LOGITS ? BM * kLogitLd * 4 : 0));
@@ -225,8 +270,40 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t f = a.f;
     const int64_t K = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * f : f;
-    const int KS = a.kpad / 32;
     const int CT = static_cast<int>((a.n_out + 15) / 16);
+    constexpr int TPR = kThreads / BM;  // epilogue: 32 or 16 threads per row, within one wavefront
+    // 8-feature chunks (16-byte accesses) when rows allow it
+    constexpr bool load_a = LOADA;
+    const bool w8 = (f % 8) == 0 && (load_a ? aligned_dev(a.a_self, 16) && aligned_dev(a.a_nbr, 16)
+                                            : aligned_dev(a.h, 16) && aligned_dev(a.agg_out, 16));
+    const int cw = w8 ? 8 : 4;
+    const int C = static_cast<int>(f / cw);  // chunks per row
+    const int a_items = BM * ((KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C);
+    const int kq = static_cast<int>((a.kpad - K) / 4);  // zero 4-element groups of the reduction tail
+
+    // A tile's first loads do not wait for the row count: its row pointers
+    // (aggregation) or first A round (A-load), and in the last layer its
+    // target ids, are read inside the block's capacity and issued before the
+    // weights, since the vector-memory counter completes loads in issue
+    // order.  Only rows below the count use what they read.
+    int64_t rp = 0, tg = 0;
+    uint4 va[kU];
+    auto prefetch = [&](int64_t row0) {
+        if (load_a) {
+            if (w8) load_a_round<KIND, 8>(a, row0, C, a_items, tid, va);
+            else load_a_round<KIND, 4>(a, row0, C, a_items, tid, va);
+        } else if (tid <= BM) {
+            rp = a.rowptr[min<int64_t>(row0 + tid, a.cap_dst)];
+        }
+        if (LOGITS) tg = a.targets[min<int64_t>(row0 + tid / TPR, a.cap_dst - 1)];
+    };
+    prefetch(static_cast<int64_t>(blockIdx.x) * BM);
+
+    // The row count: a scalar load (it waits on its own counter, not behind
+    // the vector loads) whose use is branch-free arithmetic, so that nothing
+    // waits for it before the weights have been issued.
+    typedef const __attribute__((address_space(4))) int64_t *const_i64;
+    const int64_t M = min((*(const_i64)a.counts & a.cnt_keep) | a.cnt_add, a.cap_dst);
 
     // this wavefront's weight fragments and bias values
     bf16x8 wf[TPW][KSM];
@@ -234,36 +311,37 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
         const int64_t n = static_cast<int64_t>(wave + kWaves * t) * 16 + (lane & 15);
+        if (wave + kWaves * t < CT) {  // (uniform per wavefront)
+            // columns n >= n_out read row 0: they only feed outputs that are never stored
+            const uint32_t row = static_cast<uint32_t>((n < a.n_out ? n : 0) * K);
 #pragma unroll
-        for (int ks = 0; ks < KSM; ++ks)
-            wf[t][ks] = ks < KS ? load_wfrag(a.wt, K, a.n_out, n, ks * 32 + 8 * (lane >> 4)) : bf16x8{};
-        bv[t] = (a.bias && n < a.n_out) ? a.bias[n] : 0.f;
+            for (int ks = 0; ks < KSM; ++ks)
+                wf[t][ks] = load_wfrag<W16>(a.wt, row, static_cast<uint32_t>(K), ks * 32 + 8 * (lane >> 4));
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KSM; ++ks) wf[t][ks] = bf16x8{};
+        }
+        // (a null bias reads W^T instead; the epilogue discards it)
+        bv[t] = (a.bias ? a.bias : reinterpret_cast<const float *>(a.wt))[n < a.n_out ? n : 0];
     }
-
-    const int64_t M = a.counts ? min(a.counts[0], a.cap_dst) : a.cap_dst;
-    const int64_t ntiles = (M + BM - 1) / BM;
-    // 8-feature chunks (16-byte accesses) when rows allow it
-    const bool load_a = a.a_nbr != nullptr;
-    const bool w8 = (f % 8) == 0 && (load_a ? aligned_dev(a.a_self, 16) && aligned_dev(a.a_nbr, 16)
-                                            : aligned_dev(a.h, 16) && aligned_dev(a.agg_out, 16));
-    const int cw = w8 ? 8 : 4;
-    const int C = static_cast<int>(f / cw);  // chunks per row
-    const int kq = static_cast<int>((a.kpad - K) / 4);  // zero 4-element groups of the reduction tail
-
-    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    for (int64_t tile = blockIdx.x; tile * BM < a.cap_dst; tile += gridDim.x) {
         const int64_t row0 = tile * BM;
         const int rows = static_cast<int>(min<int64_t>(BM, M - row0));
+        if (rows <= 0) break;
+        if (tile != blockIdx.x) prefetch(row0);  // later tiles (few workgroups have any)
+        const int er = tid / TPR;  // this thread's row in the last layer's epilogue
+        const bool live = LOGITS && er < rows && row0 + er < a.b;
         if (load_a) {
-            if (w8) load_a_tile<KIND, 8>(a, row0, rows, C, As);
-            else load_a_tile<KIND, 4>(a, row0, rows, C, As);
-            const int KC = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C;
-            for (int q = tid; q < (BM - rows) * KC; q += kThreads) {
-                uint16_t *dst = As + (rows + q / KC) * a.ldk + (q % KC) * cw;
-                *reinterpret_cast<uint2 *>(dst) = make_uint2(0u, 0u);
-                if (w8) *reinterpret_cast<uint2 *>(dst + 4) = make_uint2(0u, 0u);
+            for (int base = tid; base < a_items; base += kU * kThreads) {
+                if (base != tid) {
+                    if (w8) load_a_round<KIND, 8>(a, row0, C, a_items, base, va);
+                    else load_a_round<KIND, 4>(a, row0, C, a_items, base, va);
+                }
+                if (w8) store_a_round<KIND, 8>(a, rows, C, a_items, base, va, As);
+                else store_a_round<KIND, 4>(a, rows, C, a_items, base, va, As);
             }
         } else {
-        for (int r = tid; r <= rows; r += kThreads) Rs[r] = a.rowptr[row0 + r];
+        if (tid <= rows) Rs[tid] = rp;
         __syncthreads();
         const int64_t e_beg = Rs[0];
         const int64_t ne = Rs[rows] - e_beg;
@@ -294,7 +372,22 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
             const int r = q / kq, k = static_cast<int>(K) + (q % kq) * 4;
             *reinterpret_cast<uint2 *>(As + r * a.ldk + k) = make_uint2(0u, 0u);
         }
+        // last layer: the row's label, in flight during the matrix-core work
+        // (the target id's load was issued with the weights, which the matrix
+        // cores need by now anyway)
+        const int64_t y = live ? a.labels[tg] : 0;
         __syncthreads();
+
+        // The bias as the epilogue uses it.  The empty asm keeps the choice
+        // inside the loop: hoisted before it, the choice would wait for the
+        // bias load, and with it for every load issued before it.
+        float bias_t[TPW];
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            bias_t[t] = bv[t];
+            asm volatile("" : "+v"(bias_t[t]));
+            if (!a.bias) bias_t[t] = 0.f;
+        }
 
         // the update on the matrix cores
         f32x4 acc[BM / 16][TPW];
@@ -307,18 +400,15 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
         for (int t = 0; t < TPW; ++t) any |= (wave + kWaves * t) < CT;
         if (any) {
 #pragma unroll
-            for (int ks = 0; ks < KSM; ++ks) {
-                if (ks < KS) {
+            for (int ks = 0; ks < KSM; ++ks)
 #pragma unroll
-                    for (int rt = 0; rt < BM / 16; ++rt) {
-                        const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
-                            As + (rt * 16 + (lane & 15)) * a.ldk + ks * 32 + 8 * (lane >> 4));
+                for (int rt = 0; rt < BM / 16; ++rt) {
+                    const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
+                        As + (rt * 16 + (lane & 15)) * a.ldk + ks * 32 + 8 * (lane >> 4));
 #pragma unroll
-                        for (int t = 0; t < TPW; ++t)
-                            acc[rt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[t][ks], acc[rt][t], 0, 0, 0);
-                    }
+                    for (int t = 0; t < TPW; ++t)
+                        acc[rt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[t][ks], acc[rt][t], 0, 0, 0);
                 }
-            }
         }
 
         if constexpr (!LOGITS) {
@@ -333,7 +423,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
                     for (int q = 0; q < 4; ++q) {
                         const int r = rt * 16 + 4 * (lane >> 4) + q;
                         if (r < rows) {
-                            const float z = acc[rt][t][q] + bv[t];
+                            const float z = acc[rt][t][q] + bias_t[t];
                             out[(row0 + r) * a.n_out + n] = f32_to_bf16(z > 0.f ? z : 0.f);
                         }
                     }
@@ -349,13 +439,11 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
                 for (int rt = 0; rt < BM / 16; ++rt)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        Ls[(rt * 16 + 4 * (lane >> 4) + q) * kLogitLd + n] = acc[rt][0][q] + bv[0];
+                        Ls[(rt * 16 + 4 * (lane >> 4) + q) * kLogitLd + n] = acc[rt][0][q] + bias_t[0];
             }
             __syncthreads();
-            constexpr int TPR = kThreads / BM;  // 32 or 16 threads per row, within one wavefront
-            const int r = tid / TPR, j = tid % TPR;
+            const int r = er, j = tid % TPR;
             const int64_t row = row0 + r;
-            const bool live = r < rows && row < a.b;
             const float *zr = Ls + r * kLogitLd;
             float mx = -INFINITY;
             for (int n = j; n < a.n_out; n += TPR) mx = fmaxf(mx, zr[n]);
@@ -367,7 +455,6 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
             for (int o = TPR / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
             if (live) {
                 const float lse = mx + logf(s);
-                const int64_t y = a.labels[a.targets[row]];
                 const float inv_b = 1.f / static_cast<float>(a.b);
                 float *lg = static_cast<float *>(a.out) + row * a.n_out;
                 for (int n = j; n < a.n_out; n += TPR) {
@@ -415,7 +502,15 @@ size_t fused_lds(const Shape &sh, int ldk, bool logits, int32_t maxdeg) {
 
 template <int KIND, int BM, int TPW, int KSM, bool LOGITS>
 gnn_status go(const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
-    fused_layer_kernel<KIND, BM, TPW, KSM, LOGITS><<<grid, kThreads, lds, s>>>(a);
+    const int64_t K = KIND == GNN_AGG_SAGE_MEAN ? 2 * a.f : a.f;
+    const bool w16 = K % 8 == 0 && aligned(a.wt, 16);
+    if (a.a_nbr) {
+        if (w16) fused_layer_kernel<KIND, BM, TPW, KSM, LOGITS, true, true><<<grid, kThreads, lds, s>>>(a);
+        else fused_layer_kernel<KIND, BM, TPW, KSM, LOGITS, true, false><<<grid, kThreads, lds, s>>>(a);
+    } else {
+        if (w16) fused_layer_kernel<KIND, BM, TPW, KSM, LOGITS, false, true><<<grid, kThreads, lds, s>>>(a);
+        else fused_layer_kernel<KIND, BM, TPW, KSM, LOGITS, false, false><<<grid, kThreads, lds, s>>>(a);
+    }
     return launch_status("fused_layer");
 }
 
@@ -439,8 +534,8 @@ bool fused_layer_ok(int kind, int precision, int64_t f, int64_t n_out, int64_t c
     const Shape sh = fused_shape(kind, f, n_out, cap_dst, maxdeg, last);
     if (!sh.ok) return false;
     const int64_t K = kind == GNN_AGG_SAGE_MEAN ? 2 * f : f;
-    const int kpad = static_cast<int>(ceil_div(K, 32) * 32);
-    return fused_lds(sh, kpad + 8, last, maxdeg) <= 64 * 1024;
+    (void)K;
+    return fused_lds(sh, sh.ksm * 32 + 8, last, maxdeg) <= 64 * 1024;
 }
 
 namespace {
@@ -453,7 +548,10 @@ gnn_status launch_fused(const gnn_block *b, int kind, int32_t maxdeg, const void
     GNN_CHECK(sh.ok, GNN_EUNSUPPORTED, "fused_layer: shape not supported");
     const int64_t K = kind == GNN_AGG_SAGE_MEAN ? 2 * f : f;
     FusedArgs a{};
-    a.counts = b->counts;
+    // without a device row count, M = cap_dst and the count load reads W^T
+    a.counts = b->counts ? b->counts : reinterpret_cast<const int64_t *>(wt);
+    a.cnt_keep = b->counts ? -1 : 0;
+    a.cnt_add = b->counts ? 0 : b->cap_dst;
     a.rowptr = b->rowptr;
     a.col = b->col;
     a.src_norm = b->src_norm;
@@ -471,7 +569,7 @@ gnn_status launch_fused(const gnn_block *b, int kind, int32_t maxdeg, const void
     a.g = g;
     a.row_loss = row_loss;
     a.b = batch;
-    a.kpad = static_cast<int>(ceil_div(K, 32) * 32);
+    a.kpad = sh.ksm * 32;
     a.ldk = a.kpad + 8;
     a.a_self = static_cast<const uint16_t *>(a_self);
     a.a_nbr = static_cast<const uint16_t *>(a_nbr);
