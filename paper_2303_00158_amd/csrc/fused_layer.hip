@@ -11,7 +11,7 @@
 //    w, w + 8, ... (16 columns each) and holds their bf16 W^T fragments for
 //    every 32-wide reduction step, loaded once per workgroup (before the row
 //    count is even known, so their latency hides behind the first tile);
-//  * the workgroup walks row tiles of BM (16 or 32) destination rows; per
+//  * the workgroup walks row tiles of BM (4, 8, 16 or 32) destination rows; per
 //    tile the row pointers and then the column indices are staged in LDS,
 //    every thread aggregates (row, 4- or 8-feature chunk) items with up to
 //    kNbr neighbour loads in flight, and the bf16 A tile ([self || mean] for
@@ -262,23 +262,28 @@ template <int KIND, int BM, int TPW, int KSM, bool LOGITS, bool LOADA, bool W16>
 __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     args_up_front(a);
-    uint16_t *As = reinterpret_cast<uint16_t *>(smem);  // BM x ldk bf16; reused for the logits
+    // the A tile has AR >= BM rows (whole 16-row matrix-core tiles; rows
+    // BM .. AR stay zero)
+    constexpr int RT = (BM + 15) / 16, AR = 16 * RT;
+    uint16_t *As = reinterpret_cast<uint16_t *>(smem);  // AR x ldk bf16; reused for the logits
     const size_t as_bytes = static_cast<size_t>(
-        max(BM * a.ldk * 2, LOGITS ? BM * kLogitLd * 4 : 0));
+        max(AR * a.ldk * 2, LOGITS ? AR * kLogitLd * 4 : 0));
     int64_t *Rs = reinterpret_cast<int64_t *>(smem + ((as_bytes + 15) & ~size_t(15)));  // BM + 1 row pointers
     int32_t *Es = reinterpret_cast<int32_t *>(Rs + BM + 1);                              // es_cap columns
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t f = a.f;
     const int64_t K = (KIND == GNN_AGG_SAGE_MEAN) ? 2 * f : f;
     const int CT = static_cast<int>((a.n_out + 15) / 16);
-    constexpr int TPR = kThreads / BM;  // epilogue: 32 or 16 threads per row, within one wavefront
+    // epilogue: TPR threads per row (64, 32 or 16, within one wavefront);
+    // with BM = 4 only the first 4 x 64 threads have a row
+    constexpr int TPR = kThreads / BM > 64 ? 64 : kThreads / BM;
     // 8-feature chunks (16-byte accesses) when rows allow it
     constexpr bool load_a = LOADA;
     const bool w8 = (f % 8) == 0 && (load_a ? aligned_dev(a.a_self, 16) && aligned_dev(a.a_nbr, 16)
                                             : aligned_dev(a.h, 16) && aligned_dev(a.agg_out, 16));
     const int cw = w8 ? 8 : 4;
     const int C = static_cast<int>(f / cw);  // chunks per row
-    const int a_items = BM * ((KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C);
+    const int a_items = AR * ((KIND == GNN_AGG_SAGE_MEAN) ? 2 * C : C);
     const int kq = static_cast<int>((a.kpad - K) / 4);  // zero 4-element groups of the reduction tail
 
     // A tile's first loads do not wait for the row count: its row pointers
@@ -354,7 +359,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
         __syncthreads();
 
         // aggregation into the A tile (and the aggregation output)
-        for (int it = tid; it < BM * C; it += kThreads) {
+        for (int it = tid; it < AR * C; it += kThreads) {
             const int r = it / C, c = it % C;
             const int64_t e0 = static_cast<int64_t>(c) * cw;
             uint16_t *arow = As + r * a.ldk;
@@ -368,7 +373,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
             else aggregate_item<KIND, 4>(a, E, rb, re, row0 + r, e0, arow);
         }
         }  // aggregation mode
-        for (int q = tid; q < BM * kq; q += kThreads) {
+        for (int q = tid; q < AR * kq; q += kThreads) {
             const int r = q / kq, k = static_cast<int>(K) + (q % kq) * 4;
             *reinterpret_cast<uint2 *>(As + r * a.ldk + k) = make_uint2(0u, 0u);
         }
@@ -390,9 +395,9 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
         }
 
         // the update on the matrix cores
-        f32x4 acc[BM / 16][TPW];
+        f32x4 acc[RT][TPW];
 #pragma unroll
-        for (int rt = 0; rt < BM / 16; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int t = 0; t < TPW; ++t) acc[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
         bool any = false;
@@ -402,7 +407,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
 #pragma unroll
             for (int ks = 0; ks < KSM; ++ks)
 #pragma unroll
-                for (int rt = 0; rt < BM / 16; ++rt) {
+                for (int rt = 0; rt < RT; ++rt) {
                     const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
                         As + (rt * 16 + (lane & 15)) * a.ldk + ks * 32 + 8 * (lane >> 4));
 #pragma unroll
@@ -418,7 +423,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
                 const int64_t n = static_cast<int64_t>(wave + kWaves * t) * 16 + (lane & 15);
                 if (n >= a.n_out) continue;
 #pragma unroll
-                for (int rt = 0; rt < BM / 16; ++rt)
+                for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         const int r = rt * 16 + 4 * (lane >> 4) + q;
@@ -436,7 +441,7 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
             if (wave < CT) {
                 const int n = wave * 16 + (lane & 15);
 #pragma unroll
-                for (int rt = 0; rt < BM / 16; ++rt)
+                for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
                         Ls[(rt * 16 + 4 * (lane >> 4) + q) * kLogitLd + n] = acc[rt][0][q] + bias_t[0];
@@ -484,7 +489,9 @@ Shape fused_shape(int kind, int64_t f, int64_t n_out, int64_t cap_dst, int32_t m
     if (tpw == 1 && ks <= 16) sh = Shape{0, 1, 16, true};
     else if (tpw == 2 && ks <= 8) sh = Shape{0, 2, 8, true};
     else return sh;
-    sh.bm = cap_dst >= 4096 ? 32 : 16;
+    // rows per tile: enough workgroups to spread the gather over the CUs
+    // (each CU keeps a bounded number of misses in flight)
+    sh.bm = cap_dst >= 8192 ? 32 : cap_dst >= 4096 ? 16 : cap_dst >= 2048 ? 8 : 4;
     return sh;
 }
 
@@ -495,8 +502,8 @@ int32_t es_cap_of(const Shape &sh, int32_t maxdeg) {
 }
 
 size_t fused_lds(const Shape &sh, int ldk, bool logits, int32_t maxdeg) {
-    const size_t as = std::max<size_t>(static_cast<size_t>(sh.bm) * ldk * 2,
-                                       logits ? static_cast<size_t>(sh.bm) * kLogitLd * 4 : 0);
+    const size_t ar = round_up(static_cast<size_t>(sh.bm), 16);  // A tile rows
+    const size_t as = std::max<size_t>(ar * ldk * 2, logits ? ar * kLogitLd * 4 : 0);
     return round_up(as, 16) + static_cast<size_t>(sh.bm + 1) * 8 + static_cast<size_t>(es_cap_of(sh, maxdeg)) * 4;
 }
 
@@ -516,6 +523,14 @@ gnn_status go(const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
 
 template <int KIND, bool LOGITS>
 gnn_status go_shape(const Shape &sh, const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
+    if (sh.bm == 4) {
+        if (sh.tpw == 1) return go<KIND, 4, 1, 16, LOGITS>(a, grid, lds, s);
+        return go<KIND, 4, 2, 8, LOGITS>(a, grid, lds, s);
+    }
+    if (sh.bm == 8) {
+        if (sh.tpw == 1) return go<KIND, 8, 1, 16, LOGITS>(a, grid, lds, s);
+        return go<KIND, 8, 2, 8, LOGITS>(a, grid, lds, s);
+    }
     if (sh.bm == 32) {
         if (sh.tpw == 1) return go<KIND, 32, 1, 16, LOGITS>(a, grid, lds, s);
         return go<KIND, 32, 2, 8, LOGITS>(a, grid, lds, s);
