@@ -186,10 +186,24 @@ __device__ __forceinline__ void hop_prepare_body(const HopArgs &a, int64_t blk, 
 #pragma unroll
         for (int r = 0; r < R; ++r) slot[r] = 0xffffffffu;
         const uint64_t pk = mix64(mix64(mix64(mix64(a.seed) ^ a.step) ^ a.hop) ^ static_cast<uint64_t>(v));
-        for (int32_t t = 0; t < k; ++t) {
+        // The draws' candidates x_t = floor(u_t (j_t + 1)) do not depend on
+        // one another: lane t computes draw t's hash (register t / 64), and
+        // only the membership test below runs draw by draw.
+        uint32_t cand[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t t = r * 64 + lane;
             const uint64_t j = static_cast<uint64_t>(d - k + t);
             const uint64_t key = mix64(pk ^ static_cast<uint64_t>(t));
-            const uint32_t x = static_cast<uint32_t>(((key >> 32) * (j + 1)) >> 32);
+            cand[r] = static_cast<uint32_t>(((key >> 32) * (j + 1)) >> 32);
+        }
+        for (int32_t t = 0; t < k; ++t) {
+            const uint64_t j = static_cast<uint64_t>(d - k + t);
+            uint32_t cr = 0;
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (r == (t >> 6)) cr = cand[r];
+            const uint32_t x = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(cr), t & 63));
             bool mine = false;
 #pragma unroll
             for (int r = 0; r < R; ++r) mine |= (r * 64 + lane < t) && (slot[r] == x);
