@@ -30,7 +30,9 @@ constexpr int kThreads = 256;
 constexpr int kPer = 8;                          // columns per thread in the scan
 constexpr int64_t kScanTile = kThreads * kPer;   // columns per scan workgroup
 constexpr int kShort = 16;                       // longest column sorted by one lane
-constexpr int kWindow = 4096;                    // rows counted per LDS pass of a long column
+// rows counted per LDS pass of a long column; its 8 KB of LDS per workgroup
+// is reserved by every launch the sort rides in, so it stays small
+constexpr int kWindow = 1024;
 
 struct Args {
     int64_t *counts;         // block counts: n_dst, n_src, nnz, error flag

@@ -128,7 +128,7 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
 // 1 .. L-1 (0-based hops 0 .. L-2).  Launches, for hop h >= 1 (relabel(h)
 // also counts the columns of block h's transpose):
 //   A_h = relabel(h-1) + prepare(h) + place(h-2)
-//   B_h = emit(h) + scan(h-1) + sort(h-2)
+//   B_h = emit(h) + scan(h-1) + sort(h-2)   (no sort role for h < 2)
 //   F   = relabel(L-1) + gather + place(L-2)
 //   G   = sort(L-2) + aggregation of layer 1 (the input layer's block, X')
 gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
@@ -172,8 +172,12 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
                              role(job, plan[h].prep_grid), place(h - 2));
         });
         GNN_TRY(st);
-        GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", role(samp::EmitJob{plan[h].a}, plan[h].emit_grid),
-                            scan(h - 1), sort(h - 2)));
+        if (h >= 2)
+            GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", role(samp::EmitJob{plan[h].a}, plan[h].emit_grid),
+                                scan(h - 1), sort(h - 2)));
+        else
+            GNN_TRY(launch_jobs(s, "hop_emit+csc_scan", role(samp::EmitJob{plan[h].a}, plan[h].emit_grid),
+                                scan(h - 1)));
     }
     // feature loading (rows of the input layer's sources) with the last
     // hop's relabel
@@ -270,7 +274,8 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
                              place(h - 2));
         });
         GNN_TRY(st);
-        GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", emit(h), scan(h - 1), sort(h - 2)));
+        if (h >= 2) GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", emit(h), scan(h - 1), sort(h - 2)));
+        else GNN_TRY(launch_jobs(s, "hop_emit+csc_scan", emit(h), scan(h - 1)));
     }
     gath::Args ga[kMaxCopies];
     for (int c = 0; c < G; ++c) {
