@@ -338,6 +338,66 @@ class StagedStep:
         return None, None
 
 
+def effective_rates(dev, host_table):
+    """Effective device-memory bandwidth (a plain 256 MiB device copy, read +
+    write bytes over its time) and, for a host table, the pinned host ->
+    device copy bandwidth: the burst bandwidths the performance model
+    divides by."""
+    n = 64 << 20  # fp32 elements: 256 MiB
+    src = torch.empty(n, device=dev)
+    dst = torch.empty(n, device=dev)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    bw_mem = 5 * 2 * n * 4 / (e0.elapsed_time(e1) / 1e3)
+    del src, dst
+    bw_link = HOST_LINK_PEAK_GBS * 1e9
+    if host_table:
+        h = torch.empty(n // 4, pin_memory=True)
+        d = torch.empty(n // 4, device=dev)
+        d.copy_(h, non_blocking=True)
+        e0.record()
+        for _ in range(3):
+            d.copy_(h, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        bw_link = 3 * n * 4 / 4 / (e0.elapsed_time(e1) / 1e3)
+        del h, d
+    return bw_mem, bw_link
+
+
+def perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev):
+    """Section V's model for the staged step's blocks, with the published
+    MI355X peaks and with effective rates measured here, beside the measured
+    step and stage times.  T_samp is the staged run's sampling time (the
+    paper measures it too)."""
+    from paper_2303_00158_amd import perf_model as pm
+    layers = pm.layers_from_blocks(staged.block_sizes(), w.dims)
+    n_input = staged.block_sizes()[-1]["n_src"]
+    t_samp = sum(v for k, v in stage_ms.items() if k.startswith("sample_hop")) / 1e3
+    s_table = table.element_size()
+    s_act = 2 if w.precision == "bf16" else 4
+    bw_mem, bw_link = effective_rates(dev, host_table)
+    eff = pm.Hardware(bw_mem=bw_mem, bw_link=bw_link, mac_rate=pm.MI355X_PEAK.mac_rate, name="MI355X effective")
+    prop_stages = [k for k in stage_ms if not k.startswith("sample_hop") and k != "gather"]
+    measured = {"samp": t_samp, "load" if not host_table else "load+trans": stage_ms.get("gather", 0.0) / 1e3,
+                "prop (staged, one launch per stage)": sum(stage_ms[k] for k in prop_stages) / 1e3}
+    out = {"readings": "one trainer, no T_sync; (+) = max (fused aggregate -> update); t_agg over f^{l-1}-wide "
+                       "inputs of the layer's own block; t_upd with K = 2 f^{l-1} (SAGE) or f^{l-1} (GCN)",
+           "rates": {"peak": {"bw_mem_GBs": pm.MI355X_PEAK.bw_mem / 1e9, "bw_link_GBs": pm.MI355X_PEAK.bw_link / 1e9,
+                              "mac_per_s": pm.MI355X_PEAK.mac_rate},
+                     "effective": {"bw_mem_GBs": bw_mem / 1e9, "bw_link_GBs": bw_link / 1e9,
+                                   "mac_per_s": eff.mac_rate}}}
+    for name, hw in (("peak", pm.MI355X_PEAK), ("effective", eff)):
+        p = pm.predict(layers, n_input, w.kind, hw, t_samp, s_table, s_act, host_table=host_table)
+        out[name] = pm.report(p, ms_per_step / 1e3, measured)
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -533,6 +593,10 @@ def main():
                                    "unit": "GB/s", "frac": ach / HOST_LINK_PEAK_GBS}
         log(f"stages (ms): {json.dumps(result['stages_ms'])}")
         log(f"per-launch (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
+        result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev)
+        pmr = result["perf_model"]["effective"]
+        log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 8)']:.1f} us "
+            f"(max of stages), serial {pmr['predicted_us']['serial sum']:.1f} us; measured {pmr['measured_step_us']:.1f} us")
 
     # ---- CPU oracle baseline ---------------------------------------------
     if not args.no_cpu_baseline:
