@@ -290,6 +290,13 @@ gnn_status gnn_sgd(float *w, const float *dw, int64_t n, float lr, gnn_stream s)
  * hidden activations are stored bf16 and every GEMM operand is rounded to
  * bf16 (fp32 accumulate); logits, gradients and weights stay fp32.  With
  * GNN_F32 everything is fp32.
+ *
+ * Feature loading: with an fp32 table in device memory and GNN_BF16, layer
+ * 1's aggregation reads the table rows it sums (each element rounded to bf16
+ * as the gather rounds it, so the result is bitwise that of aggregating X')
+ * and X' is gathered only for the destination rows of the input layer's
+ * block, which the update and the backward read; otherwise (host table,
+ * other dtypes) every source row of X' is gathered.
  * ------------------------------------------------------------------------ */
 typedef struct gnn_model {
     int32_t num_layers;                 /* L in [1, GNN_MAX_LAYERS] */
@@ -333,7 +340,7 @@ typedef struct gnn_step_layout {
         blk_col[GNN_MAX_LAYERS], blk_cscptr[GNN_MAX_LAYERS], blk_cscrow[GNN_MAX_LAYERS],
         blk_src_norm[GNN_MAX_LAYERS]; /* per hop; 0 when absent */
     size_t blk_csc_ws[GNN_MAX_LAYERS]; /* per hop with a transpose: its scratch; else 0 */
-    size_t x0;                          /* gathered X' (cap_src of hop L rows) */
+    size_t x0;                          /* gathered X' (cap_src of hop L rows; see feature loading) */
     size_t agg[GNN_MAX_LAYERS + 1];     /* per layer l: aggregation output (layer 1's is computed by the
                                            prepare stage and lives in the prepare workspace) */
     size_t h[GNN_MAX_LAYERS + 1];       /* per layer l: H^l (l < L) or logits (l = L) */

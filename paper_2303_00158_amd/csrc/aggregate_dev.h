@@ -66,8 +66,14 @@ __device__ __forceinline__ float4 shfl4(const float4 &v, int src) {
 // the same number of iterations so the shuffles stay convergent.  Lanes past
 // the window hold index 0 (a valid row) and the loads are issued
 // unconditionally; invalid terms are masked to zero before the FMA.  The
-// caller passes an in-row chunk offset for inactive lanes.
-template <bool VEC, class T>
+// caller passes an in-row chunk offset for inactive lanes.  ROUND: every
+// loaded value is first rounded to bf16 (round to nearest even), so that
+// summing fp32 table rows gives exactly the sum over their bf16 copies.
+__device__ __forceinline__ float4 round_bf16(float4 v) {
+    return make_float4(bf16_to_f32(f32_to_bf16(v.x)), bf16_to_f32(f32_to_bf16(v.y)), bf16_to_f32(f32_to_bf16(v.z)),
+                       bf16_to_f32(f32_to_bf16(v.w)));
+}
+template <bool VEC, class T, bool ROUND = false>
 __device__ __forceinline__ void window_accumulate(float4 &acc, const T *x, int64_t stride, int64_t col_off,
                                                   int64_t f, int32_t my_idx, float my_w, int wn, int slot, int S,
                                                   bool active, int64_t e0) {
@@ -84,7 +90,10 @@ __device__ __forceinline__ void window_accumulate(float4 &acc, const T *x, int64
         }
         float4 v[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = load_chunk<VEC>(x, static_cast<int64_t>(j[q]) * stride + col_off, e0, f);
+        for (int q = 0; q < 4; ++q) {
+            v[q] = load_chunk<VEC>(x, static_cast<int64_t>(j[q]) * stride + col_off, e0, f);
+            if constexpr (ROUND) v[q] = round_bf16(v[q]);
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const float wq = ok[q] ? w[q] : 0.f;
@@ -213,6 +222,91 @@ __device__ __forceinline__ void agg_bwd_row(int64_t n_dst, const int64_t *__rest
 // hold workgroups that read the row count only to exit).
 constexpr int64_t kMaxBlocks = 2048;
 
+// The input layer's forward aggregation straight from an fp32 feature table
+// (the feature loading fused into the aggregation, for tables in device
+// memory): row i's p-th sampled neighbour is the global vertex gids[i k + p]
+// (the sampler's staging of the block, in the block's column order), whose
+// table row is read and rounded to bf16 element by element, exactly as the
+// gather would have stored it in X'.  Same lanes, slots and summation order
+// as agg_fwd_row over X', so the result is bitwise the same.  The GCN
+// self term and weights use X' (its destination rows) and the graph's
+// normalisers of the global ids (src_norm of the block holds the same
+// values).
+template <int KIND, bool VEC>
+__device__ __forceinline__ void agg_fwd_row_table(const int64_t *__restrict__ rowptr,
+                                                  const int64_t *__restrict__ gids, int32_t k,
+                                                  const float *__restrict__ src_norm,
+                                                  const float *__restrict__ gcn_norm, const float *__restrict__ table,
+                                                  int64_t row_stride, const uint16_t *__restrict__ x_self, int64_t f,
+                                                  int C, int S, uint16_t *__restrict__ out, int64_t row) {
+    const int lane = threadIdx.x & 63;
+    const int64_t beg = rowptr[row], end = rowptr[row + 1];
+    const int64_t deg = end - beg;
+    const float wi = (KIND == GNN_AGG_GCN_SYM) ? src_norm[row] : 1.f;
+    const int groups = (C + 63) / 64;
+    const int slot = (S > 1) ? lane / C : 0;
+    for (int g = 0; g < groups; ++g) {
+        const int chunk = (S > 1) ? lane % C : g * 64 + lane;
+        const bool active = (S > 1) ? (slot < S) : (chunk < C);
+        const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int64_t wb = beg; wb < end; wb += 64) {
+            const int wn = static_cast<int>(min<int64_t>(64, end - wb));
+            int32_t my_idx = 0;
+            float my_w = 0.f;
+            if (lane < wn) {
+                const int64_t gv = gids[row * k + (wb - beg) + lane];
+                my_idx = static_cast<int32_t>(gv);
+                my_w = (KIND == GNN_AGG_GCN_SYM) ? wi * gcn_norm[gv] : 1.f;
+            }
+            window_accumulate<VEC, float, true>(acc, table, row_stride, 0, f, my_idx, my_w, wn, slot, S, active, e0);
+        }
+        for (int s2 = 1; s2 < S; ++s2) {
+            const float4 o = shfl4(acc, lane + s2 * C);
+            if (slot == 0) {
+                acc.x += o.x;
+                acc.y += o.y;
+                acc.z += o.z;
+                acc.w += o.w;
+            }
+        }
+        if (slot != 0 || !active) continue;
+        if (KIND == GNN_AGG_SAGE_MEAN) {
+            if (deg > 0) {
+                const float d = static_cast<float>(deg);
+                acc.x /= d;
+                acc.y /= d;
+                acc.z /= d;
+                acc.w /= d;
+            }
+        } else {
+            const float ws = wi * wi;
+            fma4(acc, ws, load_chunk<VEC>(x_self, row * f, e0, f));
+        }
+        store_chunk<VEC>(out, row * f, e0, f, acc);
+    }
+}
+
+template <int KIND, bool VEC>
+struct FwdTableJob {
+    gnn_block b;
+    const int64_t *gids;
+    int32_t k;
+    const float *gcn_norm;
+    const float *table;
+    int64_t row_stride;
+    const uint16_t *x_self;
+    int64_t f;
+    int C, S;
+    uint16_t *out;
+    __device__ void run(int64_t blk, int64_t nblk) const {
+        const int64_t n = b.counts[0];
+        for (int64_t row = blk * kWaves + (threadIdx.x >> 6); row < n; row += nblk * kWaves)
+            agg_fwd_row_table<KIND, VEC>(b.rowptr, gids, k, b.src_norm, gcn_norm, table, row_stride, x_self, f, C, S,
+                                         out, row);
+    }
+};
+
 template <int KIND, class TIn, class TOut, bool VEC>
 struct FwdJob {
     gnn_block b;
@@ -251,6 +345,24 @@ inline void split_row(int64_t f, int *C, int *S) {
 
 inline unsigned row_grid(int64_t rows) {
     return static_cast<unsigned>(std::min<int64_t>(ceil_div(rows > 0 ? rows : 1, kWaves), kMaxBlocks));
+}
+
+// f(job) with the table-reading forward job (fp32 table -> bf16 output).
+template <class F>
+void with_fwd_table_job(const gnn_block *b, int kind, const int64_t *gids, int32_t k, const float *gcn_norm,
+                        const float *table, int64_t row_stride, const uint16_t *x_self, int64_t f, uint16_t *out,
+                        F &&fn) {
+    int C, S;
+    split_row(f, &C, &S);
+    const bool vec = (f % 4 == 0) && (row_stride % 4 == 0) && aligned(table, 16) && aligned(x_self, 8) &&
+                     aligned(out, 8);
+    auto go = [&](auto kind_tag) {
+        constexpr int KIND = decltype(kind_tag)::value;
+        if (vec) fn(FwdTableJob<KIND, true>{*b, gids, k, gcn_norm, table, row_stride, x_self, f, C, S, out});
+        else fn(FwdTableJob<KIND, false>{*b, gids, k, gcn_norm, table, row_stride, x_self, f, C, S, out});
+    };
+    if (kind == GNN_AGG_SAGE_MEAN) go(std::integral_constant<int, GNN_AGG_SAGE_MEAN>{});
+    else go(std::integral_constant<int, GNN_AGG_GCN_SYM>{});
 }
 
 // f(job) with the forward job for (kind, hdt -> odt); false if unsupported.

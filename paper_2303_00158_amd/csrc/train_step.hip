@@ -123,6 +123,14 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
     for (int h = 0; h < m->num_layers; ++h) blk[h] = block_view(o, h, prep);
 }
 
+// The feature loading fuses into layer 1's aggregation for an fp32 table in
+// device memory feeding bf16 layers (the aggregation reads the table rows it
+// sums, and X' is gathered only for the destination rows, which the update
+// and the backward read); a host table is read once over the link into X'.
+bool fused_loading(const gnn_graph *g, bool host_table, int tdt, int act) {
+    return !host_table && tdt == GNN_F32 && act == GNN_BF16 && g->n <= INT32_MAX;
+}
+
 // Sampling of all hops, the gather of X' and layer 1's aggregation (which
 // needs no weights) into a prepare workspace, with the transposes of blocks
 // 1 .. L-1 (0-based hops 0 .. L-2).  Launches, for hop h >= 1 (relabel(h)
@@ -182,8 +190,12 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     // feature loading (rows of the input layer's sources) with the last
     // hop's relabel
     const gnn_block &b0 = blk[L - 1];
-    const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0], prep + o.x0};
-    const unsigned ggrid = gath::grid_for(b0.cap_src, m->dims[0], gath::vec_ok(ga, tdt, act), host_table);
+    const bool fuse = fused_loading(g, host_table, tdt, act);
+    // X': all sources of the input layer's block, or its destination rows
+    // (counts[0]) when the aggregation reads the table itself
+    const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + (fuse ? 0 : 1), fuse ? b0.cap_dst : b0.cap_src,
+                        m->dims[0], prep + o.x0};
+    const unsigned ggrid = gath::grid_for(ga.cap, m->dims[0], gath::vec_ok(ga, tdt, act), host_table);
     gnn_status st = GNN_OK;
     const bool ok = gath::with_job(ga, tdt, act, [&](auto job) {
         st = launch_jobs(s, "hop_relabel+gather+csc_place",
@@ -192,6 +204,15 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     });
     GNN_CHECK(ok, GNN_EUNSUPPORTED, "train_step: table dtype %d cannot feed precision %d", tdt, act);
     GNN_TRY(st);
+    if (fuse) {
+        agg::with_fwd_table_job(&b0, m->kind, plan[L - 1].a.gpad, plan[L - 1].a.k, gcn_norm,
+                                static_cast<const float *>(table), row_stride,
+                                reinterpret_cast<const uint16_t *>(prep + o.x0), m->dims[0],
+                                reinterpret_cast<uint16_t *>(prep + o.agg[1]), [&](auto aj) {
+            st = launch_jobs(s, "csc_sort+aggregate_l1_from_table", sort(L - 2), role(aj, agg::row_grid(b0.cap_dst)));
+        });
+        return st;
+    }
     agg::with_fwd_job(&b0, m->kind, prep + o.x0, act, m->dims[0], prep + o.agg[1], act, [&](auto aj) {
         st = launch_jobs(s, "csc_sort+aggregate_l1", sort(L - 2), role(aj, agg::row_grid(b0.cap_dst)));
     });
@@ -277,16 +298,17 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
         if (h >= 2) GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", emit(h), scan(h - 1), sort(h - 2)));
         else GNN_TRY(launch_jobs(s, "hop_emit+csc_scan", emit(h), scan(h - 1)));
     }
+    const bool fuse = fused_loading(g, host_table, tdt, act);
     gath::Args ga[kMaxCopies];
     for (int c = 0; c < G; ++c) {
         const gnn_block &b0 = blk[c][L - 1];
-        ga[c] = gath::Args{table, row_stride, b0.src_ids, b0.counts + 1, b0.cap_src, m->dims[0],
-                           static_cast<char *>(preps[c]) + o.x0};
+        ga[c] = gath::Args{table, row_stride, b0.src_ids, b0.counts + (fuse ? 0 : 1), fuse ? b0.cap_dst : b0.cap_src,
+                           m->dims[0], static_cast<char *>(preps[c]) + o.x0};
     }
     // A host table's rows come over the host link, which a few hundred
     // workgroups in total already saturate: the copies share that budget, so
     // the rest of the GPU stays free for the compute stage running beside.
-    unsigned ggrid = gath::grid_for(blk[0][L - 1].cap_src, m->dims[0], gath::vec_ok(ga[0], tdt, act), host_table);
+    unsigned ggrid = gath::grid_for(ga[0].cap, m->dims[0], gath::vec_ok(ga[0], tdt, act), host_table);
     if (host_table) ggrid = std::max(1u, std::min(ggrid, static_cast<unsigned>(kHostGroupGrid / G)));
     bool same = true;
     const bool ok = gath::with_job(ga[0], tdt, act, [&](auto job) {
@@ -305,6 +327,29 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
     GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
     GNN_TRY(st);
     // last: the sort of block L-2 and layer 1's aggregation
+    if (fuse) {
+        auto tjob = [&](int c, auto &&f) {
+            agg::with_fwd_table_job(&blk[c][L - 1], m->kind, plan[c][L - 1].a.gpad, plan[c][L - 1].a.k, gcn_norm,
+                                    static_cast<const float *>(table), row_stride,
+                                    reinterpret_cast<const uint16_t *>(static_cast<char *>(preps[c]) + o.x0),
+                                    m->dims[0], reinterpret_cast<uint16_t *>(static_cast<char *>(preps[c]) + o.agg[1]),
+                                    f);
+        };
+        tjob(0, [&](auto aj) {
+            using J = decltype(aj);
+            J js[kMaxCopies];
+            for (int c = 0; c < G; ++c)
+                tjob(c, [&](auto jc) {
+                    if constexpr (std::is_same<decltype(jc), J>::value) js[c] = jc;
+                    else same = false;
+                });
+            if (same)
+                st = launch_jobs(s, "csc_sort+aggregate_l1_from_table", sort(L - 2),
+                                 multi_role([&](int c) { return js[c]; }, G, agg::row_grid(blk[0][L - 1].cap_dst)));
+        });
+        GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
+        return st;
+    }
     agg::with_fwd_job(&blk[0][L - 1], m->kind, static_cast<char *>(preps[0]) + o.x0, act, m->dims[0],
                       static_cast<char *>(preps[0]) + o.agg[1], act, [&](auto aj) {
         using J = decltype(aj);

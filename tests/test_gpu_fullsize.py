@@ -117,10 +117,14 @@ def _run(w: workloads.Workload, steps: int, check_x0_rows: int = 0):
             assert relerr(tr.db[l - 1].cpu().numpy(), ref["dB"][l]) <= TOL, ("dB", s, l)
             assert relerr(tr.w[l - 1].cpu().numpy(), ref["new_w"][l - 1]) <= TOL, ("W", s, l)
         if check_x0_rows:
-            n0 = ref["x0"].shape[0]
+            # an fp32 table in HBM feeding bf16 layers: the step gathers X'
+            # only for the destination rows of the input layer's block (the
+            # aggregation reads the table); otherwise every source row
+            fused = w.table_dtype == "f32" and w.table_loc != "host" and w.precision == "bf16"
+            n0 = ref["blocks"][L - 1].n_dst if fused else ref["x0"].shape[0]
             x0 = tr.tensor("x0", 0, n0, w.dims[0], torch.bfloat16)
             got = x0.cpu().view(torch.int16).numpy().view(np.uint16)
-            assert np.array_equal(got, ref["x0"])  # bf16 RNE of the gathered rows, bit for bit
+            assert np.array_equal(got, ref["x0"][:n0])  # bf16 RNE of the gathered rows, bit for bit
         print(f"[fullsize] step {s}: ok, {ref['edges']} edges, loss {ref['loss']:.4f}", flush=True)
         w_ref = [x.cpu().numpy() for x in tr.w]  # continue from the GPU's weights
         b_ref = [x.cpu().numpy() for x in tr.b]

@@ -668,6 +668,49 @@ def test_train_step_rmat_bf16(kind):
         _check_step(tr, ref, oprec, 2)
 
 
+@pytest.mark.parametrize("kind", [gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_AGG_GCN_SYM])
+def test_fused_loading_equals_gather_then_aggregate(kind):
+    # fp32 table in device memory, bf16 layers: the prepare stage sums layer
+    # 1's neighbours straight from the table and gathers X' only for the
+    # destination rows.  Its aggregation must equal, bit for bit, a full
+    # gather (bf16 round to nearest even) followed by the aggregation kernel
+    # over X' on the same block; the gathered destination rows must equal
+    # the oracle's X'.
+    dims, fan, n, m, batch = (100, 256, 47), (25, 10), 30_000, 400_000, 512
+    rowptr, col = workloads.rmat_graph(n, m, seed=3)
+    table = workloads.features(n, dims[0], seed=3)
+    labels = workloads.labels(n, dims[-1], seed=3)
+    targets = workloads.targets_for_step(workloads.target_batches(n, batch, seed=3), batch, 0)
+    sage = kind == gnn.GNN_AGG_SAGE_MEAN
+    ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], 3, l) for l in range(2)]
+    bs = [torch.zeros(dims[l + 1]) for l in range(2)]
+    g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
+    nrm = gnn.gcn_norm(g)
+    tr = gnn.Trainer(kind, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV)
+    t_d = table.to(DEV)
+    print(f"[fused loading] kind={kind}", flush=True)
+    tr.step(g, t_d, labels.to(DEV), targets.to(DEV), seed=3, step=0, lr=0.05, gcn_norm_t=nrm)
+    torch.cuda.synchronize()
+    okind = oracle.GCN if kind == gnn.GNN_AGG_GCN_SYM else oracle.SAGE
+    cfg = oracle.StepConfig(kind=okind, dims=dims, fanouts=fan, precision=oracle.BF16, seed=3, step=0, lr=0.05)
+    nrm_h = oracle.gcn_norm(rowptr.numpy())
+    ref = oracle.train_step(rowptr.numpy(), col.numpy(), nrm_h, table.numpy(), labels.numpy(), targets.numpy(),
+                            [w.numpy() for w in ws], [b.numpy() for b in bs], cfg)
+    blk = ref["blocks"][1]  # hop 2: layer 1's block
+    got_blk = tr.block_view(2)
+    assert np.array_equal(got_blk["src_ids"], blk.src_ids) and np.array_equal(got_blk["col"], blk.col)
+    x0_dst = tr.tensor("x0", 0, blk.n_dst, dims[0], torch.bfloat16).cpu().view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(x0_dst, ref["x0"][:blk.n_dst])
+    db = upload_block(blk, src_norm=nrm_h[blk.src_ids] if not sage else None)
+    x0 = torch.empty((blk.n_src, dims[0]), dtype=torch.bfloat16, device=DEV)
+    gnn.gather_features(t_d, db.src_ids, x0)
+    want = torch.empty((blk.n_dst, dims[0]), dtype=torch.bfloat16, device=DEV)
+    gnn.aggregate_fwd(db, kind, x0, want)
+    got = tr.tensor("agg", 1, blk.n_dst, dims[0], torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
 def test_train_step_three_layer_sage_bf16():
     dims, fan = (128, 256, 256, 172), (15, 10, 5)
     for tr, ref, oprec in _step_case(gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, dims, fan, 40_000, 500_000, 256,
