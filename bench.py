@@ -189,6 +189,10 @@ class StagedStep:
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
             call = lambda: gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])  # noqa
+        elif name.startswith("agg_dedup_l"):
+            l = int(name[-1])
+            blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            call = lambda: gnn.aggregate_fwd_dedup(blk, self.kind, hin, self.agg[l])  # noqa
         elif name.startswith("update_fwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -336,6 +340,81 @@ class StagedStep:
             return (rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
                     + 8 * (b["n_dst"] + 1) + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
         return None, None
+
+
+def tile_bytes(rowptr, col, f, elem, rows=16):
+    """Source bytes an aggregation fetches: per edge (every edge reads its
+    source row) and per tile-distinct source (each distinct source of a tile
+    of `rows` destination rows read once)."""
+    per_edge = int(col.size) * f * elem
+    distinct = 0
+    for r0 in range(0, rowptr.size - 1, rows):
+        seg = col[rowptr[r0]:rowptr[min(r0 + rows, rowptr.size - 1)]]
+        distinct += np.unique(seg).size
+    return per_edge, distinct * f * elem
+
+
+def time_calls(call, reps):
+    call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def hub_block_case(gnn, dev, reps, n=50_000, hubs=128, n_dst=8192, fanout=25, f=256):
+    """A sampled hub-heavy block: every non-hub vertex links to all `hubs`
+    hubs and to two random vertices, so the rows of a tile share most of
+    their sources.  Pull against tile-deduplicated aggregation (bf16 in and
+    out): time per launch and source bytes."""
+    rng = np.random.default_rng(5)
+    deg = np.full(n, hubs + 2, np.int64)
+    deg[:hubs] = 0
+    rowptr = np.zeros(n + 1, np.int64)
+    rowptr[1:] = np.cumsum(deg)
+    col = np.empty(int(rowptr[-1]), np.int64)
+    body = np.concatenate([np.tile(np.arange(hubs), (n - hubs, 1)), rng.integers(0, n, (n - hubs, 2))], axis=1)
+    col[rowptr[hubs]:] = body.reshape(-1)
+    graph = gnn.DeviceGraph(torch.from_numpy(rowptr).to(dev), torch.from_numpy(col).to(dev))
+    blk = gnn.DeviceBlock(n, n_dst, fanout, False, False, dev)
+    nb = ctypes.c_size_t()
+    gnn._check(gnn.lib().gnn_sampler_workspace_size(n, n_dst, fanout, ctypes.byref(nb)))
+    ws = torch.empty(nb.value, dtype=torch.uint8, device=dev)
+    gnn._check(gnn.lib().gnn_sampler_workspace_init(ws.data_ptr(), nb.value, n, gnn._stream(None)))
+    dst = torch.from_numpy(rng.choice(np.arange(hubs, n), n_dst, replace=False).astype(np.int64)).to(dev)
+    gnn.build_block(graph, dst, fanout, 5, 0, 1, blk, ws, want_csc=False)
+    hb = blk.host()
+    h = torch.randn((blk.c.cap_src, f), device=dev).to(torch.bfloat16)
+    out = torch.empty((n_dst, f), dtype=torch.bfloat16, device=dev)
+    out2 = torch.empty_like(out)
+    kind = gnn.GNN_AGG_SAGE_MEAN
+    t_pull = time_calls(lambda: gnn.aggregate_fwd(blk, kind, h, out), reps)
+    t_dedup = time_calls(lambda: gnn.aggregate_fwd_dedup(blk, kind, h, out2), reps)
+    same = bool(torch.equal(out.view(torch.int16), out2.view(torch.int16)))
+    per_edge, distinct = tile_bytes(hb["rowptr"], hb["col"], f, 2)
+    return {"block": {"n_dst": hb["n_dst"], "n_src": hb["n_src"], "nnz": hb["nnz"], "f": f},
+            "pull_ms": t_pull, "dedup_ms": t_dedup, "bitwise_equal": same,
+            "source_bytes_per_edge": per_edge, "source_bytes_tile_distinct": distinct}
+
+
+def dedup_report(gnn, staged, w, reps, dev):
+    """Section IV-C's feature duplicator as tile-deduplicated aggregation
+    (gnn_aggregate_fwd_dedup) against the pull kernel: on the staged step's
+    blocks and on a hub-heavy block."""
+    out = {"tile_rows": 16}
+    elem = 2 if staged.act == torch.bfloat16 else 4
+    for l in range(1, staged.L + 1):
+        hb = staged.blocks[staged.L - l].host()
+        per_edge, distinct = tile_bytes(hb["rowptr"], hb["col"], w.dims[l - 1], elem)
+        out[f"layer{l}"] = {"pull_ms": staged.replay(f"agg_fwd_l{l}", None, None, reps),
+                            "dedup_ms": staged.replay(f"agg_dedup_l{l}", None, None, reps),
+                            "source_bytes_per_edge": per_edge, "source_bytes_tile_distinct": distinct}
+    out["hub_block"] = hub_block_case(gnn, dev, reps)
+    return out
 
 
 def effective_rates(dev, host_table):
@@ -594,6 +673,8 @@ def main():
         log(f"stages (ms): {json.dumps(result['stages_ms'])}")
         log(f"per-launch (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
         result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev)
+        result["dedup_aggregation"] = dedup_report(gnn, staged, w, args.replays, dev)
+        log(f"dedup aggregation: {json.dumps(result['dedup_aggregation'])}")
         pmr = result["perf_model"]["effective"]
         log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 8)']:.1f} us "
             f"(max of stages), serial {pmr['predicted_us']['serial sum']:.1f} us; measured {pmr['measured_step_us']:.1f} us")

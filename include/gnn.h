@@ -173,6 +173,19 @@ gnn_status gnn_gather_features(const void *table, gnn_dtype tdt, gnn_loc loc, in
 gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
                              void *out, gnn_dtype odt, gnn_stream s);
 
+/* The same aggregation with source reuse inside tiles of 16 destination
+ * rows: Section IV-C's feature duplicator (each source's feature vector is
+ * fetched once and handed to every destination that samples it).  A tile's
+ * column indices are deduplicated in LDS, each distinct source's features
+ * are read from HBM once per tile, and every row sums from LDS.  The sums
+ * follow gnn_aggregate_fwd's order term for term, so the output is bitwise
+ * the same; memory traffic is the tiles' distinct sources rather than their
+ * edges, which pays where destinations share sources (hub-heavy blocks).
+ * Arguments, layouts and errors as gnn_aggregate_fwd; tiles of more than
+ * 512 edges read their sources directly. */
+gnn_status gnn_aggregate_fwd_dedup(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
+                                   void *out, gnn_dtype odt, gnn_stream s);
+
 /* Backward of the aggregation for layers above the first (the backward pass
  * repeats the forward operators in reverse, Section II-B).  Reads the block's
  * transpose; uses no atomics, so results are bitwise reproducible.

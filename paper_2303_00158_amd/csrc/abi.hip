@@ -239,6 +239,20 @@ gnn_status gnn_aggregate_fwd(const gnn_block *b, gnn_agg kind, const void *h_src
     return launch_aggregate_fwd(b, kind, h_src, hdt, f, out, odt, stream_of(s));
 }
 
+gnn_status gnn_aggregate_fwd_dedup(const gnn_block *b, gnn_agg kind, const void *h_src, gnn_dtype hdt, int64_t f,
+                                   void *out, gnn_dtype odt, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_aggregate_fwd_dedup";
+    GNN_CHECK(kind == GNN_AGG_SAGE_MEAN || kind == GNN_AGG_GCN_SYM, GNN_EINVAL, "%s: unknown aggregation %d", who,
+              kind);
+    GNN_TRY(check_block(b, false, kind == GNN_AGG_GCN_SYM, who));
+    GNN_CHECK(act_dtype(hdt) && act_dtype(odt), GNN_EUNSUPPORTED, "%s: dtypes must be GNN_F32 or GNN_BF16", who);
+    GNN_CHECK(dim_ok(f), GNN_EINVAL, "%s: f %lld out of [1, %d]", who, (long long)f, GNN_MAX_DIM);
+    GNN_CHECK((h_src || b->cap_src == 0) && (out || b->cap_dst == 0), GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK(aligned(h_src, dtype_size(hdt)) && aligned(out, dtype_size(odt)), GNN_EINVAL, "%s: misaligned data", who);
+    return launch_aggregate_fwd_dedup(b, kind, h_src, hdt, f, out, odt, stream_of(s));
+}
+
 gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, const void *h_src, int64_t f,
                          const uint16_t *wt, const float *bias, int64_t n_out, void *agg_out, void *out,
                          const int64_t *labels, int64_t batch, float *g_out, float *row_loss, gnn_stream s) {

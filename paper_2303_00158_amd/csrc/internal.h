@@ -142,6 +142,8 @@ gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_st
                          const int64_t *n_ids_dev, int64_t cap_ids, void *out, int odt, bool host, hipStream_t s);
 gnn_status launch_aggregate_fwd(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
                                 hipStream_t s);
+gnn_status launch_aggregate_fwd_dedup(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out,
+                                      int odt, hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
                                 int hbdt, float *d_src, hipStream_t s);
 // Update GEMMs.  Their workspaces hold fp32 partial tiles of split

@@ -75,6 +75,7 @@ _SIGNATURES = {
     "gnn_build_block": (_i32, [_P(Graph), _vp, _vp, _vp, _i32, _u64, _u64, _i32, _i32, _P(Block), _vp, _sz, _vp]),
     "gnn_gather_features": (_i32, [_vp, _i32, _i32, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_fwd": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
+    "gnn_aggregate_fwd_dedup": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
@@ -250,6 +251,14 @@ def aggregate_fwd(block: DeviceBlock, kind: int, h_src: torch.Tensor, out: torch
     f = h_src.shape[1]
     _check(lib().gnn_aggregate_fwd(ctypes.byref(block.c), kind, _ptr(h_src), dtype_code(h_src.dtype), f, _ptr(out),
                                    dtype_code(out.dtype), _stream(stream)))
+    return out
+
+
+def aggregate_fwd_dedup(block: DeviceBlock, kind: int, h_src: torch.Tensor, out: torch.Tensor,
+                        stream=None) -> torch.Tensor:
+    f = h_src.shape[1]
+    _check(lib().gnn_aggregate_fwd_dedup(ctypes.byref(block.c), kind, _ptr(h_src), dtype_code(h_src.dtype), f,
+                                         _ptr(out), dtype_code(out.dtype), _stream(stream)))
     return out
 
 

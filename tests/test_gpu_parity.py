@@ -301,6 +301,70 @@ def test_aggregate_fwd_parity(f, kind, code):
     assert relerr(oracle.to_float64(got), oracle.to_float64(want)) <= (1e-5 if code == oracle.F32 else 8e-3)
 
 
+def _hub_block(seed, n=6000, hubs=64, n_dst=700, fanout=25, isolated_every=53):
+    """A hub-heavy block: every non-hub vertex links to all `hubs` hub
+    vertices (plus two random vertices), some vertices are isolated, so the
+    destinations of a tile mostly sample the same few sources."""
+    rng = np.random.default_rng(seed)
+    nbrs = []
+    for v in range(n):
+        if v < hubs or v % isolated_every == 0:
+            nbrs.append(np.zeros(0, np.int64))
+        else:
+            nbrs.append(np.concatenate([np.arange(hubs), rng.integers(0, n, 2)]).astype(np.int64))
+    rp = np.zeros(n + 1, np.int64)
+    rp[1:] = np.cumsum([a.size for a in nbrs])
+    cl = np.concatenate(nbrs)
+    dst = rng.choice(np.arange(hubs, n), size=n_dst, replace=False).astype(np.int64)
+    blk = oracle.build_block(rp, cl, dst, fanout, seed, 0, 1)
+    nrm = oracle.gcn_norm(rp)[blk.src_ids]
+    return blk, nrm
+
+
+DEDUP_BLOCKS = {
+    "rmat": lambda seed: _oracle_block(seed, n_dst=500, fanout=25),
+    "hub": lambda seed: _hub_block(seed),
+    # 16 rows x 40 edges > the 512 a tile stages: those tiles read directly
+    "hub_long_rows": lambda seed: _hub_block(seed, fanout=40),
+}
+
+
+@pytest.mark.parametrize("graph", sorted(DEDUP_BLOCKS))
+@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+def test_aggregate_fwd_dedup_equals_pull(graph, f, kind):
+    # the tile-deduplicated aggregation sums in the pull kernel's order:
+    # bitwise the same output, for every dtype pair
+    blk, nrm = DEDUP_BLOCKS[graph](f + 7 * kind)
+    assert blk.nnz > 0
+    db = upload_block(blk, nrm if kind == oracle.GCN else None)
+    rng = np.random.default_rng(f + kind)
+    for hc, oc in [(oracle.BF16, oracle.BF16), (oracle.F32, oracle.F32), (oracle.BF16, oracle.F32),
+                   (oracle.F32, oracle.BF16)]:
+        h = from_np_act(_act(rng, blk.n_src, f, hc))
+        odt = torch.bfloat16 if oc == oracle.BF16 else torch.float32
+        want = torch.full((blk.n_dst, f), float("nan"), dtype=odt, device=DEV)
+        got = torch.full((blk.n_dst, f), float("nan"), dtype=odt, device=DEV)
+        print(f"[dedup] {graph} f={f} kind={kind} {hc}->{oc}", flush=True)
+        gnn.aggregate_fwd(db, kind, h, want)
+        gnn.aggregate_fwd_dedup(db, kind, h, got)
+        torch.cuda.synchronize()
+        iv = torch.int16 if oc == oracle.BF16 else torch.int32
+        assert torch.equal(got.view(iv), want.view(iv)), (graph, f, kind, hc, oc)
+
+
+def test_aggregate_fwd_dedup_against_oracle():
+    blk, nrm = _hub_block(11)
+    rng = np.random.default_rng(11)
+    for kind in (oracle.SAGE, oracle.GCN):
+        h = _act(rng, blk.n_src, 64, oracle.F32)
+        want = oracle.aggregate_fwd(kind, blk, nrm if kind == oracle.GCN else None, h, oracle.F32)
+        db = upload_block(blk, nrm if kind == oracle.GCN else None)
+        out = torch.empty((blk.n_dst, 64), dtype=torch.float32, device=DEV)
+        gnn.aggregate_fwd_dedup(db, kind, from_np_act(h), out)
+        assert relerr(out.cpu().numpy().astype(np.float64), want) <= 1e-5
+
+
 @pytest.mark.parametrize("f", [4, 13, 100, 256])
 @pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
 @pytest.mark.parametrize("hb_code", [None, oracle.F32, oracle.BF16])
