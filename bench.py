@@ -65,6 +65,9 @@ def parse():
                    help="CPU oracle baseline: run whole oracle steps until this much time has passed")
     p.add_argument("--replays", type=int, default=20, help="back-to-back launches timing the roofline kernel")
     p.add_argument("--lr", type=float, default=0.01)
+    p.add_argument("--scale-batches", default="8192,32768",
+                   help="comma-separated mini-batch sizes at which the single-kernel stages are also timed "
+                        "(same graph and model; empty: skip)")
     p.add_argument("--scale-n", type=int, default=0, help="run the workload's model on an R-MAT graph of this many "
                    "vertices (the edge count scales with it unless --scale-m is given)")
     p.add_argument("--scale-m", type=int, default=0)
@@ -340,6 +343,58 @@ class StagedStep:
             return (rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
                     + 8 * (b["n_dst"] + 1) + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
         return None, None
+
+
+def roofline_of(staged, name: str, ms: float, host_link: bool) -> dict:
+    """Roofline entry of single-kernel stage `name` of `staged` at `ms` per
+    launch: the bound (HBM, matrix cores or host link) its algorithmic bytes
+    and flops put it under, and the achieved fraction of that peak."""
+    byts, flops = staged.stage_bytes(name)
+    t = ms / 1e3
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if name == "gather" and host_link:
+        ach = byts / t / 1e9
+        r = {"bound": "host_link", "achieved": ach, "peak": HOST_LINK_PEAK_GBS, "unit": "GB/s",
+             "frac": ach / HOST_LINK_PEAK_GBS}
+    elif flops and flops / max(byts, 1) > ridge:
+        ach = flops / t / 1e12
+        r = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+             "frac": ach / BF16_PEAK_TFLOPS}
+    else:
+        ach = byts / t / 1e9
+        r = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS}
+    r.update({"algorithmic_bytes": int(byts), "flops": int(flops or 0), "avg_ms": ms})
+    return r
+
+
+def scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches, reps, lr):
+    """The single-kernel stages of the same model and graph at larger
+    mini-batches: one staged step builds the blocks, then each stage's ABI
+    call is replayed back to back.  At the workload's own batch the kernels
+    are launch- and latency-bound; these sizes show where they stand once a
+    launch has enough work to fill the chip."""
+    out = []
+    host_link = loc == gnn.GNN_LOC_HOST_PINNED
+    for B in batches:
+        st = StagedStep(gnn, w, graph, B, act, loc)
+        tg = workloads.targets_for_step(perm, B, 0).contiguous()
+        for s in range(2):
+            st.run(tr, table, labels, tg, nrm, w.seed, 20_000 + s, lr)
+        torch.cuda.synchronize()
+        L = w.num_layers
+        names = ["gather", "agg_fwd_l1", "update_fwd_l1"]
+        names += [f"layer_fwd_l{l}" if st.fused.get(l) else f"agg_fwd_l{l}" for l in range(2, L + 1)]
+        names += [f"agg_bwd_l{l}" for l in range(2, L + 1)]
+        kern = {}
+        for k in names:
+            ms = st.replay(k, tr, table, reps, labels=labels)
+            kern[k] = {kk: (round(vv, 6) if isinstance(vv, float) else vv)
+                       for kk, vv in roofline_of(st, k, ms, host_link).items()}
+        out.append({"batch": B, "block_sizes": st.block_sizes(), "kernels": kern})
+        log(f"batch {B}: " + ", ".join(f"{k} {v['frac']:.2f} of {v['bound']}" for k, v in kern.items()))
+        del st
+        torch.cuda.empty_cache()
+    return out
 
 
 def tile_bytes(rowptr, col, f, elem, rows=16):
@@ -634,25 +689,8 @@ def main():
         result["stages_ms"] = {k: round(v, 5) for k, v in stage_ms.items()}
         single = [k for k in stage_ms
                   if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd"))]
-        ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-
         def roof_of(name, ms):
-            byts, flops = staged.stage_bytes(name)
-            t = ms / 1e3
-            if name == "gather" and loc == gnn.GNN_LOC_HOST_PINNED:
-                ach = byts / t / 1e9
-                r = {"bound": "host_link", "achieved": ach, "peak": HOST_LINK_PEAK_GBS, "unit": "GB/s",
-                     "frac": ach / HOST_LINK_PEAK_GBS}
-            elif flops and flops / max(byts, 1) > ridge:
-                ach = flops / t / 1e12
-                r = {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": ach / BF16_PEAK_TFLOPS}
-            else:
-                ach = byts / t / 1e9
-                r = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBS}
-            r.update({"algorithmic_bytes": int(byts), "flops": int(flops or 0), "avg_ms": ms})
-            return r
+            return roofline_of(staged, name, ms, loc == gnn.GNN_LOC_HOST_PINNED)
 
         # per-launch time of each single-kernel stage: back-to-back replays
         launch_ms = {k: staged.replay(k, tr, table, args.replays, labels=labels) for k in single}
@@ -675,6 +713,10 @@ def main():
         result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev)
         result["dedup_aggregation"] = dedup_report(gnn, staged, w, args.replays, dev)
         log(f"dedup aggregation: {json.dumps(result['dedup_aggregation'])}")
+        batches = [int(x) for x in args.scale_batches.split(",") if x.strip()]
+        if batches:
+            result["kernels_at_batch"] = scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches,
+                                                      args.replays, args.lr)
         pmr = result["perf_model"]["effective"]
         log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 8)']:.1f} us "
             f"(max of stages), serial {pmr['predicted_us']['serial sum']:.1f} us; measured {pmr['measured_step_us']:.1f} us")

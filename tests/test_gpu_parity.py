@@ -401,12 +401,13 @@ def test_aggregate_bwd_is_bitwise_reproducible():
 
 LAYER_CASES = [
     # f, n_out, n_dst, fanout, last, row-length bound given to the kernel
-    (100, 256, 5000, 10, False, 10),   # 32-row tiles, 4-feature chunks, the first layer of the headline model
-    (256, 47, 1024, 25, True, 25),     # 16-row tiles, 8-feature chunks, its last layer with the loss
+    (100, 256, 5000, 10, False, 10),   # 16-row tiles, 4-feature chunks, the first layer of the headline model
+    (256, 47, 1024, 25, True, 25),     # 4-row tiles, 8-feature chunks, its last layer with the loss
     (32, 64, 301, 5, False, 5),        # ragged last tile
     (64, 8, 77, 3, True, 3),
     (128, 128, 600, 15, False, 15),    # K = 256 (SAGE) on the 2 x 8 register tiles
     (256, 47, 700, 25, True, 1),       # bound far below the real rows: indices read in place
+    (256, 47, 9000, 10, True, 10),     # 32-row tiles with the loss epilogue, ragged last tile
 ]
 
 
