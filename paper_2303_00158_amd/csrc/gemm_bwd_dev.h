@@ -179,11 +179,19 @@ struct DwPlan {
 
 inline DwPlan plan_dw(int64_t K, int64_t n_out, int64_t cap_m, bool bf16) {
     DwPlan p;
-    p.tile = pick_tile(K, n_out);
+    // Wide layers (K and n_out both >= 512) take 128 x 128 tiles, which read
+    // half the operand bytes per flop of 64 x 64 ones, and split the rows
+    // over up to 2,048 workgroups: with 512, a 1536 x 1024 dW has 2 splits
+    // and each workgroup walks half of all rows alone (3-6x slower at
+    // 26k-131k rows).  Narrow layers keep the 512-workgroup plan, measured
+    // best for the training step's shapes.
+    const bool wide = K >= 512 && n_out >= 512;
+    p.tile = wide ? 128 : pick_tile(K, n_out);
     p.k_tiles = ceil_div(K, p.tile);
     const int64_t tiles = p.k_tiles * ceil_div(n_out, p.tile);
     const int64_t nch = std::max<int64_t>(ceil_div(cap_m, bk_of(bf16)), 1);
-    p.nsplit = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({ceil_div(512, tiles), 64, nch})));
+    const int64_t target = wide ? 2048 : 512;
+    p.nsplit = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({ceil_div(target, tiles), 64, nch})));
     p.map = SplitMap{tiles, p.nsplit};
     return p;
 }

@@ -614,7 +614,7 @@ def test_update_fwd_device_row_count():
     assert relerr(o[:201], want) <= 1e-5 and np.all(o[201:] == 7.0)
 
 
-@pytest.mark.parametrize("m,ke,n", SHAPES + [(26624 // 8, 100, 256)])
+@pytest.mark.parametrize("m,ke,n", SHAPES + [(26624 // 8, 100, 256), (700, 768, 600)])  # last: the wide-layer dW plan
 @pytest.mark.parametrize("sage", [True, False])
 @pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
 def test_update_bwd_parity(m, ke, n, sage, code):
