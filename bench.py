@@ -397,6 +397,41 @@ def scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches,
     return out
 
 
+def wide_gemm_report(gnn, dev, reps, m=26_624, ke=768, n=1024):
+    """The update GEMMs of a wide GraphSAGE layer (the 768 -> 1024 first
+    layer of the host-table model: K = 1,536, at its hop-2 row bound of
+    26,624), where they are bound by the matrix cores rather than HBM: the
+    forward (with the bf16 W^T shadow), dA + dW, and dW alone, in TFLOP/s
+    against the dense bf16 peak; torch.matmul on the same bf16 operands is
+    timed beside them for context.  Random bf16 operands."""
+    g = torch.Generator(device=dev).manual_seed(0)
+    K = 2 * ke
+    a_s = torch.randn(m, ke, device=dev, generator=g).to(torch.bfloat16)
+    a_n = torch.randn(m, ke, device=dev, generator=g).to(torch.bfloat16)
+    w = torch.randn(K, n, device=dev, generator=g) / K ** 0.5
+    bias = torch.zeros(n, device=dev)
+    wt = w.t().contiguous().to(torch.bfloat16)
+    out = torch.empty(m, n, dtype=torch.bfloat16, device=dev)
+    grad = torch.randn(m, n, device=dev, generator=g)
+    dw, db = torch.empty(K, n, device=dev), torch.empty(n, device=dev)
+    da = torch.empty(m, K, device=dev)
+    ws = gnn.update_bwd_workspace(K, n, m, gnn.GNN_BF16, dev)
+    a_cat, w_b = torch.cat([a_s, a_n], 1), w.to(torch.bfloat16)
+    flops = 2.0 * m * K * n
+
+    def rate(ms, times=1):
+        t = times * flops / (ms / 1e3) / 1e12
+        return {"ms": round(ms, 5), "tflops": round(t, 1), "frac": round(t / BF16_PEAK_TFLOPS, 4)}
+    r = {"shape": {"m": m, "k": K, "n": n}, "peak_tflops": BF16_PEAK_TFLOPS}
+    r["update_fwd"] = rate(time_calls(lambda: gnn.update_fwd(a_s, a_n, w, bias, out, True, gnn.GNN_BF16, wt=wt), reps))
+    r["update_bwd_dA_dW"] = rate(time_calls(lambda: gnn.update_bwd(a_s, a_n, w, grad, dw, db, da, gnn.GNN_BF16,
+                                                                   ws=ws), reps), 2)
+    r["update_bwd_dW"] = rate(time_calls(lambda: gnn.update_bwd(a_s, a_n, w, grad, dw, db, None, gnn.GNN_BF16,
+                                                                ws=ws), reps))
+    r["torch_matmul_fwd"] = rate(time_calls(lambda: torch.matmul(a_cat, w_b), reps))
+    return r
+
+
 def tile_bytes(rowptr, col, f, elem, rows=16):
     """Source bytes an aggregation fetches: per edge (every edge reads its
     source row) and per tile-distinct source (each distinct source of a tile
@@ -713,6 +748,9 @@ def main():
         result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev)
         result["dedup_aggregation"] = dedup_report(gnn, staged, w, args.replays, dev)
         log(f"dedup aggregation: {json.dumps(result['dedup_aggregation'])}")
+        if precision == gnn.GNN_BF16:
+            result["wide_gemm"] = wide_gemm_report(gnn, dev, args.replays)
+            log(f"wide-layer GEMMs: {json.dumps(result['wide_gemm'])}")
         batches = [int(x) for x in args.scale_batches.split(",") if x.strip()]
         if batches:
             result["kernels_at_batch"] = scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches,
