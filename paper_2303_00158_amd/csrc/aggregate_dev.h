@@ -178,6 +178,13 @@ __device__ __forceinline__ void agg_bwd_row(int64_t n_dst, const int64_t *__rest
         const int chunk = (S > 1) ? lane % C : g * 64 + lane;
         const bool active = (S > 1) ? (slot < S) : (chunk < C);
         const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        // the self term and the ReLU mask, issued before the neighbours so
+        // that their latency overlaps the sum (a source past the destinations
+        // reads destination row 0, unused; with no mask an in-bounds stand-in
+        // address, unused; THB is float whenever h_below is null)
+        const float4 self = load_chunk<VEC>(d_a, (j < n_dst ? j : 0) * ka, e0, f);
+        const bool mask = h_below != nullptr;
+        const float4 hb = load_chunk<VEC>(mask ? h_below : reinterpret_cast<const THB *>(d_a), mask ? j * f : 0, e0, f);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int64_t wb = beg; wb < end; wb += 64) {
             const int wn = static_cast<int>(min<int64_t>(64, end - wb));
@@ -204,10 +211,9 @@ __device__ __forceinline__ void agg_bwd_row(int64_t n_dst, const int64_t *__rest
         if (slot != 0 || !active) continue;
         if (j < n_dst) {
             const float ws = (KIND == GNN_AGG_GCN_SYM) ? wj * wj : 1.f;
-            fma4(acc, ws, load_chunk<VEC>(d_a, j * ka, e0, f));
+            fma4(acc, ws, self);
         }
-        if (h_below) {
-            const float4 hb = load_chunk<VEC>(h_below, j * f, e0, f);
+        if (mask) {
             if (!(hb.x > 0.f)) acc.x = 0.f;
             if (!(hb.y > 0.f)) acc.y = 0.f;
             if (!(hb.z > 0.f)) acc.z = 0.f;
