@@ -120,6 +120,9 @@ __device__ __forceinline__ void agg_fwd_row(const int64_t *__restrict__ rowptr, 
         const int chunk = (S > 1) ? lane % C : g * 64 + lane;
         const bool active = (S > 1) ? (slot < S) : (chunk < C);
         const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        // the GCN self term, issued before the neighbours
+        const float4 self = (KIND == GNN_AGG_GCN_SYM) ? load_chunk<VEC>(h, row * f, e0, f)
+                                                        : make_float4(0.f, 0.f, 0.f, 0.f);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int64_t wb = beg; wb < end; wb += 64) {
             const int wn = static_cast<int>(min<int64_t>(64, end - wb));
@@ -152,7 +155,7 @@ __device__ __forceinline__ void agg_fwd_row(const int64_t *__restrict__ rowptr, 
             }
         } else {
             const float ws = wi * wi;
-            fma4(acc, ws, load_chunk<VEC>(h, row * f, e0, f));
+            fma4(acc, ws, self);
         }
         store_chunk<VEC>(out, row * f, e0, f, acc);
     }
@@ -255,6 +258,8 @@ __device__ __forceinline__ void agg_fwd_row_table(const int64_t *__restrict__ ro
         const int chunk = (S > 1) ? lane % C : g * 64 + lane;
         const bool active = (S > 1) ? (slot < S) : (chunk < C);
         const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        const float4 self = (KIND == GNN_AGG_GCN_SYM) ? load_chunk<VEC>(x_self, row * f, e0, f)
+                                                        : make_float4(0.f, 0.f, 0.f, 0.f);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int64_t wb = beg; wb < end; wb += 64) {
             const int wn = static_cast<int>(min<int64_t>(64, end - wb));
@@ -287,7 +292,7 @@ __device__ __forceinline__ void agg_fwd_row_table(const int64_t *__restrict__ ro
             }
         } else {
             const float ws = wi * wi;
-            fma4(acc, ws, load_chunk<VEC>(x_self, row * f, e0, f));
+            fma4(acc, ws, self);
         }
         store_chunk<VEC>(out, row * f, e0, f, acc);
     }
