@@ -571,7 +571,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
                                    "described in the design notes, not built)", "n_gpus": args.gpus}))
         sys.exit(1)
     from paper_2303_00158_amd import gnn
