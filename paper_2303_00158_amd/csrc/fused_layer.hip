@@ -486,7 +486,11 @@ Shape fused_shape(int kind, int64_t f, int64_t n_out, int64_t cap_dst, int32_t m
     const int64_t ks = ceil_div(K, 32), ct = ceil_div(n_out, 16);
     const int64_t tpw = ceil_div(ct, kWaves);
     if (logits && n_out > 64) return sh;
-    if (tpw == 1 && ks <= 16) sh = Shape{0, 1, 16, true};
+    // the reduction runs KSM steps over a zero-padded A tile: half the steps
+    // when K fits them (GCN's K = f; small layers)
+    if (tpw == 1 && ks <= 8) sh = Shape{0, 1, 8, true};
+    else if (tpw == 1 && ks <= 16) sh = Shape{0, 1, 16, true};
+    else if (tpw == 2 && ks <= 4) sh = Shape{0, 2, 4, true};
     else if (tpw == 2 && ks <= 8) sh = Shape{0, 2, 8, true};
     else return sh;
     // rows per tile: enough workgroups to spread the gather over the CUs
@@ -521,22 +525,19 @@ gnn_status go(const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
     return launch_status("fused_layer");
 }
 
+template <int KIND, int BM, bool LOGITS>
+gnn_status go_steps(const Shape &sh, const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
+    if (sh.tpw == 1) return sh.ksm == 8 ? go<KIND, BM, 1, 8, LOGITS>(a, grid, lds, s)
+                                        : go<KIND, BM, 1, 16, LOGITS>(a, grid, lds, s);
+    return sh.ksm == 4 ? go<KIND, BM, 2, 4, LOGITS>(a, grid, lds, s) : go<KIND, BM, 2, 8, LOGITS>(a, grid, lds, s);
+}
+
 template <int KIND, bool LOGITS>
 gnn_status go_shape(const Shape &sh, const FusedArgs &a, unsigned grid, size_t lds, hipStream_t s) {
-    if (sh.bm == 4) {
-        if (sh.tpw == 1) return go<KIND, 4, 1, 16, LOGITS>(a, grid, lds, s);
-        return go<KIND, 4, 2, 8, LOGITS>(a, grid, lds, s);
-    }
-    if (sh.bm == 8) {
-        if (sh.tpw == 1) return go<KIND, 8, 1, 16, LOGITS>(a, grid, lds, s);
-        return go<KIND, 8, 2, 8, LOGITS>(a, grid, lds, s);
-    }
-    if (sh.bm == 32) {
-        if (sh.tpw == 1) return go<KIND, 32, 1, 16, LOGITS>(a, grid, lds, s);
-        return go<KIND, 32, 2, 8, LOGITS>(a, grid, lds, s);
-    }
-    if (sh.tpw == 1) return go<KIND, 16, 1, 16, LOGITS>(a, grid, lds, s);
-    return go<KIND, 16, 2, 8, LOGITS>(a, grid, lds, s);
+    if (sh.bm == 4) return go_steps<KIND, 4, LOGITS>(sh, a, grid, lds, s);
+    if (sh.bm == 8) return go_steps<KIND, 8, LOGITS>(sh, a, grid, lds, s);
+    if (sh.bm == 32) return go_steps<KIND, 32, LOGITS>(sh, a, grid, lds, s);
+    return go_steps<KIND, 16, LOGITS>(sh, a, grid, lds, s);
 }
 
 }  // namespace
