@@ -668,7 +668,7 @@ def main():
     if pipeline and tr.ws is not None:
         # the same steps without the overlap (one-call steps on one stream)
         e2 = torch.zeros(args.steps, dtype=torch.int64, device=dev)
-        run_steps(0, args.warmup, pipelined=False)  # warms up the one-call path (its helper stream)
+        run_steps(0, args.warmup, pipelined=False)  # warms up the one-call path
         ms2, _, _ = timed(args.warmup + args.steps, args.steps, e2, pipelined=False)
         sequential_ms = ms2 / args.steps
         log(f"without the overlap: {sequential_ms:.3f} ms/step")
@@ -756,7 +756,7 @@ def main():
             result["kernels_at_batch"] = scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches,
                                                       args.replays, args.lr)
         pmr = result["perf_model"]["effective"]
-        log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 8)']:.1f} us "
+        log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 6)']:.1f} us "
             f"(max of stages), serial {pmr['predicted_us']['serial sum']:.1f} us; measured {pmr['measured_step_us']:.1f} us")
 
     # ---- CPU oracle baseline ---------------------------------------------

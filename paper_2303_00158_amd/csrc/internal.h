@@ -115,24 +115,6 @@ __device__ __forceinline__ int64_t dev_count(const int64_t *dev, int64_t fallbac
 }
 
 // ---------------------------------------------------------------------------
-// building blocks implemented in scan.hip
-// ---------------------------------------------------------------------------
-// Exclusive scan of n int64 values: out[0] = 0, out[i+1] = in[0] + ... + in[i]
-// for i < n (so out has n+1 entries; out[n] is the total).  n is read from
-// n_dev when given (bounded by cap), else cap.  `total_to` (may be null)
-// receives the total as well.  tmp must hold scan_tmp_bytes(cap).
-size_t scan_tmp_bytes(int64_t cap);
-gnn_status exclusive_scan(const int64_t *in, int64_t *out, const int64_t *n_dev, int64_t cap, int64_t *total_to,
-                          void *tmp, hipStream_t s);
-
-// Stable LSD radix sort of (key, value) int32 pairs by key, keys in
-// [0, 2^key_bits).  n is read from n_dev (bounded by cap).  Results land in
-// keys_out / vals_out.  tmp must hold radix_tmp_bytes(cap).
-size_t radix_tmp_bytes(int64_t cap);
-gnn_status radix_sort_pairs(const int32_t *keys_in, const int32_t *vals_in, int32_t *keys_out, int32_t *vals_out,
-                            const int64_t *n_dev, int64_t cap, int key_bits, void *tmp, hipStream_t s);
-
-// ---------------------------------------------------------------------------
 // validation helpers (abi.hip)
 // ---------------------------------------------------------------------------
 gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const char *who);
@@ -183,7 +165,6 @@ gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self,
                                const int64_t *labels, float *g, float *row_loss, int64_t batch, hipStream_t s);
 // wt = bf16(w^T) for a K x n row-major w.
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
-gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 size_t softmax_ce_ws_bytes(int64_t b);
 gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const int64_t *labels,
                              const int64_t *targets, float *g_out, float *loss_out, void *ws, hipStream_t s);

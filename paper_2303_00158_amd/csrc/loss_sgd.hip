@@ -8,12 +8,6 @@ namespace gnn {
 
 namespace {
 
-__global__ void zero_words_kernel(uint32_t *p, int64_t n) {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
-         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        p[i] = 0u;
-}
-
 __global__ void sgd_kernel(float *__restrict__ w, const float *__restrict__ dw, int64_t n, float lr) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
          i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -31,16 +25,6 @@ gnn_status launch_softmax_ce(const float *logits, int64_t b, int64_t c, const in
         GNN_TRY(launch_job(loss::SoftmaxJob{logits, b, c, labels, targets, g_out, row_loss},
                            static_cast<unsigned>(ceil_div(b, loss::kThreads / 64)), s, "softmax_ce"));
     return launch_job(loss::LossReduceJob{row_loss, b, loss_out}, 1, s, "loss_reduce");
-}
-
-gnn_status launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
-    const int64_t words = static_cast<int64_t>(bytes / 4);
-    if (words == 0) return GNN_OK;
-    int64_t blocks = ceil_div(words, 256);
-    if (blocks > 65536) blocks = 65536;
-    zero_words_kernel<<<static_cast<unsigned>(blocks), 256, 0, s>>>(static_cast<uint32_t *>(p), words);
-    GNN_LAUNCHED("fill_zero");
-    return GNN_OK;
 }
 
 gnn_status launch_sgd(float *w, const float *dw, int64_t n, float lr, hipStream_t s) {

@@ -462,7 +462,11 @@ class Trainer:
         with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream(self.device)):
             self.loss.copy_(lo[steps - 1:steps])
         self._keep = (targets, lo)  # alive until the next call; the stream orders their reuse
-        self._viewing = (self.prep_ws[(steps - 1) % nslot], self.comp_ws)
+        # the slot of the last step, as gnn_train_steps assigns them: groups of
+        # G = min(4, max(1, nslot // 2)) steps alternate between two halves
+        G = min(4, max(1, nslot // 2))
+        last = steps - 1
+        self._viewing = (self.prep_ws[((last // G) % 2) * G + last % G], self.comp_ws)
 
     def _loss_steps(self, steps: int) -> torch.Tensor:
         if getattr(self, "_loss_buf", None) is None or self._loss_buf.numel() < steps:

@@ -5,17 +5,17 @@ from the sizes of its sampled blocks and from bandwidth and compute rates,
 so that the prediction can be set beside measured stage times.
 
 The model (Section V):
-  throughput   = sum over trainers and layers of |E^l| / T_execution   (eq. 7)
-  T_execution  = max(T_samp, T_load, T_trans, T_prop)                  (eq. 8)
+  throughput   = sum over trainers and layers of |E^l| / T_execution   (eq. 5)
+  T_execution  = max(T_samp, T_load, T_trans, T_prop)                  (eq. 6)
   T_samp       measured, not modelled (the paper measures it too)
-  T_load       = |V^0| f^0 S_feat / BW_mem                             (eq. 9)
-  T_trans      = |V^0| f^0 S_feat / BW_link                            (eq. 10)
-  T_prop       = max over trainers of T_trainer + T_sync               (eq. 11)
+  T_load       = |V^0| f^0 S_feat / BW_mem                             (eq. 7)
+  T_trans      = |V^0| f^0 S_feat / BW_link                            (eq. 8)
+  T_prop       = max over trainers of T_trainer + T_sync               (eq. 9)
   T_trainer    = sum_{l=1..L} (+)(t_agg^l, t_upd^l)                    (forward)
-                 + t_upd^1 + sum_{l=2..L} (+)(t_agg^l, t_upd^l)         (backward)  (eq. 12)
-  t_agg^l      = edges x feature width x S_feat / BW_mem               (eq. 13)
-  t_upd^l      = MACs of the layer's update / (N x freq)               (eq. 14)
-  T_sync       = 2 x model bytes / BW_link                             (eq. 15)
+                 + t_upd^1 + sum_{l=2..L} (+)(t_agg^l, t_upd^l)         (backward)  (eq. 10)
+  t_agg^l      = edges x feature width x S_feat / BW_mem               (eq. 11)
+  t_upd^l      = MACs of the layer's update / (N x freq)               (eq. 12)
+  T_sync       = 2 x model bytes / BW_link                             (eq. 13)
 (+) is max when aggregation and update are pipelined (the fused kernel
 here, like the paper's FPGA datapath) and sum when they are not.
 
@@ -26,7 +26,7 @@ features of width f^{l-1} (its input), and its update multiplies
 mean concatenated) and f^{l-1} for GCN.  With one GPU there is one
 trainer and no T_sync.  T_trans applies only when the feature table
 lives in host memory.  Every stage runs on the same device here, so
-besides the paper's pipeline bound (the max of eq. 8) the serial bound
+besides the paper's pipeline bound (the max of eq. 6) the serial bound
 T_samp + T_load + T_trans + T_prop is reported: a pipelined step on one
 GPU lies between the two.
 """
@@ -69,10 +69,10 @@ class Prediction:
     t_forward: float
     t_backward: float
     t_prop: float
-    t_pipeline: float        # eq. 8: max of the stages
+    t_pipeline: float        # eq. 6: max of the stages
     t_serial: float          # the stages one after another
     edges: int
-    throughput_pipeline: float   # eq. 7 with t_pipeline
+    throughput_pipeline: float   # eq. 5 with t_pipeline
     throughput_serial: float
     stages: Dict[str, float] = field(default_factory=dict)
 
@@ -97,8 +97,8 @@ def predict(layers: Sequence[Layer], n_input: int, kind: str, hw: Hardware, t_sa
 
     layers: layers 1..L; n_input: |V^0| (rows of X'); kind: "sage" or "gcn";
     t_samp: measured sampling time; s_table: bytes per feature of the table
-    (S_feat of eqs. 9-10); s_act: bytes per activation the aggregation reads
-    (S_feat of eq. 13); fused: (+) is max, else sum."""
+    (S_feat of eqs. 7-8); s_act: bytes per activation the aggregation reads
+    (S_feat of eq. 11); fused: (+) is max, else sum."""
     if kind not in ("sage", "gcn"):
         raise ValueError(kind)
     f0 = layers[0].f_in
@@ -134,7 +134,7 @@ def report(p: Prediction, measured_step_s: float, measured: Optional[Dict[str, f
         "predicted_us": {"T_samp (measured)": us(p.t_samp), "T_load": us(p.t_load), "T_trans": us(p.t_trans),
                          "T_prop": us(p.t_prop), "t_forward": us(p.t_forward), "t_backward": us(p.t_backward),
                          "t_agg": [us(x) for x in p.t_agg], "t_upd": [us(x) for x in p.t_upd],
-                         "T_execution (max, eq. 8)": us(p.t_pipeline), "serial sum": us(p.t_serial)},
+                         "T_execution (max, eq. 6)": us(p.t_pipeline), "serial sum": us(p.t_serial)},
         "measured_step_us": us(measured_step_s),
         "ratio_measured_to_max": measured_step_s / p.t_pipeline if p.t_pipeline > 0 else None,
         "ratio_measured_to_serial": measured_step_s / p.t_serial if p.t_serial > 0 else None,

@@ -870,6 +870,7 @@ def _state(tr):
                                                           (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 2, 5),
                                                           (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 7),
                                                           (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 1),
+                                                          (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 6),
                                                           (gnn.GNN_AGG_GCN_SYM, gnn.GNN_BF16, 4, 2),
                                                           (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 8, 11),
                                                           (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 8, 3)])
