@@ -282,6 +282,28 @@ gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
                           gnn_dtype gemm_dt, float *dw, float *db, float *d_a, void *ws, size_t ws_bytes,
                           gnn_stream s);
 
+/* gnn_update_bwd for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, kernels and results, bit for bit, with the dW
+ * partials kept in a static device array of the library instead of a
+ * caller workspace.  Arguments as gnn_update_bwd without ws / ws_bytes.
+ *   - The array holds 32 MiB (GNN_UPDATE_BWD_NOALLOC_MAX_SCRATCH); a shape
+ *     whose gnn_update_bwd_workspace_size exceeds it returns GNN_ESIZE and
+ *     enqueues nothing.  Each GPU the call runs on keeps its own copy of the
+ *     array until the process ends.
+ *   - The call never allocates or frees memory.  Its first call on a device
+ *     looks up that device's copy (hipGetSymbolAddress, with the device
+ *     current); a failed lookup returns GNN_EHIP.
+ *   - Every call on one GPU shares that GPU's array: calls that overlap on
+ *     one GPU (concurrent streams, or host threads) race and give undefined
+ *     results; order them on one stream.  Nothing in the array needs
+ *     clearing between calls. */
+#define GNN_UPDATE_BWD_NOALLOC_MAX_SCRATCH (32u << 20)
+gnn_status gnn_update_bwd_noalloc(const void *a_self, const void *a_nbr, gnn_dtype adt, int64_t k_each,
+                                  const int64_t *m_dev, int64_t cap_m, const float *w, const float *g,
+                                  int64_t n_out, gnn_dtype gemm_dt, float *dw, float *db, float *d_a,
+                                  gnn_stream s);
+
 /* Loss against the ground truth (Section II-B): mean softmax cross-entropy
  * over the b target rows of logits [device] (fp32 b x c).  The label of row
  * i is labels[targets[i]] (labels/targets [device] int64; targets NULL means

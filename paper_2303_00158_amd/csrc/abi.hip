@@ -124,6 +124,23 @@ gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const 
     return GNN_OK;
 }
 
+// Host validation shared by the update-backward entry points; *ws_need is
+// the scratch the call needs.
+gnn_status check_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
+                            int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt,
+                            const float *dw, const float *db, const float *d_a, size_t *ws_need, const char *who) {
+    GNN_CHECK(act_dtype(adt) && act_dtype(gemm_dt), GNN_EUNSUPPORTED, "%s: dtypes must be GNN_F32 or GNN_BF16", who);
+    GNN_CHECK(dim_ok(k_each) && dim_ok(n_out), GNN_EINVAL, "%s: k_each / n_out out of [1, %d]", who, GNN_MAX_DIM);
+    GNN_CHECK(cap_m >= 0 && cap_m < (1ll << 40), GNN_EINVAL, "%s: bad cap_m", who);
+    GNN_CHECK((a_self || cap_m == 0) && w && (g || cap_m == 0) && dw, GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK(aligned(a_self, dtype_size(adt)) && aligned(a_nbr, dtype_size(adt)) && aligned(w, 4) && aligned(g, 4) &&
+                  aligned(dw, 4) && aligned(db, 4) && aligned(d_a, 4) && aligned(m_dev, 8),
+              GNN_EINVAL, "%s: misaligned data", who);
+    const int64_t K = a_nbr ? 2 * k_each : k_each;
+    *ws_need = update_bwd_ws_bytes(K, n_out, cap_m, gemm_dt);
+    return GNN_OK;
+}
+
 }  // namespace gnn
 
 using namespace gnn;
@@ -345,15 +362,8 @@ gnn_status gnn_update_bwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
                           gnn_stream s) {
     clear_error();
     const char *who = "gnn_update_bwd";
-    GNN_CHECK(act_dtype(adt) && act_dtype(gemm_dt), GNN_EUNSUPPORTED, "%s: dtypes must be GNN_F32 or GNN_BF16", who);
-    GNN_CHECK(dim_ok(k_each) && dim_ok(n_out), GNN_EINVAL, "%s: k_each / n_out out of [1, %d]", who, GNN_MAX_DIM);
-    GNN_CHECK(cap_m >= 0 && cap_m < (1ll << 40), GNN_EINVAL, "%s: bad cap_m", who);
-    GNN_CHECK((a_self || cap_m == 0) && w && (g || cap_m == 0) && dw, GNN_EINVAL, "%s: NULL pointer", who);
-    GNN_CHECK(aligned(a_self, dtype_size(adt)) && aligned(a_nbr, dtype_size(adt)) && aligned(w, 4) && aligned(g, 4) &&
-                  aligned(dw, 4) && aligned(db, 4) && aligned(d_a, 4) && aligned(m_dev, 8),
-              GNN_EINVAL, "%s: misaligned data", who);
-    const int64_t K = a_nbr ? 2 * k_each : k_each;
-    const size_t need = update_bwd_ws_bytes(K, n_out, cap_m, gemm_dt);
+    size_t need = 0;
+    GNN_TRY(check_update_bwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, g, n_out, gemm_dt, dw, db, d_a, &need, who));
     GNN_CHECK(ws && aligned(ws, 256), GNN_EINVAL, "%s: ws must be non-NULL and 256-byte aligned", who);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     return launch_update_bwd(a_self, a_nbr, adt, k_each, m_dev, cap_m, w, g, n_out, gemm_dt, dw, db, d_a, ws,

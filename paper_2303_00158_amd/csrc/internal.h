@@ -118,6 +118,9 @@ __device__ __forceinline__ int64_t dev_count(const int64_t *dev, int64_t fallbac
 // validation helpers (abi.hip)
 // ---------------------------------------------------------------------------
 gnn_status check_block(const gnn_block *b, bool need_csc, bool need_norm, const char *who);
+gnn_status check_update_bwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
+                            int64_t cap_m, const float *w, const float *g, int64_t n_out, int gemm_dt,
+                            const float *dw, const float *db, const float *d_a, size_t *ws_need, const char *who);
 
 // Internal launchers reused by the training step (no host validation).
 gnn_status launch_gather(const void *table, int tdt, int64_t dim, int64_t row_stride, const int64_t *ids,

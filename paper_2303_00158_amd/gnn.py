@@ -84,6 +84,7 @@ _SIGNATURES = {
     "gnn_update_bwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_bwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _sz,
                               _vp]),
+    "gnn_update_bwd_noalloc": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
     "gnn_softmax_ce_workspace_size": (_i32, [_i64, _P(_sz)]),
     "gnn_softmax_ce": (_i32, [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gnn_sgd": (_i32, [_vp, _vp, _i64, _f32, _vp]),
@@ -320,6 +321,17 @@ def update_bwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Ten
     _check(lib().gnn_update_bwd(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1], _ptr(m_dev),
                                 cap, _ptr(w), _ptr(g), w.shape[1], gemm_dtype, _ptr(dw), _ptr(db), _ptr(d_a),
                                 _ptr(ws), ws.numel(), _stream(stream)))
+    return dw, db, d_a
+
+
+def update_bwd_noalloc(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, g: torch.Tensor,
+                       dw: torch.Tensor, db: Optional[torch.Tensor], d_a: Optional[torch.Tensor], gemm_dtype: int,
+                       m_dev: Optional[torch.Tensor] = None, cap_m: Optional[int] = None, stream=None):
+    """gnn_update_bwd_noalloc: update_bwd with the library's static scratch."""
+    cap = a_self.shape[0] if cap_m is None else cap_m
+    _check(lib().gnn_update_bwd_noalloc(_ptr(a_self), _ptr(a_nbr), dtype_code(a_self.dtype), a_self.shape[1],
+                                        _ptr(m_dev), cap, _ptr(w), _ptr(g), w.shape[1], gemm_dtype, _ptr(dw),
+                                        _ptr(db), _ptr(d_a), _stream(stream)))
     return dw, db, d_a
 
 
