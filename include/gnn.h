@@ -32,8 +32,11 @@
  *    the host before anything is enqueued; a failed check returns an error
  *    code and enqueues nothing.  HIP launch failures return GNN_EHIP.  The
  *    text of the last error on the calling thread is in gnn_last_error().
- *    Device-content errors (a vertex id >= n, a label >= C, duplicate
- *    targets) are not detected and give undefined results.
+ *    Checks that only the device can make (the sampler's bounded waits and
+ *    its range checks) set flags in device memory instead, which
+ *    gnn_check_device_errors reads.  Device-content errors (a vertex id >= n,
+ *    a label >= C, duplicate targets) are not detected and give undefined
+ *    results.
  *  - Calls on different streams may run concurrently when their buffers and
  *    workspaces do not overlap.
  */
@@ -53,6 +56,13 @@ typedef int32_t gnn_status;
 #define GNN_ESIZE (-2)         /* a capacity or workspace is too small */
 #define GNN_EHIP (-3)          /* a HIP runtime call or kernel launch failed */
 #define GNN_EUNSUPPORTED (-4)  /* valid but unsupported combination (dtype, location) */
+#define GNN_EDEVICE (-5)       /* a device-side check failed (gnn_check_device_errors) */
+
+/* Device error flags, as kept in a block's counts[3] and in a training
+ * step's error word (gnn_step_layout.error).  A result computed while a flag
+ * is set is undefined. */
+#define GNN_DEVERR_WAIT 1      /* a single-pass scan's bounded wait for an earlier workgroup gave up */
+#define GNN_DEVERR_RANGE 2     /* an index derived from device data fell outside its buffer */
 
 typedef enum { GNN_F32 = 0, GNN_BF16 = 1, GNN_F16 = 2 } gnn_dtype;
 typedef enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1 } gnn_agg;
@@ -98,7 +108,13 @@ gnn_status gnn_gcn_norm(const gnn_graph *g, float *nrm_out, gnn_stream s);
  * for each source j, the rows i that sampled it, ascending.
  *
  * counts [device] int64[4] is written by gnn_build_block:
- *   counts[0] = n_dst, counts[1] = n_src, counts[2] = nnz (sampled edges).
+ *   counts[0] = n_dst, counts[1] = n_src, counts[2] = nnz (sampled edges),
+ *   counts[3] = device error flags of the build (GNN_DEVERR_*; 0 when the
+ *   block is valid): GNN_DEVERR_WAIT when a workgroup of the row-pointer,
+ *   new-source or transpose scan gave up waiting for an earlier one (every
+ *   wait is bounded, so the build always finishes), GNN_DEVERR_RANGE when a
+ *   local index or transpose position fell outside the block's capacities
+ *   (the access is skipped).  Read it with gnn_check_device_errors.
  * ------------------------------------------------------------------------ */
 typedef struct gnn_block {
     int64_t cap_dst;   /* [host] capacity of destination rows */
@@ -387,6 +403,9 @@ typedef struct gnn_step_layout {
     size_t bwd_ws, bwd_ws_bytes;        /* update-backward workspace */
     size_t loss_ws, loss_ws_bytes;      /* loss workspace */
     size_t edges;                       /* int64 sampled edges of the step */
+    size_t error;                       /* int64 device error word (GNN_DEVERR_*): the OR of counts[3] of every
+                                           block of every step of the last gnn_train_step, gnn_step_compute or
+                                           gnn_train_steps call on this compute workspace */
     size_t loss;                        /* fp32 loss of the step */
 } gnn_step_layout;
 
@@ -471,6 +490,31 @@ gnn_status gnn_train_steps(const gnn_model *m, const gnn_graph *g, const float *
                            const int64_t *targets, int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps,
                            float lr, float *loss_dev, int64_t *edges_dev, void *const *prep_ws, int32_t n_prep,
                            size_t prep_bytes, void *comp_ws, size_t comp_bytes, gnn_stream s, gnn_stream prep_s);
+
+/* ------------------------------------------------------------------------
+ * Device-side errors.
+ *
+ * gnn_decode_device_errors: host only.  Returns GNN_OK for word == 0, else
+ *   GNN_EDEVICE with gnn_last_error() naming every flag set (unknown bits
+ *   are reported as such).
+ * gnn_check_device_errors: waits for the work enqueued on s, reads the int64
+ *   word [device] (a block's &counts[3], or the step's error word at
+ *   layout.error in the compute workspace, which for gnn_train_step is at
+ *   byte prep_bytes + layout.error of its workspace), and decodes it as
+ *   above.  This call synchronises the host with the stream.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_decode_device_errors(int64_t word);
+gnn_status gnn_check_device_errors(const int64_t *word, gnn_stream s);
+
+/* Test hook for the device error path, not for production use: from the
+ * next sampler launch on (gnn_build_block and the training steps), row tile
+ * silent_row_tile (256 destination rows each) of the row-pointer scan
+ * publishes nothing, so the tile after it waits, and every row-scan wait
+ * gives up after spin_limit polls and flags GNN_DEVERR_WAIT.  The block's
+ * contents are then undefined.  gnn_debug_sampler_fault(-1, 0) restores
+ * normal operation (the default poll limit).  Process-wide; not thread-safe
+ * against concurrent sampler calls. */
+gnn_status gnn_debug_sampler_fault(int64_t silent_row_tile, uint32_t spin_limit);
 
 #ifdef __cplusplus
 }

@@ -39,7 +39,8 @@ gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
                             int tdt, bool host_table, int64_t row_stride, const int64_t *targets, int64_t batch,
                             uint64_t seed, uint64_t step, void *prep_ws, hipStream_t s);
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
-                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s);
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s,
+                            bool first = true);
 gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table, int tdt,
                            bool host_table, int64_t row_stride, const int64_t *labels, const int64_t *targets,
                            int64_t batch, uint64_t seed, uint64_t first_step, int64_t steps, float lr,
@@ -565,6 +566,47 @@ gnn_status gnn_train_steps(const gnn_model *m, const gnn_graph *g, const float *
     return run_train_steps(m, g, gcn_norm, t, tdt, loc == GNN_LOC_HOST_PINNED, row_stride, labels, targets, batch,
                            seed, first_step, steps, lr, loss_dev, edges_dev, prep_ws, n_prep, comp_ws, stream_of(s),
                            stream_of(prep_s));
+}
+
+gnn_status gnn_decode_device_errors(int64_t word) {
+    clear_error();
+    if (word == 0) return GNN_OK;
+    char text[256];
+    size_t n = 0;
+    auto add = [&](const char *what) {
+        const int w = snprintf(text + n, sizeof(text) - n, "%s%s", n ? "; " : "", what);
+        if (w > 0) n = std::min(sizeof(text) - 1, n + static_cast<size_t>(w));
+    };
+    if (word & GNN_DEVERR_WAIT) add("a single-pass scan gave up waiting for an earlier workgroup (GNN_DEVERR_WAIT)");
+    if (word & GNN_DEVERR_RANGE) add("an index derived from device data was out of range (GNN_DEVERR_RANGE)");
+    const int64_t unknown = word & ~static_cast<int64_t>(GNN_DEVERR_WAIT | GNN_DEVERR_RANGE);
+    if (unknown) {
+        char u[48];
+        snprintf(u, sizeof(u), "unknown flags 0x%llx", static_cast<unsigned long long>(unknown));
+        add(u);
+    }
+    return fail(GNN_EDEVICE, "device error flags 0x%llx: %s", static_cast<unsigned long long>(word), text);
+}
+
+gnn_status gnn_check_device_errors(const int64_t *word, gnn_stream s) {
+    clear_error();
+    GNN_CHECK(word && aligned(word, 8), GNN_EINVAL, "gnn_check_device_errors: word must be non-NULL and 8-byte aligned");
+    int64_t v = 0;
+    GNN_HIP(hipMemcpyAsync(&v, word, sizeof(v), hipMemcpyDeviceToHost, stream_of(s)));
+    GNN_HIP(hipStreamSynchronize(stream_of(s)));
+    return gnn_decode_device_errors(v);
+}
+
+gnn_status gnn_debug_sampler_fault(int64_t silent_row_tile, uint32_t spin_limit) {
+    clear_error();
+    GNN_CHECK(silent_row_tile >= -1, GNN_EINVAL, "gnn_debug_sampler_fault: silent_row_tile must be >= -1");
+    if (silent_row_tile == -1 && spin_limit == 0) {
+        set_sampler_fault(-1, samp::kSpinLimit);
+        return GNN_OK;
+    }
+    GNN_CHECK(spin_limit >= 1, GNN_EINVAL, "gnn_debug_sampler_fault: spin_limit must be >= 1");
+    set_sampler_fault(silent_row_tile, spin_limit);
+    return GNN_OK;
 }
 
 }  // extern "C"

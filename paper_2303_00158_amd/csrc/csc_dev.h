@@ -16,8 +16,8 @@
 //          sorting network, longer ones by a wavefront that counts rows in
 //          LDS and writes them out in order
 // Every index a phase derives
-// from device data is range-checked; a violation sets counts[3] and skips
-// the access.
+// from device data is range-checked; a violation flags samp::kErrRange in
+// counts[3] and skips the access.
 #pragma once
 
 #include "internal.h"
@@ -90,12 +90,12 @@ struct PlaceJob {
         for (int64_t e = blk * kThreads + threadIdx.x; e < nnz; e += nblk * kThreads) {
             const int32_t c = a.bcol[e];
             if (c < 0 || c >= n_src) {
-                a.counts[3] = 1;
+                samp::flag_error(&a.counts[3], samp::kErrRange);
                 continue;
             }
             const int64_t p = a.cscptr[c] + atomicAdd(&a.cnt[c], 1);
             if (p < 0 || p >= nnz || p >= a.cscptr[c + 1]) {
-                a.counts[3] = 1;
+                samp::flag_error(&a.counts[3], samp::kErrRange);
                 continue;
             }
             a.cscrow[p] = a.erow[e];
@@ -155,7 +155,7 @@ __device__ __forceinline__ void sort_long(uint32_t *lds, const int32_t *src, int
         for (int64_t i = lane; i < len; i += 64) {
             const int64_t r = src[i];
             if (r < 0 || r >= n_dst) {
-                *err = 1;
+                samp::flag_error(err, samp::kErrRange);
                 continue;
             }
             if (r >= w0 && r < w0 + kWindow) {
@@ -211,7 +211,7 @@ struct SortJob {
                 p0 = a.cscptr[c];
                 const int64_t p1 = a.cscptr[c + 1];
                 if (p0 < 0 || p1 < p0 || p1 > nnz) {
-                    a.counts[3] = 1;
+                    samp::flag_error(&a.counts[3], samp::kErrRange);
                     p0 = 0;
                 } else {
                     len = p1 - p0;

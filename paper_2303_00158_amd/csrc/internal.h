@@ -183,6 +183,10 @@ struct Args;
 gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const int64_t *dst_ids,
                               const int64_t *n_dst_dev, int32_t fanout, uint64_t seed, uint64_t step, int32_t hop,
                               const gnn_block *out, void *ws, const csc::Args *csc, hipStream_t s);
+// Error-path test hook: from the next sampler launch on, the row scan's
+// tile `silent_row_tile` publishes nothing (-1: none) and its waits give up
+// after `spin_limit` polls.
+void set_sampler_fault(int64_t silent_row_tile, uint32_t spin_limit);
 // Bound on a block's sources (gnn_block_bounds).
 int64_t src_bound(int64_t graph_n, int64_t cap_dst, int32_t fanout);
 // The transpose scratch inside a sampler workspace (for standalone calls).

@@ -78,7 +78,9 @@ struct LossReduceJob {
 };
 
 // End of a training step (workgroup 0 only): the loss from the row losses,
-// and the step's sampled edges (sum of the blocks' nnz counters).
+// the step's sampled edges (sum of the blocks' nnz counters) and its device
+// error flags (OR of the blocks' counts[3]), written to `error` by the first
+// step of a call and ORed into it by the later ones.
 struct TailJob {
     const int64_t *counts[GNN_MAX_LAYERS];
     int num_blocks;
@@ -86,12 +88,18 @@ struct TailJob {
     int64_t b;
     float *loss, *loss_out;
     int64_t *edges, *edges_out;
+    int64_t *error;
+    int accumulate;
     __device__ void run(int64_t blk, int64_t) const {
         if (blk != 0) return;
         const float v = reduce_row_losses(row_loss, b);
         if (threadIdx.x == 0) {
-            int64_t e = 0;
-            for (int h = 0; h < num_blocks; ++h) e += counts[h][2];
+            int64_t e = 0, err = 0;
+            for (int h = 0; h < num_blocks; ++h) {
+                e += counts[h][2];
+                err |= counts[h][3];
+            }
+            *error = accumulate ? (*error | err) : err;
             *edges = e;
             if (edges_out) *edges_out = e;
             *loss = v;

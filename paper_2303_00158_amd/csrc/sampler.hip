@@ -19,7 +19,7 @@
 // they start and add the prefix of earlier tickets (decoupled look-back,
 // one wavefront reading 64 predecessors at a time), so a workgroup only
 // waits on workgroups that are already running.  Every wait is bounded; a
-// wait that runs out flags counts[3].
+// wait that runs out flags counts[3] (samp::kErrWait).
 //
 // Device workspace (sampler_ws_bytes):
 //   map   int32[graph_n]   vertex -> local source index (valid only for the
@@ -28,6 +28,8 @@
 //   dbits uint32[W]        one bit per vertex: "destination"
 //   ... per-call scratch
 // Both bitmaps are all zero between calls; each call clears the words it set.
+#include <atomic>
+
 #include "csc_dev.h"
 #include "jobs.h"
 #include "sampler_dev.h"
@@ -35,6 +37,11 @@
 namespace gnn {
 
 namespace {
+
+// Error-path test hook (set_sampler_fault): the row scan's poll limit and
+// the row tile that never publishes (-1: none).
+std::atomic<uint32_t> g_row_spin_limit{samp::kSpinLimit};
+std::atomic<int64_t> g_silent_row_tile{-1};
 
 using namespace samp;
 
@@ -232,6 +239,8 @@ samp::HopPlan plan_hop(const gnn_graph *g, const float *gcn_norm, const int64_t 
     a.csc_status = csc ? csc->status : nullptr;
     a.csc_ticket = csc ? csc->ticket : nullptr;
     a.csc_nb = csc ? csc->nb_scan : 0;
+    a.spin_limit = g_row_spin_limit.load(std::memory_order_relaxed);
+    a.silent_row_tile = g_silent_row_tile.load(std::memory_order_relaxed);
     a.status = reinterpret_cast<uint64_t *>(hbase + hw.status);
     a.ticket = reinterpret_cast<int *>(hbase + hw.ticket);
     a.nb_rows = ceil_div(out->cap_dst > 0 ? out->cap_dst : 1, kThreads);
@@ -275,6 +284,11 @@ gnn_status launch_build_block(const gnn_graph *g, const float *gcn_norm, const i
     hop_relabel_kernel<<<p.relabel_grid, kThreads, 0, s>>>(p.a);
     GNN_LAUNCHED("hop_relabel");
     return GNN_OK;
+}
+
+void set_sampler_fault(int64_t silent_row_tile, uint32_t spin_limit) {
+    g_silent_row_tile.store(silent_row_tile, std::memory_order_relaxed);
+    g_row_spin_limit.store(spin_limit, std::memory_order_relaxed);
 }
 
 }  // namespace gnn

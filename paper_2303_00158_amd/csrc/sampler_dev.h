@@ -44,17 +44,29 @@ __device__ __forceinline__ int64_t wave_sum64(int64_t v) {
     return v;
 }
 
+// Device error flags of a block (its counts[3]; gnn.h names them): set
+// with an atomic OR, so that concurrent checks keep every flag.
+constexpr int64_t kErrWait = 1;   // a bounded wait for an earlier workgroup gave up
+constexpr int64_t kErrRange = 2;  // an index derived from device data was out of range
+__device__ __forceinline__ void flag_error(int64_t *err, int64_t flag) {
+    atomicOr(reinterpret_cast<unsigned long long *>(err), static_cast<unsigned long long>(flag));
+}
+
 // Called by all 64 lanes of one wavefront: publish this workgroup's
 // aggregate, add up the aggregates / prefixes of earlier tickets 64 at a
 // time (lane j reads ticket blk-1-j-64w), publish the inclusive prefix, and
-// return the exclusive prefix.
-__device__ inline int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, int64_t *err) {
+// return the exclusive prefix.  Waits for an earlier ticket give up after
+// spin_limit polls and flag kErrWait.  `silent` (normally -1) names a ticket
+// that publishes nothing: a host-driven test of that path.
+__device__ inline int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, int64_t *err,
+                                    uint32_t spin_limit = kSpinLimit, int64_t silent = -1) {
     const int lane = threadIdx.x & 63;
+    const bool publish = blk != silent;
     if (blk == 0) {
-        if (lane == 0) store_status(&status[0], kFlagPrefix | static_cast<uint64_t>(agg));
+        if (lane == 0 && publish) store_status(&status[0], kFlagPrefix | static_cast<uint64_t>(agg));
         return 0;
     }
-    if (lane == 0) store_status(&status[blk], kFlagAgg | static_cast<uint64_t>(agg));
+    if (lane == 0 && publish) store_status(&status[blk], kFlagAgg | static_cast<uint64_t>(agg));
     int64_t excl = 0;
     int64_t hi = blk - 1;
     uint32_t spins = 0;
@@ -67,8 +79,8 @@ __device__ inline int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, 
         const int first = pre ? static_cast<int>(__builtin_ctzll(pre)) : 63;
         const uint64_t need = (first == 63) ? ~0ull : ((1ull << (first + 1)) - 1);
         if (__ballot(flag == 0) & need) {
-            if (++spins > kSpinLimit) {
-                if (lane == 0) *err = 1;  // an earlier workgroup never published: flag it and stop
+            if (++spins > spin_limit) {
+                if (lane == 0) flag_error(err, kErrWait);  // an earlier workgroup never published
                 break;
             }
             continue;
@@ -77,7 +89,7 @@ __device__ inline int64_t look_back(uint64_t *status, int64_t blk, int64_t agg, 
         if (pre) break;
         hi -= 64;
     }
-    if (lane == 0) store_status(&status[blk], kFlagPrefix | static_cast<uint64_t>(excl + agg));
+    if (lane == 0 && publish) store_status(&status[blk], kFlagPrefix | static_cast<uint64_t>(excl + agg));
     return excl;
 }
 
@@ -132,6 +144,10 @@ struct HopArgs {
     uint64_t *csc_status;
     int *csc_ticket;
     int64_t csc_nb;
+    // the row scan's bounded wait (kSpinLimit polls) and its silent ticket
+    // (-1: none), changed only by the host's error-path test hook
+    uint32_t spin_limit;
+    int64_t silent_row_tile;
 };
 
 __device__ __forceinline__ void set_bit(uint32_t *bm, int64_t v) {
@@ -248,7 +264,7 @@ __device__ __forceinline__ void emit_rows(const HopArgs &a, int64_t blk, int64_t
     const int64_t excl_in_block = block_excl_scan(c, &total);
     __shared__ int64_t base;
     if (threadIdx.x < 64) {
-        const int64_t b = look_back(a.status, blk, total, &a.counts[3]);
+        const int64_t b = look_back(a.status, blk, total, &a.counts[3], a.spin_limit, a.silent_row_tile);
         if (threadIdx.x == 0) base = b;
     }
     __syncthreads();
@@ -331,7 +347,7 @@ __device__ __forceinline__ void hop_relabel_body(const HopArgs &a, int64_t blk, 
             if (c >= 0 && c < a.csc_cap_src)
                 atomicAdd(&a.csc_cnt[c], 1);
             else
-                a.counts[3] = 1;
+                flag_error(&a.counts[3], kErrRange);
         }
     }
 }

@@ -96,6 +96,7 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
     o->loss_ws_bytes = softmax_ce_ws_bytes(batch);
     o->loss_ws = d.take(o->loss_ws_bytes);
     o->edges = d.take(8);
+    o->error = d.take(8);
     o->loss = d.take(4);
     o->compute_bytes = round_up(d.off, 256);
     o->total_bytes = o->prep_bytes + o->compute_bytes;
@@ -371,8 +372,11 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
 // Forward, loss, backward and SGD from a prepared workspace (blocks, their
 // transposes, X' and layer 1's aggregation).  The targets are the first rows
 // of hop 1's sources (destinations come first).
+// first: the step opens a call (its tail writes the error word; later steps
+// of the call OR into it).
 gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch, float lr, float *loss_dev,
-                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o, hipStream_t s) {
+                       int64_t *edges_dev, char *prep, char *comp, const gnn_step_layout &o, bool first,
+                       hipStream_t s) {
     const int L = m->num_layers;
     const int act = m->precision;
     gnn_block blk[GNN_MAX_LAYERS];
@@ -433,6 +437,8 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     tail.loss_out = loss_dev;
     tail.edges = reinterpret_cast<int64_t *>(comp + o.edges);
     tail.edges_out = edges_dev;
+    tail.error = reinterpret_cast<int64_t *>(comp + o.error);
+    tail.accumulate = first ? 0 : 1;
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
@@ -475,7 +481,7 @@ gnn_status run_train_step(const gnn_model *m, const gnn_graph *g, const float *g
     char *prep = static_cast<char *>(ws);
     char *comp = prep + o.prep_bytes;
     GNN_TRY(run_prepare(m, g, gcn_norm, table, tdt, host_table, row_stride, targets, seed, step, prep, o, s));
-    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, s);
+    return run_compute(m, labels, batch, lr, loss_dev, edges_dev, prep, comp, o, true, s);
 }
 
 gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_norm, const void *table,
@@ -488,11 +494,12 @@ gnn_status run_step_prepare(const gnn_model *m, const gnn_graph *g, const float 
 }
 
 gnn_status run_step_compute(const gnn_model *m, int64_t graph_n, const int64_t *labels, int64_t batch, float lr,
-                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s) {
+                            float *loss_dev, int64_t *edges_dev, void *prep_ws, void *comp_ws, hipStream_t s,
+                            bool first) {
     gnn_step_layout o;
     GNN_TRY(step_layout(m, graph_n, batch, &o));
     return run_compute(m, labels, batch, lr, loss_dev, edges_dev, static_cast<char *>(prep_ws),
-                       static_cast<char *>(comp_ws), o, s);
+                       static_cast<char *>(comp_ws), o, first, s);
 }
 
 namespace {
@@ -560,7 +567,7 @@ gnn_status run_train_steps(const gnn_model *m, const gnn_graph *g, const float *
         for (int j = 0; j < G && q * G + j < steps; ++j) {
             const int64_t i = q * G + j;
             GNN_TRY(run_step_compute(m, g->n, labels, batch, lr, loss_dev ? loss_dev + i : nullptr,
-                                     edges_dev ? edges_dev + i : nullptr, prep_ws[half * G + j], comp_ws, s));
+                                     edges_dev ? edges_dev + i : nullptr, prep_ws[half * G + j], comp_ws, s, i == 0));
         }
         GNN_HIP(hipEventRecord(consumed[half], s));
     }

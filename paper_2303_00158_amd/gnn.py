@@ -16,7 +16,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgnn.so")
 
-GNN_OK, GNN_EINVAL, GNN_ESIZE, GNN_EHIP, GNN_EUNSUPPORTED = 0, -1, -2, -3, -4
+GNN_OK, GNN_EINVAL, GNN_ESIZE, GNN_EHIP, GNN_EUNSUPPORTED, GNN_EDEVICE = 0, -1, -2, -3, -4, -5
+GNN_DEVERR_WAIT, GNN_DEVERR_RANGE = 1, 2
 GNN_F32, GNN_BF16, GNN_F16 = 0, 1, 2
 GNN_AGG_SAGE_MEAN, GNN_AGG_GCN_SYM = 0, 1
 GNN_LOC_DEVICE, GNN_LOC_HOST_PINNED = 0, 1
@@ -61,7 +62,7 @@ class StepLayout(ctypes.Structure):
                 ("x0", _sz), ("agg", _sz * (_ML + 1)), ("h", _sz * (_ML + 1)), ("grad", _sz * (_ML + 1)),
                 ("d_a", _sz * (_ML + 1)), ("fwd_ws", _sz), ("fwd_ws_bytes", _sz), ("bwd_ws", _sz),
                 ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
-                ("loss_ws_bytes", _sz), ("edges", _sz), ("loss", _sz)]
+                ("loss_ws_bytes", _sz), ("edges", _sz), ("error", _sz), ("loss", _sz)]
 
 
 _P = ctypes.POINTER
@@ -98,6 +99,9 @@ _SIGNATURES = {
     "gnn_step_prepare": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _i64, _u64, _u64, _vp, _sz,
                                 _vp]),
     "gnn_step_compute": (_i32, [_P(Model), _i64, _vp, _i64, _f32, _vp, _vp, _vp, _sz, _vp, _sz, _vp]),
+    "gnn_decode_device_errors": (_i32, [_i64]),
+    "gnn_check_device_errors": (_i32, [_vp, _vp]),
+    "gnn_debug_sampler_fault": (_i32, [_i64, ctypes.c_uint32]),
     "gnn_train_steps": (_i32, [_P(Model), _P(Graph), _vp, _vp, _i32, _i32, _i64, _vp, _vp, _i64, _u64, _u64, _i64,
                                _f32, _vp, _vp, _P(_vp), _i32, _sz, _vp, _sz, _vp, _vp]),
 }
@@ -335,6 +339,23 @@ def update_bwd_noalloc(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: t
     return dw, db, d_a
 
 
+def check_device_errors(word: torch.Tensor, stream=None) -> None:
+    """gnn_check_device_errors on an int64 device word (a block's counts[3:4]
+    or a step's error word); raises GnnError (GNN_EDEVICE) if a flag is set."""
+    assert word.dtype == torch.int64 and word.is_cuda
+    _check(lib().gnn_check_device_errors(_ptr(word), _stream(stream)))
+
+
+def decode_device_errors(word: int) -> None:
+    """gnn_decode_device_errors (host only)."""
+    _check(lib().gnn_decode_device_errors(int(word)))
+
+
+def debug_sampler_fault(silent_row_tile: int, spin_limit: int) -> None:
+    """gnn_debug_sampler_fault: the test hook of the device error path."""
+    _check(lib().gnn_debug_sampler_fault(int(silent_row_tile), int(spin_limit)))
+
+
 def softmax_ce(logits: torch.Tensor, labels: torch.Tensor, targets: Optional[torch.Tensor], g_out: torch.Tensor,
                loss_out: torch.Tensor, stream=None):
     b, c = logits.shape
@@ -355,7 +376,7 @@ def sgd(w: torch.Tensor, dw: torch.Tensor, lr: float, stream=None) -> torch.Tens
 # whole training step
 # ---------------------------------------------------------------------------
 
-_COMPUTE_BUFFERS = ("agg", "h", "grad", "d_a", "fwd_ws", "bwd_ws", "loss_ws", "edges", "loss")
+_COMPUTE_BUFFERS = ("agg", "h", "grad", "d_a", "fwd_ws", "bwd_ws", "loss_ws", "edges", "error", "loss")
 
 
 class Trainer:
@@ -510,6 +531,15 @@ class Trainer:
             out["cscptr"] = self._view(lay.blk_cscptr[i], n_src + 1, torch.int64).cpu().numpy()
             out["cscrow"] = self._view(lay.blk_cscrow[i], nnz, torch.int32).cpu().numpy()
         return out
+
+    def error_word(self) -> torch.Tensor:
+        """The device error word of the last call (view of one int64)."""
+        return self._view(self.layout.error, 1, torch.int64, compute=True)
+
+    def check_device_errors(self, stream=None) -> None:
+        """Raise GnnError (GNN_EDEVICE) if the last call's blocks flagged a
+        device-side error."""
+        check_device_errors(self.error_word(), stream)
 
     def act_dtype(self) -> torch.dtype:
         return torch_dtype(self.precision)

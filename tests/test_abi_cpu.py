@@ -118,7 +118,7 @@ def test_step_layout_capacities_and_disjoint_buffers(gnn):
     prep += [(lay.blk_cscptr[0], (cs[0] + 1) * 8), (lay.blk_cscrow[0], cn[0] * 4), (lay.blk_csc_ws[0], 1)]
     prep += [(lay.agg[1], cd[1] * 100 * 2)]  # layer 1's aggregation is made by the prepare stage
     comp = [(lay.fwd_ws, lay.fwd_ws_bytes), (lay.bwd_ws, lay.bwd_ws_bytes), (lay.loss_ws, lay.loss_ws_bytes),
-            (lay.edges, 8), (lay.loss, 4)]
+            (lay.edges, 8), (lay.error, 8), (lay.loss, 4)]
     comp += [(lay.agg[2], cd[0] * 256 * 2)]
     for l, rows in ((1, cd[1]), (2, cd[0])):
         f_out = (100, 256, 47)[l]
@@ -199,3 +199,36 @@ def test_pipelined_steps_validation(gnn):
     assert call([a, b, c], prep_bytes=lay.prep_bytes - 256) == gnn.GNN_ESIZE
     assert call([a, b], comp_bytes=lay.compute_bytes - 256) == gnn.GNN_ESIZE
     assert call([a, b], comp=None) == gnn.GNN_EINVAL
+
+
+def test_device_error_decode(gnn):
+    # the device error flags of a block (counts[3]) and of a step's error
+    # word decode on the host into a status and a message naming each flag
+    lib = gnn.lib()
+    assert lib.gnn_decode_device_errors(0) == gnn.GNN_OK
+    assert lib.gnn_last_error() == b""
+    assert lib.gnn_decode_device_errors(gnn.GNN_DEVERR_WAIT) == gnn.GNN_EDEVICE
+    msg = lib.gnn_last_error()
+    assert b"GNN_DEVERR_WAIT" in msg and b"GNN_DEVERR_RANGE" not in msg
+    assert lib.gnn_decode_device_errors(gnn.GNN_DEVERR_RANGE) == gnn.GNN_EDEVICE
+    msg = lib.gnn_last_error()
+    assert b"GNN_DEVERR_RANGE" in msg and b"GNN_DEVERR_WAIT" not in msg
+    assert lib.gnn_decode_device_errors(3) == gnn.GNN_EDEVICE
+    msg = lib.gnn_last_error()
+    assert b"GNN_DEVERR_WAIT" in msg and b"GNN_DEVERR_RANGE" in msg and b"0x3" in msg
+    assert lib.gnn_decode_device_errors(0x10 | 1) == gnn.GNN_EDEVICE
+    assert b"unknown flags 0x10" in lib.gnn_last_error()
+    with pytest.raises(gnn.GnnError) as e:
+        gnn.decode_device_errors(2)
+    assert e.value.code == gnn.GNN_EDEVICE
+    # a NULL or misaligned device word is rejected before any HIP call
+    assert lib.gnn_check_device_errors(None, None) == gnn.GNN_EINVAL
+    assert lib.gnn_check_device_errors((1 << 24) + 4, None) == gnn.GNN_EINVAL
+
+
+def test_sampler_fault_hook_validation(gnn):
+    lib = gnn.lib()
+    assert lib.gnn_debug_sampler_fault(-2, 10) == gnn.GNN_EINVAL
+    assert lib.gnn_debug_sampler_fault(1, 0) == gnn.GNN_EINVAL
+    assert lib.gnn_debug_sampler_fault(1, 64) == gnn.GNN_OK
+    assert lib.gnn_debug_sampler_fault(-1, 0) == gnn.GNN_OK  # back to normal

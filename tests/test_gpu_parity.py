@@ -130,6 +130,40 @@ def test_build_block_bitexact(fanout):
         assert np.array_equal(again["col"], ref1.col) and np.array_equal(again["src_ids"], ref1.src_ids)
 
 
+def test_build_block_flags_a_scan_wait_that_gives_up():
+    # The row-pointer scan is single-pass: each row tile waits, boundedly,
+    # for the prefix of the tile before it.  The host's test hook makes row
+    # tile 1 publish nothing and every wait give up after 64 polls, so tile
+    # 2's wait runs out: the build still finishes and flags GNN_DEVERR_WAIT
+    # in counts[3], which gnn_check_device_errors reports.  With the hook
+    # cleared, the same workspace builds the oracle's block with no flag.
+    rowptr, col = workloads.rmat_graph(20_000, 150_000, seed=1)
+    rowptr, col = rowptr.numpy(), col.numpy()
+    n, n_dst, fanout = 20_000, 1000, 10  # 4 row tiles of 256
+    g = gnn.DeviceGraph(torch.from_numpy(rowptr).to(DEV), torch.from_numpy(col).to(DEV))
+    dst = np.random.default_rng(4).choice(n, size=n_dst, replace=False).astype(np.int64)
+    dst_d = torch.from_numpy(dst).to(DEV)
+    blk = gnn.DeviceBlock(n, n_dst, fanout, True, False, DEV)
+    ws = gnn.sampler_workspace(n, n_dst, fanout, DEV)
+    gnn.build_block(g, dst_d, fanout, 7, 3, 1, blk, ws)
+    gnn.check_device_errors(blk.counts[3:4])
+    try:
+        gnn.debug_sampler_fault(1, 64)
+        print("[device errors] build with a silent row tile", flush=True)
+        gnn.build_block(g, dst_d, fanout, 7, 3, 1, blk, ws)
+        with pytest.raises(gnn.GnnError) as e:
+            gnn.check_device_errors(blk.counts[3:4])
+        assert e.value.code == gnn.GNN_EDEVICE and "GNN_DEVERR_WAIT" in str(e.value)
+        assert int(blk.counts[3].item()) & gnn.GNN_DEVERR_WAIT
+    finally:
+        gnn.debug_sampler_fault(-1, 0)
+    gnn.build_block(g, dst_d, fanout, 7, 3, 1, blk, ws)
+    gnn.check_device_errors(blk.counts[3:4])
+    got, ref = blk.host(), oracle.build_block(rowptr, col, dst, fanout, 7, 3, 1)
+    for key in ("src_ids", "rowptr", "col", "cscptr", "cscrow"):
+        assert np.array_equal(got[key], getattr(ref, key)), key
+
+
 def test_build_block_degenerate_cases():
     # isolated destinations, a destination whose neighbours are all destinations, an empty batch
     rowptr = np.array([0, 0, 2, 4, 4, 5], dtype=np.int64)
@@ -908,6 +942,33 @@ def test_pipelined_two_stage_steps_equal_one_call_steps(kind, precision, nslot, 
         got, want = tr.block_view(h), ref.block_view(h)
         for key in want:
             assert np.array_equal(np.asarray(got[key]), np.asarray(want[key])), (h, key)
+
+
+def test_step_error_word_collects_the_blocks_flags():
+    # The step's tail ORs every block's counts[3] into the compute
+    # workspace's error word: a flag planted in a prepared (valid) block
+    # reaches it; the first step of the next call writes the word afresh.
+    dims, fan, n, m, batch = (32, 16, 8), (5, 5), 5_000, 40_000, 128
+    kind = gnn.GNN_AGG_SAGE_MEAN
+    _rp, _col, table, labels, ws, bs, g, targets = _pipeline_inputs(kind, dims, fan, n, m, batch)
+    table = table.to(DEV)
+    tr = gnn.Trainer(kind, dims, fan, gnn.GNN_F32, n, batch, ws, bs, device=DEV, prepare_slots=2, one_call=False)
+    tr.prepare(0, g, table, targets[0], seed=1, step=0)
+    tr.compute(0, labels, lr=0.05)
+    tr.check_device_errors()
+    tr.prepare(1, g, table, targets[1], seed=1, step=1)
+    off = tr.layout.blk_counts[1]
+    tr.prep_ws[1][off:off + 32].view(torch.int64)[3] = gnn.GNN_DEVERR_RANGE
+    tr.compute(1, labels, lr=0.05)
+    with pytest.raises(gnn.GnnError) as e:
+        tr.check_device_errors()
+    assert e.value.code == gnn.GNN_EDEVICE and "GNN_DEVERR_RANGE" in str(e.value)
+    tr.prepare(0, g, table, targets[2], seed=1, step=2)
+    tr.compute(0, labels, lr=0.05)
+    tr.check_device_errors()
+    tr.run_pipelined(g, table, labels, lambda s: targets[s], seed=1, first_step=3, steps=5, lr=0.05)
+    tr.check_device_errors()
+    assert int(tr.error_word().item()) == 0
 
 
 def test_prepare_then_compute_from_pinned_host_fp16_table_matches_oracle():
