@@ -198,6 +198,10 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
                                        nullptr, nullptr, nullptr, 0, s);
         }
     }
+    // Wide layers (K and n_out of 512 and more) are bound by the matrix
+    // cores: 256 x 256 tiles with operands copied straight to LDS.
+    if (wide_fwd_ok(a_self, a_nbr, adt, k_each, cap_m, n_out, wt, gemm_dt, out))
+        return launch_wide_fwd(a_self, a_nbr, k_each, m_dev, cap_m, wt, bias, n_out, relu, out, odt, s);
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
     FwdPlan p = plan_fwd(cap_m, n_out, K, bf);

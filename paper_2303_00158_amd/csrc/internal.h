@@ -166,6 +166,15 @@ gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, cons
 gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self, const void *a_nbr, int64_t f,
                                const uint16_t *wt, const float *bias, int64_t n_out, void *out, bool last,
                                const int64_t *labels, float *g, float *row_loss, int64_t batch, hipStream_t s);
+// The forward of wide layers (gemm_wide.hip): bf16 A rows and the bf16
+// shadow W^T, 256 x 256 tiles for the matrix cores.  wide_fwd_ok says
+// whether the shapes (K, n_out >= 512, K % 128 == 0, k_each % 64 == 0,
+// n_out % 8 == 0), sizes and alignment allow it.
+bool wide_fwd_ok(const void *a_self, const void *a_nbr, int adt, int64_t k_each, int64_t cap_m, int64_t n_out,
+                 const uint16_t *wt, int gemm_dt, const void *out);
+gnn_status launch_wide_fwd(const void *a_self, const void *a_nbr, int64_t k_each, const int64_t *m_dev,
+                           int64_t cap_m, const uint16_t *wt, const float *bias, int64_t n_out, int relu, void *out,
+                           int odt, hipStream_t s);
 // wt = bf16(w^T) for a K x n row-major w.
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
 size_t softmax_ce_ws_bytes(int64_t b);

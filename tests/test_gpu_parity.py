@@ -538,6 +538,35 @@ def test_layer_fwd_rejects_unsupported_shapes():
 SHAPES = [(1, 4, 1), (77, 3, 47), (300, 100, 256), (1000, 256, 47), (530, 16, 8), (129, 128, 130)]
 
 
+@pytest.mark.parametrize("sage,m,cap,ke,n,relu", [(True, 700, 1000, 768, 1024, True),
+                                                   (False, 513, 513, 512, 520, True),
+                                                   (True, 2000, 2048, 256, 512, True),
+                                                   (True, 300, 300, 1024, 640, False),
+                                                   (False, 1, 256, 1536, 1024, True)])
+def test_update_fwd_wide_layer_matches_oracle(sage, m, cap, ke, n, relu):
+    # wide layers (K and n_out >= 512) with the bf16 W^T take the 256 x 256
+    # matrix-core tiles: ragged rows below the capacity, a last column tile
+    # of 8 columns, the fp32 logits epilogue, a single row
+    rng = np.random.default_rng(m + ke + n + sage)
+    a_s = oracle.f32_to_bf16_bits(rng.standard_normal((cap, ke)).astype(np.float32))
+    a_n = oracle.f32_to_bf16_bits(rng.standard_normal((cap, ke)).astype(np.float32)) if sage else None
+    K = (2 if sage else 1) * ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(n)).astype(np.float32)
+    ocode = oracle.BF16 if relu else oracle.F32
+    want = oracle.update_fwd(a_s[:m], a_n[:m] if sage else None, w, b, relu, oracle.BF16, ocode)
+    wt = torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
+    out = torch.full((cap, n), float("nan"), dtype=torch.bfloat16 if relu else torch.float32, device=DEV)
+    m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
+    print(f"[update_fwd wide] sage={sage} m={m} cap={cap} ke={ke} n={n} relu={relu}", flush=True)
+    gnn.update_fwd(from_np_act(a_s), from_np_act(a_n) if sage else None, from_np_act(w), from_np_act(b), out, relu,
+                   gnn.GNN_BF16, m_dev=m_dev, cap_m=cap, wt=wt)
+    torch.cuda.synchronize()
+    got = oracle.to_float64(to_np_act(out))
+    assert relerr(got[:m], oracle.to_float64(want)) <= 8e-3
+    assert np.isnan(got[m:]).all()  # rows past the device count are not written
+
+
 @pytest.mark.parametrize("m,ke,n", SHAPES)
 @pytest.mark.parametrize("sage", [True, False])
 @pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
