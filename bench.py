@@ -76,6 +76,17 @@ def parse():
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run a plain device copy (fp32 -> int32 elementwise) of this many MiB three times, the "
                         "known-size kernel that scales HBM traffic counters")
+    p.add_argument("--other-workloads", default="rmat2.4m-gcn,tiny-er10k-gcn,fp32,rmat111m-sage3,"
+                                                 "rmat244m-sage-hosttable",
+                   help="comma-separated workloads also timed (pipelined) after the headline, each with its own "
+                        "roofline; 'fp32' is the headline workload in fp32; empty: none")
+    p.add_argument("--other-steps", type=int, default=20)
+    p.add_argument("--other-warmup", type=int, default=5)
+    p.add_argument("--host-table-n", type=int, default=30_000_000,
+                   help="vertices of the graph the host-table workload is scaled to (its full table needs 375 GB "
+                        "of pinned host memory)")
+    p.add_argument("--cpu-seconds-one-thread", type=float, default=6.0,
+                   help="CPU oracle baseline: also run it on one thread for about this long")
     p.add_argument("--pipeline", action=argparse.BooleanOptionalAction, default=None,
                    help="two-stage steps (gnn_train_steps) with the prepare stage (sampling, gather) of step s+1 "
                         "overlapping the compute stage of step s (default: on; --no-pipeline times one "
@@ -211,6 +222,18 @@ class StagedStep:
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
             call = lambda: gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1],  # noqa
                                              h_below=hin)
+        elif name.startswith("update_bwd_l"):
+            l = int(name[-1])
+            blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            call = lambda: gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None,  # noqa
+                                          trainer.w[l - 1], self.grad[l], trainer.dw[l - 1], trainer.db[l - 1],
+                                          self.da.get(l), gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
+                                          ws=self.bwd_ws[l])
+        elif name == "sgd":
+            def call():
+                for l in range(L):
+                    gnn.sgd(trainer.w[l], trainer.dw[l], 0.0)
+                    gnn.sgd(trainer.b[l], trainer.db[l], 0.0)
         else:
             raise ValueError(name)
         call()
@@ -224,6 +247,14 @@ class StagedStep:
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
+
+    def launches(self, name: str) -> int:
+        """Kernel launches of a multi-launch stage's ABI calls."""
+        if name.startswith("update_bwd"):
+            return 2  # the dA/dW GEMMs, then the split-order reduction
+        if name == "sgd":
+            return 2 * self.L  # one gnn_sgd for W and one for b per layer
+        return 1
 
     def block_sizes(self):
         return [{k: int(v) for k, v in blk.host().items() if k in ("n_dst", "n_src", "nnz")} for blk in self.blocks]
@@ -342,6 +373,21 @@ class StagedStep:
             rows_used = np.unique(b["cscrow"]).size
             return (rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
                     + 8 * (b["n_dst"] + 1) + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
+        if name.startswith("update_bwd_l"):
+            # dW = A^T G and db (reads A and G, writes dW and db); above the
+            # first layer also dA = G W^T (reads W, writes dA)
+            l = int(name[-1])
+            b = self.blocks[L - l].host()
+            M, K, N = b["n_dst"], w.k_of_layer(l), w.dims[l]
+            byts = M * K * S_H + M * N * 4 + K * N * 4 + N * 4
+            flops = 2 * M * K * N
+            if l > 1:
+                byts += K * N * 4 + M * K * 4
+                flops *= 2
+            return byts, flops
+        if name == "sgd":
+            P = sum(w.k_of_layer(l) * w.dims[l] + w.dims[l] for l in range(1, L + 1))
+            return 3 * 4 * P, 2 * P  # read W and dW, write W; one multiply-add per parameter
         return None, None
 
 
@@ -567,6 +613,190 @@ def perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev):
     return out
 
 
+class Inputs:
+    """Seeded synthetic inputs of one workload on the GPU (the graph and
+    feature table may be shared with another workload of the same graph)."""
+
+    def __init__(self, gnn, w, dev, share=None, precision=None):
+        self.w = w
+        self.host_table = w.table_loc == "host"
+        self.loc = gnn.GNN_LOC_HOST_PINNED if self.host_table else gnn.GNN_LOC_DEVICE
+        prec = precision or w.precision
+        self.act = torch.bfloat16 if prec == "bf16" else torch.float32
+        self.precision = gnn.GNN_BF16 if prec == "bf16" else gnn.GNN_F32
+        self.kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+        t0 = time.time()
+        if share is not None:
+            self.rowptr, self.col, self.graph, self.table = share.rowptr, share.col, share.graph, share.table
+            self.labels, self.perm, self.nrm = share.labels, share.perm, share.nrm
+        else:
+            log(f"generating {w.name}: {w.graph} n={w.n} m={w.m}")
+            self.rowptr, self.col = workloads.make_graph(w, device=dev)
+            self.graph = gnn.DeviceGraph(self.rowptr, self.col)
+            tdt = torch.float16 if w.table_dtype == "f16" else torch.float32
+            if self.host_table:
+                # drawn on the GPU in chunks and copied into pinned host memory
+                self.table = torch.empty((w.n, w.dims[0]), dtype=tdt, pin_memory=True)
+                workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, out=self.table)
+            else:
+                self.table = workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, dtype=tdt)
+            self.labels = workloads.labels(w.n, w.num_classes, seed=w.seed, device=dev)
+            self.perm = workloads.target_batches(w.n, w.batch, seed=w.seed, device=dev)
+            self.nrm = gnn.gcn_norm(self.graph)
+        L = w.num_layers
+        self.weights = [workloads.glorot(w.k_of_layer(l + 1), w.dims[l + 1], w.seed, l) for l in range(L)]
+        self.biases = [torch.zeros(w.dims[l + 1]) for l in range(L)]
+        torch.cuda.synchronize()
+        if share is None:
+            log(f"inputs ready in {time.time() - t0:.1f}s")
+
+
+def timed_training(gnn, inp, dev, steps, warmup, lr, pipeline, prepare_slots, one_call_compare=False):
+    """Warm up, then time `steps` training steps (pipelined through
+    gnn_train_steps, or one gnn_train_step call per step) between two HIP
+    events; the sampled edges come from the device counters."""
+    w = inp.w
+    tr = gnn.Trainer(inp.kind, w.dims, w.fanouts, inp.precision, w.n, w.batch, inp.weights, inp.biases, device=dev,
+                     prepare_slots=prepare_slots if pipeline else 0, one_call=one_call_compare or not pipeline)
+    nb = w.n // w.batch
+    n_t = min(nb, warmup + steps + (warmup + steps if one_call_compare else 0))
+    tgt = [workloads.targets_for_step(inp.perm, w.batch, s).contiguous() for s in range(max(n_t, 1))]
+    edges = torch.zeros(steps, dtype=torch.int64, device=dev)
+    prep_stream = torch.cuda.Stream(dev) if pipeline else None
+
+    def step_targets(first, count):
+        return torch.stack([tgt[(first + i) % len(tgt)] for i in range(count)])
+
+    def run_steps(first, count, edges_out=None, pipelined=pipeline, targets=None):
+        if pipelined:
+            tr.run_pipelined(inp.graph, inp.table, inp.labels,
+                             step_targets(first, count) if targets is None else targets, w.seed, first, count, lr,
+                             gcn_norm_t=inp.nrm, loc=inp.loc, edges_out=edges_out, prep_stream=prep_stream)
+            return
+        for i in range(count):
+            tr.step(inp.graph, inp.table, inp.labels, tgt[(first + i) % len(tgt)], w.seed, first + i, lr,
+                    gcn_norm_t=inp.nrm, loc=inp.loc, edges_out=None if edges_out is None else edges_out[i:i + 1])
+
+    def timed(first, count, edges_out, pipelined=pipeline):
+        targets = step_targets(first, count) if pipelined else None
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        ev0.record()
+        run_steps(first, count, edges_out, pipelined, targets)
+        t_enq = time.perf_counter() - t
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1), time.perf_counter() - t, t_enq
+
+    run_steps(0, warmup)
+    torch.cuda.synchronize()
+    log(f"{w.name}: warmup done ({warmup} steps, {'pipelined two-stage' if pipeline else 'one-call'} steps), "
+        f"loss {tr.loss.item():.4f}")
+    ms_total, t_wall, t_enqueue = timed(warmup, steps, edges)
+    if pipeline:
+        tr.check_device_errors()  # the blocks of the timed steps were built without a device-side failure
+    total_edges = int(edges.sum().item())
+    out = {"ms_per_step": ms_total / steps, "value": total_edges / (ms_total / 1e3),
+           "edges_per_step": total_edges / steps, "host_enqueue_ms_per_step": 1e3 * t_enqueue / steps,
+           "loss": tr.loss.item()}
+    log(f"{w.name}: timed {steps} steps: {out['ms_per_step']:.3f} ms/step (wall {1e3 * t_wall / steps:.3f}, host "
+        f"enqueue {out['host_enqueue_ms_per_step']:.3f}), {out['edges_per_step']:.0f} edges/step, "
+        f"loss {out['loss']:.4f}")
+    if pipeline and one_call_compare:
+        # the same steps without the overlap (one-call steps on one stream)
+        e2 = torch.zeros(steps, dtype=torch.int64, device=dev)
+        run_steps(0, warmup, pipelined=False)  # warms up the one-call path
+        ms2, _, _ = timed(warmup + steps, steps, e2, pipelined=False)
+        out["sequential_ms_per_step"] = ms2 / steps
+        log(f"{w.name}: without the overlap: {out['sequential_ms_per_step']:.3f} ms/step")
+    return out, tr, tgt
+
+
+# single-kernel stages (one launch per ABI call) and multi-launch ones
+MULTI_LAUNCH = ("update_bwd", "sgd")
+
+
+def staged_report(gnn, inp, tr, tgt, stage_steps, replays, lr):
+    """Event-timed staged steps (one ABI call per stage), then back-to-back
+    replays of each stage's call: per-stage times, the roofline of every
+    stage and of the dominant single-kernel stage."""
+    w = inp.w
+    staged = StagedStep(gnn, w, inp.graph, w.batch, inp.act, inp.loc)
+    sums, counts = {}, {}
+    for s in range(stage_steps + 1):
+        evs = []
+        torch.cuda.synchronize()
+        if hasattr(torch.cuda, "_sleep"):
+            torch.cuda._sleep(20_000_000)  # let the host enqueue the whole step before the GPU starts it
+        staged.run(tr, inp.table, inp.labels, tgt[s % len(tgt)], inp.nrm, w.seed, 10_000 + s, lr, events=evs)
+        torch.cuda.synchronize()
+        if s == 0:
+            continue  # first staged step warms up the allocations
+        for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
+            sums[n1] = sums.get(n1, 0.0) + e0.elapsed_time(e1)
+            counts[n1] = counts.get(n1, 0) + 1
+    stage_ms = {k: sums[k] / counts[k] for k in sums}
+    host_link = inp.loc == gnn.GNN_LOC_HOST_PINNED
+    replayable = [k for k in stage_ms
+                  if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd", "update_bwd"))
+                  or k == "sgd"]
+    launch_ms = {k: staged.replay(k, tr, inp.table, replays, labels=inp.labels) for k in replayable}
+    single = [k for k in replayable if not k.startswith(MULTI_LAUNCH)]
+    dom = max(single, key=lambda k: launch_ms[k])
+    roof = roofline_of(staged, dom, launch_ms[dom], host_link)
+    roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "source_hash": source_hash(dom)})
+    kernels = {}
+    for k in replayable:
+        e = {kk: (round(vv, 6) if isinstance(vv, float) else vv)
+             for kk, vv in roofline_of(staged, k, launch_ms[k], host_link).items()}
+        e["traffic"] = measured_traffic(k, w.name)
+        if k.startswith(MULTI_LAUNCH):
+            e["launches"] = staged.launches(k)
+        kernels[k] = e
+    log(f"{w.name}: stages (ms): {json.dumps({k: round(v, 5) for k, v in stage_ms.items()})}")
+    log(f"{w.name}: per-call (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
+    return staged, stage_ms, roof, kernels
+
+
+def other_workload(gnn, w, dev, args, share=None, precision=None, label=None):
+    """Measured figures of a workload besides the headline: pipelined
+    steps (edges/s, steps/s) and the roofline of its dominant kernel."""
+    inp = Inputs(gnn, w, dev, share=share, precision=precision)
+    steps, warmup = args.other_steps, args.other_warmup
+    t, tr, tgt = timed_training(gnn, inp, dev, steps, warmup, args.lr, True, args.prepare_slots)
+    staged, stage_ms, roof, kernels = staged_report(gnn, inp, tr, tgt, 2, max(5, args.replays // 2), args.lr)
+    out = {"workload": label or w.name,
+           "config": {"graph": f"{w.graph} n={w.n} m={w.m} {'directed' if w.directed else 'undirected'}",
+                      "aggregation": w.kind, "dims": list(w.dims), "fanouts": list(w.fanouts), "batch": w.batch,
+                      "features": f"{w.table_dtype} in {'pinned host memory' if inp.host_table else 'HBM'}",
+                      "precision": precision or w.precision},
+           "value": t["value"], "unit": "edges/s", "ms_per_step": t["ms_per_step"],
+           "steps_per_s": 1e3 / t["ms_per_step"], "edges_per_step": t["edges_per_step"], "steps": steps,
+           "warmup": warmup, "roofline": roof, "block_sizes": staged.block_sizes(),
+           "stages_ms": {k: round(v, 5) for k, v in stage_ms.items()}}
+    if inp.host_table:
+        link_bytes = staged.stage_bytes("gather")[0]
+        ach = link_bytes / (t["ms_per_step"] / 1e3) / 1e9
+        out["host_link"] = {"bytes_per_step": int(link_bytes), "achieved": ach, "peak": HOST_LINK_PEAK_GBS,
+                            "unit": "GB/s", "frac": ach / HOST_LINK_PEAK_GBS}
+    log(f"{out['workload']}: {t['value']:.3g} edges/s, {out['steps_per_s']:.0f} steps/s, dominant {roof['kernel']} "
+        f"{roof['frac']:.3f} of {roof['bound']}")
+    del staged, tr, inp
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -593,97 +823,26 @@ def main():
     if args.scale_n:
         m = args.scale_m or int(round(w.m * args.scale_n / w.n))
         w = workloads.scaled(w, args.scale_n, m)
-    host_table = w.table_loc == "host"
-    loc = gnn.GNN_LOC_HOST_PINNED if host_table else gnn.GNN_LOC_DEVICE
     pipeline = True if args.pipeline is None else args.pipeline
-    act = torch.bfloat16 if w.precision == "bf16" else torch.float32
-    precision = gnn.GNN_BF16 if w.precision == "bf16" else gnn.GNN_F32
-    kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
 
-    t0 = time.time()
-    log(f"generating {w.name}: {w.graph} n={w.n} m={w.m}")
-    rowptr, col = workloads.make_graph(w, device=dev)
-    graph = gnn.DeviceGraph(rowptr, col)
-    tdt = torch.float16 if w.table_dtype == "f16" else torch.float32
-    if host_table:
-        # drawn on the GPU in chunks and copied into pinned host memory
-        table = torch.empty((w.n, w.dims[0]), dtype=tdt, pin_memory=True)
-        workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, out=table)
-    else:
-        table = workloads.features(w.n, w.dims[0], seed=w.seed, device=dev, dtype=tdt)
-    labels = workloads.labels(w.n, w.num_classes, seed=w.seed, device=dev)
-    perm = workloads.target_batches(w.n, w.batch, seed=w.seed, device=dev)
-    L = w.num_layers
-    weights = [workloads.glorot(w.k_of_layer(l + 1), w.dims[l + 1], w.seed, l) for l in range(L)]
-    biases = [torch.zeros(w.dims[l + 1]) for l in range(L)]
-    nrm = gnn.gcn_norm(graph)
-    torch.cuda.synchronize()
-    stats = workloads.graph_stats(rowptr, col)
-    log(f"inputs ready in {time.time() - t0:.1f}s: {stats}")
-
-    tr = gnn.Trainer(kind, w.dims, w.fanouts, precision, w.n, w.batch, weights, biases, device=dev,
-                     prepare_slots=args.prepare_slots if pipeline else 0)
-    nb = w.n // w.batch
-    tgt = [workloads.targets_for_step(perm, w.batch, s).contiguous() for s in range(min(nb, args.warmup + args.steps))]
-    edges = torch.zeros(args.steps, dtype=torch.int64, device=dev)
-    prep_stream = torch.cuda.Stream(dev) if pipeline else None
-
-    def step_targets(first, count):
-        return torch.stack([tgt[(first + i) % len(tgt)] for i in range(count)])
-
-    def run_steps(first, count, edges_out=None, pipelined=pipeline, targets=None):
-        if pipelined:
-            tr.run_pipelined(graph, table, labels, step_targets(first, count) if targets is None else targets,
-                             w.seed, first, count, args.lr, gcn_norm_t=nrm, loc=loc, edges_out=edges_out,
-                             prep_stream=prep_stream)
-            return
-        for i in range(count):
-            tr.step(graph, table, labels, tgt[(first + i) % len(tgt)], w.seed, first + i, args.lr, gcn_norm_t=nrm,
-                    loc=loc, edges_out=None if edges_out is None else edges_out[i:i + 1])
-
-    def timed(first, count, edges_out, pipelined=pipeline):
-        targets = step_targets(first, count) if pipelined else None
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t = time.perf_counter()
-        ev0.record()
-        run_steps(first, count, edges_out, pipelined, targets)
-        t_enq = time.perf_counter() - t
-        ev1.record()
-        torch.cuda.synchronize()
-        return ev0.elapsed_time(ev1), time.perf_counter() - t, t_enq
-
-    run_steps(0, args.warmup)
-    torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps, {'pipelined two-stage' if pipeline else 'one-call'} steps), "
-        f"loss {tr.loss.item():.4f}")
-    ms_total, t_wall, t_enqueue = timed(args.warmup, args.steps, edges)
-    total_edges = int(edges.sum().item())
-    ms_per_step = ms_total / args.steps
-    value = total_edges / (ms_total / 1e3)
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}, host enqueue "
-        f"{1e3 * t_enqueue / args.steps:.3f}), "
-        f"{total_edges / args.steps:.0f} edges/step, loss {tr.loss.item():.4f}")
-    sequential_ms = None
-    if pipeline and tr.ws is not None:
-        # the same steps without the overlap (one-call steps on one stream)
-        e2 = torch.zeros(args.steps, dtype=torch.int64, device=dev)
-        run_steps(0, args.warmup, pipelined=False)  # warms up the one-call path
-        ms2, _, _ = timed(args.warmup + args.steps, args.steps, e2, pipelined=False)
-        sequential_ms = ms2 / args.steps
-        log(f"without the overlap: {sequential_ms:.3f} ms/step")
+    inp = Inputs(gnn, w, dev)
+    log(f"graph: {workloads.graph_stats(inp.rowptr, inp.col)}")
+    t, tr, tgt = timed_training(gnn, inp, dev, args.steps, args.warmup, args.lr, pipeline, args.prepare_slots,
+                                one_call_compare=pipeline)
+    ms_per_step = t["ms_per_step"]
+    host_table, loc, act, precision = inp.host_table, inp.loc, inp.act, inp.precision
 
     result = {
         "metric": "sampled edges/sec (fwd+bwd) and train steps/sec, 2-layer GraphSAGE, 1 GPU",
-        "value": value,
+        "value": t["value"],
         "unit": "edges/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
         "steps_per_s": 1e3 / ms_per_step,
-        "edges_per_step": total_edges / args.steps,
-        "host_enqueue_ms_per_step": 1e3 * t_enqueue / args.steps,
+        "edges_per_step": t["edges_per_step"],
+        "host_enqueue_ms_per_step": t["host_enqueue_ms_per_step"],
         "step_mode": "two-stage pipelined (prepare of step s+1 overlaps compute of step s)" if pipeline
                      else "one call per step",
         "higher_is_better": True,
@@ -700,42 +859,15 @@ def main():
             "parallelism": "single GPU",
         },
     }
-
-    if sequential_ms is not None:
-        result["sequential_ms_per_step"] = sequential_ms
+    if "sequential_ms_per_step" in t:
+        result["sequential_ms_per_step"] = t["sequential_ms_per_step"]
 
     # ---- staged run with events per stage --------------------------------
     if not args.no_stages:
-        staged = StagedStep(gnn, w, graph, w.batch, act, loc)
-        sums, counts = {}, {}
-        for s in range(args.stage_steps + 1):
-            evs = []
-            torch.cuda.synchronize()
-            if hasattr(torch.cuda, "_sleep"):
-                torch.cuda._sleep(20_000_000)  # let the host enqueue the whole step before the GPU starts it
-            staged.run(tr, table, labels, tgt[s % len(tgt)], nrm, w.seed, 10_000 + s, args.lr, events=evs)
-            torch.cuda.synchronize()
-            if s == 0:
-                continue  # first staged step warms up the allocations
-            for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
-                sums[n1] = sums.get(n1, 0.0) + e0.elapsed_time(e1)
-                counts[n1] = counts.get(n1, 0) + 1
-        stage_ms = {k: sums[k] / counts[k] for k in sums}
+        staged, stage_ms, roof, kernels = staged_report(gnn, inp, tr, tgt, args.stage_steps, args.replays, args.lr)
         result["stages_ms"] = {k: round(v, 5) for k, v in stage_ms.items()}
-        single = [k for k in stage_ms
-                  if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd"))]
-        def roof_of(name, ms):
-            return roofline_of(staged, name, ms, loc == gnn.GNN_LOC_HOST_PINNED)
-
-        # per-launch time of each single-kernel stage: back-to-back replays
-        launch_ms = {k: staged.replay(k, tr, table, args.replays, labels=labels) for k in single}
-        dom = max(single, key=lambda k: launch_ms[k])
-        roof = roof_of(dom, launch_ms[dom])
-        roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "source_hash": source_hash(dom)})
         result["roofline"] = roof
-        result["kernels"] = {k: {**{kk: (round(vv, 6) if isinstance(vv, float) else vv)
-                                    for kk, vv in roof_of(k, launch_ms[k]).items()},
-                                 "traffic": measured_traffic(k, w.name)} for k in single}
+        result["kernels"] = kernels
         result["block_sizes"] = staged.block_sizes()
         if host_table:
             # X' rows moved over the host link per step, against the step time
@@ -743,9 +875,7 @@ def main():
             ach = link_bytes / (ms_per_step / 1e3) / 1e9
             result["host_link"] = {"bytes_per_step": int(link_bytes), "achieved": ach, "peak": HOST_LINK_PEAK_GBS,
                                    "unit": "GB/s", "frac": ach / HOST_LINK_PEAK_GBS}
-        log(f"stages (ms): {json.dumps(result['stages_ms'])}")
-        log(f"per-launch (ms): {json.dumps({k: round(v, 5) for k, v in launch_ms.items()})}")
-        result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, table, dev)
+        result["perf_model"] = perf_model_report(w, staged, stage_ms, ms_per_step, host_table, inp.table, dev)
         result["dedup_aggregation"] = dedup_report(gnn, staged, w, args.replays, dev)
         log(f"dedup aggregation: {json.dumps(result['dedup_aggregation'])}")
         if precision == gnn.GNN_BF16:
@@ -753,44 +883,78 @@ def main():
             log(f"wide-layer GEMMs: {json.dumps(result['wide_gemm'])}")
         batches = [int(x) for x in args.scale_batches.split(",") if x.strip()]
         if batches:
-            result["kernels_at_batch"] = scale_report(gnn, w, graph, tr, table, labels, nrm, perm, act, loc, batches,
-                                                      args.replays, args.lr)
+            result["kernels_at_batch"] = scale_report(gnn, w, inp.graph, tr, inp.table, inp.labels, inp.nrm,
+                                                      inp.perm, act, loc, batches, args.replays, args.lr)
         pmr = result["perf_model"]["effective"]
         log(f"performance model (effective rates): T_execution {pmr['predicted_us']['T_execution (max, eq. 6)']:.1f} us "
             f"(max of stages), serial {pmr['predicted_us']['serial sum']:.1f} us; measured {pmr['measured_step_us']:.1f} us")
+        del staged
+
+    # ---- the other workloads, pipelined -----------------------------------
+    others = [x.strip() for x in args.other_workloads.split(",") if x.strip()] if not args.scale_n else []
+    if others:
+        result["other_workloads"] = []
+        for name in others:
+            if name == "fp32":
+                # the headline workload computed in fp32 throughout (the
+                # paper models features as 4-byte values)
+                e = other_workload(gnn, w, dev, args, share=inp, precision="f32", label=f"{w.name} (fp32)")
+            else:
+                ow = workloads.PRESETS[name]
+                lbl = None
+                if ow.table_loc == "host" and ow.n > args.host_table_n:
+                    # the 375 GB host table does not fit the host memory of one
+                    # run: same model, batch and fanouts on a smaller graph
+                    m = int(round(ow.m * args.host_table_n / ow.n))
+                    ow = workloads.scaled(ow, args.host_table_n, m)
+                    lbl = f"{name} scaled to n={ow.n}"
+                share = inp if (ow.graph == w.graph and ow.n == w.n and ow.m == w.m and ow.directed == w.directed
+                                and ow.dims[0] == w.dims[0] and ow.table_loc == w.table_loc
+                                and ow.table_dtype == w.table_dtype and ow.num_classes == w.num_classes) else None
+                e = other_workload(gnn, ow, dev, args, share=share, label=lbl)
+            result["other_workloads"].append(e)
 
     # ---- CPU oracle baseline ---------------------------------------------
     if not args.no_cpu_baseline:
         import oracle
         threads = len(os.sched_getaffinity(0))
-        oracle.set_threads(threads)
-        rp_h, col_h = rowptr.cpu().numpy(), col.cpu().numpy()
-        nrm_h = nrm.cpu().numpy()
-        table_h = table.cpu().numpy()
-        labels_h = labels.cpu().numpy()
-        w_h = [x.numpy() for x in weights]
-        b_h = [x.numpy() for x in biases]
+        rp_h, col_h = inp.rowptr.cpu().numpy(), inp.col.cpu().numpy()
+        nrm_h = inp.nrm.cpu().numpy()
+        table_h = inp.table.cpu().numpy()
+        labels_h = inp.labels.cpu().numpy()
         okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
         oprec = oracle.BF16 if w.precision == "bf16" else oracle.F32
-        tot_e, tot_t, n_steps = 0, 0.0, 0
-        while n_steps < 1 or tot_t < args.cpu_seconds:
-            s = n_steps
-            cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oprec, seed=w.seed,
-                                    step=s, lr=args.lr)
-            tt = time.perf_counter()
-            ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt[s % len(tgt)].cpu().numpy(), w_h,
-                                    b_h, cfg)
-            tot_t += time.perf_counter() - tt
-            tot_e += ref["edges"]
-            w_h, b_h = ref["new_w"], ref["new_b"]
-            n_steps += 1
+
+        def oracle_rate(nthreads, seconds):
+            oracle.set_threads(nthreads)
+            w_h = [x.numpy() for x in inp.weights]
+            b_h = [x.numpy() for x in inp.biases]
+            tot_e, tot_t, n_steps = 0, 0.0, 0
+            while n_steps < 1 or tot_t < seconds:
+                s = n_steps
+                cfg = oracle.StepConfig(kind=okind, dims=w.dims, fanouts=w.fanouts, precision=oprec, seed=w.seed,
+                                        step=s, lr=args.lr)
+                tt = time.perf_counter()
+                ref = oracle.train_step(rp_h, col_h, nrm_h, table_h, labels_h, tgt[s % len(tgt)].cpu().numpy(), w_h,
+                                        b_h, cfg)
+                tot_t += time.perf_counter() - tt
+                tot_e += ref["edges"]
+                w_h, b_h = ref["new_w"], ref["new_b"]
+                n_steps += 1
+            return tot_e, tot_t, n_steps, oracle.get_threads()
+
+        tot_e, tot_t, n_steps, used = oracle_rate(threads, args.cpu_seconds)
+        e1, t1, n1, _ = oracle_rate(1, args.cpu_seconds_one_thread)
         result["cpu_baseline"] = {
-            "value": tot_e / tot_t, "unit": "edges/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "value": tot_e / tot_t, "unit": "edges/s", "cores": used, "kind": "oracle",
             "sample": f"{n_steps} full training steps (sample, gather, forward, loss, backward, SGD) of the "
                       f"same workload, fp64 sums, {tot_t:.1f} s",
             "steps_per_s": n_steps / tot_t,
+            "one_thread": {"value": e1 / t1, "unit": "edges/s", "steps": n1, "seconds": round(t1, 2),
+                           "steps_per_s": n1 / t1},
+            "cpu_model": cpu_model(),
         }
-        log(f"cpu oracle: {tot_e / tot_t:.0f} edges/s with {oracle.get_threads()} threads")
+        log(f"cpu oracle: {tot_e / tot_t:.0f} edges/s with {used} threads, {e1 / t1:.0f} with 1 thread")
 
     print(json.dumps(result), flush=True)
 
