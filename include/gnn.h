@@ -64,9 +64,15 @@ typedef int32_t gnn_status;
 #define GNN_DEVERR_WAIT 1      /* a single-pass scan's bounded wait for an earlier workgroup gave up */
 #define GNN_DEVERR_RANGE 2     /* an index derived from device data fell outside its buffer */
 
-typedef enum { GNN_F32 = 0, GNN_BF16 = 1, GNN_F16 = 2 } gnn_dtype;
-typedef enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1 } gnn_agg;
-typedef enum { GNN_LOC_DEVICE = 0, GNN_LOC_HOST_PINNED = 1 } gnn_loc;
+/* Element types, aggregation operators and table locations.  The argument
+ * types are plain 32-bit integers (not C enums), so that any value a caller
+ * passes is representable and an unknown one is rejected by validation. */
+typedef int32_t gnn_dtype;
+typedef int32_t gnn_agg;
+typedef int32_t gnn_loc;
+enum { GNN_F32 = 0, GNN_BF16 = 1, GNN_F16 = 2 };
+enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1 };
+enum { GNN_LOC_DEVICE = 0, GNN_LOC_HOST_PINNED = 1 };
 typedef void *gnn_stream; /* hipStream_t */
 
 #define GNN_MAX_LAYERS 4
