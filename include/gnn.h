@@ -406,7 +406,7 @@ typedef struct gnn_step_layout {
     size_t grad[GNN_MAX_LAYERS + 1];    /* per layer l: G^l = dLoss/dZ^l, fp32 */
     size_t d_a[GNN_MAX_LAYERS + 1];     /* per layer l >= 2: dLoss/dA^l, fp32 */
     size_t fwd_ws, fwd_ws_bytes;        /* update-forward workspace */
-    size_t bwd_ws, bwd_ws_bytes;        /* update-backward workspace */
+    size_t bwd_ws, bwd_ws_bytes;        /* update-backward workspace (a region per layer, layer 1 first) */
     size_t loss_ws, loss_ws_bytes;      /* loss workspace */
     size_t edges;                       /* int64 sampled edges of the step */
     size_t error;                       /* int64 device error word (GNN_DEVERR_*): the OR of counts[3] of every

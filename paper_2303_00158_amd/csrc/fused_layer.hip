@@ -22,19 +22,13 @@
 // for the weight gradient.  Sums are fp32 over the edges in block order; the
 // stored A values are rounded to bf16 (round to nearest even) exactly as the
 // separate aggregation kernel stores them.
-#include "internal.h"
+#include "fused_dev.h"
 
 namespace gnn {
 
 namespace {
 
-constexpr int kThreads = 512;
-constexpr int kWaves = kThreads / 64;
-constexpr int kLogitLd = 65;  // row stride of the staged logits (fp32)
-constexpr int kNbr = 16;      // neighbour loads in flight per aggregation item
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+using namespace fl;
 
 struct FusedArgs {
     const int64_t *counts;  // M = min((counts[0] & cnt_keep) | cnt_add, cap_dst) (never null)
@@ -63,11 +57,7 @@ struct FusedArgs {
     int64_t cnt_keep, cnt_add;  // -1, 0 with a device row count; 0, cap_dst without one
 };
 
-// Kernel arguments are read with scalar loads, which the compiler otherwise
-// places next to their first use: several dependent round trips to the
-// argument buffer before the first vector load.  Naming every field in an
-// empty asm statement at entry makes all of them one batch of loads.
-template <class T> __device__ __forceinline__ void in_sgpr(const T &v) { asm volatile("" ::"s"(v)); }
+// Every kernel argument in one batch of scalar loads at entry (in_sgpr).
 __device__ __forceinline__ void args_up_front(const FusedArgs &a) {
     in_sgpr(a.counts), in_sgpr(a.rowptr), in_sgpr(a.col), in_sgpr(a.src_norm), in_sgpr(a.cap_dst);
     in_sgpr(a.es_cap), in_sgpr(a.h), in_sgpr(a.f), in_sgpr(a.wt), in_sgpr(a.bias), in_sgpr(a.n_out);
@@ -75,72 +65,6 @@ __device__ __forceinline__ void args_up_front(const FusedArgs &a) {
     in_sgpr(a.b), in_sgpr(a.kpad), in_sgpr(a.ldk), in_sgpr(a.a_self), in_sgpr(a.a_nbr), in_sgpr(a.cnt_keep);
     in_sgpr(a.cnt_add);
 }
-
-// A 16-byte MFMA operand fragment of bf16 W^T: elements k .. k+7 of the row
-// starting at element `row`.  W16 (K a multiple of 8, W^T 16-byte aligned):
-// one 16-byte load, indices past K read the row's last eight elements;
-// otherwise two 8-byte halves (K is a multiple of 4), indices past K read
-// the last four.  Those values are not zeroed: they meet A entries that are
-// zero (the A tile's padding), so a finite weight there contributes exactly
-// 0.  A wavefront's fragment is then 16 rows x 64 contiguous bytes.  Offsets
-// are 32-bit (W^T is far below 4 GiB) and the loads are unconditional and
-// branch-free: they are the first thing a wavefront issues, and a branch
-// around them would make the compiler wait for all of them at its join.
-template <bool W16>
-__device__ __forceinline__ bf16x8 load_wfrag(const uint16_t *wt, uint32_t row, uint32_t K, uint32_t k) {
-    const char *base = reinterpret_cast<const char *>(wt);
-    if constexpr (W16) {
-        return *reinterpret_cast<const bf16x8 *>(base + 2u * (row + min(k, K - 8)));
-    } else {
-        const uint32_t last = K - 4;
-        const uint2 lo = *reinterpret_cast<const uint2 *>(base + 2u * (row + min(k, last)));
-        const uint2 hi = *reinterpret_cast<const uint2 *>(base + 2u * (row + min(k + 4u, last)));
-        return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-    }
-}
-
-// Features e0 .. e0 + CW - 1 (CW = 4 or 8 bf16, one 8- or 16-byte access) of
-// a row, as floats.
-template <int CW> struct Chunk;
-template <> struct Chunk<4> {
-    using raw = uint2;
-    float v[4];
-    __device__ __forceinline__ static raw load(const uint16_t *p) { return *reinterpret_cast<const uint2 *>(p); }
-    __device__ __forceinline__ void set(raw u) {
-        v[0] = __uint_as_float(u.x << 16);
-        v[1] = __uint_as_float(u.x & 0xffff0000u);
-        v[2] = __uint_as_float(u.y << 16);
-        v[3] = __uint_as_float(u.y & 0xffff0000u);
-    }
-    __device__ __forceinline__ raw bf16() const {
-        return make_uint2(static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16),
-                          static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16));
-    }
-    __device__ __forceinline__ static void store(uint16_t *p, raw u) { *reinterpret_cast<uint2 *>(p) = u; }
-    __device__ __forceinline__ static raw zero() { return make_uint2(0u, 0u); }
-};
-template <> struct Chunk<8> {
-    using raw = uint4;
-    float v[8];
-    __device__ __forceinline__ static raw load(const uint16_t *p) { return *reinterpret_cast<const uint4 *>(p); }
-    __device__ __forceinline__ void set(raw u) {
-        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            v[2 * i] = __uint_as_float(w[i] << 16);
-            v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-        }
-    }
-    __device__ __forceinline__ raw bf16() const {
-        uint32_t w[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            w[i] = static_cast<uint32_t>(f32_to_bf16(v[2 * i])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * i + 1])) << 16);
-        return make_uint4(w[0], w[1], w[2], w[3]);
-    }
-    __device__ __forceinline__ static void store(uint16_t *p, raw u) { *reinterpret_cast<uint4 *>(p) = u; }
-    __device__ __forceinline__ static raw zero() { return make_uint4(0u, 0u, 0u, 0u); }
-};
 
 // One (row, chunk) item of the aggregation: the chunk of the A row (self and
 // mean for GraphSAGE, the normalised sum for GCN) into LDS and the
@@ -447,28 +371,8 @@ __global__ void __launch_bounds__(kThreads) fused_layer_kernel(FusedArgs a) {
                         Ls[(rt * 16 + 4 * (lane >> 4) + q) * kLogitLd + n] = acc[rt][0][q] + bias_t[0];
             }
             __syncthreads();
-            const int r = er, j = tid % TPR;
-            const int64_t row = row0 + r;
-            const float *zr = Ls + r * kLogitLd;
-            float mx = -INFINITY;
-            for (int n = j; n < a.n_out; n += TPR) mx = fmaxf(mx, zr[n]);
-#pragma unroll
-            for (int o = TPR / 2; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-            float s = 0.f;
-            for (int n = j; n < a.n_out; n += TPR) s += expf(zr[n] - mx);
-#pragma unroll
-            for (int o = TPR / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-            if (live) {
-                const float lse = mx + logf(s);
-                const float inv_b = 1.f / static_cast<float>(a.b);
-                float *lg = static_cast<float *>(a.out) + row * a.n_out;
-                for (int n = j; n < a.n_out; n += TPR) {
-                    const float p = expf(zr[n] - lse);
-                    a.g[row * a.n_out + n] = (p - (n == y ? 1.f : 0.f)) * inv_b;
-                    lg[n] = zr[n];
-                }
-                if (j == 0) a.row_loss[row] = lse - zr[y];
-            }
+            softmax_ce_row<TPR>(Ls + er * kLogitLd, tid % TPR, live, row0 + er, y, a.n_out, a.b,
+                                static_cast<float *>(a.out), a.g, a.row_loss);
             __syncthreads();
         }
     }

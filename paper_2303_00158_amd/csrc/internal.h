@@ -166,6 +166,23 @@ gnn_status launch_fused_layer(const gnn_block *b, int kind, int32_t maxdeg, cons
 gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self, const void *a_nbr, int64_t f,
                                const uint16_t *wt, const float *bias, int64_t n_out, void *out, bool last,
                                const int64_t *labels, float *g, float *row_loss, int64_t batch, hipStream_t s);
+// Forward of a two-layer model in one launch (fused_two.hip): layer 1's
+// update from its prepared aggregation m1 (and X' rows x_self, GraphSAGE),
+// computed per tile for the rows the last block's tile reads, then the last
+// layer as launch_fused_layer does with the loss.  Writes h1 (H^1, bf16),
+// agg_out (M^2, bf16), the fp32 logits, g, row_loss and, when d_a is given,
+// layer 2's input gradient dA^2 = G (W^2)^T (fp32, bf16 operands).  two_layer_ok says
+// whether the shapes (f0 % 4 == 0 and K1 <= 256, f1 % 8 == 0 and f1 <= 256,
+// n_out <= 64, or <= 48 for GraphSAGE, at most 2,048 destinations),
+// precision and alignment allow it.
+bool two_layer_ok(int kind, int precision, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_dst, int32_t fanout,
+                  const void *x_self, const void *m1, const uint16_t *wt1, const uint16_t *wt2, const void *h1,
+                  const void *agg_out);
+gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, const void *x_self, const void *m1,
+                            int64_t f0, const uint16_t *wt1, const float *bias1, int64_t f1, void *h1,
+                            const uint16_t *wt2, const float *bias2, int64_t n_out, void *agg_out, float *logits,
+                            const int64_t *labels, float *g, float *row_loss, int64_t batch, float *d_a,
+                            hipStream_t s);
 // The forward of wide layers (gemm_wide.hip): bf16 A rows and the bf16
 // shadow W^T, 256 x 256 tiles for the matrix cores.  wide_fwd_ok says
 // whether the shapes (K, n_out >= 512, K % 128 == 0, k_each % 64 == 0,

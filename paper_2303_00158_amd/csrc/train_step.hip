@@ -87,7 +87,9 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         o->grad[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * 4);
         if (l >= 2) o->d_a[l] = d.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
         fwd = std::max(fwd, update_fwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
-        bwd = std::max(bwd, update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
+        // every layer its own region: the two-layer backward reduces layer
+        // 2's partials while layer 1's are being written
+        bwd += update_bwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision);
     }
     o->fwd_ws = d.take(fwd);
     o->fwd_ws_bytes = fwd;
@@ -369,6 +371,102 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
     return st;
 }
 
+namespace {
+
+// Layer l's region of the update-backward workspace inside the compute
+// workspace comp (layers in order, as step_layout carves them).
+float *bwd_region(const gnn_model *m, const gnn_step_layout &o, char *comp, int l) {
+    size_t off = o.bwd_ws;
+    for (int j = 1; j < l; ++j)
+        off += update_bwd_ws_bytes(k_of(m, j), m->dims[j], o.cap_dst[m->num_layers - j], m->precision);
+    return reinterpret_cast<float *>(comp + off);
+}
+
+// The backward of a two-layer step whose forward was one launch that also
+// produced layer 2's input gradient dA^2: three launches.
+//   1. layer 2's dW partials, and the aggregation backward through the last
+//      block (dLoss/dZ^1, with the ReLU mask of H^1);
+//   2. layer 1's dW partials, and layer 2's reduction with SGD on W^2, b^2
+//      and its bf16 shadow (nothing else in launch 2 reads them);
+//   3. layer 1's reduction with SGD, and the end of the step.
+// Both layers' partials are live in launch 2, so each has its own region.
+struct TwoBwd {
+    gbwd::Args a2, a1;
+    gbwd::Plan p2, p1;
+    agg::BwdJob<GNN_AGG_SAGE_MEAN, uint16_t, true> sage_bwd;
+    agg::BwdJob<GNN_AGG_GCN_SYM, uint16_t, true> gcn_bwd;
+    bool ok;
+};
+
+TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *x0, const void *m1, char *comp,
+                          const gnn_step_layout &o, float lr) {
+    TwoBwd t{};
+    const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
+    const int act = m->precision;
+    const int64_t f0 = m->dims[0], f1 = m->dims[1];
+    const gnn_block &b2 = blk[0], &b1 = blk[1];
+    const uint16_t *h1 = reinterpret_cast<const uint16_t *>(comp + o.h[1]);
+    const void *agg2 = comp + o.agg[2];
+    float *d_a2 = reinterpret_cast<float *>(comp + o.d_a[2]);
+    float *g1 = reinterpret_cast<float *>(comp + o.grad[1]);
+    t.a2 = gbwd::Args{sage ? static_cast<const void *>(h1) : agg2, sage ? agg2 : nullptr, act, f1, b2.counts,
+                      b2.cap_dst, m->w[1], reinterpret_cast<const float *>(comp + o.grad[2]), m->dims[2], m->precision,
+                      m->dw[1], m->db[1], nullptr, bwd_region(m, o, comp, 2), m->w[1], m->b[1],
+                      m->wt[1], lr};
+    t.a1 = gbwd::Args{sage ? x0 : m1, sage ? m1 : nullptr, act, f0, b1.counts, b1.cap_dst, m->w[0], g1, f1,
+                      m->precision, m->dw[0], m->db[0], nullptr, bwd_region(m, o, comp, 1),
+                      m->w[0], m->b[0], m->wt[0], lr};
+    t.p2 = gbwd::plan(t.a2);
+    t.p1 = gbwd::plan(t.a1);
+    int C, S;
+    agg::split_row(f1, &C, &S);
+    t.sage_bwd = {b2, d_a2, f1, C, S, h1, g1};
+    t.gcn_bwd = {b2, d_a2, f1, C, S, h1, g1};
+    // the variants instantiated here: bf16 64-wide tiles over bf16 rows with
+    // vector A loads, and the vector aggregation backward
+    t.ok = act == GNN_BF16 && t.p2.bf && t.p1.bf && t.p2.pw.tile == 64 && t.p1.pw.tile == 64 && t.p2.vec_a &&
+           t.p1.vec_a && f1 % 4 == 0 && aligned(d_a2, 16) && aligned(g1, 16) && aligned(h1, 8) &&
+           t.p2.pw.map.blocks() <= kMaxGrid && t.p1.pw.map.blocks() <= kMaxGrid &&
+           reinterpret_cast<char *>(t.a2.part) + gbwd::dw_part_bytes(t.p2.pw, t.a2.K(), m->dims[2]) <=
+               comp + o.bwd_ws + o.bwd_ws_bytes &&
+           reinterpret_cast<char *>(t.a1.part) + gbwd::dw_part_bytes(t.p1.pw, t.a1.K(), f1) <=
+               reinterpret_cast<char *>(t.a2.part);
+    return t;
+}
+
+template <bool VG>
+gbwd::DweightJob<true, 64, uint16_t, true, VG> dweight64(const gbwd::Args &a, const gbwd::Plan &p) {
+    return gbwd::dweight_job<true, 64, uint16_t, true, VG>(a, p);
+}
+
+gnn_status two_layer_bwd(const gnn_model *m, const TwoBwd &t, unsigned bwd_grid, const loss::TailJob &tail,
+                         hipStream_t s) {
+    gnn_status st = GNN_OK;
+    auto first = [&](auto dwj) {
+        if (m->kind == GNN_AGG_SAGE_MEAN)
+            st = launch_job2(dwj, t.p2.dw_grid, t.sage_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
+        else
+            st = launch_job2(dwj, t.p2.dw_grid, t.gcn_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
+    };
+    if (t.p2.vec_g) first(dweight64<true>(t.a2, t.p2));
+    else first(dweight64<false>(t.a2, t.p2));
+    GNN_TRY(st);
+    auto second = [&](auto dwj) {
+        gbwd::with_reduce_job(t.a2, t.p2, [&](auto rj) {
+            st = launch_job2(dwj, t.p1.dw_grid, rj, t.p2.red_grid, s, "update_dweight_l1+dw_reduce_l2");
+        });
+    };
+    if (t.p1.vec_g) second(dweight64<true>(t.a1, t.p1));
+    else second(dweight64<false>(t.a1, t.p1));
+    GNN_TRY(st);
+    gbwd::with_reduce_job(t.a1, t.p1, [&](auto rj) {
+        st = launch_job2(rj, t.p1.red_grid, tail, 1, s, "update_dw_reduce+step_tail");
+    });
+    return st;
+}
+
+}  // namespace
+
 // Forward, loss, backward and SGD from a prepared workspace (blocks, their
 // transposes, X' and layer 1's aggregation).  The targets are the first rows
 // of hop 1's sources (destinations come first).
@@ -393,7 +491,24 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     float *g_last = reinterpret_cast<float *>(comp + o.grad[L]);
     bool loss_done = false;
     const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
-    for (int l = 1; l <= L; ++l) {
+    // a two-layer model at a small mini-batch: both layers in one launch
+    // (layer 1's rows computed where the last layer reads them)
+    TwoBwd tb{};
+    bool two = L == 2 && two_layer_ok(m->kind, m->precision, m->dims[0], m->dims[1], m->dims[2], blk[0].cap_dst,
+                                      m->fanouts[0], x0, agg_of(1), m->wt[0], m->wt[1], comp + o.h[1],
+                                      comp + o.agg[2]);
+    if (two) {
+        tb = two_layer_bwd_plan(m, blk, x0, agg_of(1), comp, o, lr);
+        two = tb.ok;
+    }
+    if (two) {
+        GNN_TRY(launch_two_layer(&blk[0], m->kind, m->fanouts[0], x0, agg_of(1), m->dims[0], m->wt[0], m->b[0],
+                                 m->dims[1], comp + o.h[1], m->wt[1], m->b[1], m->dims[2], comp + o.agg[2],
+                                 reinterpret_cast<float *>(comp + o.h[2]), labels, g_last, row_loss, batch,
+                                 reinterpret_cast<float *>(comp + o.d_a[2]), s));
+        loss_done = true;
+    }
+    for (int l = 1; l <= L && !two; ++l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
         void *agg = agg_of(l);
@@ -439,6 +554,7 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     tail.edges_out = edges_dev;
     tail.error = reinterpret_cast<int64_t *>(comp + o.error);
     tail.accumulate = first ? 0 : 1;
+    if (two) return two_layer_bwd(m, tb, agg::row_grid(blk[0].cap_src), tail, s);
     for (int l = L; l >= 1; --l) {
         const gnn_block &b = blk[L - l];
         const void *hin = (l == 1) ? x0 : static_cast<const void *>(comp + o.h[l - 1]);
