@@ -257,6 +257,43 @@ gnn_status gnn_layer_fwd(const gnn_block *b, gnn_agg kind, int32_t max_row_len, 
                          const int64_t *labels, int64_t batch, float *g_out, float *row_loss, gnn_stream s);
 
 /* ------------------------------------------------------------------------
+ * Both layers of a two-layer model in one launch, bf16: layer 1's update
+ * (equation 2) from its prepared aggregation, computed only for the rows
+ * the last block reads; the last layer's aggregation and update (equations
+ * 1 and 2) with the loss of Section II-B, as gnn_layer_fwd with labels
+ * gives them; and layer 2's input gradient (the backward of equation 2).
+ *   last    the last layer's block; its sources are layer 1's rows.
+ *   fanout  its row-length bound (sizes the LDS staging of its indices;
+ *           longer rows stay correct).
+ *   x_self  [device] bf16, rows x f0: layer 1's self part of A^1 (X', the
+ *           gathered features of layer 1's rows; SAGE only, may be NULL for
+ *           GCN).  m1 [device] bf16, rows x f0: layer 1's aggregation.  Row j
+ *           is layer-1 row j, for every source id of `last`.  f0 % 4 == 0.
+ *   wt1, b1 layer 1's bf16 W^T (f1 x K1, K1 = 2 f0 for SAGE, f0 for GCN;
+ *           K1 <= 256) and fp32 bias (or NULL).
+ *   h1      [device] bf16, last->cap_src x f1: H^1 = ReLU(A^1 W^1 + b^1),
+ *           written for every source row of `last` (each is a destination
+ *           or a sampled neighbour); f1 % 8 == 0, f1 <= 256.
+ *   wt2, b2 the last layer's bf16 W^T (n_out x K2, K2 = 2 f1 or f1) and
+ *           fp32 bias (or NULL); n_out <= 64, and <= 48 for SAGE.
+ *   agg_out [device] bf16 last->cap_dst x f1 and logits [device] fp32
+ *           last->cap_dst x n_out, labels, batch, g_out and row_loss: as
+ *           gnn_layer_fwd with labels.
+ *   d_a     [device] fp32 last->cap_dst x K2, or NULL: dA^2 = G (W^2)^T with
+ *           bf16 operands, bit for bit what gnn_update_bwd's input gradient
+ *           gives for the same g_out and weights (rows from batch on are 0).
+ * Bits of h1, agg_out and the logits equal those of gnn_update_fwd (A-load)
+ * followed by gnn_layer_fwd.  Needs last->cap_dst <= 2048 and 16-byte
+ * aligned wt1 (8 for GCN when f0 % 8 != 0), wt2, agg_out, and m1 / x_self
+ * (8 bytes when f0 % 8 != 0); else GNN_EUNSUPPORTED.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_two_layer_fwd(const gnn_block *last, gnn_agg kind, int32_t fanout, const void *x_self, const void *m1,
+                             int64_t f0, const uint16_t *wt1, const float *b1, int64_t f1, void *h1,
+                             const uint16_t *wt2, const float *b2, int64_t n_out, void *agg_out, float *logits,
+                             const int64_t *labels, int64_t batch, float *g_out, float *row_loss, float *d_a,
+                             gnn_stream s);
+
+/* ------------------------------------------------------------------------
  * Update (equation 2): Z = A W + b with A = [a_self || a_nbr] (SAGE) or
  * A = a_self (GCN, a_nbr NULL); K = 2*k_each or k_each.
  *   a_self, a_nbr [device] row-major, row length k_each, adt in {F32, BF16}.

@@ -79,6 +79,8 @@ _SIGNATURES = {
     "gnn_aggregate_fwd_dedup": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "gnn_two_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
+                                 _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz,
                               _vp]),
@@ -286,6 +288,23 @@ def layer_fwd(block: "DeviceBlock", kind: int, max_row_len: int, h_src: torch.Te
                                _ptr(bias), wt.shape[0], _ptr(agg_out), _ptr(out), _ptr(labels), int(batch),
                                _ptr(g_out), _ptr(row_loss), _stream(stream)))
     return out
+
+
+def two_layer_fwd(last: "DeviceBlock", kind: int, fanout: int, x_self: Optional[torch.Tensor], m1: torch.Tensor,
+                  wt1: torch.Tensor, b1: Optional[torch.Tensor], h1: torch.Tensor, wt2: torch.Tensor,
+                  b2: Optional[torch.Tensor], agg_out: torch.Tensor, logits: torch.Tensor, labels: torch.Tensor,
+                  batch: int, g_out: torch.Tensor, row_loss: torch.Tensor, d_a: Optional[torch.Tensor] = None,
+                  stream=None) -> torch.Tensor:
+    """gnn_two_layer_fwd: both layers of a two-layer model in one launch (bf16
+    rows x_self / m1 of layer 1, bf16 W^T shadows wt1 / wt2); h1, agg_out,
+    logits, g_out, row_loss and (when given) d_a receive H^1, the last
+    layer's aggregation, its logits, the loss gradient, the per-row losses and
+    layer 2's input gradient."""
+    _check(lib().gnn_two_layer_fwd(ctypes.byref(last.c), kind, int(fanout), _ptr(x_self), _ptr(m1), m1.shape[1],
+                                   _ptr(wt1), _ptr(b1), wt1.shape[0], _ptr(h1), _ptr(wt2), _ptr(b2), wt2.shape[0],
+                                   _ptr(agg_out), _ptr(logits), _ptr(labels), int(batch), _ptr(g_out),
+                                   _ptr(row_loss), _ptr(d_a), _stream(stream)))
+    return logits
 
 
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],

@@ -532,6 +532,119 @@ def test_layer_fwd_rejects_unsupported_shapes():
 
 
 # ---------------------------------------------------------------------------
+# both layers of a two-layer model in one launch
+# ---------------------------------------------------------------------------
+
+TWO_CASES = [
+    # f0, f1, n_out, n_dst, fanout, row-length bound given to the kernel
+    (100, 256, 47, 1024, 25, 25),   # the headline model: tiles of up to 104 rows in one pass
+    (32, 64, 8, 301, 5, 5),         # ragged last tile, 8-feature A^1 chunks, KSM1 = 4
+    (100, 256, 47, 300, 40, 40),    # tiles of more than 112 rows: two passes
+    (64, 128, 48, 513, 10, 2),      # bound far below the rows: indices read in place; 48 classes
+]
+
+
+def _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed):
+    blk, nrm = _oracle_block(seed, n=max(3000, 2 * n_dst), n_dst=n_dst, fanout=fanout)
+    rng = np.random.default_rng(seed)
+    sage = kind == oracle.SAGE
+    x_self = _act(rng, blk.n_src, f0, oracle.BF16)
+    m1 = _act(rng, blk.n_src, f0, oracle.BF16)
+    K1, K2 = (2 if sage else 1) * f0, (2 if sage else 1) * f1
+    w1 = (rng.standard_normal((K1, f1)) / np.sqrt(K1)).astype(np.float32)
+    w2 = (rng.standard_normal((K2, n_out)) / np.sqrt(K2)).astype(np.float32)
+    b1 = (0.1 * rng.standard_normal(f1)).astype(np.float32)
+    b2 = (0.1 * rng.standard_normal(n_out)).astype(np.float32)
+    labels = rng.integers(0, n_out, size=max(3000, 2 * n_dst)).astype(np.int64)
+    return blk, nrm, x_self, m1, w1, w2, b1, b2, labels
+
+
+def _shadow(w):
+    return torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound", TWO_CASES)
+def test_two_layer_fwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
+    # gnn_two_layer_fwd against the oracle's composition (update of layer 1,
+    # aggregation and update of layer 2, loss, input gradient of layer 2),
+    # and bit for bit against the launches it replaces
+    seed = f0 + f1 + n_out + n_dst + kind
+    sage = kind == oracle.SAGE
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed)
+    h1 = oracle.update_fwd(x_self if sage else m1, m1 if sage else None, w1, b1, True, oracle.BF16, oracle.BF16)
+    agg2 = oracle.aggregate_fwd(kind, blk, nrm if not sage else None, h1, oracle.BF16)
+    a_self, a_nbr = (h1[:blk.n_dst], agg2) if sage else (agg2, None)
+    logits = oracle.update_fwd(a_self, a_nbr, w2, b2, False, oracle.BF16, oracle.F32)
+    loss, g = oracle.softmax_ce(logits, labels[blk.src_ids[:blk.n_dst]])
+
+    db = upload_block(blk, nrm if not sage else None)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)  # noqa
+    xs_d, m1_d = from_np_act(x_self), from_np_act(m1)
+    wt1, wt2 = _shadow(w1), _shadow(w2)
+    out = dict(h1=torch.empty((blk.n_src, f1), dtype=torch.bfloat16, device=DEV),
+               agg=torch.empty((blk.n_dst, f1), dtype=torch.bfloat16, device=DEV),
+               logits=torch.empty((blk.n_dst, n_out), device=DEV), g=torch.empty((blk.n_dst, n_out), device=DEV),
+               rl=torch.empty(blk.n_dst, device=DEV), da=torch.empty((blk.n_dst, w2.shape[0]), device=DEV))
+    lab_d = d(labels)
+    print(f"[two_layer_fwd] kind={kind} f0={f0} f1={f1} n_out={n_out} n_dst={n_dst} fanout={fanout} bound={bound}",
+          flush=True)
+    gnn.two_layer_fwd(db, kind, bound, xs_d if sage else None, m1_d, wt1, d(b1), out["h1"], wt2, d(b2), out["agg"],
+                      out["logits"], lab_d, blk.n_dst, out["g"], out["rl"], out["da"])
+    torch.cuda.synchronize()
+    assert relerr(oracle.to_float64(to_np_act(out["h1"])), oracle.to_float64(h1)) <= 8e-3
+    assert relerr(oracle.to_float64(to_np_act(out["agg"])), oracle.to_float64(agg2)) <= 8e-3
+    assert relerr(out["logits"].cpu().numpy(), logits) <= 8e-3
+    assert relerr(out["g"].cpu().numpy(), g) <= 2e-2
+    assert abs(float(out["rl"].mean()) - loss) <= 2e-2 * max(1.0, abs(loss))
+    # the input gradient from the kernel's own G: bf16 operands, fp32 sums
+    g_gpu = out["g"].cpu().numpy()
+    a_s_gpu = to_np_act(out["h1"])[:blk.n_dst] if sage else to_np_act(out["agg"])
+    _, _, da = oracle.update_bwd(a_s_gpu, to_np_act(out["agg"]) if sage else None, w2, g_gpu, oracle.BF16, True)
+    assert relerr(out["da"].cpu().numpy(), da) <= 1e-5
+
+    # the launches it replaces: layer 1's update, the fused last layer, dA
+    ref = dict(h1=torch.empty_like(out["h1"]), agg=torch.empty_like(out["agg"]),
+               logits=torch.empty_like(out["logits"]), g=torch.empty_like(out["g"]), rl=torch.empty_like(out["rl"]),
+               da=torch.empty_like(out["da"]))
+    gnn.update_fwd(xs_d if sage else m1_d, m1_d if sage else None, d(w1), d(b1), ref["h1"], True, gnn.GNN_BF16,
+                   wt=wt1)
+    gnn.layer_fwd(db, kind, bound, ref["h1"], wt2, d(b2), ref["agg"], ref["logits"], labels=lab_d, batch=blk.n_dst,
+                  g_out=ref["g"], row_loss=ref["rl"])
+    K2 = w2.shape[0]
+    dw, dbias = torch.empty((K2, n_out), device=DEV), torch.empty(n_out, device=DEV)
+    gnn.update_bwd(ref["h1"][:blk.n_dst] if sage else ref["agg"], ref["agg"] if sage else None, d(w2), ref["g"], dw,
+                   dbias, ref["da"], gnn.GNN_BF16)
+    torch.cuda.synchronize()
+    for k in ("h1", "agg", "logits", "g", "rl", "da"):
+        a, b = out[k], ref[k]
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32)), k
+
+
+def test_two_layer_fwd_rejects_unsupported_shapes():
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, 32, 64, 8, 50, 4, 7)
+    db = upload_block(blk)
+    lab = torch.from_numpy(labels).to(DEV)
+
+    def call(f1, n_out, k1_rows=None):
+        wt1 = torch.zeros((f1, 64), dtype=torch.bfloat16, device=DEV)
+        wt2 = torch.zeros((n_out, 2 * f1), dtype=torch.bfloat16, device=DEV)
+        gnn.two_layer_fwd(db, oracle.SAGE, 4, from_np_act(x_self), from_np_act(m1), wt1, None,
+                          torch.empty((blk.n_src, f1), dtype=torch.bfloat16, device=DEV), wt2, None,
+                          torch.empty((blk.n_dst, f1), dtype=torch.bfloat16, device=DEV),
+                          torch.empty((blk.n_dst, n_out), device=DEV), lab, blk.n_dst,
+                          torch.empty((blk.n_dst, n_out), device=DEV), torch.empty(blk.n_dst, device=DEV))
+
+    call(64, 48)  # the largest class count GraphSAGE's staging holds
+    torch.cuda.synchronize()
+    for f1, n_out in ((512, 8), (64, 49), (60, 8)):  # f1 over 256, classes over 48, f1 % 8 != 0
+        with pytest.raises(gnn.GnnError) as e:
+            call(f1, n_out)
+        assert e.value.code == gnn.GNN_EUNSUPPORTED, (f1, n_out)
+
+
+# ---------------------------------------------------------------------------
 # update GEMMs
 # ---------------------------------------------------------------------------
 
