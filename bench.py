@@ -37,7 +37,10 @@ PROFILES = os.path.join(ROOT, "profiles")
 # Source files of each single-kernel stage's kernel (their hash ties a
 # counter measurement to the code it was taken on).
 KERNEL_SOURCES = {
-    "layer_fwd": ["paper_2303_00158_amd/csrc/fused_layer.hip", "paper_2303_00158_amd/csrc/internal.h"],
+    "fwd_l1l2": ["paper_2303_00158_amd/csrc/fused_two.hip", "paper_2303_00158_amd/csrc/fused_dev.h",
+                 "paper_2303_00158_amd/csrc/internal.h"],
+    "layer_fwd": ["paper_2303_00158_amd/csrc/fused_layer.hip", "paper_2303_00158_amd/csrc/fused_dev.h",
+                  "paper_2303_00158_amd/csrc/internal.h"],
     "update_fwd": ["paper_2303_00158_amd/csrc/gemm_fwd.hip", "paper_2303_00158_amd/csrc/fused_layer.hip",
                    "paper_2303_00158_amd/csrc/gemm_engine.h", "paper_2303_00158_amd/csrc/internal.h"],
     "agg_fwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
@@ -169,6 +172,7 @@ class StagedStep:
         self.loss = torch.zeros(1, device=dev)
         self.row_loss = torch.empty(batch_size, device=dev)
         self.fused = {}  # layer -> whether gnn_layer_fwd serves it (as inside the training step)
+        self.two = None  # whether gnn_two_layer_fwd serves both layers (as inside the training step)
         gemm = gnn.GNN_BF16 if act == torch.bfloat16 else gnn.GNN_F32
         self.fwd_ws, self.bwd_ws = {}, {}
         for l in range(1, L + 1):
@@ -187,6 +191,15 @@ class StagedStep:
             kw = dict(labels=labels, batch=self.blocks[0].c.cap_dst, g_out=self.grad[L], row_loss=self.row_loss)
         gnn.layer_fwd(blk, self.kind, self.w.fanouts[L - l], hin, trainer.wt[l - 1], trainer.b[l - 1], self.agg[l],
                       self.h[l], **kw)
+
+    def two_layer_fwd(self, trainer, labels):
+        """gnn_two_layer_fwd on the blocks of the last run (layer 1's
+        aggregation already in agg[1])."""
+        gnn = self.gnn
+        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        gnn.two_layer_fwd(self.blocks[0], self.kind, self.w.fanouts[0], self.x0 if sage else None, self.agg[1],
+                          trainer.wt[0], trainer.b[0], self.h[1], trainer.wt[1], trainer.b[1], self.agg[2], self.h[2],
+                          labels, self.blocks[0].c.cap_dst, self.grad[2], self.row_loss, self.da[2])
 
     def replay(self, name: str, trainer, table, reps: int, labels=None) -> float:
         """Launch the single ABI call of stage `name` `reps` times back to back
@@ -217,6 +230,8 @@ class StagedStep:
         elif name.startswith("layer_fwd_l"):
             l = int(name[-1])
             call = lambda: self.layer_fwd(l, trainer, labels)  # noqa
+        elif name == "fwd_l1l2":
+            call = lambda: self.two_layer_fwd(trainer, labels)  # noqa
         elif name.startswith("agg_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -225,9 +240,10 @@ class StagedStep:
         elif name.startswith("update_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
+            da = None if self.two else self.da.get(l)
             call = lambda: gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None,  # noqa
                                           trainer.w[l - 1], self.grad[l], trainer.dw[l - 1], trainer.db[l - 1],
-                                          self.da.get(l), gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
+                                          da, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
                                           ws=self.bwd_ws[l])
         elif name == "sgd":
             def call():
@@ -283,7 +299,20 @@ class StagedStep:
         sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         loss_fused = False
-        for l in range(1, L + 1):
+        if L == 2 and self.two is not False and trainer.wt:
+            # as in the training step: layer 1's aggregation (the prepare
+            # stage's), then both layers, the loss and dA^2 in one launch
+            gnn.aggregate_fwd(self.blocks[1], self.kind, self.x0, self.agg[1])
+            mark("agg_fwd_l1")
+            try:
+                self.two_layer_fwd(trainer, labels)
+                self.two = loss_fused = True
+                mark("fwd_l1l2")
+            except gnn.GnnError as e:
+                if e.code != gnn.GNN_EUNSUPPORTED:
+                    raise
+                self.two = False
+        for l in range(1, L + 1 if not self.two else 1):
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
             # as in the training step: layer 1's aggregation belongs to the
@@ -313,8 +342,9 @@ class StagedStep:
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
             gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
-                           self.grad[l], trainer.dw[l - 1], trainer.db[l - 1], self.da.get(l), gemm,
-                           m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst, ws=self.bwd_ws[l])
+                           self.grad[l], trainer.dw[l - 1], trainer.db[l - 1],
+                           None if self.two else self.da.get(l), gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
+                           ws=self.bwd_ws[l])
             mark(f"update_bwd_l{l}")
             if l > 1:
                 gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1], h_below=hin)
@@ -366,6 +396,20 @@ class StagedStep:
             else:
                 byts += M * N * S_H
             return byts, 2 * M * K * N
+        if name == "fwd_l1l2":
+            # reads: the last block, its targets and labels, the A^1 rows of
+            # its distinct sources, both layers' weights; writes: H^1 of
+            # those rows, M^2, logits, the loss gradient and row losses, dA^2
+            b = self.blocks[0].host()
+            M, B = b["n_dst"], self.blocks[0].c.cap_dst
+            f0, f1, C = w.dims
+            K1, K2 = w.k_of_layer(1), w.k_of_layer(2)
+            R = np.union1d(np.unique(b["col"]), np.arange(M)).size
+            byts = (8 * (M + 1) + 4 * b["nnz"] + 16 * M + R * K1 * S_H + K1 * f1 * 2 + 4 * f1 + K2 * C * 2 + 4 * C
+                    + R * f1 * S_H + M * f1 * S_H + M * C * 4 + B * (C * 4 + 4) + M * K2 * 4)
+            if w.kind == "gcn":
+                byts += 4 * R
+            return byts, 2 * R * K1 * f1 + 4 * M * K2 * C
         if name.startswith("agg_bwd_l"):
             l = int(name[-1])
             b = self.blocks[L - l].host()
@@ -381,7 +425,7 @@ class StagedStep:
             M, K, N = b["n_dst"], w.k_of_layer(l), w.dims[l]
             byts = M * K * S_H + M * N * 4 + K * N * 4 + N * 4
             flops = 2 * M * K * N
-            if l > 1:
+            if l > 1 and not self.two:
                 byts += K * N * 4 + M * K * 4
                 flops *= 2
             return byts, flops
@@ -739,7 +783,8 @@ def staged_report(gnn, inp, tr, tgt, stage_steps, replays, lr):
     stage_ms = {k: sums[k] / counts[k] for k in sums}
     host_link = inp.loc == gnn.GNN_LOC_HOST_PINNED
     replayable = [k for k in stage_ms
-                  if k == "gather" or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd", "update_bwd"))
+                  if k in ("gather", "fwd_l1l2")
+                  or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd", "update_bwd"))
                   or k == "sgd"]
     launch_ms = {k: staged.replay(k, tr, inp.table, replays, labels=inp.labels) for k in replayable}
     single = [k for k in replayable if not k.startswith(MULTI_LAUNCH)]
