@@ -277,6 +277,16 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
             asm volatile("" : "+v"(bias_t[t]));
             if (!a.bias1) bias_t[t] = 0.f;
         }
+        // layer 2's weights in the last pass: they stream in while the
+        // matrix cores work on layer 1 (no other memory traffic then)
+        if (s0 + kSrows >= NS && wave < CT2) {  // (uniform per wavefront)
+            const int64_t n = static_cast<int64_t>(wave) * 16 + (lane & 15);
+            const uint32_t row = static_cast<uint32_t>((n < a.n_out ? n : 0) * K2);
+#pragma unroll
+            for (int ks = 0; ks < KSM2; ++ks)
+                wf2[ks] = load_wfrag<true>(a.wt2, row, static_cast<uint32_t>(K2), ks * 32 + 8 * (lane >> 4));
+            bias2_t = (a.bias2 ? a.bias2 : reinterpret_cast<const float *>(a.wt2))[n < a.n_out ? n : 0];
+        }
         // layer 1's update of these rows, one 16-row tile at a time, then
         // bias and ReLU to bf16 into the H^1 tile
         if (wave < CT1) {
@@ -310,14 +320,6 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
             const int sr = q / C1, c = q % C1;
             Chunk<8>::store(a.h1 + s_row(s0 + sr, rows, row0, E) * f1 + c * 8,
                             *reinterpret_cast<const uint4 *>(Hs + sr * kLdh + c * 8));
-        }
-        if (s0 + kSrows >= NS && wave < CT2) {  // (uniform per wavefront)
-            const int64_t n = static_cast<int64_t>(wave) * 16 + (lane & 15);
-            const uint32_t row = static_cast<uint32_t>((n < a.n_out ? n : 0) * K2);
-#pragma unroll
-            for (int ks = 0; ks < KSM2; ++ks)
-                wf2[ks] = load_wfrag<true>(a.wt2, row, static_cast<uint32_t>(K2), ks * 32 + 8 * (lane >> 4));
-            bias2_t = (a.bias2 ? a.bias2 : reinterpret_cast<const float *>(a.wt2))[n < a.n_out ? n : 0];
         }
         // equation 1 over this pass's edges of the item's destination, in
         // edge order
@@ -414,6 +416,24 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
         for (int q = 0; q < 4; ++q) Ls[(4 * (lane >> 4) + q) * kLogitLd + n] = acc2[q] + bias2_t;
     }
     __syncthreads();
+    // the staged W^2 values dA^2 needs, read now (the barrier above made
+    // them visible), during the softmax
+    constexpr int KP2 = 32 * KSM2, KTW = KP2 / 16 / kWaves;
+    uint32_t w[KTW][2][8];
+#pragma unroll
+    for (int i = 0; i < KTW; ++i) {
+        if (!a.d_a) break;  // (uniform)
+        const int k = (wave + kWaves * i) * 16 + (lane & 15);  // < KP2
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int n = st * 32 + 8 * (lane >> 4) + t;
+                const bool in = n < a.n_out;
+                const uint32_t v = Hs[(in ? n : 0) * LDW2 + k];
+                w[i][st][t] = in ? v : 0u;
+            }
+    }
     softmax_ce_row<TPR>(Ls + er * kLogitLd, tid % TPR, live, row0 + er, y, a.n_out, a.b, a.logits, a.g, a.row_loss,
                         Gs + er * 64, 64);
     if (a.d_a) {
@@ -427,8 +447,6 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
         // unconditional, from an in-bounds address, and masked afterwards (a
         // read under a condition becomes a branch with its own wait), and all
         // of a wavefront's reads are issued before its first product.
-        constexpr int KP2 = 32 * KSM2, KTW = KP2 / 16 / kWaves;
-        const uint16_t *W2s = Hs;
         __syncthreads();  // the gradient rows are staged
         bf16x8 ga[2];
 #pragma unroll
@@ -443,20 +461,6 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
             const uint32_t p2 = (__float_as_uint(hi.x) >> 16) | (__float_as_uint(hi.y) & 0xffff0000u);
             const uint32_t p3 = (__float_as_uint(hi.z) >> 16) | (__float_as_uint(hi.w) & 0xffff0000u);
             ga[st] = __builtin_bit_cast(bf16x8, make_uint4(p0 & keep, p1 & keep, p2 & keep, p3 & keep));
-        }
-        uint32_t w[KTW][2][8];
-#pragma unroll
-        for (int i = 0; i < KTW; ++i) {
-            const int k = (wave + kWaves * i) * 16 + (lane & 15);  // < KP2
-#pragma unroll
-            for (int st = 0; st < 2; ++st)
-#pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    const int n = st * 32 + 8 * (lane >> 4) + t;
-                    const bool in = n < a.n_out;
-                    const uint32_t v = W2s[(in ? n : 0) * LDW2 + k];
-                    w[i][st][t] = in ? v : 0u;
-                }
         }
 #pragma unroll
         for (int i = 0; i < KTW; ++i) {
