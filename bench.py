@@ -49,6 +49,9 @@ KERNEL_SOURCES = {
                "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
     "agg_bwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
                 "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
+    "update_bwd": ["paper_2303_00158_amd/csrc/gemm_bwd.hip", "paper_2303_00158_amd/csrc/gemm_bwd_dev.h",
+                   "paper_2303_00158_amd/csrc/gemm_engine.h", "paper_2303_00158_amd/csrc/jobs.h",
+                   "paper_2303_00158_amd/csrc/internal.h"],
 }
 HOST_LINK_PEAK_GBS = 64.0  # PCIe Gen5 x16, one direction
 BF16_PEAK_TFLOPS = 2500.0
