@@ -83,32 +83,54 @@ struct DweightJob {
     float *part;
     SplitMap map;
     int64_t k_tiles;
-    __device__ void run(int64_t blk, int64_t) const {
-        constexpr int D = depth<TILE>();
-        using SQ = SrcCols<BF16, TILE, float, VG, D>;
-        __shared__ __attribute__((aligned(16))) char lds[lds_bytes<TILE, TILE>()];
-        __shared__ float cs[SQ::RPP][TILE];
+    static constexpr int D = depth<TILE>();
+    using SP = SrcCols<BF16, TILE, TA, VA, D>;
+    using SQ = SrcCols<BF16, TILE, float, VG, D>;
+    static constexpr int kLdsBytes = lds_bytes<TILE, TILE>();
+    using ColSums = float[SQ::RPP][TILE];
+    // One workgroup's tile between its first loads (begin) and its partial
+    // stores (finish), so that another job can run in between.
+    struct Tile {
+        SP sp;
+        SQ sq;
         int split;
+        int64_t K, row0, col0, r_beg, r_end;
+        bool do_db;
+    };
+    __device__ bool begin(int64_t blk, Tile &t) const {
         int64_t tile;
-        map.of(blk, &split, &tile);
-        if (split >= map.nsplit) return;
+        map.of(blk, &t.split, &tile);
+        if (t.split >= map.nsplit) return false;
         const int64_t tk = tile % k_tiles, tn = tile / k_tiles;
         const int64_t M = m_dev ? min(*m_dev, cap_m) : cap_m;
-        const int64_t K = a_nbr ? 2 * k_each : k_each;
-        const int64_t row0 = tk * TILE;  // over K
-        const int64_t col0 = tn * TILE;  // over n_out
-        int64_t r_beg, r_end;
-        split_range<Cfg<BF16>::BK>(M, map.nsplit, split, &r_beg, &r_end);
-        SrcCols<BF16, TILE, TA, VA, D> sp{a_self, a_nbr, k_each, k_each, K, r_end, row0, {}};
-        SQ sq{g, nullptr, n_out, n_out, n_out, r_end, col0, {}};
-        const bool do_db = want_db && tk == 0;
+        t.K = a_nbr ? 2 * k_each : k_each;
+        t.row0 = tk * TILE;  // over K
+        t.col0 = tn * TILE;  // over n_out
+        split_range<Cfg<BF16>::BK>(M, map.nsplit, t.split, &t.r_beg, &t.r_end);
+        t.sp = SP{a_self, a_nbr, k_each, k_each, t.K, t.r_end, t.row0, {}};
+        t.sq = SQ{g, nullptr, n_out, n_out, n_out, t.r_end, t.col0, {}};
+        t.do_db = want_db && tk == 0;
+        if (t.r_beg < t.r_end) tile_prefetch<BF16, D>(t.sp, t.sq, t.r_beg);
+        return true;
+    }
+    __device__ void run(int64_t blk, int64_t) const {
+        __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
+        __shared__ ColSums cs;
+        Tile t;
+        if (begin(blk, t)) finish(t, lds, cs);
+    }
+    __device__ void finish(Tile &t, char *lds, ColSums &cs) const {
+        const int64_t K = t.K, col0 = t.col0, row0 = t.row0;
+        const bool do_db = t.do_db;
         float4 colsum = make_float4(0.f, 0.f, 0.f, 0.f);
         Acc<TILE, TILE> acc;
-        run_tile<BF16, D>(acc, sp, sq, r_beg, r_end, lds, [&](const SQ &src, int s, int64_t r0, bool tail) {
-            if (do_db) src.add_colsum(s, colsum, r0, tail);
-        });
+        zero_acc(acc);
+        if (t.r_beg < t.r_end)
+            tile_rest<BF16, D>(acc, t.sp, t.sq, t.r_beg, t.r_end, lds, [&](const SQ &src, int s, int64_t r0, bool tail) {
+                if (do_db) src.add_colsum(s, colsum, r0, tail);
+            });
         const int64_t ldp = part_ld(n_out);
-        float *pp = part + static_cast<int64_t>(split) * (K + 1) * ldp;
+        float *pp = part + static_cast<int64_t>(t.split) * (K + 1) * ldp;
         if (do_db) {
             // fold the threads that share a column group, in order
             const int rr = threadIdx.x / SQ::TPR, tt = (threadIdx.x % SQ::TPR) * 4;
@@ -183,14 +205,16 @@ inline DwPlan plan_dw(int64_t K, int64_t n_out, int64_t cap_m, bool bf16) {
     // half the operand bytes per flop of 64 x 64 ones, and split the rows
     // over up to 2,048 workgroups: with 512, a 1536 x 1024 dW has 2 splits
     // and each workgroup walks half of all rows alone (3-6x slower at
-    // 26k-131k rows).  Narrow layers keep the 512-workgroup plan, measured
-    // best for the training step's shapes.
+    // 26k-131k rows).  Narrow layers split over up to 1,024 workgroups: a
+    // first layer of 200 x 256 then has 64 splits of at most 2 row chunks
+    // each, the shape the two-layer step's folded layer-1 job (which takes
+    // the same splits) is built for.
     const bool wide = K >= 512 && n_out >= 512;
     p.tile = wide ? 128 : pick_tile(K, n_out);
     p.k_tiles = ceil_div(K, p.tile);
     const int64_t tiles = p.k_tiles * ceil_div(n_out, p.tile);
     const int64_t nch = std::max<int64_t>(ceil_div(cap_m, bk_of(bf16)), 1);
-    const int64_t target = wide ? 2048 : 512;
+    const int64_t target = wide ? 2048 : 1024;
     p.nsplit = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({ceil_div(target, tiles), 64, nch})));
     p.map = SplitMap{tiles, p.nsplit};
     return p;

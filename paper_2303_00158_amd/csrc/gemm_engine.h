@@ -343,24 +343,35 @@ __device__ __forceinline__ void zero_tail(typename Cfg<BF16>::T *Ps, typename Cf
 // (their clamped addresses re-read cached lines and the data is never
 // committed): the number of loads in flight behind each stage is then the
 // same on every path, so the wait before a commit covers that stage alone.
-template <bool BF16, int D, int BM, int BN, class SP, class SQ, class ColSum>
-__device__ __forceinline__ void run_tile(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64_t r_beg, int64_t r_end, char *lds,
-                                         ColSum &&colsum) {
-    using CV = Cfg<BF16>;
-    using T = typename CV::T;
-    T *Ps = reinterpret_cast<T *>(lds);
-    T *Qs = Ps + BM * CV::LDK;
+//
+// run_tile is tile_prefetch (the first D chunks' loads) followed by tile_rest,
+// so a caller can issue a tile's first loads early and finish it later.
+template <bool BF16, int D, class SP, class SQ>
+__device__ __forceinline__ void tile_prefetch(SP &sp, SQ &sq, int64_t r_beg) {
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+        sp.fetch(s, r_beg + s * Cfg<BF16>::BK);
+        sq.fetch(s, r_beg + s * Cfg<BF16>::BK);
+    }
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ void zero_acc(Acc<BM, BN> &acc) {
 #pragma unroll
     for (int i = 0; i < Acc<BM, BN>::WI; ++i)
 #pragma unroll
         for (int j = 0; j < Acc<BM, BN>::WJ; ++j) acc.c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (r_beg >= r_end) return;
+}
+
+// The rest of run_tile after tile_prefetch (r_beg < r_end, acc zeroed).
+template <bool BF16, int D, int BM, int BN, class SP, class SQ, class ColSum>
+__device__ __forceinline__ void tile_rest(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64_t r_beg, int64_t r_end, char *lds,
+                                          ColSum &&colsum) {
+    using CV = Cfg<BF16>;
+    using T = typename CV::T;
+    T *Ps = reinterpret_cast<T *>(lds);
+    T *Qs = Ps + BM * CV::LDK;
     const int64_t nch = ceil_div(r_end - r_beg, CV::BK);
-#pragma unroll
-    for (int s = 0; s < D; ++s) {
-        sp.fetch(s, r_beg + s * CV::BK);
-        sq.fetch(s, r_beg + s * CV::BK);
-    }
     // one chunk through stage s: commit, refill the stage D chunks ahead,
     // multiply
     auto step = [&](int s, int64_t c) {
@@ -389,6 +400,15 @@ __device__ __forceinline__ void run_tile(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64
 #pragma unroll
     for (int s = 0; s < D - 1; ++s)
         if (c0 + s < nch) step(s, c0 + s);
+}
+
+template <bool BF16, int D, int BM, int BN, class SP, class SQ, class ColSum>
+__device__ __forceinline__ void run_tile(Acc<BM, BN> &acc, SP &sp, SQ &sq, int64_t r_beg, int64_t r_end, char *lds,
+                                         ColSum &&colsum) {
+    zero_acc(acc);
+    if (r_beg >= r_end) return;
+    tile_prefetch<BF16, D>(sp, sq, r_beg);
+    tile_rest<BF16, D>(acc, sp, sq, r_beg, r_end, lds, colsum);
 }
 
 // ---------------------------------------------------------------------------

@@ -18,6 +18,7 @@
 #include <type_traits>
 
 #include "aggregate_dev.h"
+#include "bwd_pull_dev.h"
 #include "csc_dev.h"
 #include "gather_dev.h"
 #include "gemm_bwd_dev.h"
@@ -395,7 +396,14 @@ struct TwoBwd {
     gbwd::Plan p2, p1;
     agg::BwdJob<GNN_AGG_SAGE_MEAN, uint16_t, true> sage_bwd;
     agg::BwdJob<GNN_AGG_GCN_SYM, uint16_t, true> gcn_bwd;
-    bool ok;
+    // layer 1's dW with layer 2's aggregation backward folded in, and layer
+    // 2's dW, in one launch (pull = the shapes allow it)
+    gnn_block b2;
+    const float *d_a2;
+    const uint16_t *h1;
+    gbwd::SplitMap pm;
+    unsigned pull_grid;
+    bool pull, ok;
 };
 
 TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *x0, const void *m1, char *comp,
@@ -422,6 +430,18 @@ TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *
     agg::split_row(f1, &C, &S);
     t.sage_bwd = {b2, d_a2, f1, C, S, h1, g1};
     t.gcn_bwd = {b2, d_a2, f1, C, S, h1, g1};
+    // The folded job repeats the aggregation backward's arithmetic when that
+    // walks each row's edges in one sequence (S == 1) and takes all of K in
+    // one workgroup; its split plan is the dW GEMM's.
+    const gbwd::SplitMap pm{ceil_div(f1, 64), t.p1.pw.nsplit};
+    t.pull = S == 1 && f1 % 4 == 0 && t.a1.K() <= gbwd::kPullMaxK && t.p1.pw.tile == 64 && t.p1.vec_a &&
+             b2.cscptr != nullptr && b2.cscrow != nullptr && (sage || b2.src_norm != nullptr) &&
+             b1.cap_dst <= b2.cap_src && pm.blocks() <= kMaxGrid;
+    t.b2 = b2;
+    t.d_a2 = d_a2;
+    t.h1 = h1;
+    t.pm = pm;
+    t.pull_grid = static_cast<unsigned>(std::max<int64_t>(pm.blocks(), t.p2.dw_grid));
     // the variants instantiated here: bf16 64-wide tiles over bf16 rows with
     // vector A loads, and the vector aggregation backward
     t.ok = act == GNN_BF16 && t.p2.bf && t.p1.bf && t.p2.pw.tile == 64 && t.p1.pw.tile == 64 && t.p2.vec_a &&
@@ -442,6 +462,33 @@ gbwd::DweightJob<true, 64, uint16_t, true, VG> dweight64(const gbwd::Args &a, co
 gnn_status two_layer_bwd(const gnn_model *m, const TwoBwd &t, unsigned bwd_grid, const loss::TailJob &tail,
                          hipStream_t s) {
     gnn_status st = GNN_OK;
+    if (t.pull) {
+        // layer 1's dW partials (G^1 pulled through the transpose) with
+        // layer 2's in the same workgroups, then both reductions with SGD
+        // and the end of the step
+        auto first = [&](auto kind_tag, auto dwj) {
+            constexpr int KIND = decltype(kind_tag)::value;
+            const gbwd::DweightPullJob<KIND, true, decltype(dwj)> j{
+                static_cast<const uint16_t *>(t.a1.a_self), static_cast<const uint16_t *>(t.a1.a_nbr), t.a1.k_each,
+                t.a1.m_dev, t.a1.cap_m, t.b2, t.d_a2, t.h1, t.a1.n_out, t.a1.db != nullptr, t.a1.part, t.pm, dwj,
+                static_cast<int64_t>(t.p2.dw_grid)};
+            st = launch_job(j, t.pull_grid, s, "update_dweight_l2+update_dweight_pull_l1");
+        };
+        auto by_kind = [&](auto dwj) {
+            if (m->kind == GNN_AGG_SAGE_MEAN) first(std::integral_constant<int, GNN_AGG_SAGE_MEAN>{}, dwj);
+            else first(std::integral_constant<int, GNN_AGG_GCN_SYM>{}, dwj);
+        };
+        if (t.p2.vec_g) by_kind(dweight64<true>(t.a2, t.p2));
+        else by_kind(dweight64<false>(t.a2, t.p2));
+        GNN_TRY(st);
+        gbwd::with_reduce_job(t.a1, t.p1, [&](auto r1) {
+            gbwd::with_reduce_job(t.a2, t.p2, [&](auto r2) {
+                st = launch_jobs(s, "dw_reduce_l1+dw_reduce_l2+step_tail", role(r1, t.p1.red_grid),
+                                 role(r2, t.p2.red_grid), role(tail, 1u));
+            });
+        });
+        return st;
+    }
     auto first = [&](auto dwj) {
         if (m->kind == GNN_AGG_SAGE_MEAN)
             st = launch_job2(dwj, t.p2.dw_grid, t.sage_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
