@@ -49,6 +49,10 @@ KERNEL_SOURCES = {
                "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
     "agg_bwd": ["paper_2303_00158_amd/csrc/aggregate.hip", "paper_2303_00158_amd/csrc/aggregate_dev.h",
                 "paper_2303_00158_amd/csrc/jobs.h", "paper_2303_00158_amd/csrc/internal.h"],
+    "bwd_l1l2": ["paper_2303_00158_amd/csrc/bwd_two.hip", "paper_2303_00158_amd/csrc/bwd_pull_dev.h",
+                 "paper_2303_00158_amd/csrc/gemm_bwd_dev.h", "paper_2303_00158_amd/csrc/gemm_engine.h",
+                 "paper_2303_00158_amd/csrc/aggregate_dev.h", "paper_2303_00158_amd/csrc/jobs.h",
+                 "paper_2303_00158_amd/csrc/internal.h"],
     "update_bwd": ["paper_2303_00158_amd/csrc/gemm_bwd.hip", "paper_2303_00158_amd/csrc/gemm_bwd_dev.h",
                    "paper_2303_00158_amd/csrc/gemm_engine.h", "paper_2303_00158_amd/csrc/jobs.h",
                    "paper_2303_00158_amd/csrc/internal.h"],
@@ -176,6 +180,8 @@ class StagedStep:
         self.row_loss = torch.empty(batch_size, device=dev)
         self.fused = {}  # layer -> whether gnn_layer_fwd serves it (as inside the training step)
         self.two = None  # whether gnn_two_layer_fwd serves both layers (as inside the training step)
+        self.two_bwd = None  # whether gnn_two_layer_bwd serves their backward (as inside the training step)
+        self.two_ws = None
         gemm = gnn.GNN_BF16 if act == torch.bfloat16 else gnn.GNN_F32
         self.fwd_ws, self.bwd_ws = {}, {}
         for l in range(1, L + 1):
@@ -203,6 +209,18 @@ class StagedStep:
         gnn.two_layer_fwd(self.blocks[0], self.kind, self.w.fanouts[0], self.x0 if sage else None, self.agg[1],
                           trainer.wt[0], trainer.b[0], self.h[1], trainer.wt[1], trainer.b[1], self.agg[2], self.h[2],
                           labels, self.blocks[0].c.cap_dst, self.grad[2], self.row_loss, self.da[2])
+
+    def two_layer_bwd(self, trainer):
+        """gnn_two_layer_bwd on the blocks and forward values of the last run."""
+        gnn = self.gnn
+        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        b0, b1 = self.blocks
+        if self.two_ws is None:
+            self.two_ws = gnn.two_layer_bwd_workspace(self.kind, self.w.dims[0], self.w.dims[1], self.w.dims[2],
+                                                      b1.c.cap_dst, b0.c.cap_dst, self.x0.device)
+        gnn.two_layer_bwd(b0, self.kind, self.x0 if sage else None, self.agg[1], b1.counts[0:1], b1.c.cap_dst,
+                          self.h[1], self.agg[2], self.da[2], self.grad[2], trainer.dw[0], trainer.db[0],
+                          trainer.dw[1], trainer.db[1], ws=self.two_ws)
 
     def replay(self, name: str, trainer, table, reps: int, labels=None) -> float:
         """Launch the single ABI call of stage `name` `reps` times back to back
@@ -235,6 +253,8 @@ class StagedStep:
             call = lambda: self.layer_fwd(l, trainer, labels)  # noqa
         elif name == "fwd_l1l2":
             call = lambda: self.two_layer_fwd(trainer, labels)  # noqa
+        elif name == "bwd_l1l2":
+            call = lambda: self.two_layer_bwd(trainer)  # noqa
         elif name.startswith("agg_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -269,7 +289,7 @@ class StagedStep:
 
     def launches(self, name: str) -> int:
         """Kernel launches of a multi-launch stage's ABI calls."""
-        if name.startswith("update_bwd"):
+        if name.startswith("update_bwd") or name == "bwd_l1l2":
             return 2  # the dA/dW GEMMs, then the split-order reduction
         if name == "sgd":
             return 2 * self.L  # one gnn_sgd for W and one for b per layer
@@ -341,7 +361,18 @@ class StagedStep:
         if not loss_fused:
             gnn.softmax_ce(self.h[L], labels, targets, self.grad[L], self.loss)
             mark("loss")
-        for l in range(L, 0, -1):
+        if self.two and self.two_bwd is not False:
+            # as in the training step: both layers' dW (layer 2's aggregation
+            # backward folded into layer 1's) and their reductions
+            try:
+                self.two_layer_bwd(trainer)
+                self.two_bwd = True
+                mark("bwd_l1l2")
+            except gnn.GnnError as e:
+                if e.code != gnn.GNN_EUNSUPPORTED:
+                    raise
+                self.two_bwd = False
+        for l in range(L, 0, -1) if not self.two_bwd else ():
             blk = self.blocks[L - l]
             hin = self.x0 if l == 1 else self.h[l - 1]
             gnn.update_bwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
@@ -413,6 +444,21 @@ class StagedStep:
             if w.kind == "gcn":
                 byts += 4 * R
             return byts, 2 * R * K1 * f1 + 4 * M * K2 * C
+        if name == "bwd_l1l2":
+            # reads: layer 1's A rows, H^1 (the mask), dA^2 (the neighbour
+            # part of every destination row, the self part of the
+            # destinations), the transpose and row pointers, layer 2's A rows
+            # and G^2; writes: both layers' dW and db (the partials of the
+            # split reductions are not counted)
+            b, b1 = self.blocks[0].host(), self.blocks[1].host()
+            M1, M2 = b1["n_dst"], b["n_dst"]
+            f0, f1, C = w.dims
+            K1, K2 = w.k_of_layer(1), w.k_of_layer(2)
+            byts = (M1 * K1 * S_H + M1 * f1 * S_H + M2 * K2 * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
+                    + 8 * (M2 + 1) + M2 * K2 * S_H + M2 * C * 4 + (K1 * f1 + f1 + K2 * C + C) * 4)
+            if w.kind == "gcn":
+                byts += 4 * b["n_src"]
+            return byts, 2 * M1 * K1 * f1 + 2 * M2 * K2 * C
         if name.startswith("agg_bwd_l"):
             l = int(name[-1])
             b = self.blocks[L - l].host()
@@ -761,7 +807,7 @@ def timed_training(gnn, inp, dev, steps, warmup, lr, pipeline, prepare_slots, on
 
 
 # single-kernel stages (one launch per ABI call) and multi-launch ones
-MULTI_LAUNCH = ("update_bwd", "sgd")
+MULTI_LAUNCH = ("update_bwd", "sgd", "bwd_l1l2")
 
 
 def staged_report(gnn, inp, tr, tgt, stage_steps, replays, lr):
@@ -786,7 +832,7 @@ def staged_report(gnn, inp, tr, tgt, stage_steps, replays, lr):
     stage_ms = {k: sums[k] / counts[k] for k in sums}
     host_link = inp.loc == gnn.GNN_LOC_HOST_PINNED
     replayable = [k for k in stage_ms
-                  if k in ("gather", "fwd_l1l2")
+                  if k in ("gather", "fwd_l1l2", "bwd_l1l2")
                   or k.startswith(("agg_fwd", "update_fwd", "layer_fwd", "agg_bwd", "update_bwd"))
                   or k == "sgd"]
     launch_ms = {k: staged.replay(k, tr, inp.table, replays, labels=inp.labels) for k in replayable}

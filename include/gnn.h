@@ -294,6 +294,44 @@ gnn_status gnn_two_layer_fwd(const gnn_block *last, gnn_agg kind, int32_t fanout
                              gnn_stream s);
 
 /* ------------------------------------------------------------------------
+ * Backward of a two-layer model below the loss (Section II-B, backward;
+ * Section V: layer 1's backward is the update alone), bf16 operands, fp32
+ * accumulate: the weight gradients of both layers,
+ *   dW^2 = (A^2)^T G^2, db^2 = colsum(G^2)   with A^2 = [H^1 || M^2] (SAGE)
+ *                                            or M^2 (GCN), the last block's rows;
+ *   G^1  = ReLU'(H^1) (aggregation backward of dA^2 through `last`);
+ *   dW^1 = (A^1)^T G^1, db^1 = colsum(G^1)   with A^1 = [x_self || m1] or m1.
+ * G^1 is never stored: each workgroup pulls its rows through the block's
+ * transpose.  No weights are updated.
+ *   last    the last layer's block, with its transpose (cscptr, cscrow) and,
+ *           for GCN, src_norm; its sources are layer 1's rows.
+ *   x_self, m1, f0   layer 1's A^1 rows as in gnn_two_layer_fwd (bf16).
+ *   m1_rows [device] int64 count of layer 1's rows (the first block's
+ *           destinations), at most cap_m1 <= last->cap_src.
+ *   h1      [device] bf16 H^1 (rows of `last`'s sources) x f1.
+ *   agg2    [device] bf16 M^2, last->cap_dst x f1.
+ *   d_a2    [device] fp32 dA^2, last->cap_dst x K2 (K2 = 2 f1 SAGE, f1 GCN),
+ *           16-byte aligned: the d_a of gnn_two_layer_fwd.
+ *   g2      [device] fp32 G^2, last->cap_dst x n_out (rows past the batch 0).
+ *   dw1 (K1 x f1), db1 (f1, or NULL), dw2 (K2 x n_out), db2 (n_out, or NULL)
+ *           [device] fp32 outputs.
+ *   ws      [device] 256-byte aligned workspace of
+ *           gnn_two_layer_bwd_workspace_size bytes (split partials; no state
+ *           kept between calls; calls sharing it must not overlap).
+ * dw1, db1, dw2 and db2 equal, bit for bit, gnn_aggregate_bwd (dA^2 -> G^1,
+ * h_below = h1) followed by gnn_update_bwd on each layer with the same caps
+ * (cap_m1 for layer 1, last->cap_dst for layer 2).  Needs f1 % 4 == 0 and
+ * f1 > 128, K1 <= 256, f0 % 4 == 0, 8-byte aligned bf16 rows and h1;
+ * else GNN_EUNSUPPORTED.
+ * ------------------------------------------------------------------------ */
+gnn_status gnn_two_layer_bwd_workspace_size(gnn_agg kind, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_m1,
+                                            int64_t cap_m2, size_t *bytes);
+gnn_status gnn_two_layer_bwd(const gnn_block *last, gnn_agg kind, const void *x_self, const void *m1, int64_t f0,
+                             const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1,
+                             const void *agg2, const float *d_a2, const float *g2, int64_t n_out, float *dw1,
+                             float *db1, float *dw2, float *db2, void *ws, size_t ws_bytes, gnn_stream s);
+
+/* ------------------------------------------------------------------------
  * Update (equation 2): Z = A W + b with A = [a_self || a_nbr] (SAGE) or
  * A = a_self (GCN, a_nbr NULL); K = 2*k_each or k_each.
  *   a_self, a_nbr [device] row-major, row length k_each, adt in {F32, BF16}.

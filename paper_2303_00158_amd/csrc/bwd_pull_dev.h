@@ -313,3 +313,36 @@ struct DweightPullJob {
 
 }  // namespace gbwd
 }  // namespace gnn
+
+namespace gnn {
+
+// Host side (bwd_two.hip): the backward of a two-layer model below the loss
+// as dW partials for both layers (layer 2's aggregation backward folded into
+// layer 1's) and their split reductions.
+struct TwoBwdPlan {
+    gbwd::Args a1, a2;  // the two layers' update backward (no dA)
+    gbwd::Plan p1, p2;
+    gnn_block b2;       // layer 2's block
+    const float *d_a2;
+    const uint16_t *h1;
+    gbwd::SplitMap pm;  // the folded job's (split, column tile) map
+    unsigned grid;      // its workgroups
+    bool gemm_ok;       // both dW GEMMs take the bf16 64 x 64 variants with vector A loads
+    bool pull;          // and the folded job applies
+};
+
+// kind: the aggregator; b2: layer 2's block (with its transpose); layer 1's A
+// rows [x_self || m1] (GraphSAGE) or m1 (GCN), bf16, f0 wide, with their row
+// count m1_rows (device) and capacity cap_m1; H^1 (bf16, f1 wide); M^2 =
+// agg2 (bf16, f1 wide); dA^2 and G^2 (fp32); per layer the weight gradient
+// outputs, the partial region (sized by gbwd::dw_part_bytes of the plan) and
+// the SGD targets (null: no update).
+TwoBwdPlan plan_two_bwd(int kind, const gnn_block &b2, const void *x_self, const void *m1, int64_t f0,
+                        const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1, const void *agg2,
+                        const float *d_a2, const float *g2, int64_t n_out, const float *w1, float *dw1, float *db1,
+                        float *part1, float *w1_upd, float *b1_upd, uint16_t *wt1_upd, const float *w2, float *dw2,
+                        float *db2, float *part2, float *w2_upd, float *b2_upd, uint16_t *wt2_upd, float lr);
+// The partials of both layers in one launch (requires t.pull).
+gnn_status launch_two_bwd_partials(const TwoBwdPlan &t, int kind, hipStream_t s);
+
+}  // namespace gnn

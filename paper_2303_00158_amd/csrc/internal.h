@@ -183,6 +183,19 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
                             const uint16_t *wt2, const float *bias2, int64_t n_out, void *agg_out, float *logits,
                             const int64_t *labels, float *g, float *row_loss, int64_t batch, float *d_a,
                             hipStream_t s);
+// Backward of a two-layer model below the loss (bwd_two.hip): both layers'
+// dW and db, with layer 2's aggregation backward folded into layer 1's dW
+// (G^1 never stored).  b2 is layer 2's block with its transpose; layer 1's A
+// rows are [x_self || m1] (GraphSAGE) or m1 (GCN), bf16, f0 wide, m1_rows
+// (device) of at most cap_m1; h1 is H^1 and agg2 is M^2 (bf16, f1 wide);
+// d_a2 and g2 are layer 2's input and output gradients (fp32).  ws holds
+// two_bwd_ws_bytes of split partials.  GNN_EUNSUPPORTED when the shapes do
+// not take the folded job (bwd_pull_dev.h).
+size_t two_bwd_ws_bytes(int kind, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_m1, int64_t cap_m2);
+gnn_status launch_two_bwd(const gnn_block *b2, int kind, const void *x_self, const void *m1, int64_t f0,
+                          const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1, const void *agg2,
+                          const float *d_a2, const float *g2, int64_t n_out, float *dw1, float *db1, float *dw2,
+                          float *db2, void *ws, hipStream_t s);
 // The forward of wide layers (gemm_wide.hip): bf16 A rows and the bf16
 // shadow W^T, 256 x 256 tiles for the matrix cores.  wide_fwd_ok says
 // whether the shapes (K, n_out >= 512, K % 128 == 0, k_each % 64 == 0,

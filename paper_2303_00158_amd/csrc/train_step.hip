@@ -392,65 +392,36 @@ float *bwd_region(const gnn_model *m, const gnn_step_layout &o, char *comp, int 
 //   3. layer 1's reduction with SGD, and the end of the step.
 // Both layers' partials are live in launch 2, so each has its own region.
 struct TwoBwd {
-    gbwd::Args a2, a1;
-    gbwd::Plan p2, p1;
-    agg::BwdJob<GNN_AGG_SAGE_MEAN, uint16_t, true> sage_bwd;
+    TwoBwdPlan q;  // both layers' dW (q.pull: layer 2's aggregation backward folded into layer 1's)
+    agg::BwdJob<GNN_AGG_SAGE_MEAN, uint16_t, true> sage_bwd;  // else G^1 through memory
     agg::BwdJob<GNN_AGG_GCN_SYM, uint16_t, true> gcn_bwd;
-    // layer 1's dW with layer 2's aggregation backward folded in, and layer
-    // 2's dW, in one launch (pull = the shapes allow it)
-    gnn_block b2;
-    const float *d_a2;
-    const uint16_t *h1;
-    gbwd::SplitMap pm;
-    unsigned pull_grid;
-    bool pull, ok;
+    bool ok;
 };
 
 TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *x0, const void *m1, char *comp,
                           const gnn_step_layout &o, float lr) {
     TwoBwd t{};
-    const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
-    const int act = m->precision;
     const int64_t f0 = m->dims[0], f1 = m->dims[1];
     const gnn_block &b2 = blk[0], &b1 = blk[1];
     const uint16_t *h1 = reinterpret_cast<const uint16_t *>(comp + o.h[1]);
-    const void *agg2 = comp + o.agg[2];
     float *d_a2 = reinterpret_cast<float *>(comp + o.d_a[2]);
     float *g1 = reinterpret_cast<float *>(comp + o.grad[1]);
-    t.a2 = gbwd::Args{sage ? static_cast<const void *>(h1) : agg2, sage ? agg2 : nullptr, act, f1, b2.counts,
-                      b2.cap_dst, m->w[1], reinterpret_cast<const float *>(comp + o.grad[2]), m->dims[2], m->precision,
-                      m->dw[1], m->db[1], nullptr, bwd_region(m, o, comp, 2), m->w[1], m->b[1],
-                      m->wt[1], lr};
-    t.a1 = gbwd::Args{sage ? x0 : m1, sage ? m1 : nullptr, act, f0, b1.counts, b1.cap_dst, m->w[0], g1, f1,
-                      m->precision, m->dw[0], m->db[0], nullptr, bwd_region(m, o, comp, 1),
-                      m->w[0], m->b[0], m->wt[0], lr};
-    t.p2 = gbwd::plan(t.a2);
-    t.p1 = gbwd::plan(t.a1);
+    t.q = plan_two_bwd(m->kind, b2, x0, m1, f0, b1.counts, b1.cap_dst, h1, f1, comp + o.agg[2], d_a2,
+                       reinterpret_cast<const float *>(comp + o.grad[2]), m->dims[2], m->w[0], m->dw[0], m->db[0],
+                       bwd_region(m, o, comp, 1), m->w[0], m->b[0], m->wt[0], m->w[1], m->dw[1], m->db[1],
+                       bwd_region(m, o, comp, 2), m->w[1], m->b[1], m->wt[1], lr);
+    t.q.a1.g = g1;  // the unfused path's G^1
     int C, S;
     agg::split_row(f1, &C, &S);
     t.sage_bwd = {b2, d_a2, f1, C, S, h1, g1};
     t.gcn_bwd = {b2, d_a2, f1, C, S, h1, g1};
-    // The folded job repeats the aggregation backward's arithmetic when that
-    // walks each row's edges in one sequence (S == 1) and takes all of K in
-    // one workgroup; its split plan is the dW GEMM's.
-    const gbwd::SplitMap pm{ceil_div(f1, 64), t.p1.pw.nsplit};
-    t.pull = S == 1 && f1 % 4 == 0 && t.a1.K() <= gbwd::kPullMaxK && t.p1.pw.tile == 64 && t.p1.vec_a &&
-             b2.cscptr != nullptr && b2.cscrow != nullptr && (sage || b2.src_norm != nullptr) &&
-             b1.cap_dst <= b2.cap_src && pm.blocks() <= kMaxGrid;
-    t.b2 = b2;
-    t.d_a2 = d_a2;
-    t.h1 = h1;
-    t.pm = pm;
-    t.pull_grid = static_cast<unsigned>(std::max<int64_t>(pm.blocks(), t.p2.dw_grid));
-    // the variants instantiated here: bf16 64-wide tiles over bf16 rows with
-    // vector A loads, and the vector aggregation backward
-    t.ok = act == GNN_BF16 && t.p2.bf && t.p1.bf && t.p2.pw.tile == 64 && t.p1.pw.tile == 64 && t.p2.vec_a &&
-           t.p1.vec_a && f1 % 4 == 0 && aligned(d_a2, 16) && aligned(g1, 16) && aligned(h1, 8) &&
-           t.p2.pw.map.blocks() <= kMaxGrid && t.p1.pw.map.blocks() <= kMaxGrid &&
-           reinterpret_cast<char *>(t.a2.part) + gbwd::dw_part_bytes(t.p2.pw, t.a2.K(), m->dims[2]) <=
+    const TwoBwdPlan &q = t.q;
+    t.ok = m->precision == GNN_BF16 && q.gemm_ok && f1 % 4 == 0 && aligned(d_a2, 16) && aligned(g1, 16) &&
+           aligned(h1, 8) &&
+           reinterpret_cast<char *>(q.a2.part) + gbwd::dw_part_bytes(q.p2.pw, q.a2.K(), m->dims[2]) <=
                comp + o.bwd_ws + o.bwd_ws_bytes &&
-           reinterpret_cast<char *>(t.a1.part) + gbwd::dw_part_bytes(t.p1.pw, t.a1.K(), f1) <=
-               reinterpret_cast<char *>(t.a2.part);
+           reinterpret_cast<char *>(q.a1.part) + gbwd::dw_part_bytes(q.p1.pw, q.a1.K(), f1) <=
+               reinterpret_cast<char *>(q.a2.part);
     return t;
 }
 
@@ -461,53 +432,39 @@ gbwd::DweightJob<true, 64, uint16_t, true, VG> dweight64(const gbwd::Args &a, co
 
 gnn_status two_layer_bwd(const gnn_model *m, const TwoBwd &t, unsigned bwd_grid, const loss::TailJob &tail,
                          hipStream_t s) {
+    const TwoBwdPlan &q = t.q;
     gnn_status st = GNN_OK;
-    if (t.pull) {
-        // layer 1's dW partials (G^1 pulled through the transpose) with
-        // layer 2's in the same workgroups, then both reductions with SGD
-        // and the end of the step
-        auto first = [&](auto kind_tag, auto dwj) {
-            constexpr int KIND = decltype(kind_tag)::value;
-            const gbwd::DweightPullJob<KIND, true, decltype(dwj)> j{
-                static_cast<const uint16_t *>(t.a1.a_self), static_cast<const uint16_t *>(t.a1.a_nbr), t.a1.k_each,
-                t.a1.m_dev, t.a1.cap_m, t.b2, t.d_a2, t.h1, t.a1.n_out, t.a1.db != nullptr, t.a1.part, t.pm, dwj,
-                static_cast<int64_t>(t.p2.dw_grid)};
-            st = launch_job(j, t.pull_grid, s, "update_dweight_l2+update_dweight_pull_l1");
-        };
-        auto by_kind = [&](auto dwj) {
-            if (m->kind == GNN_AGG_SAGE_MEAN) first(std::integral_constant<int, GNN_AGG_SAGE_MEAN>{}, dwj);
-            else first(std::integral_constant<int, GNN_AGG_GCN_SYM>{}, dwj);
-        };
-        if (t.p2.vec_g) by_kind(dweight64<true>(t.a2, t.p2));
-        else by_kind(dweight64<false>(t.a2, t.p2));
-        GNN_TRY(st);
-        gbwd::with_reduce_job(t.a1, t.p1, [&](auto r1) {
-            gbwd::with_reduce_job(t.a2, t.p2, [&](auto r2) {
-                st = launch_jobs(s, "dw_reduce_l1+dw_reduce_l2+step_tail", role(r1, t.p1.red_grid),
-                                 role(r2, t.p2.red_grid), role(tail, 1u));
+    if (q.pull) {
+        // both layers' dW partials (G^1 pulled through the transpose), then
+        // both reductions with SGD and the end of the step
+        GNN_TRY(launch_two_bwd_partials(q, m->kind, s));
+        gbwd::with_reduce_job(q.a1, q.p1, [&](auto r1) {
+            gbwd::with_reduce_job(q.a2, q.p2, [&](auto r2) {
+                st = launch_jobs(s, "dw_reduce_l1+dw_reduce_l2+step_tail", role(r1, q.p1.red_grid),
+                                 role(r2, q.p2.red_grid), role(tail, 1u));
             });
         });
         return st;
     }
     auto first = [&](auto dwj) {
         if (m->kind == GNN_AGG_SAGE_MEAN)
-            st = launch_job2(dwj, t.p2.dw_grid, t.sage_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
+            st = launch_job2(dwj, q.p2.dw_grid, t.sage_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
         else
-            st = launch_job2(dwj, t.p2.dw_grid, t.gcn_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
+            st = launch_job2(dwj, q.p2.dw_grid, t.gcn_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
     };
-    if (t.p2.vec_g) first(dweight64<true>(t.a2, t.p2));
-    else first(dweight64<false>(t.a2, t.p2));
+    if (q.p2.vec_g) first(dweight64<true>(q.a2, q.p2));
+    else first(dweight64<false>(q.a2, q.p2));
     GNN_TRY(st);
     auto second = [&](auto dwj) {
-        gbwd::with_reduce_job(t.a2, t.p2, [&](auto rj) {
-            st = launch_job2(dwj, t.p1.dw_grid, rj, t.p2.red_grid, s, "update_dweight_l1+dw_reduce_l2");
+        gbwd::with_reduce_job(q.a2, q.p2, [&](auto rj) {
+            st = launch_job2(dwj, q.p1.dw_grid, rj, q.p2.red_grid, s, "update_dweight_l1+dw_reduce_l2");
         });
     };
-    if (t.p1.vec_g) second(dweight64<true>(t.a1, t.p1));
-    else second(dweight64<false>(t.a1, t.p1));
+    if (q.p1.vec_g) second(dweight64<true>(q.a1, q.p1));
+    else second(dweight64<false>(q.a1, q.p1));
     GNN_TRY(st);
-    gbwd::with_reduce_job(t.a1, t.p1, [&](auto rj) {
-        st = launch_job2(rj, t.p1.red_grid, tail, 1, s, "update_dw_reduce+step_tail");
+    gbwd::with_reduce_job(q.a1, q.p1, [&](auto rj) {
+        st = launch_job2(rj, q.p1.red_grid, tail, 1, s, "update_dw_reduce+step_tail");
     });
     return st;
 }

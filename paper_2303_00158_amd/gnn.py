@@ -81,6 +81,9 @@ _SIGNATURES = {
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_two_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
                                  _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "gnn_two_layer_bwd_workspace_size": (_i32, [_i32, _i64, _i64, _i64, _i64, _i64, _P(_sz)]),
+    "gnn_two_layer_bwd": (_i32, [_P(Block), _i32, _vp, _vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
+                                 _vp, _vp, _vp, _vp, _sz, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz,
                               _vp]),
@@ -305,6 +308,30 @@ def two_layer_fwd(last: "DeviceBlock", kind: int, fanout: int, x_self: Optional[
                                    _ptr(agg_out), _ptr(logits), _ptr(labels), int(batch), _ptr(g_out),
                                    _ptr(row_loss), _ptr(d_a), _stream(stream)))
     return logits
+
+
+def two_layer_bwd_workspace(kind: int, f0: int, f1: int, n_out: int, cap_m1: int, cap_m2: int,
+                            device) -> torch.Tensor:
+    """A workspace for gnn_two_layer_bwd with these sizes."""
+    nb = _sz()
+    _check(lib().gnn_two_layer_bwd_workspace_size(kind, f0, f1, n_out, cap_m1, cap_m2, ctypes.byref(nb)))
+    return torch.zeros(max(nb.value, 256), dtype=torch.uint8, device=device)
+
+
+def two_layer_bwd(last: "DeviceBlock", kind: int, x_self: Optional[torch.Tensor], m1: torch.Tensor,
+                  m1_rows: torch.Tensor, cap_m1: int, h1: torch.Tensor, agg2: torch.Tensor, d_a2: torch.Tensor,
+                  g2: torch.Tensor, dw1: torch.Tensor, db1: Optional[torch.Tensor], dw2: torch.Tensor,
+                  db2: Optional[torch.Tensor], ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """gnn_two_layer_bwd: both layers' weight gradients below the loss (layer
+    2's aggregation backward folded into layer 1's dW).  m1_rows: device int64
+    count of layer 1's rows (at most cap_m1); ws: workspace (allocated when
+    None)."""
+    f0, f1, n_out = m1.shape[1], h1.shape[1], g2.shape[1]
+    if ws is None:
+        ws = two_layer_bwd_workspace(kind, f0, f1, n_out, cap_m1, last.c.cap_dst, m1.device)
+    _check(lib().gnn_two_layer_bwd(ctypes.byref(last.c), kind, _ptr(x_self), _ptr(m1), f0, _ptr(m1_rows), int(cap_m1),
+                                   _ptr(h1), f1, _ptr(agg2), _ptr(d_a2), _ptr(g2), n_out, _ptr(dw1), _ptr(db1),
+                                   _ptr(dw2), _ptr(db2), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],

@@ -622,6 +622,68 @@ def test_two_layer_fwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
                            b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32)), k
 
 
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound", TWO_CASES)
+def test_two_layer_bwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
+    # gnn_two_layer_bwd (both layers' dW and db, layer 2's aggregation
+    # backward folded into layer 1's dW) from gnn_two_layer_fwd's outputs:
+    # against the oracle's composition (aggregation backward with the ReLU
+    # mask, then each layer's update backward, bf16 operands) on the GPU's own
+    # forward values, and bit for bit against gnn_aggregate_bwd +
+    # gnn_update_bwd per layer.  Layers up to 128 wide are rejected (their
+    # aggregation backward sums a row in several slots, which the folded job
+    # does not repeat).
+    seed = 3 * f0 + f1 + n_out + n_dst + kind
+    sage = kind == oracle.SAGE
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed)
+    db = upload_block(blk, nrm if not sage else None)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)  # noqa
+    xs_d, m1_d = from_np_act(x_self), from_np_act(m1)
+    K1, K2 = w1.shape[0], w2.shape[0]
+    h1 = torch.empty((blk.n_src, f1), dtype=torch.bfloat16, device=DEV)
+    agg = torch.empty((blk.n_dst, f1), dtype=torch.bfloat16, device=DEV)
+    g = torch.empty((blk.n_dst, n_out), device=DEV)
+    da = torch.empty((blk.n_dst, K2), device=DEV)
+    gnn.two_layer_fwd(db, kind, bound, xs_d if sage else None, m1_d, _shadow(w1), d(b1), h1, _shadow(w2), d(b2), agg,
+                      torch.empty((blk.n_dst, n_out), device=DEV), d(labels), blk.n_dst, g,
+                      torch.empty(blk.n_dst, device=DEV), da)
+    m1_rows = torch.tensor([blk.n_src], dtype=torch.int64, device=DEV)
+    out = dict(dw1=torch.empty((K1, f1), device=DEV), db1=torch.empty(f1, device=DEV),
+               dw2=torch.empty((K2, n_out), device=DEV), db2=torch.empty(n_out, device=DEV))
+    print(f"[two_layer_bwd] kind={kind} f0={f0} f1={f1} n_out={n_out} n_dst={n_dst} fanout={fanout}", flush=True)
+    if f1 <= 128:
+        with pytest.raises(gnn.GnnError) as e:
+            gnn.two_layer_bwd(db, kind, xs_d if sage else None, m1_d, m1_rows, blk.n_src, h1, agg, da, g,
+                              out["dw1"], out["db1"], out["dw2"], out["db2"])
+        assert e.value.code == gnn.GNN_EUNSUPPORTED
+        return
+    gnn.two_layer_bwd(db, kind, xs_d if sage else None, m1_d, m1_rows, blk.n_src, h1, agg, da, g, out["dw1"],
+                      out["db1"], out["dw2"], out["db2"])
+    torch.cuda.synchronize()
+    # the oracle on the kernel's own forward values
+    h1_h, agg_h, g_h, da_h = to_np_act(h1), to_np_act(agg), g.cpu().numpy(), da.cpu().numpy()
+    dw2, db2, _ = oracle.update_bwd(h1_h[:blk.n_dst] if sage else agg_h, agg_h if sage else None, w2, g_h,
+                                    oracle.BF16, False)
+    g1 = oracle.aggregate_bwd(kind, blk, nrm if not sage else None, da_h, f1, h1_h, oracle.F32)
+    dw1, db1, _ = oracle.update_bwd(x_self if sage else m1, m1 if sage else None, w1, g1, oracle.BF16, False)
+    assert relerr(out["dw2"].cpu().numpy(), dw2) <= 1e-5
+    assert relerr(out["db2"].cpu().numpy(), db2) <= 1e-5
+    assert relerr(out["dw1"].cpu().numpy(), dw1) <= 2e-3
+    assert relerr(out["db1"].cpu().numpy(), db1) <= 1e-5
+
+    # the launches it replaces
+    g1_d = torch.empty((blk.n_src, f1), device=DEV)
+    gnn.aggregate_bwd(db, kind, da, f1, g1_d, h_below=h1)
+    ref = {k: torch.empty_like(v) for k, v in out.items()}
+    gnn.update_bwd(xs_d if sage else m1_d, m1_d if sage else None, d(w1), g1_d, ref["dw1"], ref["db1"], None,
+                   gnn.GNN_BF16)
+    gnn.update_bwd(h1[:blk.n_dst] if sage else agg, agg if sage else None, d(w2), g, ref["dw2"], ref["db2"], None,
+                   gnn.GNN_BF16)
+    torch.cuda.synchronize()
+    for k in out:
+        assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
+
+
 def test_two_layer_fwd_rejects_unsupported_shapes():
     blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, 32, 64, 8, 50, 4, 7)
     db = upload_block(blk)
