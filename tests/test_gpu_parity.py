@@ -544,8 +544,9 @@ TWO_CASES = [
 ]
 
 
-def _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed):
-    blk, nrm = _oracle_block(seed, n=max(3000, 2 * n_dst), n_dst=n_dst, fanout=fanout)
+def _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed, n=None):
+    n = n or max(3000, 2 * n_dst)
+    blk, nrm = _oracle_block(seed, n=n, n_dst=n_dst, fanout=fanout)
     rng = np.random.default_rng(seed)
     sage = kind == oracle.SAGE
     x_self = _act(rng, blk.n_src, f0, oracle.BF16)
@@ -555,7 +556,7 @@ def _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed):
     w2 = (rng.standard_normal((K2, n_out)) / np.sqrt(K2)).astype(np.float32)
     b1 = (0.1 * rng.standard_normal(f1)).astype(np.float32)
     b2 = (0.1 * rng.standard_normal(n_out)).astype(np.float32)
-    labels = rng.integers(0, n_out, size=max(3000, 2 * n_dst)).astype(np.int64)
+    labels = rng.integers(0, n_out, size=n).astype(np.int64)  # one per graph vertex (read by vertex id)
     return blk, nrm, x_self, m1, w1, w2, b1, b2, labels
 
 
@@ -623,8 +624,9 @@ def test_two_layer_fwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
 
 
 @pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
-@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound", TWO_CASES)
-def test_two_layer_bwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
+@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound,n", [c + (None,) for c in TWO_CASES] +
+                         [(100, 256, 47, 2048, 50, 50, 200_000)])
+def test_two_layer_bwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound, n):
     # gnn_two_layer_bwd (both layers' dW and db, layer 2's aggregation
     # backward folded into layer 1's dW) from gnn_two_layer_fwd's outputs:
     # against the oracle's composition (aggregation backward with the ReLU
@@ -632,10 +634,11 @@ def test_two_layer_bwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound):
     # forward values, and bit for bit against gnn_aggregate_bwd +
     # gnn_update_bwd per layer.  Layers up to 128 wide are rejected (their
     # aggregation backward sums a row in several slots, which the folded job
-    # does not repeat).
+    # does not repeat).  The last case has layer-1 row splits of two groups
+    # (about 9,400 rows over 64 splits of 192).
     seed = 3 * f0 + f1 + n_out + n_dst + kind
     sage = kind == oracle.SAGE
-    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed)
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(kind, f0, f1, n_out, n_dst, fanout, seed, n)
     db = upload_block(blk, nrm if not sage else None)
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)  # noqa
     xs_d, m1_d = from_np_act(x_self), from_np_act(m1)
@@ -1053,25 +1056,33 @@ def test_model_sync_shadow_is_rne_transpose():
         assert np.array_equal(got, _shadow_bits(tr.w[l]))
 
 
-def test_train_step_keeps_shadows_and_matches_unshadowed_step():
+@pytest.mark.parametrize("kind,batch", [(gnn.GNN_AGG_SAGE_MEAN, 512), (gnn.GNN_AGG_SAGE_MEAN, 2048),
+                                        (gnn.GNN_AGG_GCN_SYM, 2048)])
+def test_train_step_keeps_shadows_and_matches_unshadowed_step(kind, batch):
     # the shadow gives the GEMMs the same bf16 operands as rounding W on load,
     # so a step with shadows is bitwise the step without them; after SGD the
-    # shadows equal bf16(W_new^T)
-    dims, fan, n, m, batch = (100, 256, 47), (25, 10), 30_000, 400_000, 512
+    # shadows equal bf16(W_new^T).  With shadows a two-layer model takes the
+    # two-layer forward and the folded backward, without them the per-layer
+    # launches, so this also checks those bit for bit against each other; at
+    # batch 2048 the folded backward's row splits hold several 128-row groups
+    dims, fan, n, m = (100, 256, 47), (25, 10), 30_000, 400_000
+    sage = kind == gnn.GNN_AGG_SAGE_MEAN
     rowptr, col = workloads.rmat_graph(n, m, seed=0)
     table = workloads.features(n, dims[0], seed=0).to(DEV)
     labels = workloads.labels(n, dims[-1], seed=0).to(DEV)
     perm = workloads.target_batches(n, batch, seed=0)
-    ws = [workloads.glorot(2 * dims[l], dims[l + 1], 0, l) for l in range(2)]
+    ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], 0, l) for l in range(2)]
     bs = [torch.zeros(dims[l + 1]) for l in range(2)]
     g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
+    nrm = None if sage else gnn.gcn_norm(g)
     runs = []
+    print(f"[shadows vs none] kind={kind} batch={batch}", flush=True)
     for shadows in (True, False):
-        tr = gnn.Trainer(gnn.GNN_AGG_SAGE_MEAN, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV,
-                         shadows=shadows)
+        tr = gnn.Trainer(kind, dims, fan, gnn.GNN_BF16, n, batch, ws, bs, device=DEV, shadows=shadows)
         assert bool(tr.wt) == shadows
         for s in range(3):
-            tr.step(g, table, labels, workloads.targets_for_step(perm, batch, s).to(DEV), seed=0, step=s, lr=0.05)
+            tr.step(g, table, labels, workloads.targets_for_step(perm, batch, s).to(DEV), seed=0, step=s, lr=0.05,
+                    gcn_norm_t=nrm)
         torch.cuda.synchronize()
         if shadows:
             for l in range(2):
