@@ -1,5 +1,6 @@
 // Update gradients (equation 2's backward) on the matrix-core engine; the
 // job types are in gemm_bwd_dev.h.
+#include <algorithm>
 #include <type_traits>
 
 #include "gemm_bwd_dev.h"
@@ -23,7 +24,10 @@ __global__ void __launch_bounds__(256) shadow_sync_kernel(const float *__restric
 
 size_t update_bwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt) {
     const gbwd::DwPlan p = gbwd::plan_dw(k, n_out, cap_m, gemm_dt == GNN_BF16);
-    return round_up(gbwd::dw_part_bytes(p, k, n_out), 256);
+    size_t bytes = round_up(gbwd::dw_part_bytes(p, k, n_out), 256);
+    if (gbwd::wide_bwd_shape(k, n_out, gemm_dt))
+        bytes = std::max(bytes, static_cast<size_t>(gbwd::plan_wide_bwd(k, n_out, cap_m).ws_bytes));
+    return bytes;
 }
 
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s) {
@@ -35,6 +39,7 @@ gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt
 }
 
 gnn_status launch_update_bwd_gemms(const gbwd::Args &a, const gbwd::Plan &p, hipStream_t s) {
+    if (p.wide) return gbwd::launch_wide_bwd_gemms(a, s);
     GNN_CHECK(p.pa.map.blocks() <= kMaxGrid && p.pw.map.blocks() <= kMaxGrid, GNN_ESIZE,
               "update_bwd: too many tiles for one launch");
     // The common variants (64 x 64 tiles, vector activations and dA, the

@@ -236,9 +236,29 @@ inline size_t dw_part_bytes(const DwPlan &p, int64_t K, int64_t n_out) {
     return static_cast<size_t>(p.nsplit) * (K + 1) * part_ld(n_out) * 4;
 }
 
+// Wide layers on the matrix-core tiles of gemm_wide_bwd.hip: 256 x 256
+// tiles, dW split over the rows into as many splits as fill the CUs in one
+// wave; the workspace holds the partials, then the bf16 copies of W and G
+// that dA reads.
+struct WideBwdPlan {
+    int64_t k_tiles, tiles;
+    int64_t nsplit;     // dW alone
+    int64_t nsplit_da;  // dW sharing its launch with dA
+    int64_t part_bytes, ws_bytes;
+};
+WideBwdPlan plan_wide_bwd(int64_t K, int64_t n_out, int64_t cap_m);
+// Shapes the wide path may take (the workspace is sized for them) ...
+bool wide_bwd_shape(int64_t K, int64_t n_out, int gemm_dt);
+// ... and calls it takes: bf16 activations, a K tile in one half of
+// [a_self || a_nbr], 32-bit buffer offsets, aligned operands.
+bool wide_bwd_ok(const Args &a);
+// dA (when a.d_a is given) and the dW partials; the caller runs the
+// reduction job with the plan's split count.
+gnn_status launch_wide_bwd_gemms(const Args &a, hipStream_t s);
+
 // Everything the launch-time dispatch needs.
 struct Plan {
-    bool bf, vec_a, vec_g, vec_o, vec_r;
+    bool bf, vec_a, vec_g, vec_o, vec_r, wide;
     DinPlan pa;
     DwPlan pw;
     unsigned din_grid, dw_grid, red_grid;
@@ -256,6 +276,11 @@ inline Plan plan(const Args &a) {
               aligned(a.b_upd, 16);
     p.pa = plan_dinput(a.cap_m, K);
     p.pw = plan_dw(K, a.n_out, a.cap_m, p.bf);
+    p.wide = wide_bwd_ok(a);
+    if (p.wide) {
+        const WideBwdPlan w = plan_wide_bwd(K, a.n_out, a.cap_m);
+        p.pw.nsplit = static_cast<int>(a.d_a ? w.nsplit_da : w.nsplit);
+    }
     p.din_grid = (a.d_a && a.cap_m > 0) ? static_cast<unsigned>(p.pa.map.blocks()) : 0;
     p.dw_grid = static_cast<unsigned>(p.pw.map.blocks());
     const int64_t work = (K + 1) * (part_ld(a.n_out) / 4);

@@ -28,27 +28,19 @@
 //  * tiles are dealt to the eight XCDs in contiguous ranges of the
 //    row-major tile order, so the workgroups on one XCD share A rows (and
 //    all of W^T) in that XCD's L2;
+//  * tiles are 224 rows high instead of 256 (wavefronts of 112 x 64) where
+//    that fills the CUs' last round better: the kernel's time goes by
+//    rounds of 256 workgroups, so 476 tiles of 224 rows beat 416 of 256;
 //  * the epilogue stages each wavefront's quadrant through LDS 16 rows at a
 //    time and writes row-contiguous 16-byte (bf16) or 32-byte (fp32)
 //    chunks, with bias and ReLU applied on the way.
-#include "internal.h"
+#include "gemm_wide_dev.h"
 
 namespace gnn {
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
-constexpr int kTile = 256;        // output tile edge
-constexpr int kBK = 32;           // reduction chunk
-constexpr int kStages = 4;        // LDS ring
-constexpr int kXcds = 8;
-constexpr int kTileElems = kTile * kBK;  // one operand tile of one chunk, bf16 elements
-
-// element (row r, reduction k) of a staged operand tile
-__device__ __forceinline__ int sw_idx(int r, int k) { return r * kBK + ((((k >> 3) ^ ((r >> 1) & 3))) << 3) + (k & 7); }
+using namespace wide;
 
 // Workgroup layout: NW wavefronts as 2 x (NW / 2), each owning a 128 x WN
 // block of the tile; each wavefront copies CPW 16-row blocks of each
@@ -136,59 +128,46 @@ __device__ __forceinline__ void copy_chunk(const WideArgs &p, const Operands<NW>
 #endif
 }
 
-// Wait until this wavefront's copies of the chunk about to be used have
-// landed (the two later chunks' copies may still be in flight) and its LDS
-// reads are done, then meet the other wavefronts: after it, that chunk is
-// visible in full and the stage the next copies overwrite is no longer
-// read.  The scheduling barriers keep the compiler from moving LDS accesses
-// across.
-template <int WAIT> __device__ __forceinline__ void chunk_barrier() {
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(WAIT);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-}
-
-// MFMAs of one wavefront on one staged chunk: the eight A fragments are
-// read first; the B fragments follow one at a time, each read while the
-// eight MFMAs of the previous one run.
-template <int NW>
-__device__ __forceinline__ void mma_chunk(f32x4 (&acc)[8][Layout<NW>::WJ], const uint16_t *As, const uint16_t *Bs) {
+// MFMAs of one wavefront on one staged chunk: the FI A fragments are read
+// first; the B fragments follow one at a time, each read while the FI MFMAs
+// of the previous one run.
+template <int NW, int FI>
+__device__ __forceinline__ void mma_chunk(f32x4 (&acc)[FI][Layout<NW>::WJ], const uint16_t *As, const uint16_t *Bs) {
     constexpr int WJ = Layout<NW>::WJ;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ra = (wave / Layout<NW>::WC) * 128 + (lane & 15);
+    const int ra = (wave / Layout<NW>::WC) * 16 * FI + (lane & 15);
     const int rb = (wave % Layout<NW>::WC) * Layout<NW>::WN + (lane & 15);
     const int kq = (lane >> 4) * 8;
-    bf16x8 a[8];
+    bf16x8 a[FI];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(As + sw_idx(ra + 16 * i, kq));
+    for (int i = 0; i < FI; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(As + sw_idx(ra + 16 * i, kq));
     bf16x8 b = *reinterpret_cast<const bf16x8 *>(Bs + sw_idx(rb, kq));
 #pragma unroll
     for (int j = 0; j < WJ; ++j) {
         bf16x8 bn = b;
         if (j < WJ - 1) bn = *reinterpret_cast<const bf16x8 *>(Bs + sw_idx(rb + 16 * (j + 1), kq));
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, acc[i][j], 0, 0, 0);
+        for (int i = 0; i < FI; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, acc[i][j], 0, 0, 0);
         b = bn;
     }
-    // scheduling: 9 LDS reads (A fragments and the first B), then per B
-    // fragment one LDS read among its 8 MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 9, 0);
+    // scheduling: FI + 1 LDS reads (A fragments and the first B), then per B
+    // fragment one LDS read among its FI MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, FI + 1, 0);
 #pragma unroll
     for (int j = 0; j < WJ - 1; ++j) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 7, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, FI - 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, FI, 0);
 }
 
-__device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
-    return static_cast<uint32_t>(f32_to_bf16(x)) | (static_cast<uint32_t>(f32_to_bf16(y)) << 16);
-}
-
-template <int NW, class TO>
+// FI A fragments per wavefront: tiles of 32 FI rows (256 or 224) by 256
+// columns.  The copies always fill 256 LDS rows; with 224-row tiles the last
+// 32 are the next tile's rows (or zeros past the capacity) and go unused.
+template <int NW, int FI, class TO>
 __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
+    constexpr int TM = 32 * FI;
     using LY = Layout<NW>;
     constexpr int WJ = LY::WJ;
     __shared__ __attribute__((aligned(16))) uint16_t lds0[2][kTileElems];
@@ -202,13 +181,13 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     if (t >= p.tiles_m * p.tiles_n) return;
     const int64_t tm = t / p.tiles_n, tn = t % p.tiles_n;
     const int64_t M = p.m_dev ? min(*p.m_dev, p.cap_m) : p.cap_m;
-    const int64_t row0 = tm * kTile, col0 = tn * kTile;
+    const int64_t row0 = tm * TM, col0 = tn * kTile;
     if (row0 >= M) return;
     const int64_t nch = p.K / kBK;
 
-    f32x4 acc[8][WJ];
+    f32x4 acc[FI][WJ];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < FI; ++i)
 #pragma unroll
         for (int j = 0; j < WJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -225,16 +204,16 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     for (int64_t c = 0; c < nch; c += 4) {
         chunk_barrier<LY::kWaitTwo>();
         copy_chunk<NW>(p, ops, at(c + 3), lds3[0], lds3[1]);
-        mma_chunk<NW>(acc, lds0[0], lds0[1]);
+        mma_chunk<NW, FI>(acc, lds0[0], lds0[1]);
         chunk_barrier<LY::kWaitTwo>();
         copy_chunk<NW>(p, ops, at(c + 4), lds0[0], lds0[1]);
-        mma_chunk<NW>(acc, lds1[0], lds1[1]);
+        mma_chunk<NW, FI>(acc, lds1[0], lds1[1]);
         chunk_barrier<LY::kWaitTwo>();
         copy_chunk<NW>(p, ops, at(c + 5), lds1[0], lds1[1]);
-        mma_chunk<NW>(acc, lds2[0], lds2[1]);
+        mma_chunk<NW, FI>(acc, lds2[0], lds2[1]);
         chunk_barrier<LY::kWaitTwo>();
         copy_chunk<NW>(p, ops, at(c + 6), lds2[0], lds2[1]);
-        mma_chunk<NW>(acc, lds3[0], lds3[1]);
+        mma_chunk<NW, FI>(acc, lds3[0], lds3[1]);
     }
     chunk_barrier<0x0070>();  // vmcnt(0) lgkmcnt(0): the ring is drained
 
@@ -244,14 +223,14 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     constexpr int WN = LY::WN, LD = WN + 4, CGN = WN / 8, RPP = 64 / CGN;
     float *slab = (wave < NW / 2 ? reinterpret_cast<float *>(&lds0[0][0])
                                  : reinterpret_cast<float *>(&lds1[0][0])) + (wave % (NW / 2)) * 16 * LD;
-    const int64_t wrow0 = row0 + (wave / LY::WC) * 128, wcol0 = col0 + (wave % LY::WC) * WN;
+    const int64_t wrow0 = row0 + (wave / LY::WC) * 16 * FI, wcol0 = col0 + (wave % LY::WC) * WN;
     const int cg = lane % CGN;               // this lane's 8-column group
     const int64_t gc = wcol0 + cg * 8;
     float bv[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) bv[e] = (p.bias && gc + e < p.n_out) ? p.bias[gc + e] : 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < FI; ++i) {
 #pragma unroll
         for (int j = 0; j < WJ; ++j)
 #pragma unroll
@@ -293,6 +272,7 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
 }
 
 constexpr int kWideWaves = 8;
+constexpr int64_t kCus = 256;
 
 }  // namespace
 
@@ -321,16 +301,25 @@ gnn_status launch_wide_fwd(const void *a_self, const void *a_nbr, int64_t k_each
     p.bias = bias;
     p.relu = relu;
     p.out = out;
-    p.tiles_m = ceil_div(cap_m, kTile);
+    // Tile height: 256 or 224 rows, whichever takes the fewest rows x rounds
+    // of the CUs (at 26,624 rows and four column tiles: 416 tiles fill 1.6
+    // rounds of 256 CUs, 476 fill 1.9; the shorter tiles finish sooner).
     p.tiles_n = ceil_div(n_out, kTile);
+    auto cost = [&](int64_t tm) { return ceil_div(ceil_div(cap_m, tm) * p.tiles_n, kCus) * tm; };
+    const int fi = cost(224) < cost(256) ? 7 : 8;
+    p.tiles_m = ceil_div(cap_m, int64_t(32 * fi));
     p.per_xcd = ceil_div(p.tiles_m * p.tiles_n, kXcds);
     const int64_t blocks = p.per_xcd * kXcds;
     GNN_CHECK(blocks <= kMaxGrid, GNN_ESIZE, "update_fwd: cap_m exceeds the grid limit");
     constexpr int NT = Layout<kWideWaves>::kThreads;
-    if (odt == GNN_BF16)
-        wide_fwd_kernel<kWideWaves, uint16_t><<<static_cast<unsigned>(blocks), NT, 0, s>>>(p);
-    else
-        wide_fwd_kernel<kWideWaves, float><<<static_cast<unsigned>(blocks), NT, 0, s>>>(p);
+    const unsigned g = static_cast<unsigned>(blocks);
+    if (odt == GNN_BF16) {
+        if (fi == 8) wide_fwd_kernel<kWideWaves, 8, uint16_t><<<g, NT, 0, s>>>(p);
+        else wide_fwd_kernel<kWideWaves, 7, uint16_t><<<g, NT, 0, s>>>(p);
+    } else {
+        if (fi == 8) wide_fwd_kernel<kWideWaves, 8, float><<<g, NT, 0, s>>>(p);
+        else wide_fwd_kernel<kWideWaves, 7, float><<<g, NT, 0, s>>>(p);
+    }
     GNN_LAUNCHED("update_fwd_wide");
     return GNN_OK;
 }

@@ -745,6 +745,34 @@ def test_update_fwd_wide_layer_matches_oracle(sage, m, cap, ke, n, relu):
     assert np.isnan(got[m:]).all()  # rows past the device count are not written
 
 
+@pytest.mark.parametrize("m,cap", [(16384, 16384), (13300, 13312)])
+def test_update_fwd_wide_layer_tile_heights(m, cap):
+    # K = 1,024, n_out = 1,024: 16,384 rows fill exactly one round of 256
+    # tiles of 256 rows (taken over 224-row tiles, which would need two);
+    # 13,312 rows take 224-row tiles (60 x 4 in one round).  The layer is
+    # row-wise, so 64 sampled rows and the last rows are checked against
+    # the oracle run on just those rows.
+    rng = np.random.default_rng(cap)
+    ke, n = 512, 1024
+    a_s = _act(rng, cap, ke, oracle.BF16)
+    a_n = _act(rng, cap, ke, oracle.BF16)
+    K = 2 * ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(n)).astype(np.float32)
+    wt = torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
+    out = torch.full((cap, n), float("nan"), dtype=torch.bfloat16, device=DEV)
+    m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
+    print(f"[update_fwd wide tiles] m={m} cap={cap}", flush=True)
+    gnn.update_fwd(from_np_act(a_s), from_np_act(a_n), from_np_act(w), from_np_act(b), out, True, gnn.GNN_BF16,
+                   m_dev=m_dev, cap_m=cap, wt=wt)
+    torch.cuda.synchronize()
+    got = oracle.to_float64(to_np_act(out))
+    rows = np.unique(np.concatenate([rng.choice(m, 64, replace=False), np.arange(m - 40, m)]))
+    want = oracle.update_fwd(a_s[rows], a_n[rows], w, b, True, oracle.BF16, oracle.BF16)
+    assert relerr(got[rows], oracle.to_float64(want)) <= 8e-3
+    assert not np.isnan(got[:m]).any() and np.isnan(got[m:]).all()
+
+
 @pytest.mark.parametrize("m,ke,n", SHAPES)
 @pytest.mark.parametrize("sage", [True, False])
 @pytest.mark.parametrize("code", [oracle.F32, oracle.BF16])
@@ -875,6 +903,56 @@ def test_update_bwd_parity(m, ke, n, sage, code):
     assert relerr(dw.cpu().numpy(), dw_w) <= tol
     assert relerr(db.cpu().numpy(), db_w) <= 1e-5
     assert relerr(da.cpu().numpy(), da_w) <= tol
+
+
+@pytest.mark.parametrize("sage,m,cap,ke,n,want_da,want_db", [
+    (True, 1664, 1664, 768, 1024, True, True),   # the host-table first layer at 1/16 of its 26,624 rows
+    (True, 1000, 4096, 768, 520, True, True),    # device rows far below capacity (most splits empty); n_out % 32 != 0
+    (False, 777, 800, 600, 512, True, False),    # GCN with K = 600: the last K tile runs past K; no db
+    (True, 300, 300, 512, 1024, False, True),    # dW alone (a first layer)
+    (False, 1, 64, 512, 512, True, True),        # a single row
+])
+def test_update_bwd_wide_layer_matches_oracle(sage, m, cap, ke, n, want_da, want_db):
+    # wide layers (K and n_out >= 512, bf16) take the 256 x 256 matrix-core
+    # tiles: dA with G converted on its way to LDS, dW from transposing LDS
+    # reads with its rows split across workgroups.  Rows past the device
+    # count hold NaN and must reach no output; the workspace starts as NaN
+    # bit patterns; a second call must repeat the first bit for bit.
+    rng = np.random.default_rng(m + ke + n + sage)
+    a_s = _act(rng, cap, ke, oracle.BF16)
+    a_n = _act(rng, cap, ke, oracle.BF16) if sage else None
+    K = (2 if sage else 1) * ke
+    w = (rng.standard_normal((K, n)) / np.sqrt(K)).astype(np.float32)
+    g = rng.standard_normal((cap, n)).astype(np.float32)
+    dw_w, db_w, da_w = oracle.update_bwd(a_s[:m], a_n[:m] if sage else None, w, g[:m], oracle.BF16, want_da=True)
+    a_s[m:] = 0x7FC0  # bf16 NaN
+    if sage:
+        a_n[m:] = 0x7FC0
+    g[m:] = np.nan
+    nb = gnn._sz()
+    gnn._check(gnn.lib().gnn_update_bwd_workspace_size(K, n, cap, gnn.GNN_BF16, gnn.ctypes.byref(nb)))
+    ws = torch.full((nb.value,), 0xFF, dtype=torch.uint8, device=DEV)
+    m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
+    args = (from_np_act(a_s), from_np_act(a_n) if sage else None, from_np_act(w), from_np_act(g))
+    print(f"[update_bwd wide] sage={sage} m={m} cap={cap} ke={ke} n={n} da={want_da} db={want_db}", flush=True)
+    outs = []
+    for _ in range(2):
+        dw = torch.full((K, n), float("nan"), device=DEV)
+        db = torch.full((n,), float("nan"), device=DEV) if want_db else None
+        da = torch.full((cap, K), 5.0, device=DEV) if want_da else None
+        gnn.update_bwd(*args, dw, db, da, gnn.GNN_BF16, m_dev=m_dev, cap_m=cap, ws=ws)
+        torch.cuda.synchronize()
+        outs.append([t.cpu() for t in (dw, db, da) if t is not None])
+    dw, *rest = outs[0]
+    assert relerr(dw.numpy(), dw_w) <= 8e-3
+    if want_db:
+        assert relerr(rest.pop(0).numpy(), db_w) <= 1e-5
+    if want_da:
+        da = rest.pop(0).numpy()
+        assert relerr(da[:m], da_w) <= 8e-3
+        assert np.all(da[m:] == 5.0)  # rows past the device count untouched
+    for x, y in zip(outs[0], outs[1]):
+        assert torch.equal(x.view(torch.int32), y.view(torch.int32))
 
 
 # ---------------------------------------------------------------------------
