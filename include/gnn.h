@@ -370,7 +370,8 @@ gnn_status gnn_update_fwd(const void *a_self, const void *a_nbr, gnn_dtype adt, 
  *   fp32 partials go to ws and a second kernel sums them in split order, so
  *   results are bitwise reproducible.  Layers with K and n_out both >= 512
  *   split the rows over more workgroups, so their workspace is larger (up
- *   to 64 partial copies of dW).  ws [device] must be 256-byte aligned
+ *   to 64 partial copies of dW; in bf16 also a bf16 copy of W that dA
+ *   reads).  ws [device] must be 256-byte aligned
  *   and hold gnn_update_bwd_workspace_size bytes; no state is kept in it
  *   between calls; calls sharing it must not overlap. */
 gnn_status gnn_update_bwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes);
