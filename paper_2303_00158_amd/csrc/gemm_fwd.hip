@@ -176,7 +176,11 @@ void fwd_by_tile(const FwdLaunch &L, int tile, bool vec_a, int wsrc, bool vec_o)
 
 size_t update_fwd_ws_bytes(int64_t k, int64_t n_out, int64_t cap_m, int gemm_dt) {
     const FwdPlan p = plan_fwd(cap_m, n_out, k, gemm_dt == GNN_BF16);
-    return round_up(part_bytes(p, cap_m, n_out), 256);
+    size_t bytes = round_up(part_bytes(p, cap_m, n_out), 256);
+    // layers the wide kernel may take (its split's partial tiles)
+    if (gemm_dt == GNN_BF16 && k >= 512 && n_out >= 512 && n_out % 8 == 0 && k % 128 == 0)
+        bytes = std::max(bytes, wide_fwd_ws_bytes(n_out, cap_m));
+    return bytes;
 }
 
 gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int64_t k_each, const int64_t *m_dev,
@@ -201,7 +205,7 @@ gnn_status launch_update_fwd(const void *a_self, const void *a_nbr, int adt, int
     // Wide layers (K and n_out of 512 and more) are bound by the matrix
     // cores: 256 x 256 tiles with operands copied straight to LDS.
     if (wide_fwd_ok(a_self, a_nbr, adt, k_each, cap_m, n_out, wt, gemm_dt, out))
-        return launch_wide_fwd(a_self, a_nbr, k_each, m_dev, cap_m, wt, bias, n_out, relu, out, odt, s);
+        return launch_wide_fwd(a_self, a_nbr, k_each, m_dev, cap_m, wt, bias, n_out, relu, out, odt, ws, s);
     const int64_t K = a_nbr ? 2 * k_each : k_each;
     const bool bf = gemm_dt == GNN_BF16;
     FwdPlan p = plan_fwd(cap_m, n_out, K, bf);

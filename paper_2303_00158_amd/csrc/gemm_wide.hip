@@ -66,7 +66,26 @@ struct WideArgs {
     int relu;
     void *out;                // cap_m x n_out, bf16 or fp32
     int64_t tiles_m, tiles_n, per_xcd;
+    float *part;              // split partial tiles, or null (no split)
+    int64_t grid;             // the launch's workgroups
 };
+
+constexpr int64_t kCus = 256;
+
+// Reduction splits when only T tiles hold rows (the row count is on the
+// device): none unless the tiles fill at most a quarter of the CUs (the
+// fp32 partials cost more than a split saves above that: at 6,000 rows of
+// K = 1,536 two splits took 98 us against 86), else the largest divisor S
+// of the q four-chunk groups with S T workgroups in one round of the CUs
+// (and in the grid).
+__host__ __device__ inline int wide_split(int64_t T, int64_t q, int64_t grid) {
+    if (T > kCus / 4) return 1;
+    const int64_t lim = (grid < kCus ? grid : kCus) / (T > 0 ? T : 1);
+    int best = 1;
+    for (int64_t sp = 2; sp <= lim && sp <= q; ++sp)
+        if (q % sp == 0) best = static_cast<int>(sp);
+    return best;
+}
 
 // Buffer descriptors over the operands: a load past the buffer's bytes
 // returns zeros, so rows beyond the capacities need no clamping (they only
@@ -175,15 +194,30 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     __shared__ __attribute__((aligned(16))) uint16_t lds2[2][kTileElems];
     __shared__ __attribute__((aligned(16))) uint16_t lds3[2][kTileElems];
     // tile of this workgroup: XCD x = blockIdx % 8 takes tiles
-    // [x * per_xcd, (x + 1) * per_xcd) of the row-major tile order
+    // [x * per_xcd, (x + 1) * per_xcd) of the row-major tile order.  With a
+    // split (few tiles hold rows), work item w = s T + t is split s of tile
+    // t, dealt to the XCDs the same way.
     const int64_t b = blockIdx.x;
-    const int64_t t = (b % kXcds) * p.per_xcd + b / kXcds;
-    if (t >= p.tiles_m * p.tiles_n) return;
-    const int64_t tm = t / p.tiles_n, tn = t % p.tiles_n;
     const int64_t M = p.m_dev ? min(*p.m_dev, p.cap_m) : p.cap_m;
+    const int64_t T = ceil_div(M, int64_t(TM)) * p.tiles_n;
+    const int64_t nch_all = p.K / kBK;
+    const int S = p.part ? wide_split(T, nch_all / 4, p.grid) : 1;
+    int64_t t, c_beg = 0, nch = nch_all;
+    int split = 0;
+    if (S == 1) {
+        t = (b % kXcds) * p.per_xcd + b / kXcds;
+        if (t >= p.tiles_m * p.tiles_n) return;
+    } else {
+        const int64_t w = (b % kXcds) * ceil_div(T * S, int64_t(kXcds)) + b / kXcds;
+        if (w >= T * S) return;
+        split = static_cast<int>(w / T);
+        t = w % T;
+        nch = nch_all / S;
+        c_beg = split * nch;
+    }
+    const int64_t tm = t / p.tiles_n, tn = t % p.tiles_n;
     const int64_t row0 = tm * TM, col0 = tn * kTile;
     if (row0 >= M) return;
-    const int64_t nch = p.K / kBK;
 
     f32x4 acc[FI][WJ];
 #pragma unroll
@@ -196,8 +230,8 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     // (K % 128 == 0), so the loop body takes four chunks with no exit
     // between them; copies past the last chunk re-read it into a stage
     // nobody reads any more, so the copies need no branch.
-    const int64_t last = (nch - 1) * kBK;
-    auto at = [&](int64_t c) { return min(c * kBK, last); };
+    const int64_t last = (c_beg + nch - 1) * kBK;
+    auto at = [&](int64_t c) { return min((c_beg + c) * kBK, last); };
     copy_chunk<NW>(p, ops, at(0), lds0[0], lds0[1]);
     copy_chunk<NW>(p, ops, at(1), lds1[0], lds1[1]);
     copy_chunk<NW>(p, ops, at(2), lds2[0], lds2[1]);
@@ -244,12 +278,22 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
             const float4 v0 = *reinterpret_cast<const float4 *>(slab + r * LD + cg * 8);
             const float4 v1 = *reinterpret_cast<const float4 *>(slab + r * LD + cg * 8 + 4);
             float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            const int64_t gr = wrow0 + i * 16 + r;
+            if (S > 1) {
+                // the split's fp32 partial tile (TM x 256, row-major); bias
+                // and activation come with the sum of the splits
+                if (gr < M && gc < p.n_out) {
+                    float *o = p.part + ((split * T + t) * TM + (gr - row0)) * kTile + (gc - col0);
+                    *reinterpret_cast<float4 *>(o) = make_float4(v[0], v[1], v[2], v[3]);
+                    *reinterpret_cast<float4 *>(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+                }
+                continue;
+            }
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 v[e] += bv[e];
                 if (p.relu) v[e] = fmaxf(v[e], 0.f);
             }
-            const int64_t gr = wrow0 + i * 16 + r;
             if (gr < M && gc < p.n_out) {
                 if constexpr (sizeof(TO) == 2) {
                     uint4 o;
@@ -271,8 +315,52 @@ __global__ void __launch_bounds__(NW * 64, 1) wide_fwd_kernel(WideArgs p) {
     }
 }
 
+// out = act(sum over the splits, in order, of the partial tiles + bias) for
+// the rows held on the device, when the forward kernel split (it decides the
+// same way from the same row count); else nothing.
+template <class TO>
+__global__ void __launch_bounds__(256) wide_fwd_reduce_kernel(WideArgs p, int64_t tm_rows) {
+    const int64_t M = p.m_dev ? min(*p.m_dev, p.cap_m) : p.cap_m;
+    const int64_t T = ceil_div(M, tm_rows) * p.tiles_n;
+    const int S = wide_split(T, p.K / kBK / 4, p.grid);
+    if (S == 1) return;
+    const int64_t groups = p.n_out / 8;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < M * groups;
+         i += static_cast<int64_t>(gridDim.x) * 256) {
+        const int64_t r = i / groups, c = (i - r * groups) * 8;
+        const int64_t t = (r / tm_rows) * p.tiles_n + c / kTile;
+        const float *src = p.part + (t * tm_rows + r % tm_rows) * kTile + c % kTile;
+        const int64_t stride = T * tm_rows * kTile;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
+        for (int sp = 0; sp < S; ++sp) {
+            const float4 x = *reinterpret_cast<const float4 *>(src + sp * stride);
+            const float4 y = *reinterpret_cast<const float4 *>(src + sp * stride + 4);
+            v[0] += x.x; v[1] += x.y; v[2] += x.z; v[3] += x.w;
+            v[4] += y.x; v[5] += y.y; v[6] += y.z; v[7] += y.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            v[e] += p.bias ? p.bias[c + e] : 0.f;
+            if (p.relu) v[e] = fmaxf(v[e], 0.f);
+        }
+        if constexpr (sizeof(TO) == 2) {
+            uint4 o;
+            o.x = pack_bf16(v[0], v[1]);
+            o.y = pack_bf16(v[2], v[3]);
+            o.z = pack_bf16(v[4], v[5]);
+            o.w = pack_bf16(v[6], v[7]);
+            *reinterpret_cast<uint4 *>(static_cast<uint16_t *>(p.out) + r * p.n_out + c) = o;
+        } else {
+            float *o = static_cast<float *>(p.out) + r * p.n_out + c;
+            *reinterpret_cast<float4 *>(o) = make_float4(v[0], v[1], v[2], v[3]);
+            *reinterpret_cast<float4 *>(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        }
+    }
+}
+
 constexpr int kWideWaves = 8;
-constexpr int64_t kCus = 256;
 
 }  // namespace
 
@@ -286,9 +374,37 @@ bool wide_fwd_ok(const void *a_self, const void *a_nbr, int adt, int64_t k_each,
            aligned(a_nbr, 16) && aligned(wt, 16) && aligned(out, 16);
 }
 
+namespace {
+
+// Tile height and grid: 256 or 224 rows, whichever takes the fewest rows x
+// rounds of the CUs (at 26,624 rows and four column tiles: 416 tiles fill
+// 1.6 rounds of 256 CUs, 476 fill 1.9; the shorter tiles finish sooner).
+struct WideGrid {
+    int fi;
+    int64_t tiles_m, tiles_n, per_xcd, blocks;
+};
+WideGrid wide_grid(int64_t cap_m, int64_t n_out) {
+    WideGrid g{};
+    g.tiles_n = ceil_div(n_out, kTile);
+    auto cost = [&](int64_t tm) { return ceil_div(ceil_div(cap_m, tm) * g.tiles_n, kCus) * tm; };
+    g.fi = cost(224) < cost(256) ? 7 : 8;
+    g.tiles_m = ceil_div(cap_m, int64_t(32 * g.fi));
+    g.per_xcd = ceil_div(g.tiles_m * g.tiles_n, kXcds);
+    g.blocks = g.per_xcd * kXcds;
+    return g;
+}
+
+}  // namespace
+
+size_t wide_fwd_ws_bytes(int64_t n_out, int64_t cap_m) {
+    // at most one round of the CUs (or the grid) of partial tiles
+    const WideGrid g = wide_grid(cap_m, n_out);
+    return round_up(static_cast<size_t>(std::min<int64_t>(kCus, g.blocks)) * 32 * g.fi * kTile * 4, size_t(256));
+}
+
 gnn_status launch_wide_fwd(const void *a_self, const void *a_nbr, int64_t k_each, const int64_t *m_dev,
                            int64_t cap_m, const uint16_t *wt, const float *bias, int64_t n_out, int relu, void *out,
-                           int odt, hipStream_t s) {
+                           int odt, void *ws, hipStream_t s) {
     WideArgs p{};
     p.a0 = static_cast<const uint16_t *>(a_self);
     p.a1 = static_cast<const uint16_t *>(a_nbr);
@@ -301,26 +417,36 @@ gnn_status launch_wide_fwd(const void *a_self, const void *a_nbr, int64_t k_each
     p.bias = bias;
     p.relu = relu;
     p.out = out;
-    // Tile height: 256 or 224 rows, whichever takes the fewest rows x rounds
-    // of the CUs (at 26,624 rows and four column tiles: 416 tiles fill 1.6
-    // rounds of 256 CUs, 476 fill 1.9; the shorter tiles finish sooner).
-    p.tiles_n = ceil_div(n_out, kTile);
-    auto cost = [&](int64_t tm) { return ceil_div(ceil_div(cap_m, tm) * p.tiles_n, kCus) * tm; };
-    const int fi = cost(224) < cost(256) ? 7 : 8;
-    p.tiles_m = ceil_div(cap_m, int64_t(32 * fi));
-    p.per_xcd = ceil_div(p.tiles_m * p.tiles_n, kXcds);
-    const int64_t blocks = p.per_xcd * kXcds;
-    GNN_CHECK(blocks <= kMaxGrid, GNN_ESIZE, "update_fwd: cap_m exceeds the grid limit");
+    const WideGrid g = wide_grid(cap_m, n_out);
+    p.tiles_m = g.tiles_m;
+    p.tiles_n = g.tiles_n;
+    p.per_xcd = g.per_xcd;
+    p.grid = g.blocks;
+    GNN_CHECK(g.blocks <= kMaxGrid, GNN_ESIZE, "update_fwd: cap_m exceeds the grid limit");
+    // With a workspace and the row count on the device, the reduction is
+    // split when few tiles hold rows: the kernel decides from the row count,
+    // and a second kernel sums the splits (or does nothing when there were
+    // none).  A row count known here (cap_m) never leaves room for a split:
+    // the grid has no more workgroups than tiles.
+    const int64_t tm_rows = 32 * g.fi;
+    const bool split = ws && m_dev;
+    p.part = split ? static_cast<float *>(ws) : nullptr;
     constexpr int NT = Layout<kWideWaves>::kThreads;
-    const unsigned g = static_cast<unsigned>(blocks);
+    const unsigned gb = static_cast<unsigned>(g.blocks);
     if (odt == GNN_BF16) {
-        if (fi == 8) wide_fwd_kernel<kWideWaves, 8, uint16_t><<<g, NT, 0, s>>>(p);
-        else wide_fwd_kernel<kWideWaves, 7, uint16_t><<<g, NT, 0, s>>>(p);
+        if (g.fi == 8) wide_fwd_kernel<kWideWaves, 8, uint16_t><<<gb, NT, 0, s>>>(p);
+        else wide_fwd_kernel<kWideWaves, 7, uint16_t><<<gb, NT, 0, s>>>(p);
     } else {
-        if (fi == 8) wide_fwd_kernel<kWideWaves, 8, float><<<g, NT, 0, s>>>(p);
-        else wide_fwd_kernel<kWideWaves, 7, float><<<g, NT, 0, s>>>(p);
+        if (g.fi == 8) wide_fwd_kernel<kWideWaves, 8, float><<<gb, NT, 0, s>>>(p);
+        else wide_fwd_kernel<kWideWaves, 7, float><<<gb, NT, 0, s>>>(p);
     }
     GNN_LAUNCHED("update_fwd_wide");
+    if (split) {
+        const unsigned rg = static_cast<unsigned>(std::min<int64_t>(ceil_div(cap_m * (n_out / 8), int64_t(256)), 512));
+        if (odt == GNN_BF16) wide_fwd_reduce_kernel<uint16_t><<<rg, 256, 0, s>>>(p, tm_rows);
+        else wide_fwd_reduce_kernel<float><<<rg, 256, 0, s>>>(p, tm_rows);
+        GNN_LAUNCHED("update_fwd_wide_reduce");
+    }
     return GNN_OK;
 }
 

@@ -204,7 +204,9 @@ bool wide_fwd_ok(const void *a_self, const void *a_nbr, int adt, int64_t k_each,
                  const uint16_t *wt, int gemm_dt, const void *out);
 gnn_status launch_wide_fwd(const void *a_self, const void *a_nbr, int64_t k_each, const int64_t *m_dev,
                            int64_t cap_m, const uint16_t *wt, const float *bias, int64_t n_out, int relu, void *out,
-                           int odt, hipStream_t s);
+                           int odt, void *ws, hipStream_t s);
+// Workspace of the wide forward's split reduction (fp32 partial tiles).
+size_t wide_fwd_ws_bytes(int64_t n_out, int64_t cap_m);
 // wt = bf16(w^T) for a K x n row-major w.
 gnn_status launch_shadow_sync(const float *w, int64_t K, int64_t n, uint16_t *wt, hipStream_t s);
 size_t softmax_ce_ws_bytes(int64_t b);

@@ -745,15 +745,21 @@ def test_update_fwd_wide_layer_matches_oracle(sage, m, cap, ke, n, relu):
     assert np.isnan(got[m:]).all()  # rows past the device count are not written
 
 
-@pytest.mark.parametrize("m,cap", [(16384, 16384), (13300, 13312)])
-def test_update_fwd_wide_layer_tile_heights(m, cap):
-    # K = 1,024, n_out = 1,024: 16,384 rows fill exactly one round of 256
+@pytest.mark.parametrize("m,cap,ke", [(16384, 16384, 512), (13300, 13312, 512), (3239, 26624, 768),
+                                      (2200, 26624, 768), (1000, 26624, 512), (6000, 26624, 768)])
+def test_update_fwd_wide_layer_tile_heights(m, cap, ke):
+    # n_out = 1,024.  16,384 rows (K = 1,024) fill exactly one round of 256
     # tiles of 256 rows (taken over 224-row tiles, which would need two);
-    # 13,312 rows take 224-row tiles (60 x 4 in one round).  The layer is
+    # 13,312 rows take 224-row tiles (60 x 4 in one round).  With the row
+    # count on the device far below the capacity (26,624 rows: 476 tiles of
+    # 224 rows), the few tiles holding rows split their reduction: 60 tiles
+    # of K = 1,536 in 4 splits (the host-table model's first layer at 3,239
+    # rows), 40 tiles in 6, 20 tiles of K = 1,024 in 8; 6,000 rows (108
+    # tiles) do not split, though the summing kernel runs.  The layer is
     # row-wise, so 64 sampled rows and the last rows are checked against
     # the oracle run on just those rows.
-    rng = np.random.default_rng(cap)
-    ke, n = 512, 1024
+    rng = np.random.default_rng(cap + m)
+    n = 1024
     a_s = _act(rng, cap, ke, oracle.BF16)
     a_n = _act(rng, cap, ke, oracle.BF16)
     K = 2 * ke
@@ -762,7 +768,7 @@ def test_update_fwd_wide_layer_tile_heights(m, cap):
     wt = torch.from_numpy(np.ascontiguousarray(w.T)).to(DEV).to(torch.bfloat16)
     out = torch.full((cap, n), float("nan"), dtype=torch.bfloat16, device=DEV)
     m_dev = torch.tensor([m], dtype=torch.int64, device=DEV)
-    print(f"[update_fwd wide tiles] m={m} cap={cap}", flush=True)
+    print(f"[update_fwd wide tiles] m={m} cap={cap} k_each={ke}", flush=True)
     gnn.update_fwd(from_np_act(a_s), from_np_act(a_n), from_np_act(w), from_np_act(b), out, True, gnn.GNN_BF16,
                    m_dev=m_dev, cap_m=cap, wt=wt)
     torch.cuda.synchronize()
