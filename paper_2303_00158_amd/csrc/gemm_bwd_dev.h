@@ -153,10 +153,17 @@ struct DweightJob {
     }
 };
 
+// Lanes that share one output float4 of the split reduction: one per 16
+// splits (up to 64 splits; a lane's 16 loads are one round trip).
+__host__ __device__ inline int reduce_lanes(int nsplit) { return nsplit > 32 ? 4 : nsplit > 16 ? 2 : 1; }
+
 // dw = sum over splits of the partials (db from row K); then, when w_upd /
 // b_upd are given, w_upd -= lr * dw and b_upd -= lr * db, and wt_upd (if
-// given) = bf16(w_upd^T).  The values an update reads are loaded before the
-// partials, so each thread waits once.
+// given) = bf16(w_upd^T).  The splits are summed in blocks of 16, each in
+// split order by its own lane, and the blocks' sums are added in block
+// order by the first lane (a fixed order, so results are reproducible).
+// The values an update reads are loaded before the partials, so each
+// thread waits once.
 template <bool VO>
 struct DwReduceJob {
     const float *part;
@@ -168,13 +175,33 @@ struct DwReduceJob {
     __device__ void run(int64_t blk, int64_t nblk) const {
         const int64_t ldp = part_ld(n_out), chunks = ldp / 4;
         const int64_t rows = K + (db ? 1 : 0);
-        for (int64_t t = blk * 256 + threadIdx.x; t < rows * chunks; t += nblk * 256) {
-            const int64_t r = t / chunks, c = (t % chunks) * 4;
+        const int G = reduce_lanes(nsplit);  // divides 64: a group's lanes share a wavefront
+        const int64_t stride = (K + 1) * ldp;
+        for (int64_t t = blk * 256 + threadIdx.x; t < rows * chunks * G; t += nblk * 256) {
+            const int64_t item = t / G;
+            const int j = static_cast<int>(t % G);
+            const int64_t r = item / chunks, c = (item % chunks) * 4;
             const bool brow = r == K;
             const int64_t base = brow ? 0 : r * n_out;
             float *upd = brow ? b_upd : w_upd;
-            const float4 old = upd ? load4_clamped<VO>(upd, base, c, n_out) : make_float4(0.f, 0.f, 0.f, 0.f);
-            const float4 s = sum_splits(part + r * ldp + c, (K + 1) * ldp, nsplit);
+            const float4 old =
+                (upd && j == 0) ? load4_clamped<VO>(upd, base, c, n_out) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const int s0 = 16 * j;
+            float4 s = nsplit > s0 ? sum_splits(part + r * ldp + c + s0 * stride, stride, min(16, nsplit - s0))
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+            if (G > 1) {
+                const int lane0 = (threadIdx.x & 63) - j;
+                float4 tot = make_float4(__shfl(s.x, lane0, 64), __shfl(s.y, lane0, 64), __shfl(s.z, lane0, 64),
+                                         __shfl(s.w, lane0, 64));
+                for (int k = 1; k < G; ++k) {
+                    tot.x += __shfl(s.x, lane0 + k, 64);
+                    tot.y += __shfl(s.y, lane0 + k, 64);
+                    tot.z += __shfl(s.z, lane0 + k, 64);
+                    tot.w += __shfl(s.w, lane0 + k, 64);
+                }
+                s = tot;
+            }
+            if (j != 0) continue;
             store4_masked<VO>(brow ? db : dw, base, c, n_out, s);
             if (upd) {
                 const float4 nw = make_float4(old.x - lr * s.x, old.y - lr * s.y, old.z - lr * s.z, old.w - lr * s.w);
@@ -283,7 +310,7 @@ inline Plan plan(const Args &a) {
     }
     p.din_grid = (a.d_a && a.cap_m > 0) ? static_cast<unsigned>(p.pa.map.blocks()) : 0;
     p.dw_grid = static_cast<unsigned>(p.pw.map.blocks());
-    const int64_t work = (K + 1) * (part_ld(a.n_out) / 4);
+    const int64_t work = (K + 1) * (part_ld(a.n_out) / 4) * reduce_lanes(p.pw.nsplit);
     p.red_grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(work, 256), 1 << 20));
     return p;
 }
