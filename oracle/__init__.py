@@ -69,6 +69,11 @@ def lib():
             L.orc_gather.argtypes = [vp, ctypes.c_int, i64, i64, vp, i64, vp, ctypes.c_int]
             L.orc_aggregate_fwd.restype = None
             L.orc_aggregate_fwd.argtypes = [ctypes.c_int, i64, vp, vp, vp, vp, ctypes.c_int, i64, vp, ctypes.c_int]
+            L.orc_aggregate_fwd_max.restype = None
+            L.orc_aggregate_fwd_max.argtypes = [i64, vp, vp, vp, ctypes.c_int, i64, vp, ctypes.c_int, vp]
+            L.orc_aggregate_bwd_max.restype = None
+            L.orc_aggregate_bwd_max.argtypes = [i64, i64, vp, vp, ctypes.c_int, i64, vp, ctypes.c_int, vp,
+                                                ctypes.c_int]
             L.orc_aggregate_bwd.restype = None
             L.orc_aggregate_bwd.argtypes = [ctypes.c_int, i64, i64, vp, vp, vp, vp, ctypes.c_int, i64,
                                             vp, ctypes.c_int, vp, ctypes.c_int]
@@ -261,6 +266,32 @@ def aggregate_bwd(kind: int, blk: Block, src_norm, d_a: np.ndarray, f: int, h_be
     hb = np.ascontiguousarray(h_below) if h_below is not None else None
     lib().orc_aggregate_bwd(kind, blk.n_dst, blk.n_src, _p(blk.rowptr), _p(blk.col), _p(sn), _p(d_a), _code(d_a), f,
                             _p(hb), _code(hb) if hb is not None else F32, _p(out), out_code)
+    return out
+
+
+def aggregate_fwd_max(blk: Block, h: np.ndarray, out_code: int):
+    """GraphSAGE's max aggregator: (out, argmax) with argmax the winning
+    source of each output element (-1 for rows without neighbours)."""
+    h = np.ascontiguousarray(h)
+    f = h.shape[1]
+    assert h.shape[0] >= blk.n_src
+    out = np.zeros((blk.n_dst, f), dtype=_np_dtype(out_code))
+    arg = np.zeros((blk.n_dst, f), dtype=np.int32)
+    lib().orc_aggregate_fwd_max(blk.n_dst, _p(blk.rowptr), _p(blk.col), _p(h), _code(h), f, _p(out), out_code,
+                                _p(arg))
+    return out, arg
+
+
+def aggregate_bwd_max(blk: Block, argmax: np.ndarray, d_a: np.ndarray, f: int, h_below: Optional[np.ndarray],
+                      out_code: int) -> np.ndarray:
+    """Backward of the max aggregator from its argmax table; d_a has 2f
+    columns (self part, then max part)."""
+    d_a = np.ascontiguousarray(d_a)
+    argmax = _c(argmax, np.int32)
+    out = np.zeros((blk.n_src, f), dtype=_np_dtype(out_code))
+    hb = np.ascontiguousarray(h_below) if h_below is not None else None
+    lib().orc_aggregate_bwd_max(blk.n_dst, blk.n_src, _p(argmax), _p(d_a), _code(d_a), f, _p(hb),
+                                _code(hb) if hb is not None else F32, _p(out), out_code)
     return out
 
 

@@ -1,5 +1,6 @@
 /*
- * CPU oracle for sampled mini-batch GNN training (GCN and GraphSAGE-mean).
+ * CPU oracle for sampled mini-batch GNN training (GCN and GraphSAGE with the
+ * mean aggregator; the max aggregator's forward and backward too).
  *
  * TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
  * benchmark's CPU-baseline leg load this library.  The GPU product path never
@@ -396,6 +397,61 @@ void orc_aggregate_bwd(int kind, int64_t n_dst, int64_t n_src, const int64_t *br
             }
         }
     }
+    for (int64_t j = 0; j < n_src; ++j)
+        for (int64_t c = 0; c < f; ++c) {
+            double v = acc[j * f + c];
+            if (h_below && !(load_elem(h_below, hbdt, j * f + c) > 0.0)) v = 0.0;
+            store_elem(d_src, odt, j * f + c, v);
+        }
+    free(acc);
+}
+
+/* GraphSAGE with the max aggregator (Section II-A names mean, max and LSTM
+ * as aggregation operators):
+ *   out[i, c] = max over row i's sampled neighbours u of h[u, c]
+ * (zero, and argmax -1, for a row with no neighbours).  The row's first edge
+ * holds the running maximum and a later edge replaces it only when strictly
+ * greater, so a tie, and a duplicate edge, goes to the earliest edge;
+ * argmax[i, c] is that edge's source (its local id).  The comparison is on
+ * the stored values (no rounding); the maximum is narrowed to out's dtype. */
+void orc_aggregate_fwd_max(int64_t n_dst, const int64_t *brow, const int32_t *bcol, const void *h, int hdt,
+                           int64_t f, void *out, int odt, int32_t *argmax)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n_dst; ++i)
+        for (int64_t c = 0; c < f; ++c) {
+            double best = 0.0;
+            int32_t arg = -1;
+            for (int64_t e = brow[i]; e < brow[i + 1]; ++e) {
+                double v = load_elem(h, hdt, (int64_t)bcol[e] * f + c);
+                if (arg < 0 || v > best) {
+                    best = v;
+                    arg = bcol[e];
+                }
+            }
+            store_elem(out, odt, i * f + c, best);
+            argmax[i * f + c] = arg;
+        }
+}
+
+/* Backward of the max aggregator (Section II-B: the backward pass applies the
+ * forward operators in reverse).  The maximum passes its gradient to the
+ * source that won it; the concatenation's self part passes to the
+ * destination itself (dA has 2f columns: self part, then max part):
+ *   dH[j, c] = [j < n_dst] dA[j, c] + sum_{i: argmax[i, c] = j} dA[i, f + c]
+ *   G[j, c]  = dH[j, c] * 1[h_below[j, c] > 0]   (when h_below is given)
+ * The sum scatters over the argmax table; it does not use the block. */
+void orc_aggregate_bwd_max(int64_t n_dst, int64_t n_src, const int32_t *argmax, const void *d_a, int adt, int64_t f,
+                           const void *h_below, int hbdt, void *d_src, int odt)
+{
+    double *acc = (double *)calloc((size_t)(n_src * f > 0 ? n_src * f : 1), sizeof(double));
+    for (int64_t j = 0; j < n_dst; ++j)
+        for (int64_t c = 0; c < f; ++c) acc[j * f + c] = load_elem(d_a, adt, j * 2 * f + c);
+    for (int64_t i = 0; i < n_dst; ++i)
+        for (int64_t c = 0; c < f; ++c) {
+            int32_t j = argmax[i * f + c];
+            if (j >= 0) acc[(int64_t)j * f + c] += load_elem(d_a, adt, i * 2 * f + f + c);
+        }
     for (int64_t j = 0; j < n_src; ++j)
         for (int64_t c = 0; c < f; ++c) {
             double v = acc[j * f + c];

@@ -289,6 +289,79 @@ def test_aggregate_fwd_invariants():
         assert got[i] == float(np.float32(sn[i] * sn[i]))
 
 
+@pytest.mark.parametrize("seed,n_dst", [(0, 30), (1, 30), (2, 30), (3, 80)])
+def test_aggregate_fwd_max_is_numpy_max_with_first_argmax(seed, n_dst):
+    # small integers force ties; the multigraph repeats edges.  The maximum
+    # is numpy's, the argmax the source of numpy's first maximal position
+    # in the row's edge order; rows without neighbours (the isolated
+    # vertices, all destinations when n_dst = 80) give 0 and -1.
+    rng, _, _, blk, _ = _random_block(seed + 40, n_dst=n_dst)
+    f = 5
+    h = rng.integers(-3, 4, size=(blk.n_src, f)).astype(np.float64)
+    out, arg = oracle.aggregate_fwd_max(blk, h, oracle.F64)
+    deg = np.diff(blk.rowptr)
+    assert (deg > 1).any() and (n_dst < 80 or (deg == 0).any())
+    for i in range(blk.n_dst):
+        cols = blk.col[blk.rowptr[i]:blk.rowptr[i + 1]]
+        if cols.size == 0:
+            assert np.all(out[i] == 0) and np.all(arg[i] == -1)
+            continue
+        np.testing.assert_array_equal(out[i], h[cols].max(axis=0))
+        np.testing.assert_array_equal(arg[i], cols[np.argmax(h[cols], axis=0)])
+    # bf16 storage: the maximum of the stored values, bit for bit
+    hb = oracle.f32_to_bf16_bits(rng.standard_normal((blk.n_src, f)).astype(np.float32))
+    outb, argb = oracle.aggregate_fwd_max(blk, hb, oracle.BF16)
+    hv = oracle.to_float64(hb)
+    for i in np.nonzero(deg)[0]:
+        cols = blk.col[blk.rowptr[i]:blk.rowptr[i + 1]]
+        best = cols[np.argmax(hv[cols], axis=0)]
+        np.testing.assert_array_equal(argb[i], best)
+        np.testing.assert_array_equal(outb[i], hb[best, np.arange(f)])
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_aggregate_bwd_max_adjoint_duplicates_and_mask(seed):
+    # With the argmax fixed the forward is the linear map H -> [S H || P H]
+    # (P selects the winning source of each element), so the backward must
+    # be its transpose: <[S H || P H], dA> = <H, dH>.  Distinct values make
+    # the selection stable, so a small step along any source element moves
+    # the output by exactly dH's value there.
+    rng, _, _, blk, _ = _random_block(seed + 50, n_dst=25)
+    f = 6
+    h = rng.standard_normal((blk.n_src, f))
+    da = rng.standard_normal((blk.n_dst, 2 * f))
+    mx, arg = oracle.aggregate_fwd_max(blk, h, oracle.F64)
+    fwd = np.concatenate([h[:blk.n_dst], mx], axis=1)
+    bwd = oracle.aggregate_bwd_max(blk, arg, da, f, None, oracle.F64)
+    assert abs(np.sum(fwd * da) - np.sum(h * bwd)) <= 1e-12 * np.sum(np.abs(fwd * da))
+    eps = 1e-7
+    for _ in range(10):
+        j, c = int(rng.integers(blk.n_src)), int(rng.integers(f))
+        h2 = h.copy()
+        h2[j, c] += eps
+        mx2, _ = oracle.aggregate_fwd_max(blk, h2, oracle.F64)
+        fwd2 = np.concatenate([h2[:blk.n_dst], mx2], axis=1)
+        assert abs((np.sum(fwd2 * da) - np.sum(fwd * da)) / eps - bwd[j, c]) <= 1e-6
+    # a source sampled twice by one row and winning it takes the gradient once
+    dup = [(i, v) for i in range(blk.n_dst)
+           for v in np.unique(blk.col[blk.rowptr[i]:blk.rowptr[i + 1]], return_counts=True)[0][
+               np.unique(blk.col[blk.rowptr[i]:blk.rowptr[i + 1]], return_counts=True)[1] > 1]]
+    assert dup, "the block has no repeated edge"
+    i, v = dup[0]
+    hd = np.zeros((blk.n_src, 1))
+    hd[v, 0] = 1.0
+    _, ad = oracle.aggregate_fwd_max(blk, hd, oracle.F64)
+    assert ad[i, 0] == v
+    dd = np.zeros((blk.n_dst, 2))
+    dd[i, 1] = 1.0
+    got = oracle.aggregate_bwd_max(blk, ad, dd, 1, None, oracle.F64)
+    assert got[v, 0] == 1.0 and np.sum(np.abs(got)) == 1.0
+    # ReLU mask of the layer below
+    hbelow = rng.standard_normal((blk.n_src, f))
+    masked = oracle.aggregate_bwd_max(blk, arg, da, f, hbelow, oracle.F64)
+    np.testing.assert_array_equal(masked, np.where(hbelow > 0, bwd, 0.0))
+
+
 def test_full_fanout_equals_textbook_operators():
     rng = np.random.default_rng(3)
     n = 40
