@@ -222,6 +222,42 @@ gnn_status gnn_aggregate_fwd_dedup(const gnn_block *b, gnn_agg kind, const void 
 gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a, int64_t f, const void *h_below,
                              gnn_dtype hbdt, float *d_src, gnn_stream s);
 
+/* GraphSAGE's max aggregator (Section II-A lists mean, max and LSTM as
+ * aggregation operators; the update then reads [h_self || max] as the mean
+ * path's [h_self || mean]).
+ *   h_src   [device] block->cap_src x f of hdt (GNN_F32 or GNN_BF16).
+ *   out     [device] block->cap_dst x f of odt (GNN_F32 or GNN_BF16):
+ *           out[i, c] = max over row i's edges e of h_src[col[e], c], narrowed
+ *           to odt (round to nearest even); 0 for a row without edges.
+ *   argmax  [device] int32 block->cap_dst x f: the local source id of the
+ *           edge that holds out[i, c] (-1 for a row without edges).  The
+ *           row's first edge holds the running maximum and a later edge
+ *           replaces it only when strictly greater, so ties and duplicate
+ *           edges go to the earliest edge, and a NaN counts only as the
+ *           row's first edge.
+ * The comparisons are exact, so out and argmax are bit for bit those of the
+ * sequential rule.  Rows past block->counts[0] are left untouched.
+ * Errors: GNN_EINVAL for a bad block, f out of range, NULL or misaligned
+ * pointers; GNN_EUNSUPPORTED for other dtypes. */
+gnn_status gnn_aggregate_fwd_max(const gnn_block *b, const void *h_src, gnn_dtype hdt, int64_t f, void *out,
+                                 gnn_dtype odt, int32_t *argmax, gnn_stream s);
+
+/* Backward of the max aggregator (the forward operators in reverse, Section
+ * II-B): the maximum passes its gradient to the source that won it.
+ *   argmax  [device] int32 block->cap_dst x f from gnn_aggregate_fwd_max.
+ *   d_a     [device] fp32 rows of 2f values (self part, then max part).
+ *   h_below, hbdt: the ReLU mask as in gnn_aggregate_bwd, or NULL.
+ *   d_src   [device] fp32 block->cap_src x f, overwritten:
+ *     d_src[j, c] = [j < n_dst] d_a[j, c] + sum over the distinct rows i that
+ *                   sampled j with argmax[i, c] = j of d_a[i, f + c]
+ *     then d_src[j, c] *= 1[h_below[j, c] > 0] when h_below is given.
+ * Reads the block's transpose (no atomics, bitwise reproducible); each
+ * column must list its rows in ascending order, as gnn_build_block makes it,
+ * so that a row that sampled j several times counts once.  Sums are fp32.
+ * Errors as gnn_aggregate_bwd. */
+gnn_status gnn_aggregate_bwd_max(const gnn_block *b, const int32_t *argmax, const float *d_a, int64_t f,
+                                 const void *h_below, gnn_dtype hbdt, float *d_src, gnn_stream s);
+
 /* ------------------------------------------------------------------------
  * One layer's forward in one launch, bf16 (equations 1 and 2 together: the
  * aggregation of Section II-A feeding the update, as in the on-chip

@@ -378,6 +378,34 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
     return launch_aggregate_bwd(b, kind, d_a, f, h_below, hbdt, d_src, stream_of(s));
 }
 
+gnn_status gnn_aggregate_fwd_max(const gnn_block *b, const void *h_src, gnn_dtype hdt, int64_t f, void *out,
+                                 gnn_dtype odt, int32_t *argmax, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_aggregate_fwd_max";
+    GNN_TRY(check_block(b, false, false, who));
+    GNN_CHECK(act_dtype(hdt) && act_dtype(odt), GNN_EUNSUPPORTED, "%s: dtypes must be GNN_F32 or GNN_BF16", who);
+    GNN_CHECK(dim_ok(f), GNN_EINVAL, "%s: f %lld out of [1, %d]", who, (long long)f, GNN_MAX_DIM);
+    GNN_CHECK((h_src || b->cap_src == 0) && ((out && argmax) || b->cap_dst == 0), GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK(aligned(h_src, dtype_size(hdt)) && aligned(out, dtype_size(odt)) && aligned(argmax, 4), GNN_EINVAL,
+              "%s: misaligned data", who);
+    return launch_aggregate_fwd_max(b, h_src, hdt, f, out, odt, argmax, stream_of(s));
+}
+
+gnn_status gnn_aggregate_bwd_max(const gnn_block *b, const int32_t *argmax, const float *d_a, int64_t f,
+                                 const void *h_below, gnn_dtype hbdt, float *d_src, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_aggregate_bwd_max";
+    GNN_TRY(check_block(b, true, false, who));
+    GNN_CHECK(!h_below || act_dtype(hbdt), GNN_EUNSUPPORTED, "%s: h_below dtype must be GNN_F32 or GNN_BF16", who);
+    GNN_CHECK(dim_ok(f), GNN_EINVAL, "%s: f %lld out of [1, %d]", who, (long long)f, GNN_MAX_DIM);
+    GNN_CHECK(((d_a && argmax) || b->cap_dst == 0) && (d_src || b->cap_src == 0), GNN_EINVAL, "%s: NULL pointer",
+              who);
+    GNN_CHECK(aligned(d_a, 4) && aligned(d_src, 4) && aligned(argmax, 4) &&
+                  aligned(h_below, h_below ? dtype_size(hbdt) : 1),
+              GNN_EINVAL, "%s: misaligned data", who);
+    return launch_aggregate_bwd_max(b, argmax, d_a, f, h_below, hbdt, d_src, stream_of(s));
+}
+
 gnn_status gnn_update_fwd_workspace_size(int64_t k, int64_t n_out, int64_t cap_m, gnn_dtype gemm_dt, size_t *bytes) {
     clear_error();
     GNN_CHECK(bytes, GNN_EINVAL, "gnn_update_fwd_workspace_size: bytes is NULL");

@@ -1,5 +1,6 @@
 // Neighbour aggregation over a sampled block, forward (pull over the block
-// CSR) and backward (pull over its transpose, no atomics).
+// CSR) and backward (pull over its transpose, no atomics): the mean and GCN
+// sums, and GraphSAGE's max aggregator with its argmax table.
 //
 // Work split: one wavefront per output row.  A row of f elements is cut into
 // C = ceil(f / 4) chunks of 4; when C <= 32 the wavefront is divided into
@@ -29,6 +30,27 @@ gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, 
     gnn_status st = GNN_OK;
     agg::with_bwd_job(b, kind, d_a, f, h_below, hbdt, d_src, [&](auto job) {
         st = launch_job(job, agg::row_grid(b->cap_src), s, "aggregate_bwd");
+    });
+    return st;
+}
+
+gnn_status launch_aggregate_fwd_max(const gnn_block *b, const void *h, int hdt, int64_t f, void *out, int odt,
+                                    int32_t *argmax, hipStream_t s) {
+    if (b->cap_dst == 0 || f == 0) return GNN_OK;
+    gnn_status st = GNN_OK;
+    const bool ok = agg::with_fwd_max_job(b, h, hdt, f, out, odt, argmax, [&](auto job) {
+        st = launch_job(job, agg::row_grid(b->cap_dst), s, "aggregate_fwd_max");
+    });
+    if (!ok) return fail(GNN_EUNSUPPORTED, "aggregate_fwd_max: unsupported dtypes %d -> %d", hdt, odt);
+    return st;
+}
+
+gnn_status launch_aggregate_bwd_max(const gnn_block *b, const int32_t *argmax, const float *d_a, int64_t f,
+                                    const void *h_below, int hbdt, float *d_src, hipStream_t s) {
+    if (b->cap_src == 0 || f == 0) return GNN_OK;
+    gnn_status st = GNN_OK;
+    agg::with_bwd_max_job(b, argmax, d_a, f, h_below, hbdt, d_src, [&](auto job) {
+        st = launch_job(job, agg::row_grid(b->cap_src), s, "aggregate_bwd_max");
     });
     return st;
 }

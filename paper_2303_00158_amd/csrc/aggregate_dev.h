@@ -1,5 +1,6 @@
 // Device side of the neighbour aggregation over a sampled block, forward (pull over the block
-// CSR) and backward (pull over its transpose, no atomics).
+// CSR) and backward (pull over its transpose, no atomics): the mean and GCN
+// sums, and GraphSAGE's max aggregator with its argmax table.
 //
 // Work split: one wavefront per output row.  A row of f elements is cut into
 // C = ceil(f / 4) chunks of 4; when C <= 32 the wavefront is divided into
@@ -8,6 +9,9 @@
 // shuffles at the end.  Up to 64 neighbour indices and weights of the row are
 // held one per lane and broadcast with shuffles.  Sums are fp32.
 #pragma once
+
+#include <math.h>
+#include <stdint.h>
 
 #include <type_traits>
 
@@ -348,6 +352,237 @@ struct BwdJob {
     }
 };
 
+// ---------------------------------------------------------------------------
+// GraphSAGE's max aggregator, forward: out[i, c] = the maximum of h[u, c] over
+// row i's edges, with argmax[i, c] the local source of the edge that holds it.
+// Sequential rule: the row's first edge holds the running maximum and a later
+// edge replaces it only when strictly greater (a tie, and a duplicate edge,
+// go to the earliest edge).  The slots walk interleaved edges of the row,
+// each applying the rule to its own edges with the row's first edge taken
+// unconditionally (it belongs to slot 0); the fold keeps the greater value
+// and, on equal values, the earlier edge.  That reproduces the sequential
+// rule, NaN included: a NaN is only ever taken as the row's first edge, and
+// then nothing replaces it.  A row without edges gives 0 and argmax -1.
+// ---------------------------------------------------------------------------
+struct MaxChunk {
+    float v[4];
+    int32_t pos[4];  // edge position in the row; INT32_MAX for none
+    int32_t src[4];  // local source id; -1 for none
+};
+
+__device__ __forceinline__ void max_take(MaxChunk &m, int q, float v, int32_t pos, int32_t src) {
+    m.v[q] = v;
+    m.pos[q] = pos;
+    m.src[q] = src;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void store_arg4(int32_t *p, int64_t row_off, int64_t e0, int64_t f, const int32_t *a) {
+    if constexpr (VEC) {
+        *reinterpret_cast<int4 *>(p + row_off + e0) = make_int4(a[0], a[1], a[2], a[3]);
+        return;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (e0 + q < f) p[row_off + e0 + q] = a[q];
+}
+
+// argmax[row_off + e0 .. + 3], with `none` past f
+template <bool VEC>
+__device__ __forceinline__ int4 load_arg4(const int32_t *p, int64_t row_off, int64_t e0, int64_t f, int32_t none) {
+    if constexpr (VEC) return *reinterpret_cast<const int4 *>(p + row_off + e0);
+    int32_t a[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const bool ok = e0 + q < f;
+        const int32_t x = p[row_off + (ok ? e0 + q : f - 1)];
+        a[q] = ok ? x : none;
+    }
+    return make_int4(a[0], a[1], a[2], a[3]);
+}
+
+template <class TIn, class TOut, bool VEC>
+__device__ __forceinline__ void agg_fwd_row_max(const int64_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+                                                const TIn *__restrict__ h, int64_t f, int C, int S,
+                                                TOut *__restrict__ out, int32_t *__restrict__ argmax, int64_t row) {
+    const int lane = threadIdx.x & 63;
+    const int64_t beg = rowptr[row], end = rowptr[row + 1];
+    const int groups = (C + 63) / 64;
+    const int slot = (S > 1) ? lane / C : 0;
+    for (int g = 0; g < groups; ++g) {
+        const int chunk = (S > 1) ? lane % C : g * 64 + lane;
+        const bool active = (S > 1) ? (slot < S) : (chunk < C);
+        const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        MaxChunk m;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) max_take(m, q, -INFINITY, INT32_MAX, -1);
+        for (int64_t wb = beg; wb < end; wb += 64) {
+            const int wn = static_cast<int>(min<int64_t>(64, end - wb));
+            const int32_t base = static_cast<int32_t>(wb - beg);
+            const int32_t my_idx = (lane < wn) ? col[wb + lane] : 0;
+            for (int tb = 0; tb < wn; tb += 4 * S) {
+                int32_t j[4];
+                bool ok[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int t = tb + u * S + slot;
+                    ok[u] = active && (t < wn);
+                    j[u] = __shfl(my_idx, t & 63, 64);
+                }
+                float4 v[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) v[u] = load_chunk<VEC>(h, static_cast<int64_t>(j[u]) * f, e0, f);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (!ok[u]) continue;
+                    const int32_t pos = base + tb + u * S + slot;
+                    const float x[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (pos == 0 || x[q] > m.v[q]) max_take(m, q, x[q], pos, j[u]);
+                }
+            }
+        }
+        // fold the slots into slot 0 in slot order
+        for (int s2 = 1; s2 < S; ++s2) {
+            const int src_lane = lane + s2 * C;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float ov = __shfl(m.v[q], src_lane, 64);
+                const int32_t op = __shfl(m.pos[q], src_lane, 64);
+                const int32_t os = __shfl(m.src[q], src_lane, 64);
+                if (slot == 0 && (ov > m.v[q] || (ov == m.v[q] && op < m.pos[q]))) max_take(m, q, ov, op, os);
+            }
+        }
+        if (slot != 0 || !active) continue;
+        float r[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[q] = (m.src[q] < 0) ? 0.f : m.v[q];
+        store_chunk<VEC>(out, row * f, e0, f, make_float4(r[0], r[1], r[2], r[3]));
+        store_arg4<VEC>(argmax, row * f, e0, f, m.src);
+    }
+}
+
+// Backward of the max aggregator for source j, pulled over the block's
+// transpose: d_src[j, c] = [j < n_dst] d_a[j, c] + the sum of d_a[i, f + c]
+// over the distinct rows i that sampled j with argmax[i, c] = j, then the
+// ReLU mask.  A row that sampled j several times sits in consecutive entries
+// of j's column (the columns are in ascending row order), and only the
+// first of them counts: the maximum passes its gradient once.  The
+// neighbour rows of d_a are read only for elements that j won.
+template <class THB, bool VEC>
+__device__ __forceinline__ void agg_bwd_row_max(int64_t n_dst, const int64_t *__restrict__ cscptr,
+                                                const int32_t *__restrict__ cscrow, const int32_t *__restrict__ argmax,
+                                                const float *__restrict__ d_a, int64_t f, int C, int S,
+                                                const THB *__restrict__ h_below, float *__restrict__ d_src,
+                                                int64_t j) {
+    const int lane = threadIdx.x & 63;
+    const int64_t ka = 2 * f;
+    const int64_t beg = cscptr[j], end = cscptr[j + 1];
+    const int32_t jj = static_cast<int32_t>(j);
+    const int groups = (C + 63) / 64;
+    const int slot = (S > 1) ? lane / C : 0;
+    for (int g = 0; g < groups; ++g) {
+        const int chunk = (S > 1) ? lane % C : g * 64 + lane;
+        const bool active = (S > 1) ? (slot < S) : (chunk < C);
+        const int64_t e0 = active ? static_cast<int64_t>(chunk) * 4 : 0;
+        const float4 self = load_chunk<VEC>(d_a, (j < n_dst ? j : 0) * ka, e0, f);
+        const bool mask = h_below != nullptr;
+        const float4 hb = load_chunk<VEC>(mask ? h_below : reinterpret_cast<const THB *>(d_a), mask ? j * f : 0, e0, f);
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int64_t wb = beg; wb < end; wb += 64) {
+            const int wn = static_cast<int>(min<int64_t>(64, end - wb));
+            int32_t my_idx = 0;
+            int my_first = 0;
+            if (lane < wn) {
+                my_idx = cscrow[wb + lane];
+                my_first = (wb + lane == beg) || (cscrow[wb + lane - 1] != my_idx);
+            }
+            for (int tb = 0; tb < wn; tb += 4 * S) {
+                int32_t i[4];
+                bool ok[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    // both shuffles run in every lane: a lane left out would
+                    // read as zero to the lanes that take its value
+                    const int t = tb + u * S + slot;
+                    i[u] = __shfl(my_idx, t & 63, 64);
+                    const int first = __shfl(my_first, t & 63, 64);
+                    ok[u] = active && (t < wn) && first;
+                }
+                int4 a[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) a[u] = load_arg4<VEC>(argmax, static_cast<int64_t>(i[u]) * f, e0, f, -1);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const bool w[4] = {ok[u] && a[u].x == jj, ok[u] && a[u].y == jj, ok[u] && a[u].z == jj,
+                                       ok[u] && a[u].w == jj};
+                    if (w[0] || w[1] || w[2] || w[3]) {
+                        const float4 v = load_chunk<VEC>(d_a, static_cast<int64_t>(i[u]) * ka + f, e0, f);
+                        acc[0] += w[0] ? v.x : 0.f;
+                        acc[1] += w[1] ? v.y : 0.f;
+                        acc[2] += w[2] ? v.z : 0.f;
+                        acc[3] += w[3] ? v.w : 0.f;
+                    }
+                }
+            }
+        }
+        for (int s2 = 1; s2 < S; ++s2) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float o = __shfl(acc[q], lane + s2 * C, 64);
+                if (slot == 0) acc[q] += o;
+            }
+        }
+        if (slot != 0 || !active) continue;
+        float4 r = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        if (j < n_dst) {
+            r.x += self.x;
+            r.y += self.y;
+            r.z += self.z;
+            r.w += self.w;
+        }
+        if (mask) {
+            if (!(hb.x > 0.f)) r.x = 0.f;
+            if (!(hb.y > 0.f)) r.y = 0.f;
+            if (!(hb.z > 0.f)) r.z = 0.f;
+            if (!(hb.w > 0.f)) r.w = 0.f;
+        }
+        store_chunk<VEC>(d_src, j * f, e0, f, r);
+    }
+}
+
+template <class TIn, class TOut, bool VEC>
+struct FwdMaxJob {
+    gnn_block b;
+    const TIn *h;
+    int64_t f;
+    int C, S;
+    TOut *out;
+    int32_t *argmax;
+    __device__ void run(int64_t blk, int64_t nblk) const {
+        const int64_t n = b.counts[0];
+        for (int64_t row = blk * kWaves + (threadIdx.x >> 6); row < n; row += nblk * kWaves)
+            agg_fwd_row_max<TIn, TOut, VEC>(b.rowptr, b.col, h, f, C, S, out, argmax, row);
+    }
+};
+
+template <class THB, bool VEC>
+struct BwdMaxJob {
+    gnn_block b;
+    const int32_t *argmax;
+    const float *d_a;
+    int64_t f;
+    int C, S;
+    const THB *h_below;
+    float *d_src;
+    __device__ void run(int64_t blk, int64_t nblk) const {
+        const int64_t n_dst = b.counts[0], n_src = b.counts[1];
+        for (int64_t j = blk * kWaves + (threadIdx.x >> 6); j < n_src; j += nblk * kWaves)
+            agg_bwd_row_max<THB, VEC>(n_dst, b.cscptr, b.cscrow, argmax, d_a, f, C, S, h_below, d_src, j);
+    }
+};
+
 inline void split_row(int64_t f, int *C, int *S) {
     const int64_t c = ceil_div(f, 4);
     *C = static_cast<int>(c);
@@ -424,6 +659,48 @@ void with_bwd_job(const gnn_block *b, int kind, const float *d_a, int64_t f, con
     };
     if (kind == GNN_AGG_SAGE_MEAN) by_kind(std::integral_constant<int, GNN_AGG_SAGE_MEAN>{});
     else by_kind(std::integral_constant<int, GNN_AGG_GCN_SYM>{});
+}
+
+// f(job) with the max aggregator's forward job; false if the dtypes are
+// unsupported.
+template <class F>
+bool with_fwd_max_job(const gnn_block *b, const void *h, int hdt, int64_t f, void *out, int odt, int32_t *argmax,
+                      F &&fn) {
+    int C, S;
+    split_row(f, &C, &S);
+    const bool vec = (f % 4 == 0) && aligned(h, 4 * dtype_size(hdt)) && aligned(out, 4 * dtype_size(odt)) &&
+                     aligned(argmax, 16);
+    auto go = [&](auto ti_tag, auto to_tag) {
+        using TI = typename decltype(ti_tag)::type;
+        using TO = typename decltype(to_tag)::type;
+        const TI *hp = static_cast<const TI *>(h);
+        TO *op = static_cast<TO *>(out);
+        if (vec) fn(FwdMaxJob<TI, TO, true>{*b, hp, f, C, S, op, argmax});
+        else fn(FwdMaxJob<TI, TO, false>{*b, hp, f, C, S, op, argmax});
+    };
+    if (!((hdt == GNN_F32 || hdt == GNN_BF16) && (odt == GNN_F32 || odt == GNN_BF16))) return false;
+    if (hdt == GNN_F32 && odt == GNN_F32) go(Tag<float>{}, Tag<float>{});
+    else if (hdt == GNN_F32 && odt == GNN_BF16) go(Tag<float>{}, Tag<uint16_t>{});
+    else if (hdt == GNN_BF16 && odt == GNN_F32) go(Tag<uint16_t>{}, Tag<float>{});
+    else go(Tag<uint16_t>{}, Tag<uint16_t>{});
+    return true;
+}
+
+template <class F>
+void with_bwd_max_job(const gnn_block *b, const int32_t *argmax, const float *d_a, int64_t f, const void *h_below,
+                      int hbdt, float *d_src, F &&fn) {
+    int C, S;
+    split_row(f, &C, &S);
+    const bool vec = (f % 4 == 0) && aligned(d_a, 16) && aligned(d_src, 16) && aligned(argmax, 16) &&
+                     (!h_below || aligned(h_below, 4 * dtype_size(hbdt)));
+    auto go = [&](auto hb_tag) {
+        using THB = typename decltype(hb_tag)::type;
+        const THB *hb = static_cast<const THB *>(h_below);
+        if (vec) fn(BwdMaxJob<THB, true>{*b, argmax, d_a, f, C, S, hb, d_src});
+        else fn(BwdMaxJob<THB, false>{*b, argmax, d_a, f, C, S, hb, d_src});
+    };
+    if (!h_below || hbdt == GNN_F32) go(Tag<float>{});
+    else go(Tag<uint16_t>{});
 }
 
 }  // namespace agg

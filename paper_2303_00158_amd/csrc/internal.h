@@ -131,6 +131,10 @@ gnn_status launch_aggregate_fwd_dedup(const gnn_block *b, int kind, const void *
                                       int odt, hipStream_t s);
 gnn_status launch_aggregate_bwd(const gnn_block *b, int kind, const float *d_a, int64_t f, const void *h_below,
                                 int hbdt, float *d_src, hipStream_t s);
+gnn_status launch_aggregate_fwd_max(const gnn_block *b, const void *h, int hdt, int64_t f, void *out, int odt,
+                                    int32_t *argmax, hipStream_t s);
+gnn_status launch_aggregate_bwd_max(const gnn_block *b, const int32_t *argmax, const float *d_a, int64_t f,
+                                    const void *h_below, int hbdt, float *d_src, hipStream_t s);
 // Update GEMMs.  Their workspaces hold fp32 partial tiles of split
 // reductions (no state survives a call).  A null forward workspace disables
 // the reduction split.

@@ -78,6 +78,8 @@ _SIGNATURES = {
     "gnn_aggregate_fwd": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_fwd_dedup": (_i32, [_P(Block), _i32, _vp, _i32, _i64, _vp, _i32, _vp]),
     "gnn_aggregate_bwd": (_i32, [_P(Block), _i32, _vp, _i64, _vp, _i32, _vp, _vp]),
+    "gnn_aggregate_fwd_max": (_i32, [_P(Block), _vp, _i32, _i64, _vp, _i32, _vp, _vp]),
+    "gnn_aggregate_bwd_max": (_i32, [_P(Block), _vp, _vp, _i64, _vp, _i32, _vp, _vp]),
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_two_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
                                  _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
@@ -277,6 +279,28 @@ def aggregate_bwd(block: DeviceBlock, kind: int, d_a: torch.Tensor, f: int, d_sr
     hb_code = dtype_code(h_below.dtype) if h_below is not None else GNN_F32
     _check(lib().gnn_aggregate_bwd(ctypes.byref(block.c), kind, _ptr(d_a), f, _ptr(h_below), hb_code, _ptr(d_src),
                                    _stream(stream)))
+    return d_src
+
+
+def aggregate_fwd_max(block: DeviceBlock, h_src: torch.Tensor, out: torch.Tensor, argmax: torch.Tensor,
+                      stream=None) -> torch.Tensor:
+    """gnn_aggregate_fwd_max: GraphSAGE's max aggregator; argmax (int32, the
+    shape of out) receives the winning local source of every element."""
+    assert argmax.dtype == torch.int32
+    f = h_src.shape[1]
+    _check(lib().gnn_aggregate_fwd_max(ctypes.byref(block.c), _ptr(h_src), dtype_code(h_src.dtype), f, _ptr(out),
+                                       dtype_code(out.dtype), _ptr(argmax), _stream(stream)))
+    return out
+
+
+def aggregate_bwd_max(block: DeviceBlock, argmax: torch.Tensor, d_a: torch.Tensor, f: int, d_src: torch.Tensor,
+                      h_below: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """gnn_aggregate_bwd_max: the max aggregator's backward from its argmax
+    table (d_a rows hold 2f values: self part, then max part)."""
+    assert argmax.dtype == torch.int32
+    hb_code = dtype_code(h_below.dtype) if h_below is not None else GNN_F32
+    _check(lib().gnn_aggregate_bwd_max(ctypes.byref(block.c), _ptr(argmax), _ptr(d_a), f, _ptr(h_below), hb_code,
+                                       _ptr(d_src), _stream(stream)))
     return d_src
 
 

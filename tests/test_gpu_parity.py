@@ -430,6 +430,158 @@ def test_aggregate_bwd_is_bitwise_reproducible():
 
 
 # ---------------------------------------------------------------------------
+# GraphSAGE's max aggregator
+# ---------------------------------------------------------------------------
+
+def _multigraph_block(seed, n=1500, n_dst=300, fanout=100):
+    """A block of a multigraph: repeated edges, isolated destinations (empty
+    rows), hub rows longer than one 64-edge window, and popular sources
+    (every vertex also links to three of six, repeats allowed) whose
+    transpose columns span several windows and hold repeated rows."""
+    rng = np.random.default_rng(seed)
+    rowptr, col = dense.small_multigraph(rng, n, avg_deg=12, hubs=4, isolated=25)
+    deg = np.diff(rowptr)
+    popular = rng.choice(np.nonzero(deg > 0)[0], size=6, replace=False)
+    rows = [np.sort(np.concatenate([col[rowptr[v]:rowptr[v + 1]], rng.choice(popular, size=3)])) if deg[v] else
+            col[rowptr[v]:rowptr[v + 1]] for v in range(n)]
+    rowptr = np.concatenate([[0], np.cumsum([r.size for r in rows])]).astype(np.int64)
+    col = np.concatenate(rows).astype(np.int64)
+    deg = np.diff(rowptr)
+    special = np.concatenate([np.argsort(-deg, kind="stable")[:4], np.nonzero(deg == 0)[0][:3]])
+    rest = np.setdiff1d(np.arange(n), special)
+    dst = np.concatenate([special, rng.choice(rest, size=n_dst - special.size, replace=False)]).astype(np.int64)
+    rng.shuffle(dst)
+    blk = oracle.build_block(rowptr, col, dst, fanout, seed, 0, 1)
+    assert np.diff(blk.rowptr).max() > 64 and np.diff(blk.cscptr).max() > 96
+    return blk
+
+
+def _max_inputs(rng, blk, f, code, ties):
+    if ties:  # small integers: most maxima are tied between several edges
+        x = rng.integers(-3, 4, size=(blk.n_src, f)).astype(np.float32)
+    else:
+        x = rng.standard_normal((blk.n_src, f)).astype(np.float32)
+    return oracle.f32_to_bf16_bits(x) if code == oracle.BF16 else x
+
+
+def _has_repeated_edge(blk):
+    for i in range(blk.n_dst):
+        c = blk.col[blk.rowptr[i]:blk.rowptr[i + 1]]
+        if c.size != np.unique(c).size:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("hc,oc", [(oracle.F32, oracle.F32), (oracle.BF16, oracle.BF16), (oracle.BF16, oracle.F32),
+                                   (oracle.F32, oracle.BF16)])
+@pytest.mark.parametrize("ties", [False, True])
+def test_aggregate_fwd_max_parity(f, hc, oc, ties):
+    # exact comparisons: the maximum and its argmax match bit for bit
+    blk = _multigraph_block(f + 3 * hc + 11 * oc)
+    assert _has_repeated_edge(blk) and (np.diff(blk.rowptr) == 0).any()
+    rng = np.random.default_rng(f + hc)
+    h = _max_inputs(rng, blk, f, hc, ties)
+    want, want_arg = oracle.aggregate_fwd_max(blk, h, oc)
+    db = upload_block(blk)
+    odt = torch.bfloat16 if oc == oracle.BF16 else torch.float32
+    out = torch.full((blk.n_dst, f), float("nan"), dtype=odt, device=DEV)
+    arg = torch.full((blk.n_dst, f), -7, dtype=torch.int32, device=DEV)
+    print(f"[max fwd] f={f} {hc}->{oc} ties={ties}", flush=True)
+    gnn.aggregate_fwd_max(db, from_np_act(h), out, arg)
+    assert np.array_equal(arg.cpu().numpy(), want_arg)
+    got = to_np_act(out)
+    iv = np.uint16 if oc == oracle.BF16 else np.uint32
+    assert np.array_equal(got.view(iv), want.view(iv))
+
+
+def test_aggregate_fwd_max_nan_and_unaligned_rows():
+    # A NaN is kept only when it is the row's first edge; f = 13 takes the
+    # per-element path.  NaN payloads may differ, so NaN positions and the
+    # other values are compared separately.
+    blk = _multigraph_block(5)
+    f = 13
+    rng = np.random.default_rng(5)
+    h = rng.standard_normal((blk.n_src, f)).astype(np.float32)
+    h[rng.random((blk.n_src, f)) < 0.05] = np.nan
+    want, want_arg = oracle.aggregate_fwd_max(blk, h, oracle.F32)
+    assert np.isnan(want).any()
+    db = upload_block(blk)
+    out = torch.empty((blk.n_dst, f), dtype=torch.float32, device=DEV)
+    arg = torch.empty((blk.n_dst, f), dtype=torch.int32, device=DEV)
+    gnn.aggregate_fwd_max(db, from_np_act(h), out, arg)
+    got = out.cpu().numpy()
+    assert np.array_equal(arg.cpu().numpy(), want_arg)
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    ok = ~np.isnan(want)
+    assert np.array_equal(got[ok].view(np.uint32), want[ok].view(np.uint32))
+
+
+def test_aggregate_fwd_max_device_count_below_capacity():
+    # rows from the device count on are left untouched
+    blk = _multigraph_block(9)
+    f = 64
+    rng = np.random.default_rng(9)
+    h = _max_inputs(rng, blk, f, oracle.F32, False)
+    want, want_arg = oracle.aggregate_fwd_max(blk, h, oracle.F32)
+    db = upload_block(blk)
+    n = blk.n_dst // 2
+    db.counts[0] = n
+    out = torch.full((blk.n_dst, f), -5.0, dtype=torch.float32, device=DEV)
+    arg = torch.full((blk.n_dst, f), -7, dtype=torch.int32, device=DEV)
+    gnn.aggregate_fwd_max(db, from_np_act(h), out, arg)
+    o, a = out.cpu().numpy(), arg.cpu().numpy()
+    assert np.array_equal(o[:n], want[:n]) and np.array_equal(a[:n], want_arg[:n])
+    assert np.all(o[n:] == -5.0) and np.all(a[n:] == -7)
+
+
+@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("hb_code", [None, oracle.F32, oracle.BF16])
+@pytest.mark.parametrize("ties", [False, True])
+def test_aggregate_bwd_max_parity(f, hb_code, ties):
+    # argmax from the oracle's forward; a row that sampled a source twice
+    # passes its gradient once; with ties one source wins many elements
+    blk = _multigraph_block(100 + f + (hb_code or 0))
+    rng = np.random.default_rng(f)
+    h = _max_inputs(rng, blk, f, oracle.F32, ties)
+    _, amax = oracle.aggregate_fwd_max(blk, h, oracle.F32)
+    da = rng.standard_normal((blk.n_dst, 2 * f)).astype(np.float32)
+    hb = _act(rng, blk.n_src, f, hb_code) if hb_code is not None else None
+    want = oracle.aggregate_bwd_max(blk, amax, da, f, hb, oracle.F32)
+    db = upload_block(blk)
+    out = torch.full((blk.n_src, f), float("nan"), dtype=torch.float32, device=DEV)
+    print(f"[max bwd] f={f} hb={hb_code} ties={ties}", flush=True)
+    arg_d = torch.from_numpy(amax).to(DEV)
+    gnn.aggregate_bwd_max(db, arg_d, from_np_act(da), f, out, h_below=from_np_act(hb) if hb is not None else None)
+    got = out.cpu().numpy()
+    assert relerr(got, want) <= 1e-6
+    # no atomics: a second call gives the same bits
+    out2 = torch.empty_like(out)
+    gnn.aggregate_bwd_max(db, arg_d, from_np_act(da), f, out2, h_below=from_np_act(hb) if hb is not None else None)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), out2.view(torch.int32))
+
+
+def test_aggregate_max_round_trip_on_a_sampled_block():
+    # forward then backward through the library on a sampled R-MAT block,
+    # against the oracle's forward and backward
+    blk, _ = _oracle_block(17, n_dst=600, fanout=25)
+    f = 128
+    rng = np.random.default_rng(17)
+    h = oracle.f32_to_bf16_bits(rng.standard_normal((blk.n_src, f)).astype(np.float32))
+    want, want_arg = oracle.aggregate_fwd_max(blk, h, oracle.BF16)
+    db = upload_block(blk)
+    out = torch.empty((blk.n_dst, f), dtype=torch.bfloat16, device=DEV)
+    arg = torch.empty((blk.n_dst, f), dtype=torch.int32, device=DEV)
+    gnn.aggregate_fwd_max(db, from_np_act(h), out, arg)
+    assert np.array_equal(to_np_act(out), want) and np.array_equal(arg.cpu().numpy(), want_arg)
+    da = rng.standard_normal((blk.n_dst, 2 * f)).astype(np.float32)
+    d_src = torch.empty((blk.n_src, f), dtype=torch.float32, device=DEV)
+    gnn.aggregate_bwd_max(db, arg, from_np_act(da), f, d_src, h_below=from_np_act(h))
+    assert relerr(d_src.cpu().numpy(), oracle.aggregate_bwd_max(blk, want_arg, da, f, h, oracle.F32)) <= 1e-6
+
+
+# ---------------------------------------------------------------------------
 # one layer's forward in one launch (aggregation + update, loss for the last)
 # ---------------------------------------------------------------------------
 
