@@ -26,6 +26,7 @@ import numpy as np
 
 F32, BF16, F16, F64 = 0, 1, 2, 3
 SAGE, GCN = 0, 1
+SAGE_MAX = 2  # GraphSAGE with the max aggregator (its update reads [h_self || max] like SAGE)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
@@ -251,6 +252,8 @@ def aggregate_fwd(kind: int, blk: Block, src_norm: Optional[np.ndarray], h: np.n
     assert h.shape[0] >= blk.n_src
     out = np.zeros((blk.n_dst, f), dtype=_np_dtype(out_code))
     sn = _c(src_norm, np.float32) if src_norm is not None else None
+    if kind not in (SAGE, GCN):
+        raise ValueError(f"aggregate_fwd: kind {kind} (the max aggregator is aggregate_fwd_max)")
     if kind == GCN and sn is None:
         raise ValueError("GCN aggregation needs per-source norms")
     lib().orc_aggregate_fwd(kind, blk.n_dst, _p(blk.rowptr), _p(blk.col), _p(sn), _p(h), _code(h), f,
@@ -260,6 +263,8 @@ def aggregate_fwd(kind: int, blk: Block, src_norm: Optional[np.ndarray], h: np.n
 
 def aggregate_bwd(kind: int, blk: Block, src_norm, d_a: np.ndarray, f: int, h_below: Optional[np.ndarray],
                   out_code: int) -> np.ndarray:
+    if kind not in (SAGE, GCN):
+        raise ValueError(f"aggregate_bwd: kind {kind} (the max aggregator is aggregate_bwd_max)")
     d_a = np.ascontiguousarray(d_a)
     sn = _c(src_norm, np.float32) if src_norm is not None else None
     out = np.zeros((blk.n_src, f), dtype=_np_dtype(out_code))
@@ -352,7 +357,7 @@ def sgd(w: np.ndarray, dw: np.ndarray, lr: float) -> np.ndarray:
 
 @dataclasses.dataclass
 class StepConfig:
-    kind: int                  # SAGE or GCN
+    kind: int                  # SAGE, GCN or SAGE_MAX
     dims: Sequence[int]        # f^0..f^L
     fanouts: Sequence[int]     # hop order: fanouts[0] sampled around the targets
     precision: int             # F32, BF16 or F64 (storage of X', M, H; GEMM operand rounding)
@@ -420,14 +425,18 @@ def train_step(rowptr, col, nrm, table, labels, targets, weights, biases, cfg: S
         for l in range(1, L + 1):
             src_norms[l] = np.ascontiguousarray(nrm[layer_block[l].src_ids], dtype=np.float32)
 
+    cat = cfg.kind in (SAGE, SAGE_MAX)                    # A = [h_self || aggregation]
     H = {0: x0}
-    AGG = {}
+    AGG, ARG = {}, {}
     for l in range(1, L + 1):
         blk = layer_block[l]
-        AGG[l] = aggregate_fwd(cfg.kind, blk, src_norms.get(l), H[l - 1], act)
+        if cfg.kind == SAGE_MAX:
+            AGG[l], ARG[l] = aggregate_fwd_max(blk, H[l - 1], act)
+        else:
+            AGG[l] = aggregate_fwd(cfg.kind, blk, src_norms.get(l), H[l - 1], act)
         last = l == L
-        a_self = np.ascontiguousarray(H[l - 1][:blk.n_dst]) if cfg.kind == SAGE else AGG[l]
-        a_nbr = AGG[l] if cfg.kind == SAGE else None
+        a_self = np.ascontiguousarray(H[l - 1][:blk.n_dst]) if cat else AGG[l]
+        a_nbr = AGG[l] if cat else None
         H[l] = update_fwd(a_self, a_nbr, weights[l - 1], biases[l - 1], relu=not last, gemm_code=gemm,
                           out_code=wide if last else act)
     y = np.asarray(labels, dtype=np.int64)[np.asarray(targets, dtype=np.int64)]
@@ -436,8 +445,8 @@ def train_step(rowptr, col, nrm, table, labels, targets, weights, biases, cfg: S
     dW, dB, GR = {}, {}, {L: G}
     for l in range(L, 0, -1):
         blk = layer_block[l]
-        a_self = np.ascontiguousarray(H[l - 1][:blk.n_dst]) if cfg.kind == SAGE else AGG[l]
-        a_nbr = AGG[l] if cfg.kind == SAGE else None
+        a_self = np.ascontiguousarray(H[l - 1][:blk.n_dst]) if cat else AGG[l]
+        a_nbr = AGG[l] if cat else None
         dw, db, da = update_bwd(a_self, a_nbr, weights[l - 1], GR[l], gemm, want_da=l > 1, out_code=wide)
         dW[l], dB[l] = dw, db
         if l > 1:
@@ -445,10 +454,13 @@ def train_step(rowptr, col, nrm, table, labels, targets, weights, biases, cfg: S
             h_mask = H[l - 1]
             if relu_flip and (l - 1) in relu_flip:
                 h_mask = _flip_decisions(H[l - 1], relu_flip[l - 1])
-            GR[l - 1] = aggregate_bwd(cfg.kind, blk, src_norms.get(l), da, f, h_mask, wide)
+            if cfg.kind == SAGE_MAX:
+                GR[l - 1] = aggregate_bwd_max(blk, ARG[l], da, f, h_mask, wide)
+            else:
+                GR[l - 1] = aggregate_bwd(cfg.kind, blk, src_norms.get(l), da, f, h_mask, wide)
     new_w = [sgd(weights[l - 1], dW[l], cfg.lr) for l in range(1, L + 1)]
     new_b = [sgd(biases[l - 1], dB[l], cfg.lr) for l in range(1, L + 1)]
     return {
-        "blocks": blocks, "x0": x0, "H": H, "AGG": AGG, "loss": loss, "G": GR, "dW": dW, "dB": dB,
+        "blocks": blocks, "x0": x0, "H": H, "AGG": AGG, "ARG": ARG, "loss": loss, "G": GR, "dW": dW, "dB": dB,
         "new_w": new_w, "new_b": new_b, "edges": int(sum(b.nnz for b in blocks)),
     }

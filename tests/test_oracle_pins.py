@@ -507,7 +507,7 @@ def _tiny_problem(kind, seed=0, n=60, f=(5, 4, 3), fanouts=(4, 3), batch=8):
     L = len(f) - 1
     ws, bs = [], []
     for l in range(1, L + 1):
-        K = 2 * f[l - 1] if kind == oracle.SAGE else f[l - 1]
+        K = f[l - 1] if kind == oracle.GCN else 2 * f[l - 1]
         ws.append(rng.standard_normal((K, f[l])) * 0.7)
         bs.append(rng.standard_normal(f[l]) * 0.1)
     cfg = oracle.StepConfig(kind=kind, dims=f, fanouts=fanouts, precision=oracle.F64, seed=seed, step=3, lr=0.1)
@@ -525,6 +525,14 @@ def _autograd_reference(kind, blocks, nrm, table, labels, targets, ws, bs):
         blk = layer_block[l]
         if kind == oracle.SAGE:
             a = torch.cat([h[:blk.n_dst], torch.tensor(dense.sage_mean_matrix(blk)) @ h], 1)
+        elif kind == oracle.SAGE_MAX:
+            # torch's max over each row's sampled neighbours (its backward
+            # routes the gradient to one maximal entry); zero for empty rows
+            rows = []
+            for i in range(blk.n_dst):
+                cols = torch.tensor(blk.col[blk.rowptr[i]:blk.rowptr[i + 1]].astype(np.int64))
+                rows.append(h[cols].max(0).values if cols.numel() else torch.zeros(h.shape[1], dtype=h.dtype))
+            a = torch.cat([h[:blk.n_dst], torch.stack(rows)], 1)
         else:
             a = torch.tensor(dense.gcn_matrix(blk, nrm[blk.src_ids])) @ h
         z = a @ wt[l - 1] + bt[l - 1]
@@ -534,7 +542,7 @@ def _autograd_reference(kind, blocks, nrm, table, labels, targets, ws, bs):
     return loss.item(), [w.grad.numpy() for w in wt], [b.grad.numpy() for b in bt]
 
 
-@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN, oracle.SAGE_MAX])
 def test_train_step_matches_autograd_dense(kind):
     rowptr, col, nrm, table, labels, targets, ws, bs, cfg = _tiny_problem(kind, seed=1)
     out = oracle.train_step(rowptr, col, nrm, table, labels, targets, ws, bs, cfg)
@@ -546,7 +554,7 @@ def test_train_step_matches_autograd_dense(kind):
         np.testing.assert_allclose(out["new_w"][l - 1], ws[l - 1] - cfg.lr * gw[l - 1], rtol=1e-10, atol=1e-12)
 
 
-@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN, oracle.SAGE_MAX])
 def test_train_step_three_layers_matches_autograd(kind):
     rowptr, col, nrm, table, labels, targets, ws, bs, cfg = _tiny_problem(kind, seed=2, f=(4, 5, 3, 3),
                                                                          fanouts=(3, 2, 2))
@@ -557,7 +565,7 @@ def test_train_step_three_layers_matches_autograd(kind):
         np.testing.assert_allclose(out["dW"][l], gw[l - 1], rtol=1e-10, atol=1e-12)
 
 
-@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN])
+@pytest.mark.parametrize("kind", [oracle.SAGE, oracle.GCN, oracle.SAGE_MAX])
 def test_train_step_finite_differences(kind):
     rowptr, col, nrm, table, labels, targets, ws, bs, cfg = _tiny_problem(kind, seed=3)
     out = oracle.train_step(rowptr, col, nrm, table, labels, targets, ws, bs, cfg)
@@ -566,8 +574,8 @@ def test_train_step_finite_differences(kind):
     # stay away from ReLU kinks: every hidden pre-activation is far from 0
     for l in range(1, L):
         blk = blocks[L - l]
-        a_self = out["H"][l - 1][:blk.n_dst] if kind == oracle.SAGE else out["AGG"][l]
-        a_nbr = out["AGG"][l] if kind == oracle.SAGE else None
+        a_self = out["H"][l - 1][:blk.n_dst] if kind != oracle.GCN else out["AGG"][l]
+        a_nbr = out["AGG"][l] if kind != oracle.GCN else None
         z = oracle.update_fwd(np.ascontiguousarray(a_self), a_nbr, ws[l - 1], bs[l - 1], relu=False,
                               gemm_code=oracle.F64, out_code=oracle.F64)
         assert np.abs(z).min() > 1e-4
