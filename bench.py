@@ -86,7 +86,7 @@ def parse():
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run a plain device copy (fp32 -> int32 elementwise) of this many MiB three times, the "
                         "known-size kernel that scales HBM traffic counters")
-    p.add_argument("--other-workloads", default="rmat2.4m-gcn,tiny-er10k-gcn,fp32,rmat111m-sage3,"
+    p.add_argument("--other-workloads", default="rmat2.4m-gcn,rmat2.4m-sagemax,tiny-er10k-gcn,fp32,rmat111m-sage3,"
                                                  "rmat244m-sage-hosttable",
                    help="comma-separated workloads also timed (pipelined) after the headline, each with its own "
                         "roofline; 'fp32' is the headline workload in fp32; empty: none")
@@ -141,6 +141,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def kind_code(gnn, kind: str) -> int:
+    return {"sage": gnn.GNN_AGG_SAGE_MEAN, "gcn": gnn.GNN_AGG_GCN_SYM, "sage-max": gnn.GNN_AGG_SAGE_MAX}[kind]
+
+
 # ---------------------------------------------------------------------------
 # staged step: the same iteration through the individual ABI calls, with HIP
 # events between them (on torch's current stream, which the calls use)
@@ -152,7 +156,8 @@ class StagedStep:
         dev = graph.rowptr.device
         L = w.num_layers
         self.L = L
-        self.kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+        self.kind = kind_code(gnn, w.kind)
+        self.maxagg = self.kind == gnn.GNN_AGG_SAGE_MAX
         self.blocks = []
         cap = batch_size
         ws_bytes = 0
@@ -168,10 +173,14 @@ class StagedStep:
                                                         gnn._stream(None)))
         dims = w.dims
         self.x0 = torch.empty((self.blocks[-1].c.cap_src, dims[0]), dtype=act, device=dev)
-        self.agg, self.h, self.grad, self.da = {}, {}, {}, {}
+        self.agg, self.h, self.grad, self.da, self.argmax = {}, {}, {}, {}, {}
         for l in range(1, L + 1):
             rows = self.blocks[L - l].c.cap_dst
             self.agg[l] = torch.empty((rows, dims[l - 1]), dtype=act, device=dev)
+            # the max aggregator's argmax tables, kept for the layers whose
+            # aggregation has a backward (as in the training step)
+            self.argmax[l] = (torch.empty((rows, dims[l - 1]), dtype=torch.int32, device=dev)
+                              if self.maxagg and l > 1 else None)
             self.h[l] = torch.empty((rows, dims[l]), dtype=act if l < L else torch.float32, device=dev)
             self.grad[l] = torch.empty((rows, dims[l]), dtype=torch.float32, device=dev)
             if l > 1:
@@ -222,12 +231,25 @@ class StagedStep:
                           self.h[1], self.agg[2], self.da[2], self.grad[2], trainer.dw[0], trainer.db[0],
                           trainer.dw[1], trainer.db[1], ws=self.two_ws)
 
+    def aggregate_fwd(self, blk, l, hin):
+        if self.maxagg:
+            self.gnn.aggregate_fwd_max(blk, hin, self.agg[l], self.argmax[l])
+        else:
+            self.gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])
+
+    def aggregate_bwd(self, blk, l, hin):
+        f = self.w.dims[l - 1]
+        if self.maxagg:
+            self.gnn.aggregate_bwd_max(blk, self.argmax[l], self.da[l], f, self.grad[l - 1], h_below=hin)
+        else:
+            self.gnn.aggregate_bwd(blk, self.kind, self.da[l], f, self.grad[l - 1], h_below=hin)
+
     def replay(self, name: str, trainer, table, reps: int, labels=None) -> float:
         """Launch the single ABI call of stage `name` `reps` times back to back
         on the blocks of the last run; returns the mean ms per launch (HIP
         events on the stream the call uses)."""
         gnn, L, w = self.gnn, self.L, self.w
-        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        sage = self.kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         if name == "gather":
             b0 = self.blocks[-1]
@@ -236,7 +258,7 @@ class StagedStep:
         elif name.startswith("agg_fwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
-            call = lambda: gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])  # noqa
+            call = lambda: self.aggregate_fwd(blk, l, hin)  # noqa
         elif name.startswith("agg_dedup_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -258,8 +280,7 @@ class StagedStep:
         elif name.startswith("agg_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
-            call = lambda: gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1],  # noqa
-                                             h_below=hin)
+            call = lambda: self.aggregate_bwd(blk, l, hin)  # noqa
         elif name.startswith("update_bwd_l"):
             l = int(name[-1])
             blk, hin = self.blocks[L - l], (self.x0 if l == 1 else self.h[l - 1])
@@ -319,9 +340,11 @@ class StagedStep:
         b0 = self.blocks[-1]
         gnn.gather_features(table, b0.src_ids, self.x0, n_ids_dev=b0.counts[1:2], loc=self.loc)
         mark("gather")
-        sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
+        sage = self.kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         loss_fused = False
+        if self.maxagg:  # the fused kernels implement the sum aggregations only
+            self.two = self.two_bwd = False
         if L == 2 and self.two is not False and trainer.wt:
             # as in the training step: layer 1's aggregation (the prepare
             # stage's), then both layers, the loss and dA^2 in one launch
@@ -341,7 +364,7 @@ class StagedStep:
             # as in the training step: layer 1's aggregation belongs to the
             # prepare stage, its update reads it (fused kernel in A-load mode
             # inside gnn_update_fwd); later layers in one gnn_layer_fwd
-            if (l > 1 or L == 1) and self.fused.get(l, bool(trainer.wt)):
+            if (l > 1 or L == 1) and self.fused.get(l, bool(trainer.wt) and not self.maxagg):
                 try:
                     self.layer_fwd(l, trainer, labels)
                     self.fused[l] = True
@@ -352,7 +375,7 @@ class StagedStep:
                     if e.code != gnn.GNN_EUNSUPPORTED:
                         raise
             self.fused[l] = False
-            gnn.aggregate_fwd(blk, self.kind, hin, self.agg[l])
+            self.aggregate_fwd(blk, l, hin)
             mark(f"agg_fwd_l{l}")
             gnn.update_fwd(hin if sage else self.agg[l], self.agg[l] if sage else None, trainer.w[l - 1],
                            trainer.b[l - 1], self.h[l], l < L, gemm, m_dev=blk.counts[0:1], cap_m=blk.c.cap_dst,
@@ -381,7 +404,7 @@ class StagedStep:
                            ws=self.bwd_ws[l])
             mark(f"update_bwd_l{l}")
             if l > 1:
-                gnn.aggregate_bwd(blk, self.kind, self.da[l], w.dims[l - 1], self.grad[l - 1], h_below=hin)
+                self.aggregate_bwd(blk, l, hin)
                 mark(f"agg_bwd_l{l}")
         for l in range(L):
             gnn.sgd(trainer.w[l], trainer.dw[l], lr)
@@ -406,6 +429,8 @@ class StagedStep:
             f = w.dims[l - 1]
             R = np.unique(b["col"]).size
             extra = (b["n_dst"] * f * S_H + 4 * b["n_src"]) if w.kind == "gcn" else 0
+            if self.argmax.get(l) is not None:
+                extra = 4 * b["n_dst"] * f  # the int32 argmax table
             return R * f * S_H + 4 * b["nnz"] + 8 * (b["n_dst"] + 1) + b["n_dst"] * f * S_H + extra, 0
         if name.startswith("update_fwd_l"):
             l = int(name[-1])
@@ -464,6 +489,12 @@ class StagedStep:
             b = self.blocks[L - l].host()
             f = w.dims[l - 1]
             rows_used = np.unique(b["cscrow"]).size
+            if self.maxagg:
+                # the argmax rows and the max part of dA of the rows that
+                # sampled anything (each element read where it was won), the
+                # self part, the transpose, the mask and the output
+                return (2 * rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
+                        + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
             return (rows_used * f * 4 + b["n_dst"] * f * 4 + 4 * b["nnz"] + 8 * (b["n_src"] + 1)
                     + 8 * (b["n_dst"] + 1) + b["n_src"] * f * S_H + b["n_src"] * f * 4), 0
         if name.startswith("update_bwd_l"):
@@ -717,7 +748,7 @@ class Inputs:
         prec = precision or w.precision
         self.act = torch.bfloat16 if prec == "bf16" else torch.float32
         self.precision = gnn.GNN_BF16 if prec == "bf16" else gnn.GNN_F32
-        self.kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
+        self.kind = kind_code(gnn, w.kind)
         t0 = time.time()
         if share is not None:
             self.rowptr, self.col, self.graph, self.table = share.rowptr, share.col, share.graph, share.table

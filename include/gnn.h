@@ -71,14 +71,19 @@ typedef int32_t gnn_dtype;
 typedef int32_t gnn_agg;
 typedef int32_t gnn_loc;
 enum { GNN_F32 = 0, GNN_BF16 = 1, GNN_F16 = 2 };
-enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1 };
+/* GNN_AGG_SAGE_MAX: GraphSAGE with the max aggregator (Section II-A); its
+ * update reads [h_self || max] as the mean model reads [h_self || mean].
+ * The model-level calls (gnn_train_step and its stages) take it; the
+ * per-operator calls have their own entry points for it
+ * (gnn_aggregate_fwd_max, gnn_aggregate_bwd_max). */
+enum { GNN_AGG_SAGE_MEAN = 0, GNN_AGG_GCN_SYM = 1, GNN_AGG_SAGE_MAX = 2 };
 enum { GNN_LOC_DEVICE = 0, GNN_LOC_HOST_PINNED = 1 };
 typedef void *gnn_stream; /* hipStream_t */
 
 #define GNN_MAX_LAYERS 4
 #define GNN_MAX_FANOUT 1024
 #define GNN_MAX_DIM 65536
-#define GNN_ABI_VERSION 1
+#define GNN_ABI_VERSION 2
 
 /* Text of the last error reported on the calling thread ("" if none).  Valid
  * until the next gnn_* call on this thread. */
@@ -229,7 +234,8 @@ gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a,
  *   out     [device] block->cap_dst x f of odt (GNN_F32 or GNN_BF16):
  *           out[i, c] = max over row i's edges e of h_src[col[e], c], narrowed
  *           to odt (round to nearest even); 0 for a row without edges.
- *   argmax  [device] int32 block->cap_dst x f: the local source id of the
+ *   argmax  [device] int32 block->cap_dst x f, or NULL when the table is
+ *           not wanted (no backward follows): the local source id of the
  *           edge that holds out[i, c] (-1 for a row without edges).  The
  *           row's first edge holds the running maximum and a later edge
  *           replaces it only when strictly greater, so ties and duplicate
@@ -475,7 +481,8 @@ typedef struct gnn_model {
     int32_t precision;                  /* GNN_F32 or GNN_BF16 */
     int32_t dims[GNN_MAX_LAYERS + 1];   /* f^0 .. f^L (f^L = number of classes) */
     int32_t fanouts[GNN_MAX_LAYERS];    /* hop order: fanouts[0] is sampled around the targets */
-    float *w[GNN_MAX_LAYERS];           /* [device] fp32 K_l x f^l, K_l = 2 f^{l-1} (SAGE) or f^{l-1} (GCN) */
+    float *w[GNN_MAX_LAYERS];           /* [device] fp32 K_l x f^l, K_l = 2 f^{l-1} (SAGE mean or max) or
+                                           f^{l-1} (GCN) */
     float *b[GNN_MAX_LAYERS];           /* [device] fp32 f^l */
     float *dw[GNN_MAX_LAYERS];          /* [device] fp32 K_l x f^l, written */
     float *db[GNN_MAX_LAYERS];          /* [device] fp32 f^l, written */
@@ -525,6 +532,8 @@ typedef struct gnn_step_layout {
                                            block of every step of the last gnn_train_step, gnn_step_compute or
                                            gnn_train_steps call on this compute workspace */
     size_t loss;                        /* fp32 loss of the step */
+    size_t argmax[GNN_MAX_LAYERS + 1];  /* GNN_AGG_SAGE_MAX, per layer l >= 2: int32 argmax table of the
+                                           aggregation (rows x f^{l-1}, read by the backward); else 0 */
 } gnn_step_layout;
 
 gnn_status gnn_train_step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_step_layout *out);

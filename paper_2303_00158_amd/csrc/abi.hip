@@ -83,8 +83,8 @@ gnn_status check_model(const gnn_model *m, const char *who) {
     GNN_CHECK(m, GNN_EINVAL, "%s: model is NULL", who);
     GNN_CHECK(m->num_layers >= 1 && m->num_layers <= GNN_MAX_LAYERS, GNN_EINVAL, "%s: num_layers must be in [1, %d]",
               who, GNN_MAX_LAYERS);
-    GNN_CHECK(m->kind == GNN_AGG_SAGE_MEAN || m->kind == GNN_AGG_GCN_SYM, GNN_EINVAL, "%s: unknown aggregation %d",
-              who, m->kind);
+    GNN_CHECK(m->kind == GNN_AGG_SAGE_MEAN || m->kind == GNN_AGG_GCN_SYM || m->kind == GNN_AGG_SAGE_MAX, GNN_EINVAL,
+              "%s: unknown aggregation %d", who, m->kind);
     GNN_CHECK(act_dtype(m->precision), GNN_EUNSUPPORTED, "%s: precision must be GNN_F32 or GNN_BF16", who);
     for (int l = 0; l <= m->num_layers; ++l)
         GNN_CHECK(dim_ok(m->dims[l]), GNN_EINVAL, "%s: dims[%d] = %d out of [1, %d]", who, l, m->dims[l], GNN_MAX_DIM);
@@ -385,7 +385,7 @@ gnn_status gnn_aggregate_fwd_max(const gnn_block *b, const void *h_src, gnn_dtyp
     GNN_TRY(check_block(b, false, false, who));
     GNN_CHECK(act_dtype(hdt) && act_dtype(odt), GNN_EUNSUPPORTED, "%s: dtypes must be GNN_F32 or GNN_BF16", who);
     GNN_CHECK(dim_ok(f), GNN_EINVAL, "%s: f %lld out of [1, %d]", who, (long long)f, GNN_MAX_DIM);
-    GNN_CHECK((h_src || b->cap_src == 0) && ((out && argmax) || b->cap_dst == 0), GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK((h_src || b->cap_src == 0) && (out || b->cap_dst == 0), GNN_EINVAL, "%s: NULL pointer", who);
     GNN_CHECK(aligned(h_src, dtype_size(hdt)) && aligned(out, dtype_size(odt)) && aligned(argmax, 4), GNN_EINVAL,
               "%s: misaligned data", who);
     return launch_aggregate_fwd_max(b, h_src, hdt, f, out, odt, argmax, stream_of(s));
@@ -529,7 +529,7 @@ gnn_status gnn_model_sync_shadow(const gnn_model *m, gnn_stream s) {
     GNN_TRY(check_model_buffers(m, who));
     for (int l = 0; l < m->num_layers; ++l) {
         if (!m->wt[l]) continue;
-        const int64_t K = (m->kind == GNN_AGG_SAGE_MEAN ? 2 : 1) * static_cast<int64_t>(m->dims[l]);
+        const int64_t K = (m->kind == GNN_AGG_GCN_SYM ? 1 : 2) * static_cast<int64_t>(m->dims[l]);
         GNN_TRY(launch_shadow_sync(m->w[l], K, m->dims[l + 1], m->wt[l], stream_of(s)));
     }
     return GNN_OK;

@@ -459,7 +459,7 @@ __device__ __forceinline__ void agg_fwd_row_max(const int64_t *__restrict__ rowp
 #pragma unroll
         for (int q = 0; q < 4; ++q) r[q] = (m.src[q] < 0) ? 0.f : m.v[q];
         store_chunk<VEC>(out, row * f, e0, f, make_float4(r[0], r[1], r[2], r[3]));
-        store_arg4<VEC>(argmax, row * f, e0, f, m.src);
+        if (argmax) store_arg4<VEC>(argmax, row * f, e0, f, m.src);
     }
 }
 
@@ -661,8 +661,8 @@ void with_bwd_job(const gnn_block *b, int kind, const float *d_a, int64_t f, con
     else by_kind(std::integral_constant<int, GNN_AGG_GCN_SYM>{});
 }
 
-// f(job) with the max aggregator's forward job; false if the dtypes are
-// unsupported.
+// f(job) with the max aggregator's forward job (argmax may be null: the
+// table is not kept); false if the dtypes are unsupported.
 template <class F>
 bool with_fwd_max_job(const gnn_block *b, const void *h, int hdt, int64_t f, void *out, int odt, int32_t *argmax,
                       F &&fn) {
@@ -684,6 +684,15 @@ bool with_fwd_max_job(const gnn_block *b, const void *h, int hdt, int64_t f, voi
     else if (hdt == GNN_BF16 && odt == GNN_F32) go(Tag<uint16_t>{}, Tag<float>{});
     else go(Tag<uint16_t>{}, Tag<uint16_t>{});
     return true;
+}
+
+// f(job) with the forward job of any aggregation kind; the max aggregator
+// writes its argmax table to argmax (may be null).
+template <class F>
+bool with_fwd_kind_job(const gnn_block *b, int kind, const void *h, int hdt, int64_t f, void *out, int odt,
+                       int32_t *argmax, F &&fn) {
+    if (kind == GNN_AGG_SAGE_MAX) return with_fwd_max_job(b, h, hdt, f, out, odt, argmax, fn);
+    return with_fwd_job(b, kind, h, hdt, f, out, odt, fn);
 }
 
 template <class F>

@@ -33,7 +33,7 @@ namespace {
 
 int64_t k_of(const gnn_model *m, int l) {  // reduction width of layer l (1-based)
     const int64_t f = m->dims[l - 1];
-    return m->kind == GNN_AGG_SAGE_MEAN ? 2 * f : f;
+    return m->kind == GNN_AGG_GCN_SYM ? f : 2 * f;
 }
 
 }  // namespace
@@ -87,6 +87,8 @@ gnn_status step_layout(const gnn_model *m, int64_t graph_n, int64_t batch, gnn_s
         o->h[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * (l < L ? asz : 4));
         o->grad[l] = d.take(static_cast<size_t>(rows) * m->dims[l] * 4);
         if (l >= 2) o->d_a[l] = d.take(static_cast<size_t>(rows) * k_of(m, l) * 4);
+        if (l >= 2 && m->kind == GNN_AGG_SAGE_MAX)
+            o->argmax[l] = d.take(static_cast<size_t>(rows) * m->dims[l - 1] * 4);
         fwd = std::max(fwd, update_fwd_ws_bytes(k_of(m, l), m->dims[l], rows, m->precision));
         // every layer its own region: the two-layer backward reduces layer
         // 2's partials while layer 1's are being written
@@ -127,12 +129,13 @@ void block_views(const gnn_model *m, const gnn_step_layout &o, char *prep, gnn_b
     for (int h = 0; h < m->num_layers; ++h) blk[h] = block_view(o, h, prep);
 }
 
-// The feature loading fuses into layer 1's aggregation for an fp32 table in
-// device memory feeding bf16 layers (the aggregation reads the table rows it
-// sums, and X' is gathered only for the destination rows, which the update
-// and the backward read); a host table is read once over the link into X'.
-bool fused_loading(const gnn_graph *g, bool host_table, int tdt, int act) {
-    return !host_table && tdt == GNN_F32 && act == GNN_BF16 && g->n <= INT32_MAX;
+// The feature loading fuses into layer 1's sum aggregations for an fp32
+// table in device memory feeding bf16 layers (the aggregation reads the
+// table rows it sums, and X' is gathered only for the destination rows,
+// which the update and the backward read); a host table is read once over
+// the link into X', and so is every table of the max aggregator.
+bool fused_loading(const gnn_model *m, const gnn_graph *g, bool host_table, int tdt, int act) {
+    return m->kind != GNN_AGG_SAGE_MAX && !host_table && tdt == GNN_F32 && act == GNN_BF16 && g->n <= INT32_MAX;
 }
 
 // Sampling of all hops, the gather of X' and layer 1's aggregation (which
@@ -194,7 +197,7 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
     // feature loading (rows of the input layer's sources) with the last
     // hop's relabel
     const gnn_block &b0 = blk[L - 1];
-    const bool fuse = fused_loading(g, host_table, tdt, act);
+    const bool fuse = fused_loading(m, g, host_table, tdt, act);
     // X': all sources of the input layer's block, or its destination rows
     // (counts[0]) when the aggregation reads the table itself
     const gath::Args ga{table, row_stride, b0.src_ids, b0.counts + (fuse ? 0 : 1), fuse ? b0.cap_dst : b0.cap_src,
@@ -217,7 +220,8 @@ gnn_status run_prepare(const gnn_model *m, const gnn_graph *g, const float *gcn_
         });
         return st;
     }
-    agg::with_fwd_job(&b0, m->kind, prep + o.x0, act, m->dims[0], prep + o.agg[1], act, [&](auto aj) {
+    // (layer 1's argmax is not kept: no aggregation backward below layer 2)
+    agg::with_fwd_kind_job(&b0, m->kind, prep + o.x0, act, m->dims[0], prep + o.agg[1], act, nullptr, [&](auto aj) {
         st = launch_jobs(s, "csc_sort+aggregate_l1", sort(L - 2), role(aj, agg::row_grid(b0.cap_dst)));
     });
     return st;
@@ -302,7 +306,7 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
         if (h >= 2) GNN_TRY(launch_jobs(s, "hop_emit+csc_scan+csc_sort", emit(h), scan(h - 1), sort(h - 2)));
         else GNN_TRY(launch_jobs(s, "hop_emit+csc_scan", emit(h), scan(h - 1)));
     }
-    const bool fuse = fused_loading(g, host_table, tdt, act);
+    const bool fuse = fused_loading(m, g, host_table, tdt, act);
     gath::Args ga[kMaxCopies];
     for (int c = 0; c < G; ++c) {
         const gnn_block &b0 = blk[c][L - 1];
@@ -354,13 +358,13 @@ gnn_status run_prepare_group(const gnn_model *m, const gnn_graph *g, const float
         GNN_CHECK(same, GNN_EINVAL, "train_step: prepare workspaces differ in alignment");
         return st;
     }
-    agg::with_fwd_job(&blk[0][L - 1], m->kind, static_cast<char *>(preps[0]) + o.x0, act, m->dims[0],
-                      static_cast<char *>(preps[0]) + o.agg[1], act, [&](auto aj) {
+    agg::with_fwd_kind_job(&blk[0][L - 1], m->kind, static_cast<char *>(preps[0]) + o.x0, act, m->dims[0],
+                           static_cast<char *>(preps[0]) + o.agg[1], act, nullptr, [&](auto aj) {
         using J = decltype(aj);
         J js[kMaxCopies];
         for (int c = 0; c < G; ++c)
-            agg::with_fwd_job(&blk[c][L - 1], m->kind, static_cast<char *>(preps[c]) + o.x0, act, m->dims[0],
-                              static_cast<char *>(preps[c]) + o.agg[1], act, [&](auto jc) {
+            agg::with_fwd_kind_job(&blk[c][L - 1], m->kind, static_cast<char *>(preps[c]) + o.x0, act, m->dims[0],
+                                   static_cast<char *>(preps[c]) + o.agg[1], act, nullptr, [&](auto jc) {
                 if constexpr (std::is_same<decltype(jc), J>::value) js[c] = jc;
                 else same = false;
             });
@@ -494,11 +498,14 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     float *row_loss = reinterpret_cast<float *>(comp + o.loss_ws);
     float *g_last = reinterpret_cast<float *>(comp + o.grad[L]);
     bool loss_done = false;
-    const bool sage = m->kind == GNN_AGG_SAGE_MEAN;
+    const bool sage = m->kind != GNN_AGG_GCN_SYM;  // A = [h_self || aggregation]
+    const bool maxagg = m->kind == GNN_AGG_SAGE_MAX;
+    auto argmax_of = [&](int l) { return reinterpret_cast<int32_t *>(comp + o.argmax[l]); };
     // a two-layer model at a small mini-batch: both layers in one launch
-    // (layer 1's rows computed where the last layer reads them)
+    // (layer 1's rows computed where the last layer reads them); the fused
+    // kernels implement the sum aggregations only
     TwoBwd tb{};
-    bool two = L == 2 && two_layer_ok(m->kind, m->precision, m->dims[0], m->dims[1], m->dims[2], blk[0].cap_dst,
+    bool two = !maxagg && L == 2 && two_layer_ok(m->kind, m->precision, m->dims[0], m->dims[1], m->dims[2], blk[0].cap_dst,
                                       m->fanouts[0], x0, agg_of(1), m->wt[0], m->wt[1], comp + o.h[1],
                                       comp + o.agg[2]);
     if (two) {
@@ -518,7 +525,7 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
         void *agg = agg_of(l);
         const int64_t f_in = m->dims[l - 1];
         const int32_t maxdeg = l == 1 ? 1 : m->fanouts[L - l];
-        if ((l > 1 || l == L) && fused_layer_ok(m->kind, m->precision, f_in, m->dims[l], b.cap_dst, maxdeg, l == L,
+        if (!maxagg && (l > 1 || l == L) && fused_layer_ok(m->kind, m->precision, f_in, m->dims[l], b.cap_dst, maxdeg, l == L,
                                                  hin, m->wt[l - 1], agg)) {
             if (l == 1)  // a one-layer model: the prepared aggregation, with the loss
                 GNN_TRY(launch_fused_update(&b, m->kind, sage ? hin : nullptr, agg, f_in, m->wt[0], m->b[0],
@@ -531,7 +538,8 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
         }
         // (a hidden layer 1 with a bf16 W^T that fits takes the fused
         // kernel in A-load mode inside launch_update_fwd)
-        if (l > 1) GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
+        if (l > 1 && maxagg) GNN_TRY(launch_aggregate_fwd_max(&b, hin, act, f_in, agg, act, argmax_of(l), s));
+        else if (l > 1) GNN_TRY(launch_aggregate_fwd(&b, m->kind, hin, act, f_in, agg, act, s));
         GNN_TRY(launch_update_fwd(sage ? hin : agg, sage ? agg : nullptr, act, f_in, b.counts, b.cap_dst, m->w[l - 1],
                                   m->wt[l - 1], m->b[l - 1], m->dims[l], l < L, m->precision, comp + o.h[l],
                                   l < L ? act : GNN_F32, comp + o.fwd_ws, s));
@@ -574,11 +582,13 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
         gnn_status st = GNN_OK;
         if (l > 1) {
             float *d_src = reinterpret_cast<float *>(comp + o.grad[l - 1]);
-            agg::with_bwd_job(&b, m->kind, d_a, f_in, hin, act, d_src, [&](auto aj) {
+            auto pair = [&](auto aj) {
                 gbwd::with_reduce_job(a, p, [&](auto rj) {
                     st = launch_job2(rj, p.red_grid, aj, agg::row_grid(b.cap_src), s, "update_dw_reduce+aggregate_bwd");
                 });
-            });
+            };
+            if (maxagg) agg::with_bwd_max_job(&b, argmax_of(l), d_a, f_in, hin, act, d_src, pair);
+            else agg::with_bwd_job(&b, m->kind, d_a, f_in, hin, act, d_src, pair);
         } else {
             gbwd::with_reduce_job(a, p, [&](auto rj) {
                 st = launch_job2(rj, p.red_grid, tail, 1, s, "update_dw_reduce+step_tail");

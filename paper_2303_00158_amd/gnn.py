@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libgnn.so")
 GNN_OK, GNN_EINVAL, GNN_ESIZE, GNN_EHIP, GNN_EUNSUPPORTED, GNN_EDEVICE = 0, -1, -2, -3, -4, -5
 GNN_DEVERR_WAIT, GNN_DEVERR_RANGE = 1, 2
 GNN_F32, GNN_BF16, GNN_F16 = 0, 1, 2
-GNN_AGG_SAGE_MEAN, GNN_AGG_GCN_SYM = 0, 1
+GNN_AGG_SAGE_MEAN, GNN_AGG_GCN_SYM, GNN_AGG_SAGE_MAX = 0, 1, 2
 GNN_LOC_DEVICE, GNN_LOC_HOST_PINNED = 0, 1
 GNN_MAX_LAYERS = 4
 
@@ -62,7 +62,8 @@ class StepLayout(ctypes.Structure):
                 ("x0", _sz), ("agg", _sz * (_ML + 1)), ("h", _sz * (_ML + 1)), ("grad", _sz * (_ML + 1)),
                 ("d_a", _sz * (_ML + 1)), ("fwd_ws", _sz), ("fwd_ws_bytes", _sz), ("bwd_ws", _sz),
                 ("bwd_ws_bytes", _sz), ("loss_ws", _sz),
-                ("loss_ws_bytes", _sz), ("edges", _sz), ("error", _sz), ("loss", _sz)]
+                ("loss_ws_bytes", _sz), ("edges", _sz), ("error", _sz), ("loss", _sz),
+                ("argmax", _sz * (_ML + 1))]
 
 
 _P = ctypes.POINTER
@@ -282,11 +283,12 @@ def aggregate_bwd(block: DeviceBlock, kind: int, d_a: torch.Tensor, f: int, d_sr
     return d_src
 
 
-def aggregate_fwd_max(block: DeviceBlock, h_src: torch.Tensor, out: torch.Tensor, argmax: torch.Tensor,
+def aggregate_fwd_max(block: DeviceBlock, h_src: torch.Tensor, out: torch.Tensor, argmax: Optional[torch.Tensor],
                       stream=None) -> torch.Tensor:
     """gnn_aggregate_fwd_max: GraphSAGE's max aggregator; argmax (int32, the
-    shape of out) receives the winning local source of every element."""
-    assert argmax.dtype == torch.int32
+    shape of out, or None: not kept) receives the winning local source of
+    every element."""
+    assert argmax is None or argmax.dtype == torch.int32
     f = h_src.shape[1]
     _check(lib().gnn_aggregate_fwd_max(ctypes.byref(block.c), _ptr(h_src), dtype_code(h_src.dtype), f, _ptr(out),
                                        dtype_code(out.dtype), _ptr(argmax), _stream(stream)))
@@ -446,7 +448,7 @@ def sgd(w: torch.Tensor, dw: torch.Tensor, lr: float, stream=None) -> torch.Tens
 # whole training step
 # ---------------------------------------------------------------------------
 
-_COMPUTE_BUFFERS = ("agg", "h", "grad", "d_a", "fwd_ws", "bwd_ws", "loss_ws", "edges", "error", "loss")
+_COMPUTE_BUFFERS = ("agg", "h", "grad", "d_a", "fwd_ws", "bwd_ws", "loss_ws", "edges", "error", "loss", "argmax")
 
 
 class Trainer:
@@ -615,8 +617,9 @@ class Trainer:
         return torch_dtype(self.precision)
 
     def tensor(self, name: str, layer: int, rows: int, cols: int, dtype: torch.dtype) -> torch.Tensor:
-        """View of a step buffer of the last step (agg/h/grad/d_a per layer;
-        x0 and the rest by name)."""
-        off = getattr(self.layout, name)[layer] if name in ("agg", "h", "grad", "d_a") else getattr(self.layout, name)
+        """View of a step buffer of the last step (agg/h/grad/d_a/argmax per
+        layer; x0 and the rest by name)."""
+        per_layer = ("agg", "h", "grad", "d_a", "argmax")
+        off = getattr(self.layout, name)[layer] if name in per_layer else getattr(self.layout, name)
         compute = name in _COMPUTE_BUFFERS and not (name == "agg" and layer == 1)  # layer 1's: prepare stage
         return self._view(off, rows * cols, dtype, compute=compute).view(rows, cols)

@@ -95,11 +95,12 @@ def predict(layers: Sequence[Layer], n_input: int, kind: str, hw: Hardware, t_sa
             n_trainers: int = 1, s_model: int = 4) -> Prediction:
     """Predicted iteration time (seconds) for one trainer's blocks.
 
-    layers: layers 1..L; n_input: |V^0| (rows of X'); kind: "sage" or "gcn";
+    layers: layers 1..L; n_input: |V^0| (rows of X'); kind: "sage", "gcn" or
+    "sage-max" (the max aggregator moves the mean's bytes);
     t_samp: measured sampling time; s_table: bytes per feature of the table
     (S_feat of eqs. 7-8); s_act: bytes per activation the aggregation reads
     (S_feat of eq. 11); fused: (+) is max, else sum."""
-    if kind not in ("sage", "gcn"):
+    if kind not in ("sage", "gcn", "sage-max"):
         raise ValueError(kind)
     f0 = layers[0].f_in
     t_load = n_trainers * n_input * f0 * s_table / hw.bw_mem
@@ -107,13 +108,13 @@ def predict(layers: Sequence[Layer], n_input: int, kind: str, hw: Hardware, t_sa
     t_agg, t_upd = [], []
     for ly in layers:
         t_agg.append(ly.edges * ly.f_in * s_act / hw.bw_mem)
-        k = (2 if kind == "sage" else 1) * ly.f_in
+        k = (1 if kind == "gcn" else 2) * ly.f_in
         t_upd.append(ly.n_dst * k * ly.f_out / hw.mac_rate)
     comb = max if fused else (lambda a, b: a + b)
     L = len(layers)
     t_fwd = sum(comb(t_agg[i], t_upd[i]) for i in range(L))
     t_bwd = t_upd[0] + sum(comb(t_agg[i], t_upd[i]) for i in range(1, L))
-    model_bytes = sum((2 if kind == "sage" else 1) * ly.f_in * ly.f_out for ly in layers) * s_model
+    model_bytes = sum((1 if kind == "gcn" else 2) * ly.f_in * ly.f_out for ly in layers) * s_model
     t_sync = 2 * model_bytes / hw.bw_link if n_trainers > 1 else 0.0
     t_prop = t_fwd + t_bwd + t_sync
     t_pipe = max(t_samp, t_load, t_trans, t_prop)

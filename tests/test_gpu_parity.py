@@ -62,7 +62,7 @@ def upload_block(blk: "oracle.Block", src_norm=None) -> "gnn.DeviceBlock":
 
 
 def test_library_is_the_hip_build():
-    assert gnn.lib().gnn_abi_version() == 1
+    assert gnn.lib().gnn_abi_version() == 2
     x = torch.ones(4, device=DEV)
     gnn.sgd(x, torch.ones(4, device=DEV), 0.5)
     torch.cuda.synchronize()
@@ -1153,13 +1153,14 @@ def _step_case(kind, precision, dims, fanouts, n, m, batch, graph="er", steps=1,
     labels = workloads.labels(n, dims[-1], seed=seed)
     perm = workloads.target_batches(n, batch, seed=seed)
     L = len(dims) - 1
-    sage = kind == gnn.GNN_AGG_SAGE_MEAN
+    sage = kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
     ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], seed, l) for l in range(L)]
     bs = [torch.zeros(dims[l + 1]) for l in range(L)]
     g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
     nrm = gnn.gcn_norm(g)
     tr = gnn.Trainer(kind, dims, fanouts, precision, n, batch, ws, bs, device=DEV)
-    okind = oracle.GCN if kind == gnn.GNN_AGG_GCN_SYM else oracle.SAGE
+    okind = {gnn.GNN_AGG_SAGE_MEAN: oracle.SAGE, gnn.GNN_AGG_GCN_SYM: oracle.GCN,
+             gnn.GNN_AGG_SAGE_MAX: oracle.SAGE_MAX}[kind]
     oprec = oracle.F32 if precision == gnn.GNN_F32 else oracle.BF16
     rp_h, col_h, nrm_h = rowptr.numpy(), col.numpy(), oracle.gcn_norm(rowptr.numpy())
     w_ref = [w.numpy() for w in ws]
@@ -1203,11 +1204,35 @@ def test_train_step_tiny_gcn_fp32():
         assert np.array_equal(x0, ref["x0"])
 
 
-@pytest.mark.parametrize("kind", [gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_AGG_GCN_SYM])
+@pytest.mark.parametrize("kind", [gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_AGG_GCN_SYM, gnn.GNN_AGG_SAGE_MAX])
 def test_train_step_rmat_bf16(kind):
     dims, fan = (100, 256, 47), (25, 10)
     for tr, ref, oprec in _step_case(kind, gnn.GNN_BF16, dims, fan, 30_000, 400_000, 512, graph="rmat", steps=2):
         _check_step(tr, ref, oprec, 2)
+        if kind == gnn.GNN_AGG_SAGE_MAX:
+            _check_max_tables(tr, ref, 2)
+
+
+def _check_max_tables(tr, ref, L):
+    # the argmax tables the backward reads: each is the oracle's, except
+    # where a near-tie falls the other way on activations that differ in
+    # their last bit (the oracle sums the update in fp64); those must stay
+    # rare
+    for l in range(2, L + 1):
+        want = ref["ARG"][l]
+        got = tr.tensor("argmax", l, want.shape[0], want.shape[1], torch.int32).cpu().numpy()
+        agree = float(np.mean(got == want))
+        print(f"[max step] layer {l}: argmax agreement {agree:.6f}", flush=True)
+        assert agree >= 0.999, (l, agree)
+    assert tr.layout.argmax[1] == 0
+
+
+def test_train_step_max_fp32_three_layers():
+    # GraphSAGE-max at depth 3 in fp32: two layers keep argmax tables
+    dims, fan = (32, 24, 16, 8), (6, 4, 3)
+    for tr, ref, oprec in _step_case(gnn.GNN_AGG_SAGE_MAX, gnn.GNN_F32, dims, fan, 10_000, 60_000, 256, steps=2):
+        _check_step(tr, ref, oprec, 3)
+        _check_max_tables(tr, ref, 3)
 
 
 @pytest.mark.parametrize("kind", [gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_AGG_GCN_SYM])
@@ -1339,7 +1364,7 @@ def _pipeline_inputs(kind, dims, fanouts, n, m, batch, table_dtype=torch.float32
     labels = workloads.labels(n, dims[-1], seed=seed).to(DEV)
     perm = workloads.target_batches(n, batch, seed=seed)
     L = len(dims) - 1
-    sage = kind == gnn.GNN_AGG_SAGE_MEAN
+    sage = kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
     ws = [workloads.glorot((2 if sage else 1) * dims[l], dims[l + 1], seed, l) for l in range(L)]
     bs = [torch.zeros(dims[l + 1]) for l in range(L)]
     g = gnn.DeviceGraph(rowptr.to(DEV), col.to(DEV))
@@ -1358,7 +1383,8 @@ def _state(tr):
                                                           (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 3, 6),
                                                           (gnn.GNN_AGG_GCN_SYM, gnn.GNN_BF16, 4, 2),
                                                           (gnn.GNN_AGG_SAGE_MEAN, gnn.GNN_BF16, 8, 11),
-                                                          (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 8, 3)])
+                                                          (gnn.GNN_AGG_GCN_SYM, gnn.GNN_F32, 8, 3),
+                                                          (gnn.GNN_AGG_SAGE_MAX, gnn.GNN_BF16, 4, 6)])
 def test_pipelined_two_stage_steps_equal_one_call_steps(kind, precision, nslot, steps):
     # gnn_train_steps: steps in groups of n_prep // 2 through rotating
     # prepare slots (each refilled after the computes that read it; partial

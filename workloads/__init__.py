@@ -202,7 +202,7 @@ class Workload:
     n: int
     m: int                    # undirected pairs (er / undirected rmat) or directed edges
     directed: bool
-    kind: str                 # "gcn" or "sage"
+    kind: str                 # "gcn", "sage" (mean) or "sage-max"
     dims: Tuple[int, ...]     # f^0 .. f^L
     fanouts: Tuple[int, ...]  # hop order: fanouts[0] is sampled around the targets
     batch: int
@@ -222,7 +222,7 @@ class Workload:
     def k_of_layer(self, layer: int) -> int:
         """Width of the update GEMM's reduction for layer ``layer`` (1-based)."""
         f = self.dims[layer - 1]
-        return 2 * f if self.kind == "sage" else f
+        return f if self.kind == "gcn" else 2 * f
 
 
 TINY = Workload("tiny-er10k-gcn", "er", 10_000, 50_000, False, "gcn", (32, 16, 8), (5, 5), 256, "f32")
@@ -230,12 +230,15 @@ RMAT_SAGE = Workload("rmat2.4m-sage", "rmat", 2_449_029, 61_859_140, False, "sag
                      1024, "bf16")
 RMAT_GCN = Workload("rmat2.4m-gcn", "rmat", 2_449_029, 61_859_140, False, "gcn", (100, 256, 47), (25, 10),
                     1024, "bf16")
+# the headline model with GraphSAGE's max aggregator instead of the mean
+RMAT_SAGE_MAX = Workload("rmat2.4m-sagemax", "rmat", 2_449_029, 61_859_140, False, "sage-max", (100, 256, 47),
+                         (25, 10), 1024, "bf16")
 RMAT_SAGE3 = Workload("rmat111m-sage3", "rmat", 111_059_956, 1_615_685_872, True, "sage", (128, 256, 256, 172),
                       (15, 10, 5), 1024, "bf16")
 RMAT_HOST = Workload("rmat244m-sage-hosttable", "rmat", 244_000_000, 1_700_000_000, True, "sage", (768, 1024, 153),
                      (25, 15), 1024, "bf16", table_dtype="f16", table_loc="host")
 
-PRESETS = {w.name: w for w in (TINY, RMAT_SAGE, RMAT_GCN, RMAT_SAGE3, RMAT_HOST)}
+PRESETS = {w.name: w for w in (TINY, RMAT_SAGE, RMAT_GCN, RMAT_SAGE_MAX, RMAT_SAGE3, RMAT_HOST)}
 
 
 def scaled(w: Workload, n: int, m: int, name: Optional[str] = None) -> Workload:
