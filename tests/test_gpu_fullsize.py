@@ -71,7 +71,7 @@ def _gpu_operands(tr, ref, w: workloads.Workload, l: int) -> np.ndarray:
     blk = ref["blocks"][L - l]
     n, f = blk.n_dst, w.dims[l - 1]
     agg = oracle.to_float64(_bits(tr.tensor("agg", l, n, f, torch.bfloat16)))
-    if w.kind != "sage":
+    if w.kind == "gcn":
         return agg
     if l == 1:
         below = tr.tensor("x0", 0, n, f, torch.bfloat16)
@@ -83,7 +83,7 @@ def _gpu_operands(tr, ref, w: workloads.Workload, l: int) -> np.ndarray:
 def _oracle_operands(ref, w: workloads.Workload, l: int) -> np.ndarray:
     blk = ref["blocks"][w.num_layers - l]
     agg = oracle.to_float64(ref["AGG"][l])
-    if w.kind != "sage":
+    if w.kind == "gcn":
         return agg
     return np.concatenate([oracle.to_float64(ref["H"][l - 1][:blk.n_dst]), agg], axis=1)
 
@@ -130,6 +130,34 @@ def _check_forward(tr, ref, w: workloads.Workload, w_before, b_before, tag) -> d
     return flips
 
 
+def _check_argmax(tr, ref, w: workloads.Workload, tag):
+    """The max aggregator's argmax tables of layers 2 .. L against the
+    oracle's.  Both take the first maximal edge of the same block over their
+    own stored H^{l-1}, which may differ in the last bf16 bit; a choice g
+    that differs from the oracle's o must be a near-tie within those
+    differences: H_o[g] >= H_o[o] - (|H_g[g] - H_o[g]| + |H_g[o] - H_o[o]|),
+    and g must be maximal over the GPU's own values, H_g[g] >= H_g[o]."""
+    L = w.num_layers
+    for l in range(2, L + 1):
+        want = ref["ARG"][l]
+        n, f = want.shape
+        got = tr.tensor("argmax", l, n, f, torch.int32).cpu().numpy()
+        diff = got != want
+        if not diff.any():
+            continue
+        rows = ref["blocks"][L - l + 1].n_dst  # H^{l-1} rows: layer l's sources
+        h_o = oracle.to_float64(ref["H"][l - 1][:rows])
+        h_g = oracle.to_float64(_bits(tr.tensor("h", l - 1, rows, f, torch.bfloat16)))
+        i, c = np.nonzero(diff)
+        g, o = got[i, c], want[i, c]
+        assert np.all((g >= 0) & (o >= 0)), (tag, "argmax of a row without edges", l)
+        slack = np.abs(h_g[g, c] - h_o[g, c]) + np.abs(h_g[o, c] - h_o[o, c])
+        assert np.all(h_o[g, c] >= h_o[o, c] - slack), (tag, "argmax differs beyond rounding", l)
+        assert np.all(h_g[g, c] >= h_g[o, c]), (tag, "argmax not maximal on the GPU's values", l)
+        print(f"[fullsize] {tag} layer {l}: {i.size} argmax choices of {got.size} differ, all near-ties "
+              f"within the stored activations' last-bit differences", flush=True)
+
+
 def _inputs(w: workloads.Workload, host_table: bool = False):
     print(f"[fullsize] {w.name}: generating n={w.n} m={w.m}", flush=True)
     rowptr, col = workloads.make_graph(w, device=DEV)
@@ -158,12 +186,13 @@ def _run_pipelined(w: workloads.Workload, steps: int, host_table: bool = False, 
     L = w.num_layers
     weights = [workloads.glorot(w.k_of_layer(l + 1), w.dims[l + 1], w.seed, l) for l in range(L)]
     biases = [torch.zeros(w.dims[l + 1]) for l in range(L)]
-    kind = gnn.GNN_AGG_SAGE_MEAN if w.kind == "sage" else gnn.GNN_AGG_GCN_SYM
-    okind = oracle.SAGE if w.kind == "sage" else oracle.GCN
+    kind = {"sage": gnn.GNN_AGG_SAGE_MEAN, "gcn": gnn.GNN_AGG_GCN_SYM, "sage-max": gnn.GNN_AGG_SAGE_MAX}[w.kind]
+    okind = {"sage": oracle.SAGE, "gcn": oracle.GCN, "sage-max": oracle.SAGE_MAX}[w.kind]
     nrm = gnn.gcn_norm(graph)
     loc = gnn.GNN_LOC_HOST_PINNED if host_table else gnn.GNN_LOC_DEVICE
     tgts = torch.stack([workloads.targets_for_step(perm, w.batch, s) for s in range(steps)]).contiguous()
-    fused = w.table_dtype == "f32" and not host_table and w.precision == "bf16"
+    # (the max aggregator gathers every source row into X')
+    fused = w.table_dtype == "f32" and not host_table and w.precision == "bf16" and w.kind != "sage-max"
     w_ref = [x.numpy() for x in weights]
     b_ref = [x.numpy() for x in biases]
     prev_losses = None
@@ -198,6 +227,8 @@ def _run_pipelined(w: workloads.Workload, steps: int, host_table: bool = False, 
         x0 = _bits(tr.tensor("x0", 0, n0, w.dims[0], torch.bfloat16))
         assert np.array_equal(x0, ref["x0"][:n0]), tag  # bf16 RNE of the gathered rows
         flips = _check_forward(tr, ref, w, w_ref, b_ref, tag)
+        if w.kind == "sage-max":
+            _check_argmax(tr, ref, w, tag)
         if flips:
             ref = oracle.train_step(host["rowptr"], host["col"], host["nrm"], host["table"], host["labels"], tgt_h,
                                     w_ref, b_ref, cfg, blocks=ref["blocks"], relu_flip=flips)
@@ -232,6 +263,12 @@ def test_fullsize_rmat2_4m_sage_pipelined():
 @pytest.mark.timeout(600)
 def test_fullsize_rmat2_4m_gcn_pipelined():
     _run_pipelined(workloads.RMAT_GCN, steps=8)
+
+
+@pytest.mark.timeout(600)
+def test_fullsize_rmat2_4m_sagemax_pipelined():
+    # the headline model with GraphSAGE's max aggregator, as bench.py times it
+    _run_pipelined(workloads.RMAT_SAGE_MAX, steps=8)
 
 
 @pytest.mark.timeout(900)
