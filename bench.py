@@ -214,6 +214,12 @@ class StagedStep:
         """gnn_two_layer_fwd on the blocks of the last run (layer 1's
         aggregation already in agg[1])."""
         gnn = self.gnn
+        if self.maxagg:
+            gnn.two_layer_fwd_max(self.blocks[0], self.w.fanouts[0], self.x0, self.agg[1], trainer.wt[0],
+                                  trainer.b[0], self.h[1], trainer.wt[1], trainer.b[1], self.agg[2], self.argmax[2],
+                                  self.h[2], labels, self.blocks[0].c.cap_dst, self.grad[2], self.row_loss,
+                                  self.da[2])
+            return
         sage = self.kind == gnn.GNN_AGG_SAGE_MEAN
         gnn.two_layer_fwd(self.blocks[0], self.kind, self.w.fanouts[0], self.x0 if sage else None, self.agg[1],
                           trainer.wt[0], trainer.b[0], self.h[1], trainer.wt[1], trainer.b[1], self.agg[2], self.h[2],
@@ -343,12 +349,12 @@ class StagedStep:
         sage = self.kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         loss_fused = False
-        if self.maxagg:  # the fused kernels implement the sum aggregations only
-            self.two = self.two_bwd = False
+        if self.maxagg:  # the folded backward implements the sum aggregations only
+            self.two_bwd = False
         if L == 2 and self.two is not False and trainer.wt:
             # as in the training step: layer 1's aggregation (the prepare
             # stage's), then both layers, the loss and dA^2 in one launch
-            gnn.aggregate_fwd(self.blocks[1], self.kind, self.x0, self.agg[1])
+            self.aggregate_fwd(self.blocks[1], 1, self.x0)
             mark("agg_fwd_l1")
             try:
                 self.two_layer_fwd(trainer, labels)
@@ -364,7 +370,7 @@ class StagedStep:
             # as in the training step: layer 1's aggregation belongs to the
             # prepare stage, its update reads it (fused kernel in A-load mode
             # inside gnn_update_fwd); later layers in one gnn_layer_fwd
-            if (l > 1 or L == 1) and self.fused.get(l, bool(trainer.wt) and not self.maxagg):
+            if (l > 1 or L == 1) and self.fused.get(l, bool(trainer.wt) and not self.maxagg):  # (sums only)
                 try:
                     self.layer_fwd(l, trainer, labels)
                     self.fused[l] = True
@@ -468,6 +474,8 @@ class StagedStep:
                     + R * f1 * S_H + M * f1 * S_H + M * C * 4 + B * (C * 4 + 4) + M * K2 * 4)
             if w.kind == "gcn":
                 byts += 4 * R
+            if self.maxagg:
+                byts += 4 * M * f1  # the argmax table of M^2
             return byts, 2 * R * K1 * f1 + 4 * M * K2 * C
         if name == "bwd_l1l2":
             # reads: layer 1's A rows, H^1 (the mask), dA^2 (the neighbour

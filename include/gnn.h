@@ -335,6 +335,24 @@ gnn_status gnn_two_layer_fwd(const gnn_block *last, gnn_agg kind, int32_t fanout
                              const int64_t *labels, int64_t batch, float *g_out, float *row_loss, float *d_a,
                              gnn_stream s);
 
+/* The same launch for GraphSAGE with the max aggregator (Section II-A): layer
+ * 2's aggregation is the elementwise maximum over each destination's sampled
+ * H^1 rows, exactly as gnn_aggregate_fwd_max takes it (the first edge holds
+ * the running maximum, a later edge replaces it only when strictly greater;
+ * 0 and -1 for a row without edges).  Arguments as gnn_two_layer_fwd with
+ * GraphSAGE's layout (K1 = 2 f0, K2 = 2 f1, x_self required), plus
+ *   argmax  [device] int32 last->cap_dst x f1, 16-byte aligned: the local
+ *           source id (row of H^1) of the edge that holds each element of
+ *           agg_out, for gnn_aggregate_bwd_max.
+ * Bits of h1, agg_out, argmax and the logits equal those of gnn_update_fwd
+ * (A-load) followed by gnn_aggregate_fwd_max and gnn_update_fwd.  Shape and
+ * alignment limits and errors as gnn_two_layer_fwd (n_out <= 48). */
+gnn_status gnn_two_layer_fwd_max(const gnn_block *last, int32_t fanout, const void *x_self, const void *m1, int64_t f0,
+                                 const uint16_t *wt1, const float *b1, int64_t f1, void *h1, const uint16_t *wt2,
+                                 const float *b2, int64_t n_out, void *agg_out, int32_t *argmax, float *logits,
+                                 const int64_t *labels, int64_t batch, float *g_out, float *row_loss, float *d_a,
+                                 gnn_stream s);
+
 /* ------------------------------------------------------------------------
  * Backward of a two-layer model below the loss (Section II-B, backward;
  * Section V: layer 1's backward is the update alone), bf16 operands, fp32

@@ -319,12 +319,39 @@ gnn_status gnn_two_layer_fwd(const gnn_block *last, gnn_agg kind, int32_t fanout
                   aligned(d_a, 4),
               GNN_EINVAL, "%s: misaligned data", who);
     GNN_CHECK(two_layer_ok(kind, GNN_BF16, f0, f1, n_out, last->cap_dst, fanout,
-                           kind == GNN_AGG_SAGE_MEAN ? x_self : m1, m1, wt1, wt2, h1, agg_out),
+                           kind == GNN_AGG_SAGE_MEAN ? x_self : m1, m1, wt1, wt2, h1, agg_out, nullptr),
               GNN_EUNSUPPORTED,
               "%s: shape not supported (needs f0 %% 4 == 0 with K1 <= 256, f1 %% 8 == 0 with f1 <= 256, n_out <= 64 "
               "(48 for SAGE), cap_dst <= 2048, aligned bf16 data)", who);
     return launch_two_layer(last, kind, fanout, x_self, m1, f0, wt1, b1, f1, h1, wt2, b2, n_out, agg_out, logits,
-                            labels, g_out, row_loss, batch, d_a, stream_of(s));
+                            labels, g_out, row_loss, batch, d_a, nullptr, stream_of(s));
+}
+
+gnn_status gnn_two_layer_fwd_max(const gnn_block *last, int32_t fanout, const void *x_self, const void *m1, int64_t f0,
+                                 const uint16_t *wt1, const float *b1, int64_t f1, void *h1, const uint16_t *wt2,
+                                 const float *b2, int64_t n_out, void *agg_out, int32_t *argmax, float *logits,
+                                 const int64_t *labels, int64_t batch, float *g_out, float *row_loss, float *d_a,
+                                 gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_two_layer_fwd_max";
+    const int kind = GNN_AGG_SAGE_MAX;
+    GNN_TRY(check_block(last, false, false, who));
+    GNN_CHECK(dim_ok(f0) && dim_ok(f1) && dim_ok(n_out), GNN_EINVAL, "%s: f0 %lld, f1 %lld or n_out %lld out of [1, %d]",
+              who, (long long)f0, (long long)f1, (long long)n_out, GNN_MAX_DIM);
+    GNN_CHECK(fanout >= 1, GNN_EINVAL, "%s: fanout must be >= 1", who);
+    GNN_CHECK(x_self && m1 && wt1 && h1 && wt2 && agg_out && argmax && logits && labels && g_out && row_loss,
+              GNN_EINVAL, "%s: NULL pointer", who);
+    GNN_CHECK(batch >= 1 && batch <= last->cap_dst, GNN_EINVAL, "%s: batch must be in [1, cap_dst]", who);
+    GNN_CHECK(aligned(logits, 4) && aligned(g_out, 4) && aligned(row_loss, 4) && aligned(labels, 8) &&
+                  aligned(d_a, 4),
+              GNN_EINVAL, "%s: misaligned data", who);
+    GNN_CHECK(two_layer_ok(kind, GNN_BF16, f0, f1, n_out, last->cap_dst, fanout, x_self, m1, wt1, wt2, h1, agg_out,
+                           argmax),
+              GNN_EUNSUPPORTED,
+              "%s: shape not supported (needs f0 %% 4 == 0 with 2 f0 <= 256, f1 %% 8 == 0 with f1 <= 256, n_out <= "
+              "48, cap_dst <= 2048, aligned bf16 data, a 16-byte aligned argmax table)", who);
+    return launch_two_layer(last, kind, fanout, x_self, m1, f0, wt1, b1, f1, h1, wt2, b2, n_out, agg_out, logits,
+                            labels, g_out, row_loss, batch, d_a, argmax, stream_of(s));
 }
 
 gnn_status gnn_two_layer_bwd_workspace_size(gnn_agg kind, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_m1,

@@ -11,7 +11,7 @@ TwoBwdPlan plan_two_bwd(int kind, const gnn_block &b2, const void *x_self, const
                         float *part1, float *w1_upd, float *b1_upd, uint16_t *wt1_upd, const float *w2, float *dw2,
                         float *db2, float *part2, float *w2_upd, float *b2_upd, uint16_t *wt2_upd, float lr) {
     TwoBwdPlan t{};
-    const bool sage = kind == GNN_AGG_SAGE_MEAN;
+    const bool sage = kind != GNN_AGG_GCN_SYM;  // A = [h_self || aggregation]
     t.a2 = gbwd::Args{sage ? static_cast<const void *>(h1) : agg2, sage ? agg2 : nullptr, GNN_BF16, f1, b2.counts,
                       b2.cap_dst, w2, g2, n_out, GNN_BF16, dw2, db2, nullptr, part2, w2_upd, b2_upd, wt2_upd, lr};
     t.a1 = gbwd::Args{sage ? x_self : m1, sage ? m1 : nullptr, GNN_BF16, f0, m1_rows, cap_m1, w1, nullptr, f1,
@@ -30,7 +30,8 @@ TwoBwdPlan plan_two_bwd(int kind, const gnn_block &b2, const void *x_self, const
     t.d_a2 = d_a2;
     t.h1 = h1;
     t.grid = static_cast<unsigned>(std::max<int64_t>(t.pm.blocks(), t.p2.dw_grid));
-    t.pull = t.gemm_ok && S == 1 && f1 % 4 == 0 && t.a1.K() <= gbwd::kPullMaxK && b2.cscptr != nullptr &&
+    // (the folded job implements the sum aggregations' backward only)
+    t.pull = kind != GNN_AGG_SAGE_MAX && t.gemm_ok && S == 1 && f1 % 4 == 0 && t.a1.K() <= gbwd::kPullMaxK && b2.cscptr != nullptr &&
              b2.cscrow != nullptr && (sage || b2.src_norm != nullptr) && cap_m1 <= b2.cap_src &&
              aligned(d_a2, 16) && aligned(h1, 8) && t.pm.blocks() <= kMaxGrid;
     return t;

@@ -60,6 +60,7 @@ struct TwoArgs {
     const float *bias2;      // [n_out] or null
     int64_t n_out;
     uint16_t *agg_out;       // M^2, bf16 [cap_dst x f1]
+    int32_t *argmax;         // max aggregator: int32 argmax table of M^2 [rows x f1], else null
     float *logits;           // [cap_dst x n_out]
     const int64_t *labels;   // [graph n]
     const int64_t *targets;  // vertex ids of the destinations
@@ -155,7 +156,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t *p, b
 // (needed last).  A load's wait then covers only what was issued before it.
 template <int KIND, int KSM1, int CW0>
 __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
-    constexpr bool SAGE = KIND == GNN_AGG_SAGE_MEAN;
+    constexpr bool SAGE = KIND != GNN_AGG_GCN_SYM;  // A = [h_self || aggregation]
+    constexpr bool MAXA = KIND == GNN_AGG_SAGE_MAX;
     constexpr bool W16A = SAGE || CW0 == 8;
     constexpr int KSM2 = SAGE ? 16 : 8;
     constexpr int TPR = kThreads / kBm > 64 ? 64 : kThreads / kBm;  // epilogue threads per destination
@@ -252,6 +254,11 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
     Chunk<8> acc;
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc.v[i] = 0.f;
+    // max aggregator: acc holds the running maximum, am the local source of
+    // the edge that holds it (-1 before the row's first edge)
+    int32_t am[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) am[i] = -1;
     uint4 self_raw = make_uint4(0u, 0u, 0u, 0u);
 
     // layer 2's weights (wavefronts 0 .. CT2 - 1, one column tile each,
@@ -342,7 +349,17 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
                     if (e0 + u >= hi) break;
                     Chunk<8> x;
                     x.set(raw[u]);
-                    if (SAGE) {
+                    if constexpr (MAXA) {
+                        // the row's first edge is taken, a later one only
+                        // when strictly greater (ties go to the earliest)
+                        const int32_t src = E[e0 + u];
+#pragma unroll
+                        for (int i = 0; i < 8; ++i)
+                            if (am[i] < 0 || x.v[i] > acc.v[i]) {
+                                acc.v[i] = x.v[i];
+                                am[i] = src;
+                            }
+                    } else if (SAGE) {
 #pragma unroll
                         for (int i = 0; i < 8; ++i) acc.v[i] = acc.v[i] + x.v[i];
                     } else {
@@ -358,7 +375,20 @@ __global__ void __launch_bounds__(kThreads) two_layer_kernel(TwoArgs a) {
     // the A^2 tile (16 rows; zero past the destinations and past K2) and M^2
     if (item) {
         uint16_t *arow = A2s + ar * LDK2;
-        if (SAGE) {
+        if constexpr (MAXA) {
+            // the maximum of bf16 values is one of them: exact in bf16; a
+            // row without edges gives 0 and argmax -1
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (am[i] < 0) acc.v[i] = 0.f;
+            const uint4 m = acc.bf16();
+            Chunk<8>::store(arow + ac * 8, self_raw);
+            Chunk<8>::store(arow + f1 + ac * 8, m);
+            Chunk<8>::store(a.agg_out + (row0 + ar) * f1 + ac * 8, m);
+            int4 *ap = reinterpret_cast<int4 *>(a.argmax + (row0 + ar) * f1 + ac * 8);
+            ap[0] = make_int4(am[0], am[1], am[2], am[3]);
+            ap[1] = make_int4(am[4], am[5], am[6], am[7]);
+        } else if (SAGE) {
             if (re > rb) {
                 const float d = static_cast<float>(re - rb);
 #pragma unroll
@@ -494,7 +524,7 @@ struct TwoShape {
 
 TwoShape two_shape(int kind, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_dst, int32_t fanout) {
     TwoShape sh{};
-    const bool sage = kind == GNN_AGG_SAGE_MEAN;
+    const bool sage = kind != GNN_AGG_GCN_SYM;
     const int64_t K1 = sage ? 2 * f0 : f0;
     if (f0 <= 0 || f0 % 4 != 0 || K1 > 256) return sh;
     if (f1 <= 0 || f1 % 8 != 0 || f1 > 16 * kWaves * kTpw1) return sh;
@@ -526,12 +556,13 @@ gnn_status two_go(const TwoShape &sh, const TwoArgs &a, unsigned grid, hipStream
 
 bool two_layer_ok(int kind, int precision, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_dst, int32_t fanout,
                   const void *x_self, const void *m1, const uint16_t *wt1, const uint16_t *wt2, const void *h1,
-                  const void *agg_out) {
+                  const void *agg_out, const int32_t *argmax) {
     if (precision != GNN_BF16 || !wt1 || !wt2 || !m1 || !h1 || !agg_out) return false;
+    if (kind == GNN_AGG_SAGE_MAX && (!argmax || !aligned(argmax, 16))) return false;
     const TwoShape sh = two_shape(kind, f0, f1, n_out, cap_dst, fanout);
     if (!sh.ok) return false;
     const size_t ra = sh.cw0 == 8 ? 16 : 8;
-    const bool sage = kind == GNN_AGG_SAGE_MEAN;
+    const bool sage = kind != GNN_AGG_GCN_SYM;
     if (!aligned(m1, ra) || (sage && (!x_self || !aligned(x_self, ra)))) return false;
     if ((sage || sh.cw0 == 8) ? !aligned(wt1, 16) : !aligned(wt1, 8)) return false;
     return aligned(wt2, 16) && aligned(h1, 2) && aligned(agg_out, 16);
@@ -541,7 +572,7 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
                             int64_t f0, const uint16_t *wt1, const float *bias1, int64_t f1, void *h1,
                             const uint16_t *wt2, const float *bias2, int64_t n_out, void *agg_out, float *logits,
                             const int64_t *labels, float *g, float *row_loss, int64_t batch, float *d_a,
-                            hipStream_t s) {
+                            int32_t *argmax, hipStream_t s) {
     const TwoShape sh = two_shape(kind, f0, f1, n_out, last->cap_dst, fanout);
     GNN_CHECK(sh.ok, GNN_EUNSUPPORTED, "two_layer_fwd: shape not supported");
     TwoArgs a{};
@@ -553,7 +584,7 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
     a.src_norm = last->src_norm;
     a.cap_dst = last->cap_dst;
     a.es_cap = sh.es_cap;
-    a.x_self = static_cast<const uint16_t *>(kind == GNN_AGG_SAGE_MEAN ? x_self : m1);
+    a.x_self = static_cast<const uint16_t *>(kind != GNN_AGG_GCN_SYM ? x_self : m1);
     a.m1 = static_cast<const uint16_t *>(m1);
     a.f0 = f0;
     a.wt1 = wt1;
@@ -564,6 +595,7 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
     a.bias2 = bias2;
     a.n_out = n_out;
     a.agg_out = static_cast<uint16_t *>(agg_out);
+    a.argmax = argmax;
     a.logits = logits;
     a.labels = labels;
     a.targets = last->src_ids;
@@ -572,6 +604,7 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
     a.b = batch;
     a.d_a = d_a;
     const unsigned grid = static_cast<unsigned>(ceil_div(last->cap_dst, kBm));
+    if (kind == GNN_AGG_SAGE_MAX) return two_go<GNN_AGG_SAGE_MAX>(sh, a, grid, s);
     return kind == GNN_AGG_SAGE_MEAN ? two_go<GNN_AGG_SAGE_MEAN>(sh, a, grid, s)
                                      : two_go<GNN_AGG_GCN_SYM>(sh, a, grid, s);
 }

@@ -178,15 +178,16 @@ gnn_status launch_fused_update(const gnn_block *b, int kind, const void *a_self,
 // layer 2's input gradient dA^2 = G (W^2)^T (fp32, bf16 operands).  two_layer_ok says
 // whether the shapes (f0 % 4 == 0 and K1 <= 256, f1 % 8 == 0 and f1 <= 256,
 // n_out <= 64, or <= 48 for GraphSAGE, at most 2,048 destinations),
-// precision and alignment allow it.
+// precision and alignment allow it.  With the max aggregator, argmax
+// (int32, 16-byte aligned, rows x f1) receives M^2's argmax table.
 bool two_layer_ok(int kind, int precision, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_dst, int32_t fanout,
                   const void *x_self, const void *m1, const uint16_t *wt1, const uint16_t *wt2, const void *h1,
-                  const void *agg_out);
+                  const void *agg_out, const int32_t *argmax);
 gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, const void *x_self, const void *m1,
                             int64_t f0, const uint16_t *wt1, const float *bias1, int64_t f1, void *h1,
                             const uint16_t *wt2, const float *bias2, int64_t n_out, void *agg_out, float *logits,
                             const int64_t *labels, float *g, float *row_loss, int64_t batch, float *d_a,
-                            hipStream_t s);
+                            int32_t *argmax, hipStream_t s);
 // Backward of a two-layer model below the loss (bwd_two.hip): both layers'
 // dW and db, with layer 2's aggregation backward folded into layer 1's dW
 // (G^1 never stored).  b2 is layer 2's block with its transpose; layer 1's A

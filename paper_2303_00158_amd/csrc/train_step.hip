@@ -399,6 +399,7 @@ struct TwoBwd {
     TwoBwdPlan q;  // both layers' dW (q.pull: layer 2's aggregation backward folded into layer 1's)
     agg::BwdJob<GNN_AGG_SAGE_MEAN, uint16_t, true> sage_bwd;  // else G^1 through memory
     agg::BwdJob<GNN_AGG_GCN_SYM, uint16_t, true> gcn_bwd;
+    agg::BwdMaxJob<uint16_t, true> max_bwd;  // (the max aggregator's, through its argmax table)
     bool ok;
 };
 
@@ -419,9 +420,11 @@ TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *
     agg::split_row(f1, &C, &S);
     t.sage_bwd = {b2, d_a2, f1, C, S, h1, g1};
     t.gcn_bwd = {b2, d_a2, f1, C, S, h1, g1};
+    const int32_t *arg2 = m->kind == GNN_AGG_SAGE_MAX ? reinterpret_cast<const int32_t *>(comp + o.argmax[2]) : nullptr;
+    t.max_bwd = {b2, arg2, d_a2, f1, C, S, h1, g1};
     const TwoBwdPlan &q = t.q;
     t.ok = m->precision == GNN_BF16 && q.gemm_ok && f1 % 4 == 0 && aligned(d_a2, 16) && aligned(g1, 16) &&
-           aligned(h1, 8) &&
+           aligned(h1, 8) && aligned(arg2, 16) &&
            reinterpret_cast<char *>(q.a2.part) + gbwd::dw_part_bytes(q.p2.pw, q.a2.K(), m->dims[2]) <=
                comp + o.bwd_ws + o.bwd_ws_bytes &&
            reinterpret_cast<char *>(q.a1.part) + gbwd::dw_part_bytes(q.p1.pw, q.a1.K(), f1) <=
@@ -451,7 +454,9 @@ gnn_status two_layer_bwd(const gnn_model *m, const TwoBwd &t, unsigned bwd_grid,
         return st;
     }
     auto first = [&](auto dwj) {
-        if (m->kind == GNN_AGG_SAGE_MEAN)
+        if (m->kind == GNN_AGG_SAGE_MAX)
+            st = launch_job2(dwj, q.p2.dw_grid, t.max_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd_max");
+        else if (m->kind == GNN_AGG_SAGE_MEAN)
             st = launch_job2(dwj, q.p2.dw_grid, t.sage_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
         else
             st = launch_job2(dwj, q.p2.dw_grid, t.gcn_bwd, bwd_grid, s, "update_dweight_l2+aggregate_bwd");
@@ -502,12 +507,13 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
     const bool maxagg = m->kind == GNN_AGG_SAGE_MAX;
     auto argmax_of = [&](int l) { return reinterpret_cast<int32_t *>(comp + o.argmax[l]); };
     // a two-layer model at a small mini-batch: both layers in one launch
-    // (layer 1's rows computed where the last layer reads them); the fused
-    // kernels implement the sum aggregations only
+    // (layer 1's rows computed where the last layer reads them; with the
+    // max aggregator it also writes layer 2's argmax table); the fused layer
+    // kernel implements the sum aggregations only
     TwoBwd tb{};
-    bool two = !maxagg && L == 2 && two_layer_ok(m->kind, m->precision, m->dims[0], m->dims[1], m->dims[2], blk[0].cap_dst,
+    bool two = L == 2 && two_layer_ok(m->kind, m->precision, m->dims[0], m->dims[1], m->dims[2], blk[0].cap_dst,
                                       m->fanouts[0], x0, agg_of(1), m->wt[0], m->wt[1], comp + o.h[1],
-                                      comp + o.agg[2]);
+                                      comp + o.agg[2], maxagg ? argmax_of(2) : nullptr);
     if (two) {
         tb = two_layer_bwd_plan(m, blk, x0, agg_of(1), comp, o, lr);
         two = tb.ok;
@@ -516,7 +522,7 @@ gnn_status run_compute(const gnn_model *m, const int64_t *labels, int64_t batch,
         GNN_TRY(launch_two_layer(&blk[0], m->kind, m->fanouts[0], x0, agg_of(1), m->dims[0], m->wt[0], m->b[0],
                                  m->dims[1], comp + o.h[1], m->wt[1], m->b[1], m->dims[2], comp + o.agg[2],
                                  reinterpret_cast<float *>(comp + o.h[2]), labels, g_last, row_loss, batch,
-                                 reinterpret_cast<float *>(comp + o.d_a[2]), s));
+                                 reinterpret_cast<float *>(comp + o.d_a[2]), maxagg ? argmax_of(2) : nullptr, s));
         loss_done = true;
     }
     for (int l = 1; l <= L && !two; ++l) {

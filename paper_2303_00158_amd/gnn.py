@@ -84,6 +84,8 @@ _SIGNATURES = {
     "gnn_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gnn_two_layer_fwd": (_i32, [_P(Block), _i32, _i32, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
                                  _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "gnn_two_layer_fwd_max": (_i32, [_P(Block), _i32, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
+                                     _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
     "gnn_two_layer_bwd_workspace_size": (_i32, [_i32, _i64, _i64, _i64, _i64, _i64, _P(_sz)]),
     "gnn_two_layer_bwd": (_i32, [_P(Block), _i32, _vp, _vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
                                  _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -333,6 +335,21 @@ def two_layer_fwd(last: "DeviceBlock", kind: int, fanout: int, x_self: Optional[
                                    _ptr(wt1), _ptr(b1), wt1.shape[0], _ptr(h1), _ptr(wt2), _ptr(b2), wt2.shape[0],
                                    _ptr(agg_out), _ptr(logits), _ptr(labels), int(batch), _ptr(g_out),
                                    _ptr(row_loss), _ptr(d_a), _stream(stream)))
+    return logits
+
+
+def two_layer_fwd_max(last: "DeviceBlock", fanout: int, x_self: torch.Tensor, m1: torch.Tensor, wt1: torch.Tensor,
+                      b1: Optional[torch.Tensor], h1: torch.Tensor, wt2: torch.Tensor, b2: Optional[torch.Tensor],
+                      agg_out: torch.Tensor, argmax: torch.Tensor, logits: torch.Tensor, labels: torch.Tensor,
+                      batch: int, g_out: torch.Tensor, row_loss: torch.Tensor, d_a: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """gnn_two_layer_fwd_max: two_layer_fwd with GraphSAGE's max aggregator
+    in layer 2; argmax (int32, the shape of agg_out) receives its table."""
+    assert argmax.dtype == torch.int32
+    _check(lib().gnn_two_layer_fwd_max(ctypes.byref(last.c), int(fanout), _ptr(x_self), _ptr(m1), m1.shape[1],
+                                       _ptr(wt1), _ptr(b1), wt1.shape[0], _ptr(h1), _ptr(wt2), _ptr(b2),
+                                       wt2.shape[0], _ptr(agg_out), _ptr(argmax), _ptr(logits), _ptr(labels),
+                                       int(batch), _ptr(g_out), _ptr(row_loss), _ptr(d_a), _stream(stream)))
     return logits
 
 

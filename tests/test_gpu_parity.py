@@ -839,6 +839,84 @@ def test_two_layer_bwd_parity(kind, f0, f1, n_out, n_dst, fanout, bound, n):
         assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
 
 
+@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound", TWO_CASES)
+def test_two_layer_fwd_max_parity(f0, f1, n_out, n_dst, fanout, bound):
+    # gnn_two_layer_fwd_max against the oracle's composition (update of layer
+    # 1, max aggregation and update of layer 2, loss), and against the calls
+    # it replaces on its own H^1: the maximum and argmax bit for bit
+    # (gnn_aggregate_fwd_max), the logits from the same bf16 operands
+    seed = 2 * f0 + f1 + n_out + n_dst
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, f0, f1, n_out, n_dst, fanout, seed)
+    h1 = oracle.update_fwd(x_self, m1, w1, b1, True, oracle.BF16, oracle.BF16)
+    agg2, arg2 = oracle.aggregate_fwd_max(blk, h1, oracle.BF16)
+    logits = oracle.update_fwd(h1[:blk.n_dst], agg2, w2, b2, False, oracle.BF16, oracle.F32)
+    loss, g = oracle.softmax_ce(logits, labels[blk.src_ids[:blk.n_dst]])
+
+    db = upload_block(blk)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)  # noqa
+    xs_d, m1_d = from_np_act(x_self), from_np_act(m1)
+    wt1, wt2 = _shadow(w1), _shadow(w2)
+    out = dict(h1=torch.empty((blk.n_src, f1), dtype=torch.bfloat16, device=DEV),
+               agg=torch.empty((blk.n_dst, f1), dtype=torch.bfloat16, device=DEV),
+               arg=torch.full((blk.n_dst, f1), -7, dtype=torch.int32, device=DEV),
+               logits=torch.empty((blk.n_dst, n_out), device=DEV), g=torch.empty((blk.n_dst, n_out), device=DEV),
+               rl=torch.empty(blk.n_dst, device=DEV), da=torch.empty((blk.n_dst, w2.shape[0]), device=DEV))
+    lab_d = d(labels)
+    print(f"[two_layer_fwd_max] f0={f0} f1={f1} n_out={n_out} n_dst={n_dst} fanout={fanout} bound={bound}",
+          flush=True)
+    gnn.two_layer_fwd_max(db, bound, xs_d, m1_d, wt1, d(b1), out["h1"], wt2, d(b2), out["agg"], out["arg"],
+                          out["logits"], lab_d, blk.n_dst, out["g"], out["rl"], out["da"])
+    torch.cuda.synchronize()
+    assert relerr(oracle.to_float64(to_np_act(out["h1"])), oracle.to_float64(h1)) <= 8e-3
+    assert relerr(oracle.to_float64(to_np_act(out["agg"])), oracle.to_float64(agg2)) <= 8e-3
+    agree = float(np.mean(out["arg"].cpu().numpy() == arg2))
+    assert agree >= 0.999, agree  # near-ties may fall the other way on H^1's last bits
+    assert relerr(out["logits"].cpu().numpy(), logits) <= 8e-3
+    assert relerr(out["g"].cpu().numpy(), g) <= 2e-2
+    assert abs(float(out["rl"].mean()) - loss) <= 2e-2 * max(1.0, abs(loss))
+    # the input gradient from the kernel's own G and operands
+    _, _, da = oracle.update_bwd(to_np_act(out["h1"])[:blk.n_dst], to_np_act(out["agg"]), w2,
+                                 out["g"].cpu().numpy(), oracle.BF16, True)
+    assert relerr(out["da"].cpu().numpy(), da) <= 1e-5
+
+    # the calls it replaces, on its own values where they are inputs
+    h1_ref = torch.empty_like(out["h1"])
+    gnn.update_fwd(xs_d, m1_d, d(w1), d(b1), h1_ref, True, gnn.GNN_BF16, wt=wt1)
+    agg_ref, arg_ref = torch.empty_like(out["agg"]), torch.empty_like(out["arg"])
+    gnn.aggregate_fwd_max(db, out["h1"], agg_ref, arg_ref)
+    lg_ref = torch.empty_like(out["logits"])
+    gnn.update_fwd(out["h1"][:blk.n_dst], out["agg"], d(w2), d(b2), lg_ref, False, gnn.GNN_BF16, wt=wt2)
+    torch.cuda.synchronize()
+    assert torch.equal(out["h1"].view(torch.int16), h1_ref.view(torch.int16))
+    assert torch.equal(out["agg"].view(torch.int16), agg_ref.view(torch.int16))
+    assert torch.equal(out["arg"], arg_ref)
+    assert relerr(out["logits"].cpu().numpy(), lg_ref.cpu().numpy()) <= 1e-5
+
+
+def test_two_layer_fwd_max_rejects_unsupported():
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, 32, 64, 8, 50, 4, 7)
+    db = upload_block(blk)
+    lab = torch.from_numpy(labels).to(DEV)
+
+    def call(n_out, arg):
+        gnn.two_layer_fwd_max(db, 4, from_np_act(x_self), from_np_act(m1),
+                              torch.zeros((64, 64), dtype=torch.bfloat16, device=DEV), None,
+                              torch.empty((blk.n_src, 64), dtype=torch.bfloat16, device=DEV),
+                              torch.zeros((n_out, 128), dtype=torch.bfloat16, device=DEV), None,
+                              torch.empty((blk.n_dst, 64), dtype=torch.bfloat16, device=DEV), arg,
+                              torch.empty((blk.n_dst, n_out), device=DEV), lab, blk.n_dst,
+                              torch.empty((blk.n_dst, n_out), device=DEV), torch.empty(blk.n_dst, device=DEV))
+
+    arg = torch.empty((blk.n_dst * 64 + 4,), dtype=torch.int32, device=DEV)
+    call(48, arg[:blk.n_dst * 64].view(blk.n_dst, 64))
+    torch.cuda.synchronize()
+    for n_out, a in ((49, arg[:blk.n_dst * 64].view(blk.n_dst, 64)),        # classes over 48
+                     (8, arg[1:blk.n_dst * 64 + 1].view(blk.n_dst, 64))):   # table not 16-byte aligned
+        with pytest.raises(gnn.GnnError) as e:
+            call(n_out, a)
+        assert e.value.code == gnn.GNN_EUNSUPPORTED
+
+
 def test_two_layer_fwd_rejects_unsupported_shapes():
     blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, 32, 64, 8, 50, 4, 7)
     db = upload_block(blk)
