@@ -233,6 +233,11 @@ class StagedStep:
         if self.two_ws is None:
             self.two_ws = gnn.two_layer_bwd_workspace(self.kind, self.w.dims[0], self.w.dims[1], self.w.dims[2],
                                                       b1.c.cap_dst, b0.c.cap_dst, self.x0.device)
+        if self.maxagg:
+            gnn.two_layer_bwd_max(b0, self.x0, self.agg[1], b1.counts[0:1], b1.c.cap_dst, self.h[1], self.agg[2],
+                                  self.argmax[2], self.da[2], self.grad[2], trainer.dw[0], trainer.db[0],
+                                  trainer.dw[1], trainer.db[1], ws=self.two_ws)
+            return
         gnn.two_layer_bwd(b0, self.kind, self.x0 if sage else None, self.agg[1], b1.counts[0:1], b1.c.cap_dst,
                           self.h[1], self.agg[2], self.da[2], self.grad[2], trainer.dw[0], trainer.db[0],
                           trainer.dw[1], trainer.db[1], ws=self.two_ws)
@@ -349,8 +354,6 @@ class StagedStep:
         sage = self.kind != gnn.GNN_AGG_GCN_SYM  # A = [h_self || aggregation]
         gemm = gnn.GNN_BF16 if self.act == torch.bfloat16 else gnn.GNN_F32
         loss_fused = False
-        if self.maxagg:  # the folded backward implements the sum aggregations only
-            self.two_bwd = False
         if L == 2 and self.two is not False and trainer.wt:
             # as in the training step: layer 1's aggregation (the prepare
             # stage's), then both layers, the loss and dA^2 in one launch

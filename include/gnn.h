@@ -391,6 +391,22 @@ gnn_status gnn_two_layer_bwd(const gnn_block *last, gnn_agg kind, const void *x_
                              const void *agg2, const float *d_a2, const float *g2, int64_t n_out, float *dw1,
                              float *db1, float *dw2, float *db2, void *ws, size_t ws_bytes, gnn_stream s);
 
+/* The same for GraphSAGE with the max aggregator: layer 2's aggregation
+ * backward is gnn_aggregate_bwd_max's (each maximum's gradient to the source
+ * that won it, once per destination), folded into layer 1's dW as above.
+ *   argmax2 [device] int32 last->cap_dst x f1, 16-byte aligned: the table
+ *           gnn_two_layer_fwd_max wrote.
+ * Other arguments as gnn_two_layer_bwd with GraphSAGE's layout (x_self
+ * required); the workspace is gnn_two_layer_bwd_workspace_size with
+ * GNN_AGG_SAGE_MAX.  dw1, db1, dw2 and db2 equal, bit for bit,
+ * gnn_aggregate_bwd_max (dA^2 -> G^1, h_below = h1) followed by
+ * gnn_update_bwd on each layer.  Limits and errors as gnn_two_layer_bwd. */
+gnn_status gnn_two_layer_bwd_max(const gnn_block *last, const void *x_self, const void *m1, int64_t f0,
+                                 const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1,
+                                 const void *agg2, const int32_t *argmax2, const float *d_a2, const float *g2,
+                                 int64_t n_out, float *dw1, float *db1, float *dw2, float *db2, void *ws,
+                                 size_t ws_bytes, gnn_stream s);
+
 /* ------------------------------------------------------------------------
  * Update (equation 2): Z = A W + b with A = [a_self || a_nbr] (SAGE) or
  * A = a_self (GCN, a_nbr NULL); K = 2*k_each or k_each.

@@ -359,8 +359,8 @@ gnn_status gnn_two_layer_bwd_workspace_size(gnn_agg kind, int64_t f0, int64_t f1
     clear_error();
     const char *who = "gnn_two_layer_bwd_workspace_size";
     GNN_CHECK(bytes, GNN_EINVAL, "%s: bytes is NULL", who);
-    GNN_CHECK(kind == GNN_AGG_SAGE_MEAN || kind == GNN_AGG_GCN_SYM, GNN_EINVAL, "%s: unknown aggregation %d", who,
-              kind);
+    GNN_CHECK(kind == GNN_AGG_SAGE_MEAN || kind == GNN_AGG_GCN_SYM || kind == GNN_AGG_SAGE_MAX, GNN_EINVAL,
+              "%s: unknown aggregation %d", who, kind);
     GNN_CHECK(dim_ok(f0) && dim_ok(f1) && dim_ok(n_out) && cap_m1 >= 0 && cap_m2 >= 0, GNN_EINVAL, "%s: bad size",
               who);
     *bytes = two_bwd_ws_bytes(kind, f0, f1, n_out, cap_m1, cap_m2);
@@ -387,7 +387,30 @@ gnn_status gnn_two_layer_bwd(const gnn_block *last, gnn_agg kind, const void *x_
     const size_t need = two_bwd_ws_bytes(kind, f0, f1, n_out, cap_m1, last->cap_dst);
     GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
     return launch_two_bwd(last, kind, kind == GNN_AGG_SAGE_MEAN ? x_self : nullptr, m1, f0, m1_rows, cap_m1, h1, f1,
-                          agg2, d_a2, g2, n_out, dw1, db1, dw2, db2, ws, stream_of(s));
+                          agg2, nullptr, d_a2, g2, n_out, dw1, db1, dw2, db2, ws, stream_of(s));
+}
+
+gnn_status gnn_two_layer_bwd_max(const gnn_block *last, const void *x_self, const void *m1, int64_t f0,
+                                 const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1,
+                                 const void *agg2, const int32_t *argmax2, const float *d_a2, const float *g2,
+                                 int64_t n_out, float *dw1, float *db1, float *dw2, float *db2, void *ws,
+                                 size_t ws_bytes, gnn_stream s) {
+    clear_error();
+    const char *who = "gnn_two_layer_bwd_max";
+    const int kind = GNN_AGG_SAGE_MAX;
+    GNN_TRY(check_block(last, true, false, who));
+    GNN_CHECK(dim_ok(f0) && dim_ok(f1) && dim_ok(n_out), GNN_EINVAL, "%s: f0 %lld, f1 %lld or n_out %lld out of [1, %d]",
+              who, (long long)f0, (long long)f1, (long long)n_out, GNN_MAX_DIM);
+    GNN_CHECK(x_self && m1 && m1_rows && h1 && agg2 && argmax2 && d_a2 && g2 && dw1 && dw2 && ws, GNN_EINVAL,
+              "%s: NULL pointer", who);
+    GNN_CHECK(cap_m1 >= 1 && cap_m1 <= last->cap_src, GNN_EINVAL, "%s: cap_m1 must be in [1, last->cap_src]", who);
+    GNN_CHECK(aligned(m1_rows, 8) && aligned(g2, 4) && aligned(dw1, 4) && aligned(db1, 4) && aligned(dw2, 4) &&
+                  aligned(db2, 4) && aligned(ws, 256),
+              GNN_EINVAL, "%s: misaligned data", who);
+    const size_t need = two_bwd_ws_bytes(kind, f0, f1, n_out, cap_m1, last->cap_dst);
+    GNN_CHECK(ws_bytes >= need, GNN_ESIZE, "%s: workspace %zu bytes, need %zu", who, ws_bytes, need);
+    return launch_two_bwd(last, kind, x_self, m1, f0, m1_rows, cap_m1, h1, f1, agg2, argmax2, d_a2, g2, n_out, dw1,
+                          db1, dw2, db2, ws, stream_of(s));
 }
 
 gnn_status gnn_aggregate_bwd(const gnn_block *b, gnn_agg kind, const float *d_a, int64_t f, const void *h_below,

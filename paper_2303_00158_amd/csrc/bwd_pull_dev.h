@@ -66,11 +66,16 @@ struct DweightPullJob {
     SplitMap map;                    // tiles: the 64-column tiles of G^1
     L2 l2;                           // layer 2's dW tiles
     int64_t l2_blocks;
+    const int32_t *argmax;           // max aggregator: layer 2's argmax table (b's destinations x f), else null
 
     __device__ void run(int64_t blk, int64_t) const {
         using CV = Cfg<true>;
         constexpr int BK = CV::BK, NC = kPullChunks;
-        constexpr bool SAGE = KIND == GNN_AGG_SAGE_MEAN;
+        constexpr bool SAGE = KIND != GNN_AGG_GCN_SYM;  // dA^2 rows [self || aggregation part]
+        // the max aggregator stages each edge's argmax row beside its dA^2
+        // row, in the second half of vst: half the edges per pass
+        constexpr bool MAXA = KIND == GNN_AGG_SAGE_MAX;
+        constexpr int PE = MAXA ? kPullEdges / 2 : kPullEdges;
         using SA = SrcCols<true, kPullMaxK, uint16_t, VA, NC>;
         // vst: the staged edge rows, then the matrix-core operands, the
         // epilogue staging and layer 2's tile
@@ -152,19 +157,22 @@ struct DweightPullJob {
             for (int c = 0; c < NC; ++c)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) gv[c][i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int64_t pb = Ea;; pb += kPullEdges) {
-                const int64_t pe = min(Eb, pb + kPullEdges);
+            for (int64_t pb = Ea;; pb += PE) {
+                const int64_t pe = min(Eb, pb + PE);
                 const int n = static_cast<int>(pe - pb);
-                // step 2: the edges' destination rows
+                // step 2: the edges' destination rows (and, for the max
+                // aggregator, whether the previous edge names the same row)
                 int32_t dst = tid < n ? b.cscrow[pb + tid] : 0;
+                int32_t prev = -1;
+                if (MAXA && tid < n && pb + tid > Ea) prev = b.cscrow[pb + tid - 1];
                 dst = min(max(dst, 0), static_cast<int32_t>(b.cap_dst - 1));
                 dstl[tid] = dst;
                 __syncthreads();
                 // step 3: the neighbour rows into LDS, 4 edges (16 lanes x 16
                 // bytes each) per wavefront instruction, and the weights
                 {
-                    const int w0 = wave * (kPullEdges / 4);
-                    const int nw = min(max(n - w0, 0), kPullEdges / 4);
+                    const int w0 = wave * (PE / 4);
+                    const int nw = min(max(n - w0, 0), PE / 4);
                     const int64_t cq = col0 + (lane & 15) * 4;
                     const int64_t cl = cq < f ? cq : 0;
                     for (int i = 0; i < nw; i += 4) {
@@ -172,12 +180,22 @@ struct DweightPullJob {
                         if (slot < n) {
                             const float *src = d_a + static_cast<int64_t>(dstl[slot]) * ka + nbr_off + cl;
                             __builtin_amdgcn_global_load_lds(src, vst + (w0 + i) * 64, 16, 0, 0);
+                            if constexpr (MAXA) {
+                                const int32_t *asrc = argmax + static_cast<int64_t>(dstl[slot]) * f + cl;
+                                __builtin_amdgcn_global_load_lds(asrc, vst + (PE + w0 + i) * 64, 16, 0, 0);
+                            }
                         }
                     }
                 }
                 if (tid < n) {
                     float w;
-                    if constexpr (SAGE) {
+                    if constexpr (MAXA) {
+                        // 1: the first of a run of entries naming one row
+                        // (a destination that sampled this source several
+                        // times passes its gradient once); the column's
+                        // first entry counts whatever precedes it
+                        w = prev == b.cscrow[pb + tid] ? 0.f : 1.f;
+                    } else if constexpr (SAGE) {
                         const int64_t d0 = b.rowptr[dst], d1 = b.rowptr[dst + 1];
                         w = 1.f / static_cast<float>(d1 - d0);
                     } else {
@@ -196,6 +214,21 @@ struct DweightPullJob {
                         const int x = c * 64 + rr * 4 + i;
                         if (x >= nr) continue;
                         const int32_t lo = max(cpl[x], lo_p), hi = min(cpl[x + 1], hi_p);
+                        if constexpr (MAXA) {
+                            // the maximum passes its gradient to the source
+                            // that won it: add where argmax names this row
+                            const int32_t jj = static_cast<int32_t>(g0 + x);
+                            for (int32_t e = lo; e < hi; ++e) {
+                                if (e != cpl[x] && wst[e - lo_p] == 0.f) continue;
+                                const int4 am = *reinterpret_cast<const int4 *>(vst + (PE + e - lo_p) * 64 + tt);
+                                const float4 v = *reinterpret_cast<const float4 *>(vst + (e - lo_p) * 64 + tt);
+                                gv[c][i].x += am.x == jj ? v.x : 0.f;
+                                gv[c][i].y += am.y == jj ? v.y : 0.f;
+                                gv[c][i].z += am.z == jj ? v.z : 0.f;
+                                gv[c][i].w += am.w == jj ? v.w : 0.f;
+                            }
+                            continue;
+                        }
                         for (int32_t e = lo; e < hi; ++e) {
                             float we = wst[e - lo_p];
                             if constexpr (!SAGE) we = we * wj[c][i];
@@ -326,6 +359,7 @@ struct TwoBwdPlan {
     const float *d_a2;
     const uint16_t *h1;
     gbwd::SplitMap pm;  // the folded job's (split, column tile) map
+    const int32_t *arg2;  // max aggregator: layer 2's argmax table, else null
     unsigned grid;      // its workgroups
     bool gemm_ok;       // both dW GEMMs take the bf16 64 x 64 variants with vector A loads
     bool pull;          // and the folded job applies
@@ -334,11 +368,13 @@ struct TwoBwdPlan {
 // kind: the aggregator; b2: layer 2's block (with its transpose); layer 1's A
 // rows [x_self || m1] (GraphSAGE) or m1 (GCN), bf16, f0 wide, with their row
 // count m1_rows (device) and capacity cap_m1; H^1 (bf16, f1 wide); M^2 =
-// agg2 (bf16, f1 wide); dA^2 and G^2 (fp32); per layer the weight gradient
-// outputs, the partial region (sized by gbwd::dw_part_bytes of the plan) and
-// the SGD targets (null: no update).
+// agg2 (bf16, f1 wide) and, for the max aggregator, its argmax table arg2
+// (int32, 16-byte aligned); dA^2 and G^2 (fp32); per layer the weight
+// gradient outputs, the partial region (sized by gbwd::dw_part_bytes of the
+// plan) and the SGD targets (null: no update).
 TwoBwdPlan plan_two_bwd(int kind, const gnn_block &b2, const void *x_self, const void *m1, int64_t f0,
                         const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1, const void *agg2,
+                        const int32_t *arg2,
                         const float *d_a2, const float *g2, int64_t n_out, const float *w1, float *dw1, float *db1,
                         float *part1, float *w1_upd, float *b1_upd, uint16_t *wt1_upd, const float *w2, float *dw2,
                         float *db2, float *part2, float *w2_upd, float *b2_upd, uint16_t *wt2_upd, float lr);

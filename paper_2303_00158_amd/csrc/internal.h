@@ -199,8 +199,8 @@ gnn_status launch_two_layer(const gnn_block *last, int kind, int32_t fanout, con
 size_t two_bwd_ws_bytes(int kind, int64_t f0, int64_t f1, int64_t n_out, int64_t cap_m1, int64_t cap_m2);
 gnn_status launch_two_bwd(const gnn_block *b2, int kind, const void *x_self, const void *m1, int64_t f0,
                           const int64_t *m1_rows, int64_t cap_m1, const uint16_t *h1, int64_t f1, const void *agg2,
-                          const float *d_a2, const float *g2, int64_t n_out, float *dw1, float *db1, float *dw2,
-                          float *db2, void *ws, hipStream_t s);
+                          const int32_t *arg2, const float *d_a2, const float *g2, int64_t n_out, float *dw1,
+                          float *db1, float *dw2, float *db2, void *ws, hipStream_t s);
 // The forward of wide layers (gemm_wide.hip): bf16 A rows and the bf16
 // shadow W^T, 256 x 256 tiles for the matrix cores.  wide_fwd_ok says
 // whether the shapes (K, n_out >= 512, K % 128 == 0, k_each % 64 == 0,

@@ -411,7 +411,8 @@ TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *
     const uint16_t *h1 = reinterpret_cast<const uint16_t *>(comp + o.h[1]);
     float *d_a2 = reinterpret_cast<float *>(comp + o.d_a[2]);
     float *g1 = reinterpret_cast<float *>(comp + o.grad[1]);
-    t.q = plan_two_bwd(m->kind, b2, x0, m1, f0, b1.counts, b1.cap_dst, h1, f1, comp + o.agg[2], d_a2,
+    const int32_t *arg2 = m->kind == GNN_AGG_SAGE_MAX ? reinterpret_cast<const int32_t *>(comp + o.argmax[2]) : nullptr;
+    t.q = plan_two_bwd(m->kind, b2, x0, m1, f0, b1.counts, b1.cap_dst, h1, f1, comp + o.agg[2], arg2, d_a2,
                        reinterpret_cast<const float *>(comp + o.grad[2]), m->dims[2], m->w[0], m->dw[0], m->db[0],
                        bwd_region(m, o, comp, 1), m->w[0], m->b[0], m->wt[0], m->w[1], m->dw[1], m->db[1],
                        bwd_region(m, o, comp, 2), m->w[1], m->b[1], m->wt[1], lr);
@@ -420,7 +421,6 @@ TwoBwd two_layer_bwd_plan(const gnn_model *m, const gnn_block *blk, const void *
     agg::split_row(f1, &C, &S);
     t.sage_bwd = {b2, d_a2, f1, C, S, h1, g1};
     t.gcn_bwd = {b2, d_a2, f1, C, S, h1, g1};
-    const int32_t *arg2 = m->kind == GNN_AGG_SAGE_MAX ? reinterpret_cast<const int32_t *>(comp + o.argmax[2]) : nullptr;
     t.max_bwd = {b2, arg2, d_a2, f1, C, S, h1, g1};
     const TwoBwdPlan &q = t.q;
     t.ok = m->precision == GNN_BF16 && q.gemm_ok && f1 % 4 == 0 && aligned(d_a2, 16) && aligned(g1, 16) &&

@@ -89,6 +89,8 @@ _SIGNATURES = {
     "gnn_two_layer_bwd_workspace_size": (_i32, [_i32, _i64, _i64, _i64, _i64, _i64, _P(_sz)]),
     "gnn_two_layer_bwd": (_i32, [_P(Block), _i32, _vp, _vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _vp,
                                  _vp, _vp, _vp, _vp, _sz, _vp]),
+    "gnn_two_layer_bwd_max": (_i32, [_P(Block), _vp, _vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _i64,
+                                     _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "gnn_update_fwd_workspace_size": (_i32, [_i64, _i64, _i64, _i32, _P(_sz)]),
     "gnn_update_fwd": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _i32, _vp, _sz,
                               _vp]),
@@ -375,6 +377,22 @@ def two_layer_bwd(last: "DeviceBlock", kind: int, x_self: Optional[torch.Tensor]
     _check(lib().gnn_two_layer_bwd(ctypes.byref(last.c), kind, _ptr(x_self), _ptr(m1), f0, _ptr(m1_rows), int(cap_m1),
                                    _ptr(h1), f1, _ptr(agg2), _ptr(d_a2), _ptr(g2), n_out, _ptr(dw1), _ptr(db1),
                                    _ptr(dw2), _ptr(db2), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def two_layer_bwd_max(last: "DeviceBlock", x_self: torch.Tensor, m1: torch.Tensor, m1_rows: torch.Tensor,
+                      cap_m1: int, h1: torch.Tensor, agg2: torch.Tensor, argmax2: torch.Tensor, d_a2: torch.Tensor,
+                      g2: torch.Tensor, dw1: torch.Tensor, db1: Optional[torch.Tensor], dw2: torch.Tensor,
+                      db2: Optional[torch.Tensor], ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """gnn_two_layer_bwd_max: two_layer_bwd for GraphSAGE with the max
+    aggregator, from the argmax table gnn_two_layer_fwd_max wrote."""
+    assert argmax2.dtype == torch.int32
+    f0, f1, n_out = m1.shape[1], h1.shape[1], g2.shape[1]
+    if ws is None:
+        ws = two_layer_bwd_workspace(GNN_AGG_SAGE_MAX, f0, f1, n_out, cap_m1, last.c.cap_dst, m1.device)
+    _check(lib().gnn_two_layer_bwd_max(ctypes.byref(last.c), _ptr(x_self), _ptr(m1), f0, _ptr(m1_rows), int(cap_m1),
+                                       _ptr(h1), f1, _ptr(agg2), _ptr(argmax2), _ptr(d_a2), _ptr(g2), n_out,
+                                       _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _ptr(ws), ws.numel(),
+                                       _stream(stream)))
 
 
 def update_fwd(a_self: torch.Tensor, a_nbr: Optional[torch.Tensor], w: torch.Tensor, bias: Optional[torch.Tensor],

@@ -917,6 +917,66 @@ def test_two_layer_fwd_max_rejects_unsupported():
         assert e.value.code == gnn.GNN_EUNSUPPORTED
 
 
+@pytest.mark.parametrize("f0,f1,n_out,n_dst,fanout,bound,n", [c + (None,) for c in TWO_CASES] +
+                         [(100, 256, 47, 2048, 50, 50, 200_000)])
+def test_two_layer_bwd_max_parity(f0, f1, n_out, n_dst, fanout, bound, n):
+    # gnn_two_layer_bwd_max from gnn_two_layer_fwd_max's outputs: against the
+    # oracle's own forward and backward chain (update, max aggregation with
+    # its argmax, update, loss; then each layer's update backward and the max
+    # aggregation backward), and bit for bit against gnn_aggregate_bwd_max +
+    # gnn_update_bwd per layer on the same forward values.  Layers up to 128
+    # wide are rejected, as for the sums.
+    seed = 5 * f0 + f1 + n_out + n_dst
+    blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, f0, f1, n_out, n_dst, fanout, seed,
+                                                                     n)
+    db = upload_block(blk)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)  # noqa
+    xs_d, m1_d = from_np_act(x_self), from_np_act(m1)
+    K1, K2 = w1.shape[0], w2.shape[0]
+    h1 = torch.empty((blk.n_src, f1), dtype=torch.bfloat16, device=DEV)
+    agg = torch.empty((blk.n_dst, f1), dtype=torch.bfloat16, device=DEV)
+    arg = torch.empty((blk.n_dst, f1), dtype=torch.int32, device=DEV)
+    g = torch.empty((blk.n_dst, n_out), device=DEV)
+    da = torch.empty((blk.n_dst, K2), device=DEV)
+    gnn.two_layer_fwd_max(db, bound, xs_d, m1_d, _shadow(w1), d(b1), h1, _shadow(w2), d(b2), agg, arg,
+                          torch.empty((blk.n_dst, n_out), device=DEV), d(labels), blk.n_dst, g,
+                          torch.empty(blk.n_dst, device=DEV), da)
+    m1_rows = torch.tensor([blk.n_src], dtype=torch.int64, device=DEV)
+    out = dict(dw1=torch.empty((K1, f1), device=DEV), db1=torch.empty(f1, device=DEV),
+               dw2=torch.empty((K2, n_out), device=DEV), db2=torch.empty(n_out, device=DEV))
+    print(f"[two_layer_bwd_max] f0={f0} f1={f1} n_out={n_out} n_dst={n_dst} fanout={fanout}", flush=True)
+    args = (db, xs_d, m1_d, m1_rows, blk.n_src, h1, agg, arg, da, g, out["dw1"], out["db1"], out["dw2"], out["db2"])
+    if f1 <= 128:
+        with pytest.raises(gnn.GnnError) as e:
+            gnn.two_layer_bwd_max(*args)
+        assert e.value.code == gnn.GNN_EUNSUPPORTED
+        return
+    gnn.two_layer_bwd_max(*args)
+    torch.cuda.synchronize()
+    # the oracle's chain from the same inputs
+    h1_o = oracle.update_fwd(x_self, m1, w1, b1, True, oracle.BF16, oracle.BF16)
+    agg_o, arg_o = oracle.aggregate_fwd_max(blk, h1_o, oracle.BF16)
+    lg_o = oracle.update_fwd(h1_o[:blk.n_dst], agg_o, w2, b2, False, oracle.BF16, oracle.F32)
+    _, g_o = oracle.softmax_ce(lg_o, labels[blk.src_ids[:blk.n_dst]])
+    dw2_o, db2_o, da_o = oracle.update_bwd(h1_o[:blk.n_dst], agg_o, w2, g_o, oracle.BF16, True)
+    g1_o = oracle.aggregate_bwd_max(blk, arg_o, da_o, f1, h1_o, oracle.F32)
+    dw1_o, db1_o, _ = oracle.update_bwd(x_self, m1, w1, g1_o, oracle.BF16, False)
+    assert relerr(out["dw2"].cpu().numpy(), dw2_o) <= 2e-2
+    assert relerr(out["db2"].cpu().numpy(), db2_o) <= 2e-2
+    assert relerr(out["dw1"].cpu().numpy(), dw1_o) <= 2e-2
+    assert relerr(out["db1"].cpu().numpy(), db1_o) <= 2e-2
+
+    # the calls it replaces, on the same forward values
+    g1_d = torch.empty((blk.n_src, f1), device=DEV)
+    gnn.aggregate_bwd_max(db, arg, da, f1, g1_d, h_below=h1)
+    ref = {k: torch.empty_like(v) for k, v in out.items()}
+    gnn.update_bwd(xs_d, m1_d, d(w1), g1_d, ref["dw1"], ref["db1"], None, gnn.GNN_BF16)
+    gnn.update_bwd(h1[:blk.n_dst], agg, d(w2), g, ref["dw2"], ref["db2"], None, gnn.GNN_BF16)
+    torch.cuda.synchronize()
+    for k in out:
+        assert torch.equal(out[k].view(torch.int32), ref[k].view(torch.int32)), k
+
+
 def test_two_layer_fwd_rejects_unsupported_shapes():
     blk, nrm, x_self, m1, w1, w2, b1, b2, labels = _two_layer_inputs(oracle.SAGE, 32, 64, 8, 50, 4, 7)
     db = upload_block(blk)
