@@ -73,9 +73,10 @@ struct DweightPullJob {
         constexpr int BK = CV::BK, NC = kPullChunks;
         constexpr bool SAGE = KIND != GNN_AGG_GCN_SYM;  // dA^2 rows [self || aggregation part]
         // the max aggregator stages each edge's argmax row beside its dA^2
-        // row, in the second half of vst: half the edges per pass
+        // row, in an array of its own (the job runs one workgroup per CU at
+        // its register use, so the LDS costs no occupancy)
         constexpr bool MAXA = KIND == GNN_AGG_SAGE_MAX;
-        constexpr int PE = MAXA ? kPullEdges / 2 : kPullEdges;
+        constexpr int PE = kPullEdges;
         using SA = SrcCols<true, kPullMaxK, uint16_t, VA, NC>;
         // vst: the staged edge rows, then the matrix-core operands, the
         // epilogue staging and layer 2's tile
@@ -84,6 +85,7 @@ struct DweightPullJob {
         __shared__ int32_t dstl[kPullEdges];
         __shared__ int32_t cpl[kPullRows + 1];
         __shared__ float cs[16][64];
+        __shared__ __attribute__((aligned(16))) int32_t ast[MAXA ? kPullEdges * 64 : 4];
         static_assert(L2::kLdsBytes + sizeof(typename L2::ColSums) <= sizeof(vst), "layer 2's tile needs more LDS");
         static_assert(sizeof(float) * 4 * 64 * 64 <= sizeof(vst), "epilogue staging needs more LDS");
         static_assert((kPullMaxK + 64) * BK * 2 <= sizeof(vst), "operand tiles need more LDS");
@@ -182,7 +184,7 @@ struct DweightPullJob {
                             __builtin_amdgcn_global_load_lds(src, vst + (w0 + i) * 64, 16, 0, 0);
                             if constexpr (MAXA) {
                                 const int32_t *asrc = argmax + static_cast<int64_t>(dstl[slot]) * f + cl;
-                                __builtin_amdgcn_global_load_lds(asrc, vst + (PE + w0 + i) * 64, 16, 0, 0);
+                                __builtin_amdgcn_global_load_lds(asrc, ast + (w0 + i) * 64, 16, 0, 0);
                             }
                         }
                     }
@@ -220,7 +222,7 @@ struct DweightPullJob {
                             const int32_t jj = static_cast<int32_t>(g0 + x);
                             for (int32_t e = lo; e < hi; ++e) {
                                 if (e != cpl[x] && wst[e - lo_p] == 0.f) continue;
-                                const int4 am = *reinterpret_cast<const int4 *>(vst + (PE + e - lo_p) * 64 + tt);
+                                const int4 am = *reinterpret_cast<const int4 *>(ast + (e - lo_p) * 64 + tt);
                                 const float4 v = *reinterpret_cast<const float4 *>(vst + (e - lo_p) * 64 + tt);
                                 gv[c][i].x += am.x == jj ? v.x : 0.f;
                                 gv[c][i].y += am.y == jj ? v.y : 0.f;
