@@ -139,6 +139,74 @@ def test_step_layout_capacities_and_disjoint_buffers(gnn):
     assert lib.gnn_train_step_workspace_size(ctypes.byref(m), 1000, 2000, ctypes.byref(nb)) == gnn.GNN_EINVAL
 
 
+def test_max_aggregator_host_validation(gnn):
+    # GraphSAGE's max aggregator: every error path is taken on the host
+    lib = gnn.lib()
+    fake = 1 << 24  # aligned stand-in addresses, never dereferenced
+    blk = gnn.Block(4, 8, 8, fake, fake, fake, fake, None, None, None)  # no transpose
+    B = ctypes.byref(blk)
+    assert lib.gnn_aggregate_fwd_max(None, fake, gnn.GNN_F32, 4, fake, gnn.GNN_F32, fake, None) == gnn.GNN_EINVAL
+    assert lib.gnn_aggregate_fwd_max(B, fake, gnn.GNN_F16, 4, fake, gnn.GNN_F32, fake, None) == gnn.GNN_EUNSUPPORTED
+    assert lib.gnn_aggregate_fwd_max(B, fake, gnn.GNN_F32, 0, fake, gnn.GNN_F32, fake, None) == gnn.GNN_EINVAL
+    assert lib.gnn_aggregate_fwd_max(B, fake, gnn.GNN_F32, 4, None, gnn.GNN_F32, fake, None) == gnn.GNN_EINVAL
+    assert lib.gnn_aggregate_fwd_max(B, fake, gnn.GNN_F32, 4, fake, gnn.GNN_F32, fake + 2, None) == gnn.GNN_EINVAL
+    assert b"misaligned" in lib.gnn_last_error()
+    # the backward needs the transpose and the argmax table
+    assert lib.gnn_aggregate_bwd_max(B, fake, fake, 4, None, gnn.GNN_F32, fake, None) == gnn.GNN_EINVAL
+    assert b"transpose" in lib.gnn_last_error()
+    blk_t = gnn.Block(4, 8, 8, fake, fake, fake, fake, fake, fake, None)
+    assert lib.gnn_aggregate_bwd_max(ctypes.byref(blk_t), None, fake, 4, None, gnn.GNN_F32, fake,
+                                     None) == gnn.GNN_EINVAL
+    assert lib.gnn_aggregate_bwd_max(ctypes.byref(blk_t), fake, fake, 4, fake, gnn.GNN_F16, fake,
+                                     None) == gnn.GNN_EUNSUPPORTED
+    # the sum aggregations do not take the max kind
+    assert lib.gnn_aggregate_fwd(B, gnn.GNN_AGG_SAGE_MAX, fake, gnn.GNN_F32, 4, fake, gnn.GNN_F32,
+                                 None) == gnn.GNN_EINVAL
+    assert b"unknown aggregation" in lib.gnn_last_error()
+    # the two-layer launches: x_self and the table are required
+    lab = fake
+    assert lib.gnn_two_layer_fwd_max(B, 4, None, fake, 32, fake, None, 64, fake, fake, None, 8, fake, fake, fake, lab,
+                                     4, fake, fake, None, None) == gnn.GNN_EINVAL
+    assert lib.gnn_two_layer_fwd_max(B, 4, fake, fake, 32, fake, None, 64, fake, fake, None, 8, fake, None, fake, lab,
+                                     4, fake, fake, None, None) == gnn.GNN_EINVAL
+    assert lib.gnn_two_layer_bwd_max(ctypes.byref(blk_t), fake, fake, 32, fake, 8, fake, 64, fake, None, fake, fake,
+                                     8, fake, fake, fake, fake, fake, 1 << 20, None) == gnn.GNN_EINVAL
+    nb = ctypes.c_size_t()
+    assert lib.gnn_two_layer_bwd_workspace_size(gnn.GNN_AGG_SAGE_MAX, 100, 256, 47, 100, 10,
+                                                ctypes.byref(nb)) == gnn.GNN_OK
+    n_max = nb.value
+    assert lib.gnn_two_layer_bwd_workspace_size(gnn.GNN_AGG_SAGE_MEAN, 100, 256, 47, 100, 10,
+                                                ctypes.byref(nb)) == gnn.GNN_OK
+    assert nb.value == n_max  # the same dW partials as the mean model's
+
+
+def test_max_model_step_layout(gnn):
+    # the max model keeps an argmax table per layer from 2 on, disjoint
+    # from every other compute buffer; layer 1 keeps none
+    lib = gnn.lib()
+    m = _model(gnn, gnn.GNN_AGG_SAGE_MAX, (100, 256, 256, 47), (15, 10, 5), gnn.GNN_BF16)
+    lay = gnn.StepLayout()
+    assert lib.gnn_train_step_layout(ctypes.byref(m), 2_449_029, 1024, ctypes.byref(lay)) == gnn.GNN_OK
+    cd = lay.cap_dst
+    assert lay.argmax[1] == 0 and lay.argmax[2] and lay.argmax[3]
+    dims = (100, 256, 256, 47)
+    spans = [(lay.fwd_ws, lay.fwd_ws_bytes), (lay.bwd_ws, lay.bwd_ws_bytes), (lay.loss_ws, lay.loss_ws_bytes),
+             (lay.edges, 8), (lay.error, 8), (lay.loss, 4)]
+    for l in (1, 2, 3):
+        rows = cd[3 - l]
+        spans += [(lay.h[l], rows * dims[l] * (2 if l < 3 else 4)), (lay.grad[l], rows * dims[l] * 4)]
+        if l >= 2:
+            spans += [(lay.agg[l], rows * dims[l - 1] * 2), (lay.d_a[l], rows * 2 * dims[l - 1] * 4),
+                      (lay.argmax[l], rows * dims[l - 1] * 4)]
+    spans = sorted(spans)
+    assert all(a + n <= b for (a, n), (b, _) in zip(spans, spans[1:])), spans
+    assert spans[-1][0] + spans[-1][1] <= lay.compute_bytes
+    mean = _model(gnn, gnn.GNN_AGG_SAGE_MEAN, (100, 256, 256, 47), (15, 10, 5), gnn.GNN_BF16)
+    lay_m = gnn.StepLayout()
+    assert lib.gnn_train_step_layout(ctypes.byref(mean), 2_449_029, 1024, ctypes.byref(lay_m)) == gnn.GNN_OK
+    assert all(lay_m.argmax[l] == 0 for l in range(5))
+
+
 def test_two_stage_step_validation(gnn):
     # argument checks of the prepare / compute entry points run on the host
     # before anything is enqueued (the pointers below are never dereferenced)
