@@ -472,7 +472,7 @@ def _has_repeated_edge(blk):
     return False
 
 
-@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("f", [1, 4, 13, 100, 256, 300])
 @pytest.mark.parametrize("hc,oc", [(oracle.F32, oracle.F32), (oracle.BF16, oracle.BF16), (oracle.BF16, oracle.F32),
                                    (oracle.F32, oracle.BF16)])
 @pytest.mark.parametrize("ties", [False, True])
@@ -533,9 +533,19 @@ def test_aggregate_fwd_max_device_count_below_capacity():
     o, a = out.cpu().numpy(), arg.cpu().numpy()
     assert np.array_equal(o[:n], want[:n]) and np.array_equal(a[:n], want_arg[:n])
     assert np.all(o[n:] == -5.0) and np.all(a[n:] == -7)
+    # a device count of zero writes nothing, forward and backward
+    db.counts[0] = 0
+    db.counts[1] = 0
+    gnn.aggregate_fwd_max(db, from_np_act(h), out, arg)
+    d_src = torch.full((blk.n_src, f), -3.0, dtype=torch.float32, device=DEV)
+    gnn.aggregate_bwd_max(db, arg, torch.zeros((blk.n_dst, 2 * f), device=DEV), f, d_src)
+    torch.cuda.synchronize()
+    o, a = out.cpu().numpy(), arg.cpu().numpy()
+    assert np.array_equal(o[:n], want[:n]) and np.all(o[n:] == -5.0) and np.all(a[n:] == -7)
+    assert torch.all(d_src == -3.0)
 
 
-@pytest.mark.parametrize("f", [4, 13, 100, 256, 300])
+@pytest.mark.parametrize("f", [1, 4, 13, 100, 256, 300])
 @pytest.mark.parametrize("hb_code", [None, oracle.F32, oracle.BF16])
 @pytest.mark.parametrize("ties", [False, True])
 def test_aggregate_bwd_max_parity(f, hb_code, ties):
